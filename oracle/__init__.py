@@ -1,0 +1,250 @@
+"""CPU oracle for SparDA's selection + block-sparse attention path (test infrastructure).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may import this
+package.  It wraps ``sparda_oracle.c`` (plain float64 loops written from the paper) with ctypes
+and takes/returns numpy arrays: bf16 tensors travel as ``uint16`` bit patterns, block indices as
+``int16``.  It shares no code with the HIP library.
+
+Function map (paper sections in the C file):
+  compress_keys  -- Eq. 2 (mean-pooled compressed keys, one per 64-token block)
+  select_row / forecast_select -- Eq. 1 + Eq. 4 (forced init/local blocks U top-k Forecast scores)
+  attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
+  gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sparda_oracle.c")
+_LIB = os.path.join(_HERE, "libsparda_oracle.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_UNSUPPORTED = -2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain C11 + OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+               "-fno-fast-math", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+        ("group_size", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32), ("cmp_kernel", ctypes.c_int32), ("cmp_stride", ctypes.c_int32),
+        ("n_init", ctypes.c_int32), ("n_local", ctypes.c_int32), ("k_total", ctypes.c_int32),
+        ("t_cap", ctypes.c_int64), ("nc_cap", ctypes.c_int64),
+    ]
+
+
+@dataclass(frozen=True)
+class Shape:
+    batch: int
+    n_kv_heads: int
+    group_size: int
+    head_dim: int = 128
+    block_size: int = 64
+    n_init: int = 1
+    n_local: int = 2
+    k_total: int = 16
+    t_cap: int = 4096
+    nc_cap: int = 64
+    cmp_kernel: int | None = None
+    cmp_stride: int | None = None
+
+    @property
+    def n_q_heads(self) -> int:
+        return self.n_kv_heads * self.group_size
+
+    def c(self) -> _Shape:
+        return _Shape(self.batch, self.n_kv_heads, self.group_size, self.head_dim, self.block_size,
+                      self.block_size if self.cmp_kernel is None else self.cmp_kernel,
+                      self.block_size if self.cmp_stride is None else self.cmp_stride,
+                      self.n_init, self.n_local, self.k_total, self.t_cap, self.nc_cap)
+
+
+_lib = None
+
+
+def open_library(path: str):
+    """Load an oracle shared library and declare its prototypes."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    S = ctypes.POINTER(_Shape)
+    i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    lib.sparda_ref_bf16_to_f64.argtypes = [ctypes.c_uint16]
+    lib.sparda_ref_bf16_to_f64.restype = f64
+    lib.sparda_ref_f64_to_bf16.argtypes = [f64]
+    lib.sparda_ref_f64_to_bf16.restype = ctypes.c_uint16
+    lib.sparda_ref_compress_keys.argtypes = [S, P, i64, i32, i32, P]
+    lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P]
+    lib.sparda_ref_forecast_select.argtypes = [S, P, i32, i64, P, P, P]
+    lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
+    lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
+    lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
+    for name in ("compress_keys", "select_row", "forecast_select", "attend_row", "sparse_attn",
+                 "gather_blocks"):
+        getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        _lib = open_library(_LIB)
+    return _lib
+
+
+def build_variant(src_text: str, out_path: str) -> str:
+    """Compile an edited copy of the oracle source (used by the tests that plant mistakes)."""
+    c_path = out_path + ".c"
+    with open(c_path, "w") as fh:
+        fh.write(src_text)
+    subprocess.run(["gcc", "-std=c11", "-O1", "-fopenmp", "-fPIC", "-shared", "-fno-fast-math", c_path,
+                    "-o", out_path, "-lm"], check=True)
+    return out_path
+
+
+def source_text() -> str:
+    with open(_SRC) as fh:
+        return fh.read()
+
+
+class use_library:
+    """Context manager: route this module's functions through another oracle library."""
+
+    def __init__(self, path: str):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        self._saved = _load()
+        _lib = open_library(self.path)
+        return self
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self._saved
+        return False
+
+
+class OracleError(RuntimeError):
+    def __init__(self, rc: int, what: str):
+        super().__init__(f"oracle {what} returned {rc}")
+        self.rc = rc
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise OracleError(rc, what)
+
+
+def _u16(a: np.ndarray) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16:
+        raise TypeError("bf16 tensors are passed as uint16 bit patterns")
+    return a
+
+
+def bf16_to_f64(bits: int) -> float:
+    return _load().sparda_ref_bf16_to_f64(int(bits))
+
+
+def f64_to_bf16(x: float) -> int:
+    return int(_load().sparda_ref_f64_to_bf16(float(x)))
+
+
+def compress_keys(shape: Shape, k: np.ndarray, t_ctx: int, blk_begin: int, blk_end: int,
+                  k_cmp: np.ndarray | None = None) -> np.ndarray:
+    """K~ for blocks [blk_begin, blk_end); k: uint16 [B][Hkv][t_cap][D]."""
+    k = _u16(k)
+    if k_cmp is None:
+        k_cmp = np.zeros((shape.batch, shape.n_kv_heads, shape.nc_cap, shape.head_dim), np.uint16)
+    cs = shape.c()
+    _check(_load().sparda_ref_compress_keys(ctypes.byref(cs), _ptr(k), t_ctx, blk_begin, blk_end, _ptr(k_cmp)),
+           "compress_keys")
+    return k_cmp
+
+
+def select_row(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, b: int, m: int, r: int):
+    """(sel_row int16[k_total], cnt, scores float64[nc_cap] with NaN for non-candidates)."""
+    f, k_cmp = _u16(f), _u16(k_cmp)
+    sel = np.empty(shape.k_total, np.int16)
+    cnt = np.zeros(1, np.int16)
+    scores = np.empty(max(shape.nc_cap, 1), np.float64)
+    cs = shape.c()
+    _check(_load().sparda_ref_select_row(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), b, m, r,
+                                         _ptr(sel), _ptr(cnt), _ptr(scores)), "select_row")
+    return sel, int(cnt[0]), scores[: shape.nc_cap]
+
+
+def forecast_select(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray):
+    """sel int16 [B][Hkv][n_q][k_total], cnt int16 [B][Hkv][n_q]."""
+    f, k_cmp = _u16(f), _u16(k_cmp)
+    sel = np.empty((shape.batch, shape.n_kv_heads, n_q, shape.k_total), np.int16)
+    cnt = np.empty((shape.batch, shape.n_kv_heads, n_q), np.int16)
+    cs = shape.c()
+    _check(_load().sparda_ref_forecast_select(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), _ptr(sel),
+                                              _ptr(cnt)), "forecast_select")
+    return sel, cnt
+
+
+def attend_row(shape: Shape, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale, b, h, r) -> np.ndarray:
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    sel = np.ascontiguousarray(sel, np.int16)
+    cnt = np.ascontiguousarray(cnt, np.int16)
+    out = np.empty(shape.head_dim, np.float64)
+    cs = shape.c()
+    _check(_load().sparda_ref_attend_row(ctypes.byref(cs), _ptr(q), n_q, q_pos0, _ptr(k), _ptr(v), kv_mode,
+                                         _ptr(sel), _ptr(cnt), float(sm_scale), b, h, r, _ptr(out)),
+           "attend_row")
+    return out
+
+
+def sparse_attn(shape: Shape, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale) -> np.ndarray:
+    """float64 [B][Hq][n_q][D]."""
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    sel = np.ascontiguousarray(sel, np.int16)
+    cnt = np.ascontiguousarray(cnt, np.int16)
+    o = np.empty((shape.batch, shape.n_q_heads, n_q, shape.head_dim), np.float64)
+    cs = shape.c()
+    _check(_load().sparda_ref_sparse_attn(ctypes.byref(cs), _ptr(q), n_q, q_pos0, _ptr(k), _ptr(v), kv_mode,
+                                          _ptr(sel), _ptr(cnt), float(sm_scale), _ptr(o)), "sparse_attn")
+    return o
+
+
+def gather_blocks(shape: Shape, host_k, host_v, sel, cnt, stage_k=None, stage_v=None):
+    host_k, host_v = _u16(host_k), _u16(host_v)
+    sel = np.ascontiguousarray(sel, np.int16)
+    cnt = np.ascontiguousarray(cnt, np.int16)
+    st = (shape.batch, shape.n_kv_heads, shape.k_total, shape.block_size, shape.head_dim)
+    if stage_k is None:
+        stage_k = np.zeros(st, np.uint16)
+    if stage_v is None:
+        stage_v = np.zeros(st, np.uint16)
+    cs = shape.c()
+    _check(_load().sparda_ref_gather_blocks(ctypes.byref(cs), _ptr(host_k), _ptr(host_v), _ptr(sel), _ptr(cnt),
+                                            _ptr(stage_k), _ptr(stage_v)), "gather_blocks")
+    return stage_k, stage_v

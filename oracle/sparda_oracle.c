@@ -1,0 +1,352 @@
+/*
+ * sparda_oracle.c -- plain CPU oracle for SparDA's selection + block-sparse attention path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file exists to check the GPU library, never to stand in for
+ * it: only the test suite, the smoke check and the benchmark's CPU-baseline leg load it.  It
+ * shares no source, header, table or helper with the HIP path.
+ *
+ * Every function is the plain definition of what the method computes, written with loops in
+ * float64 (bf16 inputs are exact in float64).  Nothing is blocked, fused or reordered.
+ *
+ *   compress   Key compression, paper Sec. 3 (InfLLM-V2 recap), Eq. 2: one compressed key per
+ *              window of l_C keys with stride s_C, the mean of the window.  Windows of 64 with
+ *              stride 64 (one key per 64-token block) are the only grid this oracle accepts.
+ *   select     Sec. 4.1, Eq. 4 with the attended-set union of Eq. 1: the Forecast row of a GQA
+ *              group scores every compressed key by a plain dot product (one Forecast head per
+ *              group, no softmax, no scale -- "Forecast indexer" paragraph of Sec. 4.1); the
+ *              top-k of those scores, excluding the initial and local blocks, is merged with the
+ *              initial and local blocks.  Ties in score are broken by the lower block index.
+ *   attend     Sec. 3, Eq. 1 and Sec. 4.1, Eq. 5: softmax attention of the query over exactly the
+ *              keys/values of the attended blocks, causal within the query's own block.
+ *   gather     Sec. 4.3 and Alg. 2 (prefetch of the selected blocks): staging slot s holds the 64
+ *              keys/values of block sel[s].
+ *
+ * Readings of the paper that these definitions take (k counts the forced blocks, the local
+ * window is block-granular and contains the query's own block, score ties go to the lower
+ * index, out-of-range selected entries are skipped) are listed with their reasons in the
+ * design notes of the repository.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define REF_OK 0
+#define REF_ERR_INVALID_ARG (-1)
+#define REF_ERR_UNSUPPORTED (-2)
+
+/* The oracle's own description of a problem.  Field meanings:
+ *   batch, n_kv_heads, group_size (query heads per KV head), head_dim,
+ *   block_size (tokens per block), cmp_kernel / cmp_stride (compression window),
+ *   n_init (initial blocks always attended), n_local (local blocks always attended, counting the
+ *   query's own block), k_total (attended-set size, forced blocks included),
+ *   t_cap (token capacity = T stride of the K/V caches), nc_cap (block capacity of K~). */
+typedef struct {
+  int32_t batch, n_kv_heads, group_size, head_dim;
+  int32_t block_size, cmp_kernel, cmp_stride;
+  int32_t n_init, n_local, k_total;
+  int64_t t_cap, nc_cap;
+} ref_shape;
+
+/* ---- bf16 <-> float64 ------------------------------------------------------------------ */
+
+double sparda_ref_bf16_to_f64(uint16_t h) {
+  uint32_t u = ((uint32_t)h) << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* Round a float64 straight to the nearest bf16, ties to even (no intermediate float32 step, so
+ * no double rounding).  bf16 has 8 significant bits, 8 exponent bits (bias 127). */
+uint16_t sparda_ref_f64_to_bf16(double x) {
+  uint16_t sign = signbit(x) ? 0x8000u : 0u;
+  double a = fabs(x);
+  if (isnan(x)) return (uint16_t)(sign | 0x7FC0u);
+  if (a == 0.0) return sign;
+  if (isinf(x)) return (uint16_t)(sign | 0x7F80u);
+  int e;
+  double m = frexp(a, &e);             /* a = m * 2^e, 0.5 <= m < 1 */
+  double q = nearbyint(ldexp(m, 8));   /* 8 significant bits, default mode = ties to even */
+  if (q == 256.0) { q = 128.0; e += 1; }
+  int biased = e - 1 + 127;            /* a ~= (q/128) * 2^(e-1) */
+  if (biased >= 255) return (uint16_t)(sign | 0x7F80u);
+  if (biased <= 0) {
+    /* subnormal bf16: the grid is 2^-133 (= 2^-126 * 2^-7); q == 128 lands on the smallest
+     * normal, whose encoding is 0x0080, so the same formula covers it. */
+    double qs = nearbyint(ldexp(a, 133));
+    return (uint16_t)(sign | (uint16_t)qs);
+  }
+  return (uint16_t)(sign | (uint16_t)(biased << 7) | (uint16_t)((int)q - 128));
+}
+
+/* ---- shape checks --------------------------------------------------------------------- */
+
+static int check_shape(const ref_shape* s) {
+  if (!s) return REF_ERR_INVALID_ARG;
+  if (s->batch < 1 || s->n_kv_heads < 1 || s->group_size < 1 || s->head_dim < 1) return REF_ERR_INVALID_ARG;
+  if (s->block_size < 1 || s->n_init < 0 || s->n_local < 1) return REF_ERR_INVALID_ARG;
+  if (s->k_total < s->n_init + s->n_local) return REF_ERR_INVALID_ARG;
+  if (s->t_cap < 1 || s->nc_cap < 0) return REF_ERR_INVALID_ARG;
+  if (s->cmp_kernel != s->block_size || s->cmp_stride != s->block_size) return REF_ERR_UNSUPPORTED;
+  return REF_OK;
+}
+
+/* ---- Eq. 2: mean-pooled compressed keys ------------------------------------------------- */
+
+/* k: bf16 [B][Hkv][t_cap][D];  k_cmp: bf16 [B][Hkv][nc_cap][D].
+ * Writes K~_j for blocks j in [blk_begin, blk_end); each must be complete inside t_ctx. */
+int sparda_ref_compress_keys(const ref_shape* s, const uint16_t* k, int64_t t_ctx, int32_t blk_begin,
+                             int32_t blk_end, uint16_t* k_cmp) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  const int64_t L = s->block_size, D = s->head_dim;
+  if (blk_begin < 0 || blk_end < blk_begin || (int64_t)blk_end > s->nc_cap) return REF_ERR_INVALID_ARG;
+  if ((int64_t)blk_end * L > t_ctx || t_ctx > s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t nrows = (int64_t)s->batch * s->n_kv_heads;
+#pragma omp parallel for schedule(static)
+  for (int64_t bm = 0; bm < nrows; ++bm) {
+    const uint16_t* kh = k + bm * s->t_cap * D;
+    uint16_t* ch = k_cmp + bm * s->nc_cap * D;
+    for (int64_t j = blk_begin; j < blk_end; ++j) {
+      for (int64_t d = 0; d < D; ++d) {
+        double sum = 0.0;
+        for (int64_t t = j * L; t < j * L + L; ++t) sum += sparda_ref_bf16_to_f64(kh[t * D + d]);
+        ch[j * D + d] = sparda_ref_f64_to_bf16(sum / (double)L);
+      }
+    }
+  }
+  return REF_OK;
+}
+
+/* ---- Eq. 1 / Eq. 4: forced blocks, candidates, top-k ------------------------------------- */
+
+typedef struct {
+  double score;
+  int32_t block;
+} scored_block;
+
+/* Order: higher score first, then lower block index first. */
+static int by_score_then_index(const void* pa, const void* pb) {
+  const scored_block* a = (const scored_block*)pa;
+  const scored_block* b = (const scored_block*)pb;
+  if (a->score > b->score) return -1;
+  if (a->score < b->score) return 1;
+  return (a->block > b->block) - (a->block < b->block);
+}
+
+/* One query row (batch b, group m, row r at position p = q_pos0 + r).
+ *   f: bf16 [B][Hkv][n_q][D]; k_cmp: bf16 [B][Hkv][nc_cap][D]
+ *   sel_row: k_total entries, ascending block indices, -1 padded; cnt: number of valid entries.
+ *   scores (optional, nc_cap doubles): the Forecast score of every candidate block, NaN for a
+ *   block that is not a candidate of this row. */
+int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
+                          const uint16_t* k_cmp, int32_t b, int32_t m, int32_t r, int16_t* sel_row,
+                          int16_t* cnt, double* scores) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim, L = s->block_size;
+  const int64_t p = q_pos0 + r;
+  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t blk = p / L;
+
+  /* forced(p): the initial blocks and the local window [blk - n_local + 1, blk]. */
+  const int64_t init_hi = (s->n_init < blk + 1) ? s->n_init : blk + 1;  /* init = [0, init_hi) */
+  int64_t local_lo = blk - s->n_local + 1;
+  if (local_lo < 0) local_lo = 0;
+  if (local_lo < init_hi) local_lo = init_hi;                            /* drop duplicates */
+  const int64_t n_forced = init_hi + (blk - local_lo + 1);
+
+  /* candidates: complete blocks that are neither initial nor local. */
+  const int64_t cand_lo = s->n_init, cand_hi = blk - s->n_local;        /* inclusive */
+  const int64_t n_cand = (cand_hi >= cand_lo) ? cand_hi - cand_lo + 1 : 0;
+  if (n_cand > 0 && cand_hi >= s->nc_cap) return REF_ERR_INVALID_ARG;
+  const int64_t n_sel_budget = s->k_total - n_forced;
+  if (n_sel_budget < 0) return REF_ERR_INVALID_ARG;
+  const int64_t n_take = n_sel_budget < n_cand ? n_sel_budget : n_cand;
+
+  const uint16_t* frow = f + (((int64_t)b * s->n_kv_heads + m) * n_q + r) * D;
+  const uint16_t* kc = k_cmp + ((int64_t)b * s->n_kv_heads + m) * s->nc_cap * D;
+
+  if (scores)
+    for (int64_t j = 0; j < s->nc_cap; ++j) scores[j] = NAN;
+
+  scored_block* list = (scored_block*)malloc(sizeof(scored_block) * (size_t)(n_cand > 0 ? n_cand : 1));
+  if (!list) return REF_ERR_INVALID_ARG;
+  for (int64_t c = 0; c < n_cand; ++c) {
+    const int64_t j = cand_lo + c;
+    double dot = 0.0;
+    for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(frow[d]) * sparda_ref_bf16_to_f64(kc[j * D + d]);
+    list[c].score = dot;
+    list[c].block = (int32_t)j;
+    if (scores) scores[j] = dot;
+  }
+  qsort(list, (size_t)n_cand, sizeof(scored_block), by_score_then_index);
+
+  /* Emit forced U chosen in ascending order.  A membership table over [0, blk] keeps this a
+   * plain set union rather than a merge. */
+  unsigned char* in_set = (unsigned char*)calloc((size_t)(blk + 1), 1);
+  if (!in_set) { free(list); return REF_ERR_INVALID_ARG; }
+  for (int64_t j = 0; j < init_hi; ++j) in_set[j] = 1;
+  for (int64_t j = local_lo; j <= blk; ++j) in_set[j] = 1;
+  for (int64_t c = 0; c < n_take; ++c) in_set[list[c].block] = 1;
+  int64_t n = 0;
+  for (int64_t j = 0; j <= blk; ++j)
+    if (in_set[j]) sel_row[n++] = (int16_t)j;
+  for (int64_t i = n; i < s->k_total; ++i) sel_row[i] = -1;
+  *cnt = (int16_t)n;
+  free(in_set);
+  free(list);
+  return REF_OK;
+}
+
+/* All rows.  sel: int16 [B][Hkv][n_q][k_total]; cnt: int16 [B][Hkv][n_q]. */
+int sparda_ref_forecast_select(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
+                               const uint16_t* k_cmp, int16_t* sel, int16_t* cnt) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n_q < 1) return REF_ERR_INVALID_ARG;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  int err = REF_OK;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t i = 0; i < rows; ++i) {
+    const int32_t r = (int32_t)(i % n_q);
+    const int32_t m = (int32_t)((i / n_q) % s->n_kv_heads);
+    const int32_t b = (int32_t)(i / ((int64_t)n_q * s->n_kv_heads));
+    int e = sparda_ref_select_row(s, f, n_q, q_pos0, k_cmp, b, m, r, sel + i * s->k_total, cnt + i, NULL);
+    if (e) {
+#pragma omp critical
+      err = e;
+    }
+  }
+  return err;
+}
+
+/* ---- Eq. 1 / Eq. 5: attention over the attended blocks ---------------------------------- */
+
+/* One (batch b, query head h, row r).  q: bf16 [B][Hq][n_q][D].
+ * kv_mode 0: k, v are full caches bf16 [B][Hkv][t_cap][D], token t at row t.
+ * kv_mode 1: k, v are staging buffers bf16 [B][Hkv][k_total][block][D] for a single query row
+ *            (n_q == 1); slot s holds the tokens of block sel[s].
+ * sel/cnt as produced by select; an entry outside [0, blk(p)] is skipped.  Tokens after p are
+ * never attended.  out: D doubles; all zeros when no token is attended. */
+int sparda_ref_attend_row(const ref_shape* s, const uint16_t* q, int32_t n_q, int64_t q_pos0,
+                          const uint16_t* k, const uint16_t* v, int32_t kv_mode, const int16_t* sel,
+                          const int16_t* cnt, double sm_scale, int32_t b, int32_t h, int32_t r, double* out) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  const int64_t D = s->head_dim, L = s->block_size, G = s->group_size;
+  const int64_t Hq = (int64_t)s->n_kv_heads * G;
+  if (b < 0 || b >= s->batch || h < 0 || h >= Hq || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
+  if (kv_mode != 0 && kv_mode != 1) return REF_ERR_INVALID_ARG;
+  if (kv_mode == 1 && n_q != 1) return REF_ERR_INVALID_ARG;
+  const int64_t p = q_pos0 + r;
+  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t blk = p / L;
+  const int64_t m = h / G;  /* consecutive query heads share a KV head */
+  const int64_t row = ((int64_t)b * s->n_kv_heads + m) * n_q + r;
+  const int16_t* srow = sel + row * s->k_total;
+  int64_t n_sel = cnt[row];
+  if (n_sel > s->k_total) n_sel = s->k_total;
+
+  const uint16_t* qrow = q + (((int64_t)b * Hq + h) * n_q + r) * D;
+  /* Collect the attended tokens as (pointer to key row, pointer to value row). */
+  const int64_t max_tok = n_sel * L;
+  const uint16_t** krows = (const uint16_t**)malloc(sizeof(void*) * (size_t)(max_tok > 0 ? max_tok : 1));
+  const uint16_t** vrows = (const uint16_t**)malloc(sizeof(void*) * (size_t)(max_tok > 0 ? max_tok : 1));
+  double* z = (double*)malloc(sizeof(double) * (size_t)(max_tok > 0 ? max_tok : 1));
+  if (!krows || !vrows || !z) { free(krows); free(vrows); free(z); return REF_ERR_INVALID_ARG; }
+  int64_t n_tok = 0;
+  for (int64_t sidx = 0; sidx < n_sel; ++sidx) {
+    const int64_t j = srow[sidx];
+    if (j < 0 || j > blk) continue;
+    for (int64_t i = 0; i < L; ++i) {
+      const int64_t t = j * L + i;
+      if (t > p) break;
+      if (kv_mode == 0) {
+        const int64_t base = (((int64_t)b * s->n_kv_heads + m) * s->t_cap + t) * D;
+        krows[n_tok] = k + base;
+        vrows[n_tok] = v + base;
+      } else {
+        const int64_t base = ((((int64_t)b * s->n_kv_heads + m) * s->k_total + sidx) * L + i) * D;
+        krows[n_tok] = k + base;
+        vrows[n_tok] = v + base;
+      }
+      ++n_tok;
+    }
+  }
+  for (int64_t d = 0; d < D; ++d) out[d] = 0.0;
+  if (n_tok > 0) {
+    double zmax = -INFINITY;
+    for (int64_t t = 0; t < n_tok; ++t) {
+      double dot = 0.0;
+      for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(qrow[d]) * sparda_ref_bf16_to_f64(krows[t][d]);
+      z[t] = sm_scale * dot;
+      if (z[t] > zmax) zmax = z[t];
+    }
+    double denom = 0.0;
+    for (int64_t t = 0; t < n_tok; ++t) {
+      z[t] = exp(z[t] - zmax);
+      denom += z[t];
+    }
+    for (int64_t t = 0; t < n_tok; ++t) {
+      const double w = z[t] / denom;
+      for (int64_t d = 0; d < D; ++d) out[d] += w * sparda_ref_bf16_to_f64(vrows[t][d]);
+    }
+  }
+  free(krows);
+  free(vrows);
+  free(z);
+  return REF_OK;
+}
+
+/* All (b, h, r).  o: float64 [B][Hq][n_q][D]. */
+int sparda_ref_sparse_attn(const ref_shape* s, const uint16_t* q, int32_t n_q, int64_t q_pos0, const uint16_t* k,
+                           const uint16_t* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt,
+                           double sm_scale, double* o) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n_q < 1) return REF_ERR_INVALID_ARG;
+  const int64_t Hq = (int64_t)s->n_kv_heads * s->group_size;
+  const int64_t rows = (int64_t)s->batch * Hq * n_q;
+  int err = REF_OK;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t i = 0; i < rows; ++i) {
+    const int32_t r = (int32_t)(i % n_q);
+    const int32_t h = (int32_t)((i / n_q) % Hq);
+    const int32_t b = (int32_t)(i / ((int64_t)n_q * Hq));
+    int e = sparda_ref_attend_row(s, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale, b, h, r,
+                                  o + i * s->head_dim);
+    if (e) {
+#pragma omp critical
+      err = e;
+    }
+  }
+  return err;
+}
+
+/* ---- Sec. 4.3 / Alg. 2: copy selected blocks into staging ------------------------------- */
+
+/* host_k/host_v: bf16 [B][Hkv][t_cap][D]; sel/cnt from a single-row select ([B][Hkv][k_total],
+ * [B][Hkv]); stage_k/stage_v: bf16 [B][Hkv][k_total][block][D].  Slot s < cnt receives the whole
+ * block sel[s]; other slots and entries whose block lies outside the cache are left untouched. */
+int sparda_ref_gather_blocks(const ref_shape* s, const uint16_t* host_k, const uint16_t* host_v,
+                             const int16_t* sel, const int16_t* cnt, uint16_t* stage_k, uint16_t* stage_v) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  const int64_t D = s->head_dim, L = s->block_size;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads;
+  for (int64_t bm = 0; bm < rows; ++bm) {
+    int64_t n = cnt[bm];
+    if (n > s->k_total) n = s->k_total;
+    for (int64_t sidx = 0; sidx < n; ++sidx) {
+      const int64_t j = sel[bm * s->k_total + sidx];
+      if (j < 0 || (j + 1) * L > s->t_cap) continue;
+      const size_t bytes = (size_t)(L * D) * sizeof(uint16_t);
+      memcpy(stage_k + (bm * s->k_total + sidx) * L * D, host_k + (bm * s->t_cap + j * L) * D, bytes);
+      memcpy(stage_v + (bm * s->k_total + sidx) * L * D, host_v + (bm * s->t_cap + j * L) * D, bytes);
+    }
+  }
+  return REF_OK;
+}

@@ -1,0 +1,75 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and check that the pins catch
+each one: a flipped sort direction, a dropped softmax scale, an off-by-one local window, a
+causal mask that lets the next token in, an init block left out of the candidates' exclusion,
+a swapped operand index in the score, and a rounding mode change in the compressed keys."""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import brute
+import oracle
+from paper_2606_04511_amd import inputs
+
+MUTANTS = {
+    "sort_ascending": ("if (a->score > b->score) return -1;", "if (a->score < b->score) return -1;"),
+    "index_tiebreak_reversed": ("return (a->block > b->block) - (a->block < b->block);",
+                                "return (a->block < b->block) - (a->block > b->block);"),
+    "scale_dropped": ("z[t] = sm_scale * dot;", "z[t] = dot;"),
+    "local_window_short": ("int64_t local_lo = blk - s->n_local + 1;", "int64_t local_lo = blk - s->n_local + 2;"),
+    "causal_leak": ("if (t > p) break;", "if (t > p + 1) break;"),
+    "candidates_include_init": ("const int64_t cand_lo = s->n_init,", "const int64_t cand_lo = 0,"),
+    "score_wrong_operand": ("sparda_ref_bf16_to_f64(kc[j * D + d])", "sparda_ref_bf16_to_f64(kc[d * D + j % D])"),
+    "compress_truncates": ("double q = nearbyint(ldexp(m, 8));", "double q = floor(ldexp(m, 8));"),
+    "compress_wrong_divisor": ("sum / (double)L", "sum / (double)(L - 1)"),
+}
+
+
+def _pins_pass(o) -> bool:
+    """A compact subset of the pins: brute-force select, dense-masked attention, compress."""
+    rng_seed = 41
+    T, n_q, H, G = 640, 130, 2, 4
+    s = o.Shape(batch=1, n_kv_heads=H, group_size=G, head_dim=128, n_init=1, n_local=2, k_total=5, t_cap=640,
+                nc_cap=9)
+    u = lambda shp, tid: inputs.to_u16(inputs.normal_bf16(shp, rng_seed, tid))
+    k = u((1, H, 640, 128), 2)
+    v = u((1, H, 640, 128), 3)
+    q = u((1, H * G, n_q, 128), 0)
+    f = u((1, H, n_q, 128), 1)
+    try:
+        kc = o.compress_keys(s, k, 640, 0, 9)
+        if not np.array_equal(kc, brute.compress(k, 9)):
+            return False
+        sel, cnt = o.forecast_select(s, f, n_q, T - n_q, kc)
+        bsel, bcnt, _ = brute.select_rows(f, kc, T - n_q, 5, 1, 2)
+        if not (np.array_equal(sel, bsel) and np.array_equal(cnt, bcnt)):
+            return False
+        scale = 1.0 / math.sqrt(128)
+        got = o.sparse_attn(s, q, n_q, T - n_q, k, v, 0, bsel, bcnt, scale)
+        want = brute.attend_dense_masked(q, k, v, bsel, bcnt, T - n_q, G, scale)
+        if not np.allclose(got, want, rtol=0, atol=1e-12):
+            return False
+        # the hand-worked tie (test_select_worked_example_with_tie): block 1 beats block 3
+        to = lambda a: np.array(a, np.float32).view(np.uint32).__rshift__(16).astype(np.uint16)
+        s2 = o.Shape(batch=1, n_kv_heads=1, group_size=1, head_dim=2, n_init=1, n_local=2, k_total=5,
+                     t_cap=448, nc_cap=7)
+        kc2 = to([[[[9, 9], [1, 0], [0, 4], [2, -2], [-1, 0], [9, 9], [9, 9]]]])
+        sel2, cnt2, _ = o.select_row(s2, to([[[[1.0, 0.5]]]]), 1, 447, kc2, 0, 0, 0)
+        return cnt2 == 5 and list(sel2) == [0, 1, 2, 5, 6]
+    except oracle.OracleError:
+        return False
+
+
+def test_unmutated_oracle_passes(oracle_lib):
+    assert _pins_pass(oracle_lib)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(oracle_lib, tmp_path, name):
+    old, new = MUTANTS[name]
+    src = oracle.source_text()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    path = oracle.build_variant(src.replace(old, new), os.path.join(str(tmp_path), f"mut_{name}.so"))
+    with oracle.use_library(path):
+        assert not _pins_pass(oracle), f"mutant {name} slipped past the pins"
