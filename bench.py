@@ -1,0 +1,333 @@
+"""Benchmark of the SparDA selection + block-sparse attention path on one MI355X.
+
+Timed step (the headline): one decode layer at 128K context, batch 32, 32 query / 8 KV heads,
+head_dim 128, 64-token blocks, k = 64 blocks (1 initial + 2 local forced):
+    incremental K~ update of the block completed by the newest token
+    -> Forecast scoring + top-k of every (batch, group) row
+    -> block-sparse attention of all 32 query heads over the selected blocks.
+value = algorithmic HBM bytes of the step / step time (GB/s); ms_per_step is the layer time.
+
+Secondary legs on the same JSON line:
+  prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
+                    selects), reported in TFLOP/s of scored (row, candidate) pairs x 2 x 128;
+  prefill_attn   -- block-sparse attention of that prefill (ms);
+  gather         -- host-pool -> HBM gather of the selected blocks of a batch-64, 128K decode
+                    layer (GB/s over PCIe), with --gather (off by default: it pins ~34 GB).
+roofline -- the dominant kernel (decode attention): algorithmic bytes / its average duration
+            measured with HIP events on the stream it runs on, against 8 TB/s.
+cpu_baseline -- the CPU oracle on a sample of the decode step's rows, on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2606_04511_amd.sparda as sp  # noqa: E402
+from paper_2606_04511_amd import inputs  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+SCALE = 1.0 / math.sqrt(128)
+METRIC = "decode select+sparse-attn us/layer & HBM GB/s at 128K; prefill select TFLOP/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def ws_tensor(shape, op, n_q, q_pos0, dev):
+    n = sp.sparda_workspace_size(shape, op, n_q, q_pos0)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
+
+
+class DecodeLayer:
+    """Device buffers of one decode layer and the three library calls of its step."""
+
+    def __init__(self, w: inputs.Workload, dev):
+        self.w = w
+        T, nb = w.seq_len, w.n_blocks
+        self.T, self.nb = T, nb
+        self.shape = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size,
+                                    k_total=w.k_total, t_cap=T, nc_cap=nb, n_init=w.n_init, n_local=w.n_local)
+        t0 = time.time()
+        self.case = inputs.make_case(w, device=dev)
+        log(f"[bench] generated {w.name} on the GPU in {time.time() - t0:.1f}s")
+        c = self.case
+        self.q, self.f, self.k, self.v = c["q"], c["f"], c["k"], c["v"]
+        self.kc = torch.zeros(w.batch, w.n_kv_heads, nb, 128, dtype=torch.bfloat16, device=dev)
+        self.sel = torch.empty(w.batch, w.n_kv_heads, 1, w.k_total, dtype=torch.int16, device=dev)
+        self.cnt = torch.empty(w.batch, w.n_kv_heads, 1, dtype=torch.int16, device=dev)
+        self.o = torch.empty(w.batch, w.n_q_heads, 1, 128, dtype=torch.bfloat16, device=dev)
+        self.ws_sel = ws_tensor(self.shape, sp.SPARDA_OP_FORECAST_SELECT, 1, T - 1, dev)
+        self.ws_att = ws_tensor(self.shape, sp.SPARDA_OP_SPARSE_ATTN, 1, T - 1, dev)
+        # K~ of every complete block is precomputed (not timed); the step refreshes the newest one.
+        sp.sparda_compress_keys(self.shape, self.k, T, 0, nb, self.kc)
+        torch.cuda.synchronize()
+
+    def compress_new(self):
+        sp.sparda_compress_keys(self.shape, self.k, self.T, self.nb - 1, self.nb, self.kc)
+
+    def select(self):
+        sp.sparda_forecast_select(self.shape, self.f, 1, self.T - 1, self.kc, self.sel, self.cnt, self.ws_sel)
+
+    def attend(self):
+        sp.sparda_sparse_attn(self.shape, self.q, 1, self.T - 1, self.k, self.v, 0, self.sel, self.cnt, SCALE, self.o,
+                              self.ws_att)
+
+    def step(self):
+        self.compress_new()
+        self.select()
+        self.attend()
+
+    def bytes(self):
+        """Algorithmic HBM bytes of one step, by part."""
+        w = self.w
+        rows = w.batch * w.n_kv_heads
+        n_cand = self.nb - 1 - w.n_local - w.n_init + 1  # candidates of the decode row
+        return {
+            "compress_new": rows * (64 * 256 + 256),
+            "select": rows * (256 + n_cand * 256 + w.k_total * 2 + 2),
+            "attend": rows * (w.k_total * 2 * 64 * 256 + w.k_total * 2 + 2) + 2 * w.batch * w.n_q_heads * 256,
+        }
+
+
+def time_events(fn, iters, stream):
+    """Average ms of fn() over iters launches, HIP events on `stream` around each launch."""
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(iters)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(iters)]
+    for i in range(iters):
+        starts[i].record(stream)
+        fn()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    return float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
+
+
+def prefill_leg(dev, warmup, iters):
+    w = inputs.WORKLOADS["prefill_b1_t32k"]
+    T, nb = w.seq_len, w.n_blocks
+    shape = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size, k_total=w.k_total,
+                           t_cap=T, nc_cap=nb, n_init=w.n_init, n_local=w.n_local)
+    t0 = time.time()
+    case = inputs.make_case(w, device=dev)
+    log(f"[bench] generated {w.name} on the GPU in {time.time() - t0:.1f}s")
+    kc = torch.zeros(w.batch, w.n_kv_heads, nb, 128, dtype=torch.bfloat16, device=dev)
+    sp.sparda_compress_keys(shape, case["k"], T, 0, nb, kc)
+    sel = torch.empty(w.batch, w.n_kv_heads, T, w.k_total, dtype=torch.int16, device=dev)
+    cnt = torch.empty(w.batch, w.n_kv_heads, T, dtype=torch.int16, device=dev)
+    o = torch.empty(w.batch, w.n_q_heads, T, 128, dtype=torch.bfloat16, device=dev)
+    ws_s = ws_tensor(shape, sp.SPARDA_OP_FORECAST_SELECT, T, 0, dev)
+    ws_a = ws_tensor(shape, sp.SPARDA_OP_SPARSE_ATTN, T, 0, dev)
+    stream = torch.cuda.current_stream()
+
+    def select():
+        sp.sparda_forecast_select(shape, case["f"], T, 0, kc, sel, cnt, ws_s)
+
+    def attend():
+        sp.sparda_sparse_attn(shape, case["q"], T, 0, case["k"], case["v"], 0, sel, cnt, SCALE, o, ws_a)
+
+    for _ in range(warmup):
+        select()
+    ms_sel = time_events(select, iters, stream)
+    attend()
+    ms_att = time_events(attend, max(2, iters // 10), stream)
+    # scored (row, candidate) pairs: rows whose candidates outnumber their free slots
+    flops = 0
+    attn_flops = 0
+    for r in range(T):
+        blk = r // 64
+        n_cand = max(0, blk - w.n_local - w.n_init + 1)
+        n_forced = min(w.n_init, blk + 1) + (blk - max(max(0, blk - w.n_local + 1), min(w.n_init, blk + 1)) + 1)
+        if w.k_total - n_forced < n_cand:
+            flops += 2 * 128 * n_cand
+        n_sel_blocks = min(w.k_total, blk + 1)
+        attn_flops += 4 * 128 * ((n_sel_blocks - 1) * 64 + (r % 64) + 1)
+    flops *= w.batch * w.n_kv_heads
+    attn_flops *= w.batch * w.n_q_heads
+    return {
+        "workload": "prefill B1 T=32768 Hq32/Hkv8 D128 block64 k64, all 32768 rows",
+        "select_ms": ms_sel,
+        "select_tflops": flops / (ms_sel * 1e-3) / 1e12,
+        "select_frac_bf16_peak": flops / (ms_sel * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+        "select_gflop": flops / 1e9,
+        "attn_ms": ms_att,
+        "attn_tflops": attn_flops / (ms_att * 1e-3) / 1e12,
+    }
+
+
+def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
+    """The oracle on n_rows sampled (batch, group) rows of the decode step, all host cores."""
+    import oracle
+    w = layer.w
+    T, nb, G = layer.T, layer.nb, w.group_size
+    rng = np.random.default_rng(11)
+    pairs = [(int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads))) for _ in range(n_rows)]
+    k = np.stack([inputs.to_u16(layer.k[b, m]) for b, m in pairs])[:, None]
+    v = np.stack([inputs.to_u16(layer.v[b, m]) for b, m in pairs])[:, None]
+    f = np.stack([inputs.to_u16(layer.f[b, m]) for b, m in pairs])[:, None]
+    q = np.stack([inputs.to_u16(layer.q[b, m * G:(m + 1) * G]) for b, m in pairs])
+    kc = np.stack([inputs.to_u16(layer.kc[b, m]) for b, m in pairs])[:, None].copy()
+    oshape = oracle.Shape(batch=n_rows, n_kv_heads=1, group_size=G, k_total=w.k_total, t_cap=T, nc_cap=nb,
+                          n_init=w.n_init, n_local=w.n_local)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    reps = 0
+    t0 = time.perf_counter()
+    while True:  # repeat the sample until about min_seconds of CPU work
+        oracle.compress_keys(oshape, k, T, nb - 1, nb, kc)
+        sel, cnt = oracle.forecast_select(oshape, f, 1, T - 1, kc)
+        oracle.sparse_attn(oshape, q, 1, T - 1, k, v, 0, sel, cnt, SCALE)
+        reps += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = (time.perf_counter() - t0) / reps
+    parts = layer.bytes()
+    rows_total = w.batch * w.n_kv_heads
+    sample_bytes = sum(parts.values()) * n_rows / rows_total
+    return {"value": sample_bytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_rows} of {rows_total} (batch, group) rows of the 128K decode step "
+                      f"(incremental compress + select + attend), {dt:.3f}s per pass, {reps} passes",
+            "us_per_layer_equiv": dt * rows_total / n_rows * 1e6}
+
+
+def gather_leg(dev, iters):
+    """Gather of a batch-64, 128K decode layer's selected blocks from one pinned host pool."""
+    from paper_2606_04511_amd import hostmem
+    w = inputs.WORKLOADS["pipeline_b64_t128k_l32"]
+    B, H, T, nb, k_total = w.batch, w.n_kv_heads, w.seq_len, w.n_blocks, w.k_total
+    shape = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=w.group_size, k_total=k_total, t_cap=T, nc_cap=nb)
+    pool_bytes = B * H * T * 128 * 2
+    t0 = time.time()
+    hk = hostmem.PinnedBuffer(pool_bytes)
+    hv = hostmem.PinnedBuffer(pool_bytes)
+    fill = torch.randn(64 * 1024 * 1024, device=dev).to(torch.bfloat16)  # 128 MiB pattern
+    chunk = fill.numel() * 2
+    for buf in (hk, hv):
+        for off in range(0, pool_bytes, chunk):
+            n = min(chunk, pool_bytes - off)
+            buf.copy_from_device(off, fill.view(torch.uint8)[:n])
+    torch.cuda.synchronize()
+    log(f"[bench] pinned + filled 2 x {pool_bytes / 2**30:.1f} GiB host pools in {time.time() - t0:.1f}s")
+    g = torch.Generator(device="cpu").manual_seed(w.seed)
+    sel = torch.empty(B, H, k_total, dtype=torch.int16)
+    for i in range(B * H):
+        blocks = torch.cat([torch.tensor([0, nb - 2, nb - 1]), 1 + torch.randperm(nb - 3, generator=g)[:k_total - 3]])
+        sel.view(-1, k_total)[i] = torch.sort(blocks).values.to(torch.int16)
+    sel = sel.to(dev)
+    cnt = torch.full((B, H), k_total, dtype=torch.int16, device=dev)
+    st_k = torch.empty(B, H, k_total, 64, 128, dtype=torch.bfloat16, device=dev)
+    st_v = torch.empty_like(st_k)
+    side = torch.cuda.Stream()
+    res = {}
+    moved = 2 * B * H * k_total * 64 * 256
+    for nwg in (16, 32, 64, 128, 256):
+        with torch.cuda.stream(side):
+            sp.sparda_gather_blocks(shape, hk.ptr, hv.ptr, sel, cnt, st_k, st_v, nwg, side)
+            ms = time_events(lambda: sp.sparda_gather_blocks(shape, hk.ptr, hv.ptr, sel, cnt, st_k, st_v, nwg, side),
+                             iters, side)
+        res[str(nwg)] = {"ms": ms, "GBps": moved / (ms * 1e-3) / 1e9}
+    # H2D memcpy reference of the same byte count from the same pinned pool
+    dst = torch.empty(moved // 2, dtype=torch.uint8, device=dev)
+    ms_cp = time_events(lambda: hk.copy_to_device(0, dst), iters, torch.cuda.current_stream())
+    best = max(res.values(), key=lambda r: r["GBps"])
+    return {"workload": f"decode B{B} T={T} k{k_total}: {moved / 1e9:.3f} GB of selected K+V blocks per layer",
+            "by_workgroups": res, "best_GBps": best["GBps"], "h2d_memcpy_GBps": (moved // 2) / (ms_cp * 1e-3) / 1e9}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--gather", action="store_true", help="also time the host-pool gather (pins ~34 GB)")
+    ap.add_argument("--cpu-rows", type=int, default=32)
+    ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    sp.load()
+
+    if args.calib_copy:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("[bench] calibration copy of 1 GiB done (x3)")
+
+    w = inputs.WORKLOADS["decode_b32_t128k"]
+    layer = DecodeLayer(w, dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        layer.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer.step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    parts = layer.bytes()
+    step_bytes = sum(parts.values())
+    log(f"[bench] decode step {ms_step * 1e3:.1f} us")
+
+    # per-call event timing (the dominant kernel is the attention)
+    ms_sel = time_events(layer.select, args.steps, stream)
+    ms_att = time_events(layer.attend, args.steps, stream)
+    ms_cmp = time_events(layer.compress_new, args.steps, stream)
+    att_bytes = parts["attend"]
+    achieved = att_bytes / (ms_att * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": step_bytes / (ms_step * 1e-3) / 1e9,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 with 5% planted blocks)",
+        "config": {"workload": "decode layer B32 T=131072 Hq32/Hkv8 D128 block64 k64 (1 init + 2 local)",
+                   "batch": w.batch, "seq_len": w.seq_len, "k_blocks": w.k_total, "parallelism": "none (1 GPU)"},
+        "us_per_layer": ms_step * 1e3,
+        "frac_hbm_peak": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "step_bytes": step_bytes,
+        "parts_us": {"compress_new": ms_cmp * 1e3, "select": ms_sel * 1e3, "attend": ms_att * 1e3},
+        "roofline": {"bound": "hbm", "kernel": "sparse_attn (decode, split-K + combine)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att},
+    }
+    if not args.no_prefill:
+        del layer.case
+        out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
+        log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
+            f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
+    if args.gather:
+        out["gather"] = gather_leg(dev, 5)
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(layer, args.cpu_rows)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

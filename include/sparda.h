@@ -1,0 +1,173 @@
+/*
+ * sparda.h -- C ABI of the MI355X (gfx950) SparDA selection + block-sparse attention library.
+ *
+ * SparDA (Sparse Decoupled Attention) adds a Forecast projection F to every layer.  The
+ * Forecast row of layer l, one head per GQA group, scores the mean-pooled block keys K~ of layer
+ * l+1; the top-k blocks, merged with the initial and local blocks, are the only KV blocks that
+ * layer l+1 attends to (paper Sec. 4.1, Eq. 3-5; the attended-set structure is Eq. 1 of Sec. 3).
+ * This library implements that data path on one GPU:
+ *
+ *   sparda_compress_keys    K -> K~               (Sec. 3, Eq. 2)
+ *   sparda_forecast_select  F, K~ -> block sets   (Sec. 4.1, Eq. 4 with Eq. 1)
+ *   sparda_sparse_attn      Q, K, V, sets -> O    (Sec. 4.1, Eq. 5 with Eq. 1)
+ *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
+ *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
+ *
+ * Conventions shared by every call:
+ *   - Every function returns an int status: SPARDA_OK (0) or a negative SPARDA_ERR_* code.  No
+ *     call throws, aborts or prints.  sparda_last_error_detail() gives a human-readable reason
+ *     for the last failure of the calling thread.
+ *   - Tensors are bf16 (passed as void*, 2 bytes per element, IEEE bfloat16 bits), dense and
+ *     row-major in the layouts given per argument.  Block indices are int16.
+ *   - Device pointers must be 16-byte aligned device (HBM) memory owned by the caller.  The
+ *     library allocates nothing and keeps no state beyond a thread-local error string: every
+ *     buffer, workspace and stream belongs to the caller and must stay alive until the work
+ *     enqueued on the stream has completed.
+ *   - Every compute call only enqueues work on the given stream and returns; argument errors are
+ *     reported synchronously before anything is enqueued (nothing is written on error); a failed
+ *     launch returns SPARDA_ERR_HIP; device faults surface at the caller's next synchronisation.
+ *   - Ordering between streams (e.g. a gather on a side stream and the attention that reads its
+ *     staging buffer) is the caller's: record an event after the gather and make the compute
+ *     stream wait on it.
+ *   - v1 limits: head_dim 128, block 64, compression window (64, 64) -- one key per block --,
+ *     group_size 1..16, block indices < 32768.  Other values return SPARDA_ERR_UNSUPPORTED.
+ *
+ * Notation: B batch, Hkv KV heads (= Forecast heads = GQA groups), G query heads per group,
+ * Hq = Hkv * G, D head_dim, L block size (64), n_q query rows per (batch, group), p = q_pos0 + r
+ * the position of row r, blk(p) = p / L.  Query head h belongs to group h / G.
+ */
+#ifndef SPARDA_H
+#define SPARDA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum sparda_status {
+  SPARDA_OK = 0,
+  SPARDA_ERR_INVALID_ARG = -1,     /* null/misaligned pointer, inconsistent sizes, bad range   */
+  SPARDA_ERR_UNSUPPORTED = -2,     /* valid but outside the v1 limits listed above             */
+  SPARDA_ERR_WORKSPACE = -3,       /* workspace smaller than sparda_workspace_size() reports   */
+  SPARDA_ERR_HOST_NOT_MAPPED = -4, /* gather source is not device-accessible pinned host memory */
+  SPARDA_ERR_HIP = -5              /* a HIP runtime call or kernel launch failed                */
+};
+
+/* Problem description shared by all calls. */
+typedef struct sparda_shape {
+  uint32_t struct_size;  /* = sizeof(sparda_shape); lets the ABI grow                          */
+  int32_t batch;         /* B >= 1                                                              */
+  int32_t n_kv_heads;    /* Hkv >= 1: KV heads, one Forecast head each                          */
+  int32_t group_size;    /* G in 1..16: query heads per KV head (GQA group)                     */
+  int32_t head_dim;      /* D: 128                                                              */
+  int32_t block_size;    /* L: 64 tokens per block                                              */
+  int32_t cmp_kernel;    /* compression window length l_C: 64 (one key per block)              */
+  int32_t cmp_stride;    /* compression stride s_C: 64                                          */
+  int32_t n_init;        /* initial blocks always attended (>= 0)                               */
+  int32_t n_local;       /* local blocks always attended, the query's own block included (>= 1) */
+  int32_t k_total;       /* attended-set size per query row, forced blocks included;            */
+                         /* n_init + n_local <= k_total <= 32767                                */
+  int64_t t_cap;         /* token capacity (T stride) of the K/V caches; a multiple of L        */
+  int64_t nc_cap;        /* block capacity (stride) of the K~ cache                             */
+} sparda_shape;
+
+/* Workspace owners for sparda_workspace_size(). */
+enum sparda_op { SPARDA_OP_FORECAST_SELECT = 1, SPARDA_OP_SPARSE_ATTN = 2 };
+
+/*
+ * sparda_compress_keys -- mean-pooled block keys (Sec. 3, Eq. 2 with l_C = s_C = L).
+ *   k_cache  in : bf16 [B][Hkv][t_cap][D] device.
+ *   t_ctx       : tokens currently valid in k_cache (t_ctx <= t_cap).
+ *   blk_begin, blk_end : compress blocks j in [blk_begin, blk_end); every one must be complete,
+ *                 i.e. blk_end * L <= t_ctx, and blk_end <= nc_cap.  In decode, call it with the
+ *                 single block completed by the newest token (the incremental K~ update of
+ *                 Alg. 2); blk_begin == blk_end is a no-op.
+ *   k_cmp   out : bf16 [B][Hkv][nc_cap][D] device; only rows [blk_begin, blk_end) are written.
+ *   K~_j = round_to_nearest_even_bf16( (1/L) * sum of the L keys of block j ), the sum being
+ *   exact for bf16 inputs (float64 accumulation), so the result does not depend on order.
+ */
+int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t blk_begin,
+                         int32_t blk_end, void* k_cmp, hipStream_t stream);
+
+/*
+ * sparda_forecast_select -- attended block set of every query row (Sec. 4.1, Eq. 4; Eq. 1).
+ *   f      in  : bf16 [B][Hkv][n_q][D] device, the Forecast rows (one head per group).  For a
+ *                one-layer-ahead selection these are layer l's Forecast rows and k_cmp is layer
+ *                l+1's K~ (Eq. 4); for layer 0 they are the current-layer Forecast.
+ *   n_q        : rows per (batch, group), >= 1.  n_q == 1 is the decode form.
+ *   q_pos0     : position of row 0; row r is at p = q_pos0 + r; p < t_cap.
+ *   k_cmp  in  : bf16 [B][Hkv][nc_cap][D] device; blocks 0 .. blk(p_max) - n_local must be valid.
+ *   sel    out : int16 [B][Hkv][n_q][k_total] device: ascending block indices, -1 padded.
+ *   cnt    out : int16 [B][Hkv][n_q] device: valid entries of each row = min(k_total, blk(p)+1).
+ *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_FORECAST_SELECT).
+ * Per row: forced = blocks [0, n_init) U [blk(p) - n_local + 1, blk(p)] (clipped to >= 0);
+ * candidates = [n_init, blk(p) - n_local]; each candidate j scores s_j = F_row . K~_j (float32
+ * accumulation, no softmax, no scale); the k_total - |forced| best candidates by (score
+ * descending, block index ascending) are added to the forced blocks.  All G query heads of a
+ * group share the set.
+ */
+int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
+                           const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/*
+ * sparda_sparse_attn -- block-sparse attention over the attended sets (Sec. 4.1, Eq. 5; Eq. 1).
+ *   q      in  : bf16 [B][Hq][n_q][D] device.
+ *   n_q, q_pos0: as for select (row r is at position p = q_pos0 + r).
+ *   k, v   in  : kv_mode 0 -- bf16 [B][Hkv][t_cap][D] device, the full caches (token t in row t).
+ *                kv_mode 1 -- bf16 [B][Hkv][k_total][L][D] device staging filled by
+ *                sparda_gather_blocks: slot s holds the L tokens of block sel[s].  Decode only
+ *                (n_q == 1).
+ *   sel, cnt in: as produced by sparda_forecast_select (any order of the first cnt entries is
+ *                accepted; entries outside [0, blk(p)] are skipped; duplicates are the caller's
+ *                error and are attended twice).
+ *   sm_scale   : logit scale, normally 1/sqrt(D).
+ *   o      out : bf16 [B][Hq][n_q][D] device.  A row that attends no token gets zeros.
+ *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_SPARSE_ATTN).
+ * o = softmax(sm_scale * q K_S^T) V_S over the tokens t <= p of the attended blocks S, with bf16
+ * inputs, float32 accumulation and online softmax.
+ */
+int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
+                       const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
+                       void* o, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sparda_gather_blocks -- copy the selected blocks of a host-resident KV pool into HBM staging
+ * (Sec. 4.3 persistent prefetch; Alg. 2 "launch prefetch of B_{l+1}").
+ *   host_k, host_v in : bf16 [B][Hkv][t_cap][D] pinned host memory mapped into the device
+ *                       address space (e.g. hipHostMalloc); SPARDA_ERR_HOST_NOT_MAPPED otherwise.
+ *   sel, cnt       in : device, decode-form selection: int16 [B][Hkv][k_total] and [B][Hkv].
+ *   stage_k, stage_v out : bf16 [B][Hkv][k_total][L][D] device; slot s < cnt receives block
+ *                       sel[s]; other slots are untouched; entries with (sel+1)*L > t_cap are
+ *                       skipped.
+ *   n_workgroups      : size of the persistent grid (the CU budget the copy may occupy), >= 1;
+ *                       the grid loops over all (batch, group, slot) copy tasks.
+ *   stream            : normally a side stream distinct from the compute stream.
+ */
+int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
+                         const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
+                         hipStream_t stream);
+
+/*
+ * sparda_workspace_size -- device workspace bytes that call `op` (a sparda_op) needs for n_q
+ * rows starting at position q_pos0 (the same n_q and q_pos0 as the call).
+ *   Returns SPARDA_OK and writes *bytes (0 is possible); argument errors as for the call itself.
+ *   The workspace is scratch: its contents are not needed between calls.
+ */
+int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, int64_t q_pos0, size_t* bytes);
+
+/* Static text for a status code (never null). */
+const char* sparda_status_string(int status);
+
+/* Reason for the calling thread's last failed call ("" if none). */
+const char* sparda_last_error_detail(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARDA_H */

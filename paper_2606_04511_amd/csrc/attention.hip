@@ -1,0 +1,273 @@
+// attention.hip -- block-sparse attention over the attended block sets (paper Sec. 4.1, Eq. 5,
+// over the set of Eq. 1): o = softmax(sm_scale * q K_S^T) V_S for the tokens t <= p of the
+// attended blocks S, all G query heads of a GQA group sharing S.
+//
+// Work unit: one query row (batch b, group m, row r) and a split of its selected-block list.  A
+// workgroup has 4 wavefronts; each wavefront walks blocks split_begin + wave, +4, ... with its own
+// online-softmax state, then the 4 states are merged through LDS.  With several splits per row
+// the merged (max, sum, acc) partials go to the workspace and a combine kernel merges them by
+// log-sum-exp; with one split the workgroup writes the bf16 output directly.
+//
+// Per 64-token block a wavefront:
+//   * loads the 16 KiB K block as the MFMA A operand (token rows x head-dim columns, 16-byte
+//     loads, 64 contiguous bytes per row segment) and the 16 KiB V block as 16 fully
+//     contiguous 1 KiB wavefront loads, both issued before any math;
+//   * computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 tokens, N = the G <= 16 heads
+//     of the group, K = 32 head dims): 16 MFMAs per block;
+//   * masks tokens after p (the query's own block), exponentiates in the exp2 domain, and
+//     passes P through a 4 KiB per-wave LDS slice;
+//   * accumulates P V on the VALU (lane = 8 head dims x one token in four): decode has only G
+//     query rows per block, so the PV product is bandwidth-bound work, not an MFMA contraction.
+#include <math.h>
+
+#include "device_util.hpp"
+#include "launch.hpp"
+
+namespace sparda {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int G>
+__global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
+  __shared__ __align__(16) float p_lds[4][64][G];
+  __shared__ float st_m[4][G], st_l[4][G];
+  __shared__ __align__(16) float st_acc[4][G][kHeadDim];
+  const int64_t row = blockIdx.x;
+  const int split = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = (int)(row % a.n_q);
+  const int64_t bm = row / a.n_q;
+  const int m = (int)(bm % a.n_kv_heads);
+  const int b = (int)(bm / a.n_kv_heads);
+  const int64_t p = a.q_pos0 + r;
+  const int blk = (int)(p / kBlock);
+  int n = a.cnt[row];
+  n = n > a.k_total ? a.k_total : (n < 0 ? 0 : n);
+  const int s_begin = split * a.blocks_per_split;
+  const int s_end = min(n, s_begin + a.blocks_per_split);
+  const int64_t Hq = (int64_t)a.n_kv_heads * G;
+  const float zscale = a.sm_scale * kLog2e;
+
+  const int hh = lane & 15;   // S^T column (head) of this lane; also the PV dim chunk
+  const int grp = lane >> 4;  // k-chunk of the MFMA operands; also the PV token phase
+  bf16x8 qb[4];
+  {
+    const uint16_t* qrow = a.q + (((int64_t)b * Hq + (int64_t)m * G + hh) * a.n_q + r) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qb[ks] = as_bf16x8(hh < G ? ld16(qrow + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  float acc[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+
+  const int16_t* srow = a.sel + row * a.k_total;
+  for (int s = s_begin + wave; s < s_end; s += 4) {
+    const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
+    if (j < 0 || j > blk) continue;
+    int64_t base;
+    if (a.kv_mode == 0)
+      base = (bm * a.t_cap + (int64_t)j * kBlock) * kHeadDim;
+    else
+      base = ((bm * a.k_total + s) * kBlock) * kHeadDim;
+    const uint16_t* kb = a.k + base;
+    const uint16_t* vb = a.v + base;
+    uint4 kw[4][4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kw[tt][ks] = ld16(kb + (16 * tt + hh) * kHeadDim + 32 * ks + 8 * grp);
+    uint4 vw[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) vw[it] = ld16(vb + (4 * it + grp) * kHeadDim + 8 * hh);
+
+    f32x4 st[4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+      st[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) st[tt] = mfma16x16x32(as_bf16x8(kw[tt][ks]), qb[ks], st[tt]);
+    }
+    // lane holds S^T[token 16 tt + 4 grp + i][head hh]
+    const int last = (j == blk) ? (int)(p - (int64_t)j * kBlock) : kBlock - 1;
+    float z[4][4];
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 16 * tt + 4 * grp + i;
+        z[tt][i] = tok <= last ? st[tt][i] * zscale : -INFINITY;
+        bmax = fmaxf(bmax, z[tt][i]);
+      }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float m_new = fmaxf(m_run, bmax);  // token 0 of a block is always <= p: finite
+    const float alpha = exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float pz = exp2f(z[tt][i] - m_new);
+        psum += pz;
+        if (hh < G) p_lds[wave][16 * tt + 4 * grp + i][hh] = pz;
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    wave_lds_sync();
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float ah = readlane_f(alpha, h);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] *= ah;
+    }
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int tok = 4 * it + grp;
+      const bool ok = tok <= last;  // never multiply by unwritten values after p
+      const uint4 w = ok ? vw[it] : make_uint4(0u, 0u, 0u, 0u);
+      const float v8[8] = {bf16lo(w.x), bf16hi(w.x), bf16lo(w.y), bf16hi(w.y),
+                           bf16lo(w.z), bf16hi(w.z), bf16lo(w.w), bf16hi(w.w)};
+      float pr[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) pr[h] = p_lds[wave][tok][h];
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr[h], v8[e], acc[h][e]);
+    }
+    wave_lds_sync();
+  }
+  // Sum the four token phases of each head-dim chunk.
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x = acc[h][e];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+      acc[h][e] = x;
+    }
+  if (lane < G) {
+    st_m[wave][lane] = m_run;
+    st_l[wave][lane] = l_run;
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) st_acc[wave][h][8 * lane + e] = acc[h][e];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += 256) {
+    const int h = idx / kHeadDim, d = idx % kHeadDim;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, st_m[w][h]);
+    float L = 0.f, A = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float mw = st_m[w][h];
+        if (mw != -INFINITY) {
+          const float sc = exp2f(mw - M);
+          L = fmaf(st_l[w][h], sc, L);
+          A = fmaf(st_acc[w][h][d], sc, A);
+        }
+      }
+    }
+    if (a.n_splits == 1) {
+      a.o[(((int64_t)b * Hq + (int64_t)m * G + h) * a.n_q + r) * kHeadDim + d] = f32_to_bf16(L > 0.f ? A / L : 0.f);
+    } else {
+      float* pp = a.ws + ((row * a.n_splits + split) * G + h) * (kHeadDim + 2);
+      if (d == 0) {
+        pp[0] = M;
+        pp[1] = L;
+      }
+      pp[2 + d] = A;
+    }
+  }
+}
+
+// Merge the split partials of one row by log-sum-exp.
+template <int G>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
+  const int64_t row = blockIdx.x;
+  const int r = (int)(row % a.n_q);
+  const int64_t bm = row / a.n_q;
+  const int m = (int)(bm % a.n_kv_heads);
+  const int b = (int)(bm / a.n_kv_heads);
+  const int64_t Hq = (int64_t)a.n_kv_heads * G;
+  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += 256) {
+    const int h = idx / kHeadDim, d = idx % kHeadDim;
+    const float* base = a.ws + (row * a.n_splits * G + h) * (kHeadDim + 2);
+    const int64_t stride = (int64_t)G * (kHeadDim + 2);
+    float M = -INFINITY;
+    for (int s = 0; s < a.n_splits; ++s) M = fmaxf(M, base[s * stride]);
+    float L = 0.f, A = 0.f;
+    if (M != -INFINITY) {
+      for (int s = 0; s < a.n_splits; ++s) {
+        const float ms = base[s * stride];
+        if (ms != -INFINITY) {
+          const float sc = exp2f(ms - M);
+          L = fmaf(base[s * stride + 1], sc, L);
+          A = fmaf(base[s * stride + 2 + d], sc, A);
+        }
+      }
+    }
+    a.o[(((int64_t)b * Hq + (int64_t)m * G + h) * a.n_q + r) * kHeadDim + d] = f32_to_bf16(L > 0.f ? A / L : 0.f);
+  }
+}
+
+void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split) {
+  // Aim for ~4096 workgroups (16 per CU) so that enough K/V bytes are in flight; at least 4
+  // blocks (one per wavefront) per split.
+  const int max_splits = (k_total + 3) / 4;
+  int64_t want = rows >= 4096 ? 1 : (4096 + rows - 1) / rows;
+  int ns = (int)(want < max_splits ? want : max_splits);
+  if (ns < 1) ns = 1;
+  int bps = (k_total + ns - 1) / ns;
+  ns = (k_total + bps - 1) / bps;
+  *n_splits = ns;
+  *blocks_per_split = bps;
+}
+
+template <int G>
+static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
+  dim3 grid((unsigned)rows, (unsigned)a.n_splits);
+  hipLaunchKernelGGL(sparse_attn_kernel<G>, grid, dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_splits == 1) return e;
+  hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)rows), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream) {
+  switch (a.group_size) {
+    case 1: return launch_g<1>(a, stream);
+    case 2: return launch_g<2>(a, stream);
+    case 3: return launch_g<3>(a, stream);
+    case 4: return launch_g<4>(a, stream);
+    case 5: return launch_g<5>(a, stream);
+    case 6: return launch_g<6>(a, stream);
+    case 7: return launch_g<7>(a, stream);
+    case 8: return launch_g<8>(a, stream);
+    case 9: return launch_g<9>(a, stream);
+    case 10: return launch_g<10>(a, stream);
+    case 11: return launch_g<11>(a, stream);
+    case 12: return launch_g<12>(a, stream);
+    case 13: return launch_g<13>(a, stream);
+    case 14: return launch_g<14>(a, stream);
+    case 15: return launch_g<15>(a, stream);
+    case 16: return launch_g<16>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sparda

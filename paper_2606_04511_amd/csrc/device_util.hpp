@@ -1,0 +1,116 @@
+// device_util.hpp -- small gfx950 device helpers shared by the SparDA kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sparda {
+
+constexpr int kWave = 64;        // CDNA wavefront width
+constexpr int kHeadDim = 128;    // D
+constexpr int kBlock = 64;       // tokens per KV block
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---- bf16 <-> float -------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// float -> bf16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// float64 -> bf16 in one rounding (nearest, ties to even), by integer work on the float64 bits,
+// so that an exact float64 value is never rounded twice.
+__device__ __forceinline__ uint16_t f64_to_bf16(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint16_t sign = (uint16_t)((u >> 48) & 0x8000u);
+  const int e = (int)((u >> 52) & 0x7ff);
+  const uint64_t man = u & ((1ull << 52) - 1);
+  if (e == 0x7ff) return (uint16_t)(sign | (man ? 0x7fc0u : 0x7f80u));
+  if (e == 0) return sign;  // float64 subnormals are far below the bf16 range
+  int be = e - 1023 + 127;
+  if (be >= 1) {
+    uint64_t keep = man >> 45;
+    const uint64_t rest = man & ((1ull << 45) - 1), half = 1ull << 44;
+    if (rest > half || (rest == half && (keep & 1u))) ++keep;
+    if (keep == 128) { keep = 0; ++be; }
+    if (be >= 255) return (uint16_t)(sign | 0x7f80u);
+    return (uint16_t)(sign | (uint16_t)(be << 7) | (uint16_t)keep);
+  }
+  // bf16 subnormal: value = sig * 2^(e - 1075), grid 2^-133 => q = sig >> (942 - e), rounded.
+  const uint64_t sig = man | (1ull << 52);
+  const int sh = 942 - e;  // >= 46 here
+  if (sh >= 64) return sign;
+  uint64_t q = sig >> sh;
+  const uint64_t rest = sig & ((1ull << sh) - 1), half = 1ull << (sh - 1);
+  if (rest > half || (rest == half && (q & 1u))) ++q;
+  return (uint16_t)(sign | (uint16_t)q);
+}
+
+// Order-preserving map of a float score to uint32 (larger score -> larger key); -0 maps like +0.
+__device__ __forceinline__ uint32_t score_key(float s) {
+  uint32_t u = __float_as_uint(s == 0.0f ? 0.0f : s);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ---- cross-lane helpers ----------------------------------------------------------------
+
+// DPP move within 16-lane rows (row_ror:n has control 0x120 + n).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over each 16-lane row; every lane of the row receives the row total.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_f<0x128>(x);  // row_ror:8
+  x += dpp_f<0x124>(x);  // row_ror:4
+  x += dpp_f<0x122>(x);  // row_ror:2
+  x += dpp_f<0x121>(x);  // row_ror:1
+  return x;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+// Number of set bits of `mask` below this lane.
+__device__ __forceinline__ int mbcnt64(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ int readlane_i(int x, int lane) { return __builtin_amdgcn_readlane(x, lane); }
+__device__ __forceinline__ float readlane_f(float x, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+
+// Order this wave's LDS accesses: wait for outstanding LDS operations, then a wave barrier.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0), other counters untouched
+  __builtin_amdgcn_wave_barrier();
+  __asm__ __volatile__("" ::: "memory");
+}
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
+
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+}  // namespace sparda

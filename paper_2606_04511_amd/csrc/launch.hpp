@@ -1,0 +1,87 @@
+// launch.hpp -- host-side launchers of the SparDA kernels (private to the library).
+// Arguments have been validated by the C ABI layer before any launcher runs; each launcher only
+// computes a grid, enqueues kernels on `stream` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sparda {
+
+// Geometry of one query row at position p (Eq. 1 / Eq. 4): forced and candidate blocks.
+struct RowGeom {
+  int blk;       // p / 64
+  int init_hi;   // initial blocks [0, init_hi)
+  int local_lo;  // local blocks [local_lo, blk] (local_lo >= init_hi)
+  int n_forced;  // init_hi + blk - local_lo + 1
+  int cand_lo;   // candidates [cand_lo, cand_lo + n_cand)
+  int n_cand;
+  int n_take;    // candidates chosen: min(k_total - n_forced, n_cand)
+};
+
+__host__ __device__ inline RowGeom row_geom(int64_t p, int n_init, int n_local, int k_total) {
+  RowGeom g;
+  g.blk = (int)(p / 64);
+  g.init_hi = n_init < g.blk + 1 ? n_init : g.blk + 1;
+  int lo = g.blk - n_local + 1;
+  if (lo < 0) lo = 0;
+  if (lo < g.init_hi) lo = g.init_hi;
+  g.local_lo = lo;
+  g.n_forced = g.init_hi + (g.blk - lo + 1);
+  g.cand_lo = n_init;
+  const int hi = g.blk - n_local;
+  g.n_cand = hi >= n_init ? hi - n_init + 1 : 0;
+  const int budget = k_total - g.n_forced;
+  g.n_take = budget < g.n_cand ? budget : g.n_cand;
+  return g;
+}
+
+struct SelectArgs {
+  const uint16_t* f;
+  const uint16_t* kc;
+  int16_t* sel;
+  int16_t* cnt;
+  float* ws;           // score scratch for the row-wise path
+  int64_t ws_stride;   // floats per row in ws
+  int32_t batch, n_kv_heads, n_q;
+  int64_t q_pos0, nc_cap;
+  int32_t n_init, n_local, k_total;
+};
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int16_t* sel;
+  const int16_t* cnt;
+  uint16_t* o;
+  float* ws;           // split partials
+  int32_t batch, n_kv_heads, group_size, n_q;
+  int64_t q_pos0, t_cap;
+  int32_t kv_mode, k_total;
+  float sm_scale;
+  int32_t n_splits;        // splits of the selected-block list per row
+  int32_t blocks_per_split;
+};
+
+// Tiles of the fused multi-row selection kernel.
+constexpr int kSelTileRows = 64;
+constexpr int kSelTileMaxCand = 512;
+
+hipError_t launch_compress(const uint16_t* k, uint16_t* kc, int32_t rows, int64_t t_cap, int64_t nc_cap,
+                           int32_t blk_begin, int32_t blk_end, hipStream_t stream);
+
+// True when the multi-row fused kernel handles every tile (no score scratch needed).
+bool select_uses_fused(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local);
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+
+// Split count and blocks per split the attention launcher uses for `rows` query rows.
+void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
+hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
+
+hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const int16_t* sel, const int16_t* cnt,
+                         uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int64_t t_cap, int32_t k_total,
+                         int32_t n_workgroups, hipStream_t stream);
+
+}  // namespace sparda

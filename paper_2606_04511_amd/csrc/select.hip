@@ -1,0 +1,243 @@
+// select.hip -- Forecast scoring and top-k block selection (paper Sec. 4.1, Eq. 4, with the
+// attended-set union of Eq. 1).
+//
+// Per query row at position p: forced = initial blocks U local window, candidates = the complete
+// blocks in between, score s_j = F_row . K~_j (one Forecast head per GQA group, no softmax, no
+// scale, float32 accumulation); the k_total - |forced| best candidates by (score desc, index asc)
+// join the forced blocks; the row's set is written in ascending block order, -1 padded.
+//
+// Two paths:
+//  * row-wise (decode, n_q == 1, and long multi-row cases): a bandwidth-bound GEMV kernel writes
+//    the candidate scores of each row to a float32 scratch row; a second kernel runs one
+//    wavefront per row that finds the exact k-th key by an 8-bit-digit radix select over a
+//    wave-private LDS histogram and emits the chosen indices in ascending order with ballots.
+//  * fused tile (multi-row prefill with <= 512 candidates per 64-row tile): one workgroup scores
+//    a 64-row tile against all its candidates with bf16 MFMA (v_mfma_f32_16x16x32_bf16), keeps
+//    the float32 score tile in LDS, and runs the same wavefront radix select per row; scores
+//    never reach HBM.
+#include "device_util.hpp"
+#include "launch.hpp"
+
+namespace sparda {
+
+// Forced blocks of a row: initial blocks first, the chosen candidates after them (written by the
+// select routine), then the local window, then -1 padding up to k_total.
+__device__ __forceinline__ void emit_forced(int16_t* out, const RowGeom& g, int k_total, int lane) {
+  for (int i = lane; i < g.init_hi; i += kWave) out[i] = (int16_t)i;
+  const int n_loc = g.blk - g.local_lo + 1;
+  for (int i = lane; i < n_loc; i += kWave) out[g.init_hi + g.n_take + i] = (int16_t)(g.local_lo + i);
+  for (int i = g.n_forced + g.n_take + lane; i < k_total; i += kWave) out[i] = (int16_t)-1;
+}
+
+// One wavefront selects the n_take largest keys among n_cand candidates (ties: lower index) and
+// writes their indices cand_lo + i in ascending order to out[0 .. n_take).  key_of(i) returns
+// score_key of candidate i.  hist: 256 uint32 of wave-private, 16-byte aligned LDS.
+template <class KeyFn>
+__device__ void wave_topk_emit(KeyFn key_of, int n_cand, int n_take, int cand_lo, uint32_t* hist, int16_t* out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (n_take >= n_cand) {
+    for (int i = lane; i < n_cand; i += kWave) out[i] = (int16_t)(cand_lo + i);
+    return;
+  }
+  if (n_take <= 0) return;
+  uint32_t prefix = 0u, mask = 0u;
+  int remaining = n_take;  // still to take among keys that match `prefix` under `mask`
+  bool take_all = false;
+  for (int pass = 0; pass < 4 && !take_all; ++pass) {
+    const int shift = 24 - 8 * pass;
+    reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
+    wave_lds_sync();
+    for (int i = lane; i < n_cand; i += kWave) {
+      const uint32_t kk = key_of(i);
+      if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
+    }
+    wave_lds_sync();
+    // Lane l owns digits 255-4l (h.w) down to 252-4l (h.x): a descending scan over lanes.
+    const uint4 h = reinterpret_cast<const uint4*>(hist)[63 - lane];
+    const int lsum = (int)(h.x + h.y + h.z + h.w);
+    const int incl = wave_incl_scan(lsum);
+    const int excl = incl - lsum;
+    const uint64_t hit = __ballot(excl < remaining && remaining <= incl);
+    const int src = hit ? (int)__builtin_ctzll(hit) : 0;  // exactly one lane holds the k-th key
+    int above = excl, d = 255 - 4 * lane, eq = (int)h.w;
+    if (above + (int)h.w < remaining) {
+      above += (int)h.w; d -= 1; eq = (int)h.z;
+      if (above + (int)h.z < remaining) {
+        above += (int)h.z; d -= 1; eq = (int)h.y;
+        if (above + (int)h.y < remaining) { above += (int)h.y; d -= 1; eq = (int)h.x; }
+      }
+    }
+    above = readlane_i(above, src);
+    d = readlane_i(d, src);
+    eq = readlane_i(eq, src);
+    remaining -= above;
+    prefix |= (uint32_t)d << shift;
+    mask |= 0xffu << shift;
+    take_all = (eq == remaining);
+    wave_lds_sync();
+  }
+  int base = 0, tie_base = 0;
+  for (int i0 = 0; i0 < n_cand; i0 += kWave) {
+    const int i = i0 + lane;
+    const bool valid = i < n_cand;
+    const uint32_t kk = valid ? key_of(i) : 0u;
+    bool chosen;
+    if (take_all) {
+      chosen = valid && (kk & mask) >= prefix;
+    } else {  // prefix is the exact k-th key; equal keys go to the lowest indices
+      const bool tie = valid && kk == prefix;
+      const uint64_t tb = __ballot(tie);
+      const int trank = tie_base + mbcnt64(tb);
+      tie_base += __popcll(tb);
+      chosen = valid && (kk > prefix || (tie && trank < remaining));
+    }
+    const uint64_t cb = __ballot(chosen);
+    const int pos = base + mbcnt64(cb);
+    if (chosen && pos < n_take) out[pos] = (int16_t)(cand_lo + i);  // never past the row's slots
+    base += __popcll(cb);
+  }
+}
+
+// ---- row-wise path ----------------------------------------------------------------------
+
+// grid.x = row * n_chunks + chunk; a chunk is 256 candidates (64 per wavefront).  Lane l reads
+// dims 8*(l%16)..+7 of candidate 4 i + l/16: each wavefront load is 1 KiB contiguous of K~.
+__global__ __launch_bounds__(256) void rowwise_score_kernel(SelectArgs a, int n_chunks) {
+  const int64_t row = blockIdx.x / n_chunks;
+  const int chunk = (int)(blockIdx.x % n_chunks);
+  const int r = (int)(row % a.n_q);
+  const int64_t bm = row / a.n_q;
+  const RowGeom g = row_geom(a.q_pos0 + r, a.n_init, a.n_local, a.k_total);
+  if (g.n_take >= g.n_cand) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, rs = lane >> 4;
+  const int first = chunk * 256 + wave * 64;
+  if (first >= g.n_cand) return;
+  const uint4 fw = ld16(a.f + row * kHeadDim + c * 8);
+  const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
+  const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
+  const uint16_t* kbase = a.kc + (bm * a.nc_cap + g.cand_lo) * kHeadDim + c * 8;
+  uint4 kw[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int idx = first + 4 * i + rs;
+    kw[i] = idx < g.n_cand ? ld16(kbase + (int64_t)idx * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  float* out = a.ws + row * a.ws_stride;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float d = f0 * bf16lo(kw[i].x);
+    d = fmaf(f1, bf16hi(kw[i].x), d);
+    d = fmaf(f2, bf16lo(kw[i].y), d);
+    d = fmaf(f3, bf16hi(kw[i].y), d);
+    d = fmaf(f4, bf16lo(kw[i].z), d);
+    d = fmaf(f5, bf16hi(kw[i].z), d);
+    d = fmaf(f6, bf16lo(kw[i].w), d);
+    d = fmaf(f7, bf16hi(kw[i].w), d);
+    d = row16_sum(d);
+    const int idx = first + 4 * i + rs;
+    if (c == 0 && idx < g.n_cand) out[idx] = d;
+  }
+}
+
+// One wavefront per row: forced blocks, padding, count, and the radix top-k over the scratch row.
+__global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t n_rows) {
+  __shared__ __align__(16) uint32_t hist[4][256];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= n_rows) return;
+  const int r = (int)(row % a.n_q);
+  const RowGeom g = row_geom(a.q_pos0 + r, a.n_init, a.n_local, a.k_total);
+  int16_t* out = a.sel + row * a.k_total;
+  emit_forced(out, g, a.k_total, lane);
+  if (lane == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  const float* sc = a.ws + row * a.ws_stride;
+  wave_topk_emit([&](int i) { return score_key(sc[i]); }, g.n_cand, g.n_take, g.cand_lo, hist[wave],
+                 out + g.init_hi);
+}
+
+// ---- fused multi-row tile path -------------------------------------------------------------
+
+constexpr int kTileLd = kSelTileMaxCand + 4;  // LDS row pitch (floats): conflict-free MFMA stores
+
+// grid.x = (batch*group) * n_tiles + tile; 256 threads.  Rows r0 .. r0+63 of one (b, group).
+__global__ __launch_bounds__(256) void tile_select_kernel(SelectArgs a, int n_tiles) {
+  __shared__ __align__(16) float sc[kSelTileRows * kTileLd];
+  __shared__ __align__(16) uint32_t hist[4][256];
+  const int tile = (int)(blockIdx.x % n_tiles);
+  const int64_t bm = blockIdx.x / n_tiles;
+  const int r0 = tile * kSelTileRows;
+  const int nrows = min(kSelTileRows, a.n_q - r0);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const RowGeom gl = row_geom(a.q_pos0 + r0 + nrows - 1, a.n_init, a.n_local, a.k_total);
+  const int C = gl.n_cand;  // the tile's candidates [n_init, n_init + C); every row uses a prefix
+  if (gl.n_take < gl.n_cand) {
+    // S[row][cand] = F[row] . K~[cand]: A = F rows (M), B = K~ rows (N), K = head dim.
+    bf16x8 fa[4][4];
+    const int lr = lane & 15, kq = 8 * (lane >> 4);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int rr = mt * 16 + lr;
+      const uint16_t* fp = a.f + ((bm * a.n_q + r0 + rr) * kHeadDim + kq);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        fa[mt][ks] = as_bf16x8(rr < nrows ? ld16(fp + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
+    }
+    const int n_nt = (C + 15) >> 4;
+    const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim + kq;
+    for (int nt = wave; nt < n_nt; nt += 4) {
+      const int cand = nt * 16 + lr;
+      bf16x8 kb[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        kb[ks] = as_bf16x8(cand < C ? ld16(kcb + (int64_t)cand * kHeadDim + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) acc = mfma16x16x32(fa[mt][ks], kb[ks], acc);
+        float* dst = sc + (mt * 16 + 4 * (lane >> 4)) * kTileLd + nt * 16 + lr;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[i * kTileLd] = acc[i];
+      }
+    }
+  }
+  __syncthreads();
+  for (int rr = wave; rr < nrows; rr += 4) {
+    const int64_t row = bm * a.n_q + r0 + rr;
+    const RowGeom g = row_geom(a.q_pos0 + r0 + rr, a.n_init, a.n_local, a.k_total);
+    int16_t* out = a.sel + row * a.k_total;
+    emit_forced(out, g, a.k_total, lane);
+    if (lane == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+    const float* srow = sc + rr * kTileLd;
+    wave_topk_emit([&](int i) { return score_key(srow[i]); }, g.n_cand, g.n_take, g.cand_lo, hist[wave],
+                   out + g.init_hi);
+  }
+}
+
+bool select_uses_fused(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
+  if (n_q <= 1) return false;
+  const RowGeom g = row_geom(q_pos0 + n_q - 1, n_init, n_local, 1 << 30);
+  return g.n_cand <= kSelTileMaxCand;
+}
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
+  if (select_uses_fused(a.n_q, a.q_pos0, a.n_init, a.n_local)) {
+    const int n_tiles = (a.n_q + kSelTileRows - 1) / kSelTileRows;
+    const int64_t grid = (int64_t)a.batch * a.n_kv_heads * n_tiles;
+    hipLaunchKernelGGL(tile_select_kernel, dim3((unsigned)grid), dim3(256), 0, stream, a, n_tiles);
+    return hipGetLastError();
+  }
+  const RowGeom gl = row_geom(a.q_pos0 + a.n_q - 1, a.n_init, a.n_local, a.k_total);
+  if (gl.n_cand > 0) {
+    const int n_chunks = (gl.n_cand + 255) / 256;
+    hipLaunchKernelGGL(rowwise_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(rowwise_topk_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, a, rows);
+  return hipGetLastError();
+}
+
+}  // namespace sparda

@@ -1,0 +1,262 @@
+// sparda_abi.cpp -- the extern "C" entry points declared in include/sparda.h.
+//
+// Every entry point validates its arguments on the host (no HIP call happens before validation
+// has passed, so argument errors are reported without a GPU), sizes its workspace, and hands
+// the launch to the kernel files.  The library keeps no state except a thread-local error text.
+#include "sparda.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "launch.hpp"
+
+namespace {
+
+thread_local std::string g_detail;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return status;
+}
+
+int ok() {
+  g_detail.clear();
+  return SPARDA_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+constexpr int64_t kMaxBlocks = 32768;  // block indices are int16
+
+int check_shape(const sparda_shape* s) {
+  if (!s) return fail(SPARDA_ERR_INVALID_ARG, "shape is null");
+  if (s->struct_size != sizeof(sparda_shape))
+    return fail(SPARDA_ERR_INVALID_ARG, "shape.struct_size is %u, expected %zu", s->struct_size, sizeof(sparda_shape));
+  if (s->batch < 1 || s->n_kv_heads < 1 || s->group_size < 1)
+    return fail(SPARDA_ERR_INVALID_ARG, "batch, n_kv_heads and group_size must be >= 1");
+  if (s->group_size > 16) return fail(SPARDA_ERR_UNSUPPORTED, "group_size %d > 16", s->group_size);
+  if (s->head_dim != 128) return fail(SPARDA_ERR_UNSUPPORTED, "head_dim %d (only 128)", s->head_dim);
+  if (s->block_size != 64) return fail(SPARDA_ERR_UNSUPPORTED, "block_size %d (only 64)", s->block_size);
+  if (s->cmp_kernel != 64 || s->cmp_stride != 64)
+    return fail(SPARDA_ERR_UNSUPPORTED, "compression window (%d, %d) (only (64, 64))", s->cmp_kernel, s->cmp_stride);
+  if (s->n_init < 0 || s->n_local < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_init >= 0 and n_local >= 1 required");
+  if ((int64_t)s->k_total < (int64_t)s->n_init + s->n_local)
+    return fail(SPARDA_ERR_INVALID_ARG, "k_total %d < n_init + n_local", s->k_total);
+  if (s->k_total >= kMaxBlocks) return fail(SPARDA_ERR_UNSUPPORTED, "k_total %d too large", s->k_total);
+  if (s->t_cap < 64 || s->t_cap % 64 != 0)
+    return fail(SPARDA_ERR_INVALID_ARG, "t_cap %lld must be a positive multiple of 64", (long long)s->t_cap);
+  if (s->t_cap / 64 > kMaxBlocks)
+    return fail(SPARDA_ERR_UNSUPPORTED, "t_cap %lld exceeds 32768 blocks", (long long)s->t_cap);
+  if (s->nc_cap < 0 || s->nc_cap > kMaxBlocks) return fail(SPARDA_ERR_INVALID_ARG, "nc_cap out of range");
+  if ((int64_t)s->batch * s->n_kv_heads > 65535)
+    return fail(SPARDA_ERR_UNSUPPORTED, "batch * n_kv_heads > 65535");
+  return SPARDA_OK;
+}
+
+int check_dev(const void* p, const char* name, uintptr_t align) {
+  if (!p) return fail(SPARDA_ERR_INVALID_ARG, "%s is null", name);
+  if (!aligned(p, align)) return fail(SPARDA_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, (size_t)align);
+  return SPARDA_OK;
+}
+
+int check_rows(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
+  if (n_q < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_q %d < 1", n_q);
+  if (q_pos0 < 0 || q_pos0 + n_q > s->t_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "positions [%lld, %lld) outside t_cap %lld", (long long)q_pos0,
+                (long long)(q_pos0 + n_q), (long long)s->t_cap);
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  if (rows > (int64_t)1 << 30) return fail(SPARDA_ERR_UNSUPPORTED, "too many query rows");
+  return SPARDA_OK;
+}
+
+// Workspace of sparda_forecast_select: scores of the row-wise path (none for the fused tiles).
+size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* stride) {
+  const sparda::RowGeom g = sparda::row_geom(q_pos0 + n_q - 1, s->n_init, s->n_local, s->k_total);
+  *stride = ((int64_t)g.n_cand + 3) & ~(int64_t)3;
+  if (sparda::select_uses_fused(n_q, q_pos0, s->n_init, s->n_local)) return 0;
+  if (g.n_cand == 0) return 0;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  return (size_t)rows * (size_t)*stride * sizeof(float);
+}
+
+size_t attn_ws(const sparda_shape* s, int32_t n_q, int32_t* n_splits, int32_t* bps) {
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  sparda::attn_plan(rows, s->k_total, n_splits, bps);
+  if (*n_splits <= 1) return 0;
+  return (size_t)rows * (size_t)*n_splits * (size_t)s->group_size * (size_t)(s->head_dim + 2) * sizeof(float);
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SPARDA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sparda_status_string(int status) {
+  switch (status) {
+    case SPARDA_OK: return "SPARDA_OK";
+    case SPARDA_ERR_INVALID_ARG: return "SPARDA_ERR_INVALID_ARG";
+    case SPARDA_ERR_UNSUPPORTED: return "SPARDA_ERR_UNSUPPORTED";
+    case SPARDA_ERR_WORKSPACE: return "SPARDA_ERR_WORKSPACE";
+    case SPARDA_ERR_HOST_NOT_MAPPED: return "SPARDA_ERR_HOST_NOT_MAPPED";
+    case SPARDA_ERR_HIP: return "SPARDA_ERR_HIP";
+    default: return "SPARDA_ERR_UNKNOWN";
+  }
+}
+
+const char* sparda_last_error_detail(void) { return g_detail.c_str(); }
+
+int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, int64_t q_pos0, size_t* bytes) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!bytes) return fail(SPARDA_ERR_INVALID_ARG, "bytes is null");
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (op == SPARDA_OP_FORECAST_SELECT) {
+    int64_t stride;
+    *bytes = select_ws(shape, n_q, q_pos0, &stride);
+  } else if (op == SPARDA_OP_SPARSE_ATTN) {
+    int32_t ns, bps;
+    *bytes = attn_ws(shape, n_q, &ns, &bps);
+  } else {
+    return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
+  }
+  return ok();
+}
+
+int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t blk_begin,
+                         int32_t blk_end, void* k_cmp, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(k_cache, "k_cache", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16))) return rc;
+  if (t_ctx < 0 || t_ctx > shape->t_cap) return fail(SPARDA_ERR_INVALID_ARG, "t_ctx outside [0, t_cap]");
+  if (blk_begin < 0 || blk_end < blk_begin) return fail(SPARDA_ERR_INVALID_ARG, "bad block range");
+  if ((int64_t)blk_end * 64 > t_ctx) return fail(SPARDA_ERR_INVALID_ARG, "block %d is not complete", blk_end - 1);
+  if (blk_end > shape->nc_cap) return fail(SPARDA_ERR_INVALID_ARG, "blk_end %d > nc_cap", blk_end);
+  if (blk_end == blk_begin) return ok();
+  return hip_status(sparda::launch_compress(static_cast<const uint16_t*>(k_cache), static_cast<uint16_t*>(k_cmp),
+                                            shape->batch * shape->n_kv_heads, shape->t_cap, shape->nc_cap,
+                                            blk_begin, blk_end, stream),
+                    "compress launch");
+}
+
+int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
+                           const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(f, "f", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(sel, "sel", 2)) ||
+      (rc = check_dev(cnt, "cnt", 2)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  const sparda::RowGeom gl = sparda::row_geom(q_pos0 + n_q - 1, shape->n_init, shape->n_local, shape->k_total);
+  if (gl.n_cand > 0 && (int64_t)gl.cand_lo + gl.n_cand > shape->nc_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "candidate block %d beyond nc_cap %lld", gl.cand_lo + gl.n_cand - 1,
+                (long long)shape->nc_cap);
+  int64_t stride = 0;
+  const size_t need = select_ws(shape, n_q, q_pos0, &stride);
+  if (need > 0) {
+    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  sparda::SelectArgs a;
+  a.f = static_cast<const uint16_t*>(f);
+  a.kc = static_cast<const uint16_t*>(k_cmp);
+  a.sel = sel;
+  a.cnt = cnt;
+  a.ws = static_cast<float*>(ws);
+  a.ws_stride = stride;
+  a.batch = shape->batch;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.n_q = n_q;
+  a.q_pos0 = q_pos0;
+  a.nc_cap = shape->nc_cap;
+  a.n_init = shape->n_init;
+  a.n_local = shape->n_local;
+  a.k_total = shape->k_total;
+  return hip_status(sparda::launch_select(a, stream), "select launch");
+}
+
+int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
+                       const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
+                       void* o, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k, "k", 16)) || (rc = check_dev(v, "v", 16)) ||
+      (rc = check_dev(sel, "sel", 2)) || (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(o, "o", 16)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (kv_mode != 0 && kv_mode != 1) return fail(SPARDA_ERR_INVALID_ARG, "kv_mode %d", kv_mode);
+  if (kv_mode == 1 && n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "staging mode needs n_q == 1");
+  if (!std::isfinite(sm_scale)) return fail(SPARDA_ERR_INVALID_ARG, "sm_scale is not finite");
+  int32_t ns = 1, bps = shape->k_total;
+  const size_t need = attn_ws(shape, n_q, &ns, &bps);
+  if (need > 0) {
+    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  sparda::AttnArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.sel = sel;
+  a.cnt = cnt;
+  a.o = static_cast<uint16_t*>(o);
+  a.ws = static_cast<float*>(ws);
+  a.batch = shape->batch;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.group_size = shape->group_size;
+  a.n_q = n_q;
+  a.q_pos0 = q_pos0;
+  a.t_cap = shape->t_cap;
+  a.kv_mode = kv_mode;
+  a.k_total = shape->k_total;
+  a.sm_scale = sm_scale;
+  a.n_splits = ns;
+  a.blocks_per_split = bps;
+  return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
+}
+
+int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
+                         const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
+                         hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(host_k, "host_k", 16)) || (rc = check_dev(host_v, "host_v", 16)) ||
+      (rc = check_dev(sel, "sel", 2)) || (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(stage_k, "stage_k", 16)) ||
+      (rc = check_dev(stage_v, "stage_v", 16)))
+    return rc;
+  if (n_workgroups < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_workgroups %d < 1", n_workgroups);
+  const void* dev_ptr[2] = {nullptr, nullptr};
+  const void* host_ptr[2] = {host_k, host_v};
+  for (int i = 0; i < 2; ++i) {
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, host_ptr[i]);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();  // clear the sticky-free error state of this query
+      return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not a registered HIP allocation (%s)", i ? "host_v" : "host_k",
+                  hipGetErrorString(e));
+    }
+    if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr)
+      return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not device-mapped pinned host memory", i ? "host_v" : "host_k");
+    dev_ptr[i] = attr.devicePointer;
+  }
+  return hip_status(sparda::launch_gather(static_cast<const uint16_t*>(dev_ptr[0]), static_cast<const uint16_t*>(dev_ptr[1]),
+                                          sel, cnt, static_cast<uint16_t*>(stage_k), static_cast<uint16_t*>(stage_v),
+                                          (int64_t)shape->batch * shape->n_kv_heads, shape->t_cap, shape->k_total,
+                                          n_workgroups, stream),
+                    "gather launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,67 @@
+"""Comparison helpers for the GPU parity tests.
+
+Selection: cnt must match exactly; the block sets must match, except that a block chosen by only
+one side is accepted when the oracle's score of every such block lies within the tie window of
+the oracle's k-th chosen score s_k.  The window is max(1e-3 |s_k|, gamma_128 * sum_d |F_d K~_jd|):
+the relative window the acceptance bar states, floored by the a-priori float32 error bound of a
+128-term dot product (gamma_n = n u / (1 - n u), u = 2^-24), which only matters when s_k ~ 0.
+All scores and bounds here come from the oracle's inputs and the oracle's scores.
+
+Attention: |o_gpu - o_oracle| <= 2e-2 absolute (bf16 inputs, float32 accumulation), with the
+attended set taken from the oracle.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import brute
+import oracle
+
+ATTN_ATOL = 2e-2
+REL_TIE = 1e-3
+_U = 2.0 ** -24
+GAMMA_128 = 128 * _U / (1 - 128 * _U)
+
+
+def compare_selection(oshape, f_u16, kc_u16, n_q, q_pos0, gpu_sel, gpu_cnt, rows):
+    """rows: iterable of (b, m, r).  Returns (n_rows, n_tie_swaps).  Raises AssertionError."""
+    f64 = None
+    n_rows = n_swaps = 0
+    for (b, m, r) in rows:
+        ref, cnt, scores = oracle.select_row(oshape, f_u16, n_q, q_pos0, kc_u16, b, m, r)
+        g = gpu_sel[b, m, r]
+        gc = int(gpu_cnt[b, m, r])
+        assert gc == cnt, f"row {(b, m, r)}: cnt {gc} != oracle {cnt}"
+        assert np.all(g[cnt:] == -1), f"row {(b, m, r)}: padding"
+        gs = g[:cnt]
+        assert np.all(np.diff(gs.astype(np.int64)) > 0), f"row {(b, m, r)}: not strictly ascending: {gs}"
+        n_rows += 1
+        if np.array_equal(gs, ref[:cnt]):
+            continue
+        A, R = set(gs.tolist()), set(ref[:cnt].tolist())
+        only = (A - R) | (R - A)
+        cand = ~np.isnan(scores)
+        for j in only:
+            assert 0 <= j < len(scores) and cand[j], f"row {(b, m, r)}: non-candidate block {j} differs"
+        chosen_ref = [j for j in R if cand[j]]
+        s_k = min(scores[j] for j in chosen_ref)
+        if f64 is None:
+            f64 = brute.bf16_bits_to_f64(f_u16)
+            kc64 = brute.bf16_bits_to_f64(kc_u16)
+        absdot = lambda j: float(np.abs(f64[b, m, r] * kc64[b, m, j]).sum())
+        for j in only:
+            win = max(REL_TIE * abs(s_k), GAMMA_128 * absdot(j))
+            assert abs(scores[j] - s_k) <= win, (
+                f"row {(b, m, r)}: block {j} (score {scores[j]:.6g}) differs beyond the tie window "
+                f"{win:.3g} of s_k = {s_k:.6g}")
+        n_swaps += 1
+    return n_rows, n_swaps
+
+
+def compare_attention(o_gpu, o_ref, what=""):
+    o_gpu = np.asarray(o_gpu, np.float64)
+    err = np.abs(o_gpu - o_ref)
+    worst = float(err.max()) if err.size else 0.0
+    assert np.all(np.isfinite(o_gpu)), f"{what}: non-finite output"
+    assert worst <= ATTN_ATOL, f"{what}: max |o - oracle| = {worst:.3g} > {ATTN_ATOL}"
+    return worst

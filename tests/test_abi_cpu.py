@@ -1,0 +1,150 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+The library must load, export every function declared in include/*.h, and reject bad arguments
+before it makes any HIP call.  Every call below fails validation, so nothing is launched.
+"""
+import ctypes
+import glob
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2606_04511_amd.sparda as sp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced: validation fails before any launch
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(sp.library_path()):
+        from paper_2606_04511_amd import build
+        build.build()
+    return sp.load()
+
+
+def declared_functions():
+    names = []
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        names += re.findall(r"^(?:int|const char\*)\s+(sparda_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_every_declared_function_is_exported(lib):
+    names = declared_functions()
+    assert {"sparda_compress_keys", "sparda_forecast_select", "sparda_sparse_attn",
+            "sparda_gather_blocks"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", sp.library_path()], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (sparda_\w+)", out))
+    for n in names:
+        assert n in exported, f"{n} declared in include/ but not exported"
+        assert getattr(lib, n) is not None
+
+
+def test_no_torch_symbols_in_the_library(lib):
+    out = subprocess.run(["nm", "-D", sp.library_path()], capture_output=True, text=True, check=True).stdout
+    assert "torch" not in out and "c10" not in out
+
+
+def shape(**kw):
+    base = dict(batch=2, n_kv_heads=8, group_size=4, k_total=16, t_cap=4096, nc_cap=64)
+    base.update(kw)
+    return sp.SpardaShape(**base)
+
+
+def rc_of(fn, *args):
+    with pytest.raises(sp.SpardaError) as ei:
+        fn(*args)
+    return ei.value.status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=64), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(block_size=32), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(cmp_kernel=32, cmp_stride=16), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(group_size=17), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(group_size=0), sp.SPARDA_ERR_INVALID_ARG),
+    (dict(k_total=2), sp.SPARDA_ERR_INVALID_ARG),
+    (dict(n_local=0), sp.SPARDA_ERR_INVALID_ARG),
+    (dict(t_cap=100), sp.SPARDA_ERR_INVALID_ARG),
+    (dict(t_cap=64 * 40000), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(k_total=40000), sp.SPARDA_ERR_UNSUPPORTED),
+])
+def test_shape_validation(lib, kw, status):
+    assert rc_of(sp.sparda_compress_keys, shape(**kw), FAKE, 4096, 0, 1, FAKE, 0) == status
+    assert sp.last_error_detail() != ""
+
+
+def test_struct_size_and_null_shape(lib):
+    cs = shape().c()
+    cs.struct_size = 12
+    assert lib.sparda_compress_keys(ctypes.byref(cs), FAKE, 4096, 0, 1, FAKE, None) == sp.SPARDA_ERR_INVALID_ARG
+    assert lib.sparda_compress_keys(None, FAKE, 4096, 0, 1, FAKE, None) == sp.SPARDA_ERR_INVALID_ARG
+
+
+def test_compress_argument_errors(lib):
+    s = shape()
+    assert rc_of(sp.sparda_compress_keys, s, None, 4096, 0, 1, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(sp.sparda_compress_keys, s, FAKE + 2, 4096, 0, 1, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(sp.sparda_compress_keys, s, FAKE, 100, 0, 2, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # incomplete
+    assert rc_of(sp.sparda_compress_keys, s, FAKE, 4096, 0, 65, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # > t_ctx
+    assert rc_of(sp.sparda_compress_keys, shape(nc_cap=10), FAKE, 4096, 0, 11, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(sp.sparda_compress_keys, s, FAKE, 5000, 0, 1, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # t_ctx > t_cap
+    sp.sparda_compress_keys(s, FAKE, 4096, 3, 3, FAKE, 0)  # empty range: a no-op, nothing launched
+
+
+def test_select_argument_errors(lib):
+    s = shape()
+    f = sp.sparda_forecast_select
+    assert rc_of(f, s, FAKE, 0, 4095, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG  # n_q
+    assert rc_of(f, s, FAKE, 1, 4096, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG  # p >= t_cap
+    assert rc_of(f, s, FAKE, 1, -1, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(f, shape(nc_cap=30), FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE + 1, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG  # sel align
+    # decode needs a score workspace
+    assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
+    need = sp.sparda_workspace_size(s, sp.SPARDA_OP_FORECAST_SELECT, 1, 4095)
+    assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
+
+
+def test_attention_argument_errors(lib):
+    s = shape()
+    a = sp.sparda_sparse_attn
+    sc = 1 / math.sqrt(128)
+    assert rc_of(a, s, FAKE, 1, 4095, FAKE, FAKE, 2, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, FAKE, 2, 4094, FAKE, FAKE, 1, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, FAKE, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, float("nan"), FAKE, None, 0, 0) == \
+        sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, None, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, FAKE, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
+
+
+def test_gather_argument_errors(lib):
+    s = shape()
+    g = sp.sparda_gather_blocks
+    assert rc_of(g, s, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(g, s, None, FAKE, FAKE, FAKE, FAKE, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG
+
+
+def test_workspace_sizes(lib):
+    # decode at 128K, B32: one float score per candidate row (2045 candidates, stride 2048)
+    s2 = shape(batch=32, k_total=64, t_cap=131072, nc_cap=2048)
+    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_FORECAST_SELECT, 1, 131071) == 256 * 2048 * 4
+    # 16 splits x 4 heads x (128 + 2) floats per row
+    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_SPARSE_ATTN, 1, 131071) == 256 * 16 * 4 * 130 * 4
+    # full 32K prefill: fused tiles, no score scratch; one split per row
+    s3 = shape(batch=1, k_total=64, t_cap=32768, nc_cap=512)
+    assert sp.sparda_workspace_size(s3, sp.SPARDA_OP_FORECAST_SELECT, 32768, 0) == 0
+    assert sp.sparda_workspace_size(s3, sp.SPARDA_OP_SPARSE_ATTN, 32768, 0) == 0
+    assert rc_of(sp.sparda_workspace_size, s3, 9, 1, 0) == sp.SPARDA_ERR_INVALID_ARG
+
+
+def test_status_strings(lib):
+    assert sp.status_string(0) == "SPARDA_OK"
+    assert sp.status_string(-4) == "SPARDA_ERR_HOST_NOT_MAPPED"
+    assert sp.status_string(-99) == "SPARDA_ERR_UNKNOWN"

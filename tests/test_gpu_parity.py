@@ -1,0 +1,374 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle on the same seeded inputs.
+
+Every test is marked `gpu`.  Inputs come from paper_2606_04511_amd.inputs; expected values come
+only from the oracle.  Attention is always checked on the oracle's attended sets, uploaded to the
+GPU.  Small cases compare every output; the full-size workloads compare sampled rows.
+"""
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_04511_amd.sparda as sp
+from paper_2606_04511_amd import inputs
+from parity import compare_attention, compare_selection
+
+pytestmark = pytest.mark.gpu
+SCALE = 1.0 / math.sqrt(128)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    sp.load()  # the in-tree libsparda.so; there is no fallback
+    return torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def shapes(B, H, G, k_total, t_cap, nc_cap, n_init=1, n_local=2):
+    s = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=G, k_total=k_total, t_cap=t_cap, nc_cap=nc_cap,
+                       n_init=n_init, n_local=n_local)
+    o = oracle.Shape(batch=B, n_kv_heads=H, group_size=G, k_total=k_total, t_cap=t_cap, nc_cap=nc_cap,
+                     n_init=n_init, n_local=n_local)
+    return s, o
+
+
+def ws(shape, op, n_q, q_pos0, dev):
+    n = sp.sparda_workspace_size(shape, op, n_q, q_pos0)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
+
+
+def gpu_compress(s, k_dev, t_ctx, nb, nc_cap, dev):
+    kc = torch.zeros(s.batch, s.n_kv_heads, nc_cap, 128, dtype=torch.bfloat16, device=dev)
+    sp.sparda_compress_keys(s, k_dev, t_ctx, 0, nb, kc)
+    return kc
+
+
+def gpu_select(s, f_dev, n_q, q_pos0, kc_dev, dev):
+    sel = torch.full((s.batch, s.n_kv_heads, n_q, s.k_total), 777, dtype=torch.int16, device=dev)
+    cnt = torch.full((s.batch, s.n_kv_heads, n_q), 777, dtype=torch.int16, device=dev)
+    sp.sparda_forecast_select(s, f_dev, n_q, q_pos0, kc_dev, sel, cnt, ws(s, sp.SPARDA_OP_FORECAST_SELECT, n_q,
+                                                                          q_pos0, dev))
+    torch.cuda.synchronize()
+    return sel, cnt
+
+
+def gpu_attend(s, q_dev, n_q, q_pos0, k_dev, v_dev, kv_mode, sel_dev, cnt_dev, dev):
+    o = torch.full((s.batch, s.n_q_heads, n_q, 128), float("nan"), dtype=torch.bfloat16, device=dev)
+    sp.sparda_sparse_attn(s, q_dev, n_q, q_pos0, k_dev, v_dev, kv_mode, sel_dev, cnt_dev, SCALE, o,
+                          ws(s, sp.SPARDA_OP_SPARSE_ATTN, n_q, q_pos0, dev))
+    torch.cuda.synchronize()
+    return o
+
+
+def make(B, H, G, T, n_q, k_total, seed, t_cap=None, n_init=1, n_local=2):
+    w = inputs.Workload("t", batch=B, seq_len=T, n_q=n_q, n_kv_heads=H, group_size=G, k_total=k_total,
+                        n_init=n_init, n_local=n_local, seed=seed)
+    t_cap = -(-T // 64) * 64 if t_cap is None else t_cap
+    return w, inputs.make_case(w, t_cap=t_cap)
+
+
+# ----------------------------------------------------------------------------- compress
+
+@pytest.mark.parametrize("B,H,T,t_cap", [(1, 8, 4096, 4096), (2, 2, 1000, 1024), (3, 1, 64, 128), (2, 3, 8192, 8192)])
+def test_compress_bitwise(dev, B, H, T, t_cap):
+    say(f"compress B{B} H{H} T{T}")
+    w, case = make(B, H, 4, T, 1, 8, 2000 + T, t_cap=t_cap)
+    nb = T // 64
+    s, o = shapes(B, H, 4, 8, t_cap, max(nb, 1))
+    kc = gpu_compress(s, case["k"].to(dev), T, nb, max(nb, 1), dev)
+    torch.cuda.synchronize()
+    ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nb)
+    assert np.array_equal(inputs.to_u16(kc), ref)
+
+
+def test_compress_incremental_equals_full(dev):
+    say("compress incremental")
+    w, case = make(2, 2, 4, 2048, 1, 8, 2100)
+    s, _ = shapes(2, 2, 4, 8, 2048, 32)
+    k = case["k"].to(dev)
+    full = gpu_compress(s, k, 2048, 32, 32, dev)
+    inc = torch.zeros_like(full)
+    for t in range(64, 2049, 64):
+        sp.sparda_compress_keys(s, k, t, t // 64 - 1, t // 64, inc)
+    torch.cuda.synchronize()
+    assert torch.equal(full.view(torch.int16), inc.view(torch.int16))
+
+
+# ----------------------------------------------------------------------------- selection
+
+DECODE_SELECT = [
+    # B, H, G, T, k_total, n_init, n_local
+    (1, 8, 4, 4096, 16, 1, 2),
+    (2, 2, 4, 65, 3, 1, 2),
+    (2, 8, 4, 1000, 5, 1, 2),
+    (3, 2, 4, 8192, 64, 1, 2),
+    (1, 4, 1, 32768, 64, 1, 2),
+    (1, 2, 4, 131072, 64, 1, 2),
+    (2, 2, 4, 20000, 40, 0, 3),
+    (1, 2, 16, 50000, 96, 1, 32),
+]
+
+
+@pytest.mark.parametrize("B,H,G,T,k_total,n_init,n_local", DECODE_SELECT)
+def test_decode_select(dev, B, H, G, T, k_total, n_init, n_local):
+    say(f"decode select B{B} H{H} T{T} k{k_total} init{n_init} local{n_local}")
+    w, case = make(B, H, G, T, 1, k_total, 3000 + T, n_init=n_init, n_local=n_local)
+    nb = T // 64
+    s, o = shapes(B, H, G, k_total, case["t_cap"], max(nb, 1), n_init, n_local)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nb)
+    kc_dev = inputs.from_u16(kc_ref, dev)  # the oracle's K~ as input: this test isolates selection
+    sel, cnt = gpu_select(s, case["f"].to(dev), 1, T - 1, kc_dev, dev)
+    rows = [(b, m, 0) for b in range(B) for m in range(H)]
+    n, swaps = compare_selection(o, inputs.to_u16(case["f"]), kc_ref, 1, T - 1, sel.cpu().numpy(), cnt.cpu().numpy(),
+                                 rows)
+    say(f"  rows {n}, tie swaps {swaps}")
+
+
+PREFILL_SELECT = [
+    # B, H, T, n_q, q_pos0, k_total   (rows at positions q_pos0 .. q_pos0 + n_q - 1)
+    (1, 2, 4096, 4096, 0, 16),
+    (2, 1, 5000, 5000, 0, 8),
+    (1, 2, 8192, 700, 3000, 64),
+    (1, 1, 32768, 2048, 30720, 64),
+    (1, 1, 40000, 37, 39963, 64),  # > 512 candidates per row: row-wise path
+]
+
+
+@pytest.mark.parametrize("B,H,T,n_q,q_pos0,k_total", PREFILL_SELECT)
+def test_prefill_select(dev, B, H, T, n_q, q_pos0, k_total):
+    say(f"prefill select B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} k{k_total}")
+    w, case = make(B, H, 4, T, n_q, k_total, 4000 + T)
+    t_cap = -(-T // 64) * 64
+    nb = T // 64
+    s, o = shapes(B, H, 4, k_total, t_cap, max(nb, 1))
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nb)
+    f_u16 = inputs.to_u16(case["f"])
+    sel, cnt = gpu_select(s, case["f"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
+    rng = np.random.default_rng(0)
+    rr = sorted(set(rng.integers(0, n_q, size=min(n_q, 600)).tolist()) | {0, n_q - 1})
+    rows = [(b, m, r) for b in range(B) for m in range(H) for r in rr]
+    n, swaps = compare_selection(o, f_u16, kc_ref, n_q, q_pos0, sel.cpu().numpy(), cnt.cpu().numpy(), rows)
+    say(f"  rows {n}, tie swaps {swaps}")
+
+
+def test_select_is_deterministic(dev):
+    say("select determinism")
+    w, case = make(1, 2, 4, 32768, 32768, 64, 4100)
+    s, o = shapes(1, 2, 4, 64, 32768, 512)
+    kc = gpu_compress(s, case["k"].to(dev), 32768, 512, 512, dev)
+    f = case["f"].to(dev)
+    a, ca = gpu_select(s, f, 32768, 0, kc, dev)
+    b, cb = gpu_select(s, f, 32768, 0, kc, dev)
+    assert torch.equal(a, b) and torch.equal(ca, cb)
+
+
+# ----------------------------------------------------------------------------- attention
+
+ATTN = [
+    # B, H, G, T, n_q, k_total
+    (1, 8, 4, 4096, 1, 16),
+    (2, 2, 4, 1000, 1, 5),
+    (2, 2, 4, 32768, 1, 64),
+    (1, 2, 1, 8192, 1, 32),
+    (1, 2, 8, 8192, 1, 32),
+    (1, 1, 16, 8192, 1, 32),
+    (1, 1, 4, 77, 1, 3),
+    (1, 2, 4, 640, 640, 4),
+    (1, 1, 4, 8192, 300, 16),
+]
+
+
+@pytest.mark.parametrize("B,H,G,T,n_q,k_total", ATTN)
+def test_attention_on_oracle_sets(dev, B, H, G, T, n_q, k_total):
+    say(f"attention B{B} H{H} G{G} T{T} n_q{n_q} k{k_total}")
+    w, case = make(B, H, G, T, n_q, k_total, 5000 + T + G)
+    t_cap = -(-T // 64) * 64
+    nb = max(T // 64, 1)
+    s, o = shapes(B, H, G, k_total, t_cap, nb)
+    q_pos0 = T - n_q
+    k16, v16, q16 = inputs.to_u16(case["k"]), inputs.to_u16(case["v"]), inputs.to_u16(case["q"])
+    kc_ref = oracle.compress_keys(o, k16, T, 0, T // 64)
+    sel, cnt = oracle.forecast_select(o, inputs.to_u16(case["f"]), n_q, q_pos0, kc_ref)
+    out = gpu_attend(s, case["q"].to(dev), n_q, q_pos0, case["k"].to(dev), case["v"].to(dev), 0,
+                     torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), dev)
+    ref = oracle.sparse_attn(o, q16, n_q, q_pos0, k16, v16, 0, sel, cnt, SCALE)
+    worst = compare_attention(out.float().cpu().numpy(), ref, "attention")
+    say(f"  max err {worst:.3g}")
+
+
+def test_attention_staging_mode(dev):
+    say("attention staging mode")
+    B, H, G, T, k_total = 2, 2, 4, 8192, 16
+    w, case = make(B, H, G, T, 1, k_total, 5100)
+    s, o = shapes(B, H, G, k_total, T, T // 64)
+    k16, v16 = inputs.to_u16(case["k"]), inputs.to_u16(case["v"])
+    kc_ref = oracle.compress_keys(o, k16, T, 0, T // 64)
+    sel, cnt = oracle.forecast_select(o, inputs.to_u16(case["f"]), 1, T - 1, kc_ref)
+    st_k, st_v = oracle.gather_blocks(o, k16, v16, sel[:, :, 0], cnt[:, :, 0])
+    out = gpu_attend(s, case["q"].to(dev), 1, T - 1, inputs.from_u16(st_k, dev), inputs.from_u16(st_v, dev), 1,
+                     torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), dev)
+    ref = oracle.sparse_attn(o, inputs.to_u16(case["q"]), 1, T - 1, k16, v16, 0, sel, cnt, SCALE)
+    compare_attention(out.float().cpu().numpy(), ref, "staging")
+
+
+def test_attention_order_invariance_and_skips(dev):
+    say("attention order invariance")
+    B, H, G, T, k_total = 2, 2, 4, 8192, 16
+    w, case = make(B, H, G, T, 1, k_total, 5200)
+    s, o = shapes(B, H, G, k_total, T, T // 64)
+    k16 = inputs.to_u16(case["k"])
+    kc_ref = oracle.compress_keys(o, k16, T, 0, T // 64)
+    sel, cnt = oracle.forecast_select(o, inputs.to_u16(case["f"]), 1, T - 1, kc_ref)
+    rng = np.random.default_rng(1)
+    perm = sel.copy()
+    for b in range(B):
+        for m in range(H):
+            perm[b, m, 0, :cnt[b, m, 0]] = rng.permutation(perm[b, m, 0, :cnt[b, m, 0]])
+    args = (case["q"].to(dev), 1, T - 1, case["k"].to(dev), case["v"].to(dev), 0)
+    a = gpu_attend(s, *args, torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), dev)
+    b_ = gpu_attend(s, *args, torch.from_numpy(perm).to(dev), torch.from_numpy(cnt).to(dev), dev)
+    assert (a.float() - b_.float()).abs().max().item() <= 2e-2
+    # entries outside [0, blk(p)] are skipped
+    s2, o2 = shapes(B, H, G, k_total + 2, T, T // 64)
+    sel2 = np.concatenate([sel, np.array([-3, 30000], np.int16)[None, None, None].repeat(B, 0).repeat(H, 1)], axis=-1)
+    c = gpu_attend(s2, *args, torch.from_numpy(np.ascontiguousarray(sel2)).to(dev),
+                   torch.from_numpy(cnt + 2).to(dev), dev)
+    assert (a.float() - c.float()).abs().max().item() <= 2e-2
+
+
+# ----------------------------------------------------------------------------- gather
+
+def test_gather_bitwise_and_host_checks(dev):
+    say("gather")
+    B, H, G, T, k_total = 2, 2, 4, 8192, 16
+    w, case = make(B, H, G, T, 1, k_total, 5300)
+    s, o = shapes(B, H, G, k_total, T, T // 64)
+    k16, v16 = inputs.to_u16(case["k"]), inputs.to_u16(case["v"])
+    kc_ref = oracle.compress_keys(o, k16, T, 0, T // 64)
+    sel, cnt = oracle.forecast_select(o, inputs.to_u16(case["f"]), 1, T - 1, kc_ref)
+    hk = case["k"].pin_memory()
+    hv = case["v"].pin_memory()
+    ref_k, ref_v = oracle.gather_blocks(o, k16, v16, sel[:, :, 0], cnt[:, :, 0])
+    sel_d = torch.from_numpy(np.ascontiguousarray(sel[:, :, 0])).to(dev)
+    cnt_d = torch.from_numpy(np.ascontiguousarray(cnt[:, :, 0])).to(dev)
+    for nwg in (1, 7, 64):
+        st_k = torch.zeros(B, H, k_total, 64, 128, dtype=torch.bfloat16, device=dev)
+        st_v = torch.zeros_like(st_k)
+        side = torch.cuda.Stream()
+        sp.sparda_gather_blocks(s, hk, hv, sel_d, cnt_d, st_k, st_v, nwg, side)
+        side.synchronize()
+        assert np.array_equal(inputs.to_u16(st_k), ref_k) and np.array_equal(inputs.to_u16(st_v), ref_v)
+    with pytest.raises(sp.SpardaError) as ei:
+        sp.sparda_gather_blocks(s, case["k"], case["v"], sel_d, cnt_d, st_k, st_v, 8)  # pageable memory
+    assert ei.value.status == sp.SPARDA_ERR_HOST_NOT_MAPPED
+
+
+# ----------------------------------------------------------------------------- full-size workloads
+
+def _decode_full(dev, name, n_sample_rows, n_sample_heads):
+    w = inputs.WORKLOADS[name]
+    T, nb = w.seq_len, w.n_blocks
+    say(f"full workload {name}: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, o = shapes(w.batch, w.n_kv_heads, w.group_size, w.k_total, T, nb)
+    kc = gpu_compress(s, case["k"], T, nb, nb, dev)
+    sel, cnt = gpu_select(s, case["f"], 1, T - 1, kc, dev)
+    rng = np.random.default_rng(7)
+    pairs = sorted({(int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads))) for _ in range(n_sample_rows)})
+    sel_mixed = sel.clone()
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    _, o1 = shapes(1, 1, w.group_size, w.k_total, T, nb)
+    swaps = 0
+    for (b, m) in pairs:
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        kc_ref = oracle.compress_keys(o1, k16, T, 0, nb)
+        assert np.array_equal(inputs.to_u16(kc[b:b + 1, m:m + 1]), kc_ref), f"K~ of {(b, m)}"
+        f16 = inputs.to_u16(case["f"][b:b + 1, m:m + 1])
+        _, sw = compare_selection(o1, f16, kc_ref, 1, T - 1, sel_np[b:b + 1, m:m + 1], cnt_np[b:b + 1, m:m + 1],
+                                  [(0, 0, 0)])
+        swaps += sw
+        ref_sel, ref_cnt, _ = oracle.select_row(o1, f16, 1, T - 1, kc_ref, 0, 0, 0)
+        sel_mixed[b, m, 0] = torch.from_numpy(ref_sel)
+        # planted blocks are all chosen (5% planted <= top-k slots)
+        planted = set(case["plants"][b, m].tolist())
+        chosen = set(ref_sel[:ref_cnt].tolist()) - {0, nb - 2, nb - 1}
+        if len(planted) <= w.k_total - 3:
+            assert planted <= chosen, "every planted block is selected"
+        else:
+            assert chosen <= planted, "every selected candidate is a planted block"
+    out = gpu_attend(s, case["q"], 1, T - 1, case["k"], case["v"], 0, sel_mixed, cnt, dev)
+    worst = 0.0
+    for (b, m) in pairs[:n_sample_heads]:
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][b:b + 1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][b:b + 1, m * w.group_size:(m + 1) * w.group_size])
+        ssel = sel_mixed[b:b + 1, m:m + 1].cpu().numpy()
+        scnt = cnt[b:b + 1, m:m + 1].cpu().numpy()
+        ref = oracle.sparse_attn(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE)
+        got = out[b:b + 1, m * w.group_size:(m + 1) * w.group_size].float().cpu().numpy()
+        worst = max(worst, compare_attention(got, ref, f"{name} {(b, m)}"))
+    say(f"  sampled {len(pairs)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
+
+
+def test_full_decode_b1_t4k_all_rows(dev):
+    _decode_full(dev, "decode_b1_t4k", 64, 64)
+
+
+def test_full_decode_b8_t32k_samples(dev):
+    _decode_full(dev, "decode_b8_t32k", 24, 12)
+
+
+def test_full_decode_b32_t128k_samples(dev):
+    _decode_full(dev, "decode_b32_t128k", 16, 8)
+
+
+def test_full_prefill_t32k_samples(dev):
+    w = inputs.WORKLOADS["prefill_b1_t32k"]
+    T, nb = w.seq_len, w.n_blocks
+    say("full workload prefill_b1_t32k: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, o = shapes(w.batch, w.n_kv_heads, w.group_size, w.k_total, T, nb)
+    kc = gpu_compress(s, case["k"], T, nb, nb, dev)
+    sel, cnt = gpu_select(s, case["f"], T, 0, kc, dev)
+    rng = np.random.default_rng(9)
+    ms = [int(x) for x in rng.integers(0, w.n_kv_heads, size=3)]
+    rows_r = sorted(set(int(x) for x in rng.integers(0, T, size=40)) | {0, 63, 64, 4095, 4096, T - 1})
+    _, o1 = shapes(1, 1, w.group_size, w.k_total, T, nb)
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    sel_mixed = sel.clone()
+    swaps = 0
+    for m in ms:
+        k16 = inputs.to_u16(case["k"][0:1, m:m + 1])
+        kc_ref = oracle.compress_keys(o1, k16, T, 0, nb)
+        f16 = inputs.to_u16(case["f"][0:1, m:m + 1])
+        _, sw = compare_selection(o1, f16, kc_ref, T, 0, sel_np[0:1, m:m + 1], cnt_np[0:1, m:m + 1],
+                                  [(0, 0, r) for r in rows_r])
+        swaps += sw
+        for r in rows_r:
+            ref_sel, _, _ = oracle.select_row(o1, f16, T, 0, kc_ref, 0, 0, r)
+            sel_mixed[0, m, r] = torch.from_numpy(ref_sel)
+    out = gpu_attend(s, case["q"], T, 0, case["k"], case["v"], 0, sel_mixed, cnt, dev)
+    worst = 0.0
+    for m in ms[:2]:
+        G = w.group_size
+        k16 = inputs.to_u16(case["k"][0:1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][0:1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][0:1, m * G:(m + 1) * G])
+        ssel = sel_mixed[0:1, m:m + 1].cpu().numpy()
+        scnt = cnt[0:1, m:m + 1].cpu().numpy()
+        for r in rows_r[::3]:
+            for h in range(G):
+                ref = oracle.attend_row(o1, q16, T, 0, k16, v16, 0, ssel, scnt, SCALE, 0, h, r)
+                got = out[0, m * G + h, r].float().cpu().numpy()
+                worst = max(worst, compare_attention(got, ref, f"prefill {(m, h, r)}"))
+    say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
