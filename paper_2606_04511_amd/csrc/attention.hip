@@ -3,10 +3,11 @@
 // attended blocks S, all G query heads of a GQA group sharing S.
 //
 // Work unit: one query row (batch b, group m, row r) and a split of its selected-block list.  A
-// workgroup has 4 wavefronts; each wavefront walks blocks split_begin + wave, +4, ... with its own
-// online-softmax state, then the 4 states are merged through LDS.  With several splits per row
-// the merged (max, sum, acc) partials go to the workspace and a combine kernel merges them by
-// log-sum-exp; with one split the workgroup writes the bf16 output directly.
+// workgroup has 8 wavefronts; each wavefront walks blocks split_begin + wave, +8, ... with its own
+// online-softmax state, then the 8 states are merged through LDS.  With 256 or more rows (e.g.
+// batch 32 x 8 groups) a row is one split and the workgroup writes the bf16 output directly;
+// with fewer rows the block list is split, the merged (max, sum, acc) partials go to the
+// workspace, and a combine kernel merges them by log-sum-exp.
 //
 // Per 64-token block a wavefront:
 //   * loads the 16 KiB K block as the MFMA A operand (token rows x head-dim columns, 16-byte
@@ -26,12 +27,15 @@
 namespace sparda {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kAttnWaves = 8;        // wavefronts per attention workgroup
+constexpr int kRowsFillChip = 256;   // rows at which one workgroup per row fills 256 CUs
+constexpr int kMaxSplits = 64;
 
-template <int G>
-__global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
-  __shared__ __align__(16) float p_lds[4][64][G];
-  __shared__ float st_m[4][G], st_l[4][G];
-  __shared__ __align__(16) float st_acc[4][G][kHeadDim];
+template <int G, int NW>
+__global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
+  __shared__ __align__(16) float p_lds[NW][64][G];
+  __shared__ float st_m[NW][G], st_l[NW][G];
+  __shared__ __align__(16) float st_acc[NW][G][kHeadDim];
   const int64_t row = blockIdx.x;
   const int split = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -64,7 +68,7 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
 
   const int16_t* srow = a.sel + row * a.k_total;
-  for (int s = s_begin + wave; s < s_end; s += 4) {
+  for (int s = s_begin + wave; s < s_end; s += NW) {
     const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
     if (j < 0 || j > blk) continue;
     int64_t base;
@@ -164,15 +168,15 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
       for (int e = 0; e < 8; ++e) st_acc[wave][h][8 * lane + e] = acc[h][e];
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += 256) {
+  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += NW * 64) {
     const int h = idx / kHeadDim, d = idx % kHeadDim;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, st_m[w][h]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, st_m[w][h]);
     float L = 0.f, A = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < NW; ++w) {
         const float mw = st_m[w][h];
         if (mw != -INFINITY) {
           const float sc = exp2f(mw - M);
@@ -194,57 +198,82 @@ __global__ __launch_bounds__(256) void sparse_attn_kernel(AttnArgs a) {
   }
 }
 
-// Merge the split partials of one row by log-sum-exp.
+// Merge the split partials of one (row, head) by log-sum-exp: 128 threads, one per head dim.
 template <int G>
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
-  const int64_t row = blockIdx.x;
+__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
+  __shared__ float w_s[kMaxSplits], l_s[kMaxSplits];
+  __shared__ float total_l;
+  const int64_t rh = blockIdx.x;
+  const int64_t row = rh / G;
+  const int h = (int)(rh % G);
   const int r = (int)(row % a.n_q);
   const int64_t bm = row / a.n_q;
   const int m = (int)(bm % a.n_kv_heads);
   const int b = (int)(bm / a.n_kv_heads);
   const int64_t Hq = (int64_t)a.n_kv_heads * G;
-  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += 256) {
-    const int h = idx / kHeadDim, d = idx % kHeadDim;
-    const float* base = a.ws + (row * a.n_splits * G + h) * (kHeadDim + 2);
-    const int64_t stride = (int64_t)G * (kHeadDim + 2);
-    float M = -INFINITY;
-    for (int s = 0; s < a.n_splits; ++s) M = fmaxf(M, base[s * stride]);
-    float L = 0.f, A = 0.f;
-    if (M != -INFINITY) {
-      for (int s = 0; s < a.n_splits; ++s) {
-        const float ms = base[s * stride];
-        if (ms != -INFINITY) {
-          const float sc = exp2f(ms - M);
-          L = fmaf(base[s * stride + 1], sc, L);
-          A = fmaf(base[s * stride + 2 + d], sc, A);
-        }
-      }
-    }
-    a.o[(((int64_t)b * Hq + (int64_t)m * G + h) * a.n_q + r) * kHeadDim + d] = f32_to_bf16(L > 0.f ? A / L : 0.f);
+  const int tid = threadIdx.x;
+  const int64_t stride = (int64_t)G * (kHeadDim + 2);
+  const float* base = a.ws + (row * a.n_splits * G + h) * (kHeadDim + 2);
+  const int ns = a.n_splits;  // <= kMaxSplits
+  for (int s = tid; s < ns; s += 128) {
+    w_s[s] = base[s * stride];
+    l_s[s] = base[s * stride + 1];
   }
+  __syncthreads();
+  if (tid < 64) {
+    float M = -INFINITY;
+    for (int s = tid; s < ns; s += 64) M = fmaxf(M, w_s[s]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+    float L = 0.f;
+    for (int s = tid; s < ns; s += 64) {
+      const float ms = w_s[s];
+      const float wgt = (M == -INFINITY || ms == -INFINITY) ? 0.f : exp2f(ms - M);
+      w_s[s] = wgt;
+      L = fmaf(l_s[s], wgt, L);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o, 64);
+    if (tid == 0) total_l = L;
+  }
+  __syncthreads();
+  float A = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float wgt = w_s[s];
+    if (wgt != 0.f) A = fmaf(base[s * stride + 2 + tid], wgt, A);
+  }
+  const float L = total_l;
+  a.o[(((int64_t)b * Hq + (int64_t)m * G + h) * a.n_q + r) * kHeadDim + tid] = f32_to_bf16(L > 0.f ? A / L : 0.f);
 }
 
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split) {
-  // Aim for ~4096 workgroups (16 per CU) so that enough K/V bytes are in flight; at least 4
-  // blocks (one per wavefront) per split.
-  const int max_splits = (k_total + 3) / 4;
-  int64_t want = rows >= 4096 ? 1 : (4096 + rows - 1) / rows;
-  int ns = (int)(want < max_splits ? want : max_splits);
-  if (ns < 1) ns = 1;
-  int bps = (k_total + ns - 1) / ns;
-  ns = (k_total + bps - 1) / bps;
-  *n_splits = ns;
+  // One 8-wave workgroup per row when there are enough rows to fill the chip (no partials, no
+  // combine).  With fewer rows, split the block list so that ~512 workgroups are in flight,
+  // keeping at least one block per wavefront.
+  int ns = 1;
+  if (rows < kRowsFillChip) {
+    const int max_splits = (k_total + kAttnWaves - 1) / kAttnWaves;
+    const int64_t want = (2 * kRowsFillChip + rows - 1) / rows;
+    ns = (int)(want < max_splits ? want : max_splits);
+    if (ns > kMaxSplits) ns = kMaxSplits;
+    if (ns < 1) ns = 1;
+  }
+  const int bps = (k_total + ns - 1) / ns;
+  *n_splits = (k_total + bps - 1) / bps;
   *blocks_per_split = bps;
 }
 
 template <int G>
 static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
+  // Groups of more than 6 heads keep acc[G][8] in registers: 4 wavefronts (one per SIMD) give
+  // each wavefront the whole register file instead of spilling.
+  constexpr int NW = G <= 6 ? kAttnWaves : 4;
   dim3 grid((unsigned)rows, (unsigned)a.n_splits);
-  hipLaunchKernelGGL(sparse_attn_kernel<G>, grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL((sparse_attn_kernel<G, NW>), grid, dim3(NW * 64), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
-  hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)rows), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)(rows * G)), dim3(128), 0, stream, a);
   return hipGetLastError();
 }
 

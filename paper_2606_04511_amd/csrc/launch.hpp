@@ -68,12 +68,14 @@ struct AttnArgs {
 // Tiles of the fused multi-row selection kernel.
 constexpr int kSelTileRows = 64;
 constexpr int kSelTileMaxCand = 512;
+// Candidates a decode row may have for the fused decode kernel (scores held in 64 KiB of LDS).
+constexpr int kDecodeMaxCand = 16384;
 
 hipError_t launch_compress(const uint16_t* k, uint16_t* kc, int32_t rows, int64_t t_cap, int64_t nc_cap,
                            int32_t blk_begin, int32_t blk_end, hipStream_t stream);
 
-// True when the multi-row fused kernel handles every tile (no score scratch needed).
-bool select_uses_fused(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local);
+// True when the call takes the row-wise path, which keeps its scores in workspace scratch.
+bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 
 // Split count and blocks per split the attention launcher uses for `rows` query rows.

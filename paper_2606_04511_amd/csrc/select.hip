@@ -215,15 +215,169 @@ __global__ __launch_bounds__(256) void tile_select_kernel(SelectArgs a, int n_ti
   }
 }
 
-bool select_uses_fused(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
-  if (n_q <= 1) return false;
+// ---- fused decode path ---------------------------------------------------------------------
+
+constexpr int kDecThreads = 512;  // 8 wavefronts per row
+
+// Block-wide exclusive rank of `flag` in thread order within one pass over kDecThreads items,
+// plus the pass total.  wave_cnt: kDecThreads/64 ints of LDS.  Contains two barriers.
+__device__ __forceinline__ int block_rank(bool flag, int* wave_cnt, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t b = __ballot(flag);
+  if (lane == 0) wave_cnt[wave] = __popcll(b);
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kDecThreads / 64; ++w) {
+    const int c = wave_cnt[w];
+    before += w < wave ? c : 0;
+    all += c;
+  }
+  __syncthreads();
+  *total = all;
+  return before + mbcnt64(b);
+}
+
+// One workgroup per decode row (batch, group): the Forecast GEMV over all candidates into LDS,
+// then a block-wide radix select over the LDS scores and an ordered emission.  Scores never
+// leave the CU.
+__global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a) {
+  __shared__ float sc[kDecodeMaxCand];
+  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  const int64_t row = blockIdx.x;  // (b * Hkv + m), one query row each
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
+  int16_t* out = a.sel + row * a.k_total;
+  if (wave == 0) emit_forced(out, g, a.k_total, lane);
+  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  int16_t* chosen_out = out + g.init_hi;
+  const int C = g.n_cand;
+  if (g.n_take >= C) {
+    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
+    return;
+  }
+  if (g.n_take <= 0) return;
+
+  // Scores: lane reads dims 8*(lane%16).. of candidate base + 4 i + lane/16 (1 KiB per load).
+  {
+    const int c = lane & 15, rs = lane >> 4;
+    const uint4 fw = ld16(a.f + row * kHeadDim + c * 8);
+    const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
+    const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
+    const uint16_t* kbase = a.kc + (row * a.nc_cap + g.cand_lo) * kHeadDim + c * 8;
+    for (int base = wave * 64; base < C; base += kDecThreads) {
+      uint4 kw[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int idx = base + 4 * i + rs;
+        kw[i] = idx < C ? ld16(kbase + (int64_t)idx * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float d = f0 * bf16lo(kw[i].x);
+        d = fmaf(f1, bf16hi(kw[i].x), d);
+        d = fmaf(f2, bf16lo(kw[i].y), d);
+        d = fmaf(f3, bf16hi(kw[i].y), d);
+        d = fmaf(f4, bf16lo(kw[i].z), d);
+        d = fmaf(f5, bf16hi(kw[i].z), d);
+        d = fmaf(f6, bf16lo(kw[i].w), d);
+        d = fmaf(f7, bf16hi(kw[i].w), d);
+        d = row16_sum(d);
+        const int idx = base + 4 * i + rs;
+        if (c == 0 && idx < C) sc[idx] = d;
+      }
+    }
+  }
+  __syncthreads();
+
+  // Radix select of the n_take-th largest key, 8 bits per pass, over the whole workgroup.
+  uint32_t prefix = 0u, mask = 0u;
+  int remaining = g.n_take;
+  bool take_all = false;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (tid < 256) hist[tid] = 0u;
+    __syncthreads();
+    for (int i = tid; i < C; i += kDecThreads) {
+      const uint32_t kk = score_key(sc[i]);
+      if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const uint4 h = reinterpret_cast<const uint4*>(hist)[63 - lane];
+      const int lsum = (int)(h.x + h.y + h.z + h.w);
+      const int incl = wave_incl_scan(lsum);
+      const int excl = incl - lsum;
+      if (excl < remaining && remaining <= incl) {
+        int above = excl, d = 255 - 4 * lane, eq = (int)h.w;
+        if (above + (int)h.w < remaining) {
+          above += (int)h.w; d -= 1; eq = (int)h.z;
+          if (above + (int)h.z < remaining) {
+            above += (int)h.z; d -= 1; eq = (int)h.y;
+            if (above + (int)h.y < remaining) { above += (int)h.y; d -= 1; eq = (int)h.x; }
+          }
+        }
+        pick[0] = d;
+        pick[1] = above;
+        pick[2] = eq;
+      }
+    }
+    __syncthreads();
+    const int d = pick[0], above = pick[1], eq = pick[2];
+    remaining -= above;
+    prefix |= (uint32_t)d << shift;
+    mask |= 0xffu << shift;
+    take_all = (eq == remaining);
+    __syncthreads();
+    if (take_all) break;
+  }
+
+  // Emit in ascending candidate order; equal keys at the threshold go to the lowest indices.
+  int base = 0, tie_base = 0;
+  for (int i0 = 0; i0 < C; i0 += kDecThreads) {
+    const int i = i0 + tid;
+    const bool valid = i < C;
+    const uint32_t kk = valid ? score_key(sc[i]) : 0u;
+    bool chosen;
+    if (take_all) {
+      chosen = valid && (kk & mask) >= prefix;
+    } else {
+      const bool tie = valid && kk == prefix;
+      int n_ties;
+      const int trank = tie_base + block_rank(tie, wave_cnt, &n_ties);
+      tie_base += n_ties;
+      chosen = valid && (kk > prefix || (tie && trank < remaining));
+    }
+    int n_chosen;
+    const int pos = base + block_rank(chosen, wave_cnt, &n_chosen);
+    if (chosen && pos < g.n_take) chosen_out[pos] = (int16_t)(g.cand_lo + i);
+    base += n_chosen;
+  }
+}
+
+// Which kernels serve a select call.
+enum SelectPath { kPathDecode, kPathTile, kPathRowwise };
+
+static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
   const RowGeom g = row_geom(q_pos0 + n_q - 1, n_init, n_local, 1 << 30);
-  return g.n_cand <= kSelTileMaxCand;
+  if (n_q == 1) return g.n_cand <= kDecodeMaxCand ? kPathDecode : kPathRowwise;
+  return g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
+}
+
+bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
+  return select_path(n_q, q_pos0, n_init, n_local) == kPathRowwise;
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
-  if (select_uses_fused(a.n_q, a.q_pos0, a.n_init, a.n_local)) {
+  const SelectPath path = select_path(a.n_q, a.q_pos0, a.n_init, a.n_local);
+  if (path == kPathDecode) {
+    hipLaunchKernelGGL(decode_select_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
+    return hipGetLastError();
+  }
+  if (path == kPathTile) {
     const int n_tiles = (a.n_q + kSelTileRows - 1) / kSelTileRows;
     const int64_t grid = (int64_t)a.batch * a.n_kv_heads * n_tiles;
     hipLaunchKernelGGL(tile_select_kernel, dim3((unsigned)grid), dim3(256), 0, stream, a, n_tiles);

@@ -78,11 +78,11 @@ int check_rows(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
   return SPARDA_OK;
 }
 
-// Workspace of sparda_forecast_select: scores of the row-wise path (none for the fused tiles).
+// Workspace of sparda_forecast_select: scores of the row-wise path (none for the fused kernels).
 size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* stride) {
   const sparda::RowGeom g = sparda::row_geom(q_pos0 + n_q - 1, s->n_init, s->n_local, s->k_total);
   *stride = ((int64_t)g.n_cand + 3) & ~(int64_t)3;
-  if (sparda::select_uses_fused(n_q, q_pos0, s->n_init, s->n_local)) return 0;
+  if (!sparda::select_needs_scratch(n_q, q_pos0, s->n_init, s->n_local)) return 0;
   if (g.n_cand == 0) return 0;
   const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
   return (size_t)rows * (size_t)*stride * sizeof(float);

@@ -106,10 +106,12 @@ def test_select_argument_errors(lib):
     assert rc_of(f, s, FAKE, 1, -1, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
     assert rc_of(f, shape(nc_cap=30), FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
     assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE + 1, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG  # sel align
-    # decode needs a score workspace
-    assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
-    need = sp.sparda_workspace_size(s, sp.SPARDA_OP_FORECAST_SELECT, 1, 4095)
-    assert rc_of(f, s, FAKE, 1, 4095, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
+    # multi-row rows with more than 512 candidates take the row-wise path, which needs scratch
+    sl = shape(t_cap=65536, nc_cap=1024)
+    assert rc_of(f, sl, FAKE, 2, 65534, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
+    need = sp.sparda_workspace_size(sl, sp.SPARDA_OP_FORECAST_SELECT, 2, 65534)
+    assert need == 2 * 8 * 2 * 1024 * 4  # rows x stride(1021 -> 1024) x float
+    assert rc_of(f, sl, FAKE, 2, 65534, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
 
 
 def test_attention_argument_errors(lib):
@@ -122,6 +124,7 @@ def test_attention_argument_errors(lib):
         sp.SPARDA_ERR_INVALID_ARG
     assert rc_of(a, s, None, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
     assert rc_of(a, s, FAKE, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
+    assert sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, 4095) > 0  # 16 rows: split
 
 
 def test_gather_argument_errors(lib):
@@ -132,11 +135,13 @@ def test_gather_argument_errors(lib):
 
 
 def test_workspace_sizes(lib):
-    # decode at 128K, B32: one float score per candidate row (2045 candidates, stride 2048)
+    # decode at 128K, B32: fused select (scores stay in LDS); 256 rows fill the chip, one split
     s2 = shape(batch=32, k_total=64, t_cap=131072, nc_cap=2048)
-    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_FORECAST_SELECT, 1, 131071) == 256 * 2048 * 4
-    # 16 splits x 4 heads x (128 + 2) floats per row
-    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_SPARSE_ATTN, 1, 131071) == 256 * 16 * 4 * 130 * 4
+    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_FORECAST_SELECT, 1, 131071) == 0
+    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_SPARSE_ATTN, 1, 131071) == 0
+    # decode at 32K, B8: 64 rows -> 8 splits x 4 heads x (128 + 2) floats per row
+    s1 = shape(batch=8, k_total=64, t_cap=32768, nc_cap=512)
+    assert sp.sparda_workspace_size(s1, sp.SPARDA_OP_SPARSE_ATTN, 1, 32767) == 64 * 8 * 4 * 130 * 4
     # full 32K prefill: fused tiles, no score scratch; one split per row
     s3 = shape(batch=1, k_total=64, t_cap=32768, nc_cap=512)
     assert sp.sparda_workspace_size(s3, sp.SPARDA_OP_FORECAST_SELECT, 32768, 0) == 0
