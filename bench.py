@@ -11,8 +11,9 @@ Secondary legs on the same JSON line:
   prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
                     selects), reported in TFLOP/s of scored (row, candidate) pairs x 2 x 128;
   prefill_attn   -- block-sparse attention of that prefill (ms);
-  gather         -- host-pool -> HBM gather of the selected blocks of a batch-64, 128K decode
-                    layer (GB/s over PCIe), with --gather (off by default: it pins ~34 GB).
+  pipeline       -- the offloaded 32-layer, batch-64, 128K decode step with
+                    one-layer-ahead selection and a side-stream gather from pinned host pools
+                    (GB/s over PCIe, overlapped vs serial step time).
 roofline -- the dominant kernel (decode attention): algorithmic bytes / its average duration
             measured with HIP events on the stream it runs on, against 8 TB/s.
 cpu_baseline -- the CPU oracle on a sample of the decode step's rows, on this host's cores.
@@ -199,48 +200,84 @@ def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
             "us_per_layer_equiv": dt * rows_total / n_rows * 1e6}
 
 
-def gather_leg(dev, iters):
-    """Gather of a batch-64, 128K decode layer's selected blocks from one pinned host pool."""
+def pipeline_leg(dev, steps):
+    """Offloaded 32-layer decode at 128K, batch 64 (pinned host pools, one-layer-ahead gather).
+
+    Layer 0's KV is in HBM; layers 1..31 read their selected blocks from two pinned host pools
+    (layer l uses pool (l-1) mod 2, so 2 x 34.4 GB are pinned instead of 31 x 34.4 GB).  The
+    compressed keys, queries and Forecast rows are distinct per layer.  Reports the gather's
+    workgroup sweep, the overlapped and serial step times, and the per-layer gather and compute
+    times that bound the overlap.
+    """
     from paper_2606_04511_amd import hostmem
+    from paper_2606_04511_amd.pipeline import DecodePipeline
     w = inputs.WORKLOADS["pipeline_b64_t128k_l32"]
-    B, H, T, nb, k_total = w.batch, w.n_kv_heads, w.seq_len, w.n_blocks, w.k_total
-    shape = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=w.group_size, k_total=k_total, t_cap=T, nc_cap=nb)
+    B, H, G, T, nb, K, L = w.batch, w.n_kv_heads, w.group_size, w.seq_len, w.n_blocks, w.k_total, w.layers
+    shape = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=G, k_total=K, t_cap=T, nc_cap=nb)
     pool_bytes = B * H * T * 128 * 2
     t0 = time.time()
-    hk = hostmem.PinnedBuffer(pool_bytes)
-    hv = hostmem.PinnedBuffer(pool_bytes)
-    fill = torch.randn(64 * 1024 * 1024, device=dev).to(torch.bfloat16)  # 128 MiB pattern
-    chunk = fill.numel() * 2
-    for buf in (hk, hv):
-        for off in range(0, pool_bytes, chunk):
-            n = min(chunk, pool_bytes - off)
-            buf.copy_from_device(off, fill.view(torch.uint8)[:n])
+    bufs = [hostmem.PinnedBuffer(pool_bytes) for _ in range(4)]
+    log(f"[bench] pinned 4 x {pool_bytes / 2**30:.1f} GiB host pools in {time.time() - t0:.1f}s")
+    t0 = time.time()
+    fill = torch.randn(64 * 1024 * 1024, device=dev).to(torch.bfloat16).view(torch.uint8)  # 128 MiB
+    for buf in bufs:
+        for off in range(0, pool_bytes, fill.numel()):
+            n = min(fill.numel(), pool_bytes - off)
+            buf.copy_from_device(off, fill[:n])
     torch.cuda.synchronize()
-    log(f"[bench] pinned + filled 2 x {pool_bytes / 2**30:.1f} GiB host pools in {time.time() - t0:.1f}s")
-    g = torch.Generator(device="cpu").manual_seed(w.seed)
-    sel = torch.empty(B, H, k_total, dtype=torch.int16)
-    for i in range(B * H):
-        blocks = torch.cat([torch.tensor([0, nb - 2, nb - 1]), 1 + torch.randperm(nb - 3, generator=g)[:k_total - 3]])
-        sel.view(-1, k_total)[i] = torch.sort(blocks).values.to(torch.int16)
-    sel = sel.to(dev)
-    cnt = torch.full((B, H), k_total, dtype=torch.int16, device=dev)
-    st_k = torch.empty(B, H, k_total, 64, 128, dtype=torch.bfloat16, device=dev)
-    st_v = torch.empty_like(st_k)
+    log(f"[bench] filled the host pools in {time.time() - t0:.1f}s")
+    pools = [None] + [(bufs[2 * ((l - 1) % 2)].ptr, bufs[2 * ((l - 1) % 2) + 1].ptr) for l in range(1, L)]
+    gen = lambda shp, tid: inputs.normal_bf16(shp, w.seed, tid, dev)
+    q = [gen((B, H * G, 1, 128), 1000 + l) for l in range(L)]
+    f = [gen((B, H, 1, 128), 2000 + l) for l in range(L)]
+    f0 = gen((B, H, 1, 128), 2999)
+    kc = [gen((B, H, nb, 128), 3000 + l) for l in range(L)]
+    k0 = gen((B, H, T, 128), 4000)
+    v0 = gen((B, H, T, 128), 4001)
+    moved = 2 * B * H * K * 64 * 256  # K + V bytes gathered per offloaded layer
+
+    # gather sweep over the persistent grid size on a side stream (selection of layer 1)
+    pipe = DecodePipeline(shape, T, q, f, f0, kc, k0, v0, pools, 64, dev)
+    pipe.step()
+    torch.cuda.synchronize()
     side = torch.cuda.Stream()
-    res = {}
-    moved = 2 * B * H * k_total * 64 * 256
-    for nwg in (16, 32, 64, 128, 256):
-        with torch.cuda.stream(side):
-            sp.sparda_gather_blocks(shape, hk.ptr, hv.ptr, sel, cnt, st_k, st_v, nwg, side)
-            ms = time_events(lambda: sp.sparda_gather_blocks(shape, hk.ptr, hv.ptr, sel, cnt, st_k, st_v, nwg, side),
-                             iters, side)
-        res[str(nwg)] = {"ms": ms, "GBps": moved / (ms * 1e-3) / 1e9}
-    # H2D memcpy reference of the same byte count from the same pinned pool
+    sweep = {}
+    for nwg in (8, 16, 32, 64, 128, 256):
+        pipe.n_workgroups = nwg
+        ms = time_events(lambda: pipe._gather(1, side), 5, side)
+        sweep[str(nwg)] = {"ms": ms, "GBps": moved / (ms * 1e-3) / 1e9}
+    best_nwg = int(max(sweep, key=lambda k: sweep[k]["GBps"]))
+    pipe.n_workgroups = best_nwg
     dst = torch.empty(moved // 2, dtype=torch.uint8, device=dev)
-    ms_cp = time_events(lambda: hk.copy_to_device(0, dst), iters, torch.cuda.current_stream())
-    best = max(res.values(), key=lambda r: r["GBps"])
-    return {"workload": f"decode B{B} T={T} k{k_total}: {moved / 1e9:.3f} GB of selected K+V blocks per layer",
-            "by_workgroups": res, "best_GBps": best["GBps"], "h2d_memcpy_GBps": (moved // 2) / (ms_cp * 1e-3) / 1e9}
+    ms_cp = time_events(lambda: bufs[0].copy_to_device(0, dst), 5, torch.cuda.current_stream())
+
+    # per-layer compute alone (select of the next layer + attention from staging) and gather alone
+    comp = torch.cuda.current_stream()
+    ms_compute = time_events(lambda: (pipe._select(pipe.f[1], 2), pipe._attend(1)), 10, comp)
+    ms_gather = time_events(lambda: pipe._gather(1, comp), 5, comp)
+
+    def timed(overlap):
+        pipe.step(overlap=overlap)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            pipe.step(overlap=overlap)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+
+    ms_overlap = timed(True)
+    ms_serial = timed(False)
+    bound = (L - 1) * max(ms_gather, ms_compute) + ms_compute
+    for b in bufs:
+        b.free()
+    return {
+        "workload": f"decode pipeline, {L} layers, B{B} T={T} k{K}: {moved / 1e9:.3f} GB gathered per offloaded layer",
+        "gather_sweep": sweep, "n_workgroups": best_nwg,
+        "gather_GBps": sweep[str(best_nwg)]["GBps"], "h2d_memcpy_GBps": (moved // 2) / (ms_cp * 1e-3) / 1e9,
+        "gather_ms_per_layer": ms_gather, "compute_ms_per_layer": ms_compute,
+        "ms_per_step_overlap": ms_overlap, "ms_per_step_serial": ms_serial,
+        "ms_per_step_bound": bound, "tokens_per_s": B / (ms_overlap * 1e-3),
+    }
 
 
 def main():
@@ -250,7 +287,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--gather", action="store_true", help="also time the host-pool gather (pins ~34 GB)")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the offloaded 32-layer decode pipeline (it pins 4 x 17.2 GB of host memory)")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -322,8 +360,11 @@ def main():
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
             f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
-    if args.gather:
-        out["gather"] = gather_leg(dev, 5)
+    if not args.no_pipeline:
+        del layer.case
+        out["pipeline"] = pipeline_leg(dev, 3)
+        log(f"[bench] pipeline {out['pipeline']['ms_per_step_overlap']:.1f} ms/step overlapped, "
+            f"{out['pipeline']['ms_per_step_serial']:.1f} serial")
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layer, args.cpu_rows)
     print(json.dumps(out))

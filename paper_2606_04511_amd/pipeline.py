@@ -1,0 +1,105 @@
+"""Offloaded decode across layers with one-layer-ahead selection (paper Sec. 4.1 and 4.3, Alg. 2).
+
+Per decode step and layer l (the model's projections and FFN are outside this path):
+  * compute stream: select layer l+1's blocks from layer l's Forecast rows and layer l+1's
+    compressed keys (Eq. 4); record `selected[l+1]`;
+  * side stream: wait for `selected[l+1]` and for the attention that last read the staging
+    slot about to be overwritten, then gather layer l+1's selected K/V blocks from its pinned
+    host pool into that staging slot (`sparda_gather_blocks`); record `gathered[l+1]`;
+  * compute stream: wait for `gathered[l]` (launched during layer l-1) and attend layer l from
+    its staging slot.
+Layer 0 keeps its KV cache in HBM and selects with its current-layer Forecast (Sec. 4.1).  Two
+staging slots alternate between layers.  All device buffers are allocated up front; a step
+allocates nothing.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import sparda as sp
+
+
+class DecodePipeline:
+    """L layers of one decode step.
+
+    shape        -- sparda shape of one layer (batch, heads, k_total, t_cap, nc_cap ...)
+    t_ctx        -- tokens in the context; the query sits at position t_ctx - 1
+    q[l]         -- bf16 [B][Hq][1][D] device, query of layer l
+    f[l]         -- bf16 [B][Hkv][1][D] device, Forecast rows of layer l (scores layer l+1)
+    f0_cur       -- bf16 [B][Hkv][1][D] device, layer 0's current-layer Forecast
+    kc[l]        -- bf16 [B][Hkv][nc_cap][D] device, compressed keys of layer l
+    k0, v0       -- bf16 [B][Hkv][t_cap][D] device, layer 0's KV cache
+    pools[l]     -- (host_k_ptr, host_v_ptr) of layer l (l >= 1): device-mapped pinned memory
+                    laid out [B][Hkv][t_cap][D]; pools may be shared between layers
+    n_workgroups -- persistent-grid size of the gather (its CU budget)
+    """
+
+    def __init__(self, shape: sp.SpardaShape, t_ctx: int, q, f, f0_cur, kc, k0, v0, pools, n_workgroups: int,
+                 device, sm_scale: float | None = None):
+        L = len(q)
+        assert len(f) == L and len(kc) == L and len(pools) == L and L >= 1
+        self.shape, self.t_ctx, self.L = shape, t_ctx, L
+        self.q, self.f, self.f0_cur, self.kc, self.k0, self.v0, self.pools = q, f, f0_cur, kc, k0, v0, pools
+        self.n_workgroups = n_workgroups
+        self.scale = 1.0 / math.sqrt(shape.head_dim) if sm_scale is None else sm_scale
+        B, H, K = shape.batch, shape.n_kv_heads, shape.k_total
+        self.sel = [torch.empty(B, H, 1, K, dtype=torch.int16, device=device) for _ in range(L)]
+        self.cnt = [torch.empty(B, H, 1, dtype=torch.int16, device=device) for _ in range(L)]
+        self.o = [torch.empty(B, shape.n_q_heads, 1, shape.head_dim, dtype=torch.bfloat16, device=device)
+                  for _ in range(L)]
+        st = (B, H, K, shape.block_size, shape.head_dim)
+        self.stage = [(torch.empty(st, dtype=torch.bfloat16, device=device),
+                       torch.empty(st, dtype=torch.bfloat16, device=device)) for _ in range(2)]
+        n_sel = sp.sparda_workspace_size(shape, sp.SPARDA_OP_FORECAST_SELECT, 1, t_ctx - 1)
+        n_att = sp.sparda_workspace_size(shape, sp.SPARDA_OP_SPARSE_ATTN, 1, t_ctx - 1)
+        self.ws_sel = torch.empty(max(n_sel, 16), dtype=torch.uint8, device=device)
+        self.ws_att = torch.empty(max(n_att, 16), dtype=torch.uint8, device=device)
+        self.side = torch.cuda.Stream(device=device)
+        self.ev_sel = [torch.cuda.Event() for _ in range(L)]
+        self.ev_gather = [torch.cuda.Event() for _ in range(L)]
+        self.ev_attn = [torch.cuda.Event() for _ in range(L)]
+
+    def _select(self, f_rows, layer):
+        sp.sparda_forecast_select(self.shape, f_rows, 1, self.t_ctx - 1, self.kc[layer], self.sel[layer],
+                                  self.cnt[layer], self.ws_sel)
+
+    def _gather(self, layer, stream):
+        hk, hv = self.pools[layer]
+        sk, sv = self.stage[layer % 2]
+        sp.sparda_gather_blocks(self.shape, hk, hv, self.sel[layer], self.cnt[layer], sk, sv, self.n_workgroups,
+                                stream)
+
+    def _attend(self, layer):
+        if layer == 0:
+            k, v, mode = self.k0, self.v0, 0
+        else:
+            k, v = self.stage[layer % 2]
+            mode = 1
+        sp.sparda_sparse_attn(self.shape, self.q[layer], 1, self.t_ctx - 1, k, v, mode, self.sel[layer],
+                              self.cnt[layer], self.scale, self.o[layer], self.ws_att)
+
+    def step(self, overlap: bool = True):
+        """Enqueue one decode step over all layers on the current stream (and the side stream).
+        overlap=False runs each gather on the compute stream right before its attention."""
+        comp = torch.cuda.current_stream()
+        self._select(self.f0_cur, 0)
+        for l in range(self.L):
+            if l + 1 < self.L:
+                self._select(self.f[l], l + 1)
+                if overlap:
+                    self.ev_sel[l + 1].record(comp)
+                    self.side.wait_event(self.ev_sel[l + 1])
+                    if l >= 1:  # the slot of layer l+1 was last read by layer l-1's attention
+                        self.side.wait_event(self.ev_attn[l - 1])
+                    self._gather(l + 1, self.side)
+                    self.ev_gather[l + 1].record(self.side)
+            if l >= 1:
+                if overlap:
+                    comp.wait_event(self.ev_gather[l])
+                else:
+                    self._gather(l, comp)
+            self._attend(l)
+            self.ev_attn[l].record(comp)
+        return self.o

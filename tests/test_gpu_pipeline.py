@@ -1,0 +1,157 @@
+"""GPU tests of the offloaded decode pipeline (one-layer-ahead selection + side-stream gather).
+
+The oracle chain follows the paper: S_0 = select(F_0^cur, K~_0); S_{l+1} = select(F_l, K~_{l+1});
+O_l = attend(Q_l, K_l, V_l, S_l), with layers >= 1 reading their KV from pinned host pools that
+two layers share.  The race checks poison the staging buffers with NaN and hold the side stream
+back with a bounded spin before each gather: correct event ordering must still give the oracle's
+output, and a copy of the pipeline that drops the compute stream's wait must be caught.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_04511_amd.sparda as sp
+from paper_2606_04511_amd import hostmem, inputs
+from paper_2606_04511_amd.pipeline import DecodePipeline
+from parity import compare_attention, compare_selection
+
+pytestmark = pytest.mark.gpu
+
+B, H, G, T, K, L, P = 2, 2, 4, 8192, 16, 4, 2
+NB = T // 64
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def setup():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    sp.load()
+    dev = torch.device("cuda:0")
+    shape = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=G, k_total=K, t_cap=T, nc_cap=NB)
+    oshape = oracle.Shape(batch=B, n_kv_heads=H, group_size=G, k_total=K, t_cap=T, nc_cap=NB)
+    w = inputs.Workload("pipe", batch=B, seq_len=T, n_q=1, n_kv_heads=H, group_size=G, k_total=K, seed=6000)
+    q = [inputs.normal_bf16((B, H * G, 1, 128), 6000, 10 + l) for l in range(L)]
+    f = [inputs.normal_bf16((B, H, 1, 128), 6000, 50 + l) for l in range(L)]
+    f0 = inputs.normal_bf16((B, H, 1, 128), 6000, 99)
+    kv = []  # kv[0] is layer 0 (HBM); kv[1 + p] is host pool p
+    for i in range(1 + P):
+        kv.append((inputs.keys_with_plants(w, f0[:, :, 0] if i == 0 else f[i - 1][:, :, 0], T, tensor_id=200 + i),
+                   inputs.values(w, T, tensor_id=300 + i)))
+    pools, bufs = [], []
+    for p in range(P):
+        hk = hostmem.PinnedBuffer(kv[1 + p][0].numel() * 2)
+        hv = hostmem.PinnedBuffer(kv[1 + p][1].numel() * 2)
+        hk.as_tensor(torch.bfloat16).copy_(kv[1 + p][0].reshape(-1))
+        hv.as_tensor(torch.bfloat16).copy_(kv[1 + p][1].reshape(-1))
+        bufs += [hk, hv]
+        pools.append((hk.ptr, hv.ptr))
+    layer_kv = [kv[0]] + [kv[1 + (l - 1) % P] for l in range(1, L)]
+    layer_pool = [None] + [pools[(l - 1) % P] for l in range(1, L)]
+    kc_ref = [oracle.compress_keys(oshape, inputs.to_u16(layer_kv[l][0]), T, 0, NB) for l in range(L)]
+    kc = []
+    for l in range(L):
+        t = torch.zeros(B, H, NB, 128, dtype=torch.bfloat16, device=dev)
+        sp.sparda_compress_keys(shape, layer_kv[l][0].to(dev), T, 0, NB, t)
+        kc.append(t)
+    torch.cuda.synchronize()
+    for l in range(L):
+        assert np.array_equal(inputs.to_u16(kc[l]), kc_ref[l])
+    pipe_args = dict(shape=shape, t_ctx=T, q=[x.to(dev) for x in q], f=[x.to(dev) for x in f], f0_cur=f0.to(dev),
+                     kc=kc, k0=kv[0][0].to(dev), v0=kv[0][1].to(dev), pools=layer_pool, n_workgroups=16,
+                     device=dev)
+    # the oracle chain
+    ref_sel, ref_out = [], []
+    for l in range(L):
+        frows = f0 if l == 0 else f[l - 1]
+        s, c = oracle.forecast_select(oshape, inputs.to_u16(frows), 1, T - 1, kc_ref[l])
+        ref_sel.append((s, c, frows))
+        ref_out.append(oracle.sparse_attn(oshape, inputs.to_u16(q[l]), 1, T - 1, inputs.to_u16(layer_kv[l][0]),
+                                          inputs.to_u16(layer_kv[l][1]), 0, s, c, 1.0 / math.sqrt(128)))
+    return dict(dev=dev, oshape=oshape, pipe_args=pipe_args, ref_sel=ref_sel, ref_out=ref_out, kc_ref=kc_ref,
+                bufs=bufs)
+
+
+def check(setup, pipe):
+    torch.cuda.synchronize()
+    for l in range(L):
+        s, c, frows = setup["ref_sel"][l]
+        gs, gc = pipe.sel[l].cpu().numpy(), pipe.cnt[l].cpu().numpy()
+        compare_selection(setup["oshape"], inputs.to_u16(frows), setup["kc_ref"][l], 1, T - 1, gs, gc,
+                          [(b, m, 0) for b in range(B) for m in range(H)])
+        same = np.array_equal(gs, s)
+        assert same, f"layer {l}: selection differs within the tie window; pick another seed"
+        compare_attention(pipe.o[l].float().cpu().numpy(), setup["ref_out"][l], f"layer {l}")
+
+
+@pytest.mark.parametrize("overlap", [True, False])
+def test_pipeline_matches_oracle_chain(setup, overlap):
+    say(f"pipeline overlap={overlap}")
+    pipe = DecodePipeline(**setup["pipe_args"])
+    for _ in range(2):  # a second step reuses the staging slots and events
+        pipe.step(overlap=overlap)
+    check(setup, pipe)
+
+
+class _DelayedGather(DecodePipeline):
+    """Holds the side stream back (bounded spin) before every gather."""
+
+    def _gather(self, layer, stream):
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(2_000_000)
+        super()._gather(layer, stream)
+
+
+class _NoWait(_DelayedGather):
+    """A broken copy: the compute stream never waits for the gathers."""
+
+    def step(self, overlap=True):
+        saved = torch.cuda.Stream.wait_event
+        comp = torch.cuda.current_stream()
+
+        def skip_compute_waits(stream, event):
+            if stream == comp:
+                return None
+            return saved(stream, event)
+
+        torch.cuda.Stream.wait_event = skip_compute_waits
+        try:
+            return super().step(overlap=True)
+        finally:
+            torch.cuda.Stream.wait_event = saved
+
+
+def test_pipeline_event_ordering_with_delayed_side_stream(setup):
+    say("pipeline race check")
+    pipe = _DelayedGather(**setup["pipe_args"])
+    for sk, sv in pipe.stage:
+        sk.fill_(float("nan"))
+        sv.fill_(float("nan"))
+    torch.cuda.synchronize()
+    pipe.step()
+    check(setup, pipe)
+
+
+def test_dropped_wait_is_detected(setup):
+    say("pipeline dropped-wait check")
+    pipe = _NoWait(**setup["pipe_args"])
+    for sk, sv in pipe.stage:
+        sk.fill_(float("nan"))
+        sv.fill_(float("nan"))
+    torch.cuda.synchronize()
+    pipe.step()
+    torch.cuda.synchronize()
+    bad = 0
+    for l in range(1, L):
+        o = pipe.o[l].float().cpu().numpy()
+        if not np.all(np.isfinite(o)) or np.abs(o - setup["ref_out"][l]).max() > 2e-2:
+            bad += 1
+    assert bad > 0, "a pipeline without the gather wait went unnoticed"
