@@ -356,12 +356,12 @@ def main():
                      "traffic": None, "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att},
     }
     if not args.no_prefill:
-        del layer.case
+        layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
             f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
     if not args.no_pipeline:
-        del layer.case
+        layer.case = None
         out["pipeline"] = pipeline_leg(dev, 3)
         log(f"[bench] pipeline {out['pipeline']['ms_per_step_overlap']:.1f} ms/step overlapped, "
             f"{out['pipeline']['ms_per_step_serial']:.1f} serial")
