@@ -102,6 +102,22 @@ class DecodeLayer:
         }
 
 
+def counted_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs
+    (profiles/traffic_counters.json, calibrated on a plain 1 GiB copy), or None when the kernel's
+    sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        entry = json.load(fh)["kernels"].get(kernel)
+    if entry is None:
+        return None
+    digest = hashlib.sha256(b"".join(open(os.path.join(ROOT, f), "rb").read() for f in entry["sources"])).hexdigest()
+    return entry["traffic_bytes"] if digest == entry["sources_sha256"] else None
+
+
 def time_events(fn, iters, stream):
     """Average ms of fn() over iters launches, HIP events on `stream` around each launch."""
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(iters)]
@@ -351,9 +367,10 @@ def main():
         "frac_hbm_peak": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_bytes": step_bytes,
         "parts_us": {"compress_new": ms_cmp * 1e3, "select": ms_sel * 1e3, "attend": ms_att * 1e3},
-        "roofline": {"bound": "hbm", "kernel": "sparse_attn (decode, split-K + combine)",
+        "roofline": {"bound": "hbm", "kernel": "sparse_attn_kernel<4, 8> (decode, one workgroup per row)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att},
+                     "traffic": counted_traffic("sparse_attn_kernel<4, 8>"),
+                     "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att},
     }
     if not args.no_prefill:
         layer.case = None

@@ -78,6 +78,43 @@ __device__ __forceinline__ float row16_sum(float x) {
   return x;
 }
 
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xf, 0xf, false);
+}
+
+// Reductions over aligned groups of 8 lanes (every lane of the group receives the result):
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], then row_half_mirror (lane i <-> 7-i of the group).
+__device__ __forceinline__ float group8_sum(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x141>(x);
+  return x;
+}
+__device__ __forceinline__ int group8_sum(int x) {
+  x += dpp_i<0xB1>(x);
+  x += dpp_i<0x4E>(x);
+  x += dpp_i<0x141>(x);
+  return x;
+}
+
+// Exclusive prefix sum within aligned 8-lane groups; sub = lane index inside the group.
+__device__ __forceinline__ int group8_excl_scan(int x, int sub) {
+  int incl = x;
+  int y = __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xf, 0xf, true);  // row_shr:1
+  if (sub >= 1) incl += y;
+  y = __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xf, 0xf, true);      // row_shr:2
+  if (sub >= 2) incl += y;
+  y = __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xf, 0xf, true);      // row_shr:4
+  if (sub >= 4) incl += y;
+  return incl - x;
+}
+
+// Inverse of score_key.
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
 __device__ __forceinline__ int wave_incl_scan(int x) {
   const int lane = threadIdx.x & (kWave - 1);
 #pragma unroll

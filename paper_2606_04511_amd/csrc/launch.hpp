@@ -77,6 +77,8 @@ hipError_t launch_compress(const uint16_t* k, uint16_t* kc, int32_t rows, int64_
 // True when the call takes the row-wise path, which keeps its scores in workspace scratch.
 bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+// Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
+hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
 
 // Split count and blocks per split the attention launcher uses for `rows` query rows.
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);

@@ -11,10 +11,9 @@
 //    the candidate scores of each row to a float32 scratch row; a second kernel runs one
 //    wavefront per row that finds the exact k-th key by an 8-bit-digit radix select over a
 //    wave-private LDS histogram and emits the chosen indices in ascending order with ballots.
-//  * fused tile (multi-row prefill with <= 512 candidates per 64-row tile): one workgroup scores
-//    a 64-row tile against all its candidates with bf16 MFMA (v_mfma_f32_16x16x32_bf16), keeps
-//    the float32 score tile in LDS, and runs the same wavefront radix select per row; scores
-//    never reach HBM.
+//  * fused decode (one row per (batch, group), <= 16384 candidates): one workgroup per row keeps
+//    the row's scores in LDS and runs a block-wide radix select there.
+//  * fused tile (multi-row prefill with <= 512 candidates per 64-row tile): select_prefill.hip.
 #include "device_util.hpp"
 #include "launch.hpp"
 
@@ -154,65 +153,6 @@ __global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t
   const float* sc = a.ws + row * a.ws_stride;
   wave_topk_emit([&](int i) { return score_key(sc[i]); }, g.n_cand, g.n_take, g.cand_lo, hist[wave],
                  out + g.init_hi);
-}
-
-// ---- fused multi-row tile path -------------------------------------------------------------
-
-constexpr int kTileLd = kSelTileMaxCand + 4;  // LDS row pitch (floats): conflict-free MFMA stores
-
-// grid.x = (batch*group) * n_tiles + tile; 256 threads.  Rows r0 .. r0+63 of one (b, group).
-__global__ __launch_bounds__(256) void tile_select_kernel(SelectArgs a, int n_tiles) {
-  __shared__ __align__(16) float sc[kSelTileRows * kTileLd];
-  __shared__ __align__(16) uint32_t hist[4][256];
-  const int tile = (int)(blockIdx.x % n_tiles);
-  const int64_t bm = blockIdx.x / n_tiles;
-  const int r0 = tile * kSelTileRows;
-  const int nrows = min(kSelTileRows, a.n_q - r0);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const RowGeom gl = row_geom(a.q_pos0 + r0 + nrows - 1, a.n_init, a.n_local, a.k_total);
-  const int C = gl.n_cand;  // the tile's candidates [n_init, n_init + C); every row uses a prefix
-  if (gl.n_take < gl.n_cand) {
-    // S[row][cand] = F[row] . K~[cand]: A = F rows (M), B = K~ rows (N), K = head dim.
-    bf16x8 fa[4][4];
-    const int lr = lane & 15, kq = 8 * (lane >> 4);
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      const int rr = mt * 16 + lr;
-      const uint16_t* fp = a.f + ((bm * a.n_q + r0 + rr) * kHeadDim + kq);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        fa[mt][ks] = as_bf16x8(rr < nrows ? ld16(fp + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
-    }
-    const int n_nt = (C + 15) >> 4;
-    const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim + kq;
-    for (int nt = wave; nt < n_nt; nt += 4) {
-      const int cand = nt * 16 + lr;
-      bf16x8 kb[4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        kb[ks] = as_bf16x8(cand < C ? ld16(kcb + (int64_t)cand * kHeadDim + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) acc = mfma16x16x32(fa[mt][ks], kb[ks], acc);
-        float* dst = sc + (mt * 16 + 4 * (lane >> 4)) * kTileLd + nt * 16 + lr;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) dst[i * kTileLd] = acc[i];
-      }
-    }
-  }
-  __syncthreads();
-  for (int rr = wave; rr < nrows; rr += 4) {
-    const int64_t row = bm * a.n_q + r0 + rr;
-    const RowGeom g = row_geom(a.q_pos0 + r0 + rr, a.n_init, a.n_local, a.k_total);
-    int16_t* out = a.sel + row * a.k_total;
-    emit_forced(out, g, a.k_total, lane);
-    if (lane == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
-    const float* srow = sc + rr * kTileLd;
-    wave_topk_emit([&](int i) { return score_key(srow[i]); }, g.n_cand, g.n_take, g.cand_lo, hist[wave],
-                   out + g.init_hi);
-  }
 }
 
 // ---- fused decode path ---------------------------------------------------------------------
@@ -377,12 +317,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(decode_select_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
     return hipGetLastError();
   }
-  if (path == kPathTile) {
-    const int n_tiles = (a.n_q + kSelTileRows - 1) / kSelTileRows;
-    const int64_t grid = (int64_t)a.batch * a.n_kv_heads * n_tiles;
-    hipLaunchKernelGGL(tile_select_kernel, dim3((unsigned)grid), dim3(256), 0, stream, a, n_tiles);
-    return hipGetLastError();
-  }
+  if (path == kPathTile) return launch_prefill_select(a, stream);
   const RowGeom gl = row_geom(a.q_pos0 + a.n_q - 1, a.n_init, a.n_local, a.k_total);
   if (gl.n_cand > 0) {
     const int n_chunks = (gl.n_cand + 255) / 256;

@@ -372,3 +372,27 @@ def test_full_prefill_t32k_samples(dev):
                 got = out[0, m * G + h, r].float().cpu().numpy()
                 worst = max(worst, compare_attention(got, ref, f"prefill {(m, h, r)}"))
     say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
+
+
+# ----------------------------------------------------------------------------- exact ties
+
+@pytest.mark.parametrize("T,n_q,k_total", [(8192, 1, 16), (8192, 1024, 16), (32768, 2048, 64), (65536, 3, 64),
+                                           (40000, 1, 200)])
+def test_select_exact_ties_take_lowest_index(dev, T, n_q, k_total):
+    """F and K~ hold small integers, so every score is an exact integer in fp32 and in fp64 and
+    many candidates tie; the GPU must break ties by the lower block index exactly as the oracle."""
+    say(f"exact ties T{T} n_q{n_q} k{k_total}")
+    B, H = 1, 2
+    nb = T // 64
+    t_cap = -(-T // 64) * 64
+    s, o = shapes(B, H, 4, k_total, t_cap, nb)
+    g = torch.Generator().manual_seed(T + n_q)
+    f = torch.randint(-1, 2, (B, H, n_q, 128), generator=g).to(torch.bfloat16)
+    kc = torch.randint(-1, 2, (B, H, nb, 128), generator=g).to(torch.bfloat16)
+    m3 = nb // 3
+    kc[:, :, 0:3 * m3:3] = kc[:, :, 1:3 * m3:3]  # duplicated K~ rows: exact score ties
+    q_pos0 = T - n_q
+    sel, cnt = gpu_select(s, f.to(dev), n_q, q_pos0, kc.to(dev), dev)
+    ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(sel.cpu().numpy(), ref_sel)
