@@ -98,6 +98,36 @@ __device__ __forceinline__ int group8_sum(int x) {
   return x;
 }
 
+__device__ __forceinline__ int row16_sum(int x) {
+  x += dpp_i<0x128>(x);  // row_ror:8
+  x += dpp_i<0x124>(x);  // row_ror:4
+  x += dpp_i<0x122>(x);  // row_ror:2
+  x += dpp_i<0x121>(x);  // row_ror:1
+  return x;
+}
+
+__device__ __forceinline__ uint32_t row16_max(uint32_t x) {
+  x = max(x, (uint32_t)dpp_i<0x128>((int)x));  // row_ror:8
+  x = max(x, (uint32_t)dpp_i<0x124>((int)x));  // row_ror:4
+  x = max(x, (uint32_t)dpp_i<0x122>((int)x));  // row_ror:2
+  x = max(x, (uint32_t)dpp_i<0x121>((int)x));  // row_ror:1
+  return x;
+}
+
+// Exclusive prefix sum within each 16-lane row; sub = lane index inside the row.
+__device__ __forceinline__ int row16_excl_scan(int x, int sub) {
+  int incl = x;
+  int y = __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xf, 0xf, true);  // row_shr:1
+  if (sub >= 1) incl += y;
+  y = __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xf, 0xf, true);      // row_shr:2
+  if (sub >= 2) incl += y;
+  y = __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xf, 0xf, true);      // row_shr:4
+  if (sub >= 4) incl += y;
+  y = __builtin_amdgcn_update_dpp(0, incl, 0x118, 0xf, 0xf, true);      // row_shr:8
+  if (sub >= 8) incl += y;
+  return incl - x;
+}
+
 // Exclusive prefix sum within aligned 8-lane groups; sub = lane index inside the group.
 __device__ __forceinline__ int group8_excl_scan(int x, int sub) {
   int incl = x;
