@@ -23,8 +23,8 @@
  *
  * Readings of the paper that these definitions take (k counts the forced blocks, the local
  * window is block-granular and contains the query's own block, score ties go to the lower
- * index, out-of-range selected entries are skipped) are listed with their reasons in the
- * design notes of the repository.
+ * index, out-of-range selected entries are skipped, a block listed twice is attended once)
+ * are listed with their reasons in the design notes of the repository.
  */
 #include <math.h>
 #include <stdint.h>
@@ -261,6 +261,11 @@ int sparda_ref_attend_row(const ref_shape* s, const uint16_t* q, int32_t n_q, in
   for (int64_t sidx = 0; sidx < n_sel; ++sidx) {
     const int64_t j = srow[sidx];
     if (j < 0 || j > blk) continue;
+    /* The attended tokens are a union over the set's blocks (Eq. 1, Eq. 5): a block listed
+     * twice contributes its tokens once, through its first entry. */
+    int seen = 0;
+    for (int64_t e = 0; e < sidx; ++e) seen |= (srow[e] == j);
+    if (seen) continue;
     for (int64_t i = 0; i < L; ++i) {
       const int64_t t = j * L + i;
       if (t > p) break;

@@ -1,7 +1,8 @@
 """Plant plausible mistakes in copies of the oracle (on the CPU) and check that the pins catch
 each one: a flipped sort direction, a dropped softmax scale, an off-by-one local window, a
 causal mask that lets the next token in, an init block left out of the candidates' exclusion,
-a swapped operand index in the score, and a rounding mode change in the compressed keys."""
+a swapped operand index in the score, a rounding mode change in the compressed keys, and a block
+listed twice in a set being attended twice."""
 import math
 import os
 
@@ -23,6 +24,7 @@ MUTANTS = {
     "score_wrong_operand": ("sparda_ref_bf16_to_f64(kc[j * D + d])", "sparda_ref_bf16_to_f64(kc[d * D + j % D])"),
     "compress_truncates": ("double q = nearbyint(ldexp(m, 8));", "double q = floor(ldexp(m, 8));"),
     "compress_wrong_divisor": ("sum / (double)L", "sum / (double)(L - 1)"),
+    "duplicate_attended_twice": ("if (seen) continue;", "(void)seen;"),
 }
 
 
@@ -48,6 +50,12 @@ def _pins_pass(o) -> bool:
         scale = 1.0 / math.sqrt(128)
         got = o.sparse_attn(s, q, n_q, T - n_q, k, v, 0, bsel, bcnt, scale)
         want = brute.attend_dense_masked(q, k, v, bsel, bcnt, T - n_q, G, scale)
+        if not np.allclose(got, want, rtol=0, atol=1e-12):
+            return False
+        # a block listed twice is attended once (the attended tokens are a union of blocks)
+        sd = np.ascontiguousarray(np.concatenate([bsel[..., 2:], bsel], axis=-1))
+        s3 = o.Shape(**{**s.__dict__, "k_total": sd.shape[-1]})
+        got = o.sparse_attn(s3, q, n_q, T - n_q, k, v, 0, sd, np.full(bcnt.shape, sd.shape[-1], np.int16), scale)
         if not np.allclose(got, want, rtol=0, atol=1e-12):
             return False
         # the hand-worked tie (test_select_worked_example_with_tie): block 1 beats block 3

@@ -364,3 +364,23 @@ def test_out_of_range_entries_are_skipped(oracle_lib):
     cnt2 = (cnt + 2).astype(np.int16)
     got = oracle_lib.sparse_attn(s2, q, 1, T - 1, k, v, 0, np.ascontiguousarray(sel2), cnt2, scale)
     np.testing.assert_allclose(got, base, rtol=0, atol=0)
+
+
+def test_duplicate_entries_are_attended_once(oracle_lib):
+    # The attended tokens are the union of the set's blocks (Eq. 1, Eq. 5): listing a block again
+    # adds nothing.  Checked against the dense masked attention, whose mask is a set by
+    # construction, on decode and multi-row cases.
+    for T, n_q, k_total in ((4096, 1, 16), (640, 70, 6)):
+        s, q, k, v, sel, cnt = _attn_case(oracle_lib, T, n_q, k_total)
+        scale = 1.0 / math.sqrt(128)
+        extra = 3
+        sel2 = np.concatenate([sel, sel[..., :extra]], axis=-1)  # re-list the first three entries
+        rng = np.random.default_rng(7)
+        sel2 = np.take_along_axis(sel2, rng.permuted(np.tile(np.arange(sel2.shape[-1]), sel2.shape[:-1] + (1,)),
+                                                      axis=-1), axis=-1)
+        # rows whose count is below k_total hold -1 pads among the first entries; keep cnt = all slots
+        s2 = oracle_lib.Shape(**{**s.__dict__, "k_total": s.k_total + extra})
+        cnt2 = np.full(cnt.shape, s2.k_total, np.int16)
+        got = oracle_lib.sparse_attn(s2, q, n_q, T - n_q, k, v, 0, np.ascontiguousarray(sel2), cnt2, scale)
+        want = brute.attend_dense_masked(q, k[:, :, :T], v[:, :, :T], sel, cnt, T - n_q, 4, scale)
+        np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
