@@ -123,8 +123,8 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
  *                sparda_gather_blocks: slot s holds the L tokens of block sel[s].  Decode only
  *                (n_q == 1).
  *   sel, cnt in: as produced by sparda_forecast_select (any order of the first cnt entries is
- *                accepted; entries outside [0, blk(p)] are skipped; duplicates are the caller's
- *                error and are attended twice).
+ *                accepted; entries outside [0, blk(p)] are skipped; the attended tokens are the
+ *                union of the listed blocks, so a block listed twice is attended once).
  *   sm_scale   : logit scale, normally 1/sqrt(D).
  *   o      out : bf16 [B][Hq][n_q][D] device.  A row that attends no token gets zeros.
  *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_SPARSE_ATTN).

@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsparda.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["compress.hip", "select.hip", "select_prefill.hip", "attention.hip", "gather.hip", "sparda_abi.cpp"]
+SOURCES = ["compress.hip", "select.hip", "select_prefill.hip", "attention.hip", "attention_prefill.hip", "gather.hip", "sparda_abi.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
           "-Wall", "-Wno-unused-function"]

@@ -68,9 +68,18 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
 
   const int16_t* srow = a.sel + row * a.k_total;
+  // The attended tokens are a union of blocks: an entry whose block an earlier entry of the row
+  // already lists is skipped.  Lane e holds entry e (e < 64) for that test.
+  const int entry = lane < n ? (int)srow[lane] : -1;
   for (int s = s_begin + wave; s < s_end; s += NW) {
     const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
     if (j < 0 || j > blk) continue;
+    bool dup = __ballot(lane < s && entry == j) != 0ull;
+    for (int e0 = 64; e0 < s; e0 += 64) {
+      const int e = e0 + lane;
+      dup |= __ballot(e < s && (int)srow[e] == j) != 0ull;
+    }
+    if (dup) continue;
     int64_t base;
     if (a.kv_mode == 0)
       base = (bm * a.t_cap + (int64_t)j * kBlock) * kHeadDim;
@@ -278,6 +287,7 @@ static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream) {
+  if (a.kv_mode == 0 && attn_uses_tiles(a.group_size, a.n_q, a.q_pos0)) return launch_prefill_attn(a, stream);
   switch (a.group_size) {
     case 1: return launch_g<1>(a, stream);
     case 2: return launch_g<2>(a, stream);

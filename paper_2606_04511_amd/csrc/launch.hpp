@@ -83,6 +83,10 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
 // Split count and blocks per split the attention launcher uses for `rows` query rows.
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
+// True when a multi-row call takes the tiled kernel (attention_prefill.hip), which needs no
+// workspace: at least 16 rows, 16 % G == 0, and the tile's row bitmaps fit in LDS.
+bool attn_uses_tiles(int32_t group_size, int32_t n_q, int64_t q_pos0);
+hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream);
 
 hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const int16_t* sel, const int16_t* cnt,
                          uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int64_t t_cap, int32_t k_total,

@@ -88,7 +88,12 @@ size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* st
   return (size_t)rows * (size_t)*stride * sizeof(float);
 }
 
-size_t attn_ws(const sparda_shape* s, int32_t n_q, int32_t* n_splits, int32_t* bps) {
+size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps) {
+  if (sparda::attn_uses_tiles(s->group_size, n_q, q_pos0)) {  // tiled multi-row kernel: no partials
+    *n_splits = 1;
+    *bps = s->k_total;
+    return 0;
+  }
   const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
   sparda::attn_plan(rows, s->k_total, n_splits, bps);
   if (*n_splits <= 1) return 0;
@@ -128,7 +133,7 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
     *bytes = select_ws(shape, n_q, q_pos0, &stride);
   } else if (op == SPARDA_OP_SPARSE_ATTN) {
     int32_t ns, bps;
-    *bytes = attn_ws(shape, n_q, &ns, &bps);
+    *bytes = attn_ws(shape, n_q, q_pos0, &ns, &bps);
   } else {
     return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
   }
@@ -201,7 +206,7 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
   if (kv_mode == 1 && n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "staging mode needs n_q == 1");
   if (!std::isfinite(sm_scale)) return fail(SPARDA_ERR_INVALID_ARG, "sm_scale is not finite");
   int32_t ns = 1, bps = shape->k_total;
-  const size_t need = attn_ws(shape, n_q, &ns, &bps);
+  const size_t need = attn_ws(shape, n_q, q_pos0, &ns, &bps);
   if (need > 0) {
     if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
     if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);

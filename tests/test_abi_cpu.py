@@ -148,6 +148,16 @@ def test_workspace_sizes(lib):
     assert sp.sparda_workspace_size(s3, sp.SPARDA_OP_FORECAST_SELECT, 32768, 0) == 0
     assert sp.sparda_workspace_size(s3, sp.SPARDA_OP_SPARSE_ATTN, 32768, 0) == 0
     assert rc_of(sp.sparda_workspace_size, s3, 9, 1, 0) == sp.SPARDA_ERR_INVALID_ARG
+    # a 20-row chunk of one group: the tiled kernel (G divides 16) needs no partials; with G = 3
+    # the per-row kernel splits each row's block list over workgroups
+    s4 = shape(batch=1, n_kv_heads=1, group_size=4, k_total=16, t_cap=8192, nc_cap=128)
+    assert sp.sparda_workspace_size(s4, sp.SPARDA_OP_SPARSE_ATTN, 20, 4000) == 0
+    s5 = shape(batch=1, n_kv_heads=1, group_size=3, k_total=16, t_cap=8192, nc_cap=128)
+    assert sp.sparda_workspace_size(s5, sp.SPARDA_OP_SPARSE_ATTN, 20, 4000) > 0
+    # a chunk past 4096 blocks (256K tokens) is beyond the tiles' LDS bitmaps: the per-row kernel
+    s6 = shape(batch=1, n_kv_heads=1, group_size=4, k_total=16, t_cap=524288, nc_cap=8192)
+    assert sp.sparda_workspace_size(s6, sp.SPARDA_OP_SPARSE_ATTN, 20, 524000) > 0
+    assert sp.sparda_workspace_size(s6, sp.SPARDA_OP_SPARSE_ATTN, 20, 200000) == 0
 
 
 def test_status_strings(lib):

@@ -185,6 +185,17 @@ ATTN = [
     (1, 1, 4, 77, 1, 3),
     (1, 2, 4, 640, 640, 4),
     (1, 1, 4, 8192, 300, 16),
+    # multi-row calls on the tiled kernel (256/G rows per tile): every G it takes, ragged last
+    # tiles, chunks that start off a block boundary, the 16-row threshold, one block only
+    (1, 2, 1, 4096, 600, 16),
+    (1, 2, 2, 2048, 2048, 8),
+    (2, 1, 8, 3000, 130, 16),
+    (1, 1, 16, 1024, 40, 6),
+    (1, 1, 4, 64, 64, 3),
+    (1, 2, 4, 5000, 16, 16),
+    (1, 2, 4, 20000, 700, 64),
+    # multi-row, G does not divide 16: the per-row kernel
+    (1, 2, 3, 2048, 100, 8),
 ]
 
 
@@ -244,6 +255,29 @@ def test_attention_order_invariance_and_skips(dev):
     c = gpu_attend(s2, *args, torch.from_numpy(np.ascontiguousarray(sel2)).to(dev),
                    torch.from_numpy(cnt + 2).to(dev), dev)
     assert (a.float() - c.float()).abs().max().item() <= 2e-2
+
+
+@pytest.mark.parametrize("n_q", [1, 200])
+def test_attention_duplicate_entries_attended_once(dev, n_q):
+    say(f"attention duplicates n_q={n_q}")
+    B, H, G, T, k_total = 1, 2, 4, 6144, 12
+    extra = 4
+    w, case = make(B, H, G, T, n_q, k_total, 5250 + n_q)
+    s, o = shapes(B, H, G, k_total, T, T // 64)
+    q_pos0 = T - n_q
+    k16, v16 = inputs.to_u16(case["k"]), inputs.to_u16(case["v"])
+    kc_ref = oracle.compress_keys(o, k16, T, 0, T // 64)
+    sel, cnt = oracle.forecast_select(o, inputs.to_u16(case["f"]), n_q, q_pos0, kc_ref)
+    rng = np.random.default_rng(11)
+    dup = np.concatenate([sel, sel[..., :extra]], axis=-1)
+    dup = np.ascontiguousarray(np.take_along_axis(dup, rng.permuted(
+        np.tile(np.arange(dup.shape[-1]), dup.shape[:-1] + (1,)), axis=-1), axis=-1))
+    s2, o2 = shapes(B, H, G, k_total + extra, T, T // 64)
+    cnt2 = np.full(cnt.shape, k_total + extra, np.int16)
+    out = gpu_attend(s2, case["q"].to(dev), n_q, q_pos0, case["k"].to(dev), case["v"].to(dev), 0,
+                     torch.from_numpy(dup).to(dev), torch.from_numpy(cnt2).to(dev), dev)
+    ref = oracle.sparse_attn(o, inputs.to_u16(case["q"]), n_q, q_pos0, k16, v16, 0, sel, cnt, SCALE)
+    compare_attention(out.float().cpu().numpy(), ref, "duplicates")
 
 
 # ----------------------------------------------------------------------------- gather
