@@ -11,8 +11,8 @@
 //      ascending order, is the tile's block list.
 //   2. The tile walks its block list.  Block j's 16 KiB of K and 16 KiB of V are read from HBM
 //      once per tile (16-byte loads, 1 KiB contiguous per wavefront instruction) into a
-//      double-buffered LDS stage, one block ahead of the math.  V is stored transposed (head dim
-//      x token) so that it can be the A operand of the P V product.
+//      double-buffered LDS stage, two blocks ahead of the math.  V is stored transposed (head dim
+//      x token, XOR-swizzled against bank conflicts) so that it can be the A operand of P V.
 //   3. A wavefront skips block j for an N-tile none of whose rows lists j.  Otherwise:
 //        S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (M = 16 tokens, N = 16 query-heads, K = 32
 //        dims); query-heads whose row does not list j, and tokens after the row's position, are
@@ -35,7 +35,6 @@ namespace {
 constexpr int kPaThreads = 512;
 constexpr int kPaQh = 256;                 // query-head rows per tile
 constexpr int kPaKLd = kHeadDim + 8;       // bf16 per staged K row (272 B: conflict-free 16-byte reads)
-constexpr int kPaVLd = kBlock + 4;         // bf16 per staged V^T row (136 B: conflict-free 8-byte reads)
 constexpr int kPaMaxWords = 8192;          // row-bitmap words (32 KiB)
 constexpr int kPaMaxBlocks = 4096;         // causal blocks a tile may span
 constexpr float kLog2eP = 1.4426950408889634f;
@@ -54,7 +53,7 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
   constexpr int RN = 16 / G;     // rows per N-tile
   static_assert(16 % G == 0, "an N-tile holds whole rows");
   __shared__ __align__(16) uint16_t kst[2][kBlock * kPaKLd];
-  __shared__ __align__(16) uint16_t vst[2][kHeadDim * kPaVLd];
+  __shared__ __align__(16) uint16_t vst[2][kHeadDim * kBlock];
   __shared__ uint32_t rbm[kPaMaxWords];
   __shared__ uint32_t ubm[kPaMaxBlocks / 32];
   __shared__ int16_t ulist[kPaMaxBlocks];
@@ -123,38 +122,67 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
     for (int ks = 0; ks < 4; ++ks)
       qf[nt][ks] = as_bf16x8(ok_c[nt] ? ld16(qrow + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
   }
+  // z = zscale (q . k): a negative scale is folded into the query's sign bits (exact in bf16), so
+  // that the block maximum of z is always zscale times the maximum of q . k.
+  float zscale = a.sm_scale * kLog2eP;
+  if (zscale < 0.f) {
+    zscale = -zscale;
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        uint4 w = __builtin_bit_cast(uint4, qf[nt][ks]);
+        w.x ^= 0x80008000u;
+        w.y ^= 0x80008000u;
+        w.z ^= 0x80008000u;
+        w.w ^= 0x80008000u;
+        qf[nt][ks] = as_bf16x8(w);
+      }
+  }
+  // Wait for the query fragments here, once: the loop's own loads are then the only ones in
+  // flight, and the loop's waits can leave the prefetched blocks outstanding.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
   f32x4 acc[2][8];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
     for (int md = 0; md < 8; ++md) acc[nt][md] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const float zscale = a.sm_scale * kLog2eP;
 
-  // ---- staging roles: threads 0..255 copy K (token u/16, 16-byte part u%16 for u = lt + 256 x),
-  // threads 256..511 copy V (tokens tau + 16 x, dims 8 part .. 8 part + 7; tau = lt/16).
+  // ---- staging roles.  Threads 0..255 copy K: token u/16, 16-byte part u%16 for u = lt + 256 x.
+  // Threads 256..511 copy V: tokens tau + 16 x (x = 0..3), dims 8 part .. 8 part + 7, with lane l
+  // of V wavefront w taking tau = 4 w + l % 4, part = l / 4 (each wavefront load instruction still
+  // covers 4 whole token rows, 1 KiB contiguous).  Two register sets keep the loads of the next
+  // two blocks in flight.
+  //
+  // Staged V^T: row d (head dim) holds the block's 64 tokens in slots 4 tau + x <-> token
+  // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  The swizzle makes both
+  // the transposing 8-byte writes (16 lanes: 4 tokens x 4 parts) and the 8-byte operand reads
+  // (16 lanes: 16 consecutive dims) touch 32 distinct banks.
   const int lt = tid & 255;
-  const bool load_k = tid < 256;
-  const uint16_t* kv = (load_k ? a.k : a.v) + bm * a.t_cap * kHeadDim;
-  uint4 pre[4];
-  auto issue = [&](int j) {
+  const bool load_k = __builtin_amdgcn_readfirstlane(tid) < 256;  // whole wavefronts
+  const int v_tau = 4 * (lt >> 6) + (lt & 3), v_part = (lt & 63) >> 2;
+  const int ld_off = load_k ? lt * 8 : v_tau * kHeadDim + 8 * v_part;
+  const uint16_t* kv = (load_k ? a.k : a.v) + bm * a.t_cap * kHeadDim + ld_off;
+  auto vsw = [](int d) { return (2 * (d & 15)) ^ (8 * ((d >> 4) & 1)); };
+  uint4 pre[2][4];
+  auto issue = [&](uint4 (&r)[4], int j) {
     const uint16_t* src = kv + (int64_t)j * kBlock * kHeadDim;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) pre[x] = ld16(src + (lt + 256 * x) * 8);
+    for (int x = 0; x < 4; ++x) r[x] = ld16(src + x * 16 * kHeadDim);
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](const uint4 (&r)[4], int buf) {
     if (load_k) {
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
         const int u = lt + 256 * x;
-        *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (u & 15) * 8]) = pre[x];
+        *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (u & 15) * 8]) = r[x];
       }
     } else {
-      const int tau = lt >> 4, part = lt & 15;
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&pre[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&pre[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&pre[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&pre[3]);
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&r[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&r[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&r[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&r[3]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int wi = i >> 1;
@@ -166,24 +194,27 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
           d.x = (w0[wi] & 0xffffu) | (w1[wi] << 16);
           d.y = (w2[wi] & 0xffffu) | (w3[wi] << 16);
         }
-        *reinterpret_cast<uint2*>(&vst[buf][(8 * part + i) * kPaVLd + 4 * tau]) = d;
+        const int dim = 8 * v_part + i;
+        *reinterpret_cast<uint2*>(&vst[buf][2 * (dim * 32 + ((2 * v_tau) ^ vsw(dim)))]) = d;
       }
     }
   };
 
-  __syncthreads();  // union list and bitmaps complete
-  const int nu = n_union;
-  if (nu > 0) {
-    issue(ulist[0]);
-    stage(0);
-  }
-  __syncthreads();
+  // Online softmax with a lazily raised reference: m_ref[nt] moves only when a block's maximum
+  // exceeds it by more than kHeadroom (log2 units), so most blocks need no rescaling of acc.
+  // P = 2^(z - m_ref) then stays below 2^kHeadroom, well inside bf16 and fp32; the final
+  // normalisation by l, accumulated against the same reference, makes the result exact.
+  constexpr float kHeadroom = 8.f;
+  const int blk0 = (int)(p0 / kBlock);  // blocks >= blk0 may hold tokens after some row's position
 
-  for (int it = 0; it < nu; ++it) {
-    const int buf = it & 1;
-    const int j = ulist[it];
-    if (it + 1 < nu) issue(ulist[it + 1]);
+  // the four lanes of a column (q = 0..3) exchange through lane ^ 16 and lane ^ 32
+  const int addr32 = (lane ^ 32) << 2;
+  auto xor16 = [](float x) {  // ds_swizzle, bit-mask mode: and 0x1f, xor 0x10 (within 32 lanes)
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));
+  };
+  auto xor32 = [addr32](float x) { return __int_as_float(__builtin_amdgcn_ds_bpermute(addr32, __float_as_int(x))); };
 
+  auto compute = [&](int j, int buf) {
     bool act[2], nt_act[2];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
@@ -191,87 +222,130 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
       act[nt] = ok_c[nt] && ((rbm[rli * W + (j >> 5)] >> (j & 31)) & 1u);
       nt_act[nt] = __ballot(act[nt]) != 0ull;
     }
-    if (nt_act[0] || nt_act[1]) {
-      // S^T[token 16 mt + 4 q + i][column c] for both N-tiles
-      f32x4 st[2][4];
-      const uint16_t* kb = &kst[buf][0];
+    if (!(nt_act[0] || nt_act[1])) return;
+    // S^T[token 16 mt + 4 q + i][column c] for both N-tiles
+    f32x4 st[2][4];
+    const uint16_t* kb = &kst[buf][0];
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        bf16x8 kf[4];
+    for (int mt = 0; mt < 4; ++mt) {
+      bf16x8 kf[4];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(kb + (16 * mt + c) * kPaKLd + 32 * ks + 8 * q));
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          st[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (nt_act[nt]) {
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) st[nt][mt] = mfma16x16x32(kf[ks], qf[nt][ks], st[nt][mt]);
-          }
-        }
-      }
-      bf16x8 pb[2][2];
+      for (int ks = 0; ks < 4; ++ks)
+        kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(kb + (16 * mt + c) * kPaKLd + 32 * ks + 8 * q));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        if (!nt_act[nt]) continue;
-        // last visible token of block j for this column (-1: the row does not list j)
-        const int64_t lim64 = pc[nt] - (int64_t)j * kBlock;
-        const int lim = act[nt] ? (int)(lim64 < kBlock ? lim64 : kBlock - 1) : -1;
-        float z[4][4];
-        float bmax = -INFINITY;
+        st[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (nt_act[nt]) {
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int tok = 16 * mt + 4 * q + i;
-            z[mt][i] = tok <= lim ? st[nt][mt][i] * zscale : -INFINITY;
-            bmax = fmaxf(bmax, z[mt][i]);
-          }
-        bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
-        bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-        const float m_new = fmaxf(m_run[nt], bmax);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run[nt] - m_use);
-        float psum = 0.f;
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            z[mt][i] = exp2f(z[mt][i] - m_use);
-            psum += z[mt][i];
-          }
-        l_run[nt] = l_run[nt] * alpha + psum;
-        m_run[nt] = m_new;
-#pragma unroll
-        for (int md = 0; md < 8; ++md) acc[nt][md] *= alpha;
-        // B operand of k-step s2: slot jj holds token 16 (jj % 4) + 4 q + 2 s2 + jj / 4
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          uint4 w;
-          w.x = pack_bf16(z[0][2 * s2], z[1][2 * s2]);
-          w.y = pack_bf16(z[2][2 * s2], z[3][2 * s2]);
-          w.z = pack_bf16(z[0][2 * s2 + 1], z[1][2 * s2 + 1]);
-          w.w = pack_bf16(z[2][2 * s2 + 1], z[3][2 * s2 + 1]);
-          pb[nt][s2] = as_bf16x8(w);
-        }
-      }
-      // O^T[dim 16 md + 4 q + i][column c] += V^T P^T
-      const uint16_t* vb = &vst[buf][0];
-#pragma unroll
-      for (int md = 0; md < 8; ++md) {
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const uint16_t* src = vb + (16 * md + c) * kPaVLd + 16 * q + 8 * s2;
-          const uint2 v0 = *reinterpret_cast<const uint2*>(src);
-          const uint2 v1 = *reinterpret_cast<const uint2*>(src + 4);
-          const bf16x8 va = as_bf16x8(make_uint4(v0.x, v0.y, v1.x, v1.y));
-#pragma unroll
-          for (int nt = 0; nt < 2; ++nt)
-            if (nt_act[nt]) acc[nt][md] = mfma16x16x32(va, pb[nt][s2], acc[nt][md]);
+          for (int ks = 0; ks < 4; ++ks) st[nt][mt] = mfma16x16x32(kf[ks], qf[nt][ks], st[nt][mt]);
         }
       }
     }
-    if (it + 1 < nu) stage(buf ^ 1);
+    const bool diag = j >= blk0;  // uniform over the workgroup
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      if (!nt_act[nt]) continue;
+      // maximum over the visible scores: every token, except (in the tile's diagonal blocks)
+      // those after the row's position
+      int lim = kBlock - 1;
+      float e = -INFINITY;
+      if (diag) {
+        const int64_t lim64 = pc[nt] - (int64_t)j * kBlock;
+        lim = (int)(lim64 < kBlock ? lim64 : kBlock - 1);
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (16 * mt + 4 * q + i <= lim) e = fmaxf(e, st[nt][mt][i]);
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+          e = fmaxf(e, fmaxf(fmaxf(st[nt][mt][0], st[nt][mt][1]), fmaxf(st[nt][mt][2], st[nt][mt][3])));
+      }
+      float bmax = act[nt] ? e * zscale : -INFINITY;
+      bmax = fmaxf(bmax, xor16(bmax));
+      bmax = fmaxf(bmax, xor32(bmax));
+      const bool raise = bmax > m_run[nt] + kHeadroom;  // also true on a column's first block
+      if (__ballot(raise) != 0ull) {
+        const float m_new = raise ? bmax : m_run[nt];
+        const float alpha = raise ? __builtin_amdgcn_exp2f(m_run[nt] - m_new) : 1.f;
+        m_run[nt] = m_new;
+        l_run[nt] *= alpha;
+#pragma unroll
+        for (int md = 0; md < 8; ++md) acc[nt][md] *= alpha;
+      }
+      // z - m_ref as one FMA; an inactive column gets -inf, hence P = 0
+      const float off = act[nt] ? -m_run[nt] : -INFINITY;
+      float pz[4][4];
+      float psum = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pz[mt][i] = __builtin_amdgcn_exp2f(fmaf(st[nt][mt][i], zscale, off));
+      if (diag) {
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (16 * mt + 4 * q + i > lim) pz[mt][i] = 0.f;
+      }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) psum += pz[mt][i];
+      l_run[nt] += psum;
+      // B operand of k-step s2: slot jj holds token 16 (jj % 4) + 4 q + 2 s2 + jj / 4
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        uint4 w;
+        w.x = pack_bf16(pz[0][2 * s2], pz[1][2 * s2]);
+        w.y = pack_bf16(pz[2][2 * s2], pz[3][2 * s2]);
+        w.z = pack_bf16(pz[0][2 * s2 + 1], pz[1][2 * s2 + 1]);
+        w.w = pack_bf16(pz[2][2 * s2 + 1], pz[3][2 * s2 + 1]);
+        pb[nt][s2] = as_bf16x8(w);
+      }
+    }
+    // O^T[dim 16 md + 4 q + i][column c] += V^T P^T
+    const uint16_t* vb = &vst[buf][0];
+#pragma unroll
+    for (int md = 0; md < 8; ++md) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int dim = 16 * md + c, sw = vsw(dim), dw = 8 * q + 4 * s2;
+        const uint2 v0 = *reinterpret_cast<const uint2*>(vb + 2 * (dim * 32 + (dw ^ sw)));
+        const uint2 v1 = *reinterpret_cast<const uint2*>(vb + 2 * (dim * 32 + ((dw + 2) ^ sw)));
+        const bf16x8 va = as_bf16x8(make_uint4(v0.x, v0.y, v1.x, v1.y));
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          if (nt_act[nt]) acc[nt][md] = mfma16x16x32(va, pb[nt][s2], acc[nt][md]);
+      }
+    }
+  };
+
+  __syncthreads();  // union list and bitmaps complete
+  const int nu = n_union;
+  // Loads and stages run unconditionally (past the list's end they repeat its last block and
+  // fill a buffer nobody reads), so that every path through the loop has the same loads in
+  // flight and the compiler's waits only ever cover the block being staged.
+  auto blk_at = [&](int i) { return (int)ulist[min(i, max(nu - 1, 0))]; };
+  if (nu > 0) {
+    issue(pre[0], blk_at(0));
+    issue(pre[1], blk_at(1));
+    stage(pre[0], 0);
+  }
+  __syncthreads();
+
+  // Iteration it computes block it from buffer it % 2, requests block it + 2 into the register
+  // set block it used, and stages block it + 1 (requested one iteration earlier).
+  for (int it = 0; it < nu; it += 2) {
+    issue(pre[0], blk_at(it + 2));
+    compute(blk_at(it), 0);
+    stage(pre[1], 1);
+    __syncthreads();
+    issue(pre[1], blk_at(it + 3));
+    if (it + 1 < nu) compute(blk_at(it + 1), 1);
+    stage(pre[0], 0);
     __syncthreads();
   }
 
