@@ -34,7 +34,7 @@ namespace {
 
 constexpr int kPaThreads = 512;
 constexpr int kPaQh = 256;                 // query-head rows per tile
-constexpr int kPaKLd = kHeadDim + 8;       // bf16 per staged K row (272 B: conflict-free 16-byte reads)
+constexpr int kPaKLd = kHeadDim + 16;      // bf16 per staged K row (288 B: conflict-free 16-byte reads)
 constexpr int kPaMaxWords = 8192;          // row-bitmap words (32 KiB)
 constexpr int kPaMaxBlocks = 4096;         // causal blocks a tile may span
 constexpr float kLog2eP = 1.4426950408889634f;
@@ -156,15 +156,16 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
   // two blocks in flight.
   //
   // Staged V^T: row d (head dim) holds the block's 64 tokens in slots 4 tau + x <-> token
-  // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  The swizzle makes both
-  // the transposing 8-byte writes (16 lanes: 4 tokens x 4 parts) and the 8-byte operand reads
-  // (16 lanes: 16 consecutive dims) touch 32 distinct banks.
+  // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  LDS serves each half
+  // wavefront separately from 128 four-byte banks (4 rows of this buffer); the swizzle spreads the
+  // 8-byte operand reads of a half wavefront (16 consecutive dims x 2 k-chunks) over 64 distinct
+  // banks, leaving the transposing writes (once per block) two-way conflicted.
   const int lt = tid & 255;
   const bool load_k = __builtin_amdgcn_readfirstlane(tid) < 256;  // whole wavefronts
   const int v_tau = 4 * (lt >> 6) + (lt & 3), v_part = (lt & 63) >> 2;
   const int ld_off = load_k ? lt * 8 : v_tau * kHeadDim + 8 * v_part;
   const uint16_t* kv = (load_k ? a.k : a.v) + bm * a.t_cap * kHeadDim + ld_off;
-  auto vsw = [](int d) { return (2 * (d & 15)) ^ (8 * ((d >> 4) & 1)); };
+  auto vsw = [](int d) { return 2 * ((d >> 2) & 15); };
   uint4 pre[2][4];
   auto issue = [&](uint4 (&r)[4], int j) {
     const uint16_t* src = kv + (int64_t)j * kBlock * kHeadDim;
