@@ -4,9 +4,9 @@
 //
 // One 512-thread workgroup per 32-row tile of one (batch, group); the tile's rows share the
 // candidate range [n_init, n_init + C), C <= 512, and each row takes its own top-k.  A tile's
-// LDS (74 KB) lets two workgroups share a CU, so one tile's loads and MFMA overlap another
+// LDS (72 KB) lets two workgroups share a CU, so one tile's loads and MFMA overlap another
 // tile's selection.
-//   1. F rows of the tile are staged in LDS (272-byte row pitch: conflict-free 16-byte reads).
+//   1. F rows of the tile are staged in LDS (288-byte row pitch: conflict-free 16-byte reads).
 //   2. S = F K~^T on v_mfma_f32_16x16x32_bf16 (A = F, 2 M-tiles; B = K~ rows straight from L2,
 //      one 16-candidate N-tile per wavefront at a time).  The fp32 score tile stays in LDS; each
 //      row is split into 16 ranges of V candidates (V a multiple of 4) laid out with a stride R
@@ -43,12 +43,15 @@ constexpr int kPreWaves = kPreThreads / 64;
 constexpr int kPreRows = 32;                    // rows per tile
 constexpr int kPreMt = kPreRows / 16;           // MFMA M-tiles per tile
 constexpr int kPreVals = kSelTileMaxCand / 16;  // key slots per lane (16 lanes per row)
-constexpr int kPreLd = 16 * (kPreVals + 4) + 4; // floats per LDS score row (16 strided ranges + pad)
-constexpr int kPreFLd = kHeadDim + 8;           // bf16 per staged F row (272 B)
+constexpr int kPreLd = 16 * (kPreVals + 4);     // floats per LDS score row (16 strided ranges)
+constexpr int kPreFLd = kHeadDim + 16;          // bf16 per staged F row (288 B)
 constexpr int kPreFFloats = kPreRows * kPreFLd / 2;  // staged F tile, in floats
-// MFMA stores: a wavefront stores rows R, R+4, R+8, R+12; 4 * 580 = 16 (mod 64) banks apart.
+// LDS serves each half wavefront on its own from 128 four-byte banks.  A row pitch of 64 (mod 128)
+// banks puts the two rows a half wavefront touches (key loads: rows rr, rr + 1; MFMA stores: rows
+// 4 i + q, q = 0, 1, after the F row permutation below) on disjoint banks, and a range stride R
+// with R / 4 odd spreads the 16 ranges of a row over distinct 16-byte bank groups.
 static_assert(kSelTileRows % kPreRows == 0, "tiles stay inside the rows a 64-row block spans");
-static_assert(kPreLd == 580 && kPreLd % 16 == 4, "bank analysis assumes a row pitch of 580 floats");
+static_assert(kPreLd == 576 && kPreLd % 128 == 64, "bank analysis assumes a row pitch of 576 floats");
 
 // Forced blocks, local window and padding of one row, by its 16 lanes.
 __device__ __forceinline__ void emit_forced16(int16_t* out, const RowGeom& g, int k_total, int sub) {
@@ -113,12 +116,15 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
     static_assert(kPreThreads / 16 == kPreRows, "one thread per 16 bytes of the F tile");
     static_assert(kNtPerWave * kPreWaves * 16 == kSelTileMaxCand, "N-tiles cover every candidate slot");
     __syncthreads();
+    // A-operand row lr of an M-tile is tile row 4 (lr % 4) + lr / 4, so that accumulator element
+    // i of lane (n, q) holds the score of tile row 4 i + q.
     bf16x8 fa[kPreMt][4];
+    const int fr = 4 * (lr & 3) + (lr >> 2);
 #pragma unroll
     for (int mt = 0; mt < kPreMt; ++mt)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
-        fa[mt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(fst + (mt * 16 + lr) * kPreFLd + 32 * ks + kq));
+        fa[mt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(fst + (mt * 16 + fr) * kPreFLd + 32 * ks + kq));
     __syncthreads();  // the staged F tile is overwritten by scores below
     // V N-tiles cover all 16 V key slots; candidates past C get -inf (no key counts them).
 #pragma unroll
@@ -134,9 +140,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) acc = mfma16x16x32(fa[mt][ks], as_bf16x8(kw[i][ks]), acc);
           }
-          float* dst = sc + (mt * 16 + 4 * (lane >> 4)) * kPreLd + col;
+          float* dst = sc + (mt * 16 + (lane >> 4)) * kPreLd + col;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) dst[q * kPreLd] = cand < C ? acc[q] : -INFINITY;
+          for (int q = 0; q < 4; ++q) dst[4 * q * kPreLd] = cand < C ? acc[q] : -INFINITY;
         }
       }
     }
@@ -161,35 +167,37 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
   const bool search = row_ok && n > 0 && n < Cr;
   const int cbase = sub * V;  // this lane's candidates [cbase, cbase + V), at sc[row][sub R ..]
 
-  // Keys of all 16 V slots.  Rows of an unaligned chunk may have fewer candidates than the tile
-  // (Cr < C): their extra slots are forced to the key of -inf.
+  // Scores of all 16 V slots, compared as floats against thresholds that are kept as keys: the
+  // float key_value(t) admits exactly the scores whose key is >= t (-0 and +0 share a key, and no
+  // score has the key of -0).  Rows of an unaligned chunk may have fewer candidates than the tile
+  // (Cr < C): their extra slots hold -inf, which no threshold admits.
   constexpr uint32_t kKeyNegInf = 0x007fffffu;  // key of -inf: below every threshold used
-  uint32_t key[kPreVals];
+  float val[kPreVals];
   const float* srow = sc + rr * kPreLd + sub * R;
 #pragma unroll
-  for (int j = 0; j < kPreVals; ++j) key[j] = kKeyNegInf;
+  for (int j = 0; j < kPreVals; ++j) val[j] = -INFINITY;
   const bool short_row = search && Cr < C;
 #pragma unroll
   for (int jb = 0; jb < kPreVals; jb += 4) {
     if (jb < V) {
       const float4 v = *reinterpret_cast<const float4*>(srow + jb);
-      key[jb] = key_of_value(v.x);
-      key[jb + 1] = key_of_value(v.y);
-      key[jb + 2] = key_of_value(v.z);
-      key[jb + 3] = key_of_value(v.w);
+      val[jb] = v.x;
+      val[jb + 1] = v.y;
+      val[jb + 2] = v.z;
+      val[jb + 3] = v.w;
     }
   }
   if (__ballot(short_row) != 0ull) {
 #pragma unroll
     for (int j = 0; j < kPreVals; ++j)
-      if (short_row && cbase + j >= Cr) key[j] = kKeyNegInf;
+      if (short_row && cbase + j >= Cr) val[j] = -INFINITY;
   }
   // Mean and variance from the first four slots of each lane (a 64-score sample of the row).
   float s1 = 0.f, s2 = 0.f, ns = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const bool ok = j < V && cbase + j < Cr;
-    const float v = ok ? key_value(key[j]) : 0.f;
+    const float v = ok ? val[j] : 0.f;
     s1 += v;
     s2 = fmaf(v, v, s2);
     ns += ok ? 1.f : 0.f;
@@ -218,15 +226,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
   {  // first pass: three thresholds around the guess
     const float va = t_mid - step, vb = t_mid, vc = t_mid + step;
     const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
+    // compare against the exact values of the keys (non-finite guesses never enter the bracket)
+    const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
     int ca = 0, cb = 0, cc = 0;
 #pragma unroll
     for (int jb = 0; jb < kPreVals; jb += 4) {
       if (jb < V) {
 #pragma unroll
         for (int j = jb; j < jb + 4; ++j) {
-          ca += key[j] >= ta ? 1 : 0;
-          cb += key[j] >= tb ? 1 : 0;
-          cc += key[j] >= tc ? 1 : 0;
+          ca += val[j] >= fa ? 1 : 0;
+          cb += val[j] >= fb ? 1 : 0;
+          cc += val[j] >= fc ? 1 : 0;
         }
       }
     }
@@ -275,12 +285,13 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
         if (t <= lo) { t = lo + 1u; have_v = false; }
         if (t >= hi) { t = hi - 1u; have_v = false; }
       }
+      const float ft = key_value(t);
       int c = 0;
 #pragma unroll
       for (int jb = 0; jb < kPreVals; jb += 4) {
         if (jb < V) {
 #pragma unroll
-          for (int j = jb; j < jb + 4; ++j) c += key[j] >= t ? 1 : 0;
+          for (int j = jb; j < jb + 4; ++j) c += val[j] >= ft ? 1 : 0;
         }
       }
       c = row16_sum(c);
@@ -293,15 +304,16 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
     } else if (__ballot(want_max) != 0ull) {
       // n - 1 keys lie at or above hi: the n-th largest is the largest key below hi.  No key
       // lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
-      uint32_t m = 0u;
+      const float fhi = key_value(hi);
+      float mv = -INFINITY;
 #pragma unroll
       for (int jb = 0; jb < kPreVals; jb += 4) {
         if (jb < V) {
 #pragma unroll
-          for (int j = jb; j < jb + 4; ++j) m = max(m, key[j] < hi ? key[j] : 0u);
+          for (int j = jb; j < jb + 4; ++j) mv = val[j] < fhi ? fmaxf(mv, val[j]) : mv;
         }
       }
-      m = row16_max(m);
+      uint32_t m = row16_max(mv == -INFINITY ? 0u : key_of_value(mv));
       if (want_max) {
         lo = m;
         hi = m + 1u;
@@ -318,13 +330,14 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
   // the lowest-index n - c_hi of the keys == lo.
   const bool tie_mode = search && c_lo != n;
   const uint32_t thr = tie_mode ? lo + 1u : lo;
+  const float fthr = key_value(thr), flo = key_value(lo);
   uint32_t ch = 0u, tm = 0u;
 #pragma unroll
   for (int jb = 0; jb < kPreVals; jb += 4) {
     if (jb < V) {
 #pragma unroll
       for (int j = jb; j < jb + 4; ++j)
-        if (key[j] >= thr) ch |= 1u << j;
+        if (val[j] >= fthr) ch |= 1u << j;
     }
   }
   if (__ballot(tie_mode) != 0ull) {
@@ -333,7 +346,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs 
       if (jb < V) {
 #pragma unroll
         for (int j = jb; j < jb + 4; ++j)
-          if (key[j] == lo) tm |= 1u << j;
+          if (val[j] == flo) tm |= 1u << j;
       }
     }
   }
