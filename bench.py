@@ -296,6 +296,54 @@ def pipeline_leg(dev, steps):
     }
 
 
+def peaks_leg(dev):
+    """Hardware limits measured in the same run (the spec figures are 8 TB/s and 2.5 PFLOP/s):
+    streaming HBM reads of 4 GiB, reads of 32768 randomly placed 16 KiB blocks (537 MB, the shape
+    of a decode layer's attended KV blocks), back-to-back bf16 MFMA, and a pinned 1 GiB host to
+    device copy."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_04511_amd", "libsparda_peaks.so"))
+    lib.peaks_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.peaks_block_read.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                     ctypes.c_void_p]
+    lib.peaks_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    nbytes = 4 << 30
+    buf = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    g = torch.Generator(device="cpu").manual_seed(4242)
+    n_blocks = 32768
+    idx = torch.randint(0, nbytes // 16384, (n_blocks,), generator=g, dtype=torch.int64).to(torch.int32).to(dev)
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"peaks library call failed ({rc})")
+
+    def warm_time(fn, iters):
+        fn()
+        torch.cuda.synchronize()
+        return time_events(fn, iters, stream)
+
+    ms_stream = warm_time(lambda: check(lib.peaks_stream_read(buf.data_ptr(), nbytes, 8192, sink.data_ptr(), sh)), 5)
+    ms_block = warm_time(lambda: check(lib.peaks_block_read(buf.data_ptr(), idx.data_ptr(), n_blocks, 2048,
+                                                            sink.data_ptr(), sh)), 10)
+    grid, iters = 2048, 4000
+    ms_mfma = warm_time(lambda: check(lib.peaks_mfma_bf16(grid, iters, sink.data_ptr(), sh)), 3)
+    del buf
+    host = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    ms_h2d = warm_time(lambda: dst.copy_(host, non_blocking=True), 5)
+    del host, dst
+    torch.cuda.synchronize()
+    return {
+        "hbm_stream_read_GBps": nbytes / (ms_stream * 1e-3) / 1e9,
+        "hbm_block_read_GBps": n_blocks * 16384 / (ms_block * 1e-3) / 1e9,
+        "mfma_bf16_TFLOPs": grid * 4 * 8 * iters * 16384 / (ms_mfma * 1e-3) / 1e12,
+        "h2d_pinned_GBps": (1 << 30) / (ms_h2d * 1e-3) / 1e9,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -325,6 +373,9 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         log("[bench] calibration copy of 1 GiB done (x3)")
+
+    peaks = peaks_leg(dev)
+    log("[bench] measured peaks: " + ", ".join(f"{k} {v:.1f}" for k, v in peaks.items()))
 
     w = inputs.WORKLOADS["decode_b32_t128k"]
     layer = DecodeLayer(w, dev)
@@ -370,11 +421,16 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "sparse_attn_kernel<4, 8> (decode, one workgroup per row)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": counted_traffic("sparse_attn_kernel<4, 8>"),
-                     "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att},
+                     "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att,
+                     "measured_peak": peaks["hbm_block_read_GBps"],
+                     "frac_measured_peak": achieved / peaks["hbm_block_read_GBps"]},
+        "peaks": peaks,
+        "frac_measured_read_peak": step_bytes / (ms_step * 1e-3) / 1e9 / peaks["hbm_block_read_GBps"],
     }
     if not args.no_prefill:
         layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
+        out["prefill"]["select_frac_measured_mfma_peak"] = out["prefill"]["select_tflops"] / peaks["mfma_bf16_TFLOPs"]
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
             f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
     if not args.no_pipeline:

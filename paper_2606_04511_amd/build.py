@@ -1,7 +1,8 @@
 """Build libsparda.so for gfx950 with hipcc (in-tree, no torch extension machinery).
 
 Each translation unit is compiled to an object under ``_build/`` and linked into
-``paper_2606_04511_amd/libsparda.so``.  Every HIP object is built with packed-FP32 instruction
+``paper_2606_04511_amd/libsparda.so``; the benchmark's microbenchmarks go into
+``paper_2606_04511_amd/libsparda_peaks.so``.  Every HIP object is built with packed-FP32 instruction
 selection turned off (``-Xclang -target-feature -Xclang -packed-fp32-ops``).
 """
 from __future__ import annotations
@@ -17,6 +18,10 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsparda.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+# Microbenchmarks of the hardware limits, for the benchmark only (not part of the C ABI).
+PEAKS_SOURCE = "peaks.hip"
+PEAKS_LIB = os.path.join(PKG, "libsparda_peaks.so")
 
 SOURCES = ["compress.hip", "select.hip", "select_prefill.hip", "attention.hip", "attention_prefill.hip", "gather.hip", "sparda_abi.cpp"]
 
@@ -37,16 +42,21 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build() -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _link(objs, lib: str) -> None:
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build() -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=min(len(SOURCES) + 1, os.cpu_count() or 4)) as ex:
+        objs = list(ex.map(_compile, SOURCES + [PEAKS_SOURCE]))
+    _link(objs[:-1], LIB)
+    _link(objs[-1:], PEAKS_LIB)
     return LIB
 
 
