@@ -2,63 +2,86 @@
 // selection (paper Sec. 4.1, Eq. 4, with the attended-set union of Eq. 1; per query row as in
 // Alg. 1).
 //
-// One 512-thread workgroup per 32-row tile of one (batch, group); the tile's rows share the
-// candidate range [n_init, n_init + C), C <= 512, and each row takes its own top-k.  A tile's
-// LDS (72 KB) lets two workgroups share a CU, so one tile's loads and MFMA overlap another
-// tile's selection.
-//   1. F rows of the tile are staged in LDS (288-byte row pitch: conflict-free 16-byte reads).
-//   2. S = F K~^T on v_mfma_f32_16x16x32_bf16 (A = F, 2 M-tiles; B = K~ rows straight from L2,
-//      one 16-candidate N-tile per wavefront at a time).  The fp32 score tile stays in LDS; each
-//      row is split into 16 ranges of V candidates (V a multiple of 4) laid out with a stride R
-//      whose quarter is odd, so that the 16 lanes that later read their ranges with 16-byte loads
-//      hit disjoint bank groups.  The staged F tile occupies the tail of the score buffer until
-//      every wavefront holds its F fragments.
-//   3. Selection, 16 lanes (one DPP row) per query row, 4 rows per wavefront, 8 wavefronts:
-//      lane s holds the order-preserving keys of candidates [s V, s V + V) in registers
-//      (candidates past the tile's last one hold -inf).  The exact n-th largest key is found by
-//      passes over the keys, each a compare + add per key:
-//        - a first pass counts at three thresholds around a normal-model guess (mean and
-//          variance of a 64-score sample of the row), which usually brackets the n-th key;
+// Work unit: a slice of 16 consecutive query rows of one (batch, group), owned by one wavefront.
+// A slice's rows share their candidate range [n_init, n_init + C) up to the rows of a block
+// boundary inside the slice (those have one candidate less, masked below); each row takes its own
+// top-k.
+//
+// Workgroups are persistent units of 8 wavefronts, one unit per (batch, group) and slice range.
+// A host-side plan splits every group's slices into ranges of equal estimated cost; the unit
+// stages the K~ rows of its largest candidate range in LDS once (272-byte row pitch), then its
+// wavefronts take slices from an LDS counter, most candidates first.
+//
+// Per slice:
+//   1. S^T = K~ F^T on v_mfma_f32_16x16x32_bf16: B = the slice's 16 F rows (straight from HBM,
+//      prefetched one slice ahead), A = 16 staged K~ rows per M-tile.  A row m of M-tile t is
+//      candidate (m / 4) Q + 4 t + m % 4 with Q = 4 ceil(C / 16), so accumulator element i of lane
+//      (n, j) -- query row n, lane group j -- holds candidate j Q + 4 t + i: each row's scores sit
+//      in the accumulators of its 4 lanes, every lane holding one contiguous quarter [j Q, j Q + Q)
+//      of the candidates.  Scores never leave the registers.
+//   2. Exact n-th largest score per row by count passes over the 4 Q registers, each a compare +
+//      add per score and a 4-lane sum (two permlane swaps):
+//        - a first pass counts at three thresholds around a normal-model guess (mean and variance
+//          of a 64-score sample of the row), which usually brackets the n-th score;
 //        - regula-falsi steps on the bracketing counts (a key-space bisection step every sixth
-//          pass guarantees termination) until exactly n keys are >= the threshold;
-//        - a row that misses exactly one key above its bracket is finished by one max pass
-//          (the largest key below the bracket is the n-th); max passes wait until no row of the
-//          wavefront still counts, so the two pass kinds never run in the same iteration.
-//      If the bracket closes on a key value shared by more than the open slots, the ties are
-//      taken by lower block index.
-//   4. Emission: each lane turns its chosen keys into a 32-bit mask in candidate order; one
-//      16-lane prefix sum over the mask popcounts places every chosen index.
-// Workgroups are ordered so that consecutive ones (which the dispatcher spreads over the 8 XCDs)
-// take different groups: with 8 groups each XCD's L2 holds a single group's K~.  Tiles with the
-// most candidates go first.
+//          pass guarantees termination) until exactly n scores are >= the threshold;
+//        - a row that misses exactly one score above its bracket is finished by one max pass.
+//      Thresholds are kept as order-preserving keys and compared as the floats they encode.  If
+//      the bracket closes on a value shared by more scores than open slots, the ties are taken
+//      by lower block index.
+//   3. Emission: a lane's chosen scores become a bit mask in candidate order; a 4-lane exclusive
+//      prefix of the popcounts gives each lane its first output slot, and the lane writes its
+//      indices in ascending order.
 #include <math.h>
+
+#include <algorithm>
 
 #include "device_util.hpp"
 #include "launch.hpp"
 
 namespace sparda {
 
-constexpr int kPreThreads = 512;
-constexpr int kPreWaves = kPreThreads / 64;
-constexpr int kPreRows = 32;                    // rows per tile
-constexpr int kPreMt = kPreRows / 16;           // MFMA M-tiles per tile
-constexpr int kPreVals = kSelTileMaxCand / 16;  // key slots per lane (16 lanes per row)
-constexpr int kPreLd = 16 * (kPreVals + 4);     // floats per LDS score row (16 strided ranges)
-constexpr int kPreFLd = kHeadDim + 16;          // bf16 per staged F row (288 B)
-constexpr int kPreFFloats = kPreRows * kPreFLd / 2;  // staged F tile, in floats
-// LDS serves each half wavefront on its own from 128 four-byte banks.  A row pitch of 64 (mod 128)
-// banks puts the two rows a half wavefront touches (key loads: rows rr, rr + 1; MFMA stores: rows
-// 4 i + q, q = 0, 1, after the F row permutation below) on disjoint banks, and a range stride R
-// with R / 4 odd spreads the 16 ranges of a row over distinct 16-byte bank groups.
-static_assert(kSelTileRows % kPreRows == 0, "tiles stay inside the rows a 64-row block spans");
-static_assert(kPreLd == 576 && kPreLd % 128 == 64, "bank analysis assumes a row pitch of 576 floats");
+constexpr int kPsThreads = 512;
+constexpr int kPsWaves = kPsThreads / 64;
+constexpr int kPsRows = 16;                     // rows per slice (one MFMA N-tile)
+constexpr int kPsMaxMt = kSelTileMaxCand / 16;  // M-tiles per slice: up to 128 key slots per lane
+constexpr int kPsPitch = kHeadDim + 8;          // bf16 per staged K~ row (272 B)
+constexpr int kPsStageRows = kSelTileMaxCand + 4;  // staged K~ rows, the A read-ahead's 4 included
+constexpr int kPsStageK = 64;                   // sets of at most this many entries go through LDS
+constexpr int kPsMaxUnits = 256;                // units per (batch, group)
 
-// Forced blocks, local window and padding of one row, by its 16 lanes.
-__device__ __forceinline__ void emit_forced16(int16_t* out, const RowGeom& g, int k_total, int sub) {
-  for (int i = sub; i < g.init_hi; i += 16) out[i] = (int16_t)i;
-  const int n_loc = g.blk - g.local_lo + 1;
-  for (int i = sub; i < n_loc; i += 16) out[g.init_hi + g.n_take + i] = (int16_t)(g.local_lo + i);
-  for (int i = g.n_forced + g.n_take + sub; i < k_total; i += 16) out[i] = (int16_t)-1;
+struct PrefillPlan {
+  int32_t n_slices;                   // slices per (batch, group)
+  int32_t units;                      // units per (batch, group)
+  uint16_t bound[kPsMaxUnits + 1];    // unit u owns slices [bound[u], bound[u + 1])
+};
+
+// Sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one query row); every one of them receives it.
+__device__ __forceinline__ int row4_sum(int x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const int y = (int)p[0] + (int)p[1];
+  const auto q = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+  return (int)q[0] + (int)q[1];
+}
+__device__ __forceinline__ float row4_sum(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+__device__ __forceinline__ uint32_t row4_max(uint32_t x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const uint32_t y = max((uint32_t)p[0], (uint32_t)p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+  return max((uint32_t)q[0], (uint32_t)q[1]);
+}
+// Exclusive prefix over the row's lanes in lane-group order j = 0..3; *total gets the row sum.
+__device__ __forceinline__ int row4_excl_scan(int x, int j, int* total) {
+  const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);  // p[0]: even group, p[1]: odd
+  const int pair = (int)p[0] + (int)p[1];
+  const auto q = __builtin_amdgcn_permlane32_swap(pair, pair, false, false);  // q[0]: groups 0-1, q[1]: 2-3
+  *total = (int)q[0] + (int)q[1];
+  return ((j & 1) ? (int)p[0] : 0) + ((j & 2) ? (int)q[0] : 0);
 }
 
 // z with P(Z > z) = p for a standard normal Z (rational approximation of Abramowitz and Stegun
@@ -79,311 +102,404 @@ __device__ __forceinline__ uint32_t key_of_value(float v) {
   return u ^ (uint32_t)(((int32_t)u >> 31) | (int32_t)0x80000000);
 }
 
-__global__ __launch_bounds__(kPreThreads) void prefill_select_kernel(SelectArgs a, int n_tiles, int n_groups) {
-  __shared__ __align__(16) float sc[kPreRows * kPreLd];
-  uint16_t* fst = reinterpret_cast<uint16_t*>(sc + kPreRows * kPreLd - kPreFFloats);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t bm = blockIdx.x % n_groups;
-  const int tile = n_tiles - 1 - (int)(blockIdx.x / n_groups);
-  const int r0 = tile * kPreRows;
-  const int nrows = min(kPreRows, a.n_q - r0);
-  const RowGeom gl = row_geom(a.q_pos0 + r0 + nrows - 1, a.n_init, a.n_local, a.k_total);
-  const int C = gl.n_cand;                  // the tile's candidate count (its last row has the most)
-  const bool need = gl.n_take < gl.n_cand;  // if the last row takes every candidate, all rows do
-  const int V = max((C + 63) >> 6, 1) * 4;     // candidates per lane range, a multiple of 4
-  const int R = V + ((V & 4) ? 8 : 4);          // range stride: R / 4 is odd
-
-  if (need) {
-    // This wavefront's N-tiles are nt = wave + 8 i (V <= 32 N-tiles, so i < 4).  Their K~ rows
-    // are requested first so that the L2 latency overlaps the F staging and its barriers.
-    constexpr int kNtPerWave = kPreVals / kPreWaves;  // 4
-    const int lr = lane & 15, kq = 8 * (lane >> 4);
-    const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim + kq;
-    uint4 kw[kNtPerWave][4];
+// Runs f(score, slot) over the lane's first 4 * nmt key slots (slot = 4 t + i).
+template <class Fn>
+__device__ __forceinline__ void for_slots(const float (&acc)[kPsMaxMt][4], int nmt, Fn&& f) {
 #pragma unroll
-    for (int i = 0; i < kNtPerWave; ++i) {
-      const int cand = (wave + kPreWaves * i) * 16 + lr;
+  for (int t = 0; t < kPsMaxMt; ++t) {
+    if (t < nmt) {
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        kw[i][ks] = cand < C ? ld16(kcb + (int64_t)cand * kHeadDim + 32 * ks) : make_uint4(0u, 0u, 0u, 0u);
-    }
-    {  // stage the tile's F rows: thread -> (row tid/16, 16-byte part tid%16)
-      const int rr = tid >> 4, part = tid & 15;
-      uint4 w0 = make_uint4(0u, 0u, 0u, 0u);
-      if (rr < nrows) w0 = ld16(a.f + (bm * a.n_q + r0 + rr) * kHeadDim + part * 8);
-      *reinterpret_cast<uint4*>(fst + rr * kPreFLd + part * 8) = w0;
-    }
-    static_assert(kPreThreads / 16 == kPreRows, "one thread per 16 bytes of the F tile");
-    static_assert(kNtPerWave * kPreWaves * 16 == kSelTileMaxCand, "N-tiles cover every candidate slot");
-    __syncthreads();
-    // A-operand row lr of an M-tile is tile row 4 (lr % 4) + lr / 4, so that accumulator element
-    // i of lane (n, q) holds the score of tile row 4 i + q.
-    bf16x8 fa[kPreMt][4];
-    const int fr = 4 * (lr & 3) + (lr >> 2);
-#pragma unroll
-    for (int mt = 0; mt < kPreMt; ++mt)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        fa[mt][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(fst + (mt * 16 + fr) * kPreFLd + 32 * ks + kq));
-    __syncthreads();  // the staged F tile is overwritten by scores below
-    // V N-tiles cover all 16 V key slots; candidates past C get -inf (no key counts them).
-#pragma unroll
-    for (int i = 0; i < kNtPerWave; ++i) {
-      const int nt = wave + kPreWaves * i;
-      if (nt < V) {
-        const int cand = nt * 16 + lr;
-        const int col = (cand / V) * R + cand % V;
-#pragma unroll
-        for (int mt = 0; mt < kPreMt; ++mt) {
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-          if (nt * 16 < C) {
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) acc = mfma16x16x32(fa[mt][ks], as_bf16x8(kw[i][ks]), acc);
-          }
-          float* dst = sc + (mt * 16 + (lane >> 4)) * kPreLd + col;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) dst[4 * q * kPreLd] = cand < C ? acc[q] : -INFINITY;
-        }
-      }
-    }
-  }
-  __syncthreads();
-
-  // ---- per-row selection: 16 lanes per row, 4 rows per wavefront.
-  const int sub = lane & 15;
-  const int rr = 4 * wave + (lane >> 4);
-  const bool row_ok = rr < nrows;
-  const int64_t row = bm * a.n_q + r0 + rr;
-  const RowGeom g = row_geom(a.q_pos0 + r0 + rr, a.n_init, a.n_local, a.k_total);
-  int16_t* out = a.sel + row * a.k_total;
-  if (row_ok) {
-    emit_forced16(out, g, a.k_total, sub);
-    if (sub == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
-    if (g.n_take >= g.n_cand)
-      for (int i = sub; i < g.n_cand; i += 16) out[g.init_hi + i] = (int16_t)(g.cand_lo + i);
-  }
-  if (!need) return;
-  const int n = g.n_take, Cr = g.n_cand;
-  const bool search = row_ok && n > 0 && n < Cr;
-  const int cbase = sub * V;  // this lane's candidates [cbase, cbase + V), at sc[row][sub R ..]
-
-  // Scores of all 16 V slots, compared as floats against thresholds that are kept as keys: the
-  // float key_value(t) admits exactly the scores whose key is >= t (-0 and +0 share a key, and no
-  // score has the key of -0).  Rows of an unaligned chunk may have fewer candidates than the tile
-  // (Cr < C): their extra slots hold -inf, which no threshold admits.
-  constexpr uint32_t kKeyNegInf = 0x007fffffu;  // key of -inf: below every threshold used
-  float val[kPreVals];
-  const float* srow = sc + rr * kPreLd + sub * R;
-#pragma unroll
-  for (int j = 0; j < kPreVals; ++j) val[j] = -INFINITY;
-  const bool short_row = search && Cr < C;
-#pragma unroll
-  for (int jb = 0; jb < kPreVals; jb += 4) {
-    if (jb < V) {
-      const float4 v = *reinterpret_cast<const float4*>(srow + jb);
-      val[jb] = v.x;
-      val[jb + 1] = v.y;
-      val[jb + 2] = v.z;
-      val[jb + 3] = v.w;
-    }
-  }
-  if (__ballot(short_row) != 0ull) {
-#pragma unroll
-    for (int j = 0; j < kPreVals; ++j)
-      if (short_row && cbase + j >= Cr) val[j] = -INFINITY;
-  }
-  // Mean and variance from the first four slots of each lane (a 64-score sample of the row).
-  float s1 = 0.f, s2 = 0.f, ns = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const bool ok = j < V && cbase + j < Cr;
-    const float v = ok ? val[j] : 0.f;
-    s1 += v;
-    s2 = fmaf(v, v, s2);
-    ns += ok ? 1.f : 0.f;
-  }
-  s1 = row16_sum(s1);
-  s2 = row16_sum(s2);
-  ns = fmaxf(row16_sum(ns), 1.f);
-  const float inv_s = __builtin_amdgcn_rcpf(ns);
-  const float mu = s1 * inv_s;
-  const float sigma = sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
-  const float inv = __builtin_amdgcn_rcpf((float)(Cr > 0 ? Cr : 1));
-  const float z0 = upper_normal_quantile(((float)n - 0.5f) * inv);
-  // Counts per unit of score near the guess (normal model) and the first pass's spacing: about
-  // 1.5 sqrt(n) + 2 counts, the typical binomial error of the model guess.
-  const float dens = fmaxf((float)Cr * 0.39894228f * __expf(-0.5f * z0 * z0) / sigma, 1e-30f);
-  const float step = (1.5f * sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
-  const float t_mid = mu + sigma * z0;
-
-  // Bracket [lo, hi) in key space: count(key >= lo) = c_lo >= n > c_hi = count(key >= hi).
-  // lo starts just above -inf (every real score counts), hi just above +inf (none does).
-  uint32_t lo = kKeyNegInf + 1u, hi = 0xff800001u;
-  int c_lo = Cr, c_hi = 0;
-  float vlo = 0.f, vhi = 0.f;
-  bool lo_b = false, hi_b = false;  // vlo / vhi hold the score value of lo / hi
-  bool done = !search;
-  {  // first pass: three thresholds around the guess
-    const float va = t_mid - step, vb = t_mid, vc = t_mid + step;
-    const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
-    // compare against the exact values of the keys (non-finite guesses never enter the bracket)
-    const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
-    int ca = 0, cb = 0, cc = 0;
-#pragma unroll
-    for (int jb = 0; jb < kPreVals; jb += 4) {
-      if (jb < V) {
-#pragma unroll
-        for (int j = jb; j < jb + 4; ++j) {
-          ca += val[j] >= fa ? 1 : 0;
-          cb += val[j] >= fb ? 1 : 0;
-          cc += val[j] >= fc ? 1 : 0;
-        }
-      }
-    }
-    ca = row16_sum(ca);
-    cb = row16_sum(cb);
-    cc = row16_sum(cc);
-    if (!done) {
-      const uint32_t tt[3] = {ta, tb, tc};
-      const int cs[3] = {ca, cb, cc};
-      const float vs[3] = {va, vb, vc};
-#pragma unroll
-      for (int i = 0; i < 3; ++i) {
-        if (tt[i] > lo && tt[i] < hi) {
-          if (cs[i] >= n) { lo = tt[i]; c_lo = cs[i]; vlo = vs[i]; lo_b = true; }
-          else { hi = tt[i]; c_hi = cs[i]; vhi = vs[i]; hi_b = true; }
-        }
-      }
-      done = (c_lo == n) || (hi - lo <= 1u);
-    }
-  }
-  float grow = 2.f * step;
-  for (int it = 0; it < 100; ++it) {
-    const bool want_max = !done && hi_b && (n - c_hi == 1);
-    const bool want_cnt = !done && !want_max;
-    if (__ballot(want_cnt) != 0ull) {
-      uint32_t t = lo + ((hi - lo) >> 1);  // key-space bisection unless a model step is taken
-      float tv = 0.f;
-      bool have_v = false;
-      if (want_cnt) {
-        if (lo_b && hi_b) {
-          if (it % 6 != 5) {
-            tv = vlo + (vhi - vlo) * (((float)(c_lo - n) + 0.5f) * __builtin_amdgcn_rcpf((float)(c_lo - c_hi)));
-            have_v = true;
-          }
-        } else if (it < 6) {  // one side still open: step outwards, doubling
-          tv = lo_b ? vlo + grow : vhi - grow;
-          grow *= 2.f;
-          have_v = true;
-        }
-        if (have_v) {
-          if (isfinite(tv))
-            t = key_of_value(tv);
-          else
-            have_v = false;
-        }
-        if (t <= lo) { t = lo + 1u; have_v = false; }
-        if (t >= hi) { t = hi - 1u; have_v = false; }
-      }
-      const float ft = key_value(t);
-      int c = 0;
-#pragma unroll
-      for (int jb = 0; jb < kPreVals; jb += 4) {
-        if (jb < V) {
-#pragma unroll
-          for (int j = jb; j < jb + 4; ++j) c += val[j] >= ft ? 1 : 0;
-        }
-      }
-      c = row16_sum(c);
-      if (want_cnt) {
-        const float vt = have_v ? tv : key_value(t);
-        if (c >= n) { lo = t; c_lo = c; vlo = vt; lo_b = true; }
-        else { hi = t; c_hi = c; vhi = vt; hi_b = true; }
-        done = (c_lo == n) || (hi - lo <= 1u);
-      }
-    } else if (__ballot(want_max) != 0ull) {
-      // n - 1 keys lie at or above hi: the n-th largest is the largest key below hi.  No key
-      // lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
-      const float fhi = key_value(hi);
-      float mv = -INFINITY;
-#pragma unroll
-      for (int jb = 0; jb < kPreVals; jb += 4) {
-        if (jb < V) {
-#pragma unroll
-          for (int j = jb; j < jb + 4; ++j) mv = val[j] < fhi ? fmaxf(mv, val[j]) : mv;
-        }
-      }
-      uint32_t m = row16_max(mv == -INFINITY ? 0u : key_of_value(mv));
-      if (want_max) {
-        lo = m;
-        hi = m + 1u;
-        c_lo = -1;  // unknown: the emission takes the n - c_hi lowest-index keys equal to lo
-        done = true;
-      }
-    } else {
-      break;
-    }
-  }
-
-  // ---- emission.  Normal case: the chosen keys are those >= lo (exactly n).  Tie case (the
-  // bracket closed on one key value shared by more than the remaining slots): keys > lo, plus
-  // the lowest-index n - c_hi of the keys == lo.
-  const bool tie_mode = search && c_lo != n;
-  const uint32_t thr = tie_mode ? lo + 1u : lo;
-  const float fthr = key_value(thr), flo = key_value(lo);
-  uint32_t ch = 0u, tm = 0u;
-#pragma unroll
-  for (int jb = 0; jb < kPreVals; jb += 4) {
-    if (jb < V) {
-#pragma unroll
-      for (int j = jb; j < jb + 4; ++j)
-        if (val[j] >= fthr) ch |= 1u << j;
-    }
-  }
-  if (__ballot(tie_mode) != 0ull) {
-#pragma unroll
-    for (int jb = 0; jb < kPreVals; jb += 4) {
-      if (jb < V) {
-#pragma unroll
-        for (int j = jb; j < jb + 4; ++j)
-          if (val[j] == flo) tm |= 1u << j;
-      }
-    }
-  }
-  if (!search) ch = 0u;
-  if (!tie_mode) tm = 0u;
-  {  // ties: the first n - c_hi in index order
-    const int tcnt = __popc(tm);
-    const int tb = row16_excl_scan(tcnt, sub);
-    if (tie_mode) {
-      int take = min(max(n - c_hi - tb, 0), tcnt);
-      while (take-- > 0) {
-        const uint32_t low = tm & (~tm + 1u);
-        ch |= low;
-        tm ^= low;
-      }
-    }
-  }
-  const int cb = row16_excl_scan(__popc(ch), sub);
-  if (search) {
-    int16_t* dst = out + g.init_hi + cb;
-    const int cand0 = g.cand_lo + cbase;
-    uint32_t m = ch;
-    int k = 0;
-    while (m) {
-      const int b = __builtin_ctz(m);
-      if (cb + k < n) dst[k] = (int16_t)(cand0 + b);  // never past the row's slots
-      ++k;
-      m &= m - 1u;
+      for (int i = 0; i < 4; ++i) f(acc[t][i], 4 * t + i);
     }
   }
 }
 
+// Number of key slots >= v, summed over the row's four lanes.
+__device__ __forceinline__ int count_ge(const float (&acc)[kPsMaxMt][4], int nmt, float v) {
+  int c0 = 0, c1 = 0;
+  for_slots(acc, nmt, [&](float x, int q) {
+    if (q & 1) c1 += x >= v ? 1 : 0;
+    else c0 += x >= v ? 1 : 0;
+  });
+  return row4_sum(c0 + c1);
+}
+
+// Bit masks over the lane's key slots in shift-in order: slot 32 d + e ends up at bit 31 - e of
+// m[d], so that the leading set bit is the lowest slot.
+template <class Pred>
+__device__ __forceinline__ void slot_masks(const float (&acc)[kPsMaxMt][4], int nmt, uint32_t (&m)[4], Pred&& pred) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) m[d] = 0u;
+  for_slots(acc, nmt, [&](float x, int q) { m[q >> 5] = m[q >> 5] + m[q >> 5] + (pred(x) ? 1u : 0u); });
+  const int nq = 4 * nmt;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const int nd = nq - 32 * d;
+    if (nd > 0 && nd < 32) m[d] <<= 32 - nd;
+  }
+}
+
+// Copies the assembled sets of a slice's valid rows from LDS to the selection output.
+__device__ __forceinline__ void copy_out(const SelectArgs& a, int64_t bm, int s, const int16_t* ost, int lane) {
+  const int nr = min(kPsRows, a.n_q - s * kPsRows);
+  int16_t* dst = a.sel + (bm * a.n_q + (int64_t)s * kPsRows) * a.k_total;
+  const int n = nr * a.k_total;
+  if (((reinterpret_cast<uintptr_t>(dst) | (uintptr_t)(2 * n)) & 15u) == 0) {
+    for (int i = lane; i < n / 8; i += 64)
+      *reinterpret_cast<uint4*>(dst + 8 * i) = *reinterpret_cast<const uint4*>(ost + 8 * i);
+  } else {
+    for (int i = lane; i < n; i += 64) dst[i] = ost[i];
+  }
+}
+
+// kStaged: every set is assembled in the wavefront's LDS rows (k_total <= kPsStageK) and written
+// out with 16-byte stores; otherwise entries go straight to the output.
+template <bool kStaged>
+__global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
+  __shared__ __align__(16) uint16_t kst[kPsStageRows * kPsPitch];
+  __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsStageK : 8];
+  __shared__ int next_slice;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t bm = blockIdx.x % n_groups;
+  const int u = (int)(blockIdx.x / n_groups);
+  const int s_begin = plan.bound[u], s_end = plan.bound[u + 1];
+  if (s_begin >= s_end) return;
+
+  // ---- stage the K~ rows of the unit's largest candidate range (its last row), zero-padded to
+  // whole M-tiles and the read-ahead rows.  Rows that take every candidate are never scored, and
+  // neither is a unit whose last row takes every candidate (earlier rows have at most as many
+  // candidates and at least as large a budget).
+  {
+    const RowGeom gl = row_geom(a.q_pos0 + min(a.n_q, s_end * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
+    const int c_stage = gl.n_take < gl.n_cand ? gl.n_cand : 0;
+    const int c_fill = c_stage > 0 ? ((c_stage + 15) & ~15) + 4 : 0;
+    const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim;
+    for (int i = tid; i < c_fill * 16; i += kPsThreads) {
+      const int c = i >> 4, part = i & 15;
+      const uint4 w = c < c_stage ? ld16(kcb + (int64_t)c * kHeadDim + part * 8) : make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4*>(kst + c * kPsPitch + part * 8) = w;
+    }
+    if (tid == 0) next_slice = s_end - 1;
+  }
+  __syncthreads();
+
+  const int lr = lane & 15, lg = lane >> 4;
+  int16_t* ost = ost_all + (kStaged ? wave * kPsRows * a.k_total : 0);
+  // Slices are taken from the end of the range (most candidates first).
+  auto grab = [&]() -> int {
+    int s = 0;
+    if (lane == 0) s = atomicSub(&next_slice, 1);
+    return __builtin_amdgcn_readfirstlane(s);
+  };
+  auto load_f = [&](int s, uint4 (&fw)[4]) {
+    const int r = s * kPsRows + lr;
+    if (s >= s_begin && r < a.n_q) {
+      const uint16_t* fp = a.f + (bm * a.n_q + r) * kHeadDim + 8 * lg;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fw[ks] = ld16(fp + 32 * ks);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fw[ks] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+
+  int s = grab();
+  int s_prev = -1;  // slice whose assembled sets still wait in LDS
+  uint4 fnext[4];
+  load_f(s, fnext);
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the first slice's F is in registers
+  while (s >= s_begin) {
+    uint4 fw[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
+    const int s_next = grab();
+    load_f(s_next, fnext);
+    // The previous slice's sets leave LDS now: these stores are long complete when the next
+    // slice waits for the F rows requested just above.
+    if (kStaged && s_prev >= 0) {
+      wave_lds_sync();
+      copy_out(a, bm, s_prev, ost, lane);
+    }
+
+    // ---- row geometry, forced blocks, padding, rows that take every candidate
+    const int r = s * kPsRows + lr;
+    const bool row_ok = r < a.n_q;
+    const int64_t row = bm * a.n_q + r;
+    const RowGeom g = row_geom(a.q_pos0 + r, a.n_init, a.n_local, a.k_total);
+    int16_t* out = kStaged ? ost + lr * a.k_total : a.sel + row * a.k_total;
+    if (row_ok) {
+      for (int i = lg; i < g.init_hi; i += 4) out[i] = (int16_t)i;
+      const int n_loc = g.blk - g.local_lo + 1;
+      for (int i = lg; i < n_loc; i += 4) out[g.init_hi + g.n_take + i] = (int16_t)(g.local_lo + i);
+      for (int i = g.n_forced + g.n_take + lg; i < a.k_total; i += 4) out[i] = (int16_t)-1;
+      if (lg == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+      if (g.n_take >= g.n_cand)
+        for (int i = lg; i < g.n_cand; i += 4) out[g.init_hi + i] = (int16_t)(g.cand_lo + i);
+    }
+    const RowGeom gs = row_geom(a.q_pos0 + min(a.n_q, (s + 1) * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
+    s_prev = s;
+    s = s_next;
+    if (gs.n_take >= gs.n_cand) continue;  // the slice's last row takes every candidate: all rows do
+
+    // ---- scores: S^T = K~ F^T, one M-tile of 16 candidates at a time
+    const int C = gs.n_cand;
+    const int nmt = __builtin_amdgcn_readfirstlane((C + 15) >> 4);
+    const int Q = 4 * nmt;
+    const int n = g.n_take, Cr = g.n_cand;
+    const bool search = row_ok && n > 0 && n < Cr;
+    const int v = search ? min(max(Cr - lg * Q, 0), Q) : Q;  // this lane's valid key slots
+    float acc[kPsMaxMt][4];
+    {
+      bf16x8 fb[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fb[ks] = as_bf16x8(fw[ks]);
+      const uint16_t* ab = kst + ((lr >> 2) * Q + (lr & 3)) * kPsPitch + 8 * lg;
+      // A fragments are read one M-tile ahead of the MFMAs that use them (after the last M-tile
+      // this reads rows 16 nmt .. 16 nmt + 3: inside the staged array).
+      uint4 aw[2][4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) aw[0][ks] = *reinterpret_cast<const uint4*>(ab + 32 * ks);
+#pragma unroll
+      for (int t = 0; t < kPsMaxMt; ++t) {
+        if (t < nmt) {
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks)
+            aw[(t + 1) & 1][ks] = *reinterpret_cast<const uint4*>(ab + 4 * (t + 1) * kPsPitch + 32 * ks);
+          f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[t & 1][ks]), fb[ks], c);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[t][i] = c[i];
+        }
+      }
+      // Key slots past the row's candidates (the last lane group's tail, rows with fewer
+      // candidates than the slice) hold -inf, which no threshold admits.
+#pragma unroll
+      for (int t = 0; t < kPsMaxMt; ++t) {
+        if (t < nmt && __ballot(4 * t + 4 > v) != 0ull) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (4 * t + i >= v) acc[t][i] = -INFINITY;
+        }
+      }
+    }
+
+    // ---- exact n-th largest per row
+    // Mean and variance of a sample: the first 16 slots of each of the row's lanes.
+    float s1 = 0.f, s2 = 0.f, ns = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = t < nmt && 4 * t + i < v;
+        const float x = ok ? acc[t][i] : 0.f;
+        s1 += x;
+        s2 = fmaf(x, x, s2);
+        ns += ok ? 1.f : 0.f;
+      }
+    }
+    s1 = row4_sum(s1);
+    s2 = row4_sum(s2);
+    ns = fmaxf(row4_sum(ns), 1.f);
+    const float inv_s = __builtin_amdgcn_rcpf(ns);
+    const float mu = s1 * inv_s;
+    const float sigma = sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
+    const float inv = __builtin_amdgcn_rcpf((float)(Cr > 0 ? Cr : 1));
+    const float z0 = upper_normal_quantile(((float)n - 0.5f) * inv);
+    // Counts per unit of score near the guess (normal model) and the first pass's spacing: about
+    // 1.5 sqrt(n) + 2 counts, the typical binomial error of the model guess.
+    const float dens = fmaxf((float)Cr * 0.39894228f * __expf(-0.5f * z0 * z0) / sigma, 1e-30f);
+    const float step = (1.5f * sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
+    const float t_mid = mu + sigma * z0;
+
+    // Bracket [lo, hi) in key space: count(key >= lo) = c_lo >= n > c_hi = count(key >= hi).
+    // lo starts just above -inf (every real score counts), hi just above +inf (none does).
+    constexpr uint32_t kKeyNegInf = 0x007fffffu;  // key of -inf: below every threshold used
+    uint32_t lo = kKeyNegInf + 1u, hi = 0xff800001u;
+    int c_lo = Cr, c_hi = 0;
+    float vlo = 0.f, vhi = 0.f;
+    bool lo_b = false, hi_b = false;  // vlo / vhi hold the score value of lo / hi
+    bool done = !search;
+    {  // first pass: three thresholds around the guess
+      const float va = t_mid - step, vb = t_mid, vc = t_mid + step;
+      const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
+      // compare against the exact values of the keys (non-finite guesses never enter the bracket)
+      const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
+      int ca = 0, cb = 0, cc = 0;
+      for_slots(acc, nmt, [&](float x, int) {
+        ca += x >= fa ? 1 : 0;
+        cb += x >= fb ? 1 : 0;
+        cc += x >= fc ? 1 : 0;
+      });
+      ca = row4_sum(ca);
+      cb = row4_sum(cb);
+      cc = row4_sum(cc);
+      if (!done) {
+        const uint32_t tt[3] = {ta, tb, tc};
+        const int cs[3] = {ca, cb, cc};
+        const float vs[3] = {va, vb, vc};
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+          if (tt[i] > lo && tt[i] < hi) {
+            if (cs[i] >= n) { lo = tt[i]; c_lo = cs[i]; vlo = vs[i]; lo_b = true; }
+            else { hi = tt[i]; c_hi = cs[i]; vhi = vs[i]; hi_b = true; }
+          }
+        }
+        done = (c_lo == n) || (hi - lo <= 1u);
+      }
+    }
+    float grow = 2.f * step;
+    for (int it = 0; it < 100; ++it) {
+      const bool want_max = !done && hi_b && (n - c_hi == 1);
+      const bool want_cnt = !done && !want_max;
+      if (__ballot(want_cnt) != 0ull) {
+        uint32_t t = lo + ((hi - lo) >> 1);  // key-space bisection unless a model step is taken
+        float tv = 0.f;
+        bool have_v = false;
+        if (want_cnt) {
+          if (lo_b && hi_b) {
+            if (it % 6 != 5) {
+              tv = vlo + (vhi - vlo) * (((float)(c_lo - n) + 0.5f) * __builtin_amdgcn_rcpf((float)(c_lo - c_hi)));
+              have_v = true;
+            }
+          } else if (it < 6) {  // one side still open: step outwards, doubling
+            tv = lo_b ? vlo + grow : vhi - grow;
+            grow *= 2.f;
+            have_v = true;
+          }
+          if (have_v) {
+            if (isfinite(tv))
+              t = key_of_value(tv);
+            else
+              have_v = false;
+          }
+          if (t <= lo) { t = lo + 1u; have_v = false; }
+          if (t >= hi) { t = hi - 1u; have_v = false; }
+        }
+        const int c = count_ge(acc, nmt, key_value(t));
+        if (want_cnt) {
+          const float vt = have_v ? tv : key_value(t);
+          if (c >= n) { lo = t; c_lo = c; vlo = vt; lo_b = true; }
+          else { hi = t; c_hi = c; vhi = vt; hi_b = true; }
+          done = (c_lo == n) || (hi - lo <= 1u);
+        }
+      } else if (__ballot(want_max) != 0ull) {
+        // n - 1 scores lie at or above hi: the n-th largest is the largest score below hi.  No
+        // score lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
+        const float fhi = key_value(hi);
+        float mv = -INFINITY;
+        for_slots(acc, nmt, [&](float x, int) { mv = x < fhi ? fmaxf(mv, x) : mv; });
+        const uint32_t m = row4_max(mv == -INFINITY ? 0u : key_of_value(mv));
+        if (want_max) {
+          lo = m;
+          hi = m + 1u;
+          c_lo = -1;  // unknown: the emission takes the n - c_hi lowest-index scores equal to lo
+          done = true;
+        }
+      } else {
+        break;
+      }
+    }
+
+    // ---- emission.  Normal case: the chosen scores are those >= lo (exactly n).  Tie case (the
+    // bracket closed on one value shared by more than the remaining slots): scores > lo, plus the
+    // lowest-index n - c_hi of the scores == lo.
+    const bool tie_mode = search && c_lo != n;
+    const float fthr = key_value(tie_mode ? lo + 1u : lo), flo = key_value(lo);
+    uint32_t ch[4];
+    slot_masks(acc, nmt, ch, [&](float x) { return x >= fthr; });
+    if (__ballot(tie_mode) != 0ull) {
+      uint32_t tm[4];
+      slot_masks(acc, nmt, tm, [&](float x) { return x == flo; });
+      int tcnt = 0;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) tcnt += __popc(tm[d]);
+      int ttot;
+      const int tb = row4_excl_scan(tcnt, lg, &ttot);
+      if (tie_mode) {
+        int take = min(max(n - c_hi - tb, 0), tcnt);
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          while (take > 0 && tm[d] != 0u) {
+            const uint32_t top = 0x80000000u >> __builtin_clz(tm[d]);
+            ch[d] |= top;
+            tm[d] ^= top;
+            --take;
+          }
+        }
+      }
+    }
+    if (!search) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d) ch[d] = 0u;
+    }
+    int ccnt = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
+    int ctot;
+    const int cb = row4_excl_scan(ccnt, lg, &ctot);
+    if (search) {
+      int16_t* dst = out + g.init_hi;
+      const int cand0 = g.cand_lo + lg * Q;
+      int k = cb;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        uint32_t m = 32 * d < Q ? ch[d] : 0u;
+        while (m) {
+          const int e = __builtin_clz(m);
+          if (k < n) dst[k] = (int16_t)(cand0 + 32 * d + e);  // never past the row's slots
+          ++k;
+          m ^= 0x80000000u >> e;
+        }
+      }
+    }
+  }
+  if (kStaged && s_prev >= 0) {
+    wave_lds_sync();
+    copy_out(a, bm, s_prev, ost, lane);
+  }
+}
+
+// Splits every (batch, group)'s slices into `units` ranges of about equal estimated cost.  Per
+// slice, measured on the 32K prefill: about 230 candidates' worth of fixed work plus one unit per
+// candidate when its rows are scored, and about 40 when they take every candidate.
+static void plan_units(const SelectArgs& a, int units, PrefillPlan* plan) {
+  const int ns = (a.n_q + kPsRows - 1) / kPsRows;
+  plan->n_slices = ns;
+  plan->units = units;
+  auto cost = [&](int s) -> int64_t {
+    const RowGeom g = row_geom(a.q_pos0 + std::min<int64_t>(a.n_q, (int64_t)(s + 1) * kPsRows) - 1, a.n_init,
+                               a.n_local, a.k_total);
+    if (g.n_take >= g.n_cand) return 40;
+    return 230 + 16 * ((g.n_cand + 15) / 16);
+  };
+  int64_t total = 0;
+  for (int s = 0; s < ns; ++s) total += cost(s);
+  int64_t acc = 0;
+  int s = 0;
+  plan->bound[0] = 0;
+  for (int uu = 1; uu < units; ++uu) {
+    const int64_t target = total * uu / units;
+    while (s < ns && acc + cost(s) <= target) acc += cost(s++);
+    plan->bound[uu] = (uint16_t)s;
+  }
+  plan->bound[units] = (uint16_t)ns;
+}
+
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
-  const int n_tiles = (a.n_q + kPreRows - 1) / kPreRows;
   const int n_groups = a.batch * a.n_kv_heads;
-  hipLaunchKernelGGL(prefill_select_kernel, dim3((unsigned)((int64_t)n_groups * n_tiles)), dim3(kPreThreads), 0,
-                     stream, a, n_tiles, n_groups);
+  const int ns = (a.n_q + kPsRows - 1) / kPsRows;
+  if (ns > 65535) return hipErrorInvalidValue;
+  constexpr int kUnitsTarget = 256;  // one persistent unit per CU
+  int units = n_groups >= kUnitsTarget ? 1 : kUnitsTarget / n_groups;
+  units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
+  PrefillPlan plan;
+  plan_units(a, units, &plan);
+  const dim3 grid((unsigned)((int64_t)n_groups * units));
+  if (a.k_total <= kPsStageK)
+    hipLaunchKernelGGL(prefill_select_kernel<true>, grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+  else
+    hipLaunchKernelGGL(prefill_select_kernel<false>, grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   return hipGetLastError();
 }
 

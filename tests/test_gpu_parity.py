@@ -161,6 +161,33 @@ def test_prefill_select(dev, B, H, T, n_q, q_pos0, k_total):
     say(f"  rows {n}, tie swaps {swaps}")
 
 
+PREFILL_SELECT_WINDOWS = [
+    # B, H, T, n_q, q_pos0, k_total, n_init, n_local
+    (1, 1, 20000, 1000, 18991, 100, 1, 2),  # odd start, larger budget, a single group
+    (3, 1, 2000, 2000, 0, 4, 1, 2),  # one chosen block per row
+    (1, 2, 9000, 9000, 0, 40, 0, 3),  # no initial block
+    (1, 1, 30000, 3000, 27000, 64, 4, 16),  # 4 initial blocks, a 16-block local window
+    (1, 1, 2048, 2048, 0, 20, 1, 1),  # few candidates: lane groups past the last candidate
+]
+
+
+@pytest.mark.parametrize("B,H,T,n_q,q_pos0,k_total,n_init,n_local", PREFILL_SELECT_WINDOWS)
+def test_prefill_select_windows(dev, B, H, T, n_q, q_pos0, k_total, n_init, n_local):
+    say(f"prefill select B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} k{k_total} init {n_init} local {n_local}")
+    w, case = make(B, H, 4, T, n_q, k_total, 4500 + T, n_init=n_init, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nb = T // 64
+    s, o = shapes(B, H, 4, k_total, t_cap, max(nb, 1), n_init=n_init, n_local=n_local)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nb)
+    f_u16 = inputs.to_u16(case["f"])
+    sel, cnt = gpu_select(s, case["f"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
+    rng = np.random.default_rng(1)
+    rr = sorted(set(rng.integers(0, n_q, size=min(n_q, 500)).tolist()) | {0, n_q - 1})
+    rows = [(b, m, r) for b in range(B) for m in range(H) for r in rr]
+    n, swaps = compare_selection(o, f_u16, kc_ref, n_q, q_pos0, sel.cpu().numpy(), cnt.cpu().numpy(), rows)
+    say(f"  rows {n}, tie swaps {swaps}")
+
+
 def test_select_is_deterministic(dev):
     say("select determinism")
     w, case = make(1, 2, 4, 32768, 32768, 64, 4100)
