@@ -46,8 +46,10 @@ constexpr int kPsWaves = kPsThreads / 64;
 constexpr int kPsRows = 16;                     // rows per slice (one MFMA N-tile)
 constexpr int kPsMaxMt = kSelTileMaxCand / 16;  // M-tiles per slice: up to 128 key slots per lane
 constexpr int kPsPitch = kHeadDim + 8;          // bf16 per staged K~ row (272 B)
-constexpr int kPsStageRows = kSelTileMaxCand + 4;  // staged K~ rows, the A read-ahead's 4 included
+constexpr int kPsStageRows = kSelTileMaxCand + 8;  // staged K~ rows, the A read-ahead's 8 included
 constexpr int kPsStageK = 64;                   // sets of at most this many entries go through LDS
+constexpr int kPsOutPitch = kPsStageK + 8;      // int16 per staged set row: rows 144 B apart use
+                                                // distinct banks; entries 64.. are emission dummies
 constexpr int kPsMaxUnits = 256;                // units per (batch, group)
 
 struct PrefillPlan {
@@ -90,7 +92,7 @@ __device__ __forceinline__ float upper_normal_quantile(float p) {
   p = fminf(fmaxf(p, 1e-7f), 1.f - 1e-7f);
   const bool upper = p <= 0.5f;
   const float q = upper ? p : 1.f - p;
-  const float t = sqrtf(-2.f * __logf(q));
+  const float t = __builtin_amdgcn_sqrtf(-1.3862944f * __builtin_amdgcn_logf(q));  // -2 ln q
   const float z = t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
                           (1.f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
   return upper ? z : -z;
@@ -102,53 +104,124 @@ __device__ __forceinline__ uint32_t key_of_value(float v) {
   return u ^ (uint32_t)(((int32_t)u >> 31) | (int32_t)0x80000000);
 }
 
-// Runs f(score, slot) over the lane's first 4 * nmt key slots (slot = 4 t + i).
+// Runs f(score, slot) over the lane's key slots of the first ntg groups of 4 M-tiles (slot =
+// 4 t + i); M-tiles past the slice's last one hold -inf.
 template <class Fn>
-__device__ __forceinline__ void for_slots(const float (&acc)[kPsMaxMt][4], int nmt, Fn&& f) {
+__device__ __forceinline__ void for_slots(const float (&acc)[kPsMaxMt][4], int ntg, Fn&& f) {
 #pragma unroll
-  for (int t = 0; t < kPsMaxMt; ++t) {
-    if (t < nmt) {
+  for (int tg = 0; tg < kPsMaxMt / 4; ++tg) {
+    if (tg < ntg) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) f(acc[t][i], 4 * t + i);
+      for (int t = 4 * tg; t < 4 * tg + 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f(acc[t][i], 4 * t + i);
     }
   }
 }
 
-// Number of key slots >= v, summed over the row's four lanes.
-__device__ __forceinline__ int count_ge(const float (&acc)[kPsMaxMt][4], int nmt, float v) {
-  int c0 = 0, c1 = 0;
-  for_slots(acc, nmt, [&](float x, int q) {
-    if (q & 1) c1 += x >= v ? 1 : 0;
-    else c0 += x >= v ? 1 : 0;
-  });
-  return row4_sum(c0 + c1);
+// Shifts the "below" flag of one score into m: m << 1 | [x < v], as the sign bit of x - v
+// (v_alignbit takes the top bit of the difference).  x >= v exactly when x - v has a clear sign
+// bit: scores are finite or -inf, -0 has been turned into +0, v is finite or +inf, and float32
+// denormals are kept, so the difference of two different values is never zero.  No compare
+// result passes through VCC.
+__device__ __forceinline__ uint32_t shift_below(uint32_t m, float x, float v) {
+  return __builtin_amdgcn_alignbit(m, __float_as_uint(x - v), 31);
 }
 
-// Bit masks over the lane's key slots in shift-in order: slot 32 d + e ends up at bit 31 - e of
-// m[d], so that the leading set bit is the lowest slot.
-template <class Pred>
-__device__ __forceinline__ void slot_masks(const float (&acc)[kPsMaxMt][4], int nmt, uint32_t (&m)[4], Pred&& pred) {
+// Runs f(word, m) over the lane's slot words (32 slots, the last one possibly 16): m holds the
+// "below v" flags of the word's slots, first slot highest.
+template <class Fn>
+__device__ __forceinline__ void below_words(const float (&acc)[kPsMaxMt][4], int ntg, float v, Fn&& f) {
 #pragma unroll
-  for (int d = 0; d < 4; ++d) m[d] = 0u;
-  for_slots(acc, nmt, [&](float x, int q) { m[q >> 5] = m[q >> 5] + m[q >> 5] + (pred(x) ? 1u : 0u); });
-  const int nq = 4 * nmt;
+  for (int d = 0; d < kPsMaxMt / 8; ++d) {
+    if (2 * d < ntg) {
+      uint32_t m = 0u;
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    const int nd = nq - 32 * d;
-    if (nd > 0 && nd < 32) m[d] <<= 32 - nd;
+      for (int t = 8 * d; t < 8 * d + 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = shift_below(m, acc[t][i], v);
+      if (2 * d + 1 < ntg) {
+#pragma unroll
+        for (int t = 8 * d + 4; t < 8 * d + 8; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) m = shift_below(m, acc[t][i], v);
+      }
+      f(d, m);
+    }
   }
 }
 
-// Copies the assembled sets of a slice's valid rows from LDS to the selection output.
+// Number of key slots >= v, summed over the row's four lanes (padding slots hold -inf).
+__device__ __forceinline__ int count_ge(const float (&acc)[kPsMaxMt][4], int ntg, float v) {
+  int lt = 0;
+  below_words(acc, ntg, v, [&](int, uint32_t m) { lt += __popc(m); });
+  return 64 * ntg - row4_sum(lt);
+}
+
+// Bit masks over the lane's key slots with bit e of m[d] standing for slot 32 d + e (first slot
+// lowest): the slots with x >= v.
+__device__ __forceinline__ void ge_masks(const float (&acc)[kPsMaxMt][4], int ntg, float v, uint32_t (&m)[4]) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) m[d] = 0u;
+  below_words(acc, ntg, v, [&](int d, uint32_t w) {
+    const bool full = 2 * d + 1 < ntg;  // 32 slots, else 16 in bits 0..15
+    const uint32_t ge = full ? ~w : (~w & 0xffffu) << 16;
+    m[d] = __builtin_bitreverse32(ge);
+  });
+}
+
+// Same layout for the slots with x == v (compared as floats).
+__device__ __forceinline__ void eq_masks(const float (&acc)[kPsMaxMt][4], int ntg, float v, uint32_t (&m)[4]) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) m[d] = 0u;
+#pragma unroll
+  for (int t = 0; t < kPsMaxMt; ++t) {
+    if ((t >> 2) < ntg) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (acc[t][i] == v) m[t >> 3] |= 1u << ((4 * t + i) & 31);
+    }
+  }
+}
+
+// Writes, in ascending slot order, cand0 + slot for every set bit of m (slot = 32 d + bit) to
+// dst[k], dst[k + 1], ... while k < k_end.  The loops run while any lane of the wavefront has a bit
+// left (a uniform trip count); a lane with none left writes to *dummy.
+__device__ __forceinline__ void emit_bits(const uint32_t (&m)[4], int nwords, int16_t* dst, int k, int k_end,
+                                          int cand0, int16_t* dummy) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    if (d < nwords) {
+      uint32_t w = m[d];
+      while (__ballot(w != 0u) != 0ull) {
+        const int e = __builtin_ctz(w | 0x80000000u);  // lowest set bit (31 when none: unused)
+        const bool ok = w != 0u && k < k_end;
+        int16_t* p = ok ? dst + k : dummy;
+        *p = (int16_t)(cand0 + 32 * d + e);
+        k += w != 0u ? 1 : 0;
+        w &= w - 1u;
+      }
+    }
+  }
+}
+
+// Copies the assembled sets of a slice's valid rows (LDS rows kPsOutPitch apart) to the selection
+// output.
 __device__ __forceinline__ void copy_out(const SelectArgs& a, int64_t bm, int s, const int16_t* ost, int lane) {
   const int nr = min(kPsRows, a.n_q - s * kPsRows);
-  int16_t* dst = a.sel + (bm * a.n_q + (int64_t)s * kPsRows) * a.k_total;
-  const int n = nr * a.k_total;
-  if (((reinterpret_cast<uintptr_t>(dst) | (uintptr_t)(2 * n)) & 15u) == 0) {
-    for (int i = lane; i < n / 8; i += 64)
-      *reinterpret_cast<uint4*>(dst + 8 * i) = *reinterpret_cast<const uint4*>(ost + 8 * i);
+  const int k = a.k_total;
+  int16_t* dst = a.sel + (bm * a.n_q + (int64_t)s * kPsRows) * k;
+  if (((reinterpret_cast<uintptr_t>(dst) | (uintptr_t)(2 * k)) & 15u) == 0) {
+    const int per_row = k / 8;  // 16-byte chunks per row
+    for (int i = lane; i < nr * per_row; i += 64) {
+      const int r = i / per_row, c = i - r * per_row;
+      *reinterpret_cast<uint4*>(dst + r * k + 8 * c) = *reinterpret_cast<const uint4*>(ost + r * kPsOutPitch + 8 * c);
+    }
   } else {
-    for (int i = lane; i < n; i += 64) dst[i] = ost[i];
+    for (int i = lane; i < nr * k; i += 64) {
+      const int r = i / k;
+      dst[i] = ost[r * kPsOutPitch + (i - r * k)];
+    }
   }
 }
 
@@ -157,7 +230,7 @@ __device__ __forceinline__ void copy_out(const SelectArgs& a, int64_t bm, int s,
 template <bool kStaged>
 __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
   __shared__ __align__(16) uint16_t kst[kPsStageRows * kPsPitch];
-  __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsStageK : 8];
+  __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsOutPitch : 8];
   __shared__ int next_slice;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
@@ -172,7 +245,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
   {
     const RowGeom gl = row_geom(a.q_pos0 + min(a.n_q, s_end * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
     const int c_stage = gl.n_take < gl.n_cand ? gl.n_cand : 0;
-    const int c_fill = c_stage > 0 ? ((c_stage + 15) & ~15) + 4 : 0;
+    const int c_fill = c_stage > 0 ? ((c_stage + 15) & ~15) + 8 : 0;
     const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim;
     for (int i = tid; i < c_fill * 16; i += kPsThreads) {
       const int c = i >> 4, part = i & 15;
@@ -184,7 +257,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
   __syncthreads();
 
   const int lr = lane & 15, lg = lane >> 4;
-  int16_t* ost = ost_all + (kStaged ? wave * kPsRows * a.k_total : 0);
+  int16_t* ost = ost_all + (kStaged ? wave * kPsRows * kPsOutPitch : 0);
   // Slices are taken from the end of the range (most candidates first).
   auto grab = [&]() -> int {
     int s = 0;
@@ -226,7 +299,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     const bool row_ok = r < a.n_q;
     const int64_t row = bm * a.n_q + r;
     const RowGeom g = row_geom(a.q_pos0 + r, a.n_init, a.n_local, a.k_total);
-    int16_t* out = kStaged ? ost + lr * a.k_total : a.sel + row * a.k_total;
+    int16_t* out = kStaged ? ost + lr * kPsOutPitch : a.sel + row * a.k_total;
     if (row_ok) {
       for (int i = lg; i < g.init_hi; i += 4) out[i] = (int16_t)i;
       const int n_loc = g.blk - g.local_lo + 1;
@@ -244,6 +317,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     // ---- scores: S^T = K~ F^T, one M-tile of 16 candidates at a time
     const int C = gs.n_cand;
     const int nmt = __builtin_amdgcn_readfirstlane((C + 15) >> 4);
+    const int ntg = (nmt + 3) >> 2;  // groups of 4 M-tiles the slot loops run over
     const int Q = 4 * nmt;
     const int n = g.n_take, Cr = g.n_cand;
     const bool search = row_ok && n > 0 && n < Cr;
@@ -254,22 +328,27 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) fb[ks] = as_bf16x8(fw[ks]);
       const uint16_t* ab = kst + ((lr >> 2) * Q + (lr & 3)) * kPsPitch + 8 * lg;
-      // A fragments are read one M-tile ahead of the MFMAs that use them (after the last M-tile
-      // this reads rows 16 nmt .. 16 nmt + 3: inside the staged array).
-      uint4 aw[2][4];
+      // A fragments are read two M-tiles ahead of the MFMAs that use them (past the last M-tile
+      // this reads rows up to 16 nmt + 7: inside the staged array).
+      uint4 aw[3][4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) aw[0][ks] = *reinterpret_cast<const uint4*>(ab + 32 * ks);
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) aw[1][ks] = *reinterpret_cast<const uint4*>(ab + 4 * kPsPitch + 32 * ks);
 #pragma unroll
       for (int t = 0; t < kPsMaxMt; ++t) {
         if (t < nmt) {
 #pragma unroll
           for (int ks = 0; ks < 4; ++ks)
-            aw[(t + 1) & 1][ks] = *reinterpret_cast<const uint4*>(ab + 4 * (t + 1) * kPsPitch + 32 * ks);
+            aw[(t + 2) % 3][ks] = *reinterpret_cast<const uint4*>(ab + 4 * (t + 2) * kPsPitch + 32 * ks);
           f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[t & 1][ks]), fb[ks], c);
+          for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[t % 3][ks]), fb[ks], c);
 #pragma unroll
           for (int i = 0; i < 4; ++i) acc[t][i] = c[i];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[t][i] = -INFINITY;
         }
       }
       // Key slots past the row's candidates (the last lane group's tail, rows with fewer
@@ -303,13 +382,13 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     ns = fmaxf(row4_sum(ns), 1.f);
     const float inv_s = __builtin_amdgcn_rcpf(ns);
     const float mu = s1 * inv_s;
-    const float sigma = sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
+    const float sigma = __builtin_amdgcn_sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
     const float inv = __builtin_amdgcn_rcpf((float)(Cr > 0 ? Cr : 1));
     const float z0 = upper_normal_quantile(((float)n - 0.5f) * inv);
     // Counts per unit of score near the guess (normal model) and the first pass's spacing: about
     // 1.5 sqrt(n) + 2 counts, the typical binomial error of the model guess.
     const float dens = fmaxf((float)Cr * 0.39894228f * __expf(-0.5f * z0 * z0) / sigma, 1e-30f);
-    const float step = (1.5f * sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
+    const float step = (1.5f * __builtin_amdgcn_sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
     const float t_mid = mu + sigma * z0;
 
     // Bracket [lo, hi) in key space: count(key >= lo) = c_lo >= n > c_hi = count(key >= hi).
@@ -325,15 +404,39 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
       // compare against the exact values of the keys (non-finite guesses never enter the bracket)
       const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
-      int ca = 0, cb = 0, cc = 0;
-      for_slots(acc, nmt, [&](float x, int) {
-        ca += x >= fa ? 1 : 0;
-        cb += x >= fb ? 1 : 0;
-        cc += x >= fc ? 1 : 0;
-      });
-      ca = row4_sum(ca);
-      cb = row4_sum(cb);
-      cc = row4_sum(cc);
+#pragma unroll
+      for (int tg = 0; tg < kPsMaxMt / 4; ++tg) {
+        if (tg < ntg) {
+#pragma unroll
+          for (int t = 4 * tg; t < 4 * tg + 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[t][i] += 0.0f;  // -0 becomes +0 (shift_below relies on it)
+        }
+      }
+      int la = 0, lb = 0, lc = 0;  // slots below each threshold
+#pragma unroll
+      for (int d = 0; d < kPsMaxMt / 8; ++d) {
+        if (2 * d < ntg) {
+          uint32_t ma = 0u, mb = 0u, mc = 0u;
+#pragma unroll
+          for (int t = 8 * d; t < 8 * d + 8; ++t) {
+            if (t < 8 * d + 4 || 2 * d + 1 < ntg) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                ma = shift_below(ma, acc[t][i], fa);
+                mb = shift_below(mb, acc[t][i], fb);
+                mc = shift_below(mc, acc[t][i], fc);
+              }
+            }
+          }
+          la += __popc(ma);
+          lb += __popc(mb);
+          lc += __popc(mc);
+        }
+      }
+      const int ca = 64 * ntg - row4_sum(la);
+      const int cb = 64 * ntg - row4_sum(lb);
+      const int cc = 64 * ntg - row4_sum(lc);
       if (!done) {
         const uint32_t tt[3] = {ta, tb, tc};
         const int cs[3] = {ca, cb, cc};
@@ -349,7 +452,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       }
     }
     float grow = 2.f * step;
-    for (int it = 0; it < 100; ++it) {
+    for (int it = 0; it < 200; ++it) {  // every sixth step bisects the key range: done within 6 * 33
       const bool want_max = !done && hi_b && (n - c_hi == 1);
       const bool want_cnt = !done && !want_max;
       if (__ballot(want_cnt) != 0ull) {
@@ -376,7 +479,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
           if (t <= lo) { t = lo + 1u; have_v = false; }
           if (t >= hi) { t = hi - 1u; have_v = false; }
         }
-        const int c = count_ge(acc, nmt, key_value(t));
+        const int c = count_ge(acc, ntg, key_value(t));
         if (want_cnt) {
           const float vt = have_v ? tv : key_value(t);
           if (c >= n) { lo = t; c_lo = c; vlo = vt; lo_b = true; }
@@ -388,7 +491,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
         // score lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
         const float fhi = key_value(hi);
         float mv = -INFINITY;
-        for_slots(acc, nmt, [&](float x, int) { mv = x < fhi ? fmaxf(mv, x) : mv; });
+        for_slots(acc, ntg, [&](float x, int) { mv = x < fhi ? fmaxf(mv, x) : mv; });
         const uint32_t m = row4_max(mv == -INFINITY ? 0u : key_of_value(mv));
         if (want_max) {
           lo = m;
@@ -401,16 +504,22 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       }
     }
 
-    // ---- emission.  Normal case: the chosen scores are those >= lo (exactly n).  Tie case (the
-    // bracket closed on one value shared by more than the remaining slots): scores > lo, plus the
-    // lowest-index n - c_hi of the scores == lo.
-    const bool tie_mode = search && c_lo != n;
-    const float fthr = key_value(tie_mode ? lo + 1u : lo), flo = key_value(lo);
+    // ---- emission.  The chosen scores are those >= value(lo): exactly n of them unless several
+    // scores share that value (the bracket closed on one key, or the max pass found a repeated
+    // value).  Then (tie case) they are the scores > value(lo) -- c_hi of them, since hi = lo + 1
+    // -- plus the lowest-index n - c_hi of the scores equal to value(lo).
     uint32_t ch[4];
-    slot_masks(acc, nmt, ch, [&](float x) { return x >= fthr; });
+    ge_masks(acc, ntg, key_value(lo), ch);
+    int ccnt = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
+    int ctot;
+    int cb = row4_excl_scan(ccnt, lg, &ctot);
+    const bool tie_mode = search && ctot != n;
     if (__ballot(tie_mode) != 0ull) {
-      uint32_t tm[4];
-      slot_masks(acc, nmt, tm, [&](float x) { return x == flo; });
+      uint32_t gt[4], tm[4];
+      ge_masks(acc, ntg, key_value(lo + 1u), gt);
+      eq_masks(acc, ntg, key_value(lo), tm);
       int tcnt = 0;
 #pragma unroll
       for (int d = 0; d < 4; ++d) tcnt += __popc(tm[d]);
@@ -420,25 +529,24 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
         int take = min(max(n - c_hi - tb, 0), tcnt);
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
+          ch[d] = gt[d];
           while (take > 0 && tm[d] != 0u) {
-            const uint32_t top = 0x80000000u >> __builtin_clz(tm[d]);
-            ch[d] |= top;
-            tm[d] ^= top;
+            const uint32_t low = tm[d] & (~tm[d] + 1u);
+            ch[d] |= low;
+            tm[d] ^= low;
             --take;
           }
         }
       }
-    }
-    if (!search) {
+      ccnt = 0;
 #pragma unroll
-      for (int d = 0; d < 4; ++d) ch[d] = 0u;
+      for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
+      cb = row4_excl_scan(ccnt, lg, &ctot);
     }
-    int ccnt = 0;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
-    int ctot;
-    const int cb = row4_excl_scan(ccnt, lg, &ctot);
-    if (search) {
+    if (kStaged) {
+      // every lane runs the wave-uniform loops; rows without a search write nothing
+      emit_bits(ch, (Q + 31) >> 5, out + g.init_hi, cb, search ? n : 0, g.cand_lo + lg * Q, out + kPsStageK + lg);
+    } else if (search) {
       int16_t* dst = out + g.init_hi;
       const int cand0 = g.cand_lo + lg * Q;
       int k = cb;
@@ -446,10 +554,10 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       for (int d = 0; d < 4; ++d) {
         uint32_t m = 32 * d < Q ? ch[d] : 0u;
         while (m) {
-          const int e = __builtin_clz(m);
+          const int e = __builtin_ctz(m);
           if (k < n) dst[k] = (int16_t)(cand0 + 32 * d + e);  // never past the row's slots
           ++k;
-          m ^= 0x80000000u >> e;
+          m &= m - 1u;
         }
       }
     }
