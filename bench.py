@@ -278,17 +278,23 @@ def pipeline_leg(dev, steps):
     ms_compute = time_events(lambda: (pipe._select(pipe.f[1], 2), pipe._attend(1)), 10, comp)
     ms_gather = time_events(lambda: pipe._gather(1, comp), 5, comp)
 
-    def timed(overlap):
-        pipe.step(overlap=overlap)
+    def one_step(overlap):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(steps):
-            pipe.step(overlap=overlap)
+        pipe.step(overlap=overlap)
         torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3 / steps
+        return (time.perf_counter() - t0) * 1e3
 
-    ms_overlap = timed(True)
-    ms_serial = timed(False)
+    # The two modes alternate step by step so that drifts of the host link hit both alike; the
+    # overlap can hide at most the compute time per layer, about 1 % of a step here.
+    one_step(True)
+    one_step(False)
+    runs = {True: [], False: []}
+    for _ in range(steps):
+        for mode in (True, False):
+            runs[mode].append(one_step(mode))
+    ms_overlap = float(np.median(runs[True]))
+    ms_serial = float(np.median(runs[False]))
     bound = (L - 1) * max(ms_gather, ms_compute) + ms_compute
     for b in bufs:
         b.free()
@@ -298,6 +304,7 @@ def pipeline_leg(dev, steps):
         "gather_GBps": sweep[str(best_nwg)]["GBps"], "h2d_memcpy_GBps": (moved // 2) / (ms_cp * 1e-3) / 1e9,
         "gather_ms_per_layer": ms_gather, "compute_ms_per_layer": ms_compute,
         "ms_per_step_overlap": ms_overlap, "ms_per_step_serial": ms_serial,
+        "ms_per_step_overlap_runs": runs[True], "ms_per_step_serial_runs": runs[False],
         "ms_per_step_bound": bound, "tokens_per_s": B / (ms_overlap * 1e-3),
     }
 
@@ -305,14 +312,15 @@ def pipeline_leg(dev, steps):
 def peaks_leg(dev):
     """Hardware limits measured in the same run (the spec figures are 8 TB/s and 2.5 PFLOP/s):
     streaming HBM reads of 4 GiB, reads of 32768 randomly placed 16 KiB blocks (537 MB, the shape
-    of a decode layer's attended KV blocks), back-to-back bf16 MFMA, and a pinned 1 GiB host to
-    device copy."""
+    of a decode layer's attended KV blocks), back-to-back bf16 MFMA of both gfx950 shapes
+    (32x32x16 and 16x16x32), and a pinned 1 GiB host to device copy."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_04511_amd", "libsparda_peaks.so"))
     lib.peaks_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     lib.peaks_block_read.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                      ctypes.c_void_p]
     lib.peaks_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.peaks_mfma32_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
     stream = torch.cuda.current_stream()
     sh = ctypes.c_void_p(stream.cuda_stream)
     nbytes = 4 << 30
@@ -336,6 +344,7 @@ def peaks_leg(dev):
                                                             sink.data_ptr(), sh)), 10)
     grid, iters = 2048, 4000
     ms_mfma = warm_time(lambda: check(lib.peaks_mfma_bf16(grid, iters, sink.data_ptr(), sh)), 3)
+    ms_mfma32 = warm_time(lambda: check(lib.peaks_mfma32_bf16(grid, iters, sink.data_ptr(), sh)), 3)
     del buf
     host = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
     dst = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -345,7 +354,10 @@ def peaks_leg(dev):
     return {
         "hbm_stream_read_GBps": nbytes / (ms_stream * 1e-3) / 1e9,
         "hbm_block_read_GBps": n_blocks * 16384 / (ms_block * 1e-3) / 1e9,
-        "mfma_bf16_TFLOPs": grid * 4 * 8 * iters * 16384 / (ms_mfma * 1e-3) / 1e12,
+        # the faster of the two gfx950 bf16 shapes is the hardware's measured MFMA limit
+        "mfma_bf16_TFLOPs": grid * 4 * 4 * iters * 32768 / (ms_mfma32 * 1e-3) / 1e12,
+        "mfma_bf16_32x32x16_TFLOPs": grid * 4 * 4 * iters * 32768 / (ms_mfma32 * 1e-3) / 1e12,
+        "mfma_bf16_16x16x32_TFLOPs": grid * 4 * 8 * iters * 16384 / (ms_mfma * 1e-3) / 1e12,
         "h2d_pinned_GBps": (1 << 30) / (ms_h2d * 1e-3) / 1e9,
     }
 
@@ -445,11 +457,14 @@ def main():
         layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
         out["prefill"]["select_frac_measured_mfma_peak"] = out["prefill"]["select_tflops"] / peaks["mfma_bf16_TFLOPs"]
+        # against the rate of the 16x16x32 instruction the select kernel's layout needs
+        out["prefill"]["select_frac_measured_16x16x32_rate"] = (out["prefill"]["select_tflops"]
+                                                                / peaks["mfma_bf16_16x16x32_TFLOPs"])
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
             f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
     if not args.no_pipeline:
         layer.case = None
-        out["pipeline"] = pipeline_leg(dev, 3)
+        out["pipeline"] = pipeline_leg(dev, 4)
         log(f"[bench] pipeline {out['pipeline']['ms_per_step_overlap']:.1f} ms/step overlapped, "
             f"{out['pipeline']['ms_per_step_serial']:.1f} serial")
     if not args.no_cpu:

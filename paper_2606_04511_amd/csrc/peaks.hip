@@ -1,6 +1,6 @@
 // peaks.hip -- microbenchmarks of the hardware limits the SparDA kernels are measured against:
 // streaming HBM reads, reads of randomly placed 16 KiB blocks (the shape of attended KV blocks)
-// and back-to-back bf16 MFMA.  Built into its own library for the benchmark; not part of the
+// and back-to-back bf16 MFMA of both gfx950 bf16 shapes.  Built into its own library for the benchmark; not part of the
 // SparDA C ABI.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -60,6 +60,31 @@ __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) 
   if (s == 1.2345f) sink[0] = s;
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Four independent accumulator chains of v_mfma_f32_32x32x16_bf16 per wavefront (twice the
+// flops per instruction; on gfx950 this shape sustains about 1.5 times the 16x16x32 rate).
+__global__ __launch_bounds__(256) void mfma32_loop_kernel(int iters, float* sink) {
+  using namespace sparda;
+  const int lane = threadIdx.x & 63;
+  uint4 wa = make_uint4(0x3f803f80u + lane, 0x3f003f00u, 0x3e803e80u, 0x3f803f80u);
+  uint4 wb = make_uint4(0x3f803f80u, 0x3e803e80u + lane, 0x3f003f00u, 0x3f803f80u);
+  const bf16x8 a = as_bf16x8(wa), b = as_bf16x8(wb);
+  f32x16 c[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) c[k][j] = 0.f;
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[k], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) s += c[k][0] + c[k][15];
+  if (s == 1.2345f) sink[0] = s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -84,6 +109,13 @@ int peaks_block_read(const void* p, const uint32_t* idx, int n_idx, int grid, vo
 int peaks_mfma_bf16(int grid, int iters, void* sink, hipStream_t stream) {
   if (!sink || grid < 1 || iters < 1) return -1;
   hipLaunchKernelGGL(mfma_loop_kernel, dim3(grid), dim3(256), 0, stream, iters, static_cast<float*>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+// Each of grid x 4 wavefronts issues 4 x iters MFMAs of 32 x 32 x 16 (32768 flops each).
+int peaks_mfma32_bf16(int grid, int iters, void* sink, hipStream_t stream) {
+  if (!sink || grid < 1 || iters < 1) return -1;
+  hipLaunchKernelGGL(mfma32_loop_kernel, dim3(grid), dim3(256), 0, stream, iters, static_cast<float*>(sink));
   return hipGetLastError() == hipSuccess ? 0 : -5;
 }
 
