@@ -285,6 +285,15 @@ def pipeline_leg(dev, steps):
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) * 1e3
 
+    # The gather's workgroup count (its CU budget, the paper's CTA count) is chosen on the
+    # overlapped step, not on the gather alone: more workgroups copy no faster over the host link
+    # but crowd the CUs the concurrent select and attention need.
+    step_sweep = {}
+    for nwg in (8, 16, 32, 64):
+        pipe.n_workgroups = nwg
+        one_step(True)
+        step_sweep[str(nwg)] = float(np.median([one_step(True) for _ in range(2)]))
+    pipe.n_workgroups = int(min(step_sweep, key=lambda k: step_sweep[k]))
     # The two modes alternate step by step so that drifts of the host link hit both alike; the
     # overlap can hide at most the compute time per layer, about 1 % of a step here.
     one_step(True)
@@ -300,7 +309,7 @@ def pipeline_leg(dev, steps):
         b.free()
     return {
         "workload": f"decode pipeline, {L} layers, B{B} T={T} k{K}: {moved / 1e9:.3f} GB gathered per offloaded layer",
-        "gather_sweep": sweep, "n_workgroups": best_nwg,
+        "gather_sweep": sweep, "step_sweep_overlap_ms": step_sweep, "n_workgroups": pipe.n_workgroups,
         "gather_GBps": sweep[str(best_nwg)]["GBps"], "h2d_memcpy_GBps": (moved // 2) / (ms_cp * 1e-3) / 1e9,
         "gather_ms_per_layer": ms_gather, "compute_ms_per_layer": ms_compute,
         "ms_per_step_overlap": ms_overlap, "ms_per_step_serial": ms_serial,

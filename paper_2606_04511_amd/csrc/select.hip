@@ -207,13 +207,22 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
     const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
     const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
     const uint16_t* kbase = a.kc + (row * a.nc_cap + g.cand_lo) * kHeadDim + c * 8;
-    for (int base = wave * 64; base < C; base += kDecThreads) {
-      uint4 kw[16];
+    // Double-buffered: the next 64 candidates' loads are in flight while this wave scores the
+    // current ones.
+    uint4 kw[16], kn[16];
+    // Indices past the last candidate read the last one again (never stored), so the loads
+    // stay branch-free.
+    auto load = [&](int base, uint4 (&w)[16]) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int idx = base + 4 * i + rs;
-        kw[i] = idx < C ? ld16(kbase + (int64_t)idx * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+        const int idx = min(base + 4 * i + rs, C - 1);
+        w[i] = ld16(kbase + (int64_t)idx * kHeadDim);
       }
+    };
+    int base = wave * 64;
+    if (base < C) load(base, kw);
+    for (; base < C; base += kDecThreads) {
+      if (base + kDecThreads < C) load(base + kDecThreads, kn);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         float d = f0 * bf16lo(kw[i].x);
@@ -228,6 +237,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
         const int idx = base + 4 * i + rs;
         if (c == 0 && idx < C) sc[idx] = d;
       }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) kw[i] = kn[i];
     }
   }
   __syncthreads();
