@@ -6,8 +6,9 @@ and takes/returns numpy arrays: bf16 tensors travel as ``uint16`` bit patterns, 
 ``int16``.  It shares no code with the HIP library.
 
 Function map (paper sections in the C file):
-  compress_keys  -- Eq. 2 (mean-pooled compressed keys, one per 64-token block)
-  select_row / forecast_select -- Eq. 1 + Eq. 4 (forced init/local blocks U top-k Forecast scores)
+  compress_keys  -- Eq. 2 (mean-pooled compressed keys over windows of l_C tokens at stride s_C)
+  select_row / forecast_select -- Eq. 1 + Eq. 4 (forced init/local blocks U top-k of the
+                    max-pooled Forecast block scores)
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
 """
@@ -90,7 +91,7 @@ def open_library(path: str):
     lib.sparda_ref_f64_to_bf16.argtypes = [f64]
     lib.sparda_ref_f64_to_bf16.restype = ctypes.c_uint16
     lib.sparda_ref_compress_keys.argtypes = [S, P, i64, i32, i32, P]
-    lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P]
+    lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P, P]
     lib.sparda_ref_forecast_select.argtypes = [S, P, i32, i64, P, P, P]
     lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
@@ -176,28 +177,39 @@ def f64_to_bf16(x: float) -> int:
     return int(_load().sparda_ref_f64_to_bf16(float(x)))
 
 
-def compress_keys(shape: Shape, k: np.ndarray, t_ctx: int, blk_begin: int, blk_end: int,
+def compress_keys(shape: Shape, k: np.ndarray, t_ctx: int, w_begin: int, w_end: int,
                   k_cmp: np.ndarray | None = None) -> np.ndarray:
-    """K~ for blocks [blk_begin, blk_end); k: uint16 [B][Hkv][t_cap][D]."""
+    """K~ for compressed-key windows [w_begin, w_end) (blocks when window = stride = block);
+    k: uint16 [B][Hkv][t_cap][D]."""
     k = _u16(k)
     if k_cmp is None:
         k_cmp = np.zeros((shape.batch, shape.n_kv_heads, shape.nc_cap, shape.head_dim), np.uint16)
     cs = shape.c()
-    _check(_load().sparda_ref_compress_keys(ctypes.byref(cs), _ptr(k), t_ctx, blk_begin, blk_end, _ptr(k_cmp)),
+    _check(_load().sparda_ref_compress_keys(ctypes.byref(cs), _ptr(k), t_ctx, w_begin, w_end, _ptr(k_cmp)),
            "compress_keys")
     return k_cmp
 
 
-def select_row(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, b: int, m: int, r: int):
-    """(sel_row int16[k_total], cnt, scores float64[nc_cap] with NaN for non-candidates)."""
+def select_row_windows(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, b: int, m: int,
+                       r: int):
+    """(sel_row int16[k_total], cnt, scores float64[n_blocks] with NaN for non-candidates,
+    wins int32[n_blocks]: the window that gives each candidate block its max-pooled score)."""
     f, k_cmp = _u16(f), _u16(k_cmp)
+    nb = -(-shape.t_cap // shape.block_size)
     sel = np.empty(shape.k_total, np.int16)
     cnt = np.zeros(1, np.int16)
-    scores = np.empty(max(shape.nc_cap, 1), np.float64)
+    scores = np.empty(max(nb, 1), np.float64)
+    wins = np.empty(max(nb, 1), np.int32)
     cs = shape.c()
     _check(_load().sparda_ref_select_row(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), b, m, r,
-                                         _ptr(sel), _ptr(cnt), _ptr(scores)), "select_row")
-    return sel, int(cnt[0]), scores[: shape.nc_cap]
+                                         _ptr(sel), _ptr(cnt), _ptr(scores), _ptr(wins)), "select_row")
+    return sel, int(cnt[0]), scores[:nb], wins[:nb]
+
+
+def select_row(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, b: int, m: int, r: int):
+    """(sel_row int16[k_total], cnt, scores float64[n_blocks] with NaN for non-candidates)."""
+    sel, cnt, scores, _ = select_row_windows(shape, f, n_q, q_pos0, k_cmp, b, m, r)
+    return sel, cnt, scores
 
 
 def forecast_select(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray):

@@ -9,13 +9,19 @@
  * float64 (bf16 inputs are exact in float64).  Nothing is blocked, fused or reordered.
  *
  *   compress   Key compression, paper Sec. 3 (InfLLM-V2 recap), Eq. 2: one compressed key per
- *              window of l_C keys with stride s_C, the mean of the window.  Windows of 64 with
- *              stride 64 (one key per 64-token block) are the only grid this oracle accepts.
+ *              window of l_C keys with stride s_C, the mean of the window (window i covers
+ *              tokens [i s_C, i s_C + l_C)).  Grids with windows no longer than a block and a
+ *              stride dividing the block are accepted: (64, 64), one key per block, and the
+ *              paper's (32, 16), among others.
  *   select     Sec. 4.1, Eq. 4 with the attended-set union of Eq. 1: the Forecast row of a GQA
  *              group scores every compressed key by a plain dot product (one Forecast head per
- *              group, no softmax, no scale -- "Forecast indexer" paragraph of Sec. 4.1); the
- *              top-k of those scores, excluding the initial and local blocks, is merged with the
- *              initial and local blocks.  Ties in score are broken by the lower block index.
+ *              group, no softmax, no scale -- "Forecast indexer" paragraph of Sec. 4.1); a
+ *              max-pool turns the compressed-grid scores into block scores (the final stage of
+ *              the InfLLM-V2 selector that Sec. 3 recaps and Sec. 4.1 reuses): a block's score is
+ *              the largest score of the windows that overlap it and are complete at the query's
+ *              position.  The top-k block scores, excluding the initial and local blocks, are
+ *              merged with the initial and local blocks.  Ties in score are broken by the lower
+ *              block index.  With window = stride = block the max-pool is the identity.
  *   attend     Sec. 3, Eq. 1 and Sec. 4.1, Eq. 5: softmax attention of the query over exactly the
  *              keys/values of the attended blocks, causal within the query's own block.
  *   gather     Sec. 4.3 and Alg. 2 (prefetch of the selected blocks): staging slot s holds the 64
@@ -40,7 +46,7 @@
  *   block_size (tokens per block), cmp_kernel / cmp_stride (compression window),
  *   n_init (initial blocks always attended), n_local (local blocks always attended, counting the
  *   query's own block), k_total (attended-set size, forced blocks included),
- *   t_cap (token capacity = T stride of the K/V caches), nc_cap (block capacity of K~). */
+ *   t_cap (token capacity = T stride of the K/V caches), nc_cap (window capacity of K~). */
 typedef struct {
   int32_t batch, n_kv_heads, group_size, head_dim;
   int32_t block_size, cmp_kernel, cmp_stride;
@@ -88,31 +94,36 @@ static int check_shape(const ref_shape* s) {
   if (s->block_size < 1 || s->n_init < 0 || s->n_local < 1) return REF_ERR_INVALID_ARG;
   if (s->k_total < s->n_init + s->n_local) return REF_ERR_INVALID_ARG;
   if (s->t_cap < 1 || s->nc_cap < 0) return REF_ERR_INVALID_ARG;
-  if (s->cmp_kernel != s->block_size || s->cmp_stride != s->block_size) return REF_ERR_UNSUPPORTED;
+  /* every complete block must hold a complete window: windows no longer than a block, stride
+   * dividing the block */
+  if (s->cmp_stride < 1 || s->cmp_kernel < s->cmp_stride || s->cmp_kernel > s->block_size ||
+      s->block_size % s->cmp_stride != 0)
+    return REF_ERR_UNSUPPORTED;
   return REF_OK;
 }
 
 /* ---- Eq. 2: mean-pooled compressed keys ------------------------------------------------- */
 
 /* k: bf16 [B][Hkv][t_cap][D];  k_cmp: bf16 [B][Hkv][nc_cap][D].
- * Writes K~_j for blocks j in [blk_begin, blk_end); each must be complete inside t_ctx. */
-int sparda_ref_compress_keys(const ref_shape* s, const uint16_t* k, int64_t t_ctx, int32_t blk_begin,
-                             int32_t blk_end, uint16_t* k_cmp) {
+ * Writes K~_i for windows i in [w_begin, w_end); each window [i s_C, i s_C + l_C) must be
+ * complete inside t_ctx. */
+int sparda_ref_compress_keys(const ref_shape* s, const uint16_t* k, int64_t t_ctx, int32_t w_begin,
+                             int32_t w_end, uint16_t* k_cmp) {
   int rc = check_shape(s);
   if (rc) return rc;
-  const int64_t L = s->block_size, D = s->head_dim;
-  if (blk_begin < 0 || blk_end < blk_begin || (int64_t)blk_end > s->nc_cap) return REF_ERR_INVALID_ARG;
-  if ((int64_t)blk_end * L > t_ctx || t_ctx > s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t lw = s->cmp_kernel, sw = s->cmp_stride, D = s->head_dim;
+  if (w_begin < 0 || w_end < w_begin || (int64_t)w_end > s->nc_cap) return REF_ERR_INVALID_ARG;
+  if (w_end > w_begin && ((int64_t)(w_end - 1) * sw + lw > t_ctx || t_ctx > s->t_cap)) return REF_ERR_INVALID_ARG;
   const int64_t nrows = (int64_t)s->batch * s->n_kv_heads;
 #pragma omp parallel for schedule(static)
   for (int64_t bm = 0; bm < nrows; ++bm) {
     const uint16_t* kh = k + bm * s->t_cap * D;
     uint16_t* ch = k_cmp + bm * s->nc_cap * D;
-    for (int64_t j = blk_begin; j < blk_end; ++j) {
+    for (int64_t i = w_begin; i < w_end; ++i) {
       for (int64_t d = 0; d < D; ++d) {
         double sum = 0.0;
-        for (int64_t t = j * L; t < j * L + L; ++t) sum += sparda_ref_bf16_to_f64(kh[t * D + d]);
-        ch[j * D + d] = sparda_ref_f64_to_bf16(sum / (double)L);
+        for (int64_t t = i * sw; t < i * sw + lw; ++t) sum += sparda_ref_bf16_to_f64(kh[t * D + d]);
+        ch[i * D + d] = sparda_ref_f64_to_bf16(sum / (double)lw);
       }
     }
   }
@@ -136,17 +147,18 @@ static int by_score_then_index(const void* pa, const void* pb) {
 }
 
 /* One query row (batch b, group m, row r at position p = q_pos0 + r).
- *   f: bf16 [B][Hkv][n_q][D]; k_cmp: bf16 [B][Hkv][nc_cap][D]
+ *   f: bf16 [B][Hkv][n_q][D]; k_cmp: bf16 [B][Hkv][nc_cap][D] (compressed-key windows)
  *   sel_row: k_total entries, ascending block indices, -1 padded; cnt: number of valid entries.
- *   scores (optional, nc_cap doubles): the Forecast score of every candidate block, NaN for a
- *   block that is not a candidate of this row. */
+ *   scores (optional, one double per block of the capacity, ceil(t_cap / block) of them): the
+ *   max-pooled Forecast score of every candidate block, NaN for a block that is not a candidate.
+ *   wins (optional, same length): the lowest window index reaching that score, -1 elsewhere. */
 int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
                           const uint16_t* k_cmp, int32_t b, int32_t m, int32_t r, int16_t* sel_row,
-                          int16_t* cnt, double* scores) {
+                          int16_t* cnt, double* scores, int32_t* wins) {
   int rc = check_shape(s);
   if (rc) return rc;
   if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
-  const int64_t D = s->head_dim, L = s->block_size;
+  const int64_t D = s->head_dim, L = s->block_size, lw = s->cmp_kernel, sw = s->cmp_stride;
   const int64_t p = q_pos0 + r;
   if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
   const int64_t blk = p / L;
@@ -161,26 +173,42 @@ int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, in
   /* candidates: complete blocks that are neither initial nor local. */
   const int64_t cand_lo = s->n_init, cand_hi = blk - s->n_local;        /* inclusive */
   const int64_t n_cand = (cand_hi >= cand_lo) ? cand_hi - cand_lo + 1 : 0;
-  if (n_cand > 0 && cand_hi >= s->nc_cap) return REF_ERR_INVALID_ARG;
   const int64_t n_sel_budget = s->k_total - n_forced;
   if (n_sel_budget < 0) return REF_ERR_INVALID_ARG;
   const int64_t n_take = n_sel_budget < n_cand ? n_sel_budget : n_cand;
+  /* windows complete at position p: i s_C + l_C <= p + 1 */
+  const int64_t w_vis = (p + 1 - lw) >= 0 ? (p + 1 - lw) / sw : -1;     /* last visible window */
 
   const uint16_t* frow = f + (((int64_t)b * s->n_kv_heads + m) * n_q + r) * D;
   const uint16_t* kc = k_cmp + ((int64_t)b * s->n_kv_heads + m) * s->nc_cap * D;
 
+  const int64_t n_blk_cap = (s->t_cap + L - 1) / L;
   if (scores)
-    for (int64_t j = 0; j < s->nc_cap; ++j) scores[j] = NAN;
+    for (int64_t j = 0; j < n_blk_cap; ++j) scores[j] = NAN;
+  if (wins)
+    for (int64_t j = 0; j < n_blk_cap; ++j) wins[j] = -1;
 
   scored_block* list = (scored_block*)malloc(sizeof(scored_block) * (size_t)(n_cand > 0 ? n_cand : 1));
   if (!list) return REF_ERR_INVALID_ARG;
   for (int64_t c = 0; c < n_cand; ++c) {
     const int64_t j = cand_lo + c;
-    double dot = 0.0;
-    for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(frow[d]) * sparda_ref_bf16_to_f64(kc[j * D + d]);
-    list[c].score = dot;
+    /* windows overlapping block j: i s_C < (j + 1) L and i s_C + l_C > j L, complete at p */
+    int64_t i_lo = (j * L - lw) / sw + 1;
+    if (j * L - lw < 0) i_lo = 0;
+    int64_t i_hi = ((j + 1) * L - 1) / sw;
+    if (i_hi > w_vis) i_hi = w_vis;
+    if (i_hi >= s->nc_cap) { free(list); return REF_ERR_INVALID_ARG; }
+    double best = -INFINITY;
+    int64_t best_i = -1;
+    for (int64_t i = i_lo; i <= i_hi; ++i) {
+      double dot = 0.0;
+      for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(frow[d]) * sparda_ref_bf16_to_f64(kc[i * D + d]);
+      if (dot > best) { best = dot; best_i = i; }
+    }
+    list[c].score = best;
     list[c].block = (int32_t)j;
-    if (scores) scores[j] = dot;
+    if (scores) scores[j] = best;
+    if (wins) wins[j] = (int32_t)best_i;
   }
   qsort(list, (size_t)n_cand, sizeof(scored_block), by_score_then_index);
 
@@ -214,7 +242,7 @@ int sparda_ref_forecast_select(const ref_shape* s, const uint16_t* f, int32_t n_
     const int32_t r = (int32_t)(i % n_q);
     const int32_t m = (int32_t)((i / n_q) % s->n_kv_heads);
     const int32_t b = (int32_t)(i / ((int64_t)n_q * s->n_kv_heads));
-    int e = sparda_ref_select_row(s, f, n_q, q_pos0, k_cmp, b, m, r, sel + i * s->k_total, cnt + i, NULL);
+    int e = sparda_ref_select_row(s, f, n_q, q_pos0, k_cmp, b, m, r, sel + i * s->k_total, cnt + i, NULL, NULL);
     if (e) {
 #pragma omp critical
       err = e;

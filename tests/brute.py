@@ -52,6 +52,53 @@ def compress(k_bits: np.ndarray, n_blocks: int) -> np.ndarray:
     return f64_to_bf16_bits(mean)
 
 
+def compress_windows(k_bits: np.ndarray, n_win: int, lw: int, sw: int) -> np.ndarray:
+    """Windows of lw keys at stride sw: k uint16 [B][H][T][D] -> uint16 [B][H][n_win][D]."""
+    k = bf16_bits_to_f64(k_bits)
+    idx = np.arange(n_win)[:, None] * sw + np.arange(lw)[None, :]  # [n_win][lw] token indices
+    mean = k[:, :, idx, :].mean(axis=3)
+    return f64_to_bf16_bits(mean)
+
+
+def select_rows_pooled(f_bits, kc_bits, q_pos0, k_total, n_init, n_local, lw, sw):
+    """Dense window scores, a max over the windows that overlap each block and are complete at the
+    row's position (an explicit mask over all (block, window) pairs), then a full lexsort.
+    kc: [B][H][n_win][D] windows.  Returns sel, cnt and the pooled block scores (NaN where a
+    block has no visible window)."""
+    f = bf16_bits_to_f64(f_bits)
+    kc = bf16_bits_to_f64(kc_bits)
+    wsc = np.einsum("bhqd,bhid->bhqi", f, kc)
+    B, H, n_q, n_win = wsc.shape
+    start = np.arange(n_win) * sw
+    sel = np.full((B, H, n_q, k_total), -1, np.int16)
+    cnt = np.zeros((B, H, n_q), np.int16)
+    n_blk = (q_pos0 + n_q - 1) // BLOCK + 1
+    pooled = np.full((B, H, n_q, n_blk), np.nan)
+    for r in range(n_q):
+        p = q_pos0 + r
+        blk = p // BLOCK
+        for j in range(blk + 1):
+            overl = (start < (j + 1) * BLOCK) & (start + lw > j * BLOCK) & (start + lw <= p + 1)
+            if overl.any():
+                pooled[:, :, r, j] = wsc[:, :, r, overl].max(axis=-1)
+        forced = set(range(0, min(n_init, blk + 1))) | set(range(max(0, blk - n_local + 1), blk + 1))
+        cand = np.array([j for j in range(blk + 1) if j not in forced and j >= n_init and j <= blk - n_local],
+                        np.int64)
+        n_take = min(k_total - len(forced), len(cand))
+        for b in range(B):
+            for h in range(H):
+                if len(cand):
+                    s = pooled[b, h, r, cand]
+                    order = np.lexsort((cand, -s))
+                    chosen = set(cand[order[:n_take]].tolist())
+                else:
+                    chosen = set()
+                full = sorted(forced | chosen)
+                sel[b, h, r, : len(full)] = full
+                cnt[b, h, r] = len(full)
+    return sel, cnt, pooled
+
+
 def select_rows(f_bits, kc_bits, q_pos0, k_total, n_init, n_local):
     """Dense scores + full lexsort.  f: [B][H][n_q][D], kc: [B][H][nc][D].
     Returns sel [B][H][n_q][k_total] (ascending, -1 padded), cnt [B][H][n_q], scores [B][H][n_q][nc]."""

@@ -2,7 +2,8 @@
 
 Selection: cnt must match exactly; the block sets must match, except that a block chosen by only
 one side is accepted when the oracle's score of every such block lies within the tie window of
-the oracle's k-th chosen score s_k.  The window is max(1e-3 |s_k|, gamma_128 * sum_d |F_d K~_jd|):
+the oracle's k-th chosen score s_k.  The window is max(1e-3 |s_k|, gamma_128 * sum_d |F_d K~_id|),
+with i the compressed key that gives block j its (max-pooled) score:
 the relative window the acceptance bar states, floored by the a-priori float32 error bound of a
 128-term dot product (gamma_n = n u / (1 - n u), u = 2^-24), which only matters when s_k ~ 0.
 All scores and bounds here come from the oracle's inputs and the oracle's scores.
@@ -28,7 +29,7 @@ def compare_selection(oshape, f_u16, kc_u16, n_q, q_pos0, gpu_sel, gpu_cnt, rows
     f64 = None
     n_rows = n_swaps = 0
     for (b, m, r) in rows:
-        ref, cnt, scores = oracle.select_row(oshape, f_u16, n_q, q_pos0, kc_u16, b, m, r)
+        ref, cnt, scores, wins = oracle.select_row_windows(oshape, f_u16, n_q, q_pos0, kc_u16, b, m, r)
         g = gpu_sel[b, m, r]
         gc = int(gpu_cnt[b, m, r])
         assert gc == cnt, f"row {(b, m, r)}: cnt {gc} != oracle {cnt}"
@@ -48,7 +49,8 @@ def compare_selection(oshape, f_u16, kc_u16, n_q, q_pos0, gpu_sel, gpu_cnt, rows
         if f64 is None:
             f64 = brute.bf16_bits_to_f64(f_u16)
             kc64 = brute.bf16_bits_to_f64(kc_u16)
-        absdot = lambda j: float(np.abs(f64[b, m, r] * kc64[b, m, j]).sum())
+        # the floor for block j uses the compressed key that gives j its (max-pooled) score
+        absdot = lambda j: float(np.abs(f64[b, m, r] * kc64[b, m, wins[j]]).sum())
         for j in only:
             win = max(REL_TIE * abs(s_k), GAMMA_128 * absdot(j))
             assert abs(scores[j] - s_k) <= win, (

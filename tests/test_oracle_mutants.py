@@ -2,7 +2,8 @@
 each one: a flipped sort direction, a dropped softmax scale, an off-by-one local window, a
 causal mask that lets the next token in, an init block left out of the candidates' exclusion,
 a swapped operand index in the score, a rounding mode change in the compressed keys, and a block
-listed twice in a set being attended twice."""
+listed twice in a set being attended twice; on the paper's (32, 16) grid, a max-pool that uses
+windows not yet complete at the query and one that skips the windows straddling a block edge."""
 import math
 import os
 
@@ -21,10 +22,12 @@ MUTANTS = {
     "local_window_short": ("int64_t local_lo = blk - s->n_local + 1;", "int64_t local_lo = blk - s->n_local + 2;"),
     "causal_leak": ("if (t > p) break;", "if (t > p + 1) break;"),
     "candidates_include_init": ("const int64_t cand_lo = s->n_init,", "const int64_t cand_lo = 0,"),
-    "score_wrong_operand": ("sparda_ref_bf16_to_f64(kc[j * D + d])", "sparda_ref_bf16_to_f64(kc[d * D + j % D])"),
+    "score_wrong_operand": ("sparda_ref_bf16_to_f64(kc[i * D + d])", "sparda_ref_bf16_to_f64(kc[d * D + i % D])"),
     "compress_truncates": ("double q = nearbyint(ldexp(m, 8));", "double q = floor(ldexp(m, 8));"),
-    "compress_wrong_divisor": ("sum / (double)L", "sum / (double)(L - 1)"),
+    "compress_wrong_divisor": ("sum / (double)lw", "sum / (double)(lw - 1)"),
     "duplicate_attended_twice": ("if (seen) continue;", "(void)seen;"),
+    "pool_ignores_visibility": ("if (i_hi > w_vis) i_hi = w_vis;", "(void)w_vis;"),
+    "pool_inner_windows_only": ("int64_t i_lo = (j * L - lw) / sw + 1;", "int64_t i_lo = (j * L) / sw;"),
 }
 
 
@@ -64,7 +67,18 @@ def _pins_pass(o) -> bool:
                      t_cap=448, nc_cap=7)
         kc2 = to([[[[9, 9], [1, 0], [0, 4], [2, -2], [-1, 0], [9, 9], [9, 9]]]])
         sel2, cnt2, _ = o.select_row(s2, to([[[[1.0, 0.5]]]]), 1, 447, kc2, 0, 0, 0)
-        return cnt2 == 5 and list(sel2) == [0, 1, 2, 5, 6]
+        if not (cnt2 == 5 and list(sel2) == [0, 1, 2, 5, 6]):
+            return False
+        # the paper's (32, 16) grid: compress and max-pooled selection against the brute force,
+        # with one local block so that the visibility of the edge windows matters
+        sg = o.Shape(batch=1, n_kv_heads=H, group_size=G, head_dim=128, n_init=1, n_local=1, k_total=4, t_cap=640,
+                     nc_cap=39, cmp_kernel=32, cmp_stride=16)
+        kcg = o.compress_keys(sg, k, 640, 0, 39)
+        if not np.array_equal(kcg, brute.compress_windows(k, 39, 32, 16)):
+            return False
+        selg, cntg = o.forecast_select(sg, f, n_q, T - n_q, kcg)
+        bselg, bcntg, _ = brute.select_rows_pooled(f, kcg, T - n_q, 4, 1, 1, 32, 16)
+        return bool(np.array_equal(selg, bselg) and np.array_equal(cntg, bcntg))
     except oracle.OracleError:
         return False
 

@@ -217,6 +217,137 @@ def test_select_worked_example_with_tie(oracle_lib):
     assert list(scores[1:5]) == [1.0, 2.0, 1.0, -1.0]
 
 
+# ----------------------------------------------------------------------------- the paper's (32, 16) grid
+
+def grid_shape(oracle, B, H, T, k_total, lw=32, sw=16, n_init=1, n_local=2, D=128):
+    return oracle.Shape(batch=B, n_kv_heads=H, group_size=4, head_dim=D, block_size=64, n_init=n_init,
+                        n_local=n_local, k_total=k_total, t_cap=T, nc_cap=(T - lw) // sw + 1, cmp_kernel=lw,
+                        cmp_stride=sw)
+
+
+@pytest.mark.parametrize("lw,sw", [(32, 16), (16, 16), (64, 32), (32, 32)])
+def test_compress_windows_match_bruteforce(oracle_lib, lw, sw):
+    T = 640
+    s = grid_shape(oracle_lib, 2, 2, T, 8, lw, sw)
+    k = rnd_u16((2, 2, T, 128), 71, 0)
+    got = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    assert np.array_equal(got, brute.compress_windows(k, s.nc_cap, lw, sw))
+
+
+def test_compress_windows_incremental_and_bounds(oracle_lib):
+    """Compressing the windows completed by each 16-token step equals one full pass; a window that
+    reaches past t_ctx is refused."""
+    import oracle
+    T = 512
+    s = grid_shape(oracle_lib, 1, 2, T, 8)
+    k = rnd_u16((1, 2, T, 128), 72, 0)
+    full = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    inc = np.zeros_like(full)
+    done = 0
+    for t in range(16, T + 1, 16):
+        n_now = (t - 32) // 16 + 1 if t >= 32 else 0
+        if n_now > done:
+            oracle_lib.compress_keys(s, k, t, done, n_now, inc)
+            done = n_now
+    assert np.array_equal(inc, full)
+    with pytest.raises(oracle.OracleError):
+        oracle_lib.compress_keys(s, k, 300, 0, 18)  # window 17 ends at token 304 > 300
+
+
+@pytest.mark.parametrize("T,n_q,k_total,n_init,n_local,lw,sw", [
+    (1024, 1, 6, 1, 2, 32, 16), (1024, 200, 6, 1, 2, 32, 16), (2000, 300, 9, 0, 3, 32, 16),
+    (1500, 260, 7, 2, 1, 32, 16), (1280, 150, 5, 1, 2, 64, 32), (1280, 150, 5, 1, 1, 16, 8)])
+def test_select_pooled_matches_bruteforce(oracle_lib, T, n_q, k_total, n_init, n_local, lw, sw):
+    s = grid_shape(oracle_lib, 1, 2, T, k_total, lw, sw, n_init, n_local)
+    f = rnd_u16((1, 2, n_q, 128), 73, 1)
+    k = rnd_u16((1, 2, T, 128), 73, 2)
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    q_pos0 = T - n_q
+    sel, cnt = oracle_lib.forecast_select(s, f, n_q, q_pos0, kc)
+    bsel, bcnt, pooled = brute.select_rows_pooled(f, kc, q_pos0, k_total, n_init, n_local, lw, sw)
+    assert np.array_equal(cnt, bcnt)
+    assert np.array_equal(sel, bsel)
+    for r in (0, n_q // 2, n_q - 1):
+        _, _, scores, wins = oracle_lib.select_row_windows(s, f, n_q, q_pos0, kc, 0, 1, r)
+        cand = ~np.isnan(scores)
+        assert np.allclose(scores[cand], pooled[0, 1, r, : len(scores)][cand], rtol=0, atol=1e-12)
+        # the reported window gives exactly the block's score
+        f64, k64 = brute.bf16_bits_to_f64(f), brute.bf16_bits_to_f64(kc)
+        for j in np.flatnonzero(cand):
+            assert abs(float(f64[0, 1, r] @ k64[0, 1, wins[j]]) - scores[j]) <= 1e-12
+
+
+def test_select_pooled_closed_form_block_constant_keys(oracle_lib):
+    """Keys constant within each 64-token block: the windows inside block j equal K_j and the window
+    straddling j and j+1 is (K_j + K_{j+1}) / 2 (exact in bf16 for these values), so the pooled
+    score of block j is max(s_j, (s_{j-1} + s_j) / 2, (s_j + s_{j+1}) / 2) with s_j = F . K_j."""
+    T, D = 640, 2
+    s = oracle_lib.Shape(batch=1, n_kv_heads=1, group_size=1, head_dim=D, block_size=64, n_init=1, n_local=2,
+                         k_total=10, t_cap=T, nc_cap=(T - 32) // 16 + 1, cmp_kernel=32, cmp_stride=16)
+    to = lambda a: np.array(a, np.float32).view(np.uint32).__rshift__(16).astype(np.uint16)
+    blockv = [[0, 0], [1, 0], [3, 1], [-2, 0], [0, 2], [5, -1], [1, 1], [2, 2], [0, 0], [0, 0]]
+    k = to([[np.repeat(np.array(blockv, np.float32), 64, axis=0)]])
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    f = to([[[[1.0, 0.5]]]])
+    _, _, scores = oracle_lib.select_row(s, f, 1, T - 1, kc, 0, 0, 0)
+    sb = [1.0 * a + 0.5 * b for a, b in blockv]
+    for j in range(1, 8):  # candidates [1, 9 - 2] = [1, 7]
+        want = max(sb[j], (sb[j - 1] + sb[j]) / 2, (sb[j] + sb[j + 1]) / 2)
+        assert scores[j] == want, (j, scores[j], want)
+    assert np.isnan(scores[0]) and np.isnan(scores[8]) and np.isnan(scores[9])
+
+
+def test_select_pooled_window_visibility_at_the_local_edge(oracle_lib):
+    """With one local block the last candidate j = blk - 1 has a window reaching 16 tokens into the
+    query's own block; it counts only once those tokens exist (p >= 64 (j + 1) + 15)."""
+    T, D = 512, 2
+    s = oracle_lib.Shape(batch=1, n_kv_heads=1, group_size=1, head_dim=D, block_size=64, n_init=1, n_local=1,
+                         k_total=3, t_cap=T, nc_cap=(T - 32) // 16 + 1, cmp_kernel=32, cmp_stride=16)
+    to = lambda a: np.array(a, np.float32).view(np.uint32).__rshift__(16).astype(np.uint16)
+    kf = np.zeros((T, D), np.float32)
+    kf[4 * 64:4 * 64 + 16, 0] = 1.0   # block 4's first 16 keys: only windows 15 and 16 see them
+    k = to([[kf]])
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    f = to([[[[1.0, 0.0]]]])
+    # query in block 4: candidates [1, 3]; window 15 = tokens [240, 272) straddles blocks 3 and 4
+    for p, want in [(4 * 64 + 14, 0.0), (4 * 64 + 15, 0.5), (4 * 64 + 40, 0.5)]:
+        _, _, scores = oracle_lib.select_row(s, f, 1, p, kc, 0, 0, 0)
+        assert scores[3] == want, (p, scores[3])
+        assert scores[1] == 0.0 and scores[2] == 0.0
+
+
+def test_select_pooled_planted_recall_and_decode_equals_prefill(oracle_lib):
+    """Planted blocks carry the full shift in their inner windows, so the paper's grid still finds
+    them all; decode at position p selects what prefill row p selects."""
+    T = 4096
+    w = inputs.Workload("g", batch=1, seq_len=T, n_q=64, n_kv_heads=2, group_size=4, k_total=16, seed=77)
+    case = inputs.make_case(w)
+    s = grid_shape(oracle_lib, 1, 2, T, 16)
+    k = inputs.to_u16(case["k"])
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    f_last = inputs.to_u16(case["f"])[:, :, -1:]
+    sel, cnt = oracle_lib.forecast_select(s, f_last, 1, T - 1, kc)
+    for m in range(2):
+        chosen = set(sel[0, m, 0, : cnt[0, m, 0]].tolist())
+        planted = set(int(j) for j in case["plants"][0, m])
+        assert planted <= chosen, (planted - chosen)
+    f = inputs.to_u16(case["f"])
+    selp, cntp = oracle_lib.forecast_select(s, f, 64, T - 64, kc)
+    for r in (0, 17, 63):
+        seld, cntd = oracle_lib.forecast_select(s, np.ascontiguousarray(f[:, :, r:r + 1]), 1, T - 64 + r, kc)
+        assert np.array_equal(seld[:, :, 0], selp[:, :, r]) and np.array_equal(cntd[:, :, 0], cntp[:, :, r])
+
+
+def test_grid_shapes_outside_the_family_are_refused(oracle_lib):
+    import oracle
+    k = np.zeros((1, 1, 256, 128), np.uint16)
+    for lw, sw in [(128, 64), (32, 48), (48, 20), (16, 32)]:
+        s = grid_shape(oracle_lib, 1, 1, 256, 4, lw, sw)
+        with pytest.raises(oracle.OracleError) as e:
+            oracle_lib.compress_keys(s, k, 256, 0, 1)
+        assert e.value.rc == oracle.ERR_UNSUPPORTED
+
+
 def test_select_block_budget_from_paper(oracle_lib):
     """The paper's MiniCPM settings: 64-token blocks, 1 initial block, a 2048-token (32-block)
     local window and one overall budget of 96 blocks.  Read with k counting the forced blocks,
