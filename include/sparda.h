@@ -29,7 +29,8 @@
  *   - Ordering between streams (e.g. a gather on a side stream and the attention that reads its
  *     staging buffer) is the caller's: record an event after the gather and make the compute
  *     stream wait on it.
- *   - v1 limits: head_dim 128, block 64, compression window (64, 64) -- one key per block --,
+ *   - v1 limits: head_dim 128, block 64, compression grid (64, 64) -- one key per block -- or the
+ *     paper's (32, 16) (App. C),
  *     group_size 1..16, block indices < 32768.  Other values return SPARDA_ERR_UNSUPPORTED.
  *
  * Notation: B batch, Hkv KV heads (= Forecast heads = GQA groups), G query heads per group,
@@ -65,33 +66,35 @@ typedef struct sparda_shape {
   int32_t group_size;    /* G in 1..16: query heads per KV head (GQA group)                     */
   int32_t head_dim;      /* D: 128                                                              */
   int32_t block_size;    /* L: 64 tokens per block                                              */
-  int32_t cmp_kernel;    /* compression window length l_C: 64 (one key per block)              */
-  int32_t cmp_stride;    /* compression stride s_C: 64                                          */
+  int32_t cmp_kernel;    /* compression window length l_C: 64 (one key per block) or 32        */
+  int32_t cmp_stride;    /* compression stride s_C: 64, or 16 with l_C = 32                    */
   int32_t n_init;        /* initial blocks always attended (>= 0)                               */
   int32_t n_local;       /* local blocks always attended, the query's own block included (>= 1) */
   int32_t k_total;       /* attended-set size per query row, forced blocks included;            */
                          /* n_init + n_local <= k_total <= 32767                                */
   int64_t t_cap;         /* token capacity (T stride) of the K/V caches; a multiple of L        */
-  int64_t nc_cap;        /* block capacity (stride) of the K~ cache                             */
+  int64_t nc_cap;        /* window capacity (stride) of the K~ cache: compressed keys per row   */
 } sparda_shape;
 
 /* Workspace owners for sparda_workspace_size(). */
 enum sparda_op { SPARDA_OP_FORECAST_SELECT = 1, SPARDA_OP_SPARSE_ATTN = 2 };
 
 /*
- * sparda_compress_keys -- mean-pooled block keys (Sec. 3, Eq. 2 with l_C = s_C = L).
+ * sparda_compress_keys -- mean-pooled compressed keys (Sec. 3, Eq. 2): window i of the grid
+ * (l_C, s_C) holds the keys of tokens [i s_C, i s_C + l_C); with l_C = s_C = L window i is block i.
  *   k_cache  in : bf16 [B][Hkv][t_cap][D] device.
  *   t_ctx       : tokens currently valid in k_cache (t_ctx <= t_cap).
- *   blk_begin, blk_end : compress blocks j in [blk_begin, blk_end); every one must be complete,
- *                 i.e. blk_end * L <= t_ctx, and blk_end <= nc_cap.  In decode, call it with the
- *                 single block completed by the newest token (the incremental K~ update of
- *                 Alg. 2); blk_begin == blk_end is a no-op.
- *   k_cmp   out : bf16 [B][Hkv][nc_cap][D] device; only rows [blk_begin, blk_end) are written.
- *   K~_j = round_to_nearest_even_bf16( (1/L) * sum of the L keys of block j ), the sum being
+ *   win_begin, win_end : compress windows i in [win_begin, win_end); every one must be complete,
+ *                 i.e. (win_end - 1) s_C + l_C <= t_ctx, and win_end <= nc_cap.  In decode, call
+ *                 it with the windows completed by the newest tokens (the incremental K~ update
+ *                 of Alg. 2: one window per L tokens on the (64, 64) grid, one per 16 on
+ *                 (32, 16)); win_begin == win_end is a no-op.
+ *   k_cmp   out : bf16 [B][Hkv][nc_cap][D] device; only rows [win_begin, win_end) are written.
+ *   K~_i = round_to_nearest_even_bf16( (1/l_C) * sum of the l_C keys of window i ), the sum being
  *   exact for bf16 inputs (float64 accumulation), so the result does not depend on order.
  */
-int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t blk_begin,
-                         int32_t blk_end, void* k_cmp, hipStream_t stream);
+int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t win_begin,
+                         int32_t win_end, void* k_cmp, hipStream_t stream);
 
 /*
  * sparda_forecast_select -- attended block set of every query row (Sec. 4.1, Eq. 4; Eq. 1).
@@ -100,15 +103,18 @@ int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t
  *                l+1's K~ (Eq. 4); for layer 0 they are the current-layer Forecast.
  *   n_q        : rows per (batch, group), >= 1.  n_q == 1 is the decode form.
  *   q_pos0     : position of row 0; row r is at p = q_pos0 + r; p < t_cap.
- *   k_cmp  in  : bf16 [B][Hkv][nc_cap][D] device; blocks 0 .. blk(p_max) - n_local must be valid.
+ *   k_cmp  in  : bf16 [B][Hkv][nc_cap][D] device; every window that overlaps a candidate block
+ *                of the last row and is complete at its position must be valid and < nc_cap.
  *   sel    out : int16 [B][Hkv][n_q][k_total] device: ascending block indices, -1 padded.
  *   cnt    out : int16 [B][Hkv][n_q] device: valid entries of each row = min(k_total, blk(p)+1).
  *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_FORECAST_SELECT).
  * Per row: forced = blocks [0, n_init) U [blk(p) - n_local + 1, blk(p)] (clipped to >= 0);
- * candidates = [n_init, blk(p) - n_local]; each candidate j scores s_j = F_row . K~_j (float32
- * accumulation, no softmax, no scale); the k_total - |forced| best candidates by (score
- * descending, block index ascending) are added to the forced blocks.  All G query heads of a
- * group share the set.
+ * candidates = [n_init, blk(p) - n_local]; every window i scores F_row . K~_i (float32
+ * accumulation, no softmax, no scale) and candidate j scores s_j = the largest score of the windows
+ * that overlap block j and are complete at p (i s_C + l_C <= p + 1): the max-pool to block scores
+ * of the InfLLM-V2 selector (Sec. 3), the identity on the (64, 64) grid.  The k_total - |forced|
+ * best candidates by (score descending, block index ascending) are added to the forced blocks.
+ * All G query heads of a group share the set.
  */
 int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
                            const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,

@@ -37,6 +37,26 @@ __host__ __device__ inline RowGeom row_geom(int64_t p, int n_init, int n_local, 
   return g;
 }
 
+// The compressed-key grid (Sec. 3, Eq. 2): window i holds the mean of tokens [i s, i s + l).
+// A block's score is the largest score among the windows that overlap it and are complete at
+// the query's position (the max-pool of the InfLLM-V2 selector).  With l = s = 64 every block is
+// one window and the pool is the identity.
+struct WinGrid {
+  int32_t l, s;  // window length and stride, in tokens; l <= 64, s divides 64
+};
+
+// First and last window overlapping block j (the last one not yet clamped to visibility).
+__host__ __device__ inline int32_t grid_win_lo(const WinGrid& w, int32_t j) {
+  const int32_t t = j * 64 - w.l;
+  return t < 0 ? 0 : t / w.s + 1;
+}
+__host__ __device__ inline int32_t grid_win_hi(const WinGrid& w, int32_t j) { return ((j + 1) * 64 - 1) / w.s; }
+// Last window complete at position p (-1 if none).
+__host__ __device__ inline int32_t grid_win_vis(const WinGrid& w, int64_t p) {
+  return p + 1 >= w.l ? (int32_t)((p + 1 - w.l) / w.s) : -1;
+}
+__host__ __device__ inline bool grid_is_blocks(const WinGrid& w) { return w.l == 64 && w.s == 64; }
+
 struct SelectArgs {
   const uint16_t* f;
   const uint16_t* kc;
@@ -47,6 +67,7 @@ struct SelectArgs {
   int32_t batch, n_kv_heads, n_q;
   int64_t q_pos0, nc_cap;
   int32_t n_init, n_local, k_total;
+  WinGrid grid;        // compressed-key grid of kc (nc_cap counts its windows)
 };
 
 struct AttnArgs {
@@ -72,10 +93,18 @@ constexpr int kSelTileMaxCand = 512;
 constexpr int kDecodeMaxCand = 16384;
 
 hipError_t launch_compress(const uint16_t* k, uint16_t* kc, int32_t rows, int64_t t_cap, int64_t nc_cap,
-                           int32_t blk_begin, int32_t blk_end, hipStream_t stream);
+                           WinGrid grid, int32_t w_begin, int32_t w_end, hipStream_t stream);
+
+// Windows a row at position p scores: [first, last] (empty when last < first).
+__host__ __device__ inline void row_windows(const RowGeom& g, const WinGrid& w, int64_t p, int32_t* first,
+                                           int32_t* last) {
+  *first = grid_win_lo(w, g.cand_lo);
+  const int32_t hi = grid_win_hi(w, g.cand_lo + g.n_cand - 1), vis = grid_win_vis(w, p);
+  *last = g.n_cand > 0 ? (hi < vis ? hi : vis) : *first - 1;
+}
 
 // True when the call takes the row-wise path, which keeps its scores in workspace scratch.
-bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local);
+bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);

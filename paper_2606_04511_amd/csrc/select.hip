@@ -2,9 +2,11 @@
 // attended-set union of Eq. 1).
 //
 // Per query row at position p: forced = initial blocks U local window, candidates = the complete
-// blocks in between, score s_j = F_row . K~_j (one Forecast head per GQA group, no softmax, no
-// scale, float32 accumulation); the k_total - |forced| best candidates by (score desc, index asc)
-// join the forced blocks; the row's set is written in ascending block order, -1 padded.
+// blocks in between, window scores F_row . K~_i (one Forecast head per GQA group, no softmax, no
+// scale, float32 accumulation), block score s_j = the max over the windows that overlap block j
+// and are complete at p (the identity for the one-key-per-block grid); the k_total - |forced|
+// best candidates by (score desc, index asc) join the forced blocks; the row's set is written in
+// ascending block order, -1 padded.
 //
 // Two paths:
 //  * row-wise (decode, n_q == 1, and long multi-row cases): a bandwidth-bound GEMV kernel writes
@@ -99,28 +101,33 @@ __device__ void wave_topk_emit(KeyFn key_of, int n_cand, int n_take, int cand_lo
 
 // ---- row-wise path ----------------------------------------------------------------------
 
-// grid.x = row * n_chunks + chunk; a chunk is 256 candidates (64 per wavefront).  Lane l reads
-// dims 8*(l%16)..+7 of candidate 4 i + l/16: each wavefront load is 1 KiB contiguous of K~.
+// grid.x = row * n_chunks + chunk; a chunk is 256 windows (64 per wavefront).  Lane l reads dims
+// 8*(l%16)..+7 of window 4 i + l/16: each wavefront load is 1 KiB contiguous of K~.  Window
+// first + x of the row goes to scratch slot x.
 __global__ __launch_bounds__(256) void rowwise_score_kernel(SelectArgs a, int n_chunks) {
   const int64_t row = blockIdx.x / n_chunks;
   const int chunk = (int)(blockIdx.x % n_chunks);
   const int r = (int)(row % a.n_q);
   const int64_t bm = row / a.n_q;
-  const RowGeom g = row_geom(a.q_pos0 + r, a.n_init, a.n_local, a.k_total);
+  const int64_t p = a.q_pos0 + r;
+  const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
   if (g.n_take >= g.n_cand) return;
+  int32_t wf, wl;
+  row_windows(g, a.grid, p, &wf, &wl);
+  const int nw = wl - wf + 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, rs = lane >> 4;
   const int first = chunk * 256 + wave * 64;
-  if (first >= g.n_cand) return;
+  if (first >= nw) return;
   const uint4 fw = ld16(a.f + row * kHeadDim + c * 8);
   const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
   const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
-  const uint16_t* kbase = a.kc + (bm * a.nc_cap + g.cand_lo) * kHeadDim + c * 8;
+  const uint16_t* kbase = a.kc + (bm * a.nc_cap + wf) * kHeadDim + c * 8;
   uint4 kw[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int idx = first + 4 * i + rs;
-    kw[i] = idx < g.n_cand ? ld16(kbase + (int64_t)idx * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+    const int idx = min(first + 4 * i + rs, nw - 1);  // past the last window: a repeat, never stored
+    kw[i] = ld16(kbase + (int64_t)idx * kHeadDim);
   }
   float* out = a.ws + row * a.ws_stride;
 #pragma unroll
@@ -135,8 +142,18 @@ __global__ __launch_bounds__(256) void rowwise_score_kernel(SelectArgs a, int n_
     d = fmaf(f7, bf16hi(kw[i].w), d);
     d = row16_sum(d);
     const int idx = first + 4 * i + rs;
-    if (c == 0 && idx < g.n_cand) out[idx] = d;
+    if (c == 0 && idx < nw) out[idx] = d;
   }
+}
+
+// Max-pooled score of candidate i (block cand_lo + i) over the window scores w[0 .. ] of windows
+// wf, wf + 1, ...: the windows that overlap the block and are complete at the row's position.
+__device__ __forceinline__ float pooled_score(const float* w, const WinGrid& grid, int32_t j, int32_t wf,
+                                              int32_t wvis) {
+  const int32_t lo = grid_win_lo(grid, j), hi = min(grid_win_hi(grid, j), wvis);
+  float m = w[lo - wf];
+  for (int32_t i = lo + 1; i <= hi; ++i) m = fmaxf(m, w[i - wf]);
+  return m;
 }
 
 // One wavefront per row: forced blocks, padding, count, and the radix top-k over the scratch row.
@@ -151,8 +168,13 @@ __global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t
   emit_forced(out, g, a.k_total, lane);
   if (lane == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
   const float* sc = a.ws + row * a.ws_stride;
-  wave_topk_emit([&](int i) { return score_key(sc[i]); }, g.n_cand, g.n_take, g.cand_lo, hist[wave],
-                 out + g.init_hi);
+  const int64_t p = a.q_pos0 + r;
+  int32_t wf, wl;
+  row_windows(g, a.grid, p, &wf, &wl);
+  const int32_t wvis = grid_win_vis(a.grid, p);
+  const WinGrid grid = a.grid;
+  wave_topk_emit([&](int i) { return score_key(pooled_score(sc, grid, g.cand_lo + i, wf, wvis)); }, g.n_cand,
+                 g.n_take, g.cand_lo, hist[wave], out + g.init_hi);
 }
 
 // ---- fused decode path ---------------------------------------------------------------------
@@ -178,9 +200,10 @@ __device__ __forceinline__ int block_rank(bool flag, int* wave_cnt, int* total) 
   return before + mbcnt64(b);
 }
 
-// One workgroup per decode row (batch, group): the Forecast GEMV over all candidates into LDS,
-// then a block-wide radix select over the LDS scores and an ordered emission.  Scores never
-// leave the CU.
+// One workgroup per decode row (batch, group): the Forecast GEMV over all scored windows into LDS,
+// the max-pool of window scores to block scores (skipped for the one-key-per-block grid), then
+// a block-wide radix select over the block scores and an ordered emission.  Scores never leave
+// the CU.
 __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a) {
   __shared__ float sc[kDecodeMaxCand];
   __shared__ __align__(16) uint32_t hist[256];
@@ -200,29 +223,33 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
   }
   if (g.n_take <= 0) return;
 
-  // Scores: lane reads dims 8*(lane%16).. of candidate base + 4 i + lane/16 (1 KiB per load).
+  // Window scores: lane reads dims 8*(lane%16).. of window wf + base + 4 i + lane/16 (1 KiB per
+  // load) into sc[base + 4 i + lane/16].
+  int32_t wf, wl;
+  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
+  const int NW = wl - wf + 1;  // windows scored (C for the one-key-per-block grid)
   {
     const int c = lane & 15, rs = lane >> 4;
     const uint4 fw = ld16(a.f + row * kHeadDim + c * 8);
     const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
     const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
-    const uint16_t* kbase = a.kc + (row * a.nc_cap + g.cand_lo) * kHeadDim + c * 8;
-    // Double-buffered: the next 64 candidates' loads are in flight while this wave scores the
+    const uint16_t* kbase = a.kc + (row * a.nc_cap + wf) * kHeadDim + c * 8;
+    // Double-buffered: the next 64 windows' loads are in flight while this wave scores the
     // current ones.
     uint4 kw[16], kn[16];
-    // Indices past the last candidate read the last one again (never stored), so the loads
-    // stay branch-free.
+    // Indices past the last window read the last one again (never stored), so the loads stay
+    // branch-free.
     auto load = [&](int base, uint4 (&w)[16]) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int idx = min(base + 4 * i + rs, C - 1);
+        const int idx = min(base + 4 * i + rs, NW - 1);
         w[i] = ld16(kbase + (int64_t)idx * kHeadDim);
       }
     };
     int base = wave * 64;
-    if (base < C) load(base, kw);
-    for (; base < C; base += kDecThreads) {
-      if (base + kDecThreads < C) load(base + kDecThreads, kn);
+    if (base < NW) load(base, kw);
+    for (; base < NW; base += kDecThreads) {
+      if (base + kDecThreads < NW) load(base + kDecThreads, kn);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         float d = f0 * bf16lo(kw[i].x);
@@ -235,13 +262,27 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
         d = fmaf(f7, bf16hi(kw[i].w), d);
         d = row16_sum(d);
         const int idx = base + 4 * i + rs;
-        if (c == 0 && idx < C) sc[idx] = d;
+        if (c == 0 && idx < NW) sc[idx] = d;
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) kw[i] = kn[i];
     }
   }
   __syncthreads();
+  // Block scores: the window scores themselves, or their max-pool into sc[NW .. NW + C).
+  const float* bs = sc;
+  if (!grid_is_blocks(a.grid)) {
+    const int32_t wvis = grid_win_vis(a.grid, a.q_pos0);
+    for (int i = tid; i < C; i += kDecThreads) {
+      const int32_t j = g.cand_lo + i;
+      const int32_t lo = grid_win_lo(a.grid, j), hi = min(grid_win_hi(a.grid, j), wvis);
+      float m = sc[lo - wf];
+      for (int32_t w = lo + 1; w <= hi; ++w) m = fmaxf(m, sc[w - wf]);
+      sc[NW + i] = m;
+    }
+    bs = sc + NW;
+    __syncthreads();
+  }
 
   // Radix select of the n_take-th largest key, 8 bits per pass, over the whole workgroup.
   uint32_t prefix = 0u, mask = 0u;
@@ -252,7 +293,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
     if (tid < 256) hist[tid] = 0u;
     __syncthreads();
     for (int i = tid; i < C; i += kDecThreads) {
-      const uint32_t kk = score_key(sc[i]);
+      const uint32_t kk = score_key(bs[i]);
       if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
     }
     __syncthreads();
@@ -290,7 +331,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
   for (int i0 = 0; i0 < C; i0 += kDecThreads) {
     const int i = i0 + tid;
     const bool valid = i < C;
-    const uint32_t kk = valid ? score_key(sc[i]) : 0u;
+    const uint32_t kk = valid ? score_key(bs[i]) : 0u;
     bool chosen;
     if (take_all) {
       chosen = valid && (kk & mask) >= prefix;
@@ -311,27 +352,37 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
 // Which kernels serve a select call.
 enum SelectPath { kPathDecode, kPathTile, kPathRowwise };
 
-static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
-  const RowGeom g = row_geom(q_pos0 + n_q - 1, n_init, n_local, 1 << 30);
-  if (n_q == 1) return g.n_cand <= kDecodeMaxCand ? kPathDecode : kPathRowwise;
-  return g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
+static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  const int64_t p = q_pos0 + n_q - 1;
+  const RowGeom g = row_geom(p, n_init, n_local, 1 << 30);
+  int32_t wf, wl;
+  row_windows(g, grid, p, &wf, &wl);
+  const int64_t nw = wl >= wf ? wl - wf + 1 : 0;
+  if (n_q == 1) {  // window scores and (for a windowed grid) block scores share the LDS score array
+    const int64_t need = grid_is_blocks(grid) ? g.n_cand : nw + g.n_cand;
+    return need <= kDecodeMaxCand ? kPathDecode : kPathRowwise;
+  }
+  return grid_is_blocks(grid) && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
 }
 
-bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local) {
-  return select_path(n_q, q_pos0, n_init, n_local) == kPathRowwise;
+bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  return select_path(n_q, q_pos0, n_init, n_local, grid) == kPathRowwise;
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
-  const SelectPath path = select_path(a.n_q, a.q_pos0, a.n_init, a.n_local);
+  const SelectPath path = select_path(a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid);
   if (path == kPathDecode) {
     hipLaunchKernelGGL(decode_select_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (path == kPathTile) return launch_prefill_select(a, stream);
-  const RowGeom gl = row_geom(a.q_pos0 + a.n_q - 1, a.n_init, a.n_local, a.k_total);
-  if (gl.n_cand > 0) {
-    const int n_chunks = (gl.n_cand + 255) / 256;
+  const int64_t pl = a.q_pos0 + a.n_q - 1;
+  const RowGeom gl = row_geom(pl, a.n_init, a.n_local, a.k_total);
+  int32_t wf, wl;
+  row_windows(gl, a.grid, pl, &wf, &wl);
+  if (gl.n_cand > 0 && wl >= wf) {  // the last row scores the most windows
+    const int n_chunks = (wl - wf + 1 + 255) / 256;
     hipLaunchKernelGGL(rowwise_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

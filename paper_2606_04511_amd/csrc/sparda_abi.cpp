@@ -46,8 +46,9 @@ int check_shape(const sparda_shape* s) {
   if (s->group_size > 16) return fail(SPARDA_ERR_UNSUPPORTED, "group_size %d > 16", s->group_size);
   if (s->head_dim != 128) return fail(SPARDA_ERR_UNSUPPORTED, "head_dim %d (only 128)", s->head_dim);
   if (s->block_size != 64) return fail(SPARDA_ERR_UNSUPPORTED, "block_size %d (only 64)", s->block_size);
-  if (s->cmp_kernel != 64 || s->cmp_stride != 64)
-    return fail(SPARDA_ERR_UNSUPPORTED, "compression window (%d, %d) (only (64, 64))", s->cmp_kernel, s->cmp_stride);
+  if (!((s->cmp_kernel == 64 && s->cmp_stride == 64) || (s->cmp_kernel == 32 && s->cmp_stride == 16)))
+    return fail(SPARDA_ERR_UNSUPPORTED, "compression window (%d, %d) (only (64, 64) and (32, 16))", s->cmp_kernel,
+                s->cmp_stride);
   if (s->n_init < 0 || s->n_local < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_init >= 0 and n_local >= 1 required");
   if ((int64_t)s->k_total < (int64_t)s->n_init + s->n_local)
     return fail(SPARDA_ERR_INVALID_ARG, "k_total %d < n_init + n_local", s->k_total);
@@ -56,7 +57,8 @@ int check_shape(const sparda_shape* s) {
     return fail(SPARDA_ERR_INVALID_ARG, "t_cap %lld must be a positive multiple of 64", (long long)s->t_cap);
   if (s->t_cap / 64 > kMaxBlocks)
     return fail(SPARDA_ERR_UNSUPPORTED, "t_cap %lld exceeds 32768 blocks", (long long)s->t_cap);
-  if (s->nc_cap < 0 || s->nc_cap > kMaxBlocks) return fail(SPARDA_ERR_INVALID_ARG, "nc_cap out of range");
+  if (s->nc_cap < 0 || s->nc_cap > kMaxBlocks * (64 / s->cmp_stride))
+    return fail(SPARDA_ERR_INVALID_ARG, "nc_cap out of range");
   if ((int64_t)s->batch * s->n_kv_heads > 65535)
     return fail(SPARDA_ERR_UNSUPPORTED, "batch * n_kv_heads > 65535");
   return SPARDA_OK;
@@ -78,11 +80,18 @@ int check_rows(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
   return SPARDA_OK;
 }
 
-// Workspace of sparda_forecast_select: scores of the row-wise path (none for the fused kernels).
+sparda::WinGrid grid_of(const sparda_shape* s) { return sparda::WinGrid{s->cmp_kernel, s->cmp_stride}; }
+
+// Workspace of sparda_forecast_select: window scores of the row-wise path (none for the fused
+// kernels).  The last row scores the most windows.
 size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* stride) {
-  const sparda::RowGeom g = sparda::row_geom(q_pos0 + n_q - 1, s->n_init, s->n_local, s->k_total);
-  *stride = ((int64_t)g.n_cand + 3) & ~(int64_t)3;
-  if (!sparda::select_needs_scratch(n_q, q_pos0, s->n_init, s->n_local)) return 0;
+  const int64_t pl = q_pos0 + n_q - 1;
+  const sparda::RowGeom g = sparda::row_geom(pl, s->n_init, s->n_local, s->k_total);
+  int32_t wf, wl;
+  sparda::row_windows(g, grid_of(s), pl, &wf, &wl);
+  const int64_t nw = wl >= wf ? (int64_t)(wl - wf + 1) : 0;
+  *stride = (nw + 3) & ~(int64_t)3;
+  if (!sparda::select_needs_scratch(n_q, q_pos0, s->n_init, s->n_local, grid_of(s))) return 0;
   if (g.n_cand == 0) return 0;
   const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
   return (size_t)rows * (size_t)*stride * sizeof(float);
@@ -140,19 +149,20 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
   return ok();
 }
 
-int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t blk_begin,
-                         int32_t blk_end, void* k_cmp, hipStream_t stream) {
+int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t t_ctx, int32_t win_begin,
+                         int32_t win_end, void* k_cmp, hipStream_t stream) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_dev(k_cache, "k_cache", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16))) return rc;
   if (t_ctx < 0 || t_ctx > shape->t_cap) return fail(SPARDA_ERR_INVALID_ARG, "t_ctx outside [0, t_cap]");
-  if (blk_begin < 0 || blk_end < blk_begin) return fail(SPARDA_ERR_INVALID_ARG, "bad block range");
-  if ((int64_t)blk_end * 64 > t_ctx) return fail(SPARDA_ERR_INVALID_ARG, "block %d is not complete", blk_end - 1);
-  if (blk_end > shape->nc_cap) return fail(SPARDA_ERR_INVALID_ARG, "blk_end %d > nc_cap", blk_end);
-  if (blk_end == blk_begin) return ok();
+  if (win_begin < 0 || win_end < win_begin) return fail(SPARDA_ERR_INVALID_ARG, "bad window range");
+  if (win_end > shape->nc_cap) return fail(SPARDA_ERR_INVALID_ARG, "win_end %d > nc_cap", win_end);
+  if (win_end == win_begin) return ok();
+  if ((int64_t)(win_end - 1) * shape->cmp_stride + shape->cmp_kernel > t_ctx)
+    return fail(SPARDA_ERR_INVALID_ARG, "window %d is not complete", win_end - 1);
   return hip_status(sparda::launch_compress(static_cast<const uint16_t*>(k_cache), static_cast<uint16_t*>(k_cmp),
                                             shape->batch * shape->n_kv_heads, shape->t_cap, shape->nc_cap,
-                                            blk_begin, blk_end, stream),
+                                            grid_of(shape), win_begin, win_end, stream),
                     "compress launch");
 }
 
@@ -165,10 +175,13 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
       (rc = check_dev(cnt, "cnt", 2)))
     return rc;
   if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
-  const sparda::RowGeom gl = sparda::row_geom(q_pos0 + n_q - 1, shape->n_init, shape->n_local, shape->k_total);
-  if (gl.n_cand > 0 && (int64_t)gl.cand_lo + gl.n_cand > shape->nc_cap)
-    return fail(SPARDA_ERR_INVALID_ARG, "candidate block %d beyond nc_cap %lld", gl.cand_lo + gl.n_cand - 1,
-                (long long)shape->nc_cap);
+  const int64_t pl = q_pos0 + n_q - 1;
+  const sparda::RowGeom gl = sparda::row_geom(pl, shape->n_init, shape->n_local, shape->k_total);
+  int32_t wf, wl;
+  sparda::row_windows(gl, grid_of(shape), pl, &wf, &wl);
+  if (gl.n_cand > 0 && (int64_t)wl >= shape->nc_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "compressed key %d (for block %d) beyond nc_cap %lld", wl,
+                gl.cand_lo + gl.n_cand - 1, (long long)shape->nc_cap);
   int64_t stride = 0;
   const size_t need = select_ws(shape, n_q, q_pos0, &stride);
   if (need > 0) {
@@ -190,6 +203,7 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
   a.n_init = shape->n_init;
   a.n_local = shape->n_local;
   a.k_total = shape->k_total;
+  a.grid = grid_of(shape);
   return hip_status(sparda::launch_select(a, stream), "select launch");
 }
 

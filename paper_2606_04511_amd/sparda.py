@@ -140,9 +140,9 @@ def sparda_workspace_size(shape: SpardaShape, op: int, n_q: int, q_pos0: int) ->
     return int(n.value)
 
 
-def sparda_compress_keys(shape: SpardaShape, k_cache, t_ctx: int, blk_begin: int, blk_end: int, k_cmp, stream=None):
+def sparda_compress_keys(shape: SpardaShape, k_cache, t_ctx: int, win_begin: int, win_end: int, k_cmp, stream=None):
     cs = shape.c()
-    _check(load().sparda_compress_keys(ctypes.byref(cs), _p(k_cache), t_ctx, blk_begin, blk_end, _p(k_cmp),
+    _check(load().sparda_compress_keys(ctypes.byref(cs), _p(k_cache), t_ctx, win_begin, win_end, _p(k_cmp),
                                        _stream(stream)), "sparda_compress_keys")
 
 

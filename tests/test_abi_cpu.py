@@ -67,7 +67,8 @@ def rc_of(fn, *args):
 @pytest.mark.parametrize("kw,status", [
     (dict(head_dim=64), sp.SPARDA_ERR_UNSUPPORTED),
     (dict(block_size=32), sp.SPARDA_ERR_UNSUPPORTED),
-    (dict(cmp_kernel=32, cmp_stride=16), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(cmp_kernel=32, cmp_stride=32), sp.SPARDA_ERR_UNSUPPORTED),
+    (dict(cmp_kernel=16, cmp_stride=8), sp.SPARDA_ERR_UNSUPPORTED),
     (dict(group_size=17), sp.SPARDA_ERR_UNSUPPORTED),
     (dict(group_size=0), sp.SPARDA_ERR_INVALID_ARG),
     (dict(k_total=2), sp.SPARDA_ERR_INVALID_ARG),
@@ -113,6 +114,31 @@ def test_select_argument_errors(lib):
     need = sp.sparda_workspace_size(sl, sp.SPARDA_OP_FORECAST_SELECT, 2, 65534)
     assert need == 2 * 8 * 2 * 1024 * 4  # rows x stride(1021 -> 1024) x float
     assert rc_of(f, sl, FAKE, 2, 65534, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
+
+
+def test_paper_grid_arguments(lib):
+    """The (32, 16) grid: compress takes a window range, nc_cap counts windows, selection needs
+    every window that overlaps a candidate block of the last row."""
+    g = dict(cmp_kernel=32, cmp_stride=16)
+    s = shape(nc_cap=255, **g)  # windows of a 4096-token cache: (4096 - 32) / 16 + 1
+    c = sp.sparda_compress_keys
+    assert rc_of(c, s, FAKE, 4096, 0, 256, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG      # > nc_cap
+    assert rc_of(c, s, FAKE, 300, 0, 18, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG        # window 17 ends at 304
+    assert rc_of(c, s, FAKE, 4096, 5, 4, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG        # reversed range
+    c(s, FAKE, 4096, 7, 7, FAKE, 0)                                                   # empty: no-op
+    f = sp.sparda_forecast_select
+    # decode at p = 4095: candidates [1, 61]; block 61's last window is 4 * 61 + 3 = 247
+    assert rc_of(f, shape(nc_cap=247, **g), FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == \
+        sp.SPARDA_ERR_INVALID_ARG
+    assert sp.sparda_workspace_size(shape(nc_cap=248, **g), sp.SPARDA_OP_FORECAST_SELECT, 1, 4095) == 0  # fused
+    # multi-row calls on the windowed grid take the row-wise path: windows 3 .. 247 of the last row
+    need = sp.sparda_workspace_size(shape(nc_cap=255, **g), sp.SPARDA_OP_FORECAST_SELECT, 64, 4032)
+    assert need == 2 * 8 * 64 * 248 * 4  # rows x stride(245 -> 248) x float
+    assert rc_of(f, shape(nc_cap=255, **g), FAKE, 64, 4032, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == \
+        sp.SPARDA_ERR_WORKSPACE
+    # nc_cap may count up to four windows per block on this grid
+    assert sp.sparda_workspace_size(shape(t_cap=131072, nc_cap=8191, batch=32, k_total=64, **g),
+                                    sp.SPARDA_OP_FORECAST_SELECT, 1, 131071) == 0
 
 
 def test_attention_argument_errors(lib):

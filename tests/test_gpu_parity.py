@@ -34,11 +34,11 @@ def say(*a):
     sys.stdout.flush()
 
 
-def shapes(B, H, G, k_total, t_cap, nc_cap, n_init=1, n_local=2):
+def shapes(B, H, G, k_total, t_cap, nc_cap, n_init=1, n_local=2, lw=64, sw=64):
     s = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=G, k_total=k_total, t_cap=t_cap, nc_cap=nc_cap,
-                       n_init=n_init, n_local=n_local)
+                       n_init=n_init, n_local=n_local, cmp_kernel=lw, cmp_stride=sw)
     o = oracle.Shape(batch=B, n_kv_heads=H, group_size=G, k_total=k_total, t_cap=t_cap, nc_cap=nc_cap,
-                     n_init=n_init, n_local=n_local)
+                     n_init=n_init, n_local=n_local, cmp_kernel=lw, cmp_stride=sw)
     return s, o
 
 
@@ -457,3 +457,92 @@ def test_select_exact_ties_take_lowest_index(dev, T, n_q, k_total):
     ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
     assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
     assert np.array_equal(sel.cpu().numpy(), ref_sel)
+
+
+# ----------------------------------------------------------------------------- the paper's (32, 16) grid
+
+def n_windows(T, lw=32, sw=16):
+    return (T - lw) // sw + 1
+
+
+@pytest.mark.parametrize("B,H,T,t_cap", [(1, 8, 4096, 4096), (2, 2, 1000, 1024), (2, 3, 8192, 8192)])
+def test_grid_compress_bitwise(dev, B, H, T, t_cap):
+    say(f"grid compress B{B} H{H} T{T}")
+    w, case = make(B, H, 4, T, 1, 16, 5100 + T, t_cap=t_cap)
+    nw = n_windows(T)
+    s, o = shapes(B, H, 4, 16, t_cap, nw, lw=32, sw=16)
+    ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nw)
+    got = gpu_compress(s, case["k"].to(dev), T, nw, nw, dev)
+    assert np.array_equal(inputs.to_u16(got), ref)
+    # incremental: the windows completed by each new 16 tokens, as a decode loop would
+    inc = torch.zeros_like(got)
+    done = 0
+    for t in range(16, T + 1, 16 * 7):
+        n_now = n_windows(t) if t >= 32 else 0
+        if n_now > done:
+            sp.sparda_compress_keys(s, case["k"].to(dev), t, done, n_now, inc)
+            done = n_now
+    if nw > done:
+        sp.sparda_compress_keys(s, case["k"].to(dev), T, done, nw, inc)
+    torch.cuda.synchronize()
+    assert torch.equal(inc, got)
+
+
+GRID_DECODE = [
+    # B, H, T, k_total, n_init, n_local
+    (1, 8, 4096, 16, 1, 2),
+    (2, 2, 32768, 64, 1, 2),
+    (1, 2, 5000, 16, 0, 3),
+    (2, 2, 8200, 24, 1, 1),  # one local block: the last candidate's edge window is still open (p % 64 = 7)
+    (2, 1, 8255, 24, 1, 1),  # ... and complete (p % 64 = 62)
+    (1, 2, 131072, 64, 1, 2),
+]
+
+
+@pytest.mark.parametrize("B,H,T,k_total,n_init,n_local", GRID_DECODE)
+def test_grid_decode_select(dev, B, H, T, k_total, n_init, n_local):
+    say(f"grid decode select B{B} H{H} T{T} k{k_total} init {n_init} local {n_local}")
+    w, case = make(B, H, 4, T, 1, k_total, 5200 + T, n_init=n_init, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nw = n_windows(T)
+    s, o = shapes(B, H, 4, k_total, t_cap, nw, n_init, n_local, lw=32, sw=16)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nw)
+    sel, cnt = gpu_select(s, case["f"].to(dev), 1, T - 1, inputs.from_u16(kc_ref, dev), dev)
+    rows = [(b, m, 0) for b in range(B) for m in range(H)]
+    n, swaps = compare_selection(o, inputs.to_u16(case["f"]), kc_ref, 1, T - 1, sel.cpu().numpy(),
+                                 cnt.cpu().numpy(), rows)
+    say(f"  rows {n}, tie swaps {swaps}")
+    if T >= 4096 and n_local == 2:
+        sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+        for b in range(B):
+            for m in range(H):
+                chosen = set(sel_np[b, m, 0, : cnt_np[b, m, 0]].tolist())
+                planted = set(int(j) for j in case["plants"][b, m])
+                n_sel = k_total - n_init - n_local
+                if len(planted) <= n_sel:
+                    assert planted <= chosen, "every planted block is selected on the paper's grid too"
+
+
+GRID_PREFILL = [
+    # B, H, T, n_q, q_pos0, k_total, n_local  (multi-row calls on the windowed grid: row-wise path)
+    (1, 2, 4096, 4096, 0, 16, 2),
+    (2, 1, 3000, 700, 2300, 12, 2),
+    (1, 2, 6000, 333, 5601, 20, 1),
+]
+
+
+@pytest.mark.parametrize("B,H,T,n_q,q_pos0,k_total,n_local", GRID_PREFILL)
+def test_grid_prefill_select(dev, B, H, T, n_q, q_pos0, k_total, n_local):
+    say(f"grid prefill select B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} k{k_total} local {n_local}")
+    w, case = make(B, H, 4, T, n_q, k_total, 5300 + T, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nw = n_windows(T)
+    s, o = shapes(B, H, 4, k_total, t_cap, nw, 1, n_local, lw=32, sw=16)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nw)
+    f_u16 = inputs.to_u16(case["f"])
+    sel, cnt = gpu_select(s, case["f"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
+    rng = np.random.default_rng(2)
+    rr = sorted(set(rng.integers(0, n_q, size=min(n_q, 400)).tolist()) | {0, n_q - 1})
+    rows = [(b, m, r) for b in range(B) for m in range(H) for r in rr]
+    n, swaps = compare_selection(o, f_u16, kc_ref, n_q, q_pos0, sel.cpu().numpy(), cnt.cpu().numpy(), rows)
+    say(f"  rows {n}, tie swaps {swaps}")
