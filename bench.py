@@ -8,6 +8,8 @@ head_dim 128, 64-token blocks, k = 64 blocks (1 initial + 2 local forced):
 value = algorithmic HBM bytes of the step / step time (GB/s); ms_per_step is the layer time.
 
 Secondary legs on the same JSON line:
+  paper_grid     -- the same decode layer with K~ on the paper's (32, 16) grid (8191 windows per
+                    row, max-pooled to block scores inside the select);
   prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
                     selects), reported in TFLOP/s of scored (row, candidate) pairs x 2 x 128;
   prefill_attn   -- block-sparse attention of that prefill (ms);
@@ -56,29 +58,34 @@ class DecodeLayer:
     selection and the attention, with the compressed keys precomputed (the workload's
     definition); the one-block K~ refresh a decode step also performs is timed beside it."""
 
-    def __init__(self, w: inputs.Workload, dev):
+    def __init__(self, w: inputs.Workload, dev, grid=(64, 64), case=None):
         self.w = w
         T, nb = w.seq_len, w.n_blocks
         self.T, self.nb = T, nb
+        self.grid = grid
+        lw, sw = grid
+        self.nw = (T - lw) // sw + 1  # compressed keys complete at T (one per block on the (64, 64) grid)
         self.shape = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size,
-                                    k_total=w.k_total, t_cap=T, nc_cap=nb, n_init=w.n_init, n_local=w.n_local)
-        t0 = time.time()
-        self.case = inputs.make_case(w, device=dev)
-        log(f"[bench] generated {w.name} on the GPU in {time.time() - t0:.1f}s")
-        c = self.case
+                                    k_total=w.k_total, t_cap=T, nc_cap=self.nw, n_init=w.n_init, n_local=w.n_local,
+                                    cmp_kernel=lw, cmp_stride=sw)
+        if case is None:
+            t0 = time.time()
+            case = inputs.make_case(w, device=dev)
+            log(f"[bench] generated {w.name} on the GPU in {time.time() - t0:.1f}s")
+        self.case = c = case
         self.q, self.f, self.k, self.v = c["q"], c["f"], c["k"], c["v"]
-        self.kc = torch.zeros(w.batch, w.n_kv_heads, nb, 128, dtype=torch.bfloat16, device=dev)
+        self.kc = torch.zeros(w.batch, w.n_kv_heads, self.nw, 128, dtype=torch.bfloat16, device=dev)
         self.sel = torch.empty(w.batch, w.n_kv_heads, 1, w.k_total, dtype=torch.int16, device=dev)
         self.cnt = torch.empty(w.batch, w.n_kv_heads, 1, dtype=torch.int16, device=dev)
         self.o = torch.empty(w.batch, w.n_q_heads, 1, 128, dtype=torch.bfloat16, device=dev)
         self.ws_sel = ws_tensor(self.shape, sp.SPARDA_OP_FORECAST_SELECT, 1, T - 1, dev)
         self.ws_att = ws_tensor(self.shape, sp.SPARDA_OP_SPARSE_ATTN, 1, T - 1, dev)
-        # K~ of every complete block is precomputed (not timed); the step refreshes the newest one.
-        sp.sparda_compress_keys(self.shape, self.k, T, 0, nb, self.kc)
+        # K~ of every complete window is precomputed (not timed); the step refreshes the newest one.
+        sp.sparda_compress_keys(self.shape, self.k, T, 0, self.nw, self.kc)
         torch.cuda.synchronize()
 
     def compress_new(self):
-        sp.sparda_compress_keys(self.shape, self.k, self.T, self.nb - 1, self.nb, self.kc)
+        sp.sparda_compress_keys(self.shape, self.k, self.T, self.nw - 1, self.nw, self.kc)
 
     def select(self):
         sp.sparda_forecast_select(self.shape, self.f, 1, self.T - 1, self.kc, self.sel, self.cnt, self.ws_sel)
@@ -97,13 +104,20 @@ class DecodeLayer:
         self.attend()
 
     def bytes(self):
-        """Algorithmic HBM bytes of the step's parts (compress_new is the separate K~ refresh)."""
+        """Algorithmic HBM bytes of the step's parts (compress_new is the separate K~ refresh).
+        The select reads every compressed key that overlaps a candidate block and is complete at
+        the query: the candidate blocks themselves on the (64, 64) grid, about four windows per
+        block on the (32, 16) one."""
         w = self.w
+        lw, sw = self.grid
         rows = w.batch * w.n_kv_heads
-        n_cand = self.nb - 1 - w.n_local - w.n_init + 1  # candidates of the decode row
+        cand_lo, cand_hi = w.n_init, self.nb - 1 - w.n_local  # candidates of the decode row
+        first = 0 if cand_lo * 64 - lw < 0 else (cand_lo * 64 - lw) // sw + 1
+        last = min(((cand_hi + 1) * 64 - 1) // sw, (self.T - lw) // sw)
+        n_keys = last - first + 1
         return {
-            "compress_new": rows * (64 * 256 + 256),
-            "select": rows * (256 + n_cand * 256 + w.k_total * 2 + 2),
+            "compress_new": rows * (lw * 256 + 256),
+            "select": rows * (256 + n_keys * 256 + w.k_total * 2 + 2),
             "attend": rows * (w.k_total * 2 * 64 * 256 + w.k_total * 2 + 2) + 2 * w.batch * w.n_q_heads * 256,
         }
 
@@ -164,6 +178,22 @@ def prefill_leg(dev, warmup, iters):
     ms_sel = time_events(select, iters, stream)
     attend()
     ms_att = time_events(attend, max(2, iters // 10), stream)
+
+    # the same selection on the paper's (32, 16) key grid (row-wise path: window scores in the
+    # workspace, max-pooled to block scores by the top-k kernel)
+    nw = (T - 32) // 16 + 1
+    shape_g = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size, k_total=w.k_total,
+                             t_cap=T, nc_cap=nw, n_init=w.n_init, n_local=w.n_local, cmp_kernel=32, cmp_stride=16)
+    kc_g = torch.zeros(w.batch, w.n_kv_heads, nw, 128, dtype=torch.bfloat16, device=dev)
+    sp.sparda_compress_keys(shape_g, case["k"], T, 0, nw, kc_g)
+    ws_g = ws_tensor(shape_g, sp.SPARDA_OP_FORECAST_SELECT, T, 0, dev)
+
+    def select_grid():
+        sp.sparda_forecast_select(shape_g, case["f"], T, 0, kc_g, sel, cnt, ws_g)
+
+    select_grid()
+    ms_sel_g = time_events(select_grid, max(2, iters // 5), stream)
+    del kc_g, ws_g
     # scored (row, candidate) pairs: rows whose candidates outnumber their free slots
     flops = 0
     attn_flops = 0
@@ -185,7 +215,38 @@ def prefill_leg(dev, warmup, iters):
         "select_gflop": flops / 1e9,
         "attn_ms": ms_att,
         "attn_tflops": attn_flops / (ms_att * 1e-3) / 1e12,
+        "select_grid_32_16_ms": ms_sel_g,
     }
+
+
+def grid_leg(base: DecodeLayer, dev, warmup, steps, stream):
+    """The same decode layer with compressed keys on the paper's (32, 16) grid (windows of 32
+    tokens at stride 16, max-pooled to block scores): select + attention, same K/V/Q/F."""
+    g = DecodeLayer(base.w, dev, grid=(32, 16), case=base.case)
+    for _ in range(warmup):
+        g.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    ms_sel = time_events(g.select, steps, stream)
+    ms_att = time_events(g.attend, steps, stream)
+    ms_cmp = time_events(g.compress_new, steps, stream)
+    parts = g.bytes()
+    step_bytes = parts["select"] + parts["attend"]
+    res = {
+        "workload": "decode layer B32 T=131072 Hq32/Hkv8 D128 block64 k64, K~ on the (32, 16) grid "
+                    f"({g.nw} windows per row)",
+        "us_per_layer": ms_step * 1e3,
+        "GBps": step_bytes / (ms_step * 1e-3) / 1e9,
+        "step_bytes": step_bytes,
+        "parts_us": {"compress_new": ms_cmp * 1e3, "select": ms_sel * 1e3, "attend": ms_att * 1e3},
+        "select_GBps": parts["select"] / (ms_sel * 1e-3) / 1e9,
+    }
+    g.kc = g.ws_sel = None
+    return res
 
 
 def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
@@ -380,6 +441,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the offloaded 32-layer decode pipeline (it pins 4 x 17.2 GB of host memory)")
+    ap.add_argument("--no-grid", action="store_true", help="skip the decode layer on the (32, 16) key grid")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -462,6 +524,10 @@ def main():
         "peaks": peaks,
         "frac_measured_read_peak": step_bytes / (ms_step * 1e-3) / 1e9 / peaks["hbm_block_read_GBps"],
     }
+    if not args.no_grid:
+        out["paper_grid"] = grid_leg(layer, dev, args.warmup, args.steps, stream)
+        log(f"[bench] (32, 16) grid decode step {out['paper_grid']['us_per_layer']:.1f} us, "
+            f"select {out['paper_grid']['parts_us']['select']:.1f} us")
     if not args.no_prefill:
         layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
@@ -470,7 +536,8 @@ def main():
         out["prefill"]["select_frac_measured_16x16x32_rate"] = (out["prefill"]["select_tflops"]
                                                                 / peaks["mfma_bf16_16x16x32_TFLOPs"])
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
-            f"{out['prefill']['select_tflops']:.1f} TFLOP/s")
+            f"{out['prefill']['select_tflops']:.1f} TFLOP/s; on the (32, 16) grid "
+            f"{out['prefill']['select_grid_32_16_ms'] * 1e3:.1f} us")
     if not args.no_pipeline:
         layer.case = None
         out["pipeline"] = pipeline_leg(dev, 4)
