@@ -362,7 +362,9 @@ static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32
     const int64_t need = grid_is_blocks(grid) ? g.n_cand : nw + g.n_cand;
     return need <= kDecodeMaxCand ? kPathDecode : kPathRowwise;
   }
-  return grid_is_blocks(grid) && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
+  // multi-row: the fused tile kernel serves both grids up to kSelTileMaxCand candidates per row
+  const bool tile_grid = grid_is_blocks(grid) || (grid.l == 32 && grid.s == 16);
+  return tile_grid && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
 }
 
 bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {

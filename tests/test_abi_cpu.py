@@ -131,11 +131,14 @@ def test_paper_grid_arguments(lib):
     assert rc_of(f, shape(nc_cap=247, **g), FAKE, 1, 4095, FAKE, FAKE, FAKE, None, 0, 0) == \
         sp.SPARDA_ERR_INVALID_ARG
     assert sp.sparda_workspace_size(shape(nc_cap=248, **g), sp.SPARDA_OP_FORECAST_SELECT, 1, 4095) == 0  # fused
-    # multi-row calls on the windowed grid take the row-wise path: windows 3 .. 247 of the last row
-    need = sp.sparda_workspace_size(shape(nc_cap=255, **g), sp.SPARDA_OP_FORECAST_SELECT, 64, 4032)
-    assert need == 2 * 8 * 64 * 248 * 4  # rows x stride(245 -> 248) x float
-    assert rc_of(f, shape(nc_cap=255, **g), FAKE, 64, 4032, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == \
-        sp.SPARDA_ERR_WORKSPACE
+    # multi-row calls with at most 512 candidates per row take the fused tile kernel: no workspace
+    assert sp.sparda_workspace_size(shape(nc_cap=255, **g), sp.SPARDA_OP_FORECAST_SELECT, 64, 4032) == 0
+    # more candidates take the row-wise path: the last row (p = 40959, candidates [1, 637]) scores
+    # windows 3 .. 2551
+    big = shape(t_cap=65536, nc_cap=4095, **g)
+    need = sp.sparda_workspace_size(big, sp.SPARDA_OP_FORECAST_SELECT, 64, 40896)
+    assert need == 2 * 8 * 64 * 2552 * 4  # rows x stride(2549 -> 2552) x float
+    assert rc_of(f, big, FAKE, 64, 40896, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
     # nc_cap may count up to four windows per block on this grid
     assert sp.sparda_workspace_size(shape(t_cap=131072, nc_cap=8191, batch=32, k_total=64, **g),
                                     sp.SPARDA_OP_FORECAST_SELECT, 1, 131071) == 0

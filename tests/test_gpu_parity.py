@@ -524,20 +524,24 @@ def test_grid_decode_select(dev, B, H, T, k_total, n_init, n_local):
 
 
 GRID_PREFILL = [
-    # B, H, T, n_q, q_pos0, k_total, n_local  (multi-row calls on the windowed grid: row-wise path)
-    (1, 2, 4096, 4096, 0, 16, 2),
-    (2, 1, 3000, 700, 2300, 12, 2),
-    (1, 2, 6000, 333, 5601, 20, 1),
+    # B, H, T, n_q, q_pos0, k_total, n_local, n_init
+    (1, 2, 4096, 4096, 0, 16, 2, 1),        # fused tile kernel, sets staged in LDS
+    (2, 1, 3000, 700, 2300, 12, 2, 1),      # chunk off a block boundary, ragged last slice
+    (1, 2, 6000, 333, 5601, 20, 1, 1),      # one local block: edge windows hidden until complete
+    (1, 1, 5000, 1000, 4000, 16, 1, 0),     # no initial block: block 0 has no window 4b - 1
+    (1, 2, 8192, 2000, 6192, 96, 2, 1),     # sets longer than 64 entries: written straight out
+    (1, 2, 32960, 500, 32460, 64, 2, 1),    # the last row has 512 candidates: the tile kernel's maximum
+    (1, 2, 36000, 200, 35800, 64, 2, 1),    # more candidates: the row-wise path
 ]
 
 
-@pytest.mark.parametrize("B,H,T,n_q,q_pos0,k_total,n_local", GRID_PREFILL)
-def test_grid_prefill_select(dev, B, H, T, n_q, q_pos0, k_total, n_local):
-    say(f"grid prefill select B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} k{k_total} local {n_local}")
-    w, case = make(B, H, 4, T, n_q, k_total, 5300 + T, n_local=n_local)
+@pytest.mark.parametrize("B,H,T,n_q,q_pos0,k_total,n_local,n_init", GRID_PREFILL)
+def test_grid_prefill_select(dev, B, H, T, n_q, q_pos0, k_total, n_local, n_init):
+    say(f"grid prefill select B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} k{k_total} local {n_local} init {n_init}")
+    w, case = make(B, H, 4, T, n_q, k_total, 5300 + T, n_init=n_init, n_local=n_local)
     t_cap = -(-T // 64) * 64
     nw = n_windows(T)
-    s, o = shapes(B, H, 4, k_total, t_cap, nw, 1, n_local, lw=32, sw=16)
+    s, o = shapes(B, H, 4, k_total, t_cap, nw, n_init, n_local, lw=32, sw=16)
     kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nw)
     f_u16 = inputs.to_u16(case["f"])
     sel, cnt = gpu_select(s, case["f"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
@@ -546,3 +550,52 @@ def test_grid_prefill_select(dev, B, H, T, n_q, q_pos0, k_total, n_local):
     rows = [(b, m, r) for b in range(B) for m in range(H) for r in rr]
     n, swaps = compare_selection(o, f_u16, kc_ref, n_q, q_pos0, sel.cpu().numpy(), cnt.cpu().numpy(), rows)
     say(f"  rows {n}, tie swaps {swaps}")
+
+
+def test_grid_prefill_full_t32k_samples(dev):
+    """The 32K prefill on the (32, 16) grid, all rows selected by the fused kernel; sampled rows
+    of three groups against the oracle."""
+    w = inputs.WORKLOADS["prefill_b1_t32k"]
+    T = w.seq_len
+    nw = n_windows(T)
+    say("full workload prefill_b1_t32k on the (32, 16) grid: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, _ = shapes(w.batch, w.n_kv_heads, w.group_size, w.k_total, T, nw, lw=32, sw=16)
+    kc = gpu_compress(s, case["k"], T, nw, nw, dev)
+    sel, cnt = gpu_select(s, case["f"], T, 0, kc, dev)
+    rng = np.random.default_rng(19)
+    ms = [int(x) for x in rng.integers(0, w.n_kv_heads, size=3)]
+    rows_r = sorted(set(int(x) for x in rng.integers(0, T, size=40)) | {0, 63, 64, 4095, 4096, 4160, T - 1})
+    _, o1 = shapes(1, 1, w.group_size, w.k_total, T, nw, lw=32, sw=16)
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    swaps = 0
+    for m in ms:
+        kc_ref = oracle.compress_keys(o1, inputs.to_u16(case["k"][0:1, m:m + 1]), T, 0, nw)
+        assert np.array_equal(inputs.to_u16(kc[0:1, m:m + 1]), kc_ref)
+        f16 = inputs.to_u16(case["f"][0:1, m:m + 1])
+        _, sw = compare_selection(o1, f16, kc_ref, T, 0, sel_np[0:1, m:m + 1], cnt_np[0:1, m:m + 1],
+                                  [(0, 0, r) for r in rows_r])
+        swaps += sw
+    say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}")
+
+
+@pytest.mark.parametrize("T,n_q,k_total,n_local", [(8192, 1024, 16, 2), (20000, 700, 64, 1), (20000, 1, 64, 2)])
+def test_grid_select_exact_ties_take_lowest_index(dev, T, n_q, k_total, n_local):
+    """Integer F and window keys: every window score, and so every pooled block score, is an exact
+    integer on both sides, and duplicated windows make many blocks tie; the GPU must take the
+    lower block index exactly as the oracle, in the fused prefill kernel and in decode."""
+    say(f"grid exact ties T{T} n_q{n_q} k{k_total} local {n_local}")
+    B, H = 1, 2
+    nw = n_windows(T)
+    t_cap = -(-T // 64) * 64
+    s, o = shapes(B, H, 4, k_total, t_cap, nw, 1, n_local, lw=32, sw=16)
+    g = torch.Generator().manual_seed(T + n_q + 7)
+    f = torch.randint(-1, 2, (B, H, n_q, 128), generator=g).to(torch.bfloat16)
+    kc = torch.randint(-1, 2, (B, H, nw, 128), generator=g).to(torch.bfloat16)
+    m8 = nw // 8
+    kc[:, :, 0:8 * m8:8] = kc[:, :, 4:8 * m8:8]  # window 8i equals window 8i + 4: blocks 2i and 2i + 1 tie often
+    q_pos0 = T - n_q
+    sel, cnt = gpu_select(s, f.to(dev), n_q, q_pos0, kc.to(dev), dev)
+    ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(sel.cpu().numpy(), ref_sel)
