@@ -297,7 +297,9 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
     const int s_next = grab();
-    load_f(s_next, fnext);
+    // On the window grid the next slice's F rows are requested after the scoring, whose A
+    // read-ahead needs the registers.
+    if (!kWin) load_f(s_next, fnext);
     // The previous slice's sets leave LDS now: these stores are long complete when the next
     // slice waits for the F rows requested just above.
     if (kStaged && s_prev >= 0) {
@@ -325,7 +327,10 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     const int64_t p_first = a.q_pos0 + (int64_t)s * kPsRows;
     s_prev = s;
     s = s_next;
-    if (gs.n_take >= gs.n_cand) continue;  // the slice's last row takes every candidate: all rows do
+    if (gs.n_take >= gs.n_cand) {  // the slice's last row takes every candidate: all rows do
+      if (kWin) load_f(s, fnext);
+      continue;
+    }
 
     // ---- scores: S^T = K~ F^T, one M-tile of 16 candidates at a time
     const int C = gs.n_cand;
@@ -358,17 +363,14 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
         // windows reach past its first row's last complete window has any (n_local = 1).
         const bool need_vis = grid_win_hi(a.grid, gs.cand_lo + C - 1) > grid_win_vis(a.grid, p_first);
         const int vis = need_vis ? grid_win_vis(a.grid, a.q_pos0 + r) : 0x7fffffff;
-        uint4 aw[3][4];  // window-tile u lives in aw[(u + 1) % 3]
-        {
-          const uint16_t* p0 = arow(-1);
-          const uint16_t* p1 = arow(0);
-          const uint16_t* p2 = arow(1);
+        constexpr int kAhead = 3;  // window-tiles of read-ahead
+        constexpr int kNb = kAhead + 1;
+        uint4 aw[kNb][4];  // window-tile u lives in aw[(u + 1) % kNb]
 #pragma unroll
-          for (int ks = 0; ks < 4; ++ks) aw[0][ks] = ld16(p0 + 32 * ks);
+        for (int b = 0; b < kNb; ++b) {
+          const uint16_t* pb = arow(b - 1);
 #pragma unroll
-          for (int ks = 0; ks < 4; ++ks) aw[1][ks] = ld16(p1 + 32 * ks);
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) aw[2][ks] = ld16(p2 + 32 * ks);
+          for (int ks = 0; ks < 4; ++ks) aw[b][ks] = ld16(pb + 32 * ks);
         }
         float carry;  // window 4b - 1 of the next block: the previous tile's last window
         {
@@ -383,12 +385,12 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int u = 4 * mt + i;
-              const uint16_t* pn = arow(u + 2);
+              const uint16_t* pn = arow(u + kAhead);
 #pragma unroll
-              for (int ks = 0; ks < 4; ++ks) aw[(u + 3) % 3][ks] = ld16(pn + 32 * ks);
+              for (int ks = 0; ks < 4; ++ks) aw[u % kNb][ks] = ld16(pn + 32 * ks);
               f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-              for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[(u + 1) % 3][ks]), fb[ks], c);
+              for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[(u + 1) % kNb][ks]), fb[ks], c);
               // window 4 (bo + u) + e is visible iff it is <= vis: all-ones mask selects -inf
               const int d = vis - 4 * (bo + u);
 #pragma unroll
@@ -441,6 +443,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
         }
       }
     }
+    if (kWin) load_f(s, fnext);  // s is already the next slice
 
     // ---- exact n-th largest per row
     // Mean and variance of a sample: the first 16 slots of each of the row's lanes.
@@ -684,7 +687,7 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const bool win = !grid_is_blocks(a.grid);
   if (win && !(a.grid.l == 32 && a.grid.s == 16)) return hipErrorInvalidValue;
   PrefillPlan plan;
-  plan_units(a, units, win ? 2 : 1, &plan);
+  plan_units(a, units, win ? 3 : 1, &plan);
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
   if (win && staged)
