@@ -9,6 +9,8 @@ Function map (paper sections in the C file):
   compress_keys  -- Eq. 2 (mean-pooled compressed keys over windows of l_C tokens at stride s_C)
   select_row / forecast_select -- Eq. 1 + Eq. 4 (forced init/local blocks U top-k of the
                     max-pooled Forecast block scores)
+  multihead_select_row / multihead_select -- the InfLLM-V2 selector SparDA replaces (Sec. 3):
+                    per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
 """
@@ -93,11 +95,13 @@ def open_library(path: str):
     lib.sparda_ref_compress_keys.argtypes = [S, P, i64, i32, i32, P]
     lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P, P]
     lib.sparda_ref_forecast_select.argtypes = [S, P, i32, i64, P, P, P]
+    lib.sparda_ref_multihead_select_row.argtypes = [S, P, i32, i64, P, f64, i32, i32, i32, P, P, P, P]
+    lib.sparda_ref_multihead_select.argtypes = [S, P, i32, i64, P, f64, P, P]
     lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
     lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
-    for name in ("compress_keys", "select_row", "forecast_select", "attend_row", "sparse_attn",
-                 "gather_blocks"):
+    for name in ("compress_keys", "select_row", "forecast_select", "multihead_select_row", "multihead_select",
+                 "attend_row", "sparse_attn", "gather_blocks"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
 
@@ -220,6 +224,34 @@ def forecast_select(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: n
     cs = shape.c()
     _check(_load().sparda_ref_forecast_select(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), _ptr(sel),
                                               _ptr(cnt)), "forecast_select")
+    return sel, cnt
+
+
+def multihead_select_row(shape: Shape, q: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, sm_scale: float,
+                         b: int, m: int, r: int):
+    """The InfLLM-V2 multi-head selector for one row: (sel_row, cnt, block scores with NaN for
+    non-candidates, wins); q: uint16 [B][Hq][n_q][D]."""
+    q, k_cmp = _u16(q), _u16(k_cmp)
+    nb = -(-shape.t_cap // shape.block_size)
+    sel = np.empty(shape.k_total, np.int16)
+    cnt = np.zeros(1, np.int16)
+    scores = np.empty(max(nb, 1), np.float64)
+    wins = np.empty(max(nb, 1), np.int32)
+    cs = shape.c()
+    _check(_load().sparda_ref_multihead_select_row(ctypes.byref(cs), _ptr(q), n_q, q_pos0, _ptr(k_cmp),
+                                                   float(sm_scale), b, m, r, _ptr(sel), _ptr(cnt), _ptr(scores),
+                                                   _ptr(wins)), "multihead_select_row")
+    return sel, int(cnt[0]), scores[:nb], wins[:nb]
+
+
+def multihead_select(shape: Shape, q: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, sm_scale: float):
+    """sel int16 [B][Hkv][n_q][k_total], cnt int16 [B][Hkv][n_q] of the multi-head selector."""
+    q, k_cmp = _u16(q), _u16(k_cmp)
+    sel = np.empty((shape.batch, shape.n_kv_heads, n_q, shape.k_total), np.int16)
+    cnt = np.empty((shape.batch, shape.n_kv_heads, n_q), np.int16)
+    cs = shape.c()
+    _check(_load().sparda_ref_multihead_select(ctypes.byref(cs), _ptr(q), n_q, q_pos0, _ptr(k_cmp), float(sm_scale),
+                                               _ptr(sel), _ptr(cnt)), "multihead_select")
     return sel, cnt
 
 

@@ -22,6 +22,13 @@
  *              position.  The top-k block scores, excluding the initial and local blocks, are
  *              merged with the initial and local blocks.  Ties in score are broken by the lower
  *              block index.  With window = stride = block the max-pool is the identity.
+ *   multihead  The InfLLM-V2 selector that SparDA replaces (Sec. 3, "three-stage block
+ *              representation", whose per-head score the indexer-training section writes out as
+ *              its target): every one of the G query heads of a group scores the compressed keys,
+ *              a softmax with the attention temperature turns each head's scores into a
+ *              distribution over the keys complete at the query's position, the G distributions
+ *              are summed into one shared score per key, and the same max-pool, top-k and union
+ *              as above follow.
  *   attend     Sec. 3, Eq. 1 and Sec. 4.1, Eq. 5: softmax attention of the query over exactly the
  *              keys/values of the attended blocks, causal within the query's own block.
  *   gather     Sec. 4.3 and Alg. 2 (prefetch of the selected blocks): staging slot s holds the 64
@@ -146,21 +153,31 @@ static int by_score_then_index(const void* pa, const void* pb) {
   return (a->block > b->block) - (a->block < b->block);
 }
 
-/* One query row (batch b, group m, row r at position p = q_pos0 + r).
- *   f: bf16 [B][Hkv][n_q][D]; k_cmp: bf16 [B][Hkv][nc_cap][D] (compressed-key windows)
- *   sel_row: k_total entries, ascending block indices, -1 padded; cnt: number of valid entries.
- *   scores (optional, one double per block of the capacity, ceil(t_cap / block) of them): the
- *   max-pooled Forecast score of every candidate block, NaN for a block that is not a candidate.
- *   wins (optional, same length): the lowest window index reaching that score, -1 elsewhere. */
-int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
-                          const uint16_t* k_cmp, int32_t b, int32_t m, int32_t r, int16_t* sel_row,
-                          int16_t* cnt, double* scores, int32_t* wins) {
-  int rc = check_shape(s);
-  if (rc) return rc;
-  if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
-  const int64_t D = s->head_dim, L = s->block_size, lw = s->cmp_kernel, sw = s->cmp_stride;
-  const int64_t p = q_pos0 + r;
-  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+/* The score of compressed-key window i for one query row. */
+typedef double (*window_score_fn)(const void* ctx, int64_t i);
+
+/* Eq. 4: the Forecast row of the group dotted with window i's compressed key. */
+typedef struct {
+  const uint16_t* frow;
+  const uint16_t* kc;
+  int64_t D;
+} forecast_ctx;
+
+static double forecast_window_score(const void* vctx, int64_t i) {
+  const forecast_ctx* c = (const forecast_ctx*)vctx;
+  const int64_t D = c->D;
+  const uint16_t* frow = c->frow;
+  const uint16_t* kc = c->kc;
+  double dot = 0.0;
+  for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(frow[d]) * sparda_ref_bf16_to_f64(kc[i * D + d]);
+  return dot;
+}
+
+/* Selection of one row at position p from window scores (Eq. 1 with the max-pool and top-k of
+ * the InfLLM-V2 selector): the outputs are those of sparda_ref_select_row. */
+static int select_pooled(const ref_shape* s, int64_t p, window_score_fn score, const void* ctx, int16_t* sel_row,
+                         int16_t* cnt, double* scores, int32_t* wins) {
+  const int64_t L = s->block_size, lw = s->cmp_kernel, sw = s->cmp_stride;
   const int64_t blk = p / L;
 
   /* forced(p): the initial blocks and the local window [blk - n_local + 1, blk]. */
@@ -178,9 +195,6 @@ int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, in
   const int64_t n_take = n_sel_budget < n_cand ? n_sel_budget : n_cand;
   /* windows complete at position p: i s_C + l_C <= p + 1 */
   const int64_t w_vis = (p + 1 - lw) >= 0 ? (p + 1 - lw) / sw : -1;     /* last visible window */
-
-  const uint16_t* frow = f + (((int64_t)b * s->n_kv_heads + m) * n_q + r) * D;
-  const uint16_t* kc = k_cmp + ((int64_t)b * s->n_kv_heads + m) * s->nc_cap * D;
 
   const int64_t n_blk_cap = (s->t_cap + L - 1) / L;
   if (scores)
@@ -201,9 +215,8 @@ int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, in
     double best = -INFINITY;
     int64_t best_i = -1;
     for (int64_t i = i_lo; i <= i_hi; ++i) {
-      double dot = 0.0;
-      for (int64_t d = 0; d < D; ++d) dot += sparda_ref_bf16_to_f64(frow[d]) * sparda_ref_bf16_to_f64(kc[i * D + d]);
-      if (dot > best) { best = dot; best_i = i; }
+      const double x = score(ctx, i);
+      if (x > best) { best = x; best_i = i; }
     }
     list[c].score = best;
     list[c].block = (int32_t)j;
@@ -229,6 +242,74 @@ int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, in
   return REF_OK;
 }
 
+/* One query row (batch b, group m, row r at position p = q_pos0 + r).
+ *   f: bf16 [B][Hkv][n_q][D]; k_cmp: bf16 [B][Hkv][nc_cap][D] (compressed-key windows)
+ *   sel_row: k_total entries, ascending block indices, -1 padded; cnt: number of valid entries.
+ *   scores (optional, one double per block of the capacity, ceil(t_cap / block) of them): the
+ *   max-pooled Forecast score of every candidate block, NaN for a block that is not a candidate.
+ *   wins (optional, same length): the lowest window index reaching that score, -1 elsewhere. */
+int sparda_ref_select_row(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
+                          const uint16_t* k_cmp, int32_t b, int32_t m, int32_t r, int16_t* sel_row,
+                          int16_t* cnt, double* scores, int32_t* wins) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim;
+  const int64_t p = q_pos0 + r;
+  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+  forecast_ctx ctx;
+  ctx.frow = f + (((int64_t)b * s->n_kv_heads + m) * n_q + r) * D;
+  ctx.kc = k_cmp + ((int64_t)b * s->n_kv_heads + m) * s->nc_cap * D;
+  ctx.D = D;
+  return select_pooled(s, p, forecast_window_score, &ctx, sel_row, cnt, scores, wins);
+}
+
+/* The InfLLM-V2 selector's shared score of window i: the sum over the group's heads of each
+ * head's softmax weight on window i, precomputed for every window complete at the query. */
+static double shared_window_score(const void* vctx, int64_t i) { return ((const double*)vctx)[i]; }
+
+/* One query row of the multi-head selector (batch b, group m, row r at p = q_pos0 + r).
+ *   q: bf16 [B][Hq][n_q][D], heads m G .. m G + G - 1 belong to group m; k_cmp as above, holding
+ *   every window complete at p (nc_cap > the last of them, else INVALID_ARG).
+ *   For head h: z_i = sm_scale q_h . K~_i over the windows complete at p, a_i = softmax(z)_i;
+ *   window i's shared score is the sum of a_i over the G heads.  Block scores are the max-pool of
+ *   the shared scores, and the selection is that of sparda_ref_select_row with them (scores /
+ *   wins report them the same way). */
+int sparda_ref_multihead_select_row(const ref_shape* s, const uint16_t* q, int32_t n_q, int64_t q_pos0,
+                                    const uint16_t* k_cmp, double sm_scale, int32_t b, int32_t m, int32_t r,
+                                    int16_t* sel_row, int16_t* cnt, double* scores, int32_t* wins) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q) return REF_ERR_INVALID_ARG;
+  if (!(sm_scale > 0.0) || !isfinite(sm_scale)) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim, G = s->group_size, lw = s->cmp_kernel, sw = s->cmp_stride;
+  const int64_t p = q_pos0 + r;
+  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t n_vis = (p + 1 - lw) >= 0 ? (p + 1 - lw) / sw + 1 : 0;  /* windows 0 .. n_vis - 1 */
+  if (n_vis > s->nc_cap) return REF_ERR_INVALID_ARG;
+  const uint16_t* keys = k_cmp + ((int64_t)b * s->n_kv_heads + m) * s->nc_cap * D;
+  double* shared = (double*)calloc((size_t)(n_vis > 0 ? n_vis : 1), sizeof(double));
+  double* z = (double*)malloc(sizeof(double) * (size_t)(n_vis > 0 ? n_vis : 1));
+  if (!shared || !z) { free(shared); free(z); return REF_ERR_INVALID_ARG; }
+  for (int64_t h = m * G; h < (m + 1) * G; ++h) {
+    const uint16_t* qrow = q + (((int64_t)b * s->n_kv_heads * G + h) * n_q + r) * D;
+    double zmax = -INFINITY;
+    for (int64_t i = 0; i < n_vis; ++i) {
+      double acc = 0.0;
+      for (int64_t e = 0; e < D; ++e) acc += sparda_ref_bf16_to_f64(qrow[e]) * sparda_ref_bf16_to_f64(keys[i * D + e]);
+      z[i] = sm_scale * acc;
+      if (z[i] > zmax) zmax = z[i];
+    }
+    double denom = 0.0;
+    for (int64_t i = 0; i < n_vis; ++i) denom += exp(z[i] - zmax);
+    for (int64_t i = 0; i < n_vis; ++i) shared[i] += exp(z[i] - zmax) / denom;
+  }
+  free(z);
+  rc = select_pooled(s, p, shared_window_score, shared, sel_row, cnt, scores, wins);
+  free(shared);
+  return rc;
+}
+
 /* All rows.  sel: int16 [B][Hkv][n_q][k_total]; cnt: int16 [B][Hkv][n_q]. */
 int sparda_ref_forecast_select(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
                                const uint16_t* k_cmp, int16_t* sel, int16_t* cnt) {
@@ -243,6 +324,29 @@ int sparda_ref_forecast_select(const ref_shape* s, const uint16_t* f, int32_t n_
     const int32_t m = (int32_t)((i / n_q) % s->n_kv_heads);
     const int32_t b = (int32_t)(i / ((int64_t)n_q * s->n_kv_heads));
     int e = sparda_ref_select_row(s, f, n_q, q_pos0, k_cmp, b, m, r, sel + i * s->k_total, cnt + i, NULL, NULL);
+    if (e) {
+#pragma omp critical
+      err = e;
+    }
+  }
+  return err;
+}
+
+/* All rows of the multi-head selector.  sel: int16 [B][Hkv][n_q][k_total]; cnt: int16 [B][Hkv][n_q]. */
+int sparda_ref_multihead_select(const ref_shape* s, const uint16_t* q, int32_t n_q, int64_t q_pos0,
+                                const uint16_t* k_cmp, double sm_scale, int16_t* sel, int16_t* cnt) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n_q < 1) return REF_ERR_INVALID_ARG;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  int err = REF_OK;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t i = 0; i < rows; ++i) {
+    const int32_t r = (int32_t)(i % n_q);
+    const int32_t m = (int32_t)((i / n_q) % s->n_kv_heads);
+    const int32_t b = (int32_t)(i / ((int64_t)n_q * s->n_kv_heads));
+    int e = sparda_ref_multihead_select_row(s, q, n_q, q_pos0, k_cmp, sm_scale, b, m, r, sel + i * s->k_total,
+                                            cnt + i, NULL, NULL);
     if (e) {
 #pragma omp critical
       err = e;

@@ -68,6 +68,35 @@ def select_rows_pooled(f_bits, kc_bits, q_pos0, k_total, n_init, n_local, lw, sw
     f = bf16_bits_to_f64(f_bits)
     kc = bf16_bits_to_f64(kc_bits)
     wsc = np.einsum("bhqd,bhid->bhqi", f, kc)
+    return _pool_and_select(wsc, q_pos0, k_total, n_init, n_local, lw, sw)
+
+
+def multihead_select_rows(q_bits, kc_bits, q_pos0, k_total, n_init, n_local, G, scale, lw=64, sw=64):
+    """The InfLLM-V2 multi-head selector by brute force: dense scaled scores of every query head
+    against every window, -inf on windows not complete at the row's position, scipy's softmax
+    over the windows, the sum over each group's G heads, then the same dense max-pool mask and
+    lexsort as select_rows_pooled.  q: [B][Hq][n_q][D], kc: [B][Hkv][n_win][D]."""
+    from scipy.special import softmax
+    q = bf16_bits_to_f64(q_bits)
+    kc = bf16_bits_to_f64(kc_bits)
+    B, Hq, n_q, D = q.shape
+    Hkv, n_win = kc.shape[1], kc.shape[2]
+    assert Hq == Hkv * G
+    kc_h = np.repeat(kc, G, axis=1)  # query head h reads KV head h // G
+    z = scale * np.einsum("bhqd,bhid->bhqi", q, kc_h)
+    start = np.arange(n_win) * sw
+    pos = q_pos0 + np.arange(n_q)
+    visible = (start[None, :] + lw) <= (pos[:, None] + 1)  # [n_q][n_win]
+    z = np.where(visible[None, None], z, -np.inf)
+    a = np.zeros_like(z)
+    for r in range(n_q):
+        if visible[r].any():
+            a[:, :, r, :] = softmax(z[:, :, r, :], axis=-1)
+    shared = a.reshape(B, Hkv, G, n_q, n_win).sum(axis=2)
+    return _pool_and_select(shared, q_pos0, k_total, n_init, n_local, lw, sw)
+
+
+def _pool_and_select(wsc, q_pos0, k_total, n_init, n_local, lw, sw):
     B, H, n_q, n_win = wsc.shape
     start = np.arange(n_win) * sw
     sel = np.full((B, H, n_q, k_total), -1, np.int16)

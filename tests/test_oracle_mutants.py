@@ -3,7 +3,10 @@ each one: a flipped sort direction, a dropped softmax scale, an off-by-one local
 causal mask that lets the next token in, an init block left out of the candidates' exclusion,
 a swapped operand index in the score, a rounding mode change in the compressed keys, and a block
 listed twice in a set being attended twice; on the paper's (32, 16) grid, a max-pool that uses
-windows not yet complete at the query and one that skips the windows straddling a block edge."""
+windows not yet complete at the query and one that skips the windows straddling a block edge; in
+the InfLLM-V2 multi-head selector, raw scores summed without the softmax, an unnormalised
+softmax, a single head standing for the group, a softmax normalised over fewer keys and a
+dropped temperature."""
 import math
 import os
 
@@ -28,6 +31,13 @@ MUTANTS = {
     "duplicate_attended_twice": ("if (seen) continue;", "(void)seen;"),
     "pool_ignores_visibility": ("if (i_hi > w_vis) i_hi = w_vis;", "(void)w_vis;"),
     "pool_inner_windows_only": ("int64_t i_lo = (j * L - lw) / sw + 1;", "int64_t i_lo = (j * L) / sw;"),
+    "multihead_raw_sum": ("shared[i] += exp(z[i] - zmax) / denom;", "shared[i] += z[i];"),
+    "multihead_unnormalised": ("shared[i] += exp(z[i] - zmax) / denom;", "shared[i] += exp(z[i] - zmax);"),
+    "multihead_first_head_only": ("for (int64_t h = m * G; h < (m + 1) * G; ++h)",
+                                  "for (int64_t h = m * G; h < m * G + 1; ++h)"),
+    "multihead_softmax_over_fewer_keys": ("for (int64_t i = 0; i < n_vis; ++i) denom += exp(z[i] - zmax);",
+                                          "for (int64_t i = 1; i < n_vis - 2; ++i) denom += exp(z[i] - zmax);"),
+    "multihead_temperature_dropped": ("z[i] = sm_scale * acc;", "z[i] = acc;"),
 }
 
 
@@ -78,7 +88,23 @@ def _pins_pass(o) -> bool:
             return False
         selg, cntg = o.forecast_select(sg, f, n_q, T - n_q, kcg)
         bselg, bcntg, _ = brute.select_rows_pooled(f, kcg, T - n_q, 4, 1, 1, 32, 16)
-        return bool(np.array_equal(selg, bselg) and np.array_equal(cntg, bcntg))
+        if not (np.array_equal(selg, bselg) and np.array_equal(cntg, bcntg)):
+            return False
+        # the InfLLM-V2 multi-head selector: the hand-worked example, then brute force on both grids
+        s5 = o.Shape(batch=1, n_kv_heads=1, group_size=2, head_dim=2, n_init=1, n_local=2, k_total=5, t_cap=448,
+                     nc_cap=7)
+        kc5 = to([[[[1, 0], [0, 1], [1, 1], [2, 0], [0, 2], [1, -1], [0, 0]]]])
+        sel5, cnt5, _, _ = o.multihead_select_row(s5, to([[[[1, 0]], [[0, 1]]]]), 1, 447, kc5, math.log(2.0), 0, 0, 0)
+        if not (cnt5 == 5 and list(sel5) == [0, 3, 4, 5, 6]):
+            return False
+        s10 = o.Shape(**{**s.__dict__, "nc_cap": 10})  # the softmax reads every complete block
+        kc10 = o.compress_keys(s10, k, 640, 0, 10)
+        for shp, kcx, lw, sw, n_local in ((s10, kc10, 64, 64, 2), (sg, kcg, 32, 16, 1)):
+            msel, mcnt = o.multihead_select(shp, q, n_q, T - n_q, kcx, scale)
+            bsel, bcnt, _ = brute.multihead_select_rows(q, kcx, T - n_q, shp.k_total, 1, n_local, G, scale, lw, sw)
+            if not (np.array_equal(msel, bsel) and np.array_equal(mcnt, bcnt)):
+                return False
+        return True
     except oracle.OracleError:
         return False
 

@@ -515,3 +515,115 @@ def test_duplicate_entries_are_attended_once(oracle_lib):
         got = oracle_lib.sparse_attn(s2, q, n_q, T - n_q, k, v, 0, np.ascontiguousarray(sel2), cnt2, scale)
         want = brute.attend_dense_masked(q, k[:, :, :T], v[:, :, :T], sel, cnt, T - n_q, 4, scale)
         np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------- InfLLM-V2 multi-head selector
+
+MH_SCALE = 1.0 / math.sqrt(128)
+
+
+def mh_shape(oracle, B, H, G, T, k_total, lw=64, sw=64, n_init=1, n_local=2, D=128):
+    return oracle.Shape(batch=B, n_kv_heads=H, group_size=G, head_dim=D, block_size=64, n_init=n_init,
+                        n_local=n_local, k_total=k_total, t_cap=T, nc_cap=(T - lw) // sw + 1, cmp_kernel=lw,
+                        cmp_stride=sw)
+
+
+def test_multihead_worked_example(oracle_lib):
+    with open(os.path.join(GOLDEN, "multihead_worked_example.json")) as fh:
+        g = json.load(fh)
+    to = lambda a: torch.tensor(a, dtype=torch.float32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    kc = to([[g["k_cmp"]]])
+    q = to([[[row] for row in g["q_heads"]]])  # [1][2 heads][1 row][2]
+    for k_total, key in ((4, "k4"), (5, "k5")):
+        s = oracle_lib.Shape(batch=1, n_kv_heads=1, group_size=2, head_dim=2, n_init=1, n_local=2, k_total=k_total,
+                             t_cap=448, nc_cap=7)
+        sel, cnt, scores, _ = oracle_lib.multihead_select_row(s, q, 1, g["query_position"], kc, math.log(2.0), 0, 0, 0)
+        assert cnt == g["expected"][key]["cnt"]
+        assert list(sel[:cnt]) == g["expected"][key]["sel"]
+        for j, num in g["expected"]["block_scores_num_over_299"].items():
+            assert scores[int(j)] == pytest.approx(num / 299, rel=1e-14)
+
+
+@pytest.mark.parametrize("T,n_q,k_total,G,n_init,n_local,lw,sw", [
+    (1024, 1, 6, 4, 1, 2, 64, 64), (1024, 200, 6, 4, 1, 2, 64, 64), (1500, 150, 7, 2, 0, 3, 64, 64),
+    (1024, 1, 6, 4, 1, 2, 32, 16), (1500, 260, 7, 4, 2, 1, 32, 16), (1280, 150, 5, 3, 1, 2, 32, 16),
+    (900, 90, 5, 16, 1, 1, 32, 16)])
+def test_multihead_matches_bruteforce(oracle_lib, T, n_q, k_total, G, n_init, n_local, lw, sw):
+    H = 2
+    s = mh_shape(oracle_lib, 1, H, G, T, k_total, lw, sw, n_init, n_local)
+    q = rnd_u16((1, H * G, n_q, 128), 81, G)
+    k = rnd_u16((1, H, T, 128), 82, 0)
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    sel, cnt = oracle_lib.multihead_select(s, q, n_q, T - n_q, kc, MH_SCALE)
+    bsel, bcnt, pooled = brute.multihead_select_rows(q, kc, T - n_q, k_total, n_init, n_local, G, MH_SCALE, lw, sw)
+    assert np.array_equal(cnt, bcnt)
+    assert np.array_equal(sel, bsel)
+    for r in (0, n_q // 2, n_q - 1):
+        _, _, sc, _ = oracle_lib.multihead_select_row(s, q, n_q, T - n_q, kc, MH_SCALE, 0, 1, r)
+        ok = ~np.isnan(sc)
+        np.testing.assert_allclose(sc[ok], pooled[0, 1, r, :len(sc)][ok], rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("lw,sw", [(64, 64), (32, 16)])
+def test_multihead_single_head_ranks_like_a_forecast_row(oracle_lib, lw, sw):
+    """With one head per group the softmax is increasing in the score and the max-pool commutes
+    with it, so the multi-head selector picks exactly what the plain dot-product selector picks
+    when the Forecast row is that head's query."""
+    T, n_q = 1500, 120
+    s = mh_shape(oracle_lib, 2, 2, 1, T, 9, lw, sw)
+    q = rnd_u16((2, 2, n_q, 128), 83, 0)
+    k = rnd_u16((2, 2, T, 128), 83, 1)
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    sel, cnt = oracle_lib.multihead_select(s, q, n_q, T - n_q, kc, MH_SCALE)
+    fsel, fcnt = oracle_lib.forecast_select(s, q, n_q, T - n_q, kc)
+    assert np.array_equal(cnt, fcnt) and np.array_equal(sel, fsel)
+
+
+def test_multihead_zero_query_is_uniform_and_takes_lowest_blocks(oracle_lib):
+    """q = 0: every head's softmax is uniform, every candidate ties, the lowest indices win."""
+    T, n_q, G = 2048, 40, 4
+    s = mh_shape(oracle_lib, 1, 2, G, T, 8, 32, 16)
+    q = np.zeros((1, 2 * G, n_q, 128), np.uint16)
+    kc = oracle_lib.compress_keys(s, rnd_u16((1, 2, T, 128), 84, 0), T, 0, s.nc_cap)
+    sel, cnt = oracle_lib.multihead_select(s, q, n_q, T - n_q, kc, MH_SCALE)
+    for r in range(n_q):
+        p = T - n_q + r
+        blk = p // 64
+        forced = {0, blk - 1, blk}
+        want = sorted(forced | set(range(1, 1 + 8 - 3)))
+        assert list(sel[0, 0, r, :cnt[0, 0, r]]) == want
+        _, _, sc, _ = oracle_lib.multihead_select_row(s, q, n_q, T - n_q, kc, MH_SCALE, 0, 0, r)
+        n_vis = (p + 1 - 32) // 16 + 1
+        assert np.allclose(sc[1:blk - 1], G / n_vis, rtol=1e-14)
+
+
+def test_multihead_head_order_and_decode_equals_prefill(oracle_lib):
+    """Permuting the heads inside each group leaves the selection unchanged; a decode call at
+    position p selects what row p of a multi-row call selects."""
+    T, n_q, G = 1800, 64, 4
+    s = mh_shape(oracle_lib, 1, 2, G, T, 7, 32, 16)
+    q = rnd_u16((1, 2 * G, n_q, 128), 85, 0)
+    kc = oracle_lib.compress_keys(s, rnd_u16((1, 2, T, 128), 85, 1), T, 0, s.nc_cap)
+    sel, cnt = oracle_lib.multihead_select(s, q, n_q, T - n_q, kc, MH_SCALE)
+    perm = np.concatenate([m * G + np.array([2, 0, 3, 1]) for m in range(2)])
+    psel, pcnt = oracle_lib.multihead_select(s, np.ascontiguousarray(q[:, perm]), n_q, T - n_q, kc, MH_SCALE)
+    assert np.array_equal(sel, psel) and np.array_equal(cnt, pcnt)
+    for r in (0, 31, n_q - 1):
+        dsel, dcnt = oracle_lib.multihead_select(s, np.ascontiguousarray(q[:, :, r:r + 1]), 1, T - n_q + r, kc,
+                                                 MH_SCALE)
+        assert np.array_equal(dsel[:, :, 0], sel[:, :, r]) and np.array_equal(dcnt[:, :, 0], cnt[:, :, r])
+
+
+def test_multihead_needs_every_complete_window(oracle_lib):
+    """The softmax runs over every key complete at the query, the local blocks' included, so the
+    compressed-key capacity must hold them all."""
+    import oracle
+    T = 1024
+    s = mh_shape(oracle_lib, 1, 1, 4, T, 6, 32, 16)
+    short = oracle.Shape(**{**s.__dict__, "nc_cap": s.nc_cap - 1})
+    q = rnd_u16((1, 4, 1, 128), 86, 0)
+    kc = np.zeros((1, 1, s.nc_cap, 128), np.uint16)
+    with pytest.raises(oracle.OracleError):
+        oracle_lib.multihead_select(short, q, 1, T - 1, np.ascontiguousarray(kc[:, :, :-1]), MH_SCALE)
+    with pytest.raises(oracle.OracleError):
+        oracle_lib.multihead_select(s, q, 1, T - 1, kc, 0.0)
