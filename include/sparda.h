@@ -10,6 +10,8 @@
  *   sparda_compress_keys    K -> K~               (Sec. 3, Eq. 2)
  *   sparda_forecast_select  F, K~ -> block sets   (Sec. 4.1, Eq. 4 with Eq. 1)
  *   sparda_sparse_attn      Q, K, V, sets -> O    (Sec. 4.1, Eq. 5 with Eq. 1)
+ *   sparda_multihead_select Q, K~ -> block sets   (the InfLLM-V2 selector of Sec. 3 that the
+ *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
  *
@@ -77,7 +79,7 @@ typedef struct sparda_shape {
 } sparda_shape;
 
 /* Workspace owners for sparda_workspace_size(). */
-enum sparda_op { SPARDA_OP_FORECAST_SELECT = 1, SPARDA_OP_SPARSE_ATTN = 2 };
+enum sparda_op { SPARDA_OP_FORECAST_SELECT = 1, SPARDA_OP_SPARSE_ATTN = 2, SPARDA_OP_MULTIHEAD_SELECT = 3 };
 
 /*
  * sparda_compress_keys -- mean-pooled compressed keys (Sec. 3, Eq. 2): window i of the grid
@@ -119,6 +121,31 @@ int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t
 int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
                            const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,
                            hipStream_t stream);
+
+/*
+ * sparda_multihead_select -- the same attended sets chosen by the InfLLM-V2 multi-head selector
+ * that the Forecast indexer replaces (Sec. 3, three-stage block representation; its per-head
+ * score is the softmax written out in the indexer-training section).  A baseline for comparing
+ * selection cost and choices; it selects from the attention queries of the same layer.
+ *   q      in  : bf16 [B][Hq][n_q][D] device, Hq = n_kv_heads * group_size; heads
+ *                m G .. m G + G - 1 belong to group m.
+ *   n_q, q_pos0: as for sparda_forecast_select.
+ *   k_cmp  in  : bf16 [B][Hkv][nc_cap][D] device; every window complete at the last row's
+ *                position (i s_C + l_C <= p + 1) must be valid and < nc_cap, since each head's
+ *                softmax runs over all of them, the initial and local blocks' windows included.
+ *   sm_scale   : softmax temperature, normally 1/sqrt(D); finite and > 0.
+ *   sel, cnt out: as for sparda_forecast_select.
+ *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_MULTIHEAD_SELECT)
+ *                (0 bytes for decode with G in {1, 2, 4, 8} up to about 38K windows times G).
+ * Per row: for every head h of the group, z_hi = sm_scale q_h . K~_i over the complete windows i,
+ * a_hi = softmax_i(z_hi) (float32, exp2 domain, each head's exact maximum subtracted); window i's
+ * shared score is sum_h a_hi; candidate j scores the largest shared score of the windows that
+ * overlap block j and are complete at p; forced blocks, ordering and ties as for
+ * sparda_forecast_select.
+ */
+int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0,
+                            const void* k_cmp, float sm_scale, int16_t* sel, int16_t* cnt, void* ws,
+                            size_t ws_bytes, hipStream_t stream);
 
 /*
  * sparda_sparse_attn -- block-sparse attention over the attended sets (Sec. 4.1, Eq. 5; Eq. 1).

@@ -68,6 +68,10 @@ struct SelectArgs {
   int64_t q_pos0, nc_cap;
   int32_t n_init, n_local, k_total;
   WinGrid grid;        // compressed-key grid of kc (nc_cap counts its windows)
+  // The multi-head selector only (select_multihead.hip):
+  const uint16_t* q;   // bf16 [B][Hq][n_q][D] attention queries, Hq = n_kv_heads * group_size
+  float scale_log2;    // softmax temperature times log2(e): scores are taken in the exp2 domain
+  int32_t group_size;
 };
 
 struct AttnArgs {
@@ -108,6 +112,15 @@ bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
+
+// Row-wise top-k over pooled window scores already in a.ws (row stride a.ws_stride, window wf of
+// the row at offset 0), for the multi-head selector's row-wise path (select.hip).
+hipError_t launch_rowwise_topk(const SelectArgs& a, hipStream_t stream);
+// The InfLLM-V2 multi-head selector (select_multihead.hip).  Workspace floats of a call (0 on the
+// fused decode path); *stride gets the floats per row.
+size_t multihead_ws_floats(int64_t rows, int32_t group_size, int32_t n_q, int64_t q_pos0, int32_t n_init,
+                           int32_t n_local, int32_t k_total, WinGrid grid, int64_t* stride);
+hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream);
 
 // Split count and blocks per split the attention launcher uses for `rows` query rows.
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);

@@ -1,0 +1,314 @@
+// select_multihead.hip -- the InfLLM-V2 multi-head block selector (paper Sec. 3, "three-stage
+// block representation"), the baseline that the Forecast indexer of Sec. 4.1 replaces.
+//
+// Per query row at position p of group m: each of the group's G query heads scores every
+// compressed key complete at p (windows 0 .. vis(p)), z_hi = scale * q_h . K~_i; a softmax over i
+// turns each head's scores into weights; the shared score of window i is the sum of the G heads'
+// weights; a block's score is the max-pool of the shared scores over the windows that overlap it
+// and are complete at p; the top-k candidates join the forced blocks exactly as in select.hip.
+//
+// Scores are taken in the exp2 domain (scale * log2 e folded into the query row) with float32
+// accumulation, and each head's softmax subtracts that head's exact maximum, so every exponent
+// is <= 0.
+//
+// Paths:
+//  * fused decode (n_q == 1, G in {1, 2, 4, 8}, G * windows + candidates <= kMhLdsFloats): one
+//    512-thread workgroup per (batch, group) row.  K~ is read once, 1 KiB per wavefront load as
+//    in the Forecast decode kernel, and each loaded window is scored by all G heads into LDS;
+//    the per-head maximum and sum, the shared scores, the max-pool and the block-wide radix
+//    select (select_block.hpp) all stay on the CU.
+//  * row-wise (everything else): mh_score_kernel writes every head's score of every complete
+//    window of every row to the workspace, mh_norm_kernel (one wavefront per row) turns them into
+//    the shared scores of the windows that overlap the row's candidates, and select.hip's
+//    row-wise top-k pools and selects.
+#include <math.h>
+
+#include "device_util.hpp"
+#include "launch.hpp"
+#include "select_block.hpp"
+
+namespace sparda {
+
+constexpr int kMhLdsFloats = 38400;  // fused decode: G * windows + candidates floats (150 KiB)
+constexpr int kMhMaxRowG = 16;
+
+__device__ __forceinline__ float wave_max_f(float x) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) x = fmaxf(x, __shfl_xor(x, d, kWave));
+  return x;
+}
+__device__ __forceinline__ float wave_sum_f(float x) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, kWave);
+  return x;
+}
+
+// 8 query dims as floats, scaled into the exp2 domain.
+__device__ __forceinline__ void load_q8(const uint16_t* src, float s, float (&q)[8]) {
+  const uint4 w = ld16(src);
+  q[0] = bf16lo(w.x) * s; q[1] = bf16hi(w.x) * s; q[2] = bf16lo(w.y) * s; q[3] = bf16hi(w.y) * s;
+  q[4] = bf16lo(w.z) * s; q[5] = bf16hi(w.z) * s; q[6] = bf16lo(w.w) * s; q[7] = bf16hi(w.w) * s;
+}
+
+__device__ __forceinline__ float dot8(const float (&q)[8], const uint4& k) {
+  float d = q[0] * bf16lo(k.x);
+  d = fmaf(q[1], bf16hi(k.x), d);
+  d = fmaf(q[2], bf16lo(k.y), d);
+  d = fmaf(q[3], bf16hi(k.y), d);
+  d = fmaf(q[4], bf16lo(k.z), d);
+  d = fmaf(q[5], bf16hi(k.z), d);
+  d = fmaf(q[6], bf16lo(k.w), d);
+  d = fmaf(q[7], bf16hi(k.w), d);
+  return d;
+}
+
+// ---- fused decode ---------------------------------------------------------------------------
+
+template <int G>
+__global__ __launch_bounds__(kDecThreads) void mh_decode_kernel(SelectArgs a) {
+  __shared__ float zs[kMhLdsFloats];  // head h's score of window i at zs[h NV + i]
+  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  __shared__ float red[kDecThreads / 64][G];
+  const int64_t row = blockIdx.x;  // b * Hkv + m
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t p = a.q_pos0;
+  const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
+  int16_t* out = a.sel + row * a.k_total;
+  if (wave == 0) emit_forced(out, g, a.k_total, lane);
+  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  int16_t* chosen_out = out + g.init_hi;
+  const int C = g.n_cand;
+  if (g.n_take >= C) {
+    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
+    return;
+  }
+  if (g.n_take <= 0) return;
+  const int NV = grid_win_vis(a.grid, p) + 1;  // windows 0 .. NV - 1 (the host checked NV <= nc_cap)
+
+  {  // scores: lane reads dims 8 (lane % 16) .. of window base + 4 i + lane / 16
+    const int c = lane & 15, rs = lane >> 4;
+    float qf[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h) load_q8(a.q + (row * G + h) * kHeadDim + c * 8, a.scale_log2, qf[h]);
+    const uint16_t* kbase = a.kc + row * a.nc_cap * kHeadDim + c * 8;
+    uint4 kw[16], kn[16];
+    auto load = [&](int base, uint4 (&w)[16]) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int idx = min(base + 4 * i + rs, NV - 1);  // past the last window: a repeat, never stored
+        w[i] = ld16(kbase + (int64_t)idx * kHeadDim);
+      }
+    };
+    int base = wave * 64;
+    if (base < NV) load(base, kw);
+    for (; base < NV; base += kDecThreads) {
+      if (base + kDecThreads < NV) load(base + kDecThreads, kn);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int idx = base + 4 * i + rs;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float d = row16_sum(dot8(qf[h], kw[i]));
+          if (c == h && idx < NV) zs[h * NV + idx] = d;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) kw[i] = kn[i];
+    }
+  }
+  __syncthreads();
+
+  // Per-head softmax over the NV windows: exact maximum, then exp2 and the sum.
+  float mx[G], inv[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) mx[h] = -INFINITY;
+  for (int i = tid; i < NV; i += kDecThreads)
+#pragma unroll
+    for (int h = 0; h < G; ++h) mx[h] = fmaxf(mx[h], zs[h * NV + i]);
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float m = wave_max_f(mx[h]);
+    if (lane == 0) red[wave][h] = m;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float m = red[0][h];
+#pragma unroll
+    for (int w = 1; w < kDecThreads / 64; ++w) m = fmaxf(m, red[w][h]);
+    mx[h] = m;
+    inv[h] = 0.f;
+  }
+  __syncthreads();
+  for (int i = tid; i < NV; i += kDecThreads)
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float e = exp2f(zs[h * NV + i] - mx[h]);
+      zs[h * NV + i] = e;
+      inv[h] += e;
+    }
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float s = wave_sum_f(inv[h]);
+    if (lane == 0) red[wave][h] = s;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecThreads / 64; ++w) s += red[w][h];
+    inv[h] = 1.0f / s;
+  }
+  // Shared scores over head 0's slots: each thread reads and writes only its own windows.
+  for (int i = tid; i < NV; i += kDecThreads) {
+    float s = 0.f;
+#pragma unroll
+    for (int h = 0; h < G; ++h) s = fmaf(zs[h * NV + i], inv[h], s);
+    zs[i] = s;
+  }
+  __syncthreads();
+
+  // Block scores: max-pool of the shared scores (the identity on the one-key-per-block grid).
+  float* bs = zs + G * NV;
+  for (int i = tid; i < C; i += kDecThreads) {
+    const int32_t j = g.cand_lo + i;
+    const int32_t lo = grid_win_lo(a.grid, j), hi = min(grid_win_hi(a.grid, j), NV - 1);
+    float m = zs[lo];
+    for (int32_t w = lo + 1; w <= hi; ++w) m = fmaxf(m, zs[w]);
+    bs[i] = m;
+  }
+  __syncthreads();
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+}
+
+// ---- row-wise path --------------------------------------------------------------------------
+
+// grid.x = row * n_chunks + chunk; a chunk is 256 windows, 64 per wavefront.  Head h's score of
+// window i goes to ws[row * ws_stride + h * hstride + i].
+__global__ __launch_bounds__(256) void mh_score_kernel(SelectArgs a, int n_chunks, int64_t hstride) {
+  const int64_t row = blockIdx.x / n_chunks;
+  const int chunk = (int)(blockIdx.x % n_chunks);
+  const int r = (int)(row % a.n_q);
+  const int64_t bm = row / a.n_q;
+  const int64_t p = a.q_pos0 + r;
+  const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
+  if (g.n_take >= g.n_cand) return;  // the row takes every candidate: no scores needed
+  const int NV = grid_win_vis(a.grid, p) + 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, rs = lane >> 4;
+  const int first = chunk * 256 + wave * 64;
+  if (first >= NV) return;
+  const uint16_t* kbase = a.kc + bm * a.nc_cap * kHeadDim + c * 8;
+  uint4 kw[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) kw[i] = ld16(kbase + (int64_t)min(first + 4 * i + rs, NV - 1) * kHeadDim);
+  float* zrow = a.ws + row * a.ws_stride;
+  for (int h = 0; h < a.group_size; ++h) {
+    float qf[8];
+    load_q8(a.q + ((bm * a.group_size + h) * a.n_q + r) * kHeadDim + c * 8, a.scale_log2, qf);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float d = row16_sum(dot8(qf, kw[i]));
+      const int idx = first + 4 * i + rs;
+      if (c == 0 && idx < NV) zrow[h * hstride + idx] = d;
+    }
+  }
+}
+
+// One wavefront per row: each head's maximum and sum over the row's complete windows, then the
+// shared score of every window that overlaps a candidate, written after the G heads' rows at
+// offset (window - first such window), where select.hip's row-wise top-k reads it.
+__global__ __launch_bounds__(256) void mh_norm_kernel(SelectArgs a, int64_t n_rows, int64_t hstride) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= n_rows) return;
+  const int r = (int)(row % a.n_q);
+  const int64_t p = a.q_pos0 + r;
+  const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
+  if (g.n_take >= g.n_cand) return;
+  const int NV = grid_win_vis(a.grid, p) + 1;
+  int32_t wf, wl;
+  row_windows(g, a.grid, p, &wf, &wl);
+  const float* zrow = a.ws + row * a.ws_stride;
+  float* shared = a.ws + row * a.ws_stride + a.group_size * hstride;
+  float mx[kMhMaxRowG], inv[kMhMaxRowG];
+#pragma unroll
+  for (int h = 0; h < kMhMaxRowG; ++h) {
+    mx[h] = 0.f;
+    inv[h] = 0.f;
+    if (h < a.group_size) {
+      float m = -INFINITY;
+      for (int i = lane; i < NV; i += kWave) m = fmaxf(m, zrow[h * hstride + i]);
+      m = wave_max_f(m);
+      float s = 0.f;
+      for (int i = lane; i < NV; i += kWave) s += exp2f(zrow[h * hstride + i] - m);
+      mx[h] = m;
+      inv[h] = 1.0f / wave_sum_f(s);
+    }
+  }
+  for (int i = wf + lane; i <= wl; i += kWave) {
+    float s = 0.f;
+#pragma unroll
+    for (int h = 0; h < kMhMaxRowG; ++h)
+      if (h < a.group_size) s = fmaf(exp2f(zrow[h * hstride + i] - mx[h]), inv[h], s);
+    shared[i - wf] = s;
+  }
+}
+
+// ---- host -----------------------------------------------------------------------------------
+
+static bool mh_fused(int32_t G, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  if (n_q != 1 || !(G == 1 || G == 2 || G == 4 || G == 8)) return false;
+  const RowGeom g = row_geom(q_pos0, n_init, n_local, 1 << 30);
+  const int64_t nv = (int64_t)grid_win_vis(grid, q_pos0) + 1;
+  return (int64_t)G * nv + g.n_cand <= kMhLdsFloats;
+}
+
+size_t multihead_ws_floats(int64_t rows, int32_t group_size, int32_t n_q, int64_t q_pos0, int32_t n_init,
+                           int32_t n_local, int32_t k_total, WinGrid grid, int64_t* stride) {
+  *stride = 0;
+  if (mh_fused(group_size, n_q, q_pos0, n_init, n_local, grid)) return 0;
+  const int64_t pl = q_pos0 + n_q - 1;  // the last row scores the most windows
+  const RowGeom gl = row_geom(pl, n_init, n_local, k_total);
+  if (gl.n_take >= gl.n_cand) return 0;  // then every row takes all of its candidates
+  const int64_t nv = (int64_t)grid_win_vis(grid, pl) + 1;
+  const int64_t hstride = (nv + 3) & ~(int64_t)3;
+  *stride = (group_size + 1) * hstride;
+  return (size_t)rows * (size_t)*stride;
+}
+
+hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
+  const int G = a.group_size;
+  if (mh_fused(G, a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid)) {
+    const dim3 grid((unsigned)rows), block(kDecThreads);
+    switch (G) {
+      case 1: hipLaunchKernelGGL(mh_decode_kernel<1>, grid, block, 0, stream, a); break;
+      case 2: hipLaunchKernelGGL(mh_decode_kernel<2>, grid, block, 0, stream, a); break;
+      case 4: hipLaunchKernelGGL(mh_decode_kernel<4>, grid, block, 0, stream, a); break;
+      default: hipLaunchKernelGGL(mh_decode_kernel<8>, grid, block, 0, stream, a); break;
+    }
+    return hipGetLastError();
+  }
+  if (G > kMhMaxRowG) return hipErrorInvalidValue;
+  SelectArgs t = a;
+  if (a.ws_stride > 0) {  // some row scores its candidates
+    const int64_t hstride = a.ws_stride / (G + 1);
+    const int64_t pl = a.q_pos0 + a.n_q - 1;
+    const int nv = grid_win_vis(a.grid, pl) + 1;
+    const int n_chunks = (nv + 255) / 256;
+    hipLaunchKernelGGL(mh_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks, hstride);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(mh_norm_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, a, rows, hstride);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    t.ws = a.ws + G * hstride;  // the shared scores; the row stride stays ws_stride
+  }
+  return launch_rowwise_topk(t, stream);
+}
+
+}  // namespace sparda

@@ -97,6 +97,15 @@ size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* st
   return (size_t)rows * (size_t)*stride * sizeof(float);
 }
 
+// Workspace of sparda_multihead_select: every head's window scores plus the shared scores on the
+// row-wise path (none on the fused decode kernel).
+size_t multihead_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* stride) {
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  return sparda::multihead_ws_floats(rows, s->group_size, n_q, q_pos0, s->n_init, s->n_local, s->k_total,
+                                     grid_of(s), stride) *
+         sizeof(float);
+}
+
 size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps) {
   if (sparda::attn_uses_tiles(s->group_size, n_q, q_pos0)) {  // tiled multi-row kernel: no partials
     *n_splits = 1;
@@ -143,6 +152,9 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
   } else if (op == SPARDA_OP_SPARSE_ATTN) {
     int32_t ns, bps;
     *bytes = attn_ws(shape, n_q, q_pos0, &ns, &bps);
+  } else if (op == SPARDA_OP_MULTIHEAD_SELECT) {
+    int64_t stride;
+    *bytes = multihead_ws(shape, n_q, q_pos0, &stride);
   } else {
     return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
   }
@@ -205,6 +217,49 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
   a.k_total = shape->k_total;
   a.grid = grid_of(shape);
   return hip_status(sparda::launch_select(a, stream), "select launch");
+}
+
+int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0,
+                            const void* k_cmp, float sm_scale, int16_t* sel, int16_t* cnt, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(sel, "sel", 2)) ||
+      (rc = check_dev(cnt, "cnt", 2)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (!(sm_scale > 0.0f) || !std::isfinite(sm_scale))
+    return fail(SPARDA_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  const int64_t pl = q_pos0 + n_q - 1;
+  const int64_t last = sparda::grid_win_vis(grid_of(shape), pl);  // every head's softmax reads 0 .. last
+  if (last >= shape->nc_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "compressed key %lld (complete at position %lld) beyond nc_cap %lld",
+                (long long)last, (long long)pl, (long long)shape->nc_cap);
+  int64_t stride = 0;
+  const size_t need = multihead_ws(shape, n_q, q_pos0, &stride);
+  if (need > 0) {
+    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  sparda::SelectArgs a{};
+  a.kc = static_cast<const uint16_t*>(k_cmp);
+  a.sel = sel;
+  a.cnt = cnt;
+  a.ws = static_cast<float*>(ws);
+  a.ws_stride = stride;
+  a.batch = shape->batch;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.n_q = n_q;
+  a.q_pos0 = q_pos0;
+  a.nc_cap = shape->nc_cap;
+  a.n_init = shape->n_init;
+  a.n_local = shape->n_local;
+  a.k_total = shape->k_total;
+  a.grid = grid_of(shape);
+  a.q = static_cast<const uint16_t*>(q);
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.group_size = shape->group_size;
+  return hip_status(sparda::launch_multihead_select(a, stream), "multihead select launch");
 }
 
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,

@@ -24,8 +24,10 @@ SPARDA_ERR_HOST_NOT_MAPPED = -4
 SPARDA_ERR_HIP = -5
 SPARDA_OP_FORECAST_SELECT = 1
 SPARDA_OP_SPARSE_ATTN = 2
+SPARDA_OP_MULTIHEAD_SELECT = 3
 
-EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_sparse_attn", "sparda_gather_blocks",
+EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
+            "sparda_gather_blocks",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
 
@@ -89,10 +91,12 @@ def load() -> ctypes.CDLL:
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.sparda_compress_keys.argtypes = [S, P, i64, i32, i32, P, P]
         lib.sparda_forecast_select.argtypes = [S, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]
+        lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
-        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_sparse_attn", "sparda_gather_blocks",
+        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
+                     "sparda_gather_blocks",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
         lib.sparda_status_string.argtypes = [ctypes.c_int]
@@ -153,6 +157,15 @@ def sparda_forecast_select(shape: SpardaShape, f, n_q: int, q_pos0: int, k_cmp, 
         ws_bytes = ws.numel() * ws.element_size()
     _check(load().sparda_forecast_select(ctypes.byref(cs), _p(f), n_q, q_pos0, _p(k_cmp), _p(sel), _p(cnt), _p(ws),
                                          ws_bytes, _stream(stream)), "sparda_forecast_select")
+
+
+def sparda_multihead_select(shape: SpardaShape, q, n_q: int, q_pos0: int, k_cmp, sm_scale: float, sel, cnt, ws=None,
+                            ws_bytes: int = 0, stream=None):
+    cs = shape.c()
+    if ws is not None and not isinstance(ws, int) and ws_bytes == 0:
+        ws_bytes = ws.numel() * ws.element_size()
+    _check(load().sparda_multihead_select(ctypes.byref(cs), _p(q), n_q, q_pos0, _p(k_cmp), float(sm_scale), _p(sel),
+                                          _p(cnt), _p(ws), ws_bytes, _stream(stream)), "sparda_multihead_select")
 
 
 def sparda_sparse_attn(shape: SpardaShape, q, n_q: int, q_pos0: int, k, v, kv_mode: int, sel, cnt, sm_scale: float, o,

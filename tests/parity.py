@@ -60,6 +60,37 @@ def compare_selection(oshape, f_u16, kc_u16, n_q, q_pos0, gpu_sel, gpu_cnt, rows
     return n_rows, n_swaps
 
 
+def compare_multihead_selection(oshape, q_u16, kc_u16, n_q, q_pos0, sm_scale, gpu_sel, gpu_cnt, rows):
+    """The multi-head selector's sets against the oracle's.  Its block scores are sums of softmax
+    weights, all > 0, computed on the GPU in float32 (exp2 domain) from float32 dot products, so
+    a relative error of a few 1e-6 covers them; a block chosen by only one side is accepted when
+    its oracle score lies within 1e-3 of s_k relatively.  Returns (n_rows, n_tie_swaps)."""
+    n_rows = n_swaps = 0
+    for (b, m, r) in rows:
+        ref, cnt, scores, _ = oracle.multihead_select_row(oshape, q_u16, n_q, q_pos0, kc_u16, sm_scale, b, m, r)
+        g = gpu_sel[b, m, r]
+        gc = int(gpu_cnt[b, m, r])
+        assert gc == cnt, f"row {(b, m, r)}: cnt {gc} != oracle {cnt}"
+        assert np.all(g[cnt:] == -1), f"row {(b, m, r)}: padding"
+        gs = g[:cnt]
+        assert np.all(np.diff(gs.astype(np.int64)) > 0), f"row {(b, m, r)}: not strictly ascending: {gs}"
+        n_rows += 1
+        if np.array_equal(gs, ref[:cnt]):
+            continue
+        A, R = set(gs.tolist()), set(ref[:cnt].tolist())
+        cand = ~np.isnan(scores)
+        only = (A - R) | (R - A)
+        for j in only:
+            assert 0 <= j < len(scores) and cand[j], f"row {(b, m, r)}: non-candidate block {j} differs"
+        s_k = min(scores[j] for j in R if cand[j])
+        for j in only:
+            assert abs(scores[j] - s_k) <= REL_TIE * s_k, (
+                f"row {(b, m, r)}: block {j} (score {scores[j]:.6g}) differs beyond the tie window of "
+                f"s_k = {s_k:.6g}")
+        n_swaps += 1
+    return n_rows, n_swaps
+
+
 def compare_attention(o_gpu, o_ref, what=""):
     o_gpu = np.asarray(o_gpu, np.float64)
     err = np.abs(o_gpu - o_ref)

@@ -189,6 +189,37 @@ def test_workspace_sizes(lib):
     assert sp.sparda_workspace_size(s6, sp.SPARDA_OP_SPARSE_ATTN, 20, 200000) == 0
 
 
+def test_multihead_select_arguments(lib):
+    """The InfLLM-V2 multi-head selector: the softmax of every head runs over every compressed key
+    complete at the last row's position, so nc_cap must reach that key; the temperature must be a
+    positive number; decode with G in {1, 2, 4, 8} is fused (no workspace), other calls keep every
+    head's window scores plus the shared scores per row."""
+    m = sp.sparda_multihead_select
+    sc = 1 / math.sqrt(128)
+    s = shape(nc_cap=64)  # blocks 0 .. 63 of a 4096-token cache
+    assert rc_of(m, shape(nc_cap=63), FAKE, 1, 4095, FAKE, sc, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert rc_of(m, s, FAKE, 1, 4095, FAKE, bad, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(m, s, None, 1, 4095, FAKE, sc, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    op = sp.SPARDA_OP_MULTIHEAD_SELECT
+    assert sp.sparda_workspace_size(s, op, 1, 4095) == 0  # fused decode
+    # 128K decode on the (32, 16) grid: 4 x 8191 window scores + 2045 block scores fit in LDS
+    g = shape(batch=32, k_total=64, t_cap=131072, nc_cap=8191, cmp_kernel=32, cmp_stride=16)
+    assert sp.sparda_workspace_size(g, op, 1, 131071) == 0
+    # G = 16 there: row-wise, (16 + 1) x 8192 floats per row for 32 x 2 rows
+    g16 = shape(batch=32, n_kv_heads=2, group_size=16, k_total=64, t_cap=131072, nc_cap=8191, cmp_kernel=32,
+                cmp_stride=16)
+    assert sp.sparda_workspace_size(g16, op, 1, 131071) == 64 * 17 * 8192 * 4
+    # G = 3 decode is row-wise too: (3 + 1) x 64 floats per row
+    assert sp.sparda_workspace_size(shape(group_size=3), op, 1, 4095) == 16 * 4 * 64 * 4
+    # multi-row: the last row (p = 4095) has 64 complete blocks
+    need = sp.sparda_workspace_size(s, op, 100, 3996)
+    assert need == 2 * 8 * 100 * 5 * 64 * 4
+    assert rc_of(m, s, FAKE, 100, 3996, FAKE, sc, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
+    # rows that take every candidate need no scores
+    assert sp.sparda_workspace_size(shape(k_total=64), op, 100, 3996) == 0
+
+
 def test_status_strings(lib):
     assert sp.status_string(0) == "SPARDA_OK"
     assert sp.status_string(-4) == "SPARDA_ERR_HOST_NOT_MAPPED"

@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2606_04511_amd.sparda as sp
 from paper_2606_04511_amd import inputs
-from parity import compare_attention, compare_selection
+from parity import compare_attention, compare_multihead_selection, compare_selection
 
 pytestmark = pytest.mark.gpu
 SCALE = 1.0 / math.sqrt(128)
@@ -599,3 +599,93 @@ def test_grid_select_exact_ties_take_lowest_index(dev, T, n_q, k_total, n_local)
     ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
     assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
     assert np.array_equal(sel.cpu().numpy(), ref_sel)
+
+
+# ----------------------------------------------------------------------------- InfLLM-V2 multi-head selector
+
+def gpu_multihead(s, q_dev, n_q, q_pos0, kc_dev, dev):
+    sel = torch.full((s.batch, s.n_kv_heads, n_q, s.k_total), 777, dtype=torch.int16, device=dev)
+    cnt = torch.full((s.batch, s.n_kv_heads, n_q), 777, dtype=torch.int16, device=dev)
+    sp.sparda_multihead_select(s, q_dev, n_q, q_pos0, kc_dev, SCALE, sel, cnt,
+                               ws(s, sp.SPARDA_OP_MULTIHEAD_SELECT, n_q, q_pos0, dev))
+    torch.cuda.synchronize()
+    return sel, cnt
+
+
+MULTIHEAD = [
+    # B, H, G, T, n_q, k_total, n_init, n_local, grid (lw, sw)
+    (2, 2, 4, 4096, 1, 16, 1, 2, (64, 64)),      # fused decode
+    (1, 2, 1, 8192, 1, 16, 1, 2, (64, 64)),      # fused, one head: ranks like the dot-product selector
+    (1, 1, 2, 20000, 1, 64, 0, 1, (32, 16)),     # fused, (32, 16), no initial block, one local block
+    (2, 2, 4, 32768, 1, 64, 1, 2, (32, 16)),     # fused, (32, 16)
+    (1, 1, 8, 40000, 1, 32, 1, 3, (32, 16)),     # fused, G = 8
+    (1, 2, 3, 9000, 1, 24, 1, 2, (32, 16)),      # G = 3: row-wise
+    (1, 1, 16, 12000, 1, 40, 1, 2, (32, 16)),    # G = 16: row-wise
+    (1, 2, 4, 5000, 300, 12, 1, 2, (64, 64)),    # multi-row, chunk off a block boundary
+    (1, 1, 4, 6000, 333, 20, 1, 1, (32, 16)),    # multi-row, (32, 16), one local block
+]
+
+
+@pytest.mark.parametrize("B,H,G,T,n_q,k_total,n_init,n_local,grid", MULTIHEAD)
+def test_multihead_select(dev, B, H, G, T, n_q, k_total, n_init, n_local, grid):
+    lw, sw = grid
+    say(f"multihead select B{B} H{H} G{G} T{T} n_q{n_q} k{k_total} init {n_init} local {n_local} grid {grid}")
+    w, case = make(B, H, G, T, n_q, k_total, 6100 + T + G, n_init=n_init, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nw = (T - lw) // sw + 1
+    s, o = shapes(B, H, G, k_total, t_cap, nw, n_init, n_local, lw=lw, sw=sw)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, nw)
+    q_u16 = inputs.to_u16(case["q"])
+    q_pos0 = T - n_q
+    sel, cnt = gpu_multihead(s, case["q"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
+    rng = np.random.default_rng(3)
+    rr = sorted(set(rng.integers(0, n_q, size=min(n_q, 60)).tolist()) | {0, n_q - 1})
+    rows = [(b, m, r) for b in range(B) for m in range(H) for r in rr]
+    n, swaps = compare_multihead_selection(o, q_u16, kc_ref, n_q, q_pos0, SCALE, sel.cpu().numpy(),
+                                           cnt.cpu().numpy(), rows)
+    say(f"  rows {n}, tie swaps {swaps}")
+
+
+@pytest.mark.parametrize("T,n_q,G,grid", [(8192, 1, 4, (32, 16)), (8192, 1, 8, (64, 64)), (3000, 200, 4, (32, 16)),
+                                          (5000, 1, 3, (64, 64))])
+def test_multihead_zero_query_ties_take_lowest_index(dev, T, n_q, G, grid):
+    """q = 0: every head's softmax is exactly uniform on both sides, every candidate ties, and the
+    lowest indices must win on the fused and row-wise paths alike."""
+    lw, sw = grid
+    B, H, k_total = 1, 2, 16
+    nw = (T - lw) // sw + 1
+    t_cap = -(-T // 64) * 64
+    s, o = shapes(B, H, G, k_total, t_cap, nw, 1, 2, lw=lw, sw=sw)
+    g = torch.Generator().manual_seed(T)
+    kc = torch.randn((B, H, nw, 128), generator=g).to(torch.bfloat16)
+    q = torch.zeros((B, H * G, n_q, 128), dtype=torch.bfloat16)
+    sel, cnt = gpu_multihead(s, q.to(dev), n_q, T - n_q, kc.to(dev), dev)
+    ref_sel, ref_cnt = oracle.multihead_select(o, inputs.to_u16(q), n_q, T - n_q, inputs.to_u16(kc), SCALE)
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(sel.cpu().numpy(), ref_sel)
+
+
+def test_multihead_full_decode_t128k_samples(dev):
+    """The 128K, batch-32 decode layer on the (32, 16) grid, selected by the multi-head selector from
+    the attention queries; sampled rows against the oracle."""
+    w = inputs.WORKLOADS["decode_b32_t128k"]
+    T = w.seq_len
+    nw = (T - 32) // 16 + 1
+    say("multihead full decode_b32_t128k: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, _ = shapes(w.batch, w.n_kv_heads, w.group_size, w.k_total, T, nw, lw=32, sw=16)
+    kc = gpu_compress(s, case["k"], T, nw, nw, dev)
+    sel, cnt = gpu_multihead(s, case["q"], 1, T - 1, kc, dev)
+    _, o1 = shapes(1, 1, w.group_size, w.k_total, T, nw, lw=32, sw=16)
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    rng = np.random.default_rng(21)
+    swaps = 0
+    pairs = sorted(set((int(b), int(m)) for b, m in zip(rng.integers(0, w.batch, 6), rng.integers(0, w.n_kv_heads, 6))))
+    for b, m in pairs:
+        kc_ref = oracle.compress_keys(o1, inputs.to_u16(case["k"][b:b + 1, m:m + 1]), T, 0, nw)
+        assert np.array_equal(inputs.to_u16(kc[b:b + 1, m:m + 1]), kc_ref)
+        q16 = inputs.to_u16(case["q"][b:b + 1, m * w.group_size:(m + 1) * w.group_size])
+        _, sw_ = compare_multihead_selection(o1, q16, kc_ref, 1, T - 1, SCALE, sel_np[b:b + 1, m:m + 1],
+                                             cnt_np[b:b + 1, m:m + 1], [(0, 0, 0)])
+        swaps += sw_
+    say(f"  sampled {len(pairs)} rows, tie swaps {swaps}")
