@@ -10,6 +10,8 @@ value = algorithmic HBM bytes of the step / step time (GB/s); ms_per_step is the
 Secondary legs on the same JSON line:
   paper_grid     -- the same decode layer with K~ on the paper's (32, 16) grid (8191 windows per
                     row, max-pooled to block scores inside the select);
+  selectors      -- selection cost of the Forecast indexer against the InfLLM-V2 multi-head
+                    selector it replaces (decode at 32K/128K, a prefill chunk at 128K; G = 4, 16);
   prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
                     selects), reported in TFLOP/s of scored (row, candidate) pairs x 2 x 128;
   prefill_attn   -- block-sparse attention of that prefill (ms);
@@ -249,6 +251,46 @@ def grid_leg(base: DecodeLayer, dev, warmup, steps, stream):
     return res
 
 
+def selector_leg(dev, iters):
+    """Selection cost of the Forecast indexer (one head per group, no softmax) against the InfLLM-V2
+    multi-head selector it replaces (every query head, softmax, group sum), on the paper's (32, 16)
+    key grid and the same compressed keys: decode rows at 32K and 128K (B32) and a 4096-row prefill
+    chunk ending at 128K (B1), for G = 4 (8 KV heads) and G = 16 (2 KV heads), 32 query heads."""
+    stream = torch.cuda.current_stream()
+    out = {"grid": [32, 16], "decode": [], "prefill_chunk": []}
+
+    def one(B, Hkv, G, T, n_q, k_total=64):
+        nw = (T - 32) // 16 + 1
+        shape = sp.SpardaShape(batch=B, n_kv_heads=Hkv, group_size=G, k_total=k_total, t_cap=T, nc_cap=nw,
+                               cmp_kernel=32, cmp_stride=16)
+        g = torch.Generator(device=dev).manual_seed(T + G)
+        # compressed keys distributed like the mean of 32 N(0, 1) keys; F and Q rows N(0, 1)
+        kc = (torch.randn((B, Hkv, nw, 128), generator=g, device=dev) * (32 ** -0.5)).to(torch.bfloat16)
+        f = torch.randn((B, Hkv, n_q, 128), generator=g, device=dev).to(torch.bfloat16)
+        q = torch.randn((B, Hkv * G, n_q, 128), generator=g, device=dev).to(torch.bfloat16)
+        sel = torch.empty((B, Hkv, n_q, k_total), dtype=torch.int16, device=dev)
+        cnt = torch.empty((B, Hkv, n_q), dtype=torch.int16, device=dev)
+        q_pos0 = T - n_q
+        ws_f = ws_tensor(shape, sp.SPARDA_OP_FORECAST_SELECT, n_q, q_pos0, dev)
+        ws_m = ws_tensor(shape, sp.SPARDA_OP_MULTIHEAD_SELECT, n_q, q_pos0, dev)
+        fc = lambda: sp.sparda_forecast_select(shape, f, n_q, q_pos0, kc, sel, cnt, ws_f)
+        mh = lambda: sp.sparda_multihead_select(shape, q, n_q, q_pos0, kc, SCALE, sel, cnt, ws_m)
+        fc(); mh()
+        torch.cuda.synchronize()
+        ms_f = time_events(fc, iters, stream)
+        ms_m = time_events(mh, iters, stream)
+        return {"batch": B, "kv_heads": Hkv, "G": G, "T": T, "rows_per_group": n_q, "forecast_us": ms_f * 1e3,
+                "multihead_us": ms_m * 1e3, "multihead_over_forecast": ms_m / ms_f,
+                "multihead_path": "fused" if ws_m.numel() <= 16 else "row-wise"}
+
+    for T in (32768, 131072):
+        for Hkv, G in ((8, 4), (2, 16)):
+            out["decode"].append(one(32, Hkv, G, T, 1))
+    for Hkv, G in ((8, 4), (2, 16)):
+        out["prefill_chunk"].append(one(1, Hkv, G, 131072, 4096))
+    return out
+
+
 def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
     """The oracle on n_rows sampled (batch, group) rows of the decode step (select + attend on
     precomputed K~, as timed on the GPU), all host cores."""
@@ -442,6 +484,8 @@ def main():
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the offloaded 32-layer decode pipeline (it pins 4 x 17.2 GB of host memory)")
     ap.add_argument("--no-grid", action="store_true", help="skip the decode layer on the (32, 16) key grid")
+    ap.add_argument("--no-selectors", action="store_true",
+                    help="skip the Forecast vs multi-head selector comparison")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -528,6 +572,11 @@ def main():
         out["paper_grid"] = grid_leg(layer, dev, args.warmup, args.steps, stream)
         log(f"[bench] (32, 16) grid decode step {out['paper_grid']['us_per_layer']:.1f} us, "
             f"select {out['paper_grid']['parts_us']['select']:.1f} us")
+    if not args.no_selectors:
+        out["selectors"] = selector_leg(dev, max(5, args.steps // 5))
+        for r in out["selectors"]["decode"] + out["selectors"]["prefill_chunk"]:
+            log(f"[bench] selectors T={r['T']} n_q={r['rows_per_group']} G={r['G']}: forecast {r['forecast_us']:.1f} us, "
+                f"multi-head {r['multihead_us']:.1f} us ({r['multihead_path']}), x{r['multihead_over_forecast']:.2f}")
     if not args.no_prefill:
         layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))

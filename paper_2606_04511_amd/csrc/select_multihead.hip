@@ -17,8 +17,13 @@
 //    in the Forecast decode kernel, and each loaded window is scored by all G heads into LDS;
 //    the per-head maximum and sum, the shared scores, the max-pool and the block-wide radix
 //    select (select_block.hpp) all stay on the CU.
+//  * fused two-pass decode (n_q == 1, any other G <= 16, windows + candidates <= kMhLdsFloats):
+//    a 16-window tile times the group's heads is one MFMA chain (A = 16 windows' keys, B = the
+//    G query rows padded to 16 columns).  Pass 1 keeps an online maximum and sum of 2^z per head,
+//    pass 2 reads the keys again and adds each head's normalised weight into the shared score
+//    of the window, in LDS.
 //  * row-wise (everything else): mh_score_kernel writes every head's score of every complete
-//    window of every row to the workspace, mh_norm_kernel (one wavefront per row) turns them into
+//    window of every row to the workspace, mh_norm_kernel (one workgroup per row) turns them into
 //    the shared scores of the windows that overlap the row's candidates, and select.hip's
 //    row-wise top-k pools and selects.
 #include <math.h>
@@ -184,6 +189,134 @@ __global__ __launch_bounds__(kDecThreads) void mh_decode_kernel(SelectArgs a) {
   block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
 }
 
+// ---- fused two-pass decode (MFMA scores) ------------------------------------------------------
+
+// Lane l of a wavefront: column n = l % 16 (head n of the group), lane group j = l / 16.  A window
+// tile t covers windows 16 t .. 16 t + 15; the accumulator element e of lane (n, j) is head n's
+// score of window 16 t + 4 j + e.
+__global__ __launch_bounds__(kDecThreads) void mh_decode2_kernel(SelectArgs a) {
+  __shared__ float zs[kMhLdsFloats];  // shared scores of windows [0, NV), then block scores
+  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  __shared__ float red_m[kDecThreads / 64][16], red_s[kDecThreads / 64][16];
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 15, j = lane >> 4;
+  const int G = a.group_size;
+  const int64_t p = a.q_pos0;
+  const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
+  int16_t* out = a.sel + row * a.k_total;
+  if (wave == 0) emit_forced(out, g, a.k_total, lane);
+  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  int16_t* chosen_out = out + g.init_hi;
+  const int C = g.n_cand;
+  if (g.n_take >= C) {
+    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
+    return;
+  }
+  if (g.n_take <= 0) return;
+  const int NV = grid_win_vis(a.grid, p) + 1;
+  const int n_tiles = (NV + 15) >> 4;
+
+  // B: head n's dims 8 j + 32 ks .. + 7 (zero columns past the group's heads)
+  bf16x8 qb[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+    qb[ks] = as_bf16x8(n < G ? ld16(a.q + (row * G + n) * kHeadDim + 8 * j + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
+  // A: window 16 t + n's dims 8 j + 32 ks .. + 7 (windows past the last read the last again)
+  const uint16_t* kb = a.kc + row * a.nc_cap * kHeadDim + 8 * j;
+  auto load_tile = [&](int t, uint4 (&w)[4]) {
+    const int win = min(16 * t + n, NV - 1);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) w[ks] = ld16(kb + (int64_t)win * kHeadDim + 32 * ks);
+  };
+  auto score_tile = [&](const uint4 (&w)[4], int t, float (&z)[4]) {
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(w[ks]), qb[ks], c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) z[e] = 16 * t + 4 * j + e < NV ? c[e] * a.scale_log2 : -INFINITY;
+  };
+
+  // Pass 1: online maximum and sum of 2^z per lane, then per head (column n).
+  float m_run = -INFINITY, s_run = 0.f;
+  {
+    uint4 w0[4], w1[4];
+    int t = wave;
+    if (t < n_tiles) load_tile(t, w0);
+    for (; t < n_tiles; t += 2 * (kDecThreads / 64)) {
+      const int t1 = t + kDecThreads / 64;
+      if (t1 < n_tiles) load_tile(t1, w1);
+      float z[4];
+      score_tile(w0, t, z);
+      float mt = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+      float mn = fmaxf(m_run, mt);
+      if (mn > -INFINITY) {
+        s_run = s_run * exp2f(m_run - mn) + exp2f(z[0] - mn) + exp2f(z[1] - mn) + exp2f(z[2] - mn) + exp2f(z[3] - mn);
+        m_run = mn;
+      }
+      if (t1 >= n_tiles) break;
+      const int t2 = t1 + kDecThreads / 64;
+      if (t2 < n_tiles) load_tile(t2, w0);
+      score_tile(w1, t1, z);
+      mt = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+      mn = fmaxf(m_run, mt);
+      if (mn > -INFINITY) {
+        s_run = s_run * exp2f(m_run - mn) + exp2f(z[0] - mn) + exp2f(z[1] - mn) + exp2f(z[2] - mn) + exp2f(z[3] - mn);
+        m_run = mn;
+      }
+    }
+  }
+  // combine the four lane groups of each column, then the wavefronts
+  auto merge = [](float& m, float& s, float m2, float s2) {
+    const float mn = fmaxf(m, m2);
+    if (mn > -INFINITY) {
+      s = s * exp2f(m - mn) + s2 * exp2f(m2 - mn);
+      m = mn;
+    }
+  };
+  merge(m_run, s_run, __shfl_xor(m_run, 16, kWave), __shfl_xor(s_run, 16, kWave));
+  merge(m_run, s_run, __shfl_xor(m_run, 32, kWave), __shfl_xor(s_run, 32, kWave));
+  if (lane < 16) {
+    red_m[wave][n] = m_run;
+    red_s[wave][n] = s_run;
+  }
+  __syncthreads();
+  float M = red_m[0][n], S = red_s[0][n];
+#pragma unroll
+  for (int w = 1; w < kDecThreads / 64; ++w) merge(M, S, red_m[w][n], red_s[w][n]);
+  const float inv = n < G ? 1.0f / S : 0.f;  // columns past the group's heads add nothing
+
+  // Pass 2: the shared score of each window, the sum over the columns of each lane group.
+  {
+    uint4 w0[4];
+    for (int t = wave; t < n_tiles; t += kDecThreads / 64) {
+      load_tile(t, w0);
+      float z[4];
+      score_tile(w0, t, z);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float sh = row16_sum(n < G ? exp2f(z[e] - M) * inv : 0.f);
+        const int win = 16 * t + 4 * j + e;
+        if (n == e && win < NV) zs[win] = sh;
+      }
+    }
+  }
+  __syncthreads();
+
+  float* bs = zs + NV;
+  for (int i = tid; i < C; i += kDecThreads) {
+    const int32_t jb = g.cand_lo + i;
+    const int32_t lo = grid_win_lo(a.grid, jb), hi = min(grid_win_hi(a.grid, jb), NV - 1);
+    float m = zs[lo];
+    for (int32_t w = lo + 1; w <= hi; ++w) m = fmaxf(m, zs[w]);
+    bs[i] = m;
+  }
+  __syncthreads();
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+}
+
 // ---- row-wise path --------------------------------------------------------------------------
 
 // grid.x = row * n_chunks + chunk; a chunk is 256 windows, 64 per wavefront.  Head h's score of
@@ -206,71 +339,88 @@ __global__ __launch_bounds__(256) void mh_score_kernel(SelectArgs a, int n_chunk
 #pragma unroll
   for (int i = 0; i < 16; ++i) kw[i] = ld16(kbase + (int64_t)min(first + 4 * i + rs, NV - 1) * kHeadDim);
   float* zrow = a.ws + row * a.ws_stride;
+  // Lane c keeps head c's scores (c < G), so that each window's G scores leave in one store.
+  float keep[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) keep[i] = 0.f;
   for (int h = 0; h < a.group_size; ++h) {
     float qf[8];
     load_q8(a.q + ((bm * a.group_size + h) * a.n_q + r) * kHeadDim + c * 8, a.scale_log2, qf);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const float d = row16_sum(dot8(qf, kw[i]));
+      keep[i] = c == h ? d : keep[i];
+    }
+  }
+  if (c < a.group_size) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
       const int idx = first + 4 * i + rs;
-      if (c == 0 && idx < NV) zrow[h * hstride + idx] = d;
+      if (idx < NV) zrow[c * hstride + idx] = keep[i];
     }
   }
 }
 
-// One wavefront per row: each head's maximum and sum over the row's complete windows, then the
+// One workgroup per row: each head's maximum and sum over the row's complete windows, then the
 // shared score of every window that overlaps a candidate, written after the G heads' rows at
 // offset (window - first such window), where select.hip's row-wise top-k reads it.
-__global__ __launch_bounds__(256) void mh_norm_kernel(SelectArgs a, int64_t n_rows, int64_t hstride) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
-  if (row >= n_rows) return;
+__global__ __launch_bounds__(256) void mh_norm_kernel(SelectArgs a, int64_t hstride) {
+  __shared__ float red[4][kMhMaxRowG];
+  __shared__ float mx[kMhMaxRowG], inv[kMhMaxRowG];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t row = blockIdx.x;
   const int r = (int)(row % a.n_q);
   const int64_t p = a.q_pos0 + r;
   const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
   if (g.n_take >= g.n_cand) return;
+  const int G = a.group_size;
   const int NV = grid_win_vis(a.grid, p) + 1;
   int32_t wf, wl;
   row_windows(g, a.grid, p, &wf, &wl);
   const float* zrow = a.ws + row * a.ws_stride;
-  float* shared = a.ws + row * a.ws_stride + a.group_size * hstride;
-  float mx[kMhMaxRowG], inv[kMhMaxRowG];
-#pragma unroll
-  for (int h = 0; h < kMhMaxRowG; ++h) {
-    mx[h] = 0.f;
-    inv[h] = 0.f;
-    if (h < a.group_size) {
-      float m = -INFINITY;
-      for (int i = lane; i < NV; i += kWave) m = fmaxf(m, zrow[h * hstride + i]);
-      m = wave_max_f(m);
-      float s = 0.f;
-      for (int i = lane; i < NV; i += kWave) s += exp2f(zrow[h * hstride + i] - m);
-      mx[h] = m;
-      inv[h] = 1.0f / wave_sum_f(s);
-    }
+  float* shared = a.ws + row * a.ws_stride + G * hstride;
+  for (int h = 0; h < G; ++h) {
+    float m = -INFINITY;
+    for (int i = tid; i < NV; i += 256) m = fmaxf(m, zrow[h * hstride + i]);
+    m = wave_max_f(m);
+    if (lane == 0) red[wave][h] = m;
   }
-  for (int i = wf + lane; i <= wl; i += kWave) {
+  __syncthreads();
+  if (tid < G) mx[tid] = fmaxf(fmaxf(red[0][tid], red[1][tid]), fmaxf(red[2][tid], red[3][tid]));
+  __syncthreads();
+  for (int h = 0; h < G; ++h) {
+    const float m = mx[h];
     float s = 0.f;
-#pragma unroll
-    for (int h = 0; h < kMhMaxRowG; ++h)
-      if (h < a.group_size) s = fmaf(exp2f(zrow[h * hstride + i] - mx[h]), inv[h], s);
+    for (int i = tid; i < NV; i += 256) s += exp2f(zrow[h * hstride + i] - m);
+    s = wave_sum_f(s);
+    if (lane == 0) red[wave][h] = s;
+  }
+  __syncthreads();
+  if (tid < G) inv[tid] = 1.0f / (red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid]);
+  __syncthreads();
+  for (int i = wf + tid; i <= wl; i += 256) {
+    float s = 0.f;
+    for (int h = 0; h < G; ++h) s = fmaf(exp2f(zrow[h * hstride + i] - mx[h]), inv[h], s);
     shared[i - wf] = s;
   }
 }
 
 // ---- host -----------------------------------------------------------------------------------
 
-static bool mh_fused(int32_t G, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
-  if (n_q != 1 || !(G == 1 || G == 2 || G == 4 || G == 8)) return false;
+enum MhPath { kMhOnePass, kMhTwoPass, kMhRowwise };
+
+static MhPath mh_path(int32_t G, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  if (n_q != 1 || G > 16) return kMhRowwise;
   const RowGeom g = row_geom(q_pos0, n_init, n_local, 1 << 30);
   const int64_t nv = (int64_t)grid_win_vis(grid, q_pos0) + 1;
-  return (int64_t)G * nv + g.n_cand <= kMhLdsFloats;
+  if ((G == 1 || G == 2 || G == 4 || G == 8) && (int64_t)G * nv + g.n_cand <= kMhLdsFloats) return kMhOnePass;
+  return nv + g.n_cand <= kMhLdsFloats ? kMhTwoPass : kMhRowwise;
 }
 
 size_t multihead_ws_floats(int64_t rows, int32_t group_size, int32_t n_q, int64_t q_pos0, int32_t n_init,
                            int32_t n_local, int32_t k_total, WinGrid grid, int64_t* stride) {
   *stride = 0;
-  if (mh_fused(group_size, n_q, q_pos0, n_init, n_local, grid)) return 0;
+  if (mh_path(group_size, n_q, q_pos0, n_init, n_local, grid) != kMhRowwise) return 0;
   const int64_t pl = q_pos0 + n_q - 1;  // the last row scores the most windows
   const RowGeom gl = row_geom(pl, n_init, n_local, k_total);
   if (gl.n_take >= gl.n_cand) return 0;  // then every row takes all of its candidates
@@ -283,7 +433,12 @@ size_t multihead_ws_floats(int64_t rows, int32_t group_size, int32_t n_q, int64_
 hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
   const int G = a.group_size;
-  if (mh_fused(G, a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid)) {
+  const MhPath path = mh_path(G, a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid);
+  if (path == kMhTwoPass) {
+    hipLaunchKernelGGL(mh_decode2_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
+    return hipGetLastError();
+  }
+  if (path == kMhOnePass) {
     const dim3 grid((unsigned)rows), block(kDecThreads);
     switch (G) {
       case 1: hipLaunchKernelGGL(mh_decode_kernel<1>, grid, block, 0, stream, a); break;
@@ -303,7 +458,7 @@ hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(mh_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks, hstride);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(mh_norm_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, a, rows, hstride);
+    hipLaunchKernelGGL(mh_norm_kernel, dim3((unsigned)rows), dim3(256), 0, stream, a, hstride);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     t.ws = a.ws + G * hstride;  // the shared scores; the row stride stays ws_stride

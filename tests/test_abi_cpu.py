@@ -206,12 +206,15 @@ def test_multihead_select_arguments(lib):
     # 128K decode on the (32, 16) grid: 4 x 8191 window scores + 2045 block scores fit in LDS
     g = shape(batch=32, k_total=64, t_cap=131072, nc_cap=8191, cmp_kernel=32, cmp_stride=16)
     assert sp.sparda_workspace_size(g, op, 1, 131071) == 0
-    # G = 16 there: row-wise, (16 + 1) x 8192 floats per row for 32 x 2 rows
+    # G = 16 there, and G = 3: the two-pass fused kernel keeps only the shared scores in LDS
     g16 = shape(batch=32, n_kv_heads=2, group_size=16, k_total=64, t_cap=131072, nc_cap=8191, cmp_kernel=32,
                 cmp_stride=16)
-    assert sp.sparda_workspace_size(g16, op, 1, 131071) == 64 * 17 * 8192 * 4
-    # G = 3 decode is row-wise too: (3 + 1) x 64 floats per row
-    assert sp.sparda_workspace_size(shape(group_size=3), op, 1, 4095) == 16 * 4 * 64 * 4
+    assert sp.sparda_workspace_size(g16, op, 1, 131071) == 0
+    assert sp.sparda_workspace_size(shape(group_size=3), op, 1, 4095) == 0
+    # 512K tokens on the (32, 16) grid: 32767 windows + 8189 candidates exceed LDS: row-wise decode,
+    # (4 + 1) x 32768 floats per row
+    big = shape(batch=1, n_kv_heads=2, t_cap=524288, nc_cap=32767, k_total=64, cmp_kernel=32, cmp_stride=16)
+    assert sp.sparda_workspace_size(big, op, 1, 524287) == 2 * 5 * 32768 * 4
     # multi-row: the last row (p = 4095) has 64 complete blocks
     need = sp.sparda_workspace_size(s, op, 100, 3996)
     assert need == 2 * 8 * 100 * 5 * 64 * 4

@@ -619,8 +619,11 @@ MULTIHEAD = [
     (1, 1, 2, 20000, 1, 64, 0, 1, (32, 16)),     # fused, (32, 16), no initial block, one local block
     (2, 2, 4, 32768, 1, 64, 1, 2, (32, 16)),     # fused, (32, 16)
     (1, 1, 8, 40000, 1, 32, 1, 3, (32, 16)),     # fused, G = 8
-    (1, 2, 3, 9000, 1, 24, 1, 2, (32, 16)),      # G = 3: row-wise
-    (1, 1, 16, 12000, 1, 40, 1, 2, (32, 16)),    # G = 16: row-wise
+    (1, 2, 3, 9000, 1, 24, 1, 2, (32, 16)),      # G = 3: two-pass fused (MFMA scores)
+    (1, 1, 16, 12000, 1, 40, 1, 2, (32, 16)),    # G = 16: two-pass fused
+    (2, 2, 16, 131072, 1, 64, 1, 2, (32, 16)),   # G = 16 at 128K: two-pass fused
+    (1, 2, 4, 200000, 1, 64, 0, 1, (32, 16)),    # G = 4 past one pass's LDS: two-pass fused
+    (1, 1, 4, 524288, 1, 64, 1, 2, (32, 16)),    # 32767 windows: row-wise decode
     (1, 2, 4, 5000, 300, 12, 1, 2, (64, 64)),    # multi-row, chunk off a block boundary
     (1, 1, 4, 6000, 333, 20, 1, 1, (32, 16)),    # multi-row, (32, 16), one local block
 ]
