@@ -125,7 +125,7 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
 /*
  * sparda_multihead_select -- the same attended sets chosen by the InfLLM-V2 multi-head selector
  * that the Forecast indexer replaces (Sec. 3, three-stage block representation; its per-head
- * score is the softmax written out in the indexer-training section).  A baseline for comparing
+ * score is the softmax of the indexer-training target, Sec. 4.2).  A baseline for comparing
  * selection cost and choices; it selects from the attention queries of the same layer.
  *   q      in  : bf16 [B][Hq][n_q][D] device, Hq = n_kv_heads * group_size; heads
  *                m G .. m G + G - 1 belong to group m.

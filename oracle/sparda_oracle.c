@@ -23,7 +23,7 @@
  *              merged with the initial and local blocks.  Ties in score are broken by the lower
  *              block index.  With window = stride = block the max-pool is the identity.
  *   multihead  The InfLLM-V2 selector that SparDA replaces (Sec. 3, "three-stage block
- *              representation", whose per-head score the indexer-training section writes out as
+ *              representation", whose per-head score the indexer-training target of Sec. 4.2 writes out as
  *              its target): every one of the G query heads of a group scores the compressed keys,
  *              a softmax with the attention temperature turns each head's scores into a
  *              distribution over the keys complete at the query's position, the G distributions
