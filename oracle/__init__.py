@@ -13,6 +13,8 @@ Function map (paper sections in the C file):
                     per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
+  plan_staging                 -- App. C, NOSI step reuse (keep the previous step's staged blocks,
+                                  fetch only the newly selected ones)
 """
 from __future__ import annotations
 
@@ -100,8 +102,9 @@ def open_library(path: str):
     lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
     lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
+    lib.sparda_ref_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P]
     for name in ("compress_keys", "select_row", "forecast_select", "multihead_select_row", "multihead_select",
-                 "attend_row", "sparse_attn", "gather_blocks"):
+                 "attend_row", "sparse_attn", "gather_blocks", "plan_staging"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
 
@@ -292,3 +295,19 @@ def gather_blocks(shape: Shape, host_k, host_v, sel, cnt, stage_k=None, stage_v=
     _check(_load().sparda_ref_gather_blocks(ctypes.byref(cs), _ptr(host_k), _ptr(host_v), _ptr(sel), _ptr(cnt),
                                             _ptr(stage_k), _ptr(stage_v)), "gather_blocks")
     return stage_k, stage_v
+
+
+def plan_staging(shape: Shape, sel, cnt, q_pos: int, slot_blk, slot_len):
+    """One decode step's staging plan; slot_blk / slot_len (int16 [B][Hkv][k_total]) are updated in
+    place.  Returns (fetch, sel_staged, n_fetch)."""
+    sel = np.ascontiguousarray(sel, np.int16).reshape(shape.batch, shape.n_kv_heads, shape.k_total)
+    cnt = np.ascontiguousarray(cnt, np.int16).reshape(shape.batch, shape.n_kv_heads)
+    assert slot_blk.dtype == np.int16 and slot_len.dtype == np.int16
+    assert slot_blk.flags["C_CONTIGUOUS"] and slot_len.flags["C_CONTIGUOUS"]
+    fetch = np.empty_like(slot_blk)
+    staged = np.empty_like(slot_blk)
+    n_fetch = np.empty((shape.batch, shape.n_kv_heads), np.int32)
+    cs = shape.c()
+    _check(_load().sparda_ref_plan_staging(ctypes.byref(cs), _ptr(sel), _ptr(cnt), q_pos, _ptr(slot_blk),
+                                           _ptr(slot_len), _ptr(fetch), _ptr(staged), _ptr(n_fetch)), "plan_staging")
+    return fetch, staged, n_fetch

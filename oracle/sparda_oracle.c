@@ -33,6 +33,10 @@
  *              keys/values of the attended blocks, causal within the query's own block.
  *   gather     Sec. 4.3 and Alg. 2 (prefetch of the selected blocks): staging slot s holds the 64
  *              keys/values of block sel[s].
+ *   plan       Step-to-step reuse of the staged blocks (the NOSI engine of the efficiency setup,
+ *              App. C: each layer keeps the blocks its previous decode step attended, and a step
+ *              fetches only the newly selected ones): which staging slots keep their block and
+ *              which blocks are fetched into which slots.
  *
  * Readings of the paper that these definitions take (k counts the forced blocks, the local
  * window is block-granular and contains the query's own block, score ties go to the lower
@@ -485,5 +489,92 @@ int sparda_ref_gather_blocks(const ref_shape* s, const uint16_t* host_k, const u
       memcpy(stage_v + (bm * s->k_total + sidx) * L * D, host_v + (bm * s->t_cap + j * L) * D, bytes);
     }
   }
+  return REF_OK;
+}
+
+/* ---- App. C (NOSI step reuse): staging plan of one decode step ------------------------------- */
+
+/* A layer's staging buffer is a cache of k_total slots per (batch, group) row.  Slot s holds the
+ * first slot_len[s] tokens of block slot_blk[s] (-1: empty), as fetched by an earlier step.  Tokens
+ * never change once written, so a staged block still serves the query at position p exactly when
+ * its staged prefix covers every token of the block up to p: need(j) = min(L, p + 1 - j L).
+ *
+ * For the new attended set S (sel/cnt of a single-row select at position q_pos):
+ *   kept    -- slots holding a block of S with slot_len >= need: unchanged, no copy;
+ *   missing -- the blocks of S that no kept slot holds, in ascending block order;
+ *   free    -- every other slot, in ascending slot order; the r-th missing block goes to the r-th
+ *              free slot (fetch[s] = block, slot_blk = block, slot_len = need) and the free slots
+ *              left over are emptied (slot_blk = -1, slot_len = 0);
+ *   sel_staged[s] = the block slot s holds for this step's attention, -1 when it holds none of S.
+ * Only blocks attended by the previous step are ever kept: a slot that S does not use is emptied.
+ * fetch[s] = -1 for every slot that needs no copy; n_fetch[row] = number of missing blocks.
+ * Arrays are [B][Hkv][k_total] int16 ([B][Hkv] int32 for n_fetch); slot_blk / slot_len are read
+ * and updated in place.  Start from slot_blk = -1 everywhere. */
+int sparda_ref_plan_staging(const ref_shape* s, const int16_t* sel, const int16_t* cnt, int64_t q_pos,
+                            int16_t* slot_blk, int16_t* slot_len, int16_t* fetch, int16_t* sel_staged,
+                            int32_t* n_fetch) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (q_pos < 0 || q_pos >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t L = s->block_size, K = s->k_total;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads;
+  unsigned char* kept = (unsigned char*)malloc((size_t)K);
+  unsigned char* held = (unsigned char*)malloc((size_t)K);
+  if (!kept || !held) { free(kept); free(held); return REF_ERR_INVALID_ARG; }
+  for (int64_t row = 0; row < rows; ++row) {
+    const int16_t* srow = sel + row * K;
+    int16_t* blk = slot_blk + row * K;
+    int16_t* len = slot_len + row * K;
+    int16_t* fet = fetch + row * K;
+    int16_t* att = sel_staged + row * K;
+    int64_t n = cnt[row];
+    if (n < 0 || n > K) { free(kept); free(held); return REF_ERR_INVALID_ARG; }
+    /* kept slots, and which entries of S they hold */
+    for (int64_t i = 0; i < K; ++i) held[i] = 0;
+    for (int64_t t = 0; t < K; ++t) {
+      kept[t] = 0;
+      if (blk[t] < 0) continue;
+      const int64_t j = blk[t];
+      int64_t need = q_pos + 1 - j * L;
+      if (need > L) need = L;
+      for (int64_t i = 0; i < n; ++i) {
+        if (srow[i] == j && !held[i] && len[t] >= need) {
+          kept[t] = 1;
+          held[i] = 1;
+          break;
+        }
+      }
+    }
+    /* missing blocks in ascending order (S is ascending) into free slots in ascending order */
+    int64_t next_free = 0, fetched = 0;
+    for (int64_t t = 0; t < K; ++t) {
+      fet[t] = -1;
+      att[t] = kept[t] ? blk[t] : -1;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      if (held[i] || srow[i] < 0) continue;
+      while (next_free < K && kept[next_free]) ++next_free;
+      if (next_free >= K) { free(kept); free(held); return REF_ERR_INVALID_ARG; }
+      const int64_t j = srow[i];
+      int64_t need = q_pos + 1 - j * L;
+      if (need > L) need = L;
+      fet[next_free] = (int16_t)j;
+      att[next_free] = (int16_t)j;
+      blk[next_free] = (int16_t)j;
+      len[next_free] = (int16_t)need;
+      kept[next_free] = 1; /* taken */
+      ++next_free;
+      ++fetched;
+    }
+    for (int64_t t = 0; t < K; ++t) {
+      if (att[t] < 0) {
+        blk[t] = -1;
+        len[t] = 0;
+      }
+    }
+    n_fetch[row] = (int32_t)fetched;
+  }
+  free(kept);
+  free(held);
   return REF_OK;
 }

@@ -6,7 +6,8 @@ listed twice in a set being attended twice; on the paper's (32, 16) grid, a max-
 windows not yet complete at the query and one that skips the windows straddling a block edge; in
 the InfLLM-V2 multi-head selector, raw scores summed without the softmax, an unnormalised
 softmax, a single head standing for the group, a softmax normalised over fewer keys and a
-dropped temperature."""
+dropped temperature; in the staging plan of step-to-step reuse, a staged block kept whatever
+its token count, freed slots left holding their old blocks, and fetches placed from the top."""
 import math
 import os
 
@@ -38,6 +39,11 @@ MUTANTS = {
     "multihead_softmax_over_fewer_keys": ("for (int64_t i = 0; i < n_vis; ++i) denom += exp(z[i] - zmax);",
                                           "for (int64_t i = 1; i < n_vis - 2; ++i) denom += exp(z[i] - zmax);"),
     "multihead_temperature_dropped": ("z[i] = sm_scale * acc;", "z[i] = acc;"),
+    "plan_ignores_token_count": ("if (srow[i] == j && !held[i] && len[t] >= need) {",
+                                 "if (srow[i] == j && !held[i]) {"),
+    "plan_keeps_unattended_slots": ("      if (att[t] < 0) {\n        blk[t] = -1;", "      if (0) {\n        blk[t] = -1;"),
+    "plan_fills_from_the_top": ("while (next_free < K && kept[next_free]) ++next_free;",
+                                "while (next_free < K && kept[K - 1 - next_free]) ++next_free;"),
 }
 
 
@@ -104,8 +110,12 @@ def _pins_pass(o) -> bool:
             bsel, bcnt, _ = brute.multihead_select_rows(q, kcx, T - n_q, shp.k_total, 1, n_local, G, scale, lw, sw)
             if not (np.array_equal(msel, bsel) and np.array_equal(mcnt, bcnt)):
                 return False
+        # the staging plan of step-to-step reuse
+        import test_oracle_pins as pins
+        pins.test_plan_first_step_is_the_plain_gather_layout(o)
+        pins.test_plan_emulated_cache_serves_exact_tokens_with_minimal_fetches(o)
         return True
-    except oracle.OracleError:
+    except (oracle.OracleError, AssertionError, IndexError, TypeError):
         return False
 
 

@@ -627,3 +627,114 @@ def test_multihead_needs_every_complete_window(oracle_lib):
         oracle_lib.multihead_select(short, q, 1, T - 1, np.ascontiguousarray(kc[:, :, :-1]), MH_SCALE)
     with pytest.raises(oracle.OracleError):
         oracle_lib.multihead_select(s, q, 1, T - 1, kc, 0.0)
+
+
+# ----------------------------------------------------------------------------- NOSI step reuse: staging plan
+
+def _plan_shape(oracle, B=2, H=3, k_total=12, t_cap=64 * 200):
+    return oracle.Shape(batch=B, n_kv_heads=H, group_size=4, head_dim=128, n_init=1, n_local=2, k_total=k_total,
+                        t_cap=t_cap, nc_cap=t_cap // 64)
+
+
+def _random_set(rng, p, k_total, prev=None, keep=0.7, vary=False):
+    """An attended set for position p: initial block 0, the two local blocks, and top-k slots drawn
+    from the candidates, keeping about `keep` of the previous step's choices.  With vary, the set
+    sometimes leaves a few slots unused (the plan must handle any set, not only full ones)."""
+    blk = p // 64
+    forced = {0, blk - 1, blk}
+    cand = list(range(1, blk - 1))
+    n_sel = min(k_total - 3, len(cand))
+    if vary:
+        n_sel -= int(rng.integers(0, 4))
+    chosen = set()
+    if prev is not None:
+        old = [j for j in prev if 1 <= j <= blk - 2]
+        chosen = set(j for j in old if rng.random() < keep)
+    rest = [j for j in cand if j not in chosen]
+    rng.shuffle(rest)
+    while len(chosen) < n_sel:
+        chosen.add(rest.pop())
+    chosen = set(sorted(chosen)[:n_sel])
+    full = sorted(forced | chosen)
+    sel = np.full(k_total, -1, np.int16)
+    sel[:len(full)] = full
+    return sel, len(full)
+
+
+def test_plan_first_step_is_the_plain_gather_layout(oracle_lib):
+    s = _plan_shape(oracle_lib)
+    rng = np.random.default_rng(90)
+    sel = np.full((2, 3, 12), -1, np.int16)
+    cnt = np.zeros((2, 3), np.int16)
+    for b in range(2):
+        for m in range(3):
+            sel[b, m], cnt[b, m] = _random_set(rng, 3000, 12)
+    blk = np.full((2, 3, 12), -1, np.int16)
+    ln = np.zeros((2, 3, 12), np.int16)
+    fetch, staged, n_fetch = oracle_lib.plan_staging(s, sel, cnt, 3000, blk, ln)
+    assert np.array_equal(fetch, sel) and np.array_equal(staged, sel) and np.array_equal(n_fetch, cnt)
+    assert np.array_equal(blk, sel)
+    # the open block 3000 // 64 = 46 holds tokens 2944 .. 3000: 57 of them; complete blocks 64
+    want_len = np.where(sel == 46, 57, np.where(sel >= 0, 64, 0))
+    assert np.array_equal(ln, want_len)
+
+
+def test_plan_same_set_inside_a_block_fetches_only_the_open_block(oracle_lib):
+    s = _plan_shape(oracle_lib, B=1, H=1)
+    sel, n = _random_set(np.random.default_rng(91), 5000, 12)
+    sel, cnt = sel[None, None], np.array([[n]], np.int16)
+    blk = np.full((1, 1, 12), -1, np.int16)
+    ln = np.zeros((1, 1, 12), np.int16)
+    oracle_lib.plan_staging(s, sel, cnt, 5000, blk, ln)
+    for p in (5001, 5002, 5003):  # same block 78, one more token each step
+        fetch, staged, n_fetch = oracle_lib.plan_staging(s, sel, cnt, p, blk, ln)
+        assert n_fetch[0, 0] == 1 and set(fetch[fetch >= 0].tolist()) == {5000 // 64}
+        assert sorted(staged[staged >= 0].tolist()) == sorted(sel[0, 0, :n].tolist())
+
+
+def test_plan_emulated_cache_serves_exact_tokens_with_minimal_fetches(oracle_lib):
+    """A 300-step decode with drifting sets.  An emulated staging store records, per slot, the
+    token values copied at fetch time (tokens after the fetch position read as unwritten).  Every
+    step: the attended slots hold exactly the step's set, each of them holds every token its block
+    contributes up to p, fetches land in the lowest free slots in ascending block order, and the
+    number of fetches is |S| minus the blocks of S that the previous step attended with enough
+    tokens (the NOSI rule)."""
+    K = 12
+    s = _plan_shape(oracle_lib, B=1, H=2, k_total=K)
+    rng = np.random.default_rng(92)
+    blk = np.full((1, 2, K), -1, np.int16)
+    ln = np.zeros((1, 2, K), np.int16)
+    store = [[None] * K for _ in range(2)]  # (block, tuple of token ids written when fetched)
+    prev_sets = [None, None]
+    prev_valid = [dict(), dict()]  # block -> tokens staged, for the previous step's attended slots
+    p = 1500
+    for step in range(300):
+        p += 1 if step % 7 else 30  # mostly one token, sometimes a jump
+        sel = np.full((1, 2, K), -1, np.int16)
+        cnt = np.zeros((1, 2), np.int16)
+        for m in range(2):
+            sel[0, m], cnt[0, m] = _random_set(rng, p, K, prev_sets[m], vary=True)
+        fetch, staged, n_fetch = oracle_lib.plan_staging(s, sel, cnt, p, blk, ln)
+        for m in range(2):
+            S = set(sel[0, m, :cnt[0, m]].tolist())
+            # fetches copy the tokens written so far (<= p) of their block
+            for t in range(K):
+                j = int(fetch[0, m, t])
+                if j >= 0:
+                    store[m][t] = (j, tuple(x for x in range(64 * j, 64 * j + 64) if x <= p))
+            att = {int(staged[0, m, t]): t for t in range(K) if staged[0, m, t] >= 0}
+            assert set(att) == S and len(att) == len(S)
+            for j, t in att.items():
+                held_j, toks = store[m][t]
+                assert held_j == j
+                assert set(range(64 * j, min(64 * j + 64, p + 1))) <= set(toks), f"slot {t} stale for block {j}"
+            need = lambda j: min(64, p + 1 - 64 * j)
+            reusable = {j for j, n_tok in prev_valid[m].items() if j in S and n_tok >= need(j)}
+            assert n_fetch[0, m] == len(S) - len(reusable)
+            slots = [t for t in range(K) if fetch[0, m, t] >= 0]
+            blocks = [int(fetch[0, m, t]) for t in slots]
+            assert blocks == sorted(blocks)
+            kept = {t for t in range(K) if staged[0, m, t] >= 0 and fetch[0, m, t] < 0}
+            assert slots == [t for t in range(K) if t not in kept][:len(slots)]
+            prev_valid[m] = {int(staged[0, m, t]): len(store[m][t][1]) for t in range(K) if staged[0, m, t] >= 0}
+            prev_sets[m] = sorted(S)
