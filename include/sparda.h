@@ -14,6 +14,8 @@
  *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
+ *   sparda_plan_staging     step-to-step reuse of the staged blocks: which blocks the next gather
+ *                           must fetch (the NOSI engine of App. C)
  *
  * Conventions shared by every call:
  *   - Every function returns an int status: SPARDA_OK (0) or a negative SPARDA_ERR_* code.  No
@@ -167,6 +169,34 @@ int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
                        const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
                        void* o, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sparda_plan_staging -- step-to-step reuse of a layer's staging buffer (the NOSI inference engine
+ * of the paper's efficiency setup, App. C: each layer caches the blocks its previous decode step
+ * attended, so a step fetches only the newly selected ones).  Decode form, one call per layer and
+ * step, before that layer's gather.
+ *   sel, cnt   in : the step's selection, int16 [B][Hkv][k_total] and [B][Hkv] device (as
+ *                   sparda_forecast_select produces for n_q == 1: distinct blocks).
+ *   q_pos         : the query's position p; 0 <= p < t_cap.
+ *   slot_blk, slot_len in/out : int16 [B][Hkv][k_total] device, the staging state: slot s holds the
+ *                   first slot_len[s] tokens of block slot_blk[s] (-1: empty).  Initialise slot_blk
+ *                   to -1 (and slot_len to 0) once; the call updates both.
+ *   fetch     out : int16 [B][Hkv][k_total] device, the block to copy into slot s this step, -1
+ *                   when the slot needs no copy: pass it to sparda_gather_blocks with stage_cnt.
+ *   sel_staged out: int16 [B][Hkv][k_total] device, the block slot s holds for this step's
+ *                   attention, -1 when the step does not attend it: pass it to sparda_sparse_attn
+ *                   (kv_mode 1) with stage_cnt.
+ *   stage_cnt out : int16 [B][Hkv] device, k_total for every row.
+ *   n_fetch   out : int32 [B][Hkv] device, blocks fetched per row (the copy volume).
+ * A staged block is kept when it is an entry of the new set and covers every token of the block
+ * up to p (need(j) = min(L, p + 1 - j L) tokens; tokens never change once written); slots are
+ * examined in ascending order, each claiming the first unclaimed matching entry.  The other
+ * entries are fetched, in entry order, into the remaining slots in ascending order; slots the
+ * step does not use are emptied.  k_total <= 1024 (SPARDA_ERR_UNSUPPORTED otherwise).
+ */
+int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int16_t* cnt, int64_t q_pos,
+                        int16_t* slot_blk, int16_t* slot_len, int16_t* fetch, int16_t* sel_staged,
+                        int16_t* stage_cnt, int32_t* n_fetch, hipStream_t stream);
 
 /*
  * sparda_gather_blocks -- copy the selected blocks of a host-resident KV pool into HBM staging

@@ -56,4 +56,128 @@ hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const i
   return hipGetLastError();
 }
 
+// ---- staging plan of step-to-step reuse (the NOSI engine of the paper's efficiency setup,
+// App. C: a layer keeps the blocks its previous decode step attended and fetches only the newly
+// selected ones) --------------------------------------------------------------------------------
+//
+// Slot t of a row's staging holds the first slot_len[t] tokens of block slot_blk[t] (-1: empty).
+// A staged block serves the query at p when it covers every token of the block up to p:
+// need(j) = min(64, p + 1 - 64 j).  Slots are examined in ascending order; a slot is kept when
+// its block is an entry of the new set S not yet claimed by a lower slot and it covers need(j).
+// The entries of S that no kept slot holds are fetched, in entry order, into the free slots in
+// ascending order; slots left unused are emptied.  One wavefront per row; the set and the claim
+// flags live in the wavefront's LDS.
+
+constexpr int kPlanMaxK = 1024;
+
+__device__ __forceinline__ int plan_need(int j, int64_t p) {
+  const int64_t n = p + 1 - (int64_t)j * kBlock;
+  return n > kBlock ? kBlock : (int)n;
+}
+
+__global__ __launch_bounds__(256) void plan_staging_kernel(const int16_t* __restrict__ sel,
+                                                           const int16_t* __restrict__ cnt, int64_t p,
+                                                           int16_t* __restrict__ slot_blk, int16_t* __restrict__ slot_len,
+                                                           int16_t* __restrict__ fetch, int16_t* __restrict__ staged,
+                                                           int16_t* __restrict__ stage_cnt, int32_t* __restrict__ n_fetch,
+                                                           int64_t rows, int32_t K) {
+  __shared__ int s_set[4][kPlanMaxK];
+  __shared__ int s_held[4][kPlanMaxK];
+  __shared__ int s_kept[4][kPlanMaxK];
+  __shared__ int s_free[4][kPlanMaxK];
+  __shared__ int s_att[4][kPlanMaxK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= rows) return;
+  int* set = s_set[wave];
+  int* held = s_held[wave];
+  int* kept = s_kept[wave];
+  int* freel = s_free[wave];
+  int* satt = s_att[wave];  // the block each slot holds for this step, -1 none
+  const int16_t* srow = sel + row * K;
+  int16_t* blk = slot_blk + row * K;
+  int16_t* len = slot_len + row * K;
+  int16_t* fet = fetch + row * K;
+  int16_t* att = staged + row * K;
+  int n = cnt[row];
+  n = n < 0 ? 0 : (n > K ? K : n);
+  for (int i = lane; i < K; i += kWave) {
+    set[i] = i < n ? (int)srow[i] : -1;
+    held[i] = 0;
+  }
+  wave_lds_sync();
+  // kept slots, in ascending slot order (a slot claims the first unclaimed matching entry)
+  for (int t = 0; t < K; ++t) {
+    const int j = blk[t];
+    bool keep = false;
+    if (j >= 0 && len[t] >= plan_need(j, p)) {
+      for (int i0 = 0; i0 < n; i0 += kWave) {
+        const int i = i0 + lane;
+        const uint64_t hit = __ballot(i < n && set[i] == j && held[i] == 0);
+        if (hit) {
+          const int first = i0 + (int)__builtin_ctzll(hit);
+          if (lane == 0) held[first] = 1;
+          keep = true;
+          break;
+        }
+      }
+    }
+    if (lane == 0) kept[t] = keep ? 1 : 0;
+    wave_lds_sync();
+  }
+  // free slots in ascending order
+  int n_free = 0;
+  for (int t0 = 0; t0 < K; t0 += kWave) {
+    const int t = t0 + lane;
+    const bool fr = t < K && kept[t] == 0;
+    const uint64_t b = __ballot(fr);
+    if (fr) freel[n_free + mbcnt64(b)] = t;
+    n_free += __popcll(b);
+  }
+  for (int t = lane; t < K; t += kWave) {
+    fet[t] = -1;
+    satt[t] = kept[t] ? (int)blk[t] : -1;
+  }
+  wave_lds_sync();
+  // missing entries in entry order into the free slots in ascending order
+  int n_miss = 0;
+  for (int i0 = 0; i0 < n; i0 += kWave) {
+    const int i = i0 + lane;
+    const int j = i < n ? set[i] : -1;
+    const bool miss = i < n && held[i] == 0 && j >= 0;
+    const uint64_t b = __ballot(miss);
+    const int r = n_miss + mbcnt64(b);
+    if (miss && r < n_free) {
+      const int t = freel[r];
+      fet[t] = (int16_t)j;
+      satt[t] = j;
+      blk[t] = (int16_t)j;
+      len[t] = (int16_t)plan_need(j, p);
+    }
+    n_miss += __popcll(b);
+  }
+  wave_lds_sync();
+  for (int t = lane; t < K; t += kWave) {
+    const int a = satt[t];
+    att[t] = (int16_t)a;
+    if (a < 0) {
+      blk[t] = -1;
+      len[t] = 0;
+    }
+  }
+  if (lane == 0) {
+    stage_cnt[row] = (int16_t)K;
+    n_fetch[row] = n_miss;
+  }
+}
+
+hipError_t launch_plan_staging(const int16_t* sel, const int16_t* cnt, int64_t p, int16_t* slot_blk, int16_t* slot_len,
+                               int16_t* fetch, int16_t* staged, int16_t* stage_cnt, int32_t* n_fetch, int64_t rows,
+                               int32_t k_total, hipStream_t stream) {
+  if (k_total > kPlanMaxK) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(plan_staging_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, sel, cnt, p,
+                     slot_blk, slot_len, fetch, staged, stage_cnt, n_fetch, rows, k_total);
+  return hipGetLastError();
+}
+
 }  // namespace sparda

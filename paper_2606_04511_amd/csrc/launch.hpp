@@ -130,6 +130,9 @@ hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
 bool attn_uses_tiles(int32_t group_size, int32_t n_q, int64_t q_pos0);
 hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream);
 
+hipError_t launch_plan_staging(const int16_t* sel, const int16_t* cnt, int64_t p, int16_t* slot_blk, int16_t* slot_len,
+                               int16_t* fetch, int16_t* staged, int16_t* stage_cnt, int32_t* n_fetch, int64_t rows,
+                               int32_t k_total, hipStream_t stream);
 hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const int16_t* sel, const int16_t* cnt,
                          uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int64_t t_cap, int32_t k_total,
                          int32_t n_workgroups, hipStream_t stream);

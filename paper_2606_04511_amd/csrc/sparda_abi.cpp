@@ -302,6 +302,24 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
   return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
 }
 
+int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int16_t* cnt, int64_t q_pos,
+                        int16_t* slot_blk, int16_t* slot_len, int16_t* fetch, int16_t* sel_staged,
+                        int16_t* stage_cnt, int32_t* n_fetch, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(sel, "sel", 2)) || (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(slot_blk, "slot_blk", 2)) ||
+      (rc = check_dev(slot_len, "slot_len", 2)) || (rc = check_dev(fetch, "fetch", 2)) ||
+      (rc = check_dev(sel_staged, "sel_staged", 2)) || (rc = check_dev(stage_cnt, "stage_cnt", 2)) ||
+      (rc = check_dev(n_fetch, "n_fetch", 4)))
+    return rc;
+  if (q_pos < 0 || q_pos >= shape->t_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "q_pos %lld outside [0, t_cap)", (long long)q_pos);
+  if (shape->k_total > 1024) return fail(SPARDA_ERR_UNSUPPORTED, "k_total %d > 1024 for the staging plan", shape->k_total);
+  return hip_status(sparda::launch_plan_staging(sel, cnt, q_pos, slot_blk, slot_len, fetch, sel_staged, stage_cnt, n_fetch,
+                                                (int64_t)shape->batch * shape->n_kv_heads, shape->k_total, stream),
+                    "plan launch");
+}
+
 int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
                          const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
                          hipStream_t stream) {

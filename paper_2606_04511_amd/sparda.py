@@ -27,7 +27,7 @@ SPARDA_OP_SPARSE_ATTN = 2
 SPARDA_OP_MULTIHEAD_SELECT = 3
 
 EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
-            "sparda_gather_blocks",
+            "sparda_gather_blocks", "sparda_plan_staging",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
 
@@ -93,10 +93,11 @@ def load() -> ctypes.CDLL:
         lib.sparda_forecast_select.argtypes = [S, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]
         lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
+        lib.sparda_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P, P, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
         for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
-                     "sparda_gather_blocks",
+                     "sparda_gather_blocks", "sparda_plan_staging",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
         lib.sparda_status_string.argtypes = [ctypes.c_int]
@@ -182,3 +183,11 @@ def sparda_gather_blocks(shape: SpardaShape, host_k, host_v, sel, cnt, stage_k, 
     cs = shape.c()
     _check(load().sparda_gather_blocks(ctypes.byref(cs), _p(host_k), _p(host_v), _p(sel), _p(cnt), _p(stage_k),
                                        _p(stage_v), n_workgroups, _stream(stream)), "sparda_gather_blocks")
+
+
+def sparda_plan_staging(shape: SpardaShape, sel, cnt, q_pos: int, slot_blk, slot_len, fetch, sel_staged, stage_cnt,
+                        n_fetch, stream=None):
+    cs = shape.c()
+    _check(load().sparda_plan_staging(ctypes.byref(cs), _p(sel), _p(cnt), q_pos, _p(slot_blk), _p(slot_len), _p(fetch),
+                                      _p(sel_staged), _p(stage_cnt), _p(n_fetch), _stream(stream)),
+           "sparda_plan_staging")

@@ -223,6 +223,17 @@ def test_multihead_select_arguments(lib):
     assert sp.sparda_workspace_size(shape(k_total=64), op, 100, 3996) == 0
 
 
+def test_plan_staging_arguments(lib):
+    pl = sp.sparda_plan_staging
+    s = shape()
+    assert rc_of(pl, s, FAKE, FAKE, 4096, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # q_pos
+    assert rc_of(pl, s, FAKE, FAKE, -1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(pl, s, FAKE, FAKE, 100, None, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(pl, s, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, 0) == sp.SPARDA_ERR_INVALID_ARG
+    big = shape(k_total=1025, t_cap=131072, nc_cap=2048)
+    assert rc_of(pl, big, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_UNSUPPORTED
+
+
 def test_status_strings(lib):
     assert sp.status_string(0) == "SPARDA_OK"
     assert sp.status_string(-4) == "SPARDA_ERR_HOST_NOT_MAPPED"

@@ -692,3 +692,101 @@ def test_multihead_full_decode_t128k_samples(dev):
                                              cnt_np[b:b + 1, m:m + 1], [(0, 0, 0)])
         swaps += sw_
     say(f"  sampled {len(pairs)} rows, tie swaps {swaps}")
+
+
+# ----------------------------------------------------------------------------- step-to-step reuse of staging
+
+def _plan_run(dev, B, H, K, p0, steps, seed):
+    """GPU plan vs oracle plan, bit for bit, over a decode run with drifting sets of varying size."""
+    from test_oracle_pins import _random_set
+    s, o = shapes(B, H, 4, K, 64 * 1024, 1024)
+    rng = np.random.default_rng(seed)
+    blk_o = np.full((B, H, K), -1, np.int16)
+    len_o = np.zeros((B, H, K), np.int16)
+    blk_d = torch.full((B, H, K), -1, dtype=torch.int16, device=dev)
+    len_d = torch.zeros((B, H, K), dtype=torch.int16, device=dev)
+    fetch_d = torch.empty((B, H, K), dtype=torch.int16, device=dev)
+    staged_d = torch.empty((B, H, K), dtype=torch.int16, device=dev)
+    scnt_d = torch.empty((B, H), dtype=torch.int16, device=dev)
+    nf_d = torch.empty((B, H), dtype=torch.int32, device=dev)
+    prev = [[None] * H for _ in range(B)]
+    p = p0
+    total_fetch = total_sel = 0
+    for step in range(steps):
+        p += 1 if step % 5 else 40
+        sel = np.full((B, H, K), -1, np.int16)
+        cnt = np.zeros((B, H), np.int16)
+        for b in range(B):
+            for m in range(H):
+                sel[b, m], cnt[b, m] = _random_set(rng, p, K, prev[b][m], vary=True)
+                prev[b][m] = sel[b, m, :cnt[b, m]].tolist()
+        fetch, staged, n_fetch = oracle.plan_staging(o, sel, cnt, p, blk_o, len_o)
+        sp.sparda_plan_staging(s, torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), p, blk_d, len_d,
+                               fetch_d, staged_d, scnt_d, nf_d)
+        torch.cuda.synchronize()
+        assert np.array_equal(fetch_d.cpu().numpy(), fetch), f"step {step}: fetch"
+        assert np.array_equal(staged_d.cpu().numpy(), staged), f"step {step}: sel_staged"
+        assert np.array_equal(nf_d.cpu().numpy(), n_fetch), f"step {step}: n_fetch"
+        assert np.array_equal(blk_d.cpu().numpy(), blk_o) and np.array_equal(len_d.cpu().numpy(), len_o)
+        assert np.all(scnt_d.cpu().numpy() == K)
+        total_fetch += int(n_fetch.sum())
+        total_sel += int(cnt.sum())
+    return total_fetch, total_sel
+
+
+@pytest.mark.parametrize("B,H,K,p0,steps", [(2, 3, 12, 1500, 150), (1, 4, 64, 9000, 120), (1, 2, 200, 30000, 60)])
+def test_plan_staging_matches_oracle(dev, B, H, K, p0, steps):
+    say(f"plan staging B{B} H{H} K{K} p0 {p0} steps {steps}")
+    fetched, selected = _plan_run(dev, B, H, K, p0, steps, 77 + K)
+    say(f"  fetched {fetched} of {selected} selected blocks")
+    assert fetched < selected
+
+
+def test_reuse_pipeline_attends_exact_tokens(dev):
+    """A 45-step decode crossing block boundaries: the host pool receives each token only when it
+    is decoded (later tokens hold a sentinel), the plan decides the fetches, the gather copies only
+    them, and the staged attention must equal the oracle's attention over the true K/V."""
+    from test_oracle_pins import _random_set
+    B, H, G, K = 1, 2, 4, 16
+    T = 64 * 64
+    p0 = 64 * 50 - 20
+    w, case = make(B, H, G, T, 1, K, 8100)
+    s, o = shapes(B, H, G, K, T, T // 64)
+    k16, v16 = inputs.to_u16(case["k"]), inputs.to_u16(case["v"])
+    hk = torch.full_like(case["k"], 7.0).pin_memory()  # tokens not yet decoded: a sentinel
+    hv = torch.full_like(case["v"], -7.0).pin_memory()
+    hk[:, :, :p0] = case["k"][:, :, :p0]
+    hv[:, :, :p0] = case["v"][:, :, :p0]
+    st_k = torch.zeros(B, H, K, 64, 128, dtype=torch.bfloat16, device=dev)
+    st_v = torch.zeros_like(st_k)
+    blk_d = torch.full((B, H, K), -1, dtype=torch.int16, device=dev)
+    len_d = torch.zeros((B, H, K), dtype=torch.int16, device=dev)
+    fetch_d = torch.empty((B, H, K), dtype=torch.int16, device=dev)
+    staged_d = torch.empty((B, H, K), dtype=torch.int16, device=dev)
+    scnt_d = torch.empty((B, H), dtype=torch.int16, device=dev)
+    nf_d = torch.empty((B, H), dtype=torch.int32, device=dev)
+    rng = np.random.default_rng(5)
+    prev = [None] * H
+    worst, fetched, selected = 0.0, 0, 0
+    for step in range(45):
+        p = p0 + step
+        hk[:, :, p] = case["k"][:, :, p]  # the decoded token's K/V reach the host pool
+        hv[:, :, p] = case["v"][:, :, p]
+        sel = np.full((B, H, K), -1, np.int16)
+        cnt = np.zeros((B, H), np.int16)
+        for m in range(H):
+            sel[0, m], cnt[0, m] = _random_set(rng, p, K, prev[m], keep=0.8)
+            prev[m] = sel[0, m, :cnt[0, m]].tolist()
+        sp.sparda_plan_staging(s, torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), p, blk_d, len_d,
+                               fetch_d, staged_d, scnt_d, nf_d)
+        sp.sparda_gather_blocks(s, hk, hv, fetch_d, scnt_d, st_k, st_v, 8)
+        q = case["q"][:, :, 0:1].to(dev)
+        out = gpu_attend(s, q, 1, p, st_k, st_v, 1, staged_d, scnt_d, dev)
+        fetched += int(nf_d.sum().item())
+        selected += int(cnt.sum())
+        q16 = inputs.to_u16(case["q"][:, :, 0:1])
+        for h in range(H * G):
+            ref = oracle.attend_row(o, q16, 1, p, k16, v16, 0, sel[:, :, None], cnt[:, :, None], SCALE, 0, h, 0)
+            worst = max(worst, compare_attention(out[0, h, 0].float().cpu().numpy(), ref, f"step {step} head {h}"))
+    say(f"  fetched {fetched} of {selected} selected blocks, attention max err {worst:.3g}")
+    assert fetched < selected
