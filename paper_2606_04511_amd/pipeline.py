@@ -11,6 +11,14 @@ Per decode step and layer l (the model's projections and FFN are outside this pa
 Layer 0 keeps its KV cache in HBM and selects with its current-layer Forecast (Sec. 4.1).  Two
 staging slots alternate between layers.  All device buffers are allocated up front; a step
 allocates nothing.
+
+With reuse=True each offloaded layer keeps its own staging buffer across decode steps (the NOSI
+engine of the paper's efficiency setup, App. C): after layer l+1's selection,
+`sparda_plan_staging` keeps the staged blocks that the new set still attends and that hold every
+token up to the query, and the gather copies only the newly selected blocks (plus the open local
+block, whose newest tokens arrived since the last copy).  The attention then reads the per-slot
+block list the plan wrote.  This costs one staging buffer per offloaded layer instead of two in
+total (2 B Hkv k 64 D bytes per layer: 1.07 GB at B64, 8 KV heads, k = 64).
 """
 from __future__ import annotations
 
@@ -37,7 +45,7 @@ class DecodePipeline:
     """
 
     def __init__(self, shape: sp.SpardaShape, t_ctx: int, q, f, f0_cur, kc, k0, v0, pools, n_workgroups: int,
-                 device, sm_scale: float | None = None):
+                 device, sm_scale: float | None = None, reuse: bool = False):
         L = len(q)
         assert len(f) == L and len(kc) == L and len(pools) == L and L >= 1
         self.shape, self.t_ctx, self.L = shape, t_ctx, L
@@ -50,8 +58,19 @@ class DecodePipeline:
         self.o = [torch.empty(B, shape.n_q_heads, 1, shape.head_dim, dtype=torch.bfloat16, device=device)
                   for _ in range(L)]
         st = (B, H, K, shape.block_size, shape.head_dim)
+        self.reuse = reuse
+        n_stage = L if reuse else 2
         self.stage = [(torch.empty(st, dtype=torch.bfloat16, device=device),
-                       torch.empty(st, dtype=torch.bfloat16, device=device)) for _ in range(2)]
+                       torch.empty(st, dtype=torch.bfloat16, device=device)) if (not reuse or i >= 1) else None
+                      for i in range(n_stage)]
+        if reuse:
+            i16 = dict(dtype=torch.int16, device=device)
+            self.slot_blk = [torch.full((B, H, K), -1, **i16) for _ in range(L)]
+            self.slot_len = [torch.zeros((B, H, K), **i16) for _ in range(L)]
+            self.fetch = [torch.empty((B, H, K), **i16) for _ in range(L)]
+            self.sel_staged = [torch.empty((B, H, K), **i16) for _ in range(L)]
+            self.stage_cnt = [torch.empty((B, H), **i16) for _ in range(L)]
+            self.n_fetch = [torch.zeros((B, H), dtype=torch.int32, device=device) for _ in range(L)]
         n_sel = sp.sparda_workspace_size(shape, sp.SPARDA_OP_FORECAST_SELECT, 1, t_ctx - 1)
         n_att = sp.sparda_workspace_size(shape, sp.SPARDA_OP_SPARSE_ATTN, 1, t_ctx - 1)
         self.ws_sel = torch.empty(max(n_sel, 16), dtype=torch.uint8, device=device)
@@ -64,25 +83,47 @@ class DecodePipeline:
     def _select(self, f_rows, layer):
         sp.sparda_forecast_select(self.shape, f_rows, 1, self.t_ctx - 1, self.kc[layer], self.sel[layer],
                                   self.cnt[layer], self.ws_sel)
+        if self.reuse and layer >= 1:
+            sp.sparda_plan_staging(self.shape, self.sel[layer].view(self.shape.batch, self.shape.n_kv_heads, -1),
+                                   self.cnt[layer], self.t_ctx - 1, self.slot_blk[layer], self.slot_len[layer],
+                                   self.fetch[layer], self.sel_staged[layer], self.stage_cnt[layer],
+                                   self.n_fetch[layer])
 
     def _gather(self, layer, stream):
         hk, hv = self.pools[layer]
+        if self.reuse:
+            sk, sv = self.stage[layer]
+            sp.sparda_gather_blocks(self.shape, hk, hv, self.fetch[layer], self.stage_cnt[layer], sk, sv,
+                                    self.n_workgroups, stream)
+            return
         sk, sv = self.stage[layer % 2]
         sp.sparda_gather_blocks(self.shape, hk, hv, self.sel[layer], self.cnt[layer], sk, sv, self.n_workgroups,
                                 stream)
 
     def _attend(self, layer):
+        sel, cnt = self.sel[layer], self.cnt[layer]
         if layer == 0:
             k, v, mode = self.k0, self.v0, 0
+        elif self.reuse:
+            (k, v), mode = self.stage[layer], 1
+            sel, cnt = self.sel_staged[layer], self.stage_cnt[layer]
         else:
             k, v = self.stage[layer % 2]
             mode = 1
-        sp.sparda_sparse_attn(self.shape, self.q[layer], 1, self.t_ctx - 1, k, v, mode, self.sel[layer],
-                              self.cnt[layer], self.scale, self.o[layer], self.ws_att)
+        sp.sparda_sparse_attn(self.shape, self.q[layer], 1, self.t_ctx - 1, k, v, mode, sel, cnt, self.scale,
+                              self.o[layer], self.ws_att)
 
-    def step(self, overlap: bool = True):
+    def fetched_blocks(self) -> int:
+        """Blocks the last step's gathers copied (reuse mode; synchronises)."""
+        return int(sum(int(n.sum().item()) for n in self.n_fetch[1:]))
+
+    def step(self, overlap: bool = True, t_ctx: int | None = None):
         """Enqueue one decode step over all layers on the current stream (and the side stream).
-        overlap=False runs each gather on the compute stream right before its attention."""
+        overlap=False runs each gather on the compute stream right before its attention.  t_ctx
+        moves the query to position t_ctx - 1 (the workspaces were sized for the first t_ctx and
+        the positions of one decode run stay within the same workspace needs)."""
+        if t_ctx is not None:
+            self.t_ctx = t_ctx
         comp = torch.cuda.current_stream()
         self._select(self.f0_cur, 0)
         for l in range(self.L):
@@ -91,7 +132,7 @@ class DecodePipeline:
                 if overlap:
                     self.ev_sel[l + 1].record(comp)
                     self.side.wait_event(self.ev_sel[l + 1])
-                    if l >= 1:  # the slot of layer l+1 was last read by layer l-1's attention
+                    if l >= 1 and not self.reuse:  # the slot of layer l+1 was last read by layer l-1
                         self.side.wait_event(self.ev_attn[l - 1])
                     self._gather(l + 1, self.side)
                     self.ev_gather[l + 1].record(self.side)

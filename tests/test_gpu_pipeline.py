@@ -155,3 +155,23 @@ def test_dropped_wait_is_detected(setup):
         if not np.all(np.isfinite(o)) or np.abs(o - setup["ref_out"][l]).max() > 2e-2:
             bad += 1
     assert bad > 0, "a pipeline without the gather wait went unnoticed"
+
+
+def test_reuse_pipeline_matches_oracle_chain_and_refetches_nothing(setup):
+    """Per-layer staging with step-to-step reuse (NaN-poisoned, side stream held back): the first
+    step fetches every selected block, gives the oracle's outputs; a second step at the same
+    position (the query's block is complete, p % 64 == 63) keeps every staged block, fetches
+    nothing and gives the same outputs."""
+    say("reuse pipeline")
+    pipe = _DelayedGather(**setup["pipe_args"], reuse=True)
+    for st in pipe.stage[1:]:
+        st[0].fill_(float("nan"))
+        st[1].fill_(float("nan"))
+    torch.cuda.synchronize()
+    pipe.step()
+    check(setup, pipe)
+    first = pipe.fetched_blocks()
+    assert first == sum(int(c.sum()) for _, c, _ in setup["ref_sel"][1:])
+    pipe.step()
+    check(setup, pipe)
+    assert pipe.fetched_blocks() == 0
