@@ -13,6 +13,8 @@ Function map (paper sections in the C file):
                     per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
+  indexer_kl_row               -- Sec. 4.2, Eq. 6-7 (the indexer-training KL over the target's top-k
+                                  partition, and its gradient with respect to the Forecast row)
   plan_staging                 -- App. C, NOSI step reuse (keep the previous step's staged blocks,
                                   fetch only the newly selected ones)
 """
@@ -103,8 +105,10 @@ def open_library(path: str):
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
     lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
     lib.sparda_ref_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P]
+    lib.sparda_ref_indexer_kl_row.argtypes = [S, P, P, i64, i32, i32, P, P, i32, i64, f64, i32, i32, i32, i32, P, P,
+                                              P, P]
     for name in ("compress_keys", "select_row", "forecast_select", "multihead_select_row", "multihead_select",
-                 "attend_row", "sparse_attn", "gather_blocks", "plan_staging"):
+                 "attend_row", "sparse_attn", "gather_blocks", "plan_staging", "indexer_kl_row"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
 
@@ -311,3 +315,19 @@ def plan_staging(shape: Shape, sel, cnt, q_pos: int, slot_blk, slot_len):
     _check(_load().sparda_ref_plan_staging(ctypes.byref(cs), _ptr(sel), _ptr(cnt), q_pos, _ptr(slot_blk),
                                            _ptr(slot_len), _ptr(fetch), _ptr(staged), _ptr(n_fetch)), "plan_staging")
     return fetch, staged, n_fetch
+
+
+def indexer_kl_row(shape: Shape, q, kc_tgt, lt: int, st: int, f, kc_pred, n_q: int, q_pos0: int, sm_scale: float,
+                   k_top: int, b: int, m: int, r: int):
+    """(loss, dF float64[D], selected positions int32[k_top] (-1 padded), n_selected) of one row;
+    shape's cmp_kernel / cmp_stride give the prediction grid, kc_tgt: uint16 [B][Hkv][nt_cap][D]."""
+    q, kc_tgt, f, kc_pred = _u16(q), _u16(kc_tgt), _u16(f), _u16(kc_pred)
+    loss = np.zeros(1, np.float64)
+    dF = np.empty(shape.head_dim, np.float64)
+    sel = np.empty(max(k_top, 1), np.int32)
+    n_sel = np.zeros(1, np.int32)
+    cs = shape.c()
+    _check(_load().sparda_ref_indexer_kl_row(ctypes.byref(cs), _ptr(q), _ptr(kc_tgt), kc_tgt.shape[2], lt, st,
+                                             _ptr(f), _ptr(kc_pred), n_q, q_pos0, float(sm_scale), k_top, b, m, r,
+                                             _ptr(loss), _ptr(dF), _ptr(sel), _ptr(n_sel)), "indexer_kl_row")
+    return float(loss[0]), dF, sel[:k_top], int(n_sel[0])

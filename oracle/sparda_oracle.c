@@ -33,6 +33,12 @@
  *              keys/values of the attended blocks, causal within the query's own block.
  *   gather     Sec. 4.3 and Alg. 2 (prefetch of the selected blocks): staging slot s holds the 64
  *              keys/values of block sel[s].
+ *   kl         The indexer-training loss (Sec. 4.2, Eq. 6-7, with the fine-grained target of the
+ *              same section and the windows of the training table in App. B): a target
+ *              distribution from the attention queries over fine (2, 1) compressed keys,
+ *              max-pooled to the (32, 16) prediction grid; the Forecast softmax over that grid;
+ *              the KL divergence of their (k+1)-bucket partitions by the target's top-k set, and
+ *              its gradient with respect to the Forecast row.
  *   plan       Step-to-step reuse of the staged blocks (the NOSI engine of the efficiency setup,
  *              App. C: each layer keeps the blocks its previous decode step attended, and a step
  *              fetches only the newly selected ones): which staging slots keep their block and
@@ -576,5 +582,139 @@ int sparda_ref_plan_staging(const ref_shape* s, const int16_t* sel, const int16_
   }
   free(kept);
   free(held);
+  return REF_OK;
+}
+
+/* ---- Sec. 4.2, Eq. 6-7: the indexer-training loss of one query row --------------------------- */
+
+/* One query row (batch b, group m, row r at position p = q_pos0 + r).
+ *   s          : shape; cmp_kernel / cmp_stride give the prediction grid (l_P, s_P), normally
+ *                (32, 16); group_size G heads per group; n_init / n_local the forced blocks.
+ *   q          : bf16 [B][Hq][n_q][D] attention queries of the target layer.
+ *   kc_tgt     : bf16 [B][Hkv][nt_cap][D] target compressed keys on the grid (lt, st), normally
+ *                (2, 1): window i covers tokens [i st, i st + lt).
+ *   f          : bf16 [B][Hkv][n_q][D] Forecast rows (of the previous layer).
+ *   kc_pred    : bf16 [B][Hkv][nc_cap][D] prediction compressed keys on the grid (l_P, s_P).
+ *   sm_scale   : 1 / tau for both softmaxes.
+ *   k_top      : size of the target's selected set.
+ * Definitions:
+ *   positions  w = 0 .. N-1: the prediction windows complete at p (w s_P + l_P <= p + 1).
+ *   target     for each head h of the group, a_h = softmax over the target windows complete at p
+ *              of sm_scale q_h . K~tgt_i; the shared score is sum_h a_h,i; T_w = the largest shared
+ *              score of the target windows lying inside position w's tokens (i st >= w s_P and
+ *              i st + lt <= w s_P + l_P).
+ *   predicted  P = softmax over w < N of sm_scale F . K~pred_w.
+ *   selected   S = the k_top largest T_w (ties: lower w) among the positions whose tokens lie in
+ *              candidate blocks [n_init, blk(p) - n_local] (init and local blocks excluded).
+ *   buckets    t_c = T_c / sum_w T_w for c in S and t_rest = the rest of the target mass;
+ *              P_c for c in S and R = 1 - sum_S P_c (the predicted rest).
+ *   loss       KL(t || p) = sum_c t_c log(t_c / P_c) + t_rest log(t_rest / R), 0 log 0 = 0.
+ *   gradient   d loss / d z_w (z_w = sm_scale F . K~pred_w): P_w - t_w for w in S and
+ *              P_w (1 - t_rest / R) for the other positions; dF = sm_scale sum_w grad_w K~pred_w.
+ * Outputs: *loss, dF[D] (optional), sel[k_top] (optional: the selected positions ascending, -1
+ * padded) and *n_sel. */
+int sparda_ref_indexer_kl_row(const ref_shape* s, const uint16_t* q, const uint16_t* kc_tgt, int64_t nt_cap,
+                              int32_t lt, int32_t st, const uint16_t* f, const uint16_t* kc_pred, int32_t n_q,
+                              int64_t q_pos0, double sm_scale, int32_t k_top, int32_t b, int32_t m, int32_t r,
+                              double* loss, double* dF, int32_t* sel, int32_t* n_sel) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (b < 0 || b >= s->batch || m < 0 || m >= s->n_kv_heads || r < 0 || r >= n_q || k_top < 0) return REF_ERR_INVALID_ARG;
+  if (lt < 1 || st < 1 || !(sm_scale > 0.0)) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim, G = s->group_size, L = s->block_size, lp = s->cmp_kernel, sp_ = s->cmp_stride;
+  const int64_t p = q_pos0 + r;
+  if (p < 0 || p >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t n_pos = (p + 1 - lp) >= 0 ? (p + 1 - lp) / sp_ + 1 : 0;  /* positions 0 .. n_pos - 1 */
+  const int64_t n_tw = (p + 1 - lt) >= 0 ? (p + 1 - lt) / st + 1 : 0;    /* target windows complete at p */
+  if (n_pos > s->nc_cap || n_tw > nt_cap) return REF_ERR_INVALID_ARG;
+  const int64_t bm = (int64_t)b * s->n_kv_heads + m;
+  const uint16_t* kt = kc_tgt + bm * nt_cap * D;
+  const uint16_t* kp = kc_pred + bm * s->nc_cap * D;
+  const uint16_t* frow = f + (bm * n_q + r) * D;
+  double* shared = (double*)calloc((size_t)(n_tw > 0 ? n_tw : 1), sizeof(double));
+  double* z = (double*)malloc(sizeof(double) * (size_t)((n_tw > n_pos ? n_tw : n_pos) + 1));
+  double* T = (double*)malloc(sizeof(double) * (size_t)(n_pos + 1));
+  double* P = (double*)malloc(sizeof(double) * (size_t)(n_pos + 1));
+  scored_block* list = (scored_block*)malloc(sizeof(scored_block) * (size_t)(n_pos + 1));
+  unsigned char* in_s = (unsigned char*)calloc((size_t)(n_pos + 1), 1);
+  if (!shared || !z || !T || !P || !list || !in_s) {
+    free(shared); free(z); free(T); free(P); free(list); free(in_s);
+    return REF_ERR_INVALID_ARG;
+  }
+  /* target: per-head softmax over the fine windows, summed over the group */
+  for (int64_t hg = 0; hg < G; ++hg) {
+    const uint16_t* qh = q + (((int64_t)b * s->n_kv_heads * G + m * G + hg) * n_q + r) * D;
+    double zmax = -INFINITY;
+    for (int64_t i = 0; i < n_tw; ++i) {
+      double acc = 0.0;
+      for (int64_t e = 0; e < D; ++e) acc += sparda_ref_bf16_to_f64(qh[e]) * sparda_ref_bf16_to_f64(kt[i * D + e]);
+      z[i] = acc * sm_scale;
+      if (z[i] > zmax) zmax = z[i];
+    }
+    double den = 0.0;
+    for (int64_t i = 0; i < n_tw; ++i) den += exp(z[i] - zmax);
+    for (int64_t i = 0; i < n_tw; ++i) shared[i] += exp(z[i] - zmax) / den;
+  }
+  /* max-pool of the shared scores to the prediction positions */
+  double t_total = 0.0;
+  for (int64_t w = 0; w < n_pos; ++w) {
+    double best = 0.0;  /* shared scores are > 0; a position with no inside window pools to 0 */
+    for (int64_t i = 0; i < n_tw; ++i)
+      if (i * st >= w * sp_ && i * st + lt <= w * sp_ + lp && shared[i] > best) best = shared[i];
+    T[w] = best;
+    t_total += best;
+  }
+  /* prediction: softmax of the Forecast scores over the positions */
+  double zmax = -INFINITY;
+  for (int64_t w = 0; w < n_pos; ++w) {
+    double acc = 0.0;
+    for (int64_t e = 0; e < D; ++e) acc += sparda_ref_bf16_to_f64(frow[e]) * sparda_ref_bf16_to_f64(kp[w * D + e]);
+    z[w] = sm_scale * acc;
+    if (z[w] > zmax) zmax = z[w];
+  }
+  double pden = 0.0;
+  for (int64_t w = 0; w < n_pos; ++w) pden += exp(z[w] - zmax);
+  for (int64_t w = 0; w < n_pos; ++w) P[w] = exp(z[w] - zmax) / pden;
+  /* the target's top-k among positions inside candidate blocks */
+  const int64_t blk = p / L, cand_tok_lo = (int64_t)s->n_init * L, cand_tok_hi = (blk - s->n_local + 1) * L;
+  int64_t n_c = 0;
+  for (int64_t w = 0; w < n_pos; ++w) {
+    if (w * sp_ >= cand_tok_lo && w * sp_ + lp <= cand_tok_hi) {
+      list[n_c].score = T[w];
+      list[n_c].block = (int32_t)w;
+      ++n_c;
+    }
+  }
+  qsort(list, (size_t)n_c, sizeof(scored_block), by_score_then_index);
+  const int64_t n_take = k_top < n_c ? k_top : n_c;
+  for (int64_t c = 0; c < n_take; ++c) in_s[list[c].block] = 1;
+  /* buckets, loss and gradient */
+  double t_rest = 0.0, R = 0.0, kl = 0.0;
+  for (int64_t w = 0; w < n_pos; ++w) {
+    if (in_s[w]) {
+      const double tc = T[w] / t_total;
+      if (tc > 0.0) kl += tc * log(tc / P[w]);
+    } else {
+      t_rest += T[w] / t_total;
+      R += P[w];
+    }
+  }
+  if (t_rest > 0.0) kl += t_rest * log(t_rest / R);
+  *loss = n_pos > 0 ? kl : 0.0;
+  if (dF) {
+    for (int64_t e = 0; e < D; ++e) dF[e] = 0.0;
+    for (int64_t w = 0; w < n_pos; ++w) {
+      const double g = in_s[w] ? P[w] - T[w] / t_total : (R > 0.0 ? P[w] * (1.0 - t_rest / R) : 0.0);
+      for (int64_t e = 0; e < D; ++e) dF[e] += sm_scale * g * sparda_ref_bf16_to_f64(kp[w * D + e]);
+    }
+  }
+  if (sel) {
+    int64_t n = 0;
+    for (int64_t w = 0; w < n_pos; ++w)
+      if (in_s[w]) sel[n++] = (int32_t)w;
+    for (int64_t i = n; i < k_top; ++i) sel[i] = -1;
+  }
+  if (n_sel) *n_sel = (int32_t)n_take;
+  free(shared); free(z); free(T); free(P); free(list); free(in_s);
   return REF_OK;
 }

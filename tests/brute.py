@@ -188,3 +188,34 @@ def attend_dense_masked(q_bits, k_bits, v_bits, sel, cnt, q_pos0, group_size, sm
     w = torch.softmax(logits, dim=-1)
     w = torch.nan_to_num(w, nan=0.0)
     return torch.einsum("bhqt,bhtd->bhqd", w, vx).numpy()
+
+
+def indexer_kl(q_rows, kct, f_row, kcp, p, sm_scale, k_top, n_init, n_local, lt=2, st=1, lp=32, sp=16):
+    """The indexer-training KL of one query row, densely: q_rows [G][D], kct [n_t][D] and kcp
+    [n_p][D] as float64 arrays (compressed keys), f_row [D] float64 (a real vector, so that the
+    loss can be differentiated numerically).  Target: scipy softmax per head over the fine windows
+    complete at p, summed, then a dense (position, window) containment mask and a max; prediction:
+    scipy softmax over the positions complete at p; the top-k by a lexsort over the positions
+    inside candidate blocks; the (k+1)-bucket KL.  Returns (loss, sorted selected positions)."""
+    from scipy.special import softmax
+    n_pos = (p + 1 - lp) // sp + 1 if p + 1 >= lp else 0
+    n_tw = (p + 1 - lt) // st + 1 if p + 1 >= lt else 0
+    a = softmax(sm_scale * (q_rows @ kct[:n_tw].T), axis=-1).sum(axis=0)  # [n_tw]
+    i = np.arange(n_tw)
+    w = np.arange(n_pos)
+    inside = (i[None, :] * st >= w[:, None] * sp) & (i[None, :] * st + lt <= w[:, None] * sp + lp)
+    T = np.where(inside, a[None, :], 0.0).max(axis=1)
+    P = softmax(sm_scale * (kcp[:n_pos] @ f_row))
+    blk = p // 64
+    cand = (w * sp >= n_init * 64) & (w * sp + lp <= (blk - n_local + 1) * 64)
+    cw = w[cand]
+    order = np.lexsort((cw, -T[cw]))
+    S = np.sort(cw[order[:k_top]])
+    t = T / T.sum()
+    mask = np.zeros(n_pos, bool)
+    mask[S] = True
+    t_rest, R = t[~mask].sum(), P[~mask].sum()
+    kl = float(np.sum(t[mask] * np.log(t[mask] / P[mask])))
+    if t_rest > 0:
+        kl += float(t_rest * np.log(t_rest / R))
+    return kl, S

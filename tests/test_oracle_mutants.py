@@ -7,7 +7,9 @@ windows not yet complete at the query and one that skips the windows straddling 
 the InfLLM-V2 multi-head selector, raw scores summed without the softmax, an unnormalised
 softmax, a single head standing for the group, a softmax normalised over fewer keys and a
 dropped temperature; in the staging plan of step-to-step reuse, a staged block kept whatever
-its token count, freed slots left holding their old blocks, and fetches placed from the top."""
+its token count, freed slots left holding their old blocks, and fetches placed from the top; in
+the indexer-training loss, a sum instead of the max-pool of the target, a dropped rest bucket, a
+flipped gradient sign and local positions left among the candidates."""
 import math
 import os
 
@@ -42,6 +44,10 @@ MUTANTS = {
     "plan_ignores_token_count": ("if (srow[i] == j && !held[i] && len[t] >= need) {",
                                  "if (srow[i] == j && !held[i]) {"),
     "plan_keeps_unattended_slots": ("      if (att[t] < 0) {\n        blk[t] = -1;", "      if (0) {\n        blk[t] = -1;"),
+    "kl_sum_pool": ("&& shared[i] > best) best = shared[i];", ") best += shared[i];"),
+    "kl_no_rest_bucket": ("if (t_rest > 0.0) kl += t_rest * log(t_rest / R);", "(void)R;"),
+    "kl_gradient_sign": ("? P[w] - T[w] / t_total :", "? T[w] / t_total - P[w] :"),
+    "kl_local_positions_are_candidates": ("cand_tok_hi = (blk - s->n_local + 1) * L;", "cand_tok_hi = (blk + 1) * L;"),
     "plan_fills_from_the_top": ("while (next_free < K && kept[next_free]) ++next_free;",
                                 "while (next_free < K && kept[K - 1 - next_free]) ++next_free;"),
 }
@@ -114,6 +120,10 @@ def _pins_pass(o) -> bool:
         import test_oracle_pins as pins
         pins.test_plan_first_step_is_the_plain_gather_layout(o)
         pins.test_plan_emulated_cache_serves_exact_tokens_with_minimal_fetches(o)
+        # the indexer-training loss
+        pins.test_kl_matches_bruteforce_and_gradient_matches_finite_differences(o, 640, 2, 4, 6, 2)
+        pins.test_kl_matches_bruteforce_and_gradient_matches_finite_differences(o, 1000, 1, 2, 10, 1)
+        pins.test_kl_uniform_closed_forms(o)
         return True
     except (oracle.OracleError, AssertionError, IndexError, TypeError):
         return False

@@ -738,3 +738,67 @@ def test_plan_emulated_cache_serves_exact_tokens_with_minimal_fetches(oracle_lib
             assert slots == [t for t in range(K) if t not in kept][:len(slots)]
             prev_valid[m] = {int(staged[0, m, t]): len(store[m][t][1]) for t in range(K) if staged[0, m, t] >= 0}
             prev_sets[m] = sorted(S)
+
+
+# ----------------------------------------------------------------------------- indexer-training KL (Eq. 6-7)
+
+def _kl_case(oracle, T, n_q, G, seed, n_init=1, n_local=2, D=128):
+    """Synthetic tensors of one group: queries, fine (2, 1) and prediction (32, 16) compressed
+    keys of the same random keys, Forecast rows."""
+    s = oracle.Shape(batch=1, n_kv_heads=1, group_size=G, head_dim=D, block_size=64, n_init=n_init,
+                     n_local=n_local, k_total=8, t_cap=T, nc_cap=(T - 32) // 16 + 1, cmp_kernel=32, cmp_stride=16)
+    st_ = oracle.Shape(**{**s.__dict__, "nc_cap": T - 1, "cmp_kernel": 2, "cmp_stride": 1})
+    k = rnd_u16((1, 1, T, D), seed, 0)
+    kct = oracle.compress_keys(st_, k, T, 0, T - 1)
+    kcp = oracle.compress_keys(s, k, T, 0, s.nc_cap)
+    q = rnd_u16((1, G, n_q, D), seed, 1)
+    f = rnd_u16((1, 1, n_q, D), seed, 2)
+    return s, q, kct, f, kcp
+
+
+@pytest.mark.parametrize("T,n_q,G,k_top,n_local", [(640, 3, 4, 6, 2), (1000, 2, 2, 10, 1), (777, 2, 16, 3, 3)])
+def test_kl_matches_bruteforce_and_gradient_matches_finite_differences(oracle_lib, T, n_q, G, k_top, n_local):
+    s, q, kct, f, kcp = _kl_case(oracle_lib, T, n_q, G, 95 + G, n_local=n_local)
+    b64 = brute.bf16_bits_to_f64
+    for r in range(n_q):
+        p = T - n_q + r
+        loss, dF, sel, n_sel = oracle_lib.indexer_kl_row(s, q, kct, 2, 1, f, kcp, n_q, T - n_q, MH_SCALE, k_top, 0, 0, r)
+        qr, fr = b64(q[0, :, r]), b64(f[0, 0, r])
+        bl, bS = brute.indexer_kl(qr, b64(kct[0, 0]), fr, b64(kcp[0, 0]), p, MH_SCALE, k_top, 1, n_local)
+        assert loss == pytest.approx(bl, rel=1e-10, abs=1e-14)
+        assert list(sel[:n_sel]) == list(bS)
+        assert loss >= 0.0
+        # central differences of the brute-force loss in every coordinate of the Forecast row
+        eps = 1e-4
+        fd = np.empty(128)
+        for d in range(128):
+            e = np.zeros(128)
+            e[d] = eps
+            lp_, _ = brute.indexer_kl(qr, b64(kct[0, 0]), fr + e, b64(kcp[0, 0]), p, MH_SCALE, k_top, 1, n_local)
+            lm_, _ = brute.indexer_kl(qr, b64(kct[0, 0]), fr - e, b64(kcp[0, 0]), p, MH_SCALE, k_top, 1, n_local)
+            fd[d] = (lp_ - lm_) / (2 * eps)
+        np.testing.assert_allclose(dF, fd, rtol=1e-5, atol=1e-9)
+
+
+def test_kl_uniform_closed_forms(oracle_lib):
+    """q = 0 and F = 0: both distributions are uniform over the positions, the target's top-k is the
+    lowest candidate positions, and the partitions agree exactly, so the loss and gradient vanish.
+    k_top = 0 leaves only the rest bucket: loss 0 for any F."""
+    T, G = 900, 4
+    s, q, kct, f, kcp = _kl_case(oracle_lib, T, 1, G, 96)
+    zq, zf = np.zeros_like(q), np.zeros_like(f)
+    loss, dF, sel, n_sel = oracle_lib.indexer_kl_row(s, zq, kct, 2, 1, zf, kcp, 1, T - 1, MH_SCALE, 5, 0, 0, 0)
+    assert loss == pytest.approx(0.0, abs=1e-15) and np.allclose(dF, 0.0, atol=1e-15)
+    assert list(sel) == [4, 5, 6, 7, 8]  # positions 4.. start at token 64 (block 1, the first candidate)
+    loss, dF, _, n_sel = oracle_lib.indexer_kl_row(s, q, kct, 2, 1, f, kcp, 1, T - 1, MH_SCALE, 0, 0, 0, 0)
+    assert n_sel == 0 and loss == pytest.approx(0.0, abs=1e-15) and np.allclose(dF, 0.0, atol=1e-15)
+
+
+def test_kl_head_order_does_not_matter(oracle_lib):
+    T, G = 700, 4
+    s, q, kct, f, kcp = _kl_case(oracle_lib, T, 2, G, 97)
+    a = oracle_lib.indexer_kl_row(s, q, kct, 2, 1, f, kcp, 2, T - 2, MH_SCALE, 6, 0, 0, 1)
+    qp = np.ascontiguousarray(q[:, [3, 1, 0, 2]])
+    b = oracle_lib.indexer_kl_row(s, qp, kct, 2, 1, f, kcp, 2, T - 2, MH_SCALE, 6, 0, 0, 1)
+    assert a[0] == pytest.approx(b[0], rel=1e-13) and np.allclose(a[1], b[1], rtol=1e-12, atol=1e-16)
+    assert list(a[2]) == list(b[2])
