@@ -16,6 +16,8 @@
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
  *   sparda_plan_staging     step-to-step reuse of the staged blocks: which blocks the next gather
  *                           must fetch (the NOSI engine of App. C)
+ *   sparda_indexer_kl       Q, K, F, K~ -> the indexer-training loss and its gradient w.r.t. F
+ *                           (Sec. 4.2, Eq. 6-7)
  *
  * Conventions shared by every call:
  *   - Every function returns an int status: SPARDA_OK (0) or a negative SPARDA_ERR_* code.  No
@@ -81,7 +83,12 @@ typedef struct sparda_shape {
 } sparda_shape;
 
 /* Workspace owners for sparda_workspace_size(). */
-enum sparda_op { SPARDA_OP_FORECAST_SELECT = 1, SPARDA_OP_SPARSE_ATTN = 2, SPARDA_OP_MULTIHEAD_SELECT = 3 };
+enum sparda_op {
+  SPARDA_OP_FORECAST_SELECT = 1,
+  SPARDA_OP_SPARSE_ATTN = 2,
+  SPARDA_OP_MULTIHEAD_SELECT = 3,
+  SPARDA_OP_INDEXER_KL = 4
+};
 
 /*
  * sparda_compress_keys -- mean-pooled compressed keys (Sec. 3, Eq. 2): window i of the grid
@@ -169,6 +176,39 @@ int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
                        const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
                        void* o, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sparda_indexer_kl -- the indexer-training loss of Sec. 4.2 (Eq. 6-7) per query row, and its
+ * gradient with respect to the Forecast row (the Forecast projection is the only trained part;
+ * its weight gradient is this gradient times the layer input, a plain GEMM).
+ *   shape     : the prediction grid is shape's (cmp_kernel, cmp_stride), normally (32, 16); the
+ *               target uses fine (2, 1) windows (the training table of App. B).
+ *   q     in  : bf16 [B][Hq][n_q][D] device, the target layer's attention queries.
+ *   k     in  : bf16 [B][Hkv][t_cap][D] device, the target layer's keys (tokens up to the last
+ *               row's position are read).
+ *   f     in  : bf16 [B][Hkv][n_q][D] device, the Forecast rows of the previous layer.
+ *   k_cmp in  : bf16 [B][Hkv][nc_cap][D] device, the target layer's keys on the prediction grid;
+ *               every window complete at the last row must be < nc_cap.
+ *   n_q, q_pos0: rows and the position of row 0; every row must have a complete window
+ *               (q_pos0 >= cmp_kernel - 1); at most 16384 windows per row.
+ *   sm_scale  : 1 / tau of both softmaxes (finite, > 0).
+ *   k_top     : size of the target's selected set, 0 .. 4096.
+ *   loss  out : float [B][Hkv][n_q] device.
+ *   d_f   out : float [B][Hkv][n_q][D] device, d loss / d F.
+ *   ws, ws_bytes: device workspace of sparda_workspace_size(SPARDA_OP_INDEXER_KL) bytes (the fine
+ *               windows).
+ * Per row at position p: positions w = the prediction windows complete at p; the target T_w =
+ * max over the fine windows inside w (tokens [i, i + 2) within [w s, w s + l)) of the sum over the
+ * group's heads of softmax_i(sm_scale q_h . K~fine_i) (fine windows complete at p); the
+ * prediction P = softmax_w(sm_scale F . K~_w); S = the k_top largest T_w (ties: lower w) among
+ * positions whose tokens lie in candidate blocks [n_init, blk(p) - n_local]; loss =
+ * sum_{c in S} t_c log(t_c / P_c) + t_rest log(t_rest / R) with t = T / sum T, t_rest and R the
+ * masses outside S; d F = sm_scale sum_w g_w K~_w with g_w = P_w - t_w in S and
+ * P_w (1 - t_rest / R) outside.  float32 arithmetic (exp2 domain), bf16 inputs.
+ */
+int sparda_indexer_kl(const sparda_shape* shape, const void* q, const void* k, const void* f, const void* k_cmp,
+                      int32_t n_q, int64_t q_pos0, float sm_scale, int32_t k_top, float* loss, float* d_f,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * sparda_plan_staging -- step-to-step reuse of a layer's staging buffer (the NOSI inference engine

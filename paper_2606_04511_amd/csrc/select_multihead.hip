@@ -222,8 +222,10 @@ __global__ __launch_bounds__(kDecThreads) void mh_decode2_kernel(SelectArgs a) {
   // B: head n's dims 8 j + 32 ks .. + 7 (zero columns past the group's heads)
   bf16x8 qb[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
-    qb[ks] = as_bf16x8(n < G ? ld16(a.q + (row * G + n) * kHeadDim + 8 * j + 32 * ks) : make_uint4(0u, 0u, 0u, 0u));
+  for (int ks = 0; ks < 4; ++ks) {  // columns past the heads read head 0 (a valid address), zeroed
+    const uint4 v = ld16(a.q + (row * G + (n < G ? n : 0)) * kHeadDim + 8 * j + 32 * ks);
+    qb[ks] = as_bf16x8(n < G ? v : make_uint4(0u, 0u, 0u, 0u));
+  }
   // A: window 16 t + n's dims 8 j + 32 ks .. + 7 (windows past the last read the last again)
   const uint16_t* kb = a.kc + row * a.nc_cap * kHeadDim + 8 * j;
   auto load_tile = [&](int t, uint4 (&w)[4]) {

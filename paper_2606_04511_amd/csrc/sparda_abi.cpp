@@ -106,6 +106,12 @@ size_t multihead_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t*
          sizeof(float);
 }
 
+// Workspace of sparda_indexer_kl: the fine (2, 1) windows complete at the last row, bf16.
+size_t kl_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
+  const int64_t nt = q_pos0 + n_q - 1;
+  return (size_t)s->batch * s->n_kv_heads * (size_t)(nt > 0 ? nt : 1) * s->head_dim * sizeof(uint16_t);
+}
+
 size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps) {
   if (sparda::attn_uses_tiles(s->group_size, n_q, q_pos0)) {  // tiled multi-row kernel: no partials
     *n_splits = 1;
@@ -155,6 +161,8 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
   } else if (op == SPARDA_OP_MULTIHEAD_SELECT) {
     int64_t stride;
     *bytes = multihead_ws(shape, n_q, q_pos0, &stride);
+  } else if (op == SPARDA_OP_INDEXER_KL) {
+    *bytes = kl_ws(shape, n_q, q_pos0);
   } else {
     return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
   }
@@ -300,6 +308,36 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
   a.n_splits = ns;
   a.blocks_per_split = bps;
   return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
+}
+
+int sparda_indexer_kl(const sparda_shape* shape, const void* q, const void* k, const void* f, const void* k_cmp,
+                      int32_t n_q, int64_t q_pos0, float sm_scale, int32_t k_top, float* loss, float* d_f,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k, "k", 16)) || (rc = check_dev(f, "f", 16)) ||
+      (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(loss, "loss", 4)) || (rc = check_dev(d_f, "d_f", 4)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (!(sm_scale > 0.0f) || !std::isfinite(sm_scale))
+    return fail(SPARDA_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  if (k_top < 0 || k_top > 4096) return fail(SPARDA_ERR_INVALID_ARG, "k_top %d outside [0, 4096]", k_top);
+  if (q_pos0 < shape->cmp_kernel - 1)
+    return fail(SPARDA_ERR_INVALID_ARG, "row 0 (position %lld) has no complete window", (long long)q_pos0);
+  const int64_t pl = q_pos0 + n_q - 1;
+  const int64_t last = sparda::grid_win_vis(grid_of(shape), pl);
+  if (last >= shape->nc_cap || last + 1 > 16384)
+    return fail(SPARDA_ERR_INVALID_ARG, "window %lld of the last row beyond nc_cap %lld or 16384 per row",
+                (long long)last, (long long)shape->nc_cap);
+  const size_t need = kl_ws(shape, n_q, q_pos0);
+  if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+  if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  return hip_status(sparda::launch_indexer_kl(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                              static_cast<const uint16_t*>(f), static_cast<const uint16_t*>(k_cmp),
+                                              static_cast<uint16_t*>(ws), loss, d_f, shape->batch, shape->n_kv_heads,
+                                              shape->group_size, n_q, q_pos0, shape->t_cap, shape->nc_cap,
+                                              shape->n_init, shape->n_local, k_top, grid_of(shape), sm_scale, stream),
+                    "indexer kl launch");
 }
 
 int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int16_t* cnt, int64_t q_pos,

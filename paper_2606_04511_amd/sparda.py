@@ -25,9 +25,10 @@ SPARDA_ERR_HIP = -5
 SPARDA_OP_FORECAST_SELECT = 1
 SPARDA_OP_SPARSE_ATTN = 2
 SPARDA_OP_MULTIHEAD_SELECT = 3
+SPARDA_OP_INDEXER_KL = 4
 
 EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
-            "sparda_gather_blocks", "sparda_plan_staging",
+            "sparda_gather_blocks", "sparda_plan_staging", "sparda_indexer_kl",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
 
@@ -94,10 +95,11 @@ def load() -> ctypes.CDLL:
         lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
         lib.sparda_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P, P, P]
+        lib.sparda_indexer_kl.argtypes = [S, P, P, P, P, i32, i64, ctypes.c_float, i32, P, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
         for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
-                     "sparda_gather_blocks", "sparda_plan_staging",
+                     "sparda_gather_blocks", "sparda_plan_staging", "sparda_indexer_kl",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
         lib.sparda_status_string.argtypes = [ctypes.c_int]
@@ -191,3 +193,12 @@ def sparda_plan_staging(shape: SpardaShape, sel, cnt, q_pos: int, slot_blk, slot
     _check(load().sparda_plan_staging(ctypes.byref(cs), _p(sel), _p(cnt), q_pos, _p(slot_blk), _p(slot_len), _p(fetch),
                                       _p(sel_staged), _p(stage_cnt), _p(n_fetch), _stream(stream)),
            "sparda_plan_staging")
+
+
+def sparda_indexer_kl(shape: SpardaShape, q, k, f, k_cmp, n_q: int, q_pos0: int, sm_scale: float, k_top: int, loss, d_f,
+                      ws=None, ws_bytes: int = 0, stream=None):
+    cs = shape.c()
+    if ws is not None and not isinstance(ws, int) and ws_bytes == 0:
+        ws_bytes = ws.numel() * ws.element_size()
+    _check(load().sparda_indexer_kl(ctypes.byref(cs), _p(q), _p(k), _p(f), _p(k_cmp), n_q, q_pos0, float(sm_scale),
+                                    k_top, _p(loss), _p(d_f), _p(ws), ws_bytes, _stream(stream)), "sparda_indexer_kl")

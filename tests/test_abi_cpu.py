@@ -238,3 +238,21 @@ def test_status_strings(lib):
     assert sp.status_string(0) == "SPARDA_OK"
     assert sp.status_string(-4) == "SPARDA_ERR_HOST_NOT_MAPPED"
     assert sp.status_string(-99) == "SPARDA_ERR_UNKNOWN"
+
+
+def test_indexer_kl_arguments(lib):
+    kl = sp.sparda_indexer_kl
+    sc = 1 / math.sqrt(128)
+    g = dict(cmp_kernel=32, cmp_stride=16)
+    s = shape(nc_cap=255, **g)
+    args = lambda **kw: [kw.get("s", s), FAKE, FAKE, FAKE, FAKE, kw.get("n_q", 4), kw.get("q0", 4000), kw.get("sc", sc),
+                         kw.get("k", 8), FAKE, FAKE, kw.get("ws", FAKE), kw.get("wsb", 1 << 40), 0]
+    assert rc_of(kl, *args(sc=0.0)) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(kl, *args(k=-1)) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(kl, *args(k=4097)) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(kl, *args(q0=10, n_q=4)) == sp.SPARDA_ERR_INVALID_ARG      # row 0 has no complete window
+    assert rc_of(kl, *args(s=shape(nc_cap=200, **g))) == sp.SPARDA_ERR_INVALID_ARG  # window 248 beyond nc_cap
+    need = sp.sparda_workspace_size(s, sp.SPARDA_OP_INDEXER_KL, 4, 4000)
+    assert need == 2 * 8 * 4003 * 128 * 2  # the fine windows complete at the last row (p = 4003)
+    assert rc_of(kl, *args(ws=None)) == sp.SPARDA_ERR_WORKSPACE
+    assert rc_of(kl, *args(wsb=need - 2)) == sp.SPARDA_ERR_WORKSPACE

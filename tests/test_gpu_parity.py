@@ -790,3 +790,57 @@ def test_reuse_pipeline_attends_exact_tokens(dev):
             worst = max(worst, compare_attention(out[0, h, 0].float().cpu().numpy(), ref, f"step {step} head {h}"))
     say(f"  fetched {fetched} of {selected} selected blocks, attention max err {worst:.3g}")
     assert fetched < selected
+
+
+# ----------------------------------------------------------------------------- indexer-training loss (Eq. 6-7)
+
+KL_CASES = [
+    # B, H, G, T, n_q, k_top, n_init, n_local, grid
+    (1, 2, 4, 2048, 48, 16, 1, 2, (32, 16)),
+    (1, 1, 16, 3000, 20, 30, 1, 1, (32, 16)),
+    (2, 1, 4, 1500, 16, 0, 0, 2, (32, 16)),      # k_top = 0: only the rest bucket, loss 0
+    (1, 1, 4, 1200, 10, 4096, 1, 2, (32, 16)),   # k_top beyond the candidates: all of them
+    (1, 2, 2, 4096, 12, 12, 1, 2, (64, 64)),     # block-granular prediction grid
+    (1, 1, 4, 16384, 6, 64, 1, 2, (32, 16)),     # 1022 positions, 16K fine windows
+]
+
+
+@pytest.mark.parametrize("B,H,G,T,n_q,k_top,n_init,n_local,grid", KL_CASES)
+def test_indexer_kl_matches_oracle(dev, B, H, G, T, n_q, k_top, n_init, n_local, grid):
+    """Loss and gradient per row against the oracle.  float32 softmaxes over up to 16K keys and
+    bucket sums over up to 1K positions carry relative errors of a few 1e-6, so the bars are
+    |loss - ref| <= 2e-4 + 1e-3 |ref| and |dF - ref| <= 1e-3 |ref| + 1e-3 max |ref| + 1e-6; the
+    absolute 1e-6 covers rows whose exact gradient vanishes (k_top = 0), where float32 leaves
+    a residue of a few ulps of the bucket weights times sm_scale max |K~| ~ 1e-8."""
+    lw, sw = grid
+    say(f"indexer kl B{B} H{H} G{G} T{T} n_q{n_q} k{k_top} init {n_init} local {n_local} grid {grid}")
+    w, case = make(B, H, G, T, n_q, 8, 9100 + T + G, n_init=n_init, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nw = (T - lw) // sw + 1
+    s, o = shapes(B, H, G, 8, t_cap, nw, n_init, n_local, lw=lw, sw=sw)
+    k16 = inputs.to_u16(case["k"])
+    kcp = oracle.compress_keys(o, k16, T, 0, nw)
+    q_pos0 = T - n_q
+    ofine = oracle.Shape(**{**o.__dict__, "nc_cap": T - 1, "cmp_kernel": 2, "cmp_stride": 1})
+    kct = oracle.compress_keys(ofine, k16, T, 0, T - 1)
+    loss = torch.full((B, H, n_q), float("nan"), dtype=torch.float32, device=dev)
+    dF = torch.full((B, H, n_q, 128), float("nan"), dtype=torch.float32, device=dev)
+    wsb = sp.sparda_workspace_size(s, sp.SPARDA_OP_INDEXER_KL, n_q, q_pos0)
+    wst = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    sp.sparda_indexer_kl(s, case["q"].to(dev), case["k"].to(dev), case["f"].to(dev), inputs.from_u16(kcp, dev), n_q,
+                         q_pos0, SCALE, k_top, loss, dF, wst)
+    torch.cuda.synchronize()
+    loss_g, dF_g = loss.cpu().numpy(), dF.cpu().numpy()
+    q16, f16 = inputs.to_u16(case["q"]), inputs.to_u16(case["f"])
+    worst_l = worst_d = 0.0
+    for b in range(B):
+        for m in range(H):
+            for r in range(n_q):
+                ref, dref, _, _ = oracle.indexer_kl_row(o, q16, kct, 2, 1, f16, kcp, n_q, q_pos0, SCALE, k_top, b, m, r)
+                gl = float(loss_g[b, m, r])
+                assert abs(gl - ref) <= 2e-4 + 1e-3 * abs(ref), f"row {(b, m, r)}: loss {gl} vs {ref}"
+                tol = 1e-3 * np.abs(dref) + 1e-3 * np.abs(dref).max() + 1e-6
+                assert np.all(np.abs(dF_g[b, m, r] - dref) <= tol), f"row {(b, m, r)}: gradient"
+                worst_l = max(worst_l, abs(gl - ref))
+                worst_d = max(worst_d, float(np.abs(dF_g[b, m, r] - dref).max()))
+    say(f"  worst |loss - ref| {worst_l:.3g}, worst |dF - ref| {worst_d:.3g}")
