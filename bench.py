@@ -12,6 +12,8 @@ Secondary legs on the same JSON line:
                     row, max-pooled to block scores inside the select);
   selectors      -- selection cost of the Forecast indexer against the InfLLM-V2 multi-head
                     selector it replaces (decode at 32K/128K, a prefill chunk at 128K; G = 4, 16);
+  indexer_training -- the indexer-training loss and its Forecast gradient on a 256-row chunk at
+                    64K (Sec. 4.2);
   prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
                     selects), reported in TFLOP/s of scored (row, candidate) pairs x 2 x 128;
   prefill_attn   -- block-sparse attention of that prefill (ms);
@@ -292,6 +294,35 @@ def selector_leg(dev, iters):
     return out
 
 
+def training_leg(dev, iters):
+    """The indexer-training loss (Sec. 4.2, Eq. 6-7) with its gradient for a chunk of 256 query rows
+    at the end of a 64K-token sequence (the paper's training length), 32 query / 8 KV heads, the
+    (2, 1) target pooled to the (32, 16) prediction grid, k = 64; synthetic keys, queries and
+    Forecast rows N(0, 1).  Useful work: the target's two passes of G scores per fine window."""
+    B, H, G, T, n_q, k_top = 1, 8, 4, 65536, 256, 64
+    nw = (T - 32) // 16 + 1
+    shape = sp.SpardaShape(batch=B, n_kv_heads=H, group_size=G, k_total=64, t_cap=T, nc_cap=nw, cmp_kernel=32,
+                           cmp_stride=16)
+    g = torch.Generator(device=dev).manual_seed(77)
+    k = torch.randn((B, H, T, 128), generator=g, device=dev).to(torch.bfloat16)
+    q = torch.randn((B, H * G, n_q, 128), generator=g, device=dev).to(torch.bfloat16)
+    f = torch.randn((B, H, n_q, 128), generator=g, device=dev).to(torch.bfloat16)
+    kc = torch.empty((B, H, nw, 128), dtype=torch.bfloat16, device=dev)
+    sp.sparda_compress_keys(shape, k, T, 0, nw, kc)
+    loss = torch.empty((B, H, n_q), dtype=torch.float32, device=dev)
+    dF = torch.empty((B, H, n_q, 128), dtype=torch.float32, device=dev)
+    ws = ws_tensor(shape, sp.SPARDA_OP_INDEXER_KL, n_q, T - n_q, dev)
+    fn = lambda: sp.sparda_indexer_kl(shape, q, k, f, kc, n_q, T - n_q, SCALE, k_top, loss, dF, ws)
+    fn()
+    torch.cuda.synchronize()
+    ms = time_events(fn, iters, torch.cuda.current_stream())
+    fine = sum(T - n_q + r for r in range(n_q))  # fine windows complete per row, summed
+    flops = 2 * 2 * 128 * G * fine * B * H      # two passes of G dot products per fine window
+    return {"workload": f"indexer KL + gradient, B{B} Hq{H * G}/Hkv{H} T={T}, {n_q}-row chunk, k={k_top}, "
+                        "(2, 1) target -> (32, 16) prediction", "ms": ms, "rows_per_s": B * H * n_q / (ms * 1e-3),
+            "target_tflops": flops / (ms * 1e-3) / 1e12, "target_gflop": flops / 1e9}
+
+
 def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
     """The oracle on n_rows sampled (batch, group) rows of the decode step (select + attend on
     precomputed K~, as timed on the GPU), all host cores."""
@@ -519,6 +550,7 @@ def main():
     ap.add_argument("--no-grid", action="store_true", help="skip the decode layer on the (32, 16) key grid")
     ap.add_argument("--no-selectors", action="store_true",
                     help="skip the Forecast vs multi-head selector comparison")
+    ap.add_argument("--no-training", action="store_true", help="skip the indexer-training loss leg")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -613,6 +645,11 @@ def main():
         for r in out["selectors"]["decode"] + out["selectors"]["prefill_chunk"]:
             log(f"[bench] selectors T={r['T']} n_q={r['rows_per_group']} G={r['G']}: forecast {r['forecast_us']:.1f} us, "
                 f"multi-head {r['multihead_us']:.1f} us ({r['multihead_path']}), x{r['multihead_over_forecast']:.2f}")
+    if not args.no_training:
+        out["indexer_training"] = training_leg(dev, max(3, args.steps // 10))
+        log(f"[bench] indexer KL + gradient: {out['indexer_training']['ms']:.2f} ms for "
+            f"{out['indexer_training']['rows_per_s'] * out['indexer_training']['ms'] * 1e-3:.0f} rows at 64K, "
+            f"{out['indexer_training']['target_tflops']:.1f} TFLOP/s on the target scores")
     if not args.no_prefill:
         layer.case = None
         out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
