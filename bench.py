@@ -12,6 +12,8 @@ Secondary legs on the same JSON line:
                     row, max-pooled to block scores inside the select);
   selectors      -- selection cost of the Forecast indexer against the InfLLM-V2 multi-head
                     selector it replaces (decode at 32K/128K, a prefill chunk at 128K; G = 4, 16);
+  paper_config   -- decode (128K, B32) and chunked prefill (32K) at the paper's model configuration:
+                    32 query / 2 KV heads, k = 96 with a 32-block local window, (32, 16) grid;
   indexer_training -- the indexer-training loss and its Forecast gradient on a 256-row chunk at
                     64K (Sec. 4.2);
   prefill_select -- the fused score + top-k kernel of a 32K chunked prefill (batch 1, every row
@@ -294,6 +296,53 @@ def selector_leg(dev, iters):
     return out
 
 
+def paper_config_leg(dev, warmup, steps):
+    """The paper's model configuration (MiniCPM4.1-8B, App. C): 32 query / 2 KV heads, k = 96
+    blocks including the 32-block local window and the initial block, keys on the (32, 16) grid.
+    Decode at 128K (B32): select + attention per layer; chunked prefill at 32K (B1, all rows):
+    the fused windowed select and the tiled attention."""
+    stream = torch.cuda.current_stream()
+    res = {}
+    w = inputs.WORKLOADS["paper_decode_b32_t128k"]
+    lay = DecodeLayer(w, dev, grid=(32, 16))
+    for _ in range(warmup):
+        lay.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        lay.step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    parts = lay.bytes()
+    res["decode"] = {"workload": "decode B32 T=131072 Hq32/Hkv2 D128 block64 k96 (1 init + 32 local), (32, 16) grid",
+                     "us_per_layer": ms * 1e3, "GBps": (parts["select"] + parts["attend"]) / (ms * 1e-3) / 1e9,
+                     "select_us": time_events(lay.select, steps, stream) * 1e3,
+                     "attend_us": time_events(lay.attend, steps, stream) * 1e3}
+    del lay
+    w = inputs.WORKLOADS["paper_prefill_b1_t32k"]
+    T = w.seq_len
+    nw = (T - 32) // 16 + 1
+    shape = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size, k_total=w.k_total,
+                           t_cap=T, nc_cap=nw, n_init=w.n_init, n_local=w.n_local, cmp_kernel=32, cmp_stride=16)
+    case = inputs.make_case(w, device=dev)
+    kc = torch.zeros(w.batch, w.n_kv_heads, nw, 128, dtype=torch.bfloat16, device=dev)
+    sp.sparda_compress_keys(shape, case["k"], T, 0, nw, kc)
+    sel = torch.empty(w.batch, w.n_kv_heads, T, w.k_total, dtype=torch.int16, device=dev)
+    cnt = torch.empty(w.batch, w.n_kv_heads, T, dtype=torch.int16, device=dev)
+    o = torch.empty(w.batch, w.n_q_heads, T, 128, dtype=torch.bfloat16, device=dev)
+    ws_s = ws_tensor(shape, sp.SPARDA_OP_FORECAST_SELECT, T, 0, dev)
+    ws_a = ws_tensor(shape, sp.SPARDA_OP_SPARSE_ATTN, T, 0, dev)
+    sel_fn = lambda: sp.sparda_forecast_select(shape, case["f"], T, 0, kc, sel, cnt, ws_s)
+    att_fn = lambda: sp.sparda_sparse_attn(shape, case["q"], T, 0, case["k"], case["v"], 0, sel, cnt, SCALE, o, ws_a)
+    sel_fn()
+    att_fn()
+    torch.cuda.synchronize()
+    res["prefill"] = {"workload": "prefill B1 T=32768 Hq32/Hkv2 D128 block64 k96 (1 init + 32 local), (32, 16) grid, "
+                                  "all rows", "select_ms": time_events(sel_fn, max(3, steps // 10), stream),
+                      "attn_ms": time_events(att_fn, 3, stream)}
+    return res
+
+
 def training_leg(dev, iters):
     """The indexer-training loss (Sec. 4.2, Eq. 6-7) with its gradient for a chunk of 256 query rows
     at the end of a 64K-token sequence (the paper's training length), 32 query / 8 KV heads, the
@@ -551,6 +600,8 @@ def main():
     ap.add_argument("--no-selectors", action="store_true",
                     help="skip the Forecast vs multi-head selector comparison")
     ap.add_argument("--no-training", action="store_true", help="skip the indexer-training loss leg")
+    ap.add_argument("--no-paper-config", action="store_true",
+                    help="skip the decode and prefill at the paper's model configuration")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -645,6 +696,12 @@ def main():
         for r in out["selectors"]["decode"] + out["selectors"]["prefill_chunk"]:
             log(f"[bench] selectors T={r['T']} n_q={r['rows_per_group']} G={r['G']}: forecast {r['forecast_us']:.1f} us, "
                 f"multi-head {r['multihead_us']:.1f} us ({r['multihead_path']}), x{r['multihead_over_forecast']:.2f}")
+    if not args.no_paper_config:
+        out["paper_config"] = paper_config_leg(dev, args.warmup, args.steps)
+        pc = out["paper_config"]
+        log(f"[bench] paper configuration (Hkv2 G16 k96 local 32, (32, 16)): decode {pc['decode']['us_per_layer']:.1f} us "
+            f"(select {pc['decode']['select_us']:.1f}, attend {pc['decode']['attend_us']:.1f}); prefill 32K select "
+            f"{pc['prefill']['select_ms'] * 1e3:.0f} us, attention {pc['prefill']['attn_ms']:.2f} ms")
     if not args.no_training:
         out["indexer_training"] = training_leg(dev, max(3, args.steps // 10))
         log(f"[bench] indexer KL + gradient: {out['indexer_training']['ms']:.2f} ms for "

@@ -65,6 +65,13 @@ WORKLOADS = {
     "prefill_b1_t32k": Workload("prefill_b1_t32k", batch=1, seq_len=32768, n_q=32768, k_total=64, seed=1003),
     "pipeline_b64_t128k_l32": Workload("pipeline_b64_t128k_l32", batch=64, seq_len=131072, n_q=1, k_total=64,
                                        seed=1004, layers=32),
+    # The paper's model configuration (MiniCPM4.1-8B, App. C: 32 query / 2 KV heads, a 96-block
+    # budget holding the 32-block (2048-token) local window and one initial block), with keys on
+    # the (32, 16) grid.
+    "paper_decode_b32_t128k": Workload("paper_decode_b32_t128k", batch=32, seq_len=131072, n_q=1, n_kv_heads=2,
+                                       group_size=16, k_total=96, n_local=32, seed=1005),
+    "paper_prefill_b1_t32k": Workload("paper_prefill_b1_t32k", batch=1, seq_len=32768, n_q=32768, n_kv_heads=2,
+                                      group_size=16, k_total=96, n_local=32, seed=1006),
 }
 
 

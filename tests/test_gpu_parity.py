@@ -844,3 +844,45 @@ def test_indexer_kl_matches_oracle(dev, B, H, G, T, n_q, k_top, n_init, n_local,
                 worst_l = max(worst_l, abs(gl - ref))
                 worst_d = max(worst_d, float(np.abs(dF_g[b, m, r] - dref).max()))
     say(f"  worst |loss - ref| {worst_l:.3g}, worst |dF - ref| {worst_d:.3g}")
+
+
+def test_paper_configuration_decode_samples(dev):
+    """The paper's model configuration at full size: decode at 128K, B32, 32 query / 2 KV heads,
+    k = 96 with a 32-block local window, keys on the (32, 16) grid; sampled rows of the selection
+    and of the attention over the oracle's sets."""
+    w = inputs.WORKLOADS["paper_decode_b32_t128k"]
+    T, G = w.seq_len, w.group_size
+    nw = (T - 32) // 16 + 1
+    say("paper configuration decode: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, _ = shapes(w.batch, w.n_kv_heads, G, w.k_total, T, nw, w.n_init, w.n_local, lw=32, sw=16)
+    kc = gpu_compress(s, case["k"], T, nw, nw, dev)
+    sel, cnt = gpu_select(s, case["f"], 1, T - 1, kc, dev)
+    _, o1 = shapes(1, 1, G, w.k_total, T, nw, w.n_init, w.n_local, lw=32, sw=16)
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    rng = np.random.default_rng(31)
+    pairs = sorted(set((int(b), int(m)) for b, m in zip(rng.integers(0, w.batch, 5), rng.integers(0, w.n_kv_heads, 5))))
+    sel_mixed = sel.clone()
+    swaps = 0
+    for b, m in pairs:
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        kc_ref = oracle.compress_keys(o1, k16, T, 0, nw)
+        assert np.array_equal(inputs.to_u16(kc[b:b + 1, m:m + 1]), kc_ref)
+        f16 = inputs.to_u16(case["f"][b:b + 1, m:m + 1])
+        _, sw_ = compare_selection(o1, f16, kc_ref, 1, T - 1, sel_np[b:b + 1, m:m + 1], cnt_np[b:b + 1, m:m + 1],
+                                   [(0, 0, 0)])
+        swaps += sw_
+        ref_sel, _, _ = oracle.select_row(o1, f16, 1, T - 1, kc_ref, 0, 0, 0)
+        sel_mixed[b, m, 0] = torch.from_numpy(ref_sel)
+    out = gpu_attend(s, case["q"], 1, T - 1, case["k"], case["v"], 0, sel_mixed, cnt, dev)
+    worst = 0.0
+    for b, m in pairs[:3]:
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][b:b + 1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][b:b + 1, m * G:(m + 1) * G])
+        ssel = sel_mixed[b:b + 1, m:m + 1].cpu().numpy()
+        scnt = cnt[b:b + 1, m:m + 1].cpu().numpy()
+        for h in range(0, G, 5):
+            ref = oracle.attend_row(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE, 0, h, 0)
+            worst = max(worst, compare_attention(out[b, m * G + h, 0].float().cpu().numpy(), ref, f"{(b, m, h)}"))
+    say(f"  sampled {len(pairs)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
