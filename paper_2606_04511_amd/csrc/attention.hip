@@ -207,6 +207,192 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
   }
 }
 
+// Decode attention for groups of 7 to 16 heads: P V on MFMA.  With this many query rows per
+// block the VALU P V of sparse_attn_kernel (G x 8 FMAs per token per lane) no longer hides under
+// the loads, while P V fills a 16-column MFMA tile.  Per 64-token block a wavefront:
+//   * loads K and V as sparse_attn_kernel does and computes S^T = K Q^T (lane (n, g) holds
+//     head n's scores of tokens 16 tt + 4 g + i);
+//   * stages V in its LDS slice (272-byte rows; tokens after p are zeroed) and computes
+//     O^T += V^T P^T on v_mfma_f32_16x16x32_bf16 in two 32-token chunks: the B operand of chunk c
+//     is lane (n, g)'s own probabilities of tiles 2c and 2c + 1 rounded to bf16 (k = 8 g + j holds
+//     token 16 (2 c + j / 4) + 4 g + j % 4), the A operand (dims x those tokens) is read from LDS;
+//   * the softmax denominator sums the same bf16-rounded probabilities.
+// Lane (n, g) accumulates dims 16 dt + 4 g + e of head n in o[dt]; the wavefronts' states merge
+// through LDS (the V slices' space) as in sparse_attn_kernel.
+constexpr int kWidePitch = 136;  // uint16 per staged V row (272 B: 16-byte aligned, bank-spread)
+
+template <int G>
+__global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnArgs a) {
+  constexpr int NW = kAttnWaves;
+  __shared__ __align__(16) uint16_t vst[NW][kBlock * kWidePitch];
+  const int64_t row = blockIdx.x;
+  const int split = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = (int)(row % a.n_q);
+  const int64_t bm = row / a.n_q;
+  const int m = (int)(bm % a.n_kv_heads);
+  const int b = (int)(bm / a.n_kv_heads);
+  const int64_t p = a.q_pos0 + r;
+  const int blk = (int)(p / kBlock);
+  int n = a.cnt[row];
+  n = n > a.k_total ? a.k_total : (n < 0 ? 0 : n);
+  const int s_begin = split * a.blocks_per_split;
+  const int s_end = min(n, s_begin + a.blocks_per_split);
+  const int64_t Hq = (int64_t)a.n_kv_heads * G;
+  const float zscale = a.sm_scale * kLog2e;
+  const int hh = lane & 15;   // head (S^T column, O^T column)
+  const int grp = lane >> 4;  // k-chunk of the QK operands; token group of P; dim group of O^T
+  bf16x8 qb[4];
+  {  // columns past the group's heads read head 0 (a valid address) and are zeroed
+    const uint16_t* qrow =
+        a.q + (((int64_t)b * Hq + (int64_t)m * G + (hh < G ? hh : 0)) * a.n_q + r) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = ld16(qrow + 32 * ks);
+      qb[ks] = as_bf16x8(hh < G ? v : make_uint4(0u, 0u, 0u, 0u));
+    }
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint16_t* vs = vst[wave];
+
+  const int16_t* srow = a.sel + row * a.k_total;
+  const int entry = lane < n ? (int)srow[lane] : -1;
+  for (int s = s_begin + wave; s < s_end; s += NW) {
+    const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
+    if (j < 0 || j > blk) continue;
+    bool dup = __ballot(lane < s && entry == j) != 0ull;
+    for (int e0 = 64; e0 < s; e0 += 64) {
+      const int e = e0 + lane;
+      dup |= __ballot(e < s && (int)srow[e] == j) != 0ull;
+    }
+    if (dup) continue;
+    const int64_t base = a.kv_mode == 0 ? (bm * a.t_cap + (int64_t)j * kBlock) * kHeadDim
+                                        : ((bm * a.k_total + s) * kBlock) * kHeadDim;
+    const uint16_t* kb = a.k + base;
+    const uint16_t* vb = a.v + base;
+    uint4 kw[4][4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kw[tt][ks] = ld16(kb + (16 * tt + hh) * kHeadDim + 32 * ks + 8 * grp);
+    uint4 vw[16];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) vw[it] = ld16(vb + (4 * it + grp) * kHeadDim + 8 * hh);
+
+    f32x4 st[4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+      st[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) st[tt] = mfma16x16x32(as_bf16x8(kw[tt][ks]), qb[ks], st[tt]);
+    }
+    const int last = (j == blk) ? (int)(p - (int64_t)j * kBlock) : kBlock - 1;
+    // V into the wavefront's LDS slice, tokens after p as zeros (their values are not written)
+#pragma unroll
+    for (int it = 0; it < 16; ++it) {
+      const int tok = 4 * it + grp;
+      *reinterpret_cast<uint4*>(vs + tok * kWidePitch + 8 * hh) = tok <= last ? vw[it] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    float z[4][4];
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 16 * tt + 4 * grp + i;
+        z[tt][i] = tok <= last ? st[tt][i] * zscale : -INFINITY;
+        bmax = fmaxf(bmax, z[tt][i]);
+      }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float m_new = fmaxf(m_run, bmax);  // token 0 of a block is always <= p: finite
+    const float alpha = exp2f(m_run - m_new);
+    uint32_t pw[4][2];  // bf16 pairs of tile tt: (i = 0, 1), (i = 2, 3)
+    float psum = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int q2 = 0; q2 < 2; ++q2) {
+        const uint16_t lo = f32_to_bf16(exp2f(z[tt][2 * q2] - m_new));
+        const uint16_t hi = f32_to_bf16(exp2f(z[tt][2 * q2 + 1] - m_new));
+        psum += __uint_as_float((uint32_t)lo << 16) + __uint_as_float((uint32_t)hi << 16);
+        pw[tt][q2] = (uint32_t)lo | ((uint32_t)hi << 16);
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+    wave_lds_sync();
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 pb = as_bf16x8(make_uint4(pw[2 * c][0], pw[2 * c][1], pw[2 * c + 1][0], pw[2 * c + 1][1]));
+      // A rows: dim 16 dt + hh; k = 8 grp + jj -> token 16 (2 c + jj / 4) + 4 grp + jj % 4
+      const uint16_t* r0 = vs + (16 * (2 * c) + 4 * grp) * kWidePitch + hh;
+      const uint16_t* r1 = vs + (16 * (2 * c + 1) + 4 * grp) * kWidePitch + hh;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        uint32_t aw[4];
+#pragma unroll
+        for (int q2 = 0; q2 < 2; ++q2) {
+          aw[q2] = (uint32_t)r0[(2 * q2) * kWidePitch + 16 * dt] | ((uint32_t)r0[(2 * q2 + 1) * kWidePitch + 16 * dt] << 16);
+          aw[2 + q2] =
+              (uint32_t)r1[(2 * q2) * kWidePitch + 16 * dt] | ((uint32_t)r1[(2 * q2 + 1) * kWidePitch + 16 * dt] << 16);
+        }
+        o[dt] = mfma16x16x32(as_bf16x8(make_uint4(aw[0], aw[1], aw[2], aw[3])), pb, o[dt]);
+      }
+    }
+    wave_lds_sync();
+  }
+
+  // Merge the wavefronts' states through the V slices' space.
+  __syncthreads();
+  float* st_m = reinterpret_cast<float*>(&vst[0][0]);  // [NW][16]
+  float* st_l = st_m + NW * 16;                         // [NW][16]
+  float* st_acc = st_l + NW * 16;                       // [NW][16][128]
+  if (grp == 0) {
+    st_m[wave * 16 + hh] = m_run;
+    st_l[wave * 16 + hh] = l_run;
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) st_acc[(wave * 16 + hh) * kHeadDim + 16 * dt + 4 * grp + e] = o[dt][e];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * kHeadDim; idx += NW * 64) {
+    const int h = idx / kHeadDim, d = idx % kHeadDim;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, st_m[w * 16 + h]);
+    float L = 0.f, A = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float mw = st_m[w * 16 + h];
+        if (mw != -INFINITY) {
+          const float sc = exp2f(mw - M);
+          L = fmaf(st_l[w * 16 + h], sc, L);
+          A = fmaf(st_acc[(w * 16 + h) * kHeadDim + d], sc, A);
+        }
+      }
+    }
+    if (a.n_splits == 1) {
+      a.o[(((int64_t)b * Hq + (int64_t)m * G + h) * a.n_q + r) * kHeadDim + d] = f32_to_bf16(L > 0.f ? A / L : 0.f);
+    } else {
+      float* pp = a.ws + ((row * a.n_splits + split) * G + h) * (kHeadDim + 2);
+      if (d == 0) {
+        pp[0] = M;
+        pp[1] = L;
+      }
+      pp[2 + d] = A;
+    }
+  }
+}
+
 // Merge the split partials of one (row, head) by log-sum-exp: 128 threads, one per head dim.
 template <int G>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
@@ -275,11 +461,12 @@ void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks
 template <int G>
 static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
-  // Groups of more than 6 heads keep acc[G][8] in registers: 4 wavefronts (one per SIMD) give
-  // each wavefront the whole register file instead of spilling.
-  constexpr int NW = G <= 6 ? kAttnWaves : 4;
+  // Up to 6 heads: P V on the VALU.  7 to 16 heads: P V on MFMA (sparse_attn_wide_kernel).
   dim3 grid((unsigned)rows, (unsigned)a.n_splits);
-  hipLaunchKernelGGL((sparse_attn_kernel<G, NW>), grid, dim3(NW * 64), 0, stream, a);
+  if constexpr (G <= 6)
+    hipLaunchKernelGGL((sparse_attn_kernel<G, kAttnWaves>), grid, dim3(kAttnWaves * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((sparse_attn_wide_kernel<G>), grid, dim3(kAttnWaves * 64), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
   hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)(rows * G)), dim3(128), 0, stream, a);
