@@ -107,8 +107,9 @@ __host__ __device__ inline void row_windows(const RowGeom& g, const WinGrid& w, 
   *last = g.n_cand > 0 ? (hi < vis ? hi : vis) : *first - 1;
 }
 
-// True when the call takes the row-wise path, which keeps its scores in workspace scratch.
-bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
+// True when the call keeps its window scores in workspace scratch: the row-wise path, and decode
+// calls with fewer rows than CUs (scored by many workgroups per row).
+bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);

@@ -258,10 +258,53 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
   block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
 }
 
-// Which kernels serve a select call.
-enum SelectPath { kPathDecode, kPathTile, kPathRowwise };
+// Decode rows with their window scores already in the workspace (row stride ws_stride, window
+// wf of the row at offset 0): one workgroup per row loads them into LDS, max-pools them to block
+// scores and runs the block-wide radix select.  The second kernel of the split decode path.
+__global__ __launch_bounds__(kDecThreads) void decode_topk_kernel(SelectArgs a) {
+  __shared__ float sc[kDecodeMaxCand];
+  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
+  int16_t* out = a.sel + row * a.k_total;
+  if (wave == 0) emit_forced(out, g, a.k_total, lane);
+  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  int16_t* chosen_out = out + g.init_hi;
+  const int C = g.n_cand;
+  if (g.n_take >= C) {
+    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
+    return;
+  }
+  if (g.n_take <= 0) return;
+  int32_t wf, wl;
+  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
+  const int NW = wl - wf + 1;
+  const float* src = a.ws + row * a.ws_stride;
+  for (int i = tid; i < NW; i += kDecThreads) sc[i] = src[i];
+  __syncthreads();
+  const float* bs = sc;
+  if (!grid_is_blocks(a.grid)) {
+    const int32_t wvis = grid_win_vis(a.grid, a.q_pos0);
+    for (int i = tid; i < C; i += kDecThreads) sc[NW + i] = pooled_score(sc, a.grid, g.cand_lo + i, wf, wvis);
+    bs = sc + NW;
+    __syncthreads();
+  }
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+}
 
-static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+// Which kernels serve a select call.
+enum SelectPath { kPathDecode, kPathDecodeSplit, kPathTile, kPathRowwise };
+
+// Decode calls with fewer rows than CUs score each row with many workgroups (the row-wise score
+// kernel, 256 windows each) and select with one workgroup per row; otherwise one fused workgroup
+// per row.
+constexpr int64_t kDecodeSplitRows = 256;
+
+static SelectPath select_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local,
+                              WinGrid grid) {
   const int64_t p = q_pos0 + n_q - 1;
   const RowGeom g = row_geom(p, n_init, n_local, 1 << 30);
   int32_t wf, wl;
@@ -269,15 +312,17 @@ static SelectPath select_path(int32_t n_q, int64_t q_pos0, int32_t n_init, int32
   const int64_t nw = wl >= wf ? wl - wf + 1 : 0;
   if (n_q == 1) {  // window scores and (for a windowed grid) block scores share the LDS score array
     const int64_t need = grid_is_blocks(grid) ? g.n_cand : nw + g.n_cand;
-    return need <= kDecodeMaxCand ? kPathDecode : kPathRowwise;
+    if (need > kDecodeMaxCand) return kPathRowwise;
+    return rows < kDecodeSplitRows && nw >= 1024 ? kPathDecodeSplit : kPathDecode;
   }
   // multi-row: the fused tile kernel serves both grids up to kSelTileMaxCand candidates per row
   const bool tile_grid = grid_is_blocks(grid) || (grid.l == 32 && grid.s == 16);
   return tile_grid && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
 }
 
-bool select_needs_scratch(int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
-  return select_path(n_q, q_pos0, n_init, n_local, grid) == kPathRowwise;
+bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  const SelectPath path = select_path(rows, n_q, q_pos0, n_init, n_local, grid);
+  return path == kPathRowwise || path == kPathDecodeSplit;
 }
 
 hipError_t launch_rowwise_topk(const SelectArgs& a, hipStream_t stream) {
@@ -288,7 +333,7 @@ hipError_t launch_rowwise_topk(const SelectArgs& a, hipStream_t stream) {
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
-  const SelectPath path = select_path(a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid);
+  const SelectPath path = select_path(rows, a.n_q, a.q_pos0, a.n_init, a.n_local, a.grid);
   if (path == kPathDecode) {
     hipLaunchKernelGGL(decode_select_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
     return hipGetLastError();
@@ -304,7 +349,10 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(rowwise_topk_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, a, rows);
+  if (path == kPathDecodeSplit)
+    hipLaunchKernelGGL(decode_topk_kernel, dim3((unsigned)rows), dim3(kDecThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(rowwise_topk_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, a, rows);
   return hipGetLastError();
 }
 

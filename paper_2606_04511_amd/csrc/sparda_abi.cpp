@@ -91,9 +91,9 @@ size_t select_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t* st
   sparda::row_windows(g, grid_of(s), pl, &wf, &wl);
   const int64_t nw = wl >= wf ? (int64_t)(wl - wf + 1) : 0;
   *stride = (nw + 3) & ~(int64_t)3;
-  if (!sparda::select_needs_scratch(n_q, q_pos0, s->n_init, s->n_local, grid_of(s))) return 0;
-  if (g.n_cand == 0) return 0;
   const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  if (!sparda::select_needs_scratch(rows, n_q, q_pos0, s->n_init, s->n_local, grid_of(s))) return 0;
+  if (g.n_cand == 0) return 0;
   return (size_t)rows * (size_t)*stride * sizeof(float);
 }
 
