@@ -9,6 +9,8 @@ Function map (paper sections in the C file):
   compress_keys  -- Eq. 2 (mean-pooled compressed keys over windows of l_C tokens at stride s_C)
   select_row / forecast_select -- Eq. 1 + Eq. 4 (forced init/local blocks U top-k of the
                     max-pooled Forecast block scores)
+  forecast_score_max -- Eq. 4 scores of each row's candidates reduced to their maximum (the
+                    scoring of the selection without its top-k)
   multihead_select_row / multihead_select -- the InfLLM-V2 selector SparDA replaces (Sec. 3):
                     per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
@@ -99,6 +101,7 @@ def open_library(path: str):
     lib.sparda_ref_compress_keys.argtypes = [S, P, i64, i32, i32, P]
     lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P, P]
     lib.sparda_ref_forecast_select.argtypes = [S, P, i32, i64, P, P, P]
+    lib.sparda_ref_forecast_score_max.argtypes = [S, P, i32, i64, P, P]
     lib.sparda_ref_multihead_select_row.argtypes = [S, P, i32, i64, P, f64, i32, i32, i32, P, P, P, P]
     lib.sparda_ref_multihead_select.argtypes = [S, P, i32, i64, P, f64, P, P]
     lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
@@ -107,7 +110,7 @@ def open_library(path: str):
     lib.sparda_ref_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P]
     lib.sparda_ref_indexer_kl_row.argtypes = [S, P, P, i64, i32, i32, P, P, i32, i64, f64, i32, i32, i32, i32, P, P,
                                               P, P]
-    for name in ("compress_keys", "select_row", "forecast_select", "multihead_select_row", "multihead_select",
+    for name in ("compress_keys", "select_row", "forecast_select", "forecast_score_max", "multihead_select_row", "multihead_select",
                  "attend_row", "sparse_attn", "gather_blocks", "plan_staging", "indexer_kl_row"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
@@ -232,6 +235,16 @@ def forecast_select(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: n
     _check(_load().sparda_ref_forecast_select(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), _ptr(sel),
                                               _ptr(cnt)), "forecast_select")
     return sel, cnt
+
+
+def forecast_score_max(shape: Shape, f: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray) -> np.ndarray:
+    """Each row's largest candidate score, float64 [B][Hkv][n_q] (-inf without candidates)."""
+    f, k_cmp = _u16(f), _u16(k_cmp)
+    out = np.empty((shape.batch, shape.n_kv_heads, n_q), np.float64)
+    cs = shape.c()
+    _check(_load().sparda_ref_forecast_score_max(ctypes.byref(cs), _ptr(f), n_q, q_pos0, _ptr(k_cmp), _ptr(out)),
+           "forecast_score_max")
+    return out
 
 
 def multihead_select_row(shape: Shape, q: np.ndarray, n_q: int, q_pos0: int, k_cmp: np.ndarray, sm_scale: float,

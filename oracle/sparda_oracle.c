@@ -342,6 +342,48 @@ int sparda_ref_forecast_select(const ref_shape* s, const uint16_t* f, int32_t n_
   return err;
 }
 
+/* Each row's largest candidate score: the Eq. 4 scores of sparda_ref_forecast_select's
+ * candidates [n_init, blk(p) - n_local], max-pooled per block as there, reduced to their maximum
+ * (-inf when the row has no candidate).  It is the scoring of the selection without its top-k.
+ * row_max: double [B][Hkv][n_q]. */
+int sparda_ref_forecast_score_max(const ref_shape* s, const uint16_t* f, int32_t n_q, int64_t q_pos0,
+                                  const uint16_t* k_cmp, double* row_max) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n_q < 1 || q_pos0 < 0 || q_pos0 + n_q > s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t L = s->block_size, lw = s->cmp_kernel, sw = s->cmp_stride, D = s->head_dim;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads * n_q;
+  int err = REF_OK;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t row = 0; row < rows; ++row) {
+    const int64_t bm = row / n_q, p = q_pos0 + row % n_q;
+    forecast_ctx ctx;
+    ctx.frow = f + row * D;
+    ctx.kc = k_cmp + bm * s->nc_cap * D;
+    ctx.D = D;
+    const int64_t w_vis = (p + 1 - lw) >= 0 ? (p + 1 - lw) / sw : -1;
+    double best = -INFINITY;
+    for (int64_t j = s->n_init; j <= p / L - s->n_local; ++j) {
+      /* windows overlapping block j and complete at p, as in the selection */
+      int64_t i_lo = (j * L - lw) / sw + 1;
+      if (j * L - lw < 0) i_lo = 0;
+      int64_t i_hi = ((j + 1) * L - 1) / sw;
+      if (i_hi > w_vis) i_hi = w_vis;
+      if (i_hi >= s->nc_cap) {
+#pragma omp critical
+        err = REF_ERR_INVALID_ARG;
+        break;
+      }
+      for (int64_t i = i_lo; i <= i_hi; ++i) {
+        const double x = forecast_window_score(&ctx, i);
+        if (x > best) best = x;
+      }
+    }
+    row_max[row] = best;
+  }
+  return err;
+}
+
 /* All rows of the multi-head selector.  sel: int16 [B][Hkv][n_q][k_total]; cnt: int16 [B][Hkv][n_q]. */
 int sparda_ref_multihead_select(const ref_shape* s, const uint16_t* q, int32_t n_q, int64_t q_pos0,
                                 const uint16_t* k_cmp, double sm_scale, int16_t* sel, int16_t* cnt) {

@@ -9,7 +9,8 @@ softmax, a single head standing for the group, a softmax normalised over fewer k
 dropped temperature; in the staging plan of step-to-step reuse, a staged block kept whatever
 its token count, freed slots left holding their old blocks, and fetches placed from the top; in
 the indexer-training loss, a sum instead of the max-pool of the target, a dropped rest bucket, a
-flipped gradient sign and local positions left among the candidates."""
+flipped gradient sign and local positions left among the candidates; in the row maximum of the
+scores, a local or an initial block counted as a candidate."""
 import math
 import os
 
@@ -48,6 +49,10 @@ MUTANTS = {
     "kl_no_rest_bucket": ("if (t_rest > 0.0) kl += t_rest * log(t_rest / R);", "(void)R;"),
     "kl_gradient_sign": ("? P[w] - T[w] / t_total :", "? T[w] / t_total - P[w] :"),
     "kl_local_positions_are_candidates": ("cand_tok_hi = (blk - s->n_local + 1) * L;", "cand_tok_hi = (blk + 1) * L;"),
+    "score_max_counts_a_local_block": ("for (int64_t j = s->n_init; j <= p / L - s->n_local; ++j) {",
+                                       "for (int64_t j = s->n_init; j <= p / L - s->n_local + 1; ++j) {"),
+    "score_max_counts_the_init_block": ("for (int64_t j = s->n_init; j <= p / L - s->n_local; ++j) {",
+                                        "for (int64_t j = 0; j <= p / L - s->n_local; ++j) {"),
     "plan_fills_from_the_top": ("while (next_free < K && kept[next_free]) ++next_free;",
                                 "while (next_free < K && kept[K - 1 - next_free]) ++next_free;"),
 }
@@ -124,6 +129,9 @@ def _pins_pass(o) -> bool:
         pins.test_kl_matches_bruteforce_and_gradient_matches_finite_differences(o, 640, 2, 4, 6, 2)
         pins.test_kl_matches_bruteforce_and_gradient_matches_finite_differences(o, 1000, 1, 2, 10, 1)
         pins.test_kl_uniform_closed_forms(o)
+        # the scoring contraction alone: each row's largest candidate score
+        pins.test_score_max_closed_form_skips_forced_blocks(o)
+        pins.test_score_max_matches_bruteforce(o, 1024, 200, 1, 2, 32, 16)
         return True
     except (oracle.OracleError, AssertionError, IndexError, TypeError):
         return False

@@ -297,6 +297,46 @@ def test_select_pooled_closed_form_block_constant_keys(oracle_lib):
     assert np.isnan(scores[0]) and np.isnan(scores[8]) and np.isnan(scores[9])
 
 
+@pytest.mark.parametrize("T,n_q,n_init,n_local,lw,sw", [
+    (1280, 300, 1, 2, 64, 64), (1000, 1000, 0, 3, 64, 64), (1024, 200, 1, 2, 32, 16), (777, 97, 2, 1, 32, 16)])
+def test_score_max_matches_bruteforce(oracle_lib, T, n_q, n_init, n_local, lw, sw):
+    """Each row's largest candidate score against dense numpy scores, the explicit (block, window)
+    overlap mask of the brute-force selection, and the candidate range [n_init, blk - n_local]."""
+    s = grid_shape(oracle_lib, 2, 2, T, n_init + n_local + 3, lw, sw, n_init, n_local)
+    f = rnd_u16((2, 2, n_q, 128), 75, 1)
+    k = rnd_u16((2, 2, T, 128), 75, 2)
+    kc = oracle_lib.compress_keys(s, k, T, 0, s.nc_cap)
+    q_pos0 = T - n_q
+    got = oracle_lib.forecast_score_max(s, f, n_q, q_pos0, kc)
+    _, _, pooled = brute.select_rows_pooled(f, kc, q_pos0, s.k_total, n_init, n_local, lw, sw)
+    for r in range(n_q):
+        hi = (q_pos0 + r) // 64 - n_local
+        if hi < n_init:
+            assert np.all(got[:, :, r] == -np.inf)
+            continue
+        want = pooled[:, :, r, n_init: hi + 1].max(axis=-1)
+        assert np.allclose(got[:, :, r], want, rtol=1e-12, atol=1e-12), r
+
+
+def test_score_max_closed_form_skips_forced_blocks(oracle_lib):
+    """One key per block with known scores (F = e0): the maximum is the largest score among the
+    candidates; larger keys planted in the initial and local blocks never count, and rows whose
+    candidate range is empty get -inf."""
+    T, D = 640, 2
+    s = oracle_lib.Shape(batch=1, n_kv_heads=1, group_size=1, head_dim=D, block_size=64, n_init=1, n_local=2,
+                         k_total=4, t_cap=T, nc_cap=10)
+    to = lambda a: np.array(a, np.float32).view(np.uint32).__rshift__(16).astype(np.uint16)
+    val = [50.0, 3.0, -1.0, 7.0, 2.0, -4.0, 6.0, 1.0, 40.0, 60.0]  # blocks 0, 8, 9 are forced at p = 639
+    kc = to([[[[v, 0.0] for v in val]]])
+    pos = [0, 100, 191, 192, 300, 320, 450, 512, 575, 576, 639]
+    f = to([[[[1.0, 0.0]] * len(pos)]])
+    for i, p in enumerate(pos):
+        got = oracle_lib.forecast_score_max(s, np.ascontiguousarray(f[:, :, i:i + 1]), 1, p, kc)[0, 0, 0]
+        hi = p // 64 - 2
+        want = max(val[1: hi + 1]) if hi >= 1 else -np.inf
+        assert got == want, (p, got, want)
+
+
 def test_select_pooled_window_visibility_at_the_local_edge(oracle_lib):
     """With one local block the last candidate j = blk - 1 has a window reaching 16 tokens into the
     query's own block; it counts only once those tokens exist (p >= 64 (j + 1) + 15)."""
