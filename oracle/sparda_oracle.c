@@ -183,6 +183,20 @@ static double forecast_window_score(const void* vctx, int64_t i) {
   return dot;
 }
 
+/* The windows whose scores block j max-pools at a query whose last complete window is w_vis:
+ * every window overlapping the block's tokens [j L, (j + 1) L), i s_C < (j + 1) L and
+ * i s_C + l_C > j L, that is complete at the query (Sec. 3; the footprint and visibility
+ * readings).  The range [*i_lo, *i_hi] is empty when *i_hi < *i_lo. */
+static void block_windows(const ref_shape* s, int64_t j, int64_t w_vis, int64_t* i_lo, int64_t* i_hi) {
+  const int64_t L = s->block_size, lw = s->cmp_kernel, sw = s->cmp_stride;
+  int64_t lo = (j * L - lw) / sw + 1;
+  if (j * L - lw < 0) lo = 0;
+  int64_t hi = ((j + 1) * L - 1) / sw;
+  if (hi > w_vis) hi = w_vis;
+  *i_lo = lo;
+  *i_hi = hi;
+}
+
 /* Selection of one row at position p from window scores (Eq. 1 with the max-pool and top-k of
  * the InfLLM-V2 selector): the outputs are those of sparda_ref_select_row. */
 static int select_pooled(const ref_shape* s, int64_t p, window_score_fn score, const void* ctx, int16_t* sel_row,
@@ -216,11 +230,8 @@ static int select_pooled(const ref_shape* s, int64_t p, window_score_fn score, c
   if (!list) return REF_ERR_INVALID_ARG;
   for (int64_t c = 0; c < n_cand; ++c) {
     const int64_t j = cand_lo + c;
-    /* windows overlapping block j: i s_C < (j + 1) L and i s_C + l_C > j L, complete at p */
-    int64_t i_lo = (j * L - lw) / sw + 1;
-    if (j * L - lw < 0) i_lo = 0;
-    int64_t i_hi = ((j + 1) * L - 1) / sw;
-    if (i_hi > w_vis) i_hi = w_vis;
+    int64_t i_lo, i_hi;
+    block_windows(s, j, w_vis, &i_lo, &i_hi);
     if (i_hi >= s->nc_cap) { free(list); return REF_ERR_INVALID_ARG; }
     double best = -INFINITY;
     int64_t best_i = -1;
@@ -364,11 +375,8 @@ int sparda_ref_forecast_score_max(const ref_shape* s, const uint16_t* f, int32_t
     const int64_t w_vis = (p + 1 - lw) >= 0 ? (p + 1 - lw) / sw : -1;
     double best = -INFINITY;
     for (int64_t j = s->n_init; j <= p / L - s->n_local; ++j) {
-      /* windows overlapping block j and complete at p, as in the selection */
-      int64_t i_lo = (j * L - lw) / sw + 1;
-      if (j * L - lw < 0) i_lo = 0;
-      int64_t i_hi = ((j + 1) * L - 1) / sw;
-      if (i_hi > w_vis) i_hi = w_vis;
+      int64_t i_lo, i_hi;
+      block_windows(s, j, w_vis, &i_lo, &i_hi);
       if (i_hi >= s->nc_cap) {
 #pragma omp critical
         err = REF_ERR_INVALID_ARG;

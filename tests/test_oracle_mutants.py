@@ -33,8 +33,8 @@ MUTANTS = {
     "compress_truncates": ("double q = nearbyint(ldexp(m, 8));", "double q = floor(ldexp(m, 8));"),
     "compress_wrong_divisor": ("sum / (double)lw", "sum / (double)(lw - 1)"),
     "duplicate_attended_twice": ("if (seen) continue;", "(void)seen;"),
-    "pool_ignores_visibility": ("if (i_hi > w_vis) i_hi = w_vis;", "(void)w_vis;"),
-    "pool_inner_windows_only": ("int64_t i_lo = (j * L - lw) / sw + 1;", "int64_t i_lo = (j * L) / sw;"),
+    "pool_ignores_visibility": ("if (hi > w_vis) hi = w_vis;", "(void)w_vis;"),
+    "pool_inner_windows_only": ("int64_t lo = (j * L - lw) / sw + 1;", "int64_t lo = (j * L) / sw;"),
     "multihead_raw_sum": ("shared[i] += exp(z[i] - zmax) / denom;", "shared[i] += z[i];"),
     "multihead_unnormalised": ("shared[i] += exp(z[i] - zmax) / denom;", "shared[i] += exp(z[i] - zmax);"),
     "multihead_first_head_only": ("for (int64_t h = m * G; h < (m + 1) * G; ++h)",
