@@ -186,6 +186,17 @@ def prefill_leg(dev, warmup, iters):
     attend()
     ms_att = time_events(attend, max(2, iters // 10), stream)
 
+    # diagnostic: the score contraction alone (every candidate of every row scored on MFMA, each
+    # row's scores reduced to their maximum on chip; no top-k, 1 float per row written)
+    row_max = torch.empty(w.batch, w.n_kv_heads, T, dtype=torch.float32, device=dev)
+
+    def score_only():
+        sp.sparda_forecast_score_max(shape, case["f"], T, 0, kc, row_max)
+
+    for _ in range(warmup):
+        score_only()
+    ms_score = time_events(score_only, iters, stream)
+
     # the same selection on the paper's (32, 16) key grid (row-wise path: window scores in the
     # workspace, max-pooled to block scores by the top-k kernel)
     nw = (T - 32) // 16 + 1
@@ -203,17 +214,22 @@ def prefill_leg(dev, warmup, iters):
     del kc_g, ws_g
     # scored (row, candidate) pairs: rows whose candidates outnumber their free slots
     flops = 0
+    score_flops = 0  # every causal (row, candidate) pair
     attn_flops = 0
     for r in range(T):
         blk = r // 64
         n_cand = max(0, blk - w.n_local - w.n_init + 1)
+        score_flops += 2 * 128 * n_cand
         n_forced = min(w.n_init, blk + 1) + (blk - max(max(0, blk - w.n_local + 1), min(w.n_init, blk + 1)) + 1)
         if w.k_total - n_forced < n_cand:
             flops += 2 * 128 * n_cand
         n_sel_blocks = min(w.k_total, blk + 1)
         attn_flops += 4 * 128 * ((n_sel_blocks - 1) * 64 + (r % 64) + 1)
     flops *= w.batch * w.n_kv_heads
+    score_flops *= w.batch * w.n_kv_heads
     attn_flops *= w.batch * w.n_q_heads
+    # bytes the score-only kernel must move: F in, K~ in, one float per row out
+    score_bytes = case["f"].numel() * 2 + kc.numel() * 2 + row_max.numel() * 4
     return {
         "workload": "prefill B1 T=32768 Hq32/Hkv8 D128 block64 k64, all 32768 rows",
         "select_ms": ms_sel,
@@ -223,6 +239,11 @@ def prefill_leg(dev, warmup, iters):
         "attn_ms": ms_att,
         "attn_tflops": attn_flops / (ms_att * 1e-3) / 1e12,
         "select_grid_32_16_ms": ms_sel_g,
+        "score_only_ms": ms_score,
+        "score_only_gflop": score_flops / 1e9,
+        "score_only_tflops": score_flops / (ms_score * 1e-3) / 1e12,
+        "score_only_frac_bf16_peak": score_flops / (ms_score * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+        "score_only_GBps": score_bytes / (ms_score * 1e-3) / 1e9,
     }
 
 
@@ -714,9 +735,13 @@ def main():
         # against the rate of the 16x16x32 instruction the select kernel's layout needs
         out["prefill"]["select_frac_measured_16x16x32_rate"] = (out["prefill"]["select_tflops"]
                                                                 / peaks["mfma_bf16_16x16x32_TFLOPs"])
+        out["prefill"]["score_only_frac_measured_mfma_peak"] = (out["prefill"]["score_only_tflops"]
+                                                                 / peaks["mfma_bf16_TFLOPs"])
         log(f"[bench] prefill select {out['prefill']['select_ms'] * 1e3:.1f} us, "
             f"{out['prefill']['select_tflops']:.1f} TFLOP/s; on the (32, 16) grid "
-            f"{out['prefill']['select_grid_32_16_ms'] * 1e3:.1f} us")
+            f"{out['prefill']['select_grid_32_16_ms'] * 1e3:.1f} us; score contraction alone "
+            f"{out['prefill']['score_only_ms'] * 1e3:.1f} us, {out['prefill']['score_only_tflops']:.0f} TFLOP/s "
+            f"({out['prefill']['score_only_frac_bf16_peak'] * 100:.1f} % of 2.5 PF)")
     if args.pipeline and not args.no_pipeline:
         # A child process, so that a failure there cannot take the rest of this line down.
         import subprocess

@@ -9,6 +9,8 @@
  *
  *   sparda_compress_keys    K -> K~               (Sec. 3, Eq. 2)
  *   sparda_forecast_select  F, K~ -> block sets   (Sec. 4.1, Eq. 4 with Eq. 1)
+ *   sparda_forecast_score_max F, K~ -> each row's largest candidate score (the scoring
+ *                           contraction alone, a measurement of Eq. 4 without the top-k)
  *   sparda_sparse_attn      Q, K, V, sets -> O    (Sec. 4.1, Eq. 5 with Eq. 1)
  *   sparda_multihead_select Q, K~ -> block sets   (the InfLLM-V2 selector of Sec. 3 that the
  *                           Forecast indexer replaces; a baseline)
@@ -130,6 +132,21 @@ int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t
 int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
                            const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,
                            hipStream_t stream);
+
+/*
+ * sparda_forecast_score_max -- the scoring contraction of sparda_forecast_select alone (Sec. 4.1,
+ * Eq. 4): every candidate block of every query row is scored and each row's largest score is
+ * written.  It measures the dense F . K~ contraction apart from the per-row top-k (the scores
+ * are reduced on chip; nothing else is written).  (64, 64) grid only.
+ *   f, n_q, q_pos0, k_cmp : as for sparda_forecast_select.
+ *   row_max out : float32 [B][Hkv][n_q] device (4-byte aligned): max over the row's candidates
+ *                [n_init, blk(p) - n_local] of F_row . K~_j (float32 accumulation), -inf for a
+ *                row without candidates.
+ * Errors: SPARDA_ERR_UNSUPPORTED for the (32, 16) grid; SPARDA_ERR_INVALID_ARG for null or
+ * misaligned pointers, rows outside t_cap, or a candidate at or beyond nc_cap.
+ */
+int sparda_forecast_score_max(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
+                              const void* k_cmp, float* row_max, hipStream_t stream);
 
 /*
  * sparda_multihead_select -- the same attended sets chosen by the InfLLM-V2 multi-head selector

@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 PEAKS_SOURCE = "peaks.hip"
 PEAKS_LIB = os.path.join(PKG, "libsparda_peaks.so")
 
-SOURCES = ["compress.hip", "select.hip", "select_prefill.hip", "select_multihead.hip", "indexer_kl.hip", "attention.hip", "attention_prefill.hip", "gather.hip", "sparda_abi.cpp"]
+SOURCES = ["compress.hip", "select.hip", "select_prefill.hip", "score_max.hip", "select_multihead.hip", "indexer_kl.hip", "attention.hip", "attention_prefill.hip", "gather.hip", "sparda_abi.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
           "-Wall", "-Wno-unused-function"]

@@ -114,6 +114,19 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
 
+// Each query row's largest Forecast score over its candidate blocks, (64, 64) grid
+// (score_max.hip).  Units are the rows of one (batch, group) inside one 64-token block.
+struct ScoreMaxArgs {
+  const uint16_t* f;   // bf16 [n_groups][n_q][128]
+  const uint16_t* kc;  // bf16 [n_groups][nc_cap][128]
+  float* row_max;      // [n_groups][n_q]
+  int64_t nc_cap, q_pos0;
+  int32_t n_q, n_groups;  // n_groups = batch * n_kv_heads
+  int32_t blk0, n_units;  // blocks of the first and following rows: [blk0, blk0 + n_units)
+  int32_t n_init, n_local;
+};
+hipError_t launch_score_rowmax(const ScoreMaxArgs& a, hipStream_t stream);
+
 // Row-wise top-k over pooled window scores already in a.ws (row stride a.ws_stride, window wf of
 // the row at offset 0), for the multi-head selector's row-wise path (select.hip).
 hipError_t launch_rowwise_topk(const SelectArgs& a, hipStream_t stream);

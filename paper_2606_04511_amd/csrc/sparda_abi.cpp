@@ -227,6 +227,35 @@ int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q
   return hip_status(sparda::launch_select(a, stream), "select launch");
 }
 
+int sparda_forecast_score_max(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
+                              const void* k_cmp, float* row_max, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(f, "f", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(row_max, "row_max", 4)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (shape->cmp_kernel != 64 || shape->cmp_stride != 64)
+    return fail(SPARDA_ERR_UNSUPPORTED, "the score-only contraction covers the (64, 64) grid only");
+  const int64_t pl = q_pos0 + n_q - 1;
+  const sparda::RowGeom gl = sparda::row_geom(pl, shape->n_init, shape->n_local, shape->k_total);
+  if (gl.n_cand > 0 && (int64_t)(gl.cand_lo + gl.n_cand - 1) >= shape->nc_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "compressed key %d beyond nc_cap %lld", gl.cand_lo + gl.n_cand - 1,
+                (long long)shape->nc_cap);
+  sparda::ScoreMaxArgs a;
+  a.f = static_cast<const uint16_t*>(f);
+  a.kc = static_cast<const uint16_t*>(k_cmp);
+  a.row_max = row_max;
+  a.nc_cap = shape->nc_cap;
+  a.q_pos0 = q_pos0;
+  a.n_q = n_q;
+  a.n_groups = shape->batch * shape->n_kv_heads;
+  a.blk0 = (int32_t)(q_pos0 / 64);
+  a.n_units = (int32_t)(pl / 64) - a.blk0 + 1;
+  a.n_init = shape->n_init;
+  a.n_local = shape->n_local;
+  return hip_status(sparda::launch_score_rowmax(a, stream), "score-max launch");
+}
+
 int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0,
                             const void* k_cmp, float sm_scale, int16_t* sel, int16_t* cnt, void* ws,
                             size_t ws_bytes, hipStream_t stream) {

@@ -27,7 +27,7 @@ SPARDA_OP_SPARSE_ATTN = 2
 SPARDA_OP_MULTIHEAD_SELECT = 3
 SPARDA_OP_INDEXER_KL = 4
 
-EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
+EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select", "sparda_sparse_attn",
             "sparda_gather_blocks", "sparda_plan_staging", "sparda_indexer_kl",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
@@ -92,13 +92,14 @@ def load() -> ctypes.CDLL:
         i32, i64 = ctypes.c_int32, ctypes.c_int64
         lib.sparda_compress_keys.argtypes = [S, P, i64, i32, i32, P, P]
         lib.sparda_forecast_select.argtypes = [S, P, i32, i64, P, P, P, P, ctypes.c_size_t, P]
+        lib.sparda_forecast_score_max.argtypes = [S, P, i32, i64, P, P, P]
         lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
         lib.sparda_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P, P, P]
         lib.sparda_indexer_kl.argtypes = [S, P, P, P, P, i32, i64, ctypes.c_float, i32, P, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
-        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_multihead_select", "sparda_sparse_attn",
+        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select", "sparda_sparse_attn",
                      "sparda_gather_blocks", "sparda_plan_staging", "sparda_indexer_kl",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
@@ -160,6 +161,12 @@ def sparda_forecast_select(shape: SpardaShape, f, n_q: int, q_pos0: int, k_cmp, 
         ws_bytes = ws.numel() * ws.element_size()
     _check(load().sparda_forecast_select(ctypes.byref(cs), _p(f), n_q, q_pos0, _p(k_cmp), _p(sel), _p(cnt), _p(ws),
                                          ws_bytes, _stream(stream)), "sparda_forecast_select")
+
+
+def sparda_forecast_score_max(shape: SpardaShape, f, n_q: int, q_pos0: int, k_cmp, row_max, stream=None):
+    cs = shape.c()
+    _check(load().sparda_forecast_score_max(ctypes.byref(cs), _p(f), n_q, q_pos0, _p(k_cmp), _p(row_max),
+                                            _stream(stream)), "sparda_forecast_score_max")
 
 
 def sparda_multihead_select(shape: SpardaShape, q, n_q: int, q_pos0: int, k_cmp, sm_scale: float, sel, cnt, ws=None,

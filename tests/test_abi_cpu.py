@@ -116,6 +116,20 @@ def test_select_argument_errors(lib):
     assert rc_of(f, sl, FAKE, 2, 65534, FAKE, FAKE, FAKE, FAKE, need - 4, 0) == sp.SPARDA_ERR_WORKSPACE
 
 
+def test_score_max_argument_errors(lib):
+    """The scoring contraction alone: the (64, 64) grid only, the same row and K~ checks as the
+    selection, a 4-byte aligned float output."""
+    s = shape()
+    m = sp.sparda_forecast_score_max
+    assert rc_of(m, s, FAKE, 0, 4095, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG       # n_q
+    assert rc_of(m, s, FAKE, 1, 4096, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG       # p >= t_cap
+    assert rc_of(m, s, None, 1, 4095, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG       # f
+    assert rc_of(m, s, FAKE, 1, 4095, FAKE, FAKE + 2, 0) == sp.SPARDA_ERR_INVALID_ARG   # row_max align
+    assert rc_of(m, shape(nc_cap=61), FAKE, 1, 4095, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # block 61
+    assert rc_of(m, shape(nc_cap=255, cmp_kernel=32, cmp_stride=16), FAKE, 1, 4095, FAKE, FAKE, 0) == \
+        sp.SPARDA_ERR_UNSUPPORTED
+
+
 def test_paper_grid_arguments(lib):
     """The (32, 16) grid: compress takes a window range, nc_cap counts windows, selection needs
     every window that overlaps a candidate block of the last row."""

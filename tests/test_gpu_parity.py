@@ -435,6 +435,87 @@ def test_full_prefill_t32k_samples(dev):
     say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
 
 
+# ----------------------------------------------------------------------------- score contraction alone
+
+SCORE_MAX = [
+    # B, H, T, n_q, q_pos0, n_init, n_local
+    (1, 8, 4096, 4096, 0, 1, 2),  # a whole 4K prefill (persistent form): rows without candidates
+    (2, 3, 5000, 700, 4300, 1, 2),  # an unaligned, ragged chunk; 6 (batch, group) pairs
+    (1, 2, 20000, 1000, 18991, 0, 3),  # odd start, no initial block
+    (1, 1, 100, 100, 0, 1, 2),  # no row has a candidate
+    (1, 1, 70000, 130, 69870, 1, 2),  # 1089 candidates: the general kernel, 35 M-tiles
+    (2, 2, 40000, 300, 39700, 1, 2),  # 617 candidates: the general kernel, ragged chunk
+    (1, 2, 32768, 4096, 28672, 1, 2),  # 509 candidates at the end: the persistent form, 8 slots
+    (1, 4, 8192, 1, 8191, 4, 16),  # one row, 4 initial blocks, a 16-block local window
+]
+
+
+def gpu_score_max(s, f_dev, n_q, q_pos0, kc_dev, dev):
+    out = torch.full((s.batch, s.n_kv_heads, n_q), float("nan"), dtype=torch.float32, device=dev)
+    sp.sparda_forecast_score_max(s, f_dev, n_q, q_pos0, kc_dev, out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def check_score_max(got, want, f_u16, kc_u16, q_pos0, n_init, n_local, label):
+    """Rows without candidates must be -inf on both sides; elsewhere the float32 maximum may differ
+    from the float64 one by the a-priori bound of a 128-term float32 dot product, gamma_128 times
+    the largest sum of |F_d K~_d| over the row's candidates."""
+    u = 2.0 ** -24
+    gamma = 128 * u / (1 - 128 * u)
+    to64 = lambda a: np.abs((np.ascontiguousarray(a).astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    fa, ka = to64(f_u16), to64(kc_u16)
+    B, H, n_q = want.shape
+    worst = 0.0
+    for b in range(B):
+        for m in range(H):
+            for r in range(n_q):
+                hi = (q_pos0 + r) // 64 - n_local
+                if hi < n_init:
+                    assert want[b, m, r] == -np.inf and got[b, m, r] == -np.inf, (label, b, m, r)
+                    continue
+                bound = gamma * float((ka[b, m, n_init:hi + 1] @ fa[b, m, r]).max()) + 1e-6
+                err = abs(float(got[b, m, r]) - want[b, m, r])
+                assert err <= bound, (label, b, m, r, float(got[b, m, r]), want[b, m, r], bound)
+                worst = max(worst, err / bound)
+    return worst
+
+
+@pytest.mark.parametrize("B,H,T,n_q,q_pos0,n_init,n_local", SCORE_MAX)
+def test_score_max_matches_oracle(dev, B, H, T, n_q, q_pos0, n_init, n_local):
+    say(f"score max B{B} H{H} T{T} n_q{n_q} q_pos0 {q_pos0} init {n_init} local {n_local}")
+    w, case = make(B, H, 4, T, n_q, n_init + n_local + 1, 5000 + T, n_init=n_init, n_local=n_local)
+    t_cap = -(-T // 64) * 64
+    nb = max(T // 64, 1)
+    s, o = shapes(B, H, 4, n_init + n_local + 1, t_cap, nb, n_init=n_init, n_local=n_local)
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, T // 64)
+    f_u16 = inputs.to_u16(case["f"])
+    got = gpu_score_max(s, case["f"].to(dev), n_q, q_pos0, inputs.from_u16(kc_ref, dev), dev)
+    want = oracle.forecast_score_max(o, f_u16, n_q, q_pos0, kc_ref)
+    worst = check_score_max(got, want, f_u16, kc_ref, q_pos0, n_init, n_local, "score max")
+    say(f"  worst error / bound {worst:.3g}")
+
+
+def test_score_max_full_prefill_t32k(dev):
+    """The 32K prefill workload at full size, in the launch the benchmark times; every row of two
+    groups against the oracle."""
+    w = inputs.WORKLOADS["prefill_b1_t32k"]
+    T, nb = w.seq_len, w.n_blocks
+    say("full workload prefill_b1_t32k (score max): generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, _ = shapes(w.batch, w.n_kv_heads, w.group_size, w.k_total, T, nb)
+    kc = gpu_compress(s, case["k"], T, nb, nb, dev)
+    got = gpu_score_max(s, case["f"], T, 0, kc, dev)
+    _, o1 = shapes(1, 1, w.group_size, w.k_total, T, nb)
+    worst = 0.0
+    for m in (0, w.n_kv_heads - 1):
+        kc_ref = oracle.compress_keys(o1, inputs.to_u16(case["k"][0:1, m:m + 1]), T, 0, nb)
+        f16 = inputs.to_u16(case["f"][0:1, m:m + 1])
+        want = oracle.forecast_score_max(o1, f16, T, 0, kc_ref)
+        worst = max(worst, check_score_max(got[0:1, m:m + 1], want, f16, kc_ref, 0, w.n_init, w.n_local, f"m{m}"))
+    say(f"  2 x {T} rows, worst error / bound {worst:.3g}")
+
+
 # ----------------------------------------------------------------------------- exact ties
 
 @pytest.mark.parametrize("T,n_q,k_total", [(8192, 1, 16), (8192, 1024, 16), (32768, 2048, 64), (65536, 3, 64),
