@@ -91,10 +91,10 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kw[tt][ks] = ld16(kb + (16 * tt + hh) * kHeadDim + 32 * ks + 8 * grp);
+      for (int ks = 0; ks < 4; ++ks) kw[tt][ks] = ld16_nt(kb + (16 * tt + hh) * kHeadDim + 32 * ks + 8 * grp);
     uint4 vw[16];
 #pragma unroll
-    for (int it = 0; it < 16; ++it) vw[it] = ld16(vb + (4 * it + grp) * kHeadDim + 8 * hh);
+    for (int it = 0; it < 16; ++it) vw[it] = ld16_nt(vb + (4 * it + grp) * kHeadDim + 8 * hh);
 
     f32x4 st[4];
 #pragma unroll

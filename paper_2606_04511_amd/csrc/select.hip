@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int idx = min(base + 4 * i + rs, NW - 1);
-        w[i] = ld16(kbase + (int64_t)idx * kHeadDim);
+        w[i] = ld16_nt(kbase + (int64_t)idx * kHeadDim);
       }
     };
     int base = wave * 64;
