@@ -126,6 +126,9 @@ struct ScoreMaxArgs {
   int32_t n_init, n_local;
 };
 hipError_t launch_score_rowmax(const ScoreMaxArgs& a, hipStream_t stream);
+// Window scores of multi-row calls into the row-wise workspace on MFMA (score_max.hip): units of
+// the rows inside one 64-token block, the windows of each unit's last row.
+hipError_t launch_tile_scores(const SelectArgs& a, hipStream_t stream);
 
 // Row-wise top-k over pooled window scores already in a.ws (row stride a.ws_stride, window wf of
 // the row at offset 0), for the multi-head selector's row-wise path (select.hip).

@@ -1,4 +1,8 @@
-// score_max.hip -- the Forecast prefill score contraction on its own (Sec. 4.1, Eq. 4): every
+// score_max.hip -- the Forecast prefill score contraction on 32x32x16 MFMA (Sec. 4.1, Eq. 4):
+// each row's largest candidate score (a measurement of the contraction alone), and the window
+// scores of the row-wise selection path (at the end of this file).
+//
+// The score contraction on its own: every
 // candidate block of every query row is scored and each row's scores are reduced on chip to
 // their maximum, so that one float per row leaves the kernel.  It isolates the dense contraction
 // that the fused select kernel performs before its per-row top-k, on the (64, 64) key grid.
@@ -41,6 +45,18 @@ __device__ __forceinline__ void load_frags(const uint4* row, int h, uint4 (&x)[8
   for (int u = 0; u < 2; ++u)
 #pragma unroll
     for (int i = 0; i < 4; ++i) x[4 * u + i] = row[8 * u + 4 * h + i];
+}
+
+// One M-tile of 32 keys against both N-tiles: the products only.
+__device__ __forceinline__ void mma_tile(const uint4 (&a)[8], const uint4 (&fb)[2][8], f32x16& c0, f32x16& c1) {
+#pragma unroll
+  for (int e = 0; e < 16; ++e) c0[e] = c1[e] = 0.f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const bf16x8 av = as_bf16x8(a[s]);
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(fb[0][s]), c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(fb[1][s]), c1, 0, 0, 0);
+  }
 }
 
 // One M-tile of 32 candidates against both N-tiles; folds the scores into the running maxima.
@@ -279,6 +295,76 @@ __global__ __launch_bounds__(kSlThreads) void score_rowmax_lds_kernel(ScoreMaxAr
   }
 }
 
+// ---- window scores of many rows, for the row-wise selection path -----------------------------
+//
+// Multi-row calls whose rows have more than kSelTileMaxCand candidates keep every window score in
+// the workspace (row stride ws_stride, window wf at slot 0) for the row-wise top-k.  The same
+// units (the rows of one (batch, group) inside one 64-token block) score the windows [wf, wl] of
+// their last row on 32x32x16 MFMA, A = 32 windows of K~ per M-tile (from L2, one M-tile ahead),
+// B = the unit's 64 F rows, so each key fragment serves 64 rows.  Accumulator element e of lane
+// (n, h) is window 8 (e / 4) + 4 h + e % 4 of the M-tile for query column n: each group of four
+// elements is one 16-byte store.  Earlier rows of a unit get up to three windows past their own
+// last visible one; the top-k never reads them.
+
+__global__ __launch_bounds__(kSmThreads) void tile_score_kernel(SelectArgs a, int blk0, int n_units) {
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n = lane & 31, h = lane >> 5;
+  const int n_groups = a.batch * a.n_kv_heads;
+  const int grp = blockIdx.x % n_groups;
+  const int unit = n_units - 1 - (int)(blockIdx.x / n_groups);
+  const int blk = blk0 + unit;
+  const int64_t p_lo = max((int64_t)blk * kBlock, a.q_pos0);
+  const int64_t p_hi = min((int64_t)blk * kBlock + kBlock, a.q_pos0 + a.n_q);
+  const int nr = (int)(p_hi - p_lo);
+  const int64_t row0 = (int64_t)grp * a.n_q + (p_lo - a.q_pos0);
+  const RowGeom g = row_geom(p_hi - 1, a.n_init, a.n_local, a.k_total);
+  if (g.n_take >= g.n_cand) return;  // then every row of the unit takes all its candidates
+  int32_t wf, wl;
+  row_windows(g, a.grid, p_hi - 1, &wf, &wl);
+  const int nwu = wl - wf + 1;
+
+  uint4 fb[2][8];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    const int r = min(32 * nt + n, nr - 1);
+    load_frags(reinterpret_cast<const uint4*>(a.f) + (row0 + r) * kRowU4, h, fb[nt]);
+  }
+  const uint4* kc = reinterpret_cast<const uint4*>(a.kc) + ((int64_t)grp * a.nc_cap + wf) * kRowU4;
+  const int n_mt = (nwu + 31) / 32;
+  float* out0 = a.ws + (row0 + n) * a.ws_stride;
+  float* out1 = a.ws + (row0 + 32 + n) * a.ws_stride;
+  auto store = [&](int mt, const f32x16& c0, const f32x16& c1) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int x = 32 * mt + 8 * q + 4 * h;
+      if (x < nwu) {
+        if (n < nr) *reinterpret_cast<float4*>(out0 + x) = make_float4(c0[4 * q], c0[4 * q + 1], c0[4 * q + 2], c0[4 * q + 3]);
+        if (32 + n < nr)
+          *reinterpret_cast<float4*>(out1 + x) = make_float4(c1[4 * q], c1[4 * q + 1], c1[4 * q + 2], c1[4 * q + 3]);
+      }
+    }
+  };
+  if (w < n_mt) {
+    uint4 ab[2][8];
+    auto arow = [&](int mt) { return kc + (int64_t)min(32 * min(mt, n_mt - 1) + n, nwu - 1) * kRowU4; };
+    load_frags(arow(w), h, ab[0]);
+    for (int mt = w; mt < n_mt; mt += 2 * kSmWaves) {
+      load_frags(arow(mt + kSmWaves), h, ab[1]);
+      __builtin_amdgcn_sched_barrier(0);  // keep the request ahead of the products
+      f32x16 c0, c1;
+      mma_tile(ab[0], fb, c0, c1);
+      store(mt, c0, c1);
+      load_frags(arow(mt + 2 * kSmWaves), h, ab[0]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (mt + kSmWaves < n_mt) {
+        mma_tile(ab[1], fb, c0, c1);
+        store(mt + kSmWaves, c0, c1);
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_score_rowmax(const ScoreMaxArgs& a, hipStream_t stream) {
@@ -295,6 +381,14 @@ hipError_t launch_score_rowmax(const ScoreMaxArgs& a, hipStream_t stream) {
   }
   const int64_t wgs = (int64_t)a.n_units * a.n_groups;
   hipLaunchKernelGGL(score_rowmax_kernel, dim3((unsigned)wgs), dim3(kSmThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_tile_scores(const SelectArgs& a, hipStream_t stream) {
+  const int blk0 = (int)(a.q_pos0 / kBlock);
+  const int n_units = (int)((a.q_pos0 + a.n_q - 1) / kBlock) - blk0 + 1;
+  const int64_t wgs = (int64_t)n_units * a.batch * a.n_kv_heads;
+  hipLaunchKernelGGL(tile_score_kernel, dim3((unsigned)wgs), dim3(kSmThreads), 0, stream, a, blk0, n_units);
   return hipGetLastError();
 }
 

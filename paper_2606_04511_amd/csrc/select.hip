@@ -302,6 +302,8 @@ enum SelectPath { kPathDecode, kPathDecodeSplit, kPathTile, kPathRowwise };
 // kernel, 256 windows each) and select with one workgroup per row; otherwise one fused workgroup
 // per row.
 constexpr int64_t kDecodeSplitRows = 256;
+// Multi-row calls on the row-wise path with at least this many rows score on MFMA.
+constexpr int32_t kTileScoreMinRows = 16;
 
 static SelectPath select_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local,
                               WinGrid grid) {
@@ -343,7 +345,11 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
   const RowGeom gl = row_geom(pl, a.n_init, a.n_local, a.k_total);
   int32_t wf, wl;
   row_windows(gl, a.grid, pl, &wf, &wl);
-  if (gl.n_cand > 0 && wl >= wf) {  // the last row scores the most windows
+  if (gl.n_cand > 0 && wl >= wf && a.n_q >= kTileScoreMinRows) {
+    // many rows: 64-row units score on MFMA, each key fragment shared by the unit's rows
+    hipError_t e = launch_tile_scores(a, stream);
+    if (e != hipSuccess) return e;
+  } else if (gl.n_cand > 0 && wl >= wf) {  // the last row scores the most windows
     const int n_chunks = (wl - wf + 1 + 255) / 256;
     hipLaunchKernelGGL(rowwise_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks);
     hipError_t e = hipGetLastError();

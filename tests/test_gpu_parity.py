@@ -140,7 +140,9 @@ PREFILL_SELECT = [
     (2, 1, 5000, 5000, 0, 8),
     (1, 2, 8192, 700, 3000, 64),
     (1, 1, 32768, 2048, 30720, 64),
-    (1, 1, 40000, 37, 39963, 64),  # > 512 candidates per row: row-wise path
+    (1, 1, 40000, 37, 39963, 64),  # > 512 candidates per row: row-wise path, MFMA window scores
+    (2, 2, 70000, 300, 69650, 64),  # 1089 candidates, 300 rows over 6 blocks: ragged first and last units
+    (1, 1, 40000, 9, 39990, 64),  # fewer rows than the MFMA scorer takes: the per-row score kernel
 ]
 
 
@@ -612,7 +614,8 @@ GRID_PREFILL = [
     (1, 1, 5000, 1000, 4000, 16, 1, 0),     # no initial block: block 0 has no window 4b - 1
     (1, 2, 8192, 2000, 6192, 96, 2, 1),     # sets longer than 64 entries: written straight out
     (1, 2, 32960, 500, 32460, 64, 2, 1),    # the last row has 512 candidates: the tile kernel's maximum
-    (1, 2, 36000, 200, 35800, 64, 2, 1),    # more candidates: the row-wise path
+    (1, 2, 36000, 200, 35800, 64, 2, 1),    # more candidates: the row-wise path (MFMA window scores)
+    (1, 1, 70000, 130, 69870, 40, 1, 1),    # 2176 windows per row, one local block: edge windows
 ]
 
 
