@@ -307,7 +307,8 @@ def selector_leg(dev, iters):
         ms_m = time_events(mh, iters, stream)
         return {"batch": B, "kv_heads": Hkv, "G": G, "T": T, "rows_per_group": n_q, "forecast_us": ms_f * 1e3,
                 "multihead_us": ms_m * 1e3, "multihead_over_forecast": ms_m / ms_f,
-                "multihead_path": "fused" if ws_m.numel() <= 16 else "row-wise"}
+                "multihead_path": "fused" if ws_m.numel() <= 16 else (
+                    "MFMA tiles + row-wise top-k" if n_q >= 16 else "row-wise")}
 
     for T in (32768, 131072):
         for Hkv, G in ((8, 4), (2, 16)):

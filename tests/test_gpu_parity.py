@@ -708,8 +708,14 @@ MULTIHEAD = [
     (2, 2, 16, 131072, 1, 64, 1, 2, (32, 16)),   # G = 16 at 128K: two-pass fused
     (1, 2, 4, 200000, 1, 64, 0, 1, (32, 16)),    # G = 4 past one pass's LDS: two-pass fused
     (1, 1, 4, 524288, 1, 64, 1, 2, (32, 16)),    # 32767 windows: row-wise decode
-    (1, 2, 4, 5000, 300, 12, 1, 2, (64, 64)),    # multi-row, chunk off a block boundary
-    (1, 1, 4, 6000, 333, 20, 1, 1, (32, 16)),    # multi-row, (32, 16), one local block
+    (1, 2, 4, 5000, 300, 12, 1, 2, (64, 64)),    # multi-row MFMA tiles, chunk off a block boundary
+    (1, 1, 4, 6000, 333, 20, 1, 1, (32, 16)),    # multi-row tiles, (32, 16), one local block
+    (1, 1, 16, 9000, 130, 24, 1, 2, (32, 16)),   # tiles of 4 rows x 16 heads, ragged last unit
+    (2, 1, 2, 3000, 77, 10, 0, 2, (64, 64)),     # tiles of 32 rows x 2 heads, no initial block
+    (1, 2, 8, 7000, 40, 16, 1, 2, (32, 16)),     # tiles of 8 rows x 8 heads
+    (1, 1, 1, 4500, 100, 12, 1, 2, (32, 16)),    # tiles of 64 rows x 1 head
+    (1, 2, 4, 5000, 9, 12, 1, 2, (32, 16)),      # fewer rows than the tiles take: per-row kernels
+    (1, 1, 3, 5000, 50, 12, 1, 2, (32, 16)),     # G = 3 (does not divide 64): per-row kernels
 ]
 
 
