@@ -148,9 +148,14 @@ __device__ __forceinline__ float pooled_score(const float* w, const WinGrid& gri
   return m;
 }
 
+// Rows with at most this many candidates keep their pooled block keys in LDS for the radix passes
+// (8 KiB per wavefront); longer rows pool from the workspace on every pass.
+constexpr int kRowTopkLdsKeys = 2048;
+
 // One wavefront per row: forced blocks, padding, count, and the radix top-k over the scratch row.
 __global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t n_rows) {
   __shared__ __align__(16) uint32_t hist[4][256];
+  __shared__ uint32_t keys[4][kRowTopkLdsKeys];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + wave;
   if (row >= n_rows) return;
@@ -165,6 +170,15 @@ __global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t
   row_windows(g, a.grid, p, &wf, &wl);
   const int32_t wvis = grid_win_vis(a.grid, p);
   const WinGrid grid = a.grid;
+  if (g.n_take < g.n_cand && g.n_cand <= kRowTopkLdsKeys) {
+    // pool once: the passes and the emission then read LDS instead of the workspace
+    uint32_t* kw = keys[wave];
+#pragma unroll 4
+    for (int i = lane; i < g.n_cand; i += kWave) kw[i] = score_key(pooled_score(sc, grid, g.cand_lo + i, wf, wvis));
+    wave_lds_sync();
+    wave_topk_emit([&](int i) { return kw[i]; }, g.n_cand, g.n_take, g.cand_lo, hist[wave], out + g.init_hi);
+    return;
+  }
   wave_topk_emit([&](int i) { return score_key(pooled_score(sc, grid, g.cand_lo + i, wf, wvis)); }, g.n_cand,
                  g.n_take, g.cand_lo, hist[wave], out + g.init_hi);
 }
