@@ -213,7 +213,7 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
  *   loss  out : float [B][Hkv][n_q] device.
  *   d_f   out : float [B][Hkv][n_q][D] device, d loss / d F.
  *   ws, ws_bytes: device workspace of sparda_workspace_size(SPARDA_OP_INDEXER_KL) bytes (the fine
- *               windows).
+ *               windows, then every row's target weight of each fine window).
  * Per row at position p: positions w = the prediction windows complete at p; the target T_w =
  * max over the fine windows inside w (tokens [i, i + 2) within [w s, w s + l)) of the sum over the
  * group's heads of softmax_i(sm_scale q_h . K~fine_i) (fine windows complete at p); the

@@ -16,7 +16,12 @@
 // Kernels:
 //   pair_compress_kernel -- the (2, 1) windows of the raw keys into the workspace: float64 sum of
 //                           the pair, one rounding to bf16 (as every compressed key).
-//   kl_row_kernel        -- one 512-thread workgroup per query row.  Target: 16-window x 16-head
+//   kl_target_kernel     -- for G in {1, 2, 4, 8, 16}: the target's shared weight of every fine
+//                           window for 64 / G rows at a time (64 (row, head) columns on 32x32x16
+//                           MFMA, head_tiles.hpp), into the workspace, so that every fine key
+//                           fragment serves 64 / G rows.
+//   kl_row_kernel        -- one 512-thread workgroup per query row.  Target: the max-pool of those
+//                           weights into the positions, or for other G 16-window x 16-head
 //                           MFMA tiles (A = the windows, B = the group's query rows padded to 16
 //                           columns), an online maximum and sum of 2^z per head, then a second
 //                           pass that sums each window's normalised head weights across the
@@ -29,6 +34,7 @@
 
 #include "device_util.hpp"
 #include "launch.hpp"
+#include "head_tiles.hpp"
 #include "select_block.hpp"
 
 namespace sparda {
@@ -64,6 +70,8 @@ struct KlArgs {
   const uint16_t* kp;     // [B][Hkv][nc_cap][D] prediction windows
   float* loss;            // [B][Hkv][n_q]
   float* dF;              // [B][Hkv][n_q][D]
+  float* sw;              // [B][Hkv][n_q][sw_stride] shared target weights per fine window (workspace)
+  int64_t sw_stride;
   int64_t nt, nc_cap, q_pos0;
   int32_t n_kv_heads, group_size, n_q, n_init, n_local, k_top;
   WinGrid grid;           // prediction grid
@@ -96,6 +104,39 @@ __device__ __forceinline__ float block_max_f(float x, float* red, int wave, int 
   return m;
 }
 
+// The target's shared weights of many rows on MFMA (G in {1, 2, 4, 8, 16}): a unit is 64 / G rows
+// of one (batch, group) with their heads (head_tiles.hpp), scored against the fine windows
+// complete at the unit's last row; each row stores its weights of the fine windows 0 .. p - 1.
+template <int G>
+__global__ __launch_bounds__(kMtThreads) void kl_target_kernel(KlArgs a, int n_units) {
+  constexpr int U = 64 / G;
+  __shared__ float red_m[kMtWaves][64], red_s[kMtWaves][64];
+  const int n = threadIdx.x & 31;
+  const int n_groups = (int)(gridDim.x / n_units);
+  const int grp = blockIdx.x % n_groups;
+  const int unit = n_units - 1 - (int)(blockIdx.x / n_groups);  // latest rows (most windows) first
+  const int r0 = unit * U;
+  const int nr = min(U, a.n_q - r0);
+  HeadTileRows t;
+  t.n_keys = (int)(a.q_pos0 + r0 + nr - 1);  // fine windows 0 .. p - 1 of the unit's last row
+  t.lo = 0;
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    const int c = 32 * nt + n;
+    const int rr = min(c / G, nr - 1);
+    const int64_t p = a.q_pos0 + r0 + rr;
+    t.q[nt] = reinterpret_cast<const uint4*>(a.q) + (((int64_t)grp * G + c % G) * a.n_q + r0 + rr) * kMtRowU4;
+    t.vis[nt] = (int)p - 1;
+    t.hi[nt] = ((n % G) == 0 && c / G < nr) ? (int)p - 1 : -1;
+    t.out[nt] = a.sw + ((int64_t)grp * a.n_q + r0 + rr) * a.sw_stride;
+  }
+  head_tile_shared_weights<G>(t, reinterpret_cast<const uint4*>(a.kt) + (int64_t)grp * a.nt * kMtRowU4,
+                              a.scale_log2, red_m, red_s);
+}
+
+// kPre: the target's shared weights are in a.sw (kl_target_kernel); the row max-pools them into
+// its positions.  Otherwise the row computes them itself (16-window x 16-column MFMA tiles).
+template <bool kPre>
 __global__ __launch_bounds__(kDecThreads) void kl_row_kernel(KlArgs a) {
   __shared__ float Tp[kKlMaxPos];  // pooled target per position (as float bits for atomic max)
   __shared__ float Pp[kKlMaxPos];  // predicted distribution per position
@@ -121,8 +162,19 @@ __global__ __launch_bounds__(kDecThreads) void kl_row_kernel(KlArgs a) {
   }
   __syncthreads();
 
-  // ---- target: MFMA tiles of 16 fine windows x the group's heads
-  {
+  // ---- target
+  if (kPre) {
+    // T_w = the largest shared weight among the fine windows inside position w: tokens [i, i + 2)
+    // within [w s, w s + l), i.e. i in [w s, w s + l - 2]; every position complete at p has them
+    const float* srow = a.sw + row * a.sw_stride;
+    const int gl = a.grid.l, gs = a.grid.s;
+    for (int w = tid; w < N; w += kDecThreads) {
+      const int i0 = w * gs, i1 = min(w * gs + gl - 2, n_tw - 1);
+      float m = 0.f;
+      for (int i = i0; i <= i1; ++i) m = fmaxf(m, srow[i]);
+      Tp[w] = m;
+    }
+  } else {  // MFMA tiles of 16 fine windows x the group's heads
     bf16x8 qb[4];
     // columns past the group's heads read head 0 (a valid address) and are zeroed
     const uint16_t* qrow = a.q + ((bm * G + (n < G ? n : 0)) * a.n_q + r) * kHeadDim + 8 * j;
@@ -292,7 +344,7 @@ __global__ __launch_bounds__(kDecThreads) void kl_row_kernel(KlArgs a) {
 }
 
 hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_t* f, const uint16_t* kp,
-                             uint16_t* kt_ws, float* loss, float* dF, int32_t batch, int32_t n_kv_heads,
+                             uint16_t* kt_ws, float* sw_ws, float* loss, float* dF, int32_t batch, int32_t n_kv_heads,
                              int32_t group_size, int32_t n_q, int64_t q_pos0, int64_t t_cap, int64_t nc_cap,
                              int32_t n_init, int32_t n_local, int32_t k_top, WinGrid grid, float sm_scale,
                              hipStream_t stream) {
@@ -324,7 +376,25 @@ hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_
   a.grid = grid;
   a.sm_scale = sm_scale;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
-  hipLaunchKernelGGL(kl_row_kernel, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), 0, stream, a);
+  a.sw = sw_ws;
+  a.sw_stride = (a.nt + 3) & ~(int64_t)3;
+  const int G = group_size;
+  if (G == 1 || G == 2 || G == 4 || G == 8 || G == 16) {  // the target of 64 / G rows per MFMA unit
+    const int n_units = (n_q + 64 / G - 1) / (64 / G);
+    const dim3 grid((unsigned)(rows_g * n_units)), block(kMtThreads);
+    switch (G) {
+      case 1: hipLaunchKernelGGL(kl_target_kernel<1>, grid, block, 0, stream, a, n_units); break;
+      case 2: hipLaunchKernelGGL(kl_target_kernel<2>, grid, block, 0, stream, a, n_units); break;
+      case 4: hipLaunchKernelGGL(kl_target_kernel<4>, grid, block, 0, stream, a, n_units); break;
+      case 8: hipLaunchKernelGGL(kl_target_kernel<8>, grid, block, 0, stream, a, n_units); break;
+      default: hipLaunchKernelGGL(kl_target_kernel<16>, grid, block, 0, stream, a, n_units); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kl_row_kernel<true>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(kl_row_kernel<false>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

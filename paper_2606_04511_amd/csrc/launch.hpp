@@ -149,7 +149,7 @@ hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream);
 
 // The indexer-training loss (indexer_kl.hip); kt_ws holds (q_pos0 + n_q - 1) fine windows per row.
 hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_t* f, const uint16_t* kp,
-                             uint16_t* kt_ws, float* loss, float* dF, int32_t batch, int32_t n_kv_heads,
+                             uint16_t* kt_ws, float* sw_ws, float* loss, float* dF, int32_t batch, int32_t n_kv_heads,
                              int32_t group_size, int32_t n_q, int64_t q_pos0, int64_t t_cap, int64_t nc_cap,
                              int32_t n_init, int32_t n_local, int32_t k_top, WinGrid grid, float sm_scale,
                              hipStream_t stream);

@@ -34,6 +34,7 @@
 
 #include "device_util.hpp"
 #include "launch.hpp"
+#include "head_tiles.hpp"
 #include "select_block.hpp"
 
 namespace sparda {
@@ -415,49 +416,16 @@ __global__ __launch_bounds__(256) void mh_norm_kernel(SelectArgs a, int64_t hstr
 // ---- multi-row tiles (MFMA, two passes) ------------------------------------------------------
 //
 // Multi-row calls with G in {1, 2, 4, 8, 16}: a unit is U = 64 / G consecutive rows of one
-// (batch, group), i.e. 64 (row, head) columns; column c is head c % G of row c / G, the B operand
-// of v_mfma_f32_32x32x16_bf16 as two N-tiles of 32 columns.  The four wavefronts of a workgroup
-// take every fourth M-tile of 32 windows over [0, NV) of the unit's last row, reading the K~
-// fragments from L2 one M-tile ahead.  The dimension order of the contraction is free: lane half
-// h of k-step 4 u + i holds dimensions 64 u + 32 h + 8 i .. + 7 of both operands.  Accumulator
-// element e of lane (n, h) is window 8 (e / 4) + 4 h + e % 4 of the M-tile for column n.
-//  * pass 1: per column, an online maximum and sum of 2^z over the windows complete at the
-//    column's row; lane halves and wavefronts merge through LDS;
-//  * pass 2: the same products again; each column's normalised weight, summed over the G lanes
-//    of one row by shuffles, is that row's shared score of the window, stored where the row-wise
-//    top-k reads it (window wf + x at slot x).
-
-constexpr int kMtThreads = 256;
-constexpr int kMtWaves = kMtThreads / kWave;
-constexpr int kMtRowU4 = kHeadDim * 2 / 16;  // 16-byte pieces per 128-dim bf16 row
-
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ void mt_load_frags(const uint4* row, int h, uint4 (&x)[8]) {
-#pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) x[4 * u + i] = row[8 * u + 4 * h + i];
-}
-
-__device__ __forceinline__ void mt_mma(const uint4 (&a)[8], const uint4 (&fb)[2][8], f32x16& c0, f32x16& c1) {
-#pragma unroll
-  for (int e = 0; e < 16; ++e) c0[e] = c1[e] = 0.f;
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
-    const bf16x8 av = as_bf16x8(a[s]);
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(fb[0][s]), c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(fb[1][s]), c1, 0, 0, 0);
-  }
-}
+// (batch, group) with their heads, 64 (row, head) columns (head_tiles.hpp), scored against the
+// windows complete at the unit's last row; each row stores its shared scores of the windows
+// [wf, wl] it selects from, where the row-wise top-k reads them (window wf + x at slot x).
 
 template <int G>
 __global__ __launch_bounds__(kMtThreads) void mh_tile_kernel(SelectArgs a, int n_units, int64_t hstride) {
   constexpr int U = 64 / G;
   __shared__ float red_m[kMtWaves][64], red_s[kMtWaves][64];
   const int lane = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int n = lane & 31, h = lane >> 5;
+  const int n = lane & 31;
   const int n_groups = a.batch * a.n_kv_heads;
   const int grp = blockIdx.x % n_groups;
   const int unit = n_units - 1 - (int)(blockIdx.x / n_groups);  // latest rows (most windows) first
@@ -466,135 +434,26 @@ __global__ __launch_bounds__(kMtThreads) void mh_tile_kernel(SelectArgs a, int n
   const int64_t p_last = a.q_pos0 + r0 + nr - 1;
   const RowGeom gl = row_geom(p_last, a.n_init, a.n_local, a.k_total);
   if (gl.n_take >= gl.n_cand) return;  // then every row of the unit takes all its candidates
-  const int NV = grid_win_vis(a.grid, p_last) + 1;
-  const int n_mt = (NV + 31) / 32;
-
-  // column 32 nt + n: row rr[nt] of the unit (clamped), head hd[nt]; windows <= vis[nt] count
-  int rr[2], vis[2];
-  uint4 fb[2][8];
+  HeadTileRows t;
+  t.n_keys = grid_win_vis(a.grid, p_last) + 1;
+  t.lo = 0;
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
     const int c = 32 * nt + n;
-    rr[nt] = min(c / G, nr - 1);
-    const int hd = c % G;
-    vis[nt] = grid_win_vis(a.grid, a.q_pos0 + r0 + rr[nt]);
-    mt_load_frags(reinterpret_cast<const uint4*>(a.q) + (((int64_t)grp * G + hd) * a.n_q + r0 + rr[nt]) * kMtRowU4,
-                  h, fb[nt]);
-  }
-  const uint4* kc = reinterpret_cast<const uint4*>(a.kc) + (int64_t)grp * a.nc_cap * kMtRowU4;
-  auto arow = [&](int mt) { return kc + (int64_t)min(32 * min(mt, n_mt - 1) + n, NV - 1) * kMtRowU4; };
-  const float sl2 = a.scale_log2;
-
-  // Pass 1: online maximum and sum of 2^z per column.
-  float mr[2] = {-INFINITY, -INFINITY}, sr[2] = {0.f, 0.f};
-  auto fold = [&](int mt, const f32x16& c0, const f32x16& c1) {
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      const f32x16& c = nt == 0 ? c0 : c1;
-      float z[16];
-      float mt_max = -INFINITY;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int win = 32 * mt + 8 * (e >> 2) + 4 * h + (e & 3);
-        z[e] = win <= vis[nt] ? c[e] * sl2 : -INFINITY;
-        mt_max = fmaxf(mt_max, z[e]);
-      }
-      const float mn = fmaxf(mr[nt], mt_max);
-      if (mn > -INFINITY) {
-        float acc = sr[nt] * exp2f(mr[nt] - mn);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc += exp2f(z[e] - mn);
-        sr[nt] = acc;
-        mr[nt] = mn;
-      }
-    }
-  };
-  if (w < n_mt) {
-    uint4 ab[2][8];
-    mt_load_frags(arow(w), h, ab[0]);
-    for (int mt = w; mt < n_mt; mt += 2 * kMtWaves) {
-      mt_load_frags(arow(mt + kMtWaves), h, ab[1]);
-      __builtin_amdgcn_sched_barrier(0);  // keep the request ahead of the products
-      f32x16 c0, c1;
-      mt_mma(ab[0], fb, c0, c1);
-      fold(mt, c0, c1);
-      mt_load_frags(arow(mt + 2 * kMtWaves), h, ab[0]);
-      __builtin_amdgcn_sched_barrier(0);
-      if (mt + kMtWaves < n_mt) {
-        mt_mma(ab[1], fb, c0, c1);
-        fold(mt + kMtWaves, c0, c1);
-      }
-    }
-  }
-  auto merge = [](float& m, float& s, float m2, float s2) {
-    const float mn = fmaxf(m, m2);
-    if (mn > -INFINITY) {
-      s = s * exp2f(m - mn) + s2 * exp2f(m2 - mn);
-      m = mn;
-    }
-  };
-  float M[2], inv[2];
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    merge(mr[nt], sr[nt], __shfl_xor(mr[nt], 32, kWave), __shfl_xor(sr[nt], 32, kWave));
-    if (h == 0) {
-      red_m[w][32 * nt + n] = mr[nt];
-      red_s[w][32 * nt + n] = sr[nt];
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    float m = red_m[0][32 * nt + n], sm = red_s[0][32 * nt + n];
-#pragma unroll
-    for (int v = 1; v < kMtWaves; ++v) merge(m, sm, red_m[v][32 * nt + n], red_s[v][32 * nt + n]);
-    M[nt] = m;
-    inv[nt] = sm > 0.f ? 1.0f / sm : 0.f;
-  }
-
-  // Pass 2: each row's shared score of every window it selects from, [wf, wl] of the row.
-  int32_t wf = 0, wl[2] = {-1, -1};
-  float* out[2];
-#pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    const int64_t p = a.q_pos0 + r0 + rr[nt];
+    const int rr = min(c / G, nr - 1);
+    const int64_t p = a.q_pos0 + r0 + rr;
+    t.q[nt] = reinterpret_cast<const uint4*>(a.q) + (((int64_t)grp * G + c % G) * a.n_q + r0 + rr) * kMtRowU4;
+    t.vis[nt] = grid_win_vis(a.grid, p);
     const RowGeom g = row_geom(p, a.n_init, a.n_local, a.k_total);
-    row_windows(g, a.grid, p, &wf, &wl[nt]);
-    const bool own = (n % G) == 0 && (32 * nt + n) / G < nr && g.n_take < g.n_cand;
-    if (!own) wl[nt] = -1;  // this lane stores nothing for the tile
-    out[nt] = a.ws + ((int64_t)grp * a.n_q + r0 + rr[nt]) * a.ws_stride + G * hstride;
+    int32_t wf, wl;
+    row_windows(g, a.grid, p, &wf, &wl);
+    t.lo = wf;  // the same for every row
+    const bool own = (n % G) == 0 && c / G < nr && g.n_take < g.n_cand;
+    t.hi[nt] = own ? wl : -1;
+    t.out[nt] = a.ws + ((int64_t)grp * a.n_q + r0 + rr) * a.ws_stride + G * hstride;
   }
-  auto emit = [&](int mt, const f32x16& c0, const f32x16& c1) {
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-      const f32x16& c = nt == 0 ? c0 : c1;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int win = 32 * mt + 8 * (e >> 2) + 4 * h + (e & 3);
-        float wt = win <= vis[nt] ? exp2f(c[e] * sl2 - M[nt]) * inv[nt] : 0.f;
-#pragma unroll
-        for (int d = 1; d < G; d <<= 1) wt += __shfl_xor(wt, d, kWave);
-        if (win >= wf && win <= wl[nt]) out[nt][win - wf] = wt;
-      }
-    }
-  };
-  if (w < n_mt) {
-    uint4 ab[2][8];
-    mt_load_frags(arow(w), h, ab[0]);
-    for (int mt = w; mt < n_mt; mt += 2 * kMtWaves) {
-      mt_load_frags(arow(mt + kMtWaves), h, ab[1]);
-      __builtin_amdgcn_sched_barrier(0);
-      f32x16 c0, c1;
-      mt_mma(ab[0], fb, c0, c1);
-      emit(mt, c0, c1);
-      mt_load_frags(arow(mt + 2 * kMtWaves), h, ab[0]);
-      __builtin_amdgcn_sched_barrier(0);
-      if (mt + kMtWaves < n_mt) {
-        mt_mma(ab[1], fb, c0, c1);
-        emit(mt + kMtWaves, c0, c1);
-      }
-    }
-  }
+  head_tile_shared_weights<G>(t, reinterpret_cast<const uint4*>(a.kc) + (int64_t)grp * a.nc_cap * kMtRowU4,
+                              a.scale_log2, red_m, red_s);
 }
 
 // ---- host -----------------------------------------------------------------------------------

@@ -106,10 +106,16 @@ size_t multihead_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int64_t*
          sizeof(float);
 }
 
-// Workspace of sparda_indexer_kl: the fine (2, 1) windows complete at the last row, bf16.
-size_t kl_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
+// Workspace of sparda_indexer_kl: the fine (2, 1) windows complete at the last row (bf16), then
+// every row's target weight of each of them (float, rows padded to 4).
+size_t kl_keys_bytes(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
   const int64_t nt = q_pos0 + n_q - 1;
   return (size_t)s->batch * s->n_kv_heads * (size_t)(nt > 0 ? nt : 1) * s->head_dim * sizeof(uint16_t);
+}
+size_t kl_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
+  const int64_t nt = q_pos0 + n_q - 1;
+  const int64_t stride = ((nt > 0 ? nt : 1) + 3) & ~(int64_t)3;
+  return kl_keys_bytes(s, n_q, q_pos0) + (size_t)s->batch * s->n_kv_heads * n_q * (size_t)stride * sizeof(float);
 }
 
 size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps) {
@@ -363,7 +369,10 @@ int sparda_indexer_kl(const sparda_shape* shape, const void* q, const void* k, c
   if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   return hip_status(sparda::launch_indexer_kl(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                               static_cast<const uint16_t*>(f), static_cast<const uint16_t*>(k_cmp),
-                                              static_cast<uint16_t*>(ws), loss, d_f, shape->batch, shape->n_kv_heads,
+                                              static_cast<uint16_t*>(ws),
+                                              reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                                       kl_keys_bytes(shape, n_q, q_pos0)),
+                                              loss, d_f, shape->batch, shape->n_kv_heads,
                                               shape->group_size, n_q, q_pos0, shape->t_cap, shape->nc_cap,
                                               shape->n_init, shape->n_local, k_top, grid_of(shape), sm_scale, stream),
                     "indexer kl launch");

@@ -267,6 +267,7 @@ def test_indexer_kl_arguments(lib):
     assert rc_of(kl, *args(q0=10, n_q=4)) == sp.SPARDA_ERR_INVALID_ARG      # row 0 has no complete window
     assert rc_of(kl, *args(s=shape(nc_cap=200, **g))) == sp.SPARDA_ERR_INVALID_ARG  # window 248 beyond nc_cap
     need = sp.sparda_workspace_size(s, sp.SPARDA_OP_INDEXER_KL, 4, 4000)
-    assert need == 2 * 8 * 4003 * 128 * 2  # the fine windows complete at the last row (p = 4003)
+    # the fine windows complete at the last row (p = 4003), then each row's weight of each of them
+    assert need == 2 * 8 * 4003 * 128 * 2 + 2 * 8 * 4 * 4004 * 4
     assert rc_of(kl, *args(ws=None)) == sp.SPARDA_ERR_WORKSPACE
     assert rc_of(kl, *args(wsb=need - 2)) == sp.SPARDA_ERR_WORKSPACE

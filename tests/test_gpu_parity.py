@@ -892,6 +892,9 @@ KL_CASES = [
     (1, 1, 4, 1200, 10, 4096, 1, 2, (32, 16)),   # k_top beyond the candidates: all of them
     (1, 2, 2, 4096, 12, 12, 1, 2, (64, 64)),     # block-granular prediction grid
     (1, 1, 4, 16384, 6, 64, 1, 2, (32, 16)),     # 1022 positions, 16K fine windows
+    (1, 2, 8, 5000, 37, 20, 1, 2, (32, 16)),     # G = 8: units of 8 rows, ragged last unit
+    (1, 1, 1, 3000, 70, 10, 1, 2, (64, 64)),     # G = 1: units of 64 rows, two units
+    (1, 1, 3, 2500, 9, 12, 1, 2, (32, 16)),      # G = 3: the target computed inside the row kernel
 ]
 
 
