@@ -15,6 +15,7 @@ Function map (paper sections in the C file):
                     per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
+  writeback_kv                 -- Sec. 5.2 (new K/V rows written into the host pools)
   indexer_kl_row               -- Sec. 4.2, Eq. 6-7 (the indexer-training KL over the target's top-k
                                   partition, and its gradient with respect to the Forecast row)
   plan_staging                 -- App. C, NOSI step reuse (keep the previous step's staged blocks,
@@ -107,11 +108,12 @@ def open_library(path: str):
     lib.sparda_ref_attend_row.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, i32, i32, i32, P]
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
     lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
+    lib.sparda_ref_writeback_kv.argtypes = [S, P, P, i32, i64, P, P]
     lib.sparda_ref_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P]
     lib.sparda_ref_indexer_kl_row.argtypes = [S, P, P, i64, i32, i32, P, P, i32, i64, f64, i32, i32, i32, i32, P, P,
                                               P, P]
     for name in ("compress_keys", "select_row", "forecast_select", "forecast_score_max", "multihead_select_row", "multihead_select",
-                 "attend_row", "sparse_attn", "gather_blocks", "plan_staging", "indexer_kl_row"):
+                 "attend_row", "sparse_attn", "gather_blocks", "writeback_kv", "plan_staging", "indexer_kl_row"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
 
@@ -312,6 +314,16 @@ def gather_blocks(shape: Shape, host_k, host_v, sel, cnt, stage_k=None, stage_v=
     _check(_load().sparda_ref_gather_blocks(ctypes.byref(cs), _ptr(host_k), _ptr(host_v), _ptr(sel), _ptr(cnt),
                                             _ptr(stage_k), _ptr(stage_v)), "gather_blocks")
     return stage_k, stage_v
+
+
+def writeback_kv(shape: Shape, k_new, v_new, n_new: int, pos0: int, host_k, host_v):
+    """Copies of host_k, host_v (uint16 [B][Hkv][t_cap][D]) with the new rows written at pos0."""
+    k_new, v_new = _u16(k_new), _u16(v_new)
+    hk, hv = np.array(_u16(host_k), copy=True), np.array(_u16(host_v), copy=True)
+    cs = shape.c()
+    _check(_load().sparda_ref_writeback_kv(ctypes.byref(cs), _ptr(k_new), _ptr(v_new), n_new, pos0, _ptr(hk),
+                                           _ptr(hv)), "writeback_kv")
+    return hk, hv
 
 
 def plan_staging(shape: Shape, sel, cnt, q_pos: int, slot_blk, slot_len):

@@ -548,6 +548,24 @@ int sparda_ref_gather_blocks(const ref_shape* s, const uint16_t* host_k, const u
   return REF_OK;
 }
 
+/* Sec. 5.2: the write-back of newly created KV rows into the host pools.  k_new, v_new: bf16
+ * [B][Hkv][n_new][D]; the rows land at positions pos0 .. pos0 + n_new - 1 of the pools
+ * host_k, host_v: bf16 [B][Hkv][t_cap][D]; nothing else is written. */
+int sparda_ref_writeback_kv(const ref_shape* s, const uint16_t* k_new, const uint16_t* v_new, int32_t n_new,
+                            int64_t pos0, uint16_t* host_k, uint16_t* host_v) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n_new < 1 || pos0 < 0 || pos0 + n_new > s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads;
+  for (int64_t bm = 0; bm < rows; ++bm)
+    for (int64_t t = 0; t < n_new; ++t) {
+      memcpy(host_k + (bm * s->t_cap + pos0 + t) * D, k_new + (bm * n_new + t) * D, (size_t)D * sizeof(uint16_t));
+      memcpy(host_v + (bm * s->t_cap + pos0 + t) * D, v_new + (bm * n_new + t) * D, (size_t)D * sizeof(uint16_t));
+    }
+  return REF_OK;
+}
+
 /* ---- App. C (NOSI step reuse): staging plan of one decode step ------------------------------- */
 
 /* A layer's staging buffer is a cache of k_total slots per (batch, group) row.  Slot s holds the

@@ -701,6 +701,24 @@ def _random_set(rng, p, k_total, prev=None, keep=0.7, vary=False):
     return sel, len(full)
 
 
+def test_writeback_places_new_rows_and_touches_nothing_else(oracle_lib):
+    """The write-back is a placement: numpy slice assignment of the new rows at [pos0, pos0 + n)
+    of every (batch, group) pool row; every other position keeps its bytes; a range past t_cap
+    is refused."""
+    s = shape_for(oracle_lib, 2, 3, 4, 640, 8)
+    pool_k = rnd_u16((2, 3, 640, 128), 81, 1)
+    pool_v = rnd_u16((2, 3, 640, 128), 81, 2)
+    new_k = rnd_u16((2, 3, 5, 128), 81, 3)
+    new_v = rnd_u16((2, 3, 5, 128), 81, 4)
+    hk, hv = oracle_lib.writeback_kv(s, new_k, new_v, 5, 300, pool_k, pool_v)
+    want_k, want_v = pool_k.copy(), pool_v.copy()
+    want_k[:, :, 300:305] = new_k
+    want_v[:, :, 300:305] = new_v
+    assert np.array_equal(hk, want_k) and np.array_equal(hv, want_v)
+    with pytest.raises(oracle_lib.OracleError):
+        oracle_lib.writeback_kv(s, new_k, new_v, 5, 636, pool_k, pool_v)
+
+
 def test_plan_first_step_is_the_plain_gather_layout(oracle_lib):
     s = _plan_shape(oracle_lib)
     rng = np.random.default_rng(90)
