@@ -16,6 +16,8 @@
  *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
+ *   sparda_writeback_kv     new K/V rows -> the pinned host pools (the asynchronous write-back of
+ *                           Sec. 5.2), for a side stream
  *   sparda_plan_staging     step-to-step reuse of the staged blocks: which blocks the next gather
  *                           must fetch (the NOSI engine of App. C)
  *   sparda_indexer_kl       Q, K, F, K~ -> the indexer-training loss and its gradient w.r.t. F
@@ -271,6 +273,23 @@ int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int
 int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
                          const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
                          hipStream_t stream);
+
+/*
+ * sparda_writeback_kv -- stores newly created K/V rows into the pinned host pools that the
+ * offloaded layers gather from: the asynchronous CPU write-back of new KV entries after they are
+ * used for attention (Sec. 5.2; in decode, the token Alg. 2 appends each step).  Meant for a side
+ * stream, like the gather.
+ *   k_new, v_new in : bf16 [B][Hkv][n_new][D] device (16-byte aligned).
+ *   n_new, pos0     : the rows land at positions [pos0, pos0 + n_new) of every (batch, group)
+ *                     pool row; n_new >= 1, pos0 >= 0, pos0 + n_new <= t_cap.
+ *   host_k, host_v out: bf16 [B][Hkv][t_cap][D] pinned host memory mapped for the device (as for
+ *                     sparda_gather_blocks; SPARDA_ERR_HOST_NOT_MAPPED otherwise).
+ *   n_workgroups    : persistent workgroups writing over PCIe (the CU budget), >= 1.
+ * The copy is bitwise; positions outside the range are not touched.  Ordering against gathers
+ * or host reads of the same positions is the caller's (record an event, synchronise).
+ */
+int sparda_writeback_kv(const sparda_shape* shape, const void* k_new, const void* v_new, int32_t n_new, int64_t pos0,
+                        void* host_k, void* host_v, int32_t n_workgroups, hipStream_t stream);
 
 /*
  * sparda_workspace_size -- device workspace bytes that call `op` (a sparda_op) needs for n_q

@@ -56,6 +56,44 @@ hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const i
   return hipGetLastError();
 }
 
+// ---- write-back of new KV rows into the host pools ------------------------------------------
+//
+// The asynchronous CPU write-back of newly created KV entries (Sec. 5.2): rows produced on the GPU
+// (the decoded token's K and V, or a prefill chunk's) are stored into the pinned host pools that
+// later gathers read.  A persistent grid of n_workgroups; each thread moves 16-byte pieces with
+// zero-copy stores through the mapped pointers.  Task = one (row, token) pair of K and V:
+// 2 x 256 bytes, 16 pieces each, so 16 threads per task and 16 tasks per 256-thread workgroup pass.
+__global__ __launch_bounds__(256) void writeback_kernel(const uint4* __restrict__ kn, const uint4* __restrict__ vn,
+                                                        uint4* __restrict__ hk, uint4* __restrict__ hv, int64_t rows,
+                                                        int32_t n_new, int64_t pos0, int64_t t_cap) {
+  constexpr int kPieces = kHeadDim * 2 / 16;  // 16-byte pieces per token row
+  const int64_t n_tasks = rows * n_new;
+  const int piece = threadIdx.x % kPieces, slot = threadIdx.x / kPieces;
+  for (int64_t task = (int64_t)blockIdx.x * (256 / kPieces) + slot; task < n_tasks;
+       task += (int64_t)gridDim.x * (256 / kPieces)) {
+    const int64_t bm = task / n_new;
+    const int64_t t = task - bm * n_new;
+    const int64_t src = task * kPieces + piece;
+    const int64_t dst = (bm * t_cap + pos0 + t) * kPieces + piece;
+    const uint4 a = kn[src], b = vn[src];
+    hk[dst] = a;
+    hv[dst] = b;
+  }
+}
+
+hipError_t launch_writeback(const uint16_t* k_new, const uint16_t* v_new, uint16_t* host_k, uint16_t* host_v,
+                            int64_t rows, int32_t n_new, int64_t pos0, int64_t t_cap, int32_t n_workgroups,
+                            hipStream_t stream) {
+  const int64_t n_tasks = rows * n_new;
+  const int64_t need = (n_tasks + 15) / 16;
+  const int64_t grid = n_workgroups < need ? n_workgroups : need;
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL(writeback_kernel, dim3((unsigned)grid), dim3(256), 0, stream, reinterpret_cast<const uint4*>(k_new),
+                     reinterpret_cast<const uint4*>(v_new), reinterpret_cast<uint4*>(host_k),
+                     reinterpret_cast<uint4*>(host_v), rows, n_new, pos0, t_cap);
+  return hipGetLastError();
+}
+
 // ---- staging plan of step-to-step reuse (the NOSI engine of the paper's efficiency setup,
 // App. C: a layer keeps the blocks its previous decode step attended and fetches only the newly
 // selected ones) --------------------------------------------------------------------------------

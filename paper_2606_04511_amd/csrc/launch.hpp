@@ -156,6 +156,11 @@ hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_
 hipError_t launch_plan_staging(const int16_t* sel, const int16_t* cnt, int64_t p, int16_t* slot_blk, int16_t* slot_len,
                                int16_t* fetch, int16_t* staged, int16_t* stage_cnt, int32_t* n_fetch, int64_t rows,
                                int32_t k_total, hipStream_t stream);
+// New K/V rows [B][Hkv][n_new][D] (device) into the mapped host pools at positions
+// [pos0, pos0 + n_new) (gather.hip).
+hipError_t launch_writeback(const uint16_t* k_new, const uint16_t* v_new, uint16_t* host_k, uint16_t* host_v,
+                            int64_t rows, int32_t n_new, int64_t pos0, int64_t t_cap, int32_t n_workgroups,
+                            hipStream_t stream);
 hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const int16_t* sel, const int16_t* cnt,
                          uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int64_t t_cap, int32_t k_total,
                          int32_t n_workgroups, hipStream_t stream);

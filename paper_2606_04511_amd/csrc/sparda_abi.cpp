@@ -396,6 +396,42 @@ int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int
                     "plan launch");
 }
 
+// The device address of a pinned host pool mapped for the device, or null (with the failure set).
+static int mapped_pool(const void* host, const char* name, void** dev) {
+  hipPointerAttribute_t attr;
+  hipError_t e = hipPointerGetAttributes(&attr, host);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // clear the error state of this query
+    return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not a registered HIP allocation (%s)", name, hipGetErrorString(e));
+  }
+  if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr)
+    return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not device-mapped pinned host memory", name);
+  *dev = attr.devicePointer;
+  return SPARDA_OK;
+}
+
+int sparda_writeback_kv(const sparda_shape* shape, const void* k_new, const void* v_new, int32_t n_new, int64_t pos0,
+                        void* host_k, void* host_v, int32_t n_workgroups, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(k_new, "k_new", 16)) || (rc = check_dev(v_new, "v_new", 16)) ||
+      (rc = check_dev(host_k, "host_k", 16)) || (rc = check_dev(host_v, "host_v", 16)))
+    return rc;
+  if (n_new < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_new %d < 1", n_new);
+  if (pos0 < 0 || pos0 + n_new > shape->t_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "positions [%lld, %lld) outside t_cap %lld", (long long)pos0,
+                (long long)(pos0 + n_new), (long long)shape->t_cap);
+  if (n_workgroups < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_workgroups %d < 1", n_workgroups);
+  void* dk = nullptr;
+  void* dv = nullptr;
+  if ((rc = mapped_pool(host_k, "host_k", &dk)) || (rc = mapped_pool(host_v, "host_v", &dv))) return rc;
+  return hip_status(sparda::launch_writeback(static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                                             static_cast<uint16_t*>(dk), static_cast<uint16_t*>(dv),
+                                             (int64_t)shape->batch * shape->n_kv_heads, n_new, pos0, shape->t_cap,
+                                             n_workgroups, stream),
+                    "write-back launch");
+}
+
 int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
                          const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
                          hipStream_t stream) {

@@ -130,6 +130,17 @@ def test_score_max_argument_errors(lib):
         sp.SPARDA_ERR_UNSUPPORTED
 
 
+def test_writeback_argument_errors(lib):
+    s = shape()
+    wb = sp.sparda_writeback_kv
+    assert rc_of(wb, s, FAKE, FAKE, 0, 100, FAKE, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG      # n_new
+    assert rc_of(wb, s, FAKE, FAKE, 2, 4095, FAKE, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG     # past t_cap
+    assert rc_of(wb, s, FAKE, FAKE, 1, -1, FAKE, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(wb, s, FAKE, FAKE, 1, 100, FAKE, FAKE, 0, 0) == sp.SPARDA_ERR_INVALID_ARG      # n_workgroups
+    assert rc_of(wb, s, None, FAKE, 1, 100, FAKE, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(wb, s, FAKE, FAKE, 1, 100, FAKE + 8, FAKE, 8, 0) == sp.SPARDA_ERR_INVALID_ARG  # alignment
+
+
 def test_paper_grid_arguments(lib):
     """The (32, 16) grid: compress takes a window range, nc_cap counts windows, selection needs
     every window that overlaps a candidate block of the last row."""

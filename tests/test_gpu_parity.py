@@ -336,6 +336,27 @@ def test_gather_bitwise_and_host_checks(dev):
     assert ei.value.status == sp.SPARDA_ERR_HOST_NOT_MAPPED
 
 
+@pytest.mark.parametrize("n_new,pos0,nwg", [(1, 8191, 16), (1, 4000, 1), (300, 1000, 7), (64, 0, 64)])
+def test_writeback_bitwise_and_host_checks(dev, n_new, pos0, nwg):
+    say(f"write-back n_new {n_new} pos0 {pos0} workgroups {nwg}")
+    B, H, T = 2, 3, 8192
+    s, o = shapes(B, H, 4, 16, T, T // 64)
+    pool_k = inputs.normal_bf16((B, H, T, 128), 5400, 1).pin_memory()
+    pool_v = inputs.normal_bf16((B, H, T, 128), 5400, 2).pin_memory()
+    new_k = inputs.normal_bf16((B, H, n_new, 128), 5400 + n_new, 3)
+    new_v = inputs.normal_bf16((B, H, n_new, 128), 5400 + n_new, 4)
+    ref_k, ref_v = oracle.writeback_kv(o, inputs.to_u16(new_k), inputs.to_u16(new_v), n_new, pos0,
+                                       inputs.to_u16(pool_k), inputs.to_u16(pool_v))
+    side = torch.cuda.Stream()
+    sp.sparda_writeback_kv(s, new_k.to(dev), new_v.to(dev), n_new, pos0, pool_k, pool_v, nwg, side)
+    side.synchronize()
+    assert np.array_equal(inputs.to_u16(pool_k), ref_k) and np.array_equal(inputs.to_u16(pool_v), ref_v)
+    with pytest.raises(sp.SpardaError) as ei:  # pageable host memory is refused
+        sp.sparda_writeback_kv(s, new_k.to(dev), new_v.to(dev), n_new, pos0, torch.empty(pool_k.shape, dtype=torch.bfloat16),
+                               pool_v, nwg, side)
+    assert ei.value.status == sp.SPARDA_ERR_HOST_NOT_MAPPED
+
+
 # ----------------------------------------------------------------------------- full-size workloads
 
 def _decode_full(dev, name, n_sample_rows, n_sample_heads):
