@@ -606,6 +606,54 @@ def peaks_leg(dev):
     }
 
 
+def gather_sweep_leg(dev):
+    """Gather rate against the persistent workgroup count, and the time of a decode attention
+    launched while one gather runs, at B = 8 .. 64, T = 32K, 8 KV heads, k = 64 (the shape of the
+    paper's CTA sweep): the data behind pipeline.gather_workgroups."""
+    T, H, K = 32768, 8, 64
+    rows = []
+    for B in (8, 16, 32, 64):
+        w = inputs.Workload("gather_sweep", batch=B, seq_len=T, n_q=1, n_kv_heads=H, group_size=4, k_total=K,
+                            n_init=1, n_local=2, seed=77)
+        L = DecodeLayer(w, dev)
+        L.select()
+        torch.cuda.synchronize()
+        hk = torch.empty((B, H, T, 128), dtype=torch.bfloat16, pin_memory=True)
+        hv = torch.empty((B, H, T, 128), dtype=torch.bfloat16, pin_memory=True)
+        hk.copy_(L.k.cpu())
+        hv.copy_(L.v.cpu())
+        stg_k = torch.empty((B, H, K, 64, 128), dtype=torch.bfloat16, device=dev)
+        stg_v = torch.empty_like(stg_k)
+        side = torch.cuda.Stream()
+        main = torch.cuda.current_stream()
+        nbytes = 2 * B * H * K * 64 * 256
+        for _ in range(3):
+            L.attend()
+        att_alone = time_events(L.attend, 20, main)
+        for nwg in (4, 8, 16, 32, 64):
+            g = lambda: sp.sparda_gather_blocks(L.shape, hk, hv, L.sel[:, :, 0], L.cnt[:, :, 0], stg_k, stg_v, nwg,
+                                                side)
+            g()
+            side.synchronize()
+            ms_g = time_events(g, 3, side)
+            torch.cuda.synchronize()
+            g()  # one gather on the side stream while the main stream runs attention launches
+            n_att = max(1, int(ms_g / att_alone / 2))
+            a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a0.record(main)
+            for _ in range(n_att):
+                L.attend()
+            a1.record(main)
+            torch.cuda.synchronize()
+            rows.append({"batch": B, "n_workgroups": nwg, "gather_ms": ms_g, "gather_GBps": nbytes / ms_g / 1e6,
+                         "attend_alone_us": att_alone * 1e3,
+                         "attend_during_gather_us": a0.elapsed_time(a1) / n_att * 1e3})
+            log("[bench] gather sweep " + json.dumps(rows[-1]))
+        del L, hk, hv, stg_k, stg_v
+        torch.cuda.empty_cache()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -618,6 +666,8 @@ def main():
                          "child process; off by default while a host-side crash seen in it is unexplained")
     ap.add_argument("--no-pipeline", action="store_true", help="kept for compatibility (the default)")
     ap.add_argument("--pipeline-only", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--gather-sweep", action="store_true",
+                    help="only the gather workgroup sweep (host-link rate and interference), one JSON line")
     ap.add_argument("--no-grid", action="store_true", help="skip the decode layer on the (32, 16) key grid")
     ap.add_argument("--no-selectors", action="store_true",
                     help="skip the Forecast vs multi-head selector comparison")
@@ -638,6 +688,9 @@ def main():
     sp.load()
     if args.pipeline_only:  # the child process of --pipeline
         print(json.dumps(pipeline_leg(dev, 4)))
+        return
+    if args.gather_sweep:
+        print(json.dumps({"gather_sweep": gather_sweep_leg(dev)}))
         return
 
     if args.calib_copy:

@@ -29,6 +29,19 @@ import torch
 from . import sparda as sp
 
 
+def gather_workgroups(batch: int) -> int:
+    """Persistent gather workgroups for a decode step at this batch size (the batch-adaptive CTA
+    budget of Sec. 4.3 / App. D): the smallest count that reaches the host link's rate.  Measured
+    on MI355X at 32K with 8 KV heads and k = 64, from B8 to B64: 4 workgroups move 37.3-37.7 GB/s,
+    8 move 54.9-56.9 GB/s and 16-64 move 55.8-57.3 GB/s, while a concurrent decode attention slows
+    more as the count grows (at B64: 186 us alone, 256 us beside 8 workgroups, 380 us beside 32).
+    Unlike the H100 heuristic (16 CTAs below B32, 32 above), the link saturates at the same small
+    count at every batch size here, so the budget stays at 8."""
+    if batch < 1:
+        raise ValueError("batch must be >= 1")
+    return 8
+
+
 class DecodePipeline:
     """L layers of one decode step.
 
@@ -41,16 +54,17 @@ class DecodePipeline:
     k0, v0       -- bf16 [B][Hkv][t_cap][D] device, layer 0's KV cache
     pools[l]     -- (host_k_ptr, host_v_ptr) of layer l (l >= 1): device-mapped pinned memory
                     laid out [B][Hkv][t_cap][D]; pools may be shared between layers
-    n_workgroups -- persistent-grid size of the gather (its CU budget)
+    n_workgroups -- persistent-grid size of the gather (its CU budget); None takes
+                    gather_workgroups(batch)
     """
 
-    def __init__(self, shape: sp.SpardaShape, t_ctx: int, q, f, f0_cur, kc, k0, v0, pools, n_workgroups: int,
-                 device, sm_scale: float | None = None, reuse: bool = False):
+    def __init__(self, shape: sp.SpardaShape, t_ctx: int, q, f, f0_cur, kc, k0, v0, pools,
+                 n_workgroups: int | None, device, sm_scale: float | None = None, reuse: bool = False):
         L = len(q)
         assert len(f) == L and len(kc) == L and len(pools) == L and L >= 1
         self.shape, self.t_ctx, self.L = shape, t_ctx, L
         self.q, self.f, self.f0_cur, self.kc, self.k0, self.v0, self.pools = q, f, f0_cur, kc, k0, v0, pools
-        self.n_workgroups = n_workgroups
+        self.n_workgroups = gather_workgroups(shape.batch) if n_workgroups is None else n_workgroups
         self.scale = 1.0 / math.sqrt(shape.head_dim) if sm_scale is None else sm_scale
         B, H, K = shape.batch, shape.n_kv_heads, shape.k_total
         self.sel = [torch.empty(B, H, 1, K, dtype=torch.int16, device=device) for _ in range(L)]
