@@ -39,8 +39,8 @@
 
 namespace sparda {
 
-constexpr int kKlMaxPos = 16384;  // positions per row (LDS)
-constexpr int kKlMaxTop = 4096;   // k_top limit (the selected positions' list in LDS)
+// Limits (checked by the entry point): 16384 positions per row and k_top <= 4096, so that the row
+// kernel's per-position LDS arrays (9 bytes per position plus 2 per top-k entry) fit one CU.
 
 __global__ __launch_bounds__(256) void pair_compress_kernel(const uint16_t* __restrict__ k, uint16_t* __restrict__ kt,
                                                             int64_t t_cap, int64_t n_win, int64_t rows) {
@@ -72,6 +72,7 @@ struct KlArgs {
   float* dF;              // [B][Hkv][n_q][D]
   float* sw;              // [B][Hkv][n_q][sw_stride] shared target weights per fine window (workspace)
   int64_t sw_stride;
+  int32_t lds_pos, lds_top;  // per-position LDS entries (>= 512, a multiple of 16) and top-k list entries
   int64_t nt, nc_cap, q_pos0;
   int32_t n_kv_heads, group_size, n_q, n_init, n_local, k_top;
   WinGrid grid;           // prediction grid
@@ -138,10 +139,14 @@ __global__ __launch_bounds__(kMtThreads) void kl_target_kernel(KlArgs a, int n_u
 // its positions.  Otherwise the row computes them itself (16-window x 16-column MFMA tiles).
 template <bool kPre>
 __global__ __launch_bounds__(kDecThreads) void kl_row_kernel(KlArgs a) {
-  __shared__ float Tp[kKlMaxPos];  // pooled target per position (as float bits for atomic max)
-  __shared__ float Pp[kKlMaxPos];  // predicted distribution per position
-  __shared__ uint8_t chosen[kKlMaxPos];  // 1 for the positions of the target's top-k set
-  __shared__ int16_t idx[kKlMaxTop];
+  // Per-position arrays, sized by the host for the call's largest row (kl_lds_layout): the pooled
+  // target (float bits for the atomic max), the predicted distribution, the top-k list and the
+  // chosen flags.  A small footprint lets several rows share a CU.
+  extern __shared__ __align__(16) float kl_lds[];
+  float* Tp = kl_lds;
+  float* Pp = kl_lds + a.lds_pos;
+  int16_t* idx = reinterpret_cast<int16_t*>(Pp + a.lds_pos);
+  uint8_t* chosen = reinterpret_cast<uint8_t*>(idx + a.lds_top);
   __shared__ __align__(16) uint32_t hist[256];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
@@ -378,6 +383,11 @@ hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.sw = sw_ws;
   a.sw_stride = (a.nt + 3) & ~(int64_t)3;
+  // the last row has the most positions; the gradient's reduction reuses 512 entries of Tp
+  const int n_max = grid_win_vis(grid, q_pos0 + n_q - 1) + 1;
+  a.lds_pos = n_max > 512 ? (n_max + 15) & ~15 : 512;
+  a.lds_top = ((k_top < n_max ? k_top : n_max) + 8) & ~7;
+  const size_t lds = (size_t)a.lds_pos * 2 * sizeof(float) + (size_t)a.lds_top * sizeof(int16_t) + (size_t)a.lds_pos;
   const int G = group_size;
   if (G == 1 || G == 2 || G == 4 || G == 8 || G == 16) {  // the target of 64 / G rows per MFMA unit
     const int n_units = (n_q + 64 / G - 1) / (64 / G);
@@ -391,9 +401,9 @@ hipError_t launch_indexer_kl(const uint16_t* q, const uint16_t* k, const uint16_
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kl_row_kernel<true>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), 0, stream, a);
+    hipLaunchKernelGGL(kl_row_kernel<true>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), lds, stream, a);
   } else {
-    hipLaunchKernelGGL(kl_row_kernel<false>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), 0, stream, a);
+    hipLaunchKernelGGL(kl_row_kernel<false>, dim3((unsigned)(rows_g * n_q)), dim3(kDecThreads), lds, stream, a);
   }
   return hipGetLastError();
 }
