@@ -11,8 +11,10 @@
 //      ascending order, is the tile's block list.
 //   2. The tile walks its block list.  Block j's 16 KiB of K and 16 KiB of V are read from HBM
 //      once per tile (16-byte loads, 1 KiB contiguous per wavefront instruction) into a
-//      double-buffered LDS stage, two blocks ahead of the math.  V is stored transposed (head dim
-//      x token, XOR-swizzled against bank conflicts) so that it can be the A operand of P V.
+//      double-buffered LDS stage, two blocks ahead of the math.  K rows keep their 16-byte pieces
+//      XOR-swizzled by the row; V is stored transposed (head dim x token, XOR-swizzled as well) so
+//      that it can be the A operand of P V.  Both swizzles make the operand reads conflict-free
+//      whether LDS serves 16 lanes of a 16-byte read from 64 banks or 32 lanes from 128.
 //   3. A wavefront skips block j for an N-tile none of whose rows lists j.  Otherwise:
 //        S^T = K Q^T on v_mfma_f32_16x16x32_bf16 (M = 16 tokens, N = 16 query-heads, K = 32
 //        dims); query-heads whose row does not list j, and tokens after the row's position, are
@@ -34,7 +36,7 @@ namespace {
 
 constexpr int kPaThreads = 512;
 constexpr int kPaQh = 256;                 // query-head rows per tile
-constexpr int kPaKLd = kHeadDim + 16;      // bf16 per staged K row (288 B: conflict-free 16-byte reads)
+constexpr int kPaKLd = kHeadDim;           // bf16 per staged K row; piece x of row r sits at x ^ (r % 16)
 constexpr int kPaMaxWords = 8192;          // row-bitmap words (32 KiB)
 constexpr int kPaMaxBlocks = 4096;         // causal blocks a tile may span
 constexpr float kLog2eP = 1.4426950408889634f;
@@ -156,16 +158,18 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
   // two blocks in flight.
   //
   // Staged V^T: row d (head dim) holds the block's 64 tokens in slots 4 tau + x <-> token
-  // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  LDS serves each half
-  // wavefront separately from 128 four-byte banks (4 rows of this buffer); the swizzle spreads the
-  // 8-byte operand reads of a half wavefront (16 consecutive dims x 2 k-chunks) over 64 distinct
-  // banks, leaving the transposing writes (once per block) two-way conflicted.
+  // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  An operand read takes
+  // 16 consecutive dims (16 md + c) x 4 k-chunks; vsw's low bits (from dim bits 1..3) give the
+  // dims of one parity distinct dword pairs, so a half wavefront covers 64 banks of 64 and a whole
+  // wavefront 128 of 128.  Its high bits (from dim bits 4, 5, constant over one read) spread the
+  // transposing writes (once per block) to two lanes per bank, the least that 32 lanes of 8-byte
+  // writes into one bank half can take.
   const int lt = tid & 255;
   const bool load_k = __builtin_amdgcn_readfirstlane(tid) < 256;  // whole wavefronts
   const int v_tau = 4 * (lt >> 6) + (lt & 3), v_part = (lt & 63) >> 2;
   const int ld_off = load_k ? lt * 8 : v_tau * kHeadDim + 8 * v_part;
   const uint16_t* kv = (load_k ? a.k : a.v) + bm * a.t_cap * kHeadDim + ld_off;
-  auto vsw = [](int d) { return 2 * ((d >> 2) & 15); };
+  auto vsw = [](int d) { return 2 * ((((d >> 2) & 3) | (((d >> 1) & 1) << 3)) ^ (((d >> 4) & 3) << 2)); };
   uint4 pre[2][4];
   auto issue = [&](uint4 (&r)[4], int j) {
     const uint16_t* src = kv + (int64_t)j * kBlock * kHeadDim;
@@ -177,7 +181,7 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
         const int u = lt + 256 * x;
-        *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (u & 15) * 8]) = r[x];
+        *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (((u & 15) ^ ((u >> 4) & 15)) * 8)]) = r[x];
       }
     } else {
       const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&r[0]);
@@ -232,7 +236,7 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
       bf16x8 kf[4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
-        kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(kb + (16 * mt + c) * kPaKLd + 32 * ks + 8 * q));
+        kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(kb + (16 * mt + c) * kPaKLd + (((4 * ks + q) ^ c) * 8)));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         st[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
