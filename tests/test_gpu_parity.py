@@ -458,6 +458,51 @@ def test_full_prefill_t32k_samples(dev):
     say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
 
 
+def test_paper_configuration_prefill_samples(dev):
+    """The paper's model configuration at full size, chunked prefill: 32K, all rows, 32 query /
+    2 KV heads (G = 16), k = 96 with a 32-block local window, keys on the (32, 16) grid, in the
+    launch configuration the benchmark times; sampled rows of the selection of both groups, and
+    of the attention over the oracle's sets."""
+    w = inputs.WORKLOADS["paper_prefill_b1_t32k"]
+    T, G = w.seq_len, w.group_size
+    nw = n_windows(T)
+    say("paper configuration prefill: generating on the GPU")
+    case = inputs.make_case(w, device=dev)
+    s, _ = shapes(w.batch, w.n_kv_heads, G, w.k_total, T, nw, w.n_init, w.n_local, lw=32, sw=16)
+    kc = gpu_compress(s, case["k"], T, nw, nw, dev)
+    sel, cnt = gpu_select(s, case["f"], T, 0, kc, dev)
+    _, o1 = shapes(1, 1, G, w.k_total, T, nw, w.n_init, w.n_local, lw=32, sw=16)
+    rng = np.random.default_rng(41)
+    rows_r = sorted(set(int(x) for x in rng.integers(0, T, size=30)) | {0, 2047, 2048, 2111, 6143, 6144, T - 1})
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    sel_mixed = sel.clone()
+    swaps = 0
+    for m in range(w.n_kv_heads):
+        kc_ref = oracle.compress_keys(o1, inputs.to_u16(case["k"][0:1, m:m + 1]), T, 0, nw)
+        assert np.array_equal(inputs.to_u16(kc[0:1, m:m + 1]), kc_ref)
+        f16 = inputs.to_u16(case["f"][0:1, m:m + 1])
+        _, sw = compare_selection(o1, f16, kc_ref, T, 0, sel_np[0:1, m:m + 1], cnt_np[0:1, m:m + 1],
+                                  [(0, 0, r) for r in rows_r])
+        swaps += sw
+        for r in rows_r:
+            ref_sel, _, _ = oracle.select_row(o1, f16, T, 0, kc_ref, 0, 0, r)
+            sel_mixed[0, m, r] = torch.from_numpy(ref_sel)
+    out = gpu_attend(s, case["q"], T, 0, case["k"], case["v"], 0, sel_mixed, cnt, dev)
+    worst = 0.0
+    for m in range(w.n_kv_heads):
+        k16 = inputs.to_u16(case["k"][0:1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][0:1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][0:1, m * G:(m + 1) * G])
+        ssel = sel_mixed[0:1, m:m + 1].cpu().numpy()
+        scnt = cnt[0:1, m:m + 1].cpu().numpy()
+        for r in rows_r[::3]:
+            for h in range(0, G, 5):
+                ref = oracle.attend_row(o1, q16, T, 0, k16, v16, 0, ssel, scnt, SCALE, 0, h, r)
+                got = out[0, m * G + h, r].float().cpu().numpy()
+                worst = max(worst, compare_attention(got, ref, f"paper prefill {(m, h, r)}"))
+    say(f"  sampled {len(rows_r) * w.n_kv_heads} rows, tie swaps {swaps}, attention max err {worst:.3g}")
+
+
 # ----------------------------------------------------------------------------- score contraction alone
 
 SCORE_MAX = [
