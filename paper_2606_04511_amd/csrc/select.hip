@@ -297,7 +297,17 @@ __global__ __launch_bounds__(kDecThreads) void decode_topk_kernel(SelectArgs a) 
   row_windows(g, a.grid, a.q_pos0, &wf, &wl);
   const int NW = wl - wf + 1;
   const float* src = a.ws + row * a.ws_stride;
-  for (int i = tid; i < NW; i += kDecThreads) sc[i] = src[i];
+  // Sixteen loads in flight per thread before any is stored (indices past the row read its last
+  // score again and are not stored): one memory latency per 8192 scores instead of sixteen.
+  constexpr int kLdBatch = 16;
+  for (int b0 = 0; b0 < NW; b0 += kLdBatch * kDecThreads) {
+    float t[kLdBatch];
+#pragma unroll
+    for (int k = 0; k < kLdBatch; ++k) t[k] = src[min(b0 + k * kDecThreads + tid, NW - 1)];
+#pragma unroll
+    for (int k = 0; k < kLdBatch; ++k)
+      if (b0 + k * kDecThreads + tid < NW) sc[b0 + k * kDecThreads + tid] = t[k];
+  }
   __syncthreads();
   const float* bs = sc;
   if (!grid_is_blocks(a.grid)) {
