@@ -16,7 +16,9 @@ template <int NX>  // token rows per thread: window length / 16
 __global__ __launch_bounds__(256) void compress_kernel(const uint16_t* __restrict__ k, uint16_t* __restrict__ kc,
                                                        int64_t t_cap, int64_t nc_cap, int32_t stride,
                                                        int32_t w_begin) {
-  __shared__ double part[16][kHeadDim + 1];
+  // Partial sums, dim 8 c + e at 9 c + e of its row: groups of 8 doubles 9 apart and rows 144
+  // apart put the writes of 32 lanes on distinct banks (the reads take at most two per bank).
+  __shared__ double part[16][144];
   const int i = w_begin + (int)blockIdx.x;
   const int64_t row = blockIdx.y;
   const int tid = threadIdx.x;
@@ -37,12 +39,12 @@ __global__ __launch_bounds__(256) void compress_kernel(const uint16_t* __restric
     acc[6] += bf16lo(w[x].w); acc[7] += bf16hi(w[x].w);
   }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) part[rg][c * 8 + e] = acc[e];
+  for (int e = 0; e < 8; ++e) part[rg][c * 9 + e] = acc[e];
   __syncthreads();
   if (tid < kHeadDim) {
     double s = 0.0;
 #pragma unroll
-    for (int g = 0; g < 16; ++g) s += part[g][tid];
+    for (int g = 0; g < 16; ++g) s += part[g][(tid >> 3) * 9 + (tid & 7)];
     kc[(row * nc_cap + i) * kHeadDim + tid] = f64_to_bf16(s * (1.0 / (16 * NX)));  // exact: 16 NX is a power of 2
   }
 }
