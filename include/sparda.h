@@ -17,7 +17,7 @@
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
  *   sparda_writeback_kv     new K/V rows -> the pinned host pools (the asynchronous write-back of
- *                           Sec. 5.2), for a side stream
+ *                           Sec. 5.3, Efficiency Results), for a side stream
  *   sparda_plan_staging     step-to-step reuse of the staged blocks: which blocks the next gather
  *                           must fetch (the NOSI engine of App. C)
  *   sparda_indexer_kl       Q, K, F, K~ -> the indexer-training loss and its gradient w.r.t. F
@@ -277,7 +277,8 @@ int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const vo
 /*
  * sparda_writeback_kv -- stores newly created K/V rows into the pinned host pools that the
  * offloaded layers gather from: the asynchronous CPU write-back of new KV entries after they are
- * used for attention (Sec. 5.2; in decode, the token Alg. 2 appends each step).  Meant for a side
+ * used for attention (Sec. 5.3, prefill-throughput paragraph; in decode, the token Alg. 2 appends
+ * each step).  Meant for a side
  * stream, like the gather.
  *   k_new, v_new in : bf16 [B][Hkv][n_new][D] device (16-byte aligned).
  *   n_new, pos0     : the rows land at positions [pos0, pos0 + n_new) of every (batch, group)

@@ -15,7 +15,7 @@ Function map (paper sections in the C file):
                     per-head softmax over the compressed keys, summed over the group, max-pooled
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
-  writeback_kv                 -- Sec. 5.2 (new K/V rows written into the host pools)
+  writeback_kv                 -- Sec. 5.3 (new K/V rows written into the host pools)
   indexer_kl_row               -- Sec. 4.2, Eq. 6-7 (the indexer-training KL over the target's top-k
                                   partition, and its gradient with respect to the Forecast row)
   plan_staging                 -- App. C, NOSI step reuse (keep the previous step's staged blocks,

@@ -548,7 +548,7 @@ int sparda_ref_gather_blocks(const ref_shape* s, const uint16_t* host_k, const u
   return REF_OK;
 }
 
-/* Sec. 5.2: the write-back of newly created KV rows into the host pools.  k_new, v_new: bf16
+/* Sec. 5.3 (Efficiency Results, prefill throughput): the write-back of newly created KV rows into the host pools.  k_new, v_new: bf16
  * [B][Hkv][n_new][D]; the rows land at positions pos0 .. pos0 + n_new - 1 of the pools
  * host_k, host_v: bf16 [B][Hkv][t_cap][D]; nothing else is written. */
 int sparda_ref_writeback_kv(const ref_shape* s, const uint16_t* k_new, const uint16_t* v_new, int32_t n_new,

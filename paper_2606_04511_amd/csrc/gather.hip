@@ -58,7 +58,7 @@ hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const i
 
 // ---- write-back of new KV rows into the host pools ------------------------------------------
 //
-// The asynchronous CPU write-back of newly created KV entries (Sec. 5.2): rows produced on the GPU
+// The asynchronous CPU write-back of newly created KV entries (Sec. 5.3, prefill throughput): rows produced on the GPU
 // (the decoded token's K and V, or a prefill chunk's) are stored into the pinned host pools that
 // later gathers read.  A persistent grid of n_workgroups; each thread moves 16-byte pieces with
 // zero-copy stores through the mapped pointers.  Task = one (row, token) pair of K and V:
