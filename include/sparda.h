@@ -12,6 +12,8 @@
  *   sparda_forecast_score_max F, K~ -> each row's largest candidate score (the scoring
  *                           contraction alone, a measurement of Eq. 4 without the top-k)
  *   sparda_sparse_attn      Q, K, V, sets -> O    (Sec. 4.1, Eq. 5 with Eq. 1)
+ *   sparda_sparse_attn_noalloc  the same without a workspace argument (a static scratch array),
+ *                           for callers that cannot allocate
  *   sparda_multihead_select Q, K~ -> block sets   (the InfLLM-V2 selector of Sec. 3 that the
  *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
@@ -30,8 +32,9 @@
  *   - Tensors are bf16 (passed as void*, 2 bytes per element, IEEE bfloat16 bits), dense and
  *     row-major in the layouts given per argument.  Block indices are int16.
  *   - Device pointers must be 16-byte aligned device (HBM) memory owned by the caller.  The
- *     library allocates nothing and keeps no state beyond a thread-local error string: every
- *     buffer, workspace and stream belongs to the caller and must stay alive until the work
+ *     library allocates nothing and keeps no state beyond a thread-local error string and, for
+ *     sparda_sparse_attn_noalloc, one static scratch array per device with its looked-up address:
+ *     every buffer, workspace and stream belongs to the caller and must stay alive until the work
  *     enqueued on the stream has completed.
  *   - Every compute call only enqueues work on the given stream and returns; argument errors are
  *     reported synchronously before anything is enqueued (nothing is written on error); a failed
@@ -195,6 +198,27 @@ int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
                        const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
                        void* o, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sparda_sparse_attn_noalloc -- sparda_sparse_attn without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, layouts, kernels and results as sparda_sparse_attn;
+ * the split partials of calls with fewer rows than the chip has CUs go to a scratch array of
+ * SPARDA_NOALLOC_SCRATCH_BYTES that the library holds in every device's memory (a static device
+ * array, one copy per GPU, kept until the process ends).  The call allocates nothing.
+ *   - The first call on a device looks the array's address up (hipGetSymbolAddress) with that
+ *     device current; the stream must belong to the current device, as for any HIP launch.
+ *   - Every call on one GPU shares that GPU's array: calls whose work overlaps on that GPU (two
+ *     streams, two threads) race on it and must be ordered by the caller.  The array keeps the
+ *     last call's partials; nothing in it needs to start at zero.
+ *   - A call whose partials exceed the array returns SPARDA_ERR_WORKSPACE.  The array holds
+ *     511 rows x splits x 16 heads x (D + 2) floats, which covers every call the v1 limits allow
+ *     (partials exist only below 256 rows, with at most ceil(256 / rows) splits per row).
+ */
+#define SPARDA_NOALLOC_SCRATCH_BYTES ((size_t)4718592) /* 4.5 MiB */
+int sparda_sparse_attn_noalloc(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
+                               const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt,
+                               float sm_scale, void* o, hipStream_t stream);
 
 /*
  * sparda_indexer_kl -- the indexer-training loss of Sec. 4.2 (Eq. 6-7) per query row, and its

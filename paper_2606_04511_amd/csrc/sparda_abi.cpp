@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "launch.hpp"
@@ -133,6 +134,90 @@ size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_sp
 int hip_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(SPARDA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
   return ok();
+}
+
+// Scratch of sparda_sparse_attn_noalloc: the split partials of attention calls with fewer rows
+// than CUs.  Partials exist only below 256 rows, with at most ceil(256 / rows) splits per row,
+// so rows x splits <= 511 and 511 x 16 heads x (128 + 2) floats = 4.25 MB covers every call.
+// One copy per GPU, for the life of the process.  Host code never uses the array's name as an
+// address: the device address comes from hipGetSymbolAddress, once per device.
+static_assert(SPARDA_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size is a multiple of its alignment");
+static_assert(SPARDA_NOALLOC_SCRATCH_BYTES >= (size_t)511 * 16 * (128 + 2) * sizeof(float),
+              "scratch covers the largest split partials");
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[SPARDA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up on the first call on that device.
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPARDA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SPARDA_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SPARDA_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SPARDA_OK;
+}
+
+// sparda_sparse_attn and its no-allocation variant (static_ws: the partials go to `scratch`).
+int attn_call(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k, const void* v,
+              int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale, void* o, void* ws,
+              size_t ws_bytes, bool static_ws, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k, "k", 16)) || (rc = check_dev(v, "v", 16)) ||
+      (rc = check_dev(sel, "sel", 2)) || (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(o, "o", 16)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  if (kv_mode != 0 && kv_mode != 1) return fail(SPARDA_ERR_INVALID_ARG, "kv_mode %d", kv_mode);
+  if (kv_mode == 1 && n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "staging mode needs n_q == 1");
+  if (!std::isfinite(sm_scale)) return fail(SPARDA_ERR_INVALID_ARG, "sm_scale is not finite");
+  int32_t ns = 1, bps = shape->k_total;
+  const size_t need = attn_ws(shape, n_q, q_pos0, &ns, &bps);
+  if (static_ws) {
+    if (need > SPARDA_NOALLOC_SCRATCH_BYTES)
+      return fail(SPARDA_ERR_WORKSPACE, "split partials of %zu bytes exceed the %zu-byte static scratch", need,
+                  (size_t)SPARDA_NOALLOC_SCRATCH_BYTES);
+    ws = nullptr;
+    if (need > 0 && (rc = scratch_address(&ws))) return rc;
+  } else if (need > 0) {
+    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  sparda::AttnArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.sel = sel;
+  a.cnt = cnt;
+  a.o = static_cast<uint16_t*>(o);
+  a.ws = static_cast<float*>(ws);
+  a.batch = shape->batch;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.group_size = shape->group_size;
+  a.n_q = n_q;
+  a.q_pos0 = q_pos0;
+  a.t_cap = shape->t_cap;
+  a.kv_mode = kv_mode;
+  a.k_total = shape->k_total;
+  a.sm_scale = sm_scale;
+  a.n_splits = ns;
+  a.blocks_per_split = bps;
+  return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
 }
 
 }  // namespace
@@ -308,41 +393,13 @@ int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
                        const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
                        void* o, void* ws, size_t ws_bytes, hipStream_t stream) {
-  int rc = check_shape(shape);
-  if (rc) return rc;
-  if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k, "k", 16)) || (rc = check_dev(v, "v", 16)) ||
-      (rc = check_dev(sel, "sel", 2)) || (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(o, "o", 16)))
-    return rc;
-  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
-  if (kv_mode != 0 && kv_mode != 1) return fail(SPARDA_ERR_INVALID_ARG, "kv_mode %d", kv_mode);
-  if (kv_mode == 1 && n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "staging mode needs n_q == 1");
-  if (!std::isfinite(sm_scale)) return fail(SPARDA_ERR_INVALID_ARG, "sm_scale is not finite");
-  int32_t ns = 1, bps = shape->k_total;
-  const size_t need = attn_ws(shape, n_q, q_pos0, &ns, &bps);
-  if (need > 0) {
-    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
-    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  }
-  sparda::AttnArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k);
-  a.v = static_cast<const uint16_t*>(v);
-  a.sel = sel;
-  a.cnt = cnt;
-  a.o = static_cast<uint16_t*>(o);
-  a.ws = static_cast<float*>(ws);
-  a.batch = shape->batch;
-  a.n_kv_heads = shape->n_kv_heads;
-  a.group_size = shape->group_size;
-  a.n_q = n_q;
-  a.q_pos0 = q_pos0;
-  a.t_cap = shape->t_cap;
-  a.kv_mode = kv_mode;
-  a.k_total = shape->k_total;
-  a.sm_scale = sm_scale;
-  a.n_splits = ns;
-  a.blocks_per_split = bps;
-  return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
+  return attn_call(shape, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale, o, ws, ws_bytes, false, stream);
+}
+
+int sparda_sparse_attn_noalloc(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
+                               const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt,
+                               float sm_scale, void* o, hipStream_t stream) {
+  return attn_call(shape, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale, o, nullptr, 0, true, stream);
 }
 
 int sparda_indexer_kl(const sparda_shape* shape, const void* q, const void* k, const void* f, const void* k_cmp,

@@ -26,9 +26,10 @@ SPARDA_OP_FORECAST_SELECT = 1
 SPARDA_OP_SPARSE_ATTN = 2
 SPARDA_OP_MULTIHEAD_SELECT = 3
 SPARDA_OP_INDEXER_KL = 4
+SPARDA_NOALLOC_SCRATCH_BYTES = 4718592  # the static scratch of sparda_sparse_attn_noalloc (include/sparda.h)
 
-EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select", "sparda_sparse_attn",
-            "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
+EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select",
+            "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
 
@@ -95,13 +96,14 @@ def load() -> ctypes.CDLL:
         lib.sparda_forecast_score_max.argtypes = [S, P, i32, i64, P, P, P]
         lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
+        lib.sparda_sparse_attn_noalloc.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P]
         lib.sparda_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P, P, P]
         lib.sparda_indexer_kl.argtypes = [S, P, P, P, P, i32, i64, ctypes.c_float, i32, P, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_writeback_kv.argtypes = [S, P, P, i32, i64, P, P, i32, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
-        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select", "sparda_sparse_attn",
-                     "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
+        for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max",
+                     "sparda_multihead_select", "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
         lib.sparda_status_string.argtypes = [ctypes.c_int]
@@ -186,6 +188,14 @@ def sparda_sparse_attn(shape: SpardaShape, q, n_q: int, q_pos0: int, k, v, kv_mo
         ws_bytes = ws.numel() * ws.element_size()
     _check(load().sparda_sparse_attn(ctypes.byref(cs), _p(q), n_q, q_pos0, _p(k), _p(v), kv_mode, _p(sel), _p(cnt),
                                      float(sm_scale), _p(o), _p(ws), ws_bytes, _stream(stream)), "sparda_sparse_attn")
+
+
+def sparda_sparse_attn_noalloc(shape: SpardaShape, q, n_q: int, q_pos0: int, k, v, kv_mode: int, sel, cnt,
+                               sm_scale: float, o, stream=None):
+    cs = shape.c()
+    _check(load().sparda_sparse_attn_noalloc(ctypes.byref(cs), _p(q), n_q, q_pos0, _p(k), _p(v), kv_mode, _p(sel),
+                                             _p(cnt), float(sm_scale), _p(o), _stream(stream)),
+           "sparda_sparse_attn_noalloc")
 
 
 def sparda_gather_blocks(shape: SpardaShape, host_k, host_v, sel, cnt, stage_k, stage_v, n_workgroups: int,

@@ -182,6 +182,26 @@ def test_attention_argument_errors(lib):
     assert sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, 4095) > 0  # 16 rows: split
 
 
+def test_attention_noalloc_argument_errors(lib):
+    # the same validation as sparda_sparse_attn, before any HIP call; no workspace is needed
+    s = shape()
+    a = sp.sparda_sparse_attn_noalloc
+    sc = 1 / math.sqrt(128)
+    assert rc_of(a, s, FAKE, 1, 4095, FAKE, FAKE, 2, FAKE, FAKE, sc, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, FAKE, 2, 4094, FAKE, FAKE, 1, FAKE, FAKE, sc, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, None, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, shape(head_dim=64), FAKE, 1, 4095, FAKE, FAKE, 0, FAKE, FAKE, sc, FAKE, 0) == \
+        sp.SPARDA_ERR_UNSUPPORTED
+    # the largest split partials any call can need fit the static scratch: below 256 rows there are
+    # at most ceil(256 / rows) splits per row, so rows x splits <= 511, at 16 heads of 130 floats
+    worst = 0
+    for rows in range(1, 256):
+        s2 = shape(batch=rows, n_kv_heads=1, group_size=16, k_total=1024, t_cap=65536, nc_cap=1024)
+        worst = max(worst, sp.sparda_workspace_size(s2, sp.SPARDA_OP_SPARSE_ATTN, 1, 65535))
+    assert 0 < worst <= sp.SPARDA_NOALLOC_SCRATCH_BYTES
+    assert worst == 510 * 16 * 130 * 4
+
+
 def test_gather_argument_errors(lib):
     s = shape()
     g = sp.sparda_gather_blocks
