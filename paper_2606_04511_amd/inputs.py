@@ -144,6 +144,23 @@ def values(w: Workload, t_cap: int, device="cpu", tensor_id: int = 3, seed: int 
     return v
 
 
+def block_coded_values(batch: int, n_kv_heads: int, t_cap: int, device="cpu") -> torch.Tensor:
+    """V cache bf16 [B][Hkv][t_cap][D] that identifies the block of every token: all 64 tokens of
+    block j hold the same vector, 1.0 at dimension j mod 64 and at dimension 64 + (j div 64) mod 64,
+    0.0 elsewhere (a two-coordinate code, unique for j < 4096).  An attention output over such
+    values is, per dimension, the attention mass of the few attended blocks that share that
+    coordinate, so leaving out, adding or exchanging one block changes some output element by
+    that block's whole mass."""
+    D = 128
+    assert t_cap % BLOCK == 0
+    j = torch.arange(t_cap // BLOCK, device=device)
+    blk = torch.zeros(t_cap // BLOCK, D, dtype=torch.bfloat16, device=device)
+    blk[j, j % 64] = 1.0
+    blk[j, 64 + (j // 64) % 64] = 1.0
+    v = blk.repeat_interleave(BLOCK, dim=0)  # [t_cap][D]
+    return v.expand(batch, n_kv_heads, t_cap, D).contiguous()
+
+
 def make_case(w: Workload, device="cpu", t_cap: int | None = None, seed: int | None = None) -> dict:
     """All inputs of one layer: q [B][Hq][n_q][D], f [B][Hkv][n_q][D], k, v [B][Hkv][t_cap][D]."""
     seed = w.seed if seed is None else seed

@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2606_04511_amd.sparda as sp
 from paper_2606_04511_amd import inputs
-from parity import compare_attention, compare_multihead_selection, compare_selection
+from parity import abs_bits, compare_attention, compare_multihead_selection, compare_selection
 
 pytestmark = pytest.mark.gpu
 SCALE = 1.0 / math.sqrt(128)
@@ -242,8 +242,9 @@ def test_attention_on_oracle_sets(dev, B, H, G, T, n_q, k_total):
     out = gpu_attend(s, case["q"].to(dev), n_q, q_pos0, case["k"].to(dev), case["v"].to(dev), 0,
                      torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), dev)
     ref = oracle.sparse_attn(o, q16, n_q, q_pos0, k16, v16, 0, sel, cnt, SCALE)
-    worst = compare_attention(out.float().cpu().numpy(), ref, "attention")
-    say(f"  max err {worst:.3g}")
+    wab = oracle.sparse_attn(o, q16, n_q, q_pos0, k16, abs_bits(v16), 0, sel, cnt, SCALE)
+    worst = compare_attention(out.float().cpu().numpy(), ref, "attention", wab)
+    say(f"  max err {worst:.3g} ({compare_attention.last_tight_ratio:.3f} of the tight bar)")
 
 
 def test_attention_staging_mode(dev):
@@ -258,7 +259,8 @@ def test_attention_staging_mode(dev):
     out = gpu_attend(s, case["q"].to(dev), 1, T - 1, inputs.from_u16(st_k, dev), inputs.from_u16(st_v, dev), 1,
                      torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), dev)
     ref = oracle.sparse_attn(o, inputs.to_u16(case["q"]), 1, T - 1, k16, v16, 0, sel, cnt, SCALE)
-    compare_attention(out.float().cpu().numpy(), ref, "staging")
+    wab = oracle.sparse_attn(o, inputs.to_u16(case["q"]), 1, T - 1, k16, abs_bits(v16), 0, sel, cnt, SCALE)
+    compare_attention(out.float().cpu().numpy(), ref, "staging", wab)
 
 
 def test_attention_order_invariance_and_skips(dev):
@@ -306,7 +308,8 @@ def test_attention_duplicate_entries_attended_once(dev, n_q):
     out = gpu_attend(s2, case["q"].to(dev), n_q, q_pos0, case["k"].to(dev), case["v"].to(dev), 0,
                      torch.from_numpy(dup).to(dev), torch.from_numpy(cnt2).to(dev), dev)
     ref = oracle.sparse_attn(o, inputs.to_u16(case["q"]), n_q, q_pos0, k16, v16, 0, sel, cnt, SCALE)
-    compare_attention(out.float().cpu().numpy(), ref, "duplicates")
+    wab = oracle.sparse_attn(o, inputs.to_u16(case["q"]), n_q, q_pos0, k16, abs_bits(v16), 0, sel, cnt, SCALE)
+    compare_attention(out.float().cpu().numpy(), ref, "duplicates", wab)
 
 
 # ----------------------------------------------------------------------------- gather
@@ -399,8 +402,9 @@ def _decode_full(dev, name, n_sample_rows, n_sample_heads):
         ssel = sel_mixed[b:b + 1, m:m + 1].cpu().numpy()
         scnt = cnt[b:b + 1, m:m + 1].cpu().numpy()
         ref = oracle.sparse_attn(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE)
+        wab = oracle.sparse_attn(o1, q16, 1, T - 1, k16, abs_bits(v16), 0, ssel, scnt, SCALE)
         got = out[b:b + 1, m * w.group_size:(m + 1) * w.group_size].float().cpu().numpy()
-        worst = max(worst, compare_attention(got, ref, f"{name} {(b, m)}"))
+        worst = max(worst, compare_attention(got, ref, f"{name} {(b, m)}", wab))
     say(f"  sampled {len(pairs)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
 
 
@@ -453,9 +457,69 @@ def test_full_prefill_t32k_samples(dev):
         for r in rows_r[::3]:
             for h in range(G):
                 ref = oracle.attend_row(o1, q16, T, 0, k16, v16, 0, ssel, scnt, SCALE, 0, h, r)
+                wab = oracle.attend_row(o1, q16, T, 0, k16, abs_bits(v16), 0, ssel, scnt, SCALE, 0, h, r)
                 got = out[0, m * G + h, r].float().cpu().numpy()
-                worst = max(worst, compare_attention(got, ref, f"prefill {(m, h, r)}"))
+                worst = max(worst, compare_attention(got, ref, f"prefill {(m, h, r)}", wab))
     say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
+
+
+# Block-coded V (every token of block j holds a 0/1 code of j, see inputs.block_coded_values) at full
+# size, in the launch configurations the benchmark times, checked on sampled rows against both
+# attention bars.  On these values a kernel that attends one wrong block, drops one or counts one
+# twice misses the tight bar by a factor of ten or more (tests/test_parity_bars.py shows it on the
+# CPU for every attended block of rows of the same shapes).
+BLOCK_CODED = [
+    # name, B, Hkv, G, T, n_q, k_total, n_local, sampled (b, m) pairs or rows
+    ("decode B32 128K k64 (one workgroup per row)", 32, 8, 4, 131072, 1, 64, 2, 12),
+    ("decode B8 32K k64 (split rows + combine)", 8, 8, 4, 32768, 1, 64, 2, 12),
+    ("decode B32 128K k96 (entries past 64 in the repeat scan)", 32, 8, 4, 131072, 1, 96, 2, 8),
+    ("decode B32 128K Hkv2 G16 k96 local 32 (paper layout, split, P V on MFMA)", 32, 2, 16, 131072, 1, 96, 32, 8),
+    ("decode B128 32K Hkv2 G16 k64 (one workgroup per row, P V on MFMA)", 128, 2, 16, 32768, 1, 64, 2, 8),
+    ("prefill 32K k64 (tiles of 64 rows)", 1, 8, 4, 32768, 32768, 64, 2, 24),
+    ("prefill 32K Hkv2 G16 k96 local 32 (tiles of 16 rows)", 1, 2, 16, 32768, 32768, 96, 32, 24),
+]
+
+
+@pytest.mark.parametrize("name,B,H,G,T,n_q,k_total,n_local,n_sample", BLOCK_CODED)
+def test_block_coded_attention_full_size(dev, name, B, H, G, T, n_q, k_total, n_local, n_sample):
+    say(f"block-coded V: {name}: generating on the GPU")
+    w = inputs.Workload("blockcoded", batch=B, seq_len=T, n_q=n_q, n_kv_heads=H, group_size=G, k_total=k_total,
+                        n_local=n_local, seed=8800 + T // 1024 + G + k_total)
+    nb = T // 64
+    q = inputs.normal_bf16((B, H * G, n_q, 128), w.seed, 0, dev)
+    f = inputs.normal_bf16((B, H, n_q, 128), w.seed, 1, dev)
+    k = inputs.keys_with_plants(w, f[:, :, -1, :], T, dev, seed=w.seed)
+    v = inputs.block_coded_values(B, H, T, dev)
+    s, _ = shapes(B, H, G, k_total, T, nb, 1, n_local)
+    kc = gpu_compress(s, k, T, nb, nb, dev)
+    q_pos0 = T - n_q
+    sel, cnt = gpu_select(s, f, n_q, q_pos0, kc, dev)
+    out = gpu_attend(s, q, n_q, q_pos0, k, v, 0, sel, cnt, dev)
+    _, o1 = shapes(1, 1, G, k_total, T, nb, 1, n_local)
+    rng = np.random.default_rng(13)
+    if n_q == 1:
+        picks = sorted({(int(rng.integers(B)), int(rng.integers(H)), 0) for _ in range(n_sample)})
+    else:
+        rows = sorted(set(int(x) for x in rng.integers(4096, T, size=n_sample)) | {4096, T - 1})
+        picks = [(0, int(rng.integers(H)), r) for r in rows]
+    sel_np, cnt_np = sel.cpu().numpy(), cnt.cpu().numpy()
+    worst = ratio = 0.0
+    cache = {}
+    for (b, m, r) in picks:
+        if (b, m) not in cache:
+            cache[(b, m)] = (inputs.to_u16(k[b:b + 1, m:m + 1]), inputs.to_u16(v[b:b + 1, m:m + 1]))
+        k16, v16 = cache[(b, m)]
+        q16 = inputs.to_u16(q[b:b + 1, m * G:(m + 1) * G, r:r + 1])
+        p = q_pos0 + r
+        ssel = sel_np[b:b + 1, m:m + 1, r:r + 1]
+        scnt = cnt_np[b:b + 1, m:m + 1, r:r + 1]
+        assert int(scnt[0, 0, 0]) >= 1
+        ref = oracle.sparse_attn(o1, q16, 1, p, k16, v16, 0, ssel, scnt, SCALE)
+        wab = oracle.sparse_attn(o1, q16, 1, p, k16, abs_bits(v16), 0, ssel, scnt, SCALE)
+        got = out[b:b + 1, m * G:(m + 1) * G, r:r + 1].float().cpu().numpy()
+        worst = max(worst, compare_attention(got, ref, f"{name} {(b, m, r)}", wab))
+        ratio = max(ratio, compare_attention.last_tight_ratio)
+    say(f"  {len(picks)} rows: max |o - oracle| {worst:.3g}, at most {ratio:.3f} of the tight bar")
 
 
 def test_paper_configuration_prefill_samples(dev):
@@ -498,8 +562,9 @@ def test_paper_configuration_prefill_samples(dev):
         for r in rows_r[::3]:
             for h in range(0, G, 5):
                 ref = oracle.attend_row(o1, q16, T, 0, k16, v16, 0, ssel, scnt, SCALE, 0, h, r)
+                wab = oracle.attend_row(o1, q16, T, 0, k16, abs_bits(v16), 0, ssel, scnt, SCALE, 0, h, r)
                 got = out[0, m * G + h, r].float().cpu().numpy()
-                worst = max(worst, compare_attention(got, ref, f"paper prefill {(m, h, r)}"))
+                worst = max(worst, compare_attention(got, ref, f"paper prefill {(m, h, r)}", wab))
     say(f"  sampled {len(rows_r) * w.n_kv_heads} rows, tie swaps {swaps}, attention max err {worst:.3g}")
 
 
@@ -943,7 +1008,10 @@ def test_reuse_pipeline_attends_exact_tokens(dev):
         q16 = inputs.to_u16(case["q"][:, :, 0:1])
         for h in range(H * G):
             ref = oracle.attend_row(o, q16, 1, p, k16, v16, 0, sel[:, :, None], cnt[:, :, None], SCALE, 0, h, 0)
-            worst = max(worst, compare_attention(out[0, h, 0].float().cpu().numpy(), ref, f"step {step} head {h}"))
+            wab = oracle.attend_row(o, q16, 1, p, k16, abs_bits(v16), 0, sel[:, :, None], cnt[:, :, None], SCALE,
+                                    0, h, 0)
+            worst = max(worst, compare_attention(out[0, h, 0].float().cpu().numpy(), ref, f"step {step} head {h}",
+                                                 wab))
     say(f"  fetched {fetched} of {selected} selected blocks, attention max err {worst:.3g}")
     assert fetched < selected
 
@@ -966,11 +1034,16 @@ KL_CASES = [
 
 @pytest.mark.parametrize("B,H,G,T,n_q,k_top,n_init,n_local,grid", KL_CASES)
 def test_indexer_kl_matches_oracle(dev, B, H, G, T, n_q, k_top, n_init, n_local, grid):
-    """Loss and gradient per row against the oracle.  float32 softmaxes over up to 16K keys and
-    bucket sums over up to 1K positions carry relative errors of a few 1e-6, so the bars are
-    |loss - ref| <= 2e-4 + 1e-3 |ref| and |dF - ref| <= 1e-3 |ref| + 1e-3 max |ref| + 1e-6; the
-    absolute 1e-6 covers rows whose exact gradient vanishes (k_top = 0), where float32 leaves
-    a residue of a few ulps of the bucket weights times sm_scale max |K~| ~ 1e-8."""
+    """Loss and gradient per row against the oracle.  The kernels accumulate every softmax and
+    bucket sum in float32 as per-lane partial sums of at most a few hundred terms merged in a tree,
+    so each normalised weight carries a relative error of order 100 ulps (1e-5) at most; the loss
+    is a difference of cross-entropy terms of size ~1-10 with weights summing to 1 and the gradient
+    a weighted sum of the compressed keys, hence the bars
+        |loss - ref| <= 4e-6 + 1e-5 |ref|,   |dF - ref| <= 1e-5 (|ref| + max |ref|) + 2e-8,
+    where 2e-8 covers rows whose exact gradient vanishes (k_top = 0: float32 leaves a residue of a
+    few ulps of the bucket weights times sm_scale |K~|).  The largest errors measured over these
+    cases were 2.4e-7 (loss, rows with loss 0.005-0.2) and 1.7e-9 (gradient, max |dF| 2e-4 to 1e-2),
+    about 20 times inside the bars."""
     lw, sw = grid
     say(f"indexer kl B{B} H{H} G{G} T{T} n_q{n_q} k{k_top} init {n_init} local {n_local} grid {grid}")
     w, case = make(B, H, G, T, n_q, 8, 9100 + T + G, n_init=n_init, n_local=n_local)
@@ -991,18 +1064,23 @@ def test_indexer_kl_matches_oracle(dev, B, H, G, T, n_q, k_top, n_init, n_local,
     torch.cuda.synchronize()
     loss_g, dF_g = loss.cpu().numpy(), dF.cpu().numpy()
     q16, f16 = inputs.to_u16(case["q"]), inputs.to_u16(case["f"])
-    worst_l = worst_d = 0.0
+    worst_l = worst_d = ratio_l = ratio_d = 0.0
     for b in range(B):
         for m in range(H):
             for r in range(n_q):
                 ref, dref, _, _ = oracle.indexer_kl_row(o, q16, kct, 2, 1, f16, kcp, n_q, q_pos0, SCALE, k_top, b, m, r)
                 gl = float(loss_g[b, m, r])
-                assert abs(gl - ref) <= 2e-4 + 1e-3 * abs(ref), f"row {(b, m, r)}: loss {gl} vs {ref}"
-                tol = 1e-3 * np.abs(dref) + 1e-3 * np.abs(dref).max() + 1e-6
-                assert np.all(np.abs(dF_g[b, m, r] - dref) <= tol), f"row {(b, m, r)}: gradient"
+                bar_l = 4e-6 + 1e-5 * abs(ref)
+                assert abs(gl - ref) <= bar_l, f"row {(b, m, r)}: loss {gl} vs {ref}"
+                tol = 1e-5 * (np.abs(dref) + np.abs(dref).max()) + 2e-8
+                err_d = np.abs(dF_g[b, m, r] - dref)
+                assert np.all(err_d <= tol), f"row {(b, m, r)}: gradient off by {float(err_d.max()):.3g}"
                 worst_l = max(worst_l, abs(gl - ref))
-                worst_d = max(worst_d, float(np.abs(dF_g[b, m, r] - dref).max()))
-    say(f"  worst |loss - ref| {worst_l:.3g}, worst |dF - ref| {worst_d:.3g}")
+                worst_d = max(worst_d, float(err_d.max()))
+                ratio_l = max(ratio_l, abs(gl - ref) / bar_l)
+                ratio_d = max(ratio_d, float((err_d / tol).max()))
+    say(f"  worst |loss - ref| {worst_l:.3g} ({ratio_l:.3f} of its bar), worst |dF - ref| {worst_d:.3g} "
+        f"({ratio_d:.3f} of its bar)")
 
 
 def test_paper_configuration_decode_samples(dev):
@@ -1043,5 +1121,7 @@ def test_paper_configuration_decode_samples(dev):
         scnt = cnt[b:b + 1, m:m + 1].cpu().numpy()
         for h in range(0, G, 5):
             ref = oracle.attend_row(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE, 0, h, 0)
-            worst = max(worst, compare_attention(out[b, m * G + h, 0].float().cpu().numpy(), ref, f"{(b, m, h)}"))
+            wab = oracle.attend_row(o1, q16, 1, T - 1, k16, abs_bits(v16), 0, ssel, scnt, SCALE, 0, h, 0)
+            worst = max(worst, compare_attention(out[b, m * G + h, 0].float().cpu().numpy(), ref, f"{(b, m, h)}",
+                                                 wab))
     say(f"  sampled {len(pairs)} rows, tie swaps {swaps}, attention max err {worst:.3g}")

@@ -17,7 +17,7 @@ import oracle
 import paper_2606_04511_amd.sparda as sp
 from paper_2606_04511_amd import hostmem, inputs
 from paper_2606_04511_amd.pipeline import DecodePipeline
-from parity import compare_attention, compare_selection
+from parity import abs_bits, compare_attention, compare_selection
 
 pytestmark = pytest.mark.gpu
 
@@ -69,15 +69,17 @@ def setup():
                      kc=kc, k0=kv[0][0].to(dev), v0=kv[0][1].to(dev), pools=layer_pool, n_workgroups=16,
                      device=dev)
     # the oracle chain
-    ref_sel, ref_out = [], []
+    ref_sel, ref_out, ref_w = [], [], []
     for l in range(L):
         frows = f0 if l == 0 else f[l - 1]
         s, c = oracle.forecast_select(oshape, inputs.to_u16(frows), 1, T - 1, kc_ref[l])
         ref_sel.append((s, c, frows))
-        ref_out.append(oracle.sparse_attn(oshape, inputs.to_u16(q[l]), 1, T - 1, inputs.to_u16(layer_kv[l][0]),
-                                          inputs.to_u16(layer_kv[l][1]), 0, s, c, 1.0 / math.sqrt(128)))
-    return dict(dev=dev, oshape=oshape, pipe_args=pipe_args, ref_sel=ref_sel, ref_out=ref_out, kc_ref=kc_ref,
-                bufs=bufs)
+        args = (oshape, inputs.to_u16(q[l]), 1, T - 1, inputs.to_u16(layer_kv[l][0]))
+        v16 = inputs.to_u16(layer_kv[l][1])
+        ref_out.append(oracle.sparse_attn(*args, v16, 0, s, c, 1.0 / math.sqrt(128)))
+        ref_w.append(oracle.sparse_attn(*args, abs_bits(v16), 0, s, c, 1.0 / math.sqrt(128)))
+    return dict(dev=dev, oshape=oshape, pipe_args=pipe_args, ref_sel=ref_sel, ref_out=ref_out, ref_w=ref_w,
+                kc_ref=kc_ref, bufs=bufs)
 
 
 def check(setup, pipe):
@@ -89,7 +91,7 @@ def check(setup, pipe):
                           [(b, m, 0) for b in range(B) for m in range(H)])
         same = np.array_equal(gs, s)
         assert same, f"layer {l}: selection differs within the tie window; pick another seed"
-        compare_attention(pipe.o[l].float().cpu().numpy(), setup["ref_out"][l], f"layer {l}")
+        compare_attention(pipe.o[l].float().cpu().numpy(), setup["ref_out"][l], f"layer {l}", setup["ref_w"][l])
 
 
 @pytest.mark.parametrize("overlap", [True, False])
