@@ -286,6 +286,9 @@ int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int
  * (Sec. 4.3 persistent prefetch; Alg. 2 "launch prefetch of B_{l+1}").
  *   host_k, host_v in : bf16 [B][Hkv][t_cap][D] pinned host memory mapped into the device
  *                       address space (e.g. hipHostMalloc); SPARDA_ERR_HOST_NOT_MAPPED otherwise.
+ *                       The allocation holding each pointer must extend B Hkv t_cap D 2 bytes
+ *                       from it (looked up with hipMemGetAddressRange); SPARDA_ERR_INVALID_ARG
+ *                       otherwise, so a short pool is refused before any PCIe access.
  *   sel, cnt       in : device, decode-form selection: int16 [B][Hkv][k_total] and [B][Hkv].
  *   stage_k, stage_v out : bf16 [B][Hkv][k_total][L][D] device; slot s < cnt receives block
  *                       sel[s]; other slots are untouched; entries with (sel+1)*L > t_cap are
@@ -307,8 +310,9 @@ int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const vo
  *   k_new, v_new in : bf16 [B][Hkv][n_new][D] device (16-byte aligned).
  *   n_new, pos0     : the rows land at positions [pos0, pos0 + n_new) of every (batch, group)
  *                     pool row; n_new >= 1, pos0 >= 0, pos0 + n_new <= t_cap.
- *   host_k, host_v out: bf16 [B][Hkv][t_cap][D] pinned host memory mapped for the device (as for
- *                     sparda_gather_blocks; SPARDA_ERR_HOST_NOT_MAPPED otherwise).
+ *   host_k, host_v out: bf16 [B][Hkv][t_cap][D] pinned host memory mapped for the device, each
+ *                     allocation extending B Hkv t_cap D 2 bytes from the pointer (as for
+ *                     sparda_gather_blocks: SPARDA_ERR_HOST_NOT_MAPPED, SPARDA_ERR_INVALID_ARG).
  *   n_workgroups    : persistent workgroups writing over PCIe (the CU budget), >= 1.
  * The copy is bitwise; positions outside the range are not touched.  Ordering against gathers
  * or host reads of the same positions is the caller's (record an event, synchronise).

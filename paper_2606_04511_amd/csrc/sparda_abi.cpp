@@ -453,8 +453,11 @@ int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int
                     "plan launch");
 }
 
-// The device address of a pinned host pool mapped for the device, or null (with the failure set).
-static int mapped_pool(const void* host, const char* name, void** dev) {
+// The device address of a pinned host pool mapped for the device.  Fails with
+// SPARDA_ERR_HOST_NOT_MAPPED unless `host` is device-mapped pinned host memory, and with
+// SPARDA_ERR_INVALID_ARG unless the allocation holding it extends at least `need` bytes from it
+// (the largest offset a gather or write-back over the pool layout can touch).
+static int mapped_pool(const void* host, const char* name, size_t need, void** dev) {
   hipPointerAttribute_t attr;
   hipError_t e = hipPointerGetAttributes(&attr, host);
   if (e != hipSuccess) {
@@ -463,8 +466,25 @@ static int mapped_pool(const void* host, const char* name, void** dev) {
   }
   if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr)
     return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not device-mapped pinned host memory", name);
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  e = hipMemGetAddressRange(&base, &size, attr.devicePointer);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s: the extent of its allocation is unknown (%s)", name,
+                hipGetErrorString(e));
+  }
+  const uintptr_t p = reinterpret_cast<uintptr_t>(attr.devicePointer), b = reinterpret_cast<uintptr_t>(base);
+  if (p < b || p - b > size || size - (p - b) < need)
+    return fail(SPARDA_ERR_INVALID_ARG, "%s: %zu bytes of its allocation lie past the pointer, the pool layout "
+                "[B][Hkv][t_cap][D] needs %zu", name, p < b ? (size_t)0 : size - (size_t)(p - b), need);
   *dev = attr.devicePointer;
   return SPARDA_OK;
+}
+
+// Bytes of one host pool: bf16 [B][Hkv][t_cap][D].
+static size_t pool_bytes(const sparda_shape* s) {
+  return (size_t)s->batch * s->n_kv_heads * (size_t)s->t_cap * s->head_dim * sizeof(uint16_t);
 }
 
 int sparda_writeback_kv(const sparda_shape* shape, const void* k_new, const void* v_new, int32_t n_new, int64_t pos0,
@@ -481,7 +501,9 @@ int sparda_writeback_kv(const sparda_shape* shape, const void* k_new, const void
   if (n_workgroups < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_workgroups %d < 1", n_workgroups);
   void* dk = nullptr;
   void* dv = nullptr;
-  if ((rc = mapped_pool(host_k, "host_k", &dk)) || (rc = mapped_pool(host_v, "host_v", &dv))) return rc;
+  if ((rc = mapped_pool(host_k, "host_k", pool_bytes(shape), &dk)) ||
+      (rc = mapped_pool(host_v, "host_v", pool_bytes(shape), &dv)))
+    return rc;
   return hip_status(sparda::launch_writeback(static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
                                              static_cast<uint16_t*>(dk), static_cast<uint16_t*>(dv),
                                              (int64_t)shape->batch * shape->n_kv_heads, n_new, pos0, shape->t_cap,
@@ -499,20 +521,10 @@ int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const vo
       (rc = check_dev(stage_v, "stage_v", 16)))
     return rc;
   if (n_workgroups < 1) return fail(SPARDA_ERR_INVALID_ARG, "n_workgroups %d < 1", n_workgroups);
-  const void* dev_ptr[2] = {nullptr, nullptr};
-  const void* host_ptr[2] = {host_k, host_v};
-  for (int i = 0; i < 2; ++i) {
-    hipPointerAttribute_t attr;
-    hipError_t e = hipPointerGetAttributes(&attr, host_ptr[i]);
-    if (e != hipSuccess) {
-      (void)hipGetLastError();  // clear the sticky-free error state of this query
-      return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not a registered HIP allocation (%s)", i ? "host_v" : "host_k",
-                  hipGetErrorString(e));
-    }
-    if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr)
-      return fail(SPARDA_ERR_HOST_NOT_MAPPED, "%s is not device-mapped pinned host memory", i ? "host_v" : "host_k");
-    dev_ptr[i] = attr.devicePointer;
-  }
+  void* dev_ptr[2] = {nullptr, nullptr};
+  if ((rc = mapped_pool(host_k, "host_k", pool_bytes(shape), &dev_ptr[0])) ||
+      (rc = mapped_pool(host_v, "host_v", pool_bytes(shape), &dev_ptr[1])))
+    return rc;
   return hip_status(sparda::launch_gather(static_cast<const uint16_t*>(dev_ptr[0]), static_cast<const uint16_t*>(dev_ptr[1]),
                                           sel, cnt, static_cast<uint16_t*>(stage_k), static_cast<uint16_t*>(stage_v),
                                           (int64_t)shape->batch * shape->n_kv_heads, shape->t_cap, shape->k_total,

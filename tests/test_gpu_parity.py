@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import paper_2606_04511_amd.sparda as sp
-from paper_2606_04511_amd import inputs
+from paper_2606_04511_amd import hostmem, inputs
 from parity import abs_bits, compare_attention, compare_multihead_selection, compare_selection
 
 pytestmark = pytest.mark.gpu
@@ -337,6 +337,22 @@ def test_gather_bitwise_and_host_checks(dev):
     with pytest.raises(sp.SpardaError) as ei:
         sp.sparda_gather_blocks(s, case["k"], case["v"], sel_d, cnt_d, st_k, st_v, 8)  # pageable memory
     assert ei.value.status == sp.SPARDA_ERR_HOST_NOT_MAPPED
+    # pools shorter than the [B][Hkv][t_cap][D] layout are refused before any launch: one 16-byte
+    # piece short, and a pointer 4 KiB into an allocation of exactly the layout's size
+    need = B * H * T * 128 * 2
+    short = hostmem.PinnedBuffer(need - 16)
+    exact = hostmem.PinnedBuffer(need)
+    for hk_bad, hv_ok in ((short.ptr, hv), (hk, short.ptr), (exact.ptr + 4096, hv)):
+        with pytest.raises(sp.SpardaError) as ei:
+            sp.sparda_gather_blocks(s, hk_bad, hv_ok, sel_d, cnt_d, st_k, st_v, 8)
+        assert ei.value.status == sp.SPARDA_ERR_INVALID_ARG, ei.value
+    with pytest.raises(sp.SpardaError) as ei:
+        sp.sparda_writeback_kv(s, st_k, st_v, 1, T - 1, short.ptr, hv, 8)
+    assert ei.value.status == sp.SPARDA_ERR_INVALID_ARG
+    sp.sparda_gather_blocks(s, exact.ptr, hv, sel_d, cnt_d, st_k, st_v, 8)  # exactly the layout: accepted
+    torch.cuda.synchronize()
+    short.free()
+    exact.free()
 
 
 @pytest.mark.parametrize("n_new,pos0,nwg", [(1, 8191, 16), (1, 4000, 1), (300, 1000, 7), (64, 0, 64)])
