@@ -18,6 +18,8 @@
  *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
  *                           stream so that layer l+1's fetch overlaps layer l (Sec. 4.3, Alg. 2)
+ *   sparda_stage_append_kv  the decoded token -> the staged copy of its own block (Alg. 2's append,
+ *                           for offloaded layers whose blocks were gathered before the token existed)
  *   sparda_writeback_kv     new K/V rows -> the pinned host pools (the asynchronous write-back of
  *                           Sec. 5.3, Efficiency Results), for a side stream
  *   sparda_plan_staging     step-to-step reuse of the staged blocks: which blocks the next gather
@@ -300,6 +302,22 @@ int sparda_plan_staging(const sparda_shape* shape, const int16_t* sel, const int
 int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
                          const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
                          hipStream_t stream);
+
+/*
+ * sparda_stage_append_kv -- appends the decoded token to the staged copy of its own block (Alg. 2
+ * appends each step's K/V to the cache; in an offloaded layer the attended blocks were gathered
+ * before the token existed, because layer l's prefetch is launched during layer l-1).
+ *   k_new, v_new in : bf16 [B][Hkv][D] device (16-byte aligned), the token at position q_pos.
+ *   q_pos           : the token's position, 0 <= q_pos < t_cap.
+ *   sel, cnt     in : device, the staging layout the attention will read: int16 [B][Hkv][k_total]
+ *                     and [B][Hkv] (the gather's sel/cnt, or the staging plan's sel_staged/stage_cnt).
+ *   stage_k, stage_v in/out: bf16 [B][Hkv][k_total][L][D] device staging.
+ * Every slot s < cnt with sel[s] == q_pos / L receives the row at q_pos mod L; nothing else is
+ * written.  Call it on the compute stream after the gather into that staging has completed and
+ * before the attention.
+ */
+int sparda_stage_append_kv(const sparda_shape* shape, const void* k_new, const void* v_new, int64_t q_pos,
+                           const int16_t* sel, const int16_t* cnt, void* stage_k, void* stage_v, hipStream_t stream);
 
 /*
  * sparda_writeback_kv -- stores newly created K/V rows into the pinned host pools that the

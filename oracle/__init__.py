@@ -16,6 +16,7 @@ Function map (paper sections in the C file):
   attend_row / sparse_attn     -- Eq. 1 + Eq. 5 (softmax attention over the attended blocks)
   gather_blocks                -- Sec. 4.3 / Alg. 2 (selected blocks copied into staging)
   writeback_kv                 -- Sec. 5.3 (new K/V rows written into the host pools)
+  stage_append_kv              -- Alg. 2 (the decoded token appended to the staged copy of its block)
   indexer_kl_row               -- Sec. 4.2, Eq. 6-7 (the indexer-training KL over the target's top-k
                                   partition, and its gradient with respect to the Forecast row)
   plan_staging                 -- App. C, NOSI step reuse (keep the previous step's staged blocks,
@@ -109,11 +110,13 @@ def open_library(path: str):
     lib.sparda_ref_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, f64, P]
     lib.sparda_ref_gather_blocks.argtypes = [S, P, P, P, P, P, P]
     lib.sparda_ref_writeback_kv.argtypes = [S, P, P, i32, i64, P, P]
+    lib.sparda_ref_stage_append_kv.argtypes = [S, P, P, i64, P, P, P, P]
     lib.sparda_ref_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P]
     lib.sparda_ref_indexer_kl_row.argtypes = [S, P, P, i64, i32, i32, P, P, i32, i64, f64, i32, i32, i32, i32, P, P,
                                               P, P]
     for name in ("compress_keys", "select_row", "forecast_select", "forecast_score_max", "multihead_select_row", "multihead_select",
-                 "attend_row", "sparse_attn", "gather_blocks", "writeback_kv", "plan_staging", "indexer_kl_row"):
+                 "attend_row", "sparse_attn", "gather_blocks", "writeback_kv", "stage_append_kv", "plan_staging",
+                 "indexer_kl_row"):
         getattr(lib, "sparda_ref_" + name).restype = ctypes.c_int
     return lib
 
@@ -324,6 +327,19 @@ def writeback_kv(shape: Shape, k_new, v_new, n_new: int, pos0: int, host_k, host
     _check(_load().sparda_ref_writeback_kv(ctypes.byref(cs), _ptr(k_new), _ptr(v_new), n_new, pos0, _ptr(hk),
                                            _ptr(hv)), "writeback_kv")
     return hk, hv
+
+
+def stage_append_kv(shape: Shape, k_new, v_new, q_pos: int, sel, cnt, stage_k, stage_v):
+    """Copies of stage_k, stage_v (uint16 [B][Hkv][k_total][L][D]) with the token at q_pos (k_new,
+    v_new: uint16 [B][Hkv][D]) written into every slot s < cnt that holds its block."""
+    k_new, v_new = _u16(k_new), _u16(v_new)
+    sk, sv = np.array(_u16(stage_k), copy=True), np.array(_u16(stage_v), copy=True)
+    sel = np.ascontiguousarray(sel, np.int16)
+    cnt = np.ascontiguousarray(cnt, np.int16)
+    cs = shape.c()
+    _check(_load().sparda_ref_stage_append_kv(ctypes.byref(cs), _ptr(k_new), _ptr(v_new), q_pos, _ptr(sel), _ptr(cnt),
+                                              _ptr(sk), _ptr(sv)), "stage_append_kv")
+    return sk, sv
 
 
 def plan_staging(shape: Shape, sel, cnt, q_pos: int, slot_blk, slot_len):

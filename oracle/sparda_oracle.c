@@ -548,8 +548,8 @@ int sparda_ref_gather_blocks(const ref_shape* s, const uint16_t* host_k, const u
   return REF_OK;
 }
 
-/* Sec. 5.3 (Efficiency Results, prefill throughput): the write-back of newly created KV rows into the host pools.  k_new, v_new: bf16
- * [B][Hkv][n_new][D]; the rows land at positions pos0 .. pos0 + n_new - 1 of the pools
+/* Sec. 5.3 (Efficiency Results, prefill throughput): the write-back of newly created KV rows
+ * into the host pools.  k_new, v_new: bf16 [B][Hkv][n_new][D]; the rows land at positions pos0 .. pos0 + n_new - 1 of the pools
  * host_k, host_v: bf16 [B][Hkv][t_cap][D]; nothing else is written. */
 int sparda_ref_writeback_kv(const ref_shape* s, const uint16_t* k_new, const uint16_t* v_new, int32_t n_new,
                             int64_t pos0, uint16_t* host_k, uint16_t* host_v) {
@@ -563,6 +563,32 @@ int sparda_ref_writeback_kv(const ref_shape* s, const uint16_t* k_new, const uin
       memcpy(host_k + (bm * s->t_cap + pos0 + t) * D, k_new + (bm * n_new + t) * D, (size_t)D * sizeof(uint16_t));
       memcpy(host_v + (bm * s->t_cap + pos0 + t) * D, v_new + (bm * n_new + t) * D, (size_t)D * sizeof(uint16_t));
     }
+  return REF_OK;
+}
+
+/* Alg. 2 (decode step): the token decoded at position q_pos is appended to the KV cache.  In an
+ * offloaded layer the attended blocks were copied to staging before the token existed (the
+ * prefetch of B_l is launched during layer l-1), so the token's K/V row is written into every
+ * staging slot s < cnt whose block sel[s] is the token's own block q_pos / L, at row q_pos mod L.
+ * k_new, v_new: bf16 [B][Hkv][D]; sel, cnt: decode-form [B][Hkv][k_total] and [B][Hkv];
+ * stage_k, stage_v: bf16 [B][Hkv][k_total][L][D].  Nothing else is written. */
+int sparda_ref_stage_append_kv(const ref_shape* s, const uint16_t* k_new, const uint16_t* v_new, int64_t q_pos,
+                               const int16_t* sel, const int16_t* cnt, uint16_t* stage_k, uint16_t* stage_v) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (q_pos < 0 || q_pos >= s->t_cap) return REF_ERR_INVALID_ARG;
+  const int64_t D = s->head_dim, L = s->block_size, K = s->k_total;
+  const int64_t rows = (int64_t)s->batch * s->n_kv_heads;
+  const int64_t j = q_pos / L, t = q_pos % L;
+  for (int64_t bm = 0; bm < rows; ++bm) {
+    int64_t n = cnt[bm];
+    if (n > K) n = K;
+    for (int64_t slot = 0; slot < n; ++slot) {
+      if (sel[bm * K + slot] != j) continue;
+      memcpy(stage_k + ((bm * K + slot) * L + t) * D, k_new + bm * D, (size_t)D * sizeof(uint16_t));
+      memcpy(stage_v + ((bm * K + slot) * L + t) * D, v_new + bm * D, (size_t)D * sizeof(uint16_t));
+    }
+  }
   return REF_OK;
 }
 

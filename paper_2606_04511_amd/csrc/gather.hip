@@ -94,6 +94,50 @@ hipError_t launch_writeback(const uint16_t* k_new, const uint16_t* v_new, uint16
   return hipGetLastError();
 }
 
+// ---- the decoded token into the staged copy of its own block ------------------------------------
+//
+// Alg. 2 appends each decoded token's K/V to the cache.  In an offloaded layer the attended blocks
+// were copied into staging before the token existed (layer l's prefetch is launched during layer
+// l - 1), so the token's row is written into every staging slot s < cnt whose block is the
+// token's own, p / 64, at row p % 64.  One wavefront per (batch, group) row: a ballot over the set
+// finds the slots, lanes 0-15 move the 256-byte K row and lanes 16-31 the V row of each.
+__global__ __launch_bounds__(256) void stage_append_kernel(const uint4* __restrict__ kn, const uint4* __restrict__ vn,
+                                                           const int16_t* __restrict__ sel,
+                                                           const int16_t* __restrict__ cnt, int64_t p,
+                                                           uint4* __restrict__ sk, uint4* __restrict__ sv, int64_t rows,
+                                                           int32_t K) {
+  constexpr int kPieces = kHeadDim * 2 / 16;  // 16-byte pieces per token row
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= rows) return;
+  int n = cnt[row];
+  n = n < 0 ? 0 : (n > K ? K : n);
+  const int j = (int)(p / kBlock), t = (int)(p % kBlock);
+  const int piece = lane & (kPieces - 1);
+  const bool is_k = lane < kPieces, is_v = lane >= kPieces && lane < 2 * kPieces;
+  const uint4 w = is_k ? kn[row * kPieces + piece] : (is_v ? vn[row * kPieces + piece] : make_uint4(0u, 0u, 0u, 0u));
+  for (int s0 = 0; s0 < n; s0 += kWave) {
+    const int s = s0 + lane;
+    uint64_t hit = __ballot(s < n && (int)sel[row * K + s] == j);
+    while (hit) {
+      const int slot = s0 + (int)__builtin_ctzll(hit);
+      hit &= hit - 1;
+      const int64_t dst = ((row * K + slot) * kBlock + t) * kPieces + piece;
+      if (is_k) sk[dst] = w;
+      if (is_v) sv[dst] = w;
+    }
+  }
+}
+
+hipError_t launch_stage_append(const uint16_t* k_new, const uint16_t* v_new, const int16_t* sel, const int16_t* cnt,
+                               int64_t p, uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int32_t k_total,
+                               hipStream_t stream) {
+  hipLaunchKernelGGL(stage_append_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
+                     reinterpret_cast<const uint4*>(k_new), reinterpret_cast<const uint4*>(v_new), sel, cnt, p,
+                     reinterpret_cast<uint4*>(stage_k), reinterpret_cast<uint4*>(stage_v), rows, k_total);
+  return hipGetLastError();
+}
+
 // ---- staging plan of step-to-step reuse (the NOSI engine of the paper's efficiency setup,
 // App. C: a layer keeps the blocks its previous decode step attended and fetches only the newly
 // selected ones) --------------------------------------------------------------------------------

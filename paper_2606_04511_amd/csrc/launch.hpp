@@ -161,6 +161,11 @@ hipError_t launch_plan_staging(const int16_t* sel, const int16_t* cnt, int64_t p
 hipError_t launch_writeback(const uint16_t* k_new, const uint16_t* v_new, uint16_t* host_k, uint16_t* host_v,
                             int64_t rows, int32_t n_new, int64_t pos0, int64_t t_cap, int32_t n_workgroups,
                             hipStream_t stream);
+// The decoded token's K/V rows [B][Hkv][D] into every staging slot that holds block p / 64, at row
+// p % 64 (gather.hip).
+hipError_t launch_stage_append(const uint16_t* k_new, const uint16_t* v_new, const int16_t* sel, const int16_t* cnt,
+                               int64_t p, uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int32_t k_total,
+                               hipStream_t stream);
 hipError_t launch_gather(const uint16_t* host_k, const uint16_t* host_v, const int16_t* sel, const int16_t* cnt,
                          uint16_t* stage_k, uint16_t* stage_v, int64_t rows, int64_t t_cap, int32_t k_total,
                          int32_t n_workgroups, hipStream_t stream);

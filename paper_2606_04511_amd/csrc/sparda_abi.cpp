@@ -511,6 +511,23 @@ int sparda_writeback_kv(const sparda_shape* shape, const void* k_new, const void
                     "write-back launch");
 }
 
+int sparda_stage_append_kv(const sparda_shape* shape, const void* k_new, const void* v_new, int64_t q_pos,
+                           const int16_t* sel, const int16_t* cnt, void* stage_k, void* stage_v, hipStream_t stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(k_new, "k_new", 16)) || (rc = check_dev(v_new, "v_new", 16)) || (rc = check_dev(sel, "sel", 2)) ||
+      (rc = check_dev(cnt, "cnt", 2)) || (rc = check_dev(stage_k, "stage_k", 16)) ||
+      (rc = check_dev(stage_v, "stage_v", 16)))
+    return rc;
+  if (q_pos < 0 || q_pos >= shape->t_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "q_pos %lld outside [0, t_cap)", (long long)q_pos);
+  return hip_status(sparda::launch_stage_append(static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                                                sel, cnt, q_pos, static_cast<uint16_t*>(stage_k),
+                                                static_cast<uint16_t*>(stage_v),
+                                                (int64_t)shape->batch * shape->n_kv_heads, shape->k_total, stream),
+                    "stage append launch");
+}
+
 int sparda_gather_blocks(const sparda_shape* shape, const void* host_k, const void* host_v, const int16_t* sel,
                          const int16_t* cnt, void* stage_k, void* stage_v, int32_t n_workgroups,
                          hipStream_t stream) {

@@ -27,8 +27,20 @@ def _rt():
         lib.hipHostFree.restype = ctypes.c_int
         lib.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
         lib.hipMemcpyAsync.restype = ctypes.c_int
+        lib.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
+        lib.hipHostGetDevicePointer.restype = ctypes.c_int
         _hip = lib
     return _hip
+
+
+def device_pointer(host_ptr: int) -> int:
+    """The device address of pinned host memory mapped for the device (hipHostMalloc'd, including
+    torch's pinned tensors)."""
+    d = ctypes.c_void_p()
+    rc = _rt().hipHostGetDevicePointer(ctypes.byref(d), ctypes.c_void_p(host_ptr), 0)
+    if rc != 0 or not d.value:
+        raise RuntimeError(f"hipHostGetDevicePointer failed with {rc}")
+    return int(d.value)
 
 
 class PinnedBuffer:

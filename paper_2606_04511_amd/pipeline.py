@@ -12,6 +12,16 @@ Layer 0 keeps its KV cache in HBM and selects with its current-layer Forecast (S
 staging slots alternate between layers.  All device buffers are allocated up front; a step
 allocates nothing.
 
+Alg. 2 appends each decoded token's K/V to the cache.  Given the token's K/V per layer (new_kv),
+a step appends it to layer 0's HBM cache; in an offloaded layer, whose blocks were gathered during
+layer l-1 before the token existed, it writes the token into the staged copy of its own block
+(`sparda_stage_append_kv`) before the attention, and after the attention stores it into the
+layer's host pool on the side stream (`sparda_writeback_kv`, the asynchronous CPU write-back of
+new KV entries of Sec. 5.3), where the stream order puts it before the next step's gathers.  A
+compressed key that the token completes is computed from the cache (Alg. 2's incremental K~
+update; for an offloaded layer from its host pool, after the write-back), and the next step's
+selection of that layer waits for it.
+
 With reuse=True each offloaded layer keeps its own staging buffer across decode steps (the NOSI
 engine of the paper's efficiency setup, App. C): after layer l+1's selection,
 `sparda_plan_staging` keeps the staged blocks that the new set still attends and that hold every
@@ -26,6 +36,7 @@ import math
 
 import torch
 
+from . import hostmem
 from . import sparda as sp
 
 
@@ -53,7 +64,8 @@ class DecodePipeline:
     kc[l]        -- bf16 [B][Hkv][nc_cap][D] device, compressed keys of layer l
     k0, v0       -- bf16 [B][Hkv][t_cap][D] device, layer 0's KV cache
     pools[l]     -- (host_k_ptr, host_v_ptr) of layer l (l >= 1): device-mapped pinned memory
-                    laid out [B][Hkv][t_cap][D]; pools may be shared between layers
+                    laid out [B][Hkv][t_cap][D]; pools may be shared between layers (only when
+                    steps write nothing back: a write-back goes to the layer's pool)
     n_workgroups -- persistent-grid size of the gather (its CU budget); None takes
                     gather_workgroups(batch)
     """
@@ -90,11 +102,17 @@ class DecodePipeline:
         self.ws_sel = torch.empty(max(n_sel, 16), dtype=torch.uint8, device=device)
         self.ws_att = torch.empty(max(n_att, 16), dtype=torch.uint8, device=device)
         self.side = torch.cuda.Stream(device=device)
+        self.pool_dev = [None] + [(hostmem.device_pointer(hk), hostmem.device_pointer(hv)) for hk, hv in pools[1:]]
+        self.ev_kc = [torch.cuda.Event() for _ in range(L)]
+        self.kc_pending = [False] * L
         self.ev_sel = [torch.cuda.Event() for _ in range(L)]
         self.ev_gather = [torch.cuda.Event() for _ in range(L)]
         self.ev_attn = [torch.cuda.Event() for _ in range(L)]
 
     def _select(self, f_rows, layer):
+        if self.kc_pending[layer]:  # a compressed key completed by the last token is being written
+            torch.cuda.current_stream().wait_event(self.ev_kc[layer])
+            self.kc_pending[layer] = False
         sp.sparda_forecast_select(self.shape, f_rows, 1, self.t_ctx - 1, self.kc[layer], self.sel[layer],
                                   self.cnt[layer], self.ws_sel)
         if self.reuse and layer >= 1:
@@ -127,18 +145,56 @@ class DecodePipeline:
         sp.sparda_sparse_attn(self.shape, self.q[layer], 1, self.t_ctx - 1, k, v, mode, sel, cnt, self.scale,
                               self.o[layer], self.ws_att)
 
+    def _new_windows(self, p):
+        """Compressed keys [begin, end) that the token at position p completes."""
+        lw, sw = self.shape.cmp_kernel, self.shape.cmp_stride
+        last = (p + 1 - lw) // sw if p + 1 >= lw else -1
+        prev = (p - lw) // sw if p >= lw else -1
+        return prev + 1, last + 1
+
+    def _append_layer0(self, k_new, v_new, p):
+        """Alg. 2's append on the HBM-resident layer 0 (a device copy into its cache), then the
+        compressed keys the token completes."""
+        self.k0[:, :, p].copy_(k_new[:, :, 0])
+        self.v0[:, :, p].copy_(v_new[:, :, 0])
+        w0, w1 = self._new_windows(p)
+        if w1 > w0:
+            sp.sparda_compress_keys(self.shape, self.k0, p + 1, w0, w1, self.kc[0])
+
+    def _staging_of(self, layer):
+        if self.reuse:
+            return self.stage[layer], self.sel_staged[layer], self.stage_cnt[layer]
+        return self.stage[layer % 2], self.sel[layer], self.cnt[layer]
+
+    def _writeback(self, layer, k_new, v_new, p, stream):
+        """The token into the layer's host pool (Sec. 5.3's asynchronous write-back), then the
+        compressed keys it completes, read from the pool; ev_kc[layer] marks the end."""
+        hk, hv = self.pools[layer]
+        sp.sparda_writeback_kv(self.shape, k_new, v_new, 1, p, hk, hv, self.n_workgroups, stream)
+        w0, w1 = self._new_windows(p)
+        if w1 > w0:
+            sp.sparda_compress_keys(self.shape, self.pool_dev[layer][0], p + 1, w0, w1, self.kc[layer], stream)
+            self.ev_kc[layer].record(stream)
+            self.kc_pending[layer] = True
+
     def fetched_blocks(self) -> int:
         """Blocks the last step's gathers copied (reuse mode; synchronises)."""
         return int(sum(int(n.sum().item()) for n in self.n_fetch[1:]))
 
-    def step(self, overlap: bool = True, t_ctx: int | None = None):
+    def step(self, overlap: bool = True, t_ctx: int | None = None, new_kv=None):
         """Enqueue one decode step over all layers on the current stream (and the side stream).
-        overlap=False runs each gather on the compute stream right before its attention.  t_ctx
-        moves the query to position t_ctx - 1 (the workspaces were sized for the first t_ctx and
-        the positions of one decode run stay within the same workspace needs)."""
+        overlap=False runs each gather (and write-back) on the compute stream right before (after)
+        its attention.  t_ctx moves the query to position t_ctx - 1 (the workspaces were sized for
+        the first t_ctx and the positions of one decode run stay within the same workspace needs).
+        new_kv[l] = (k_new, v_new), bf16 [B][Hkv][1][D] device: the decoded token's K/V of layer l
+        at position t_ctx - 1, appended as the class docstring describes; None leaves the caches
+        and host pools as they are (they must then already hold the token)."""
         if t_ctx is not None:
             self.t_ctx = t_ctx
+        p = self.t_ctx - 1
         comp = torch.cuda.current_stream()
+        if new_kv is not None:
+            self._append_layer0(new_kv[0][0], new_kv[0][1], p)
         self._select(self.f0_cur, 0)
         for l in range(self.L):
             if l + 1 < self.L:
@@ -155,6 +211,15 @@ class DecodePipeline:
                     comp.wait_event(self.ev_gather[l])
                 else:
                     self._gather(l, comp)
+                if new_kv is not None:
+                    (sk, sv), ssel, scnt = self._staging_of(l)
+                    sp.sparda_stage_append_kv(self.shape, new_kv[l][0], new_kv[l][1], p, ssel, scnt, sk, sv)
             self._attend(l)
             self.ev_attn[l].record(comp)
+            if l >= 1 and new_kv is not None:
+                if overlap:
+                    self.side.wait_event(self.ev_attn[l])
+                    self._writeback(l, new_kv[l][0], new_kv[l][1], p, self.side)
+                else:
+                    self._writeback(l, new_kv[l][0], new_kv[l][1], p, comp)
         return self.o

@@ -29,7 +29,7 @@ SPARDA_OP_INDEXER_KL = 4
 SPARDA_NOALLOC_SCRATCH_BYTES = 4718592  # the static scratch of sparda_sparse_attn_noalloc (include/sparda.h)
 
 EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select",
-            "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
+            "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks", "sparda_stage_append_kv", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
             "sparda_workspace_size", "sparda_status_string", "sparda_last_error_detail")
 
 
@@ -101,9 +101,11 @@ def load() -> ctypes.CDLL:
         lib.sparda_indexer_kl.argtypes = [S, P, P, P, P, i32, i64, ctypes.c_float, i32, P, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
         lib.sparda_writeback_kv.argtypes = [S, P, P, i32, i64, P, P, i32, P]
+        lib.sparda_stage_append_kv.argtypes = [S, P, P, i64, P, P, P, P, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
         for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max",
-                     "sparda_multihead_select", "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
+                     "sparda_multihead_select", "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks",
+                     "sparda_stage_append_kv", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
         lib.sparda_status_string.argtypes = [ctypes.c_int]
@@ -203,6 +205,12 @@ def sparda_gather_blocks(shape: SpardaShape, host_k, host_v, sel, cnt, stage_k, 
     cs = shape.c()
     _check(load().sparda_gather_blocks(ctypes.byref(cs), _p(host_k), _p(host_v), _p(sel), _p(cnt), _p(stage_k),
                                        _p(stage_v), n_workgroups, _stream(stream)), "sparda_gather_blocks")
+
+
+def sparda_stage_append_kv(shape: SpardaShape, k_new, v_new, q_pos: int, sel, cnt, stage_k, stage_v, stream=None):
+    cs = shape.c()
+    _check(load().sparda_stage_append_kv(ctypes.byref(cs), _p(k_new), _p(v_new), q_pos, _p(sel), _p(cnt), _p(stage_k),
+                                         _p(stage_v), _stream(stream)), "sparda_stage_append_kv")
 
 
 def sparda_writeback_kv(shape: SpardaShape, k_new, v_new, n_new: int, pos0: int, host_k, host_v, n_workgroups: int,

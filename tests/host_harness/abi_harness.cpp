@@ -160,6 +160,7 @@ void offloaded_pipeline() {
                SPARDA_OK);
       EXPECT(sparda_gather_blocks(&s, hk[(l - 1) % 2], hv[(l - 1) % 2], sel, cnt, stage_k, stage_v, 8, nullptr),
              SPARDA_OK);
+      EXPECT(sparda_stage_append_kv(&s, k_new, v_new, p, staged, scnt, stage_k, stage_v, nullptr), SPARDA_OK);
       EXPECT(sparda_sparse_attn(&s, q, 1, p, stage_k, stage_v, 1, staged, scnt, kScale, o,
                                 ws_a ? dev(ws_a) : nullptr, ws_a, nullptr),
              SPARDA_OK);
@@ -227,6 +228,9 @@ void argument_errors() {
   EXPECT(sparda_gather_blocks(&s, p, p, i16, i16, p, p, 0, nullptr), SPARDA_ERR_INVALID_ARG);
   EXPECT(sparda_writeback_kv(&s, p, p, 0, 0, p, p, 8, nullptr), SPARDA_ERR_INVALID_ARG);
   EXPECT(sparda_writeback_kv(&s, p, p, 2, 4095, p, p, 8, nullptr), SPARDA_ERR_INVALID_ARG);
+  EXPECT(sparda_stage_append_kv(&s, p, p, 4096, i16, i16, p, p, nullptr), SPARDA_ERR_INVALID_ARG);
+  EXPECT(sparda_stage_append_kv(&s, p, p, -1, i16, i16, p, p, nullptr), SPARDA_ERR_INVALID_ARG);
+  EXPECT(sparda_stage_append_kv(&s, p, nullptr, 10, i16, i16, p, p, nullptr), SPARDA_ERR_INVALID_ARG);
   EXPECT(sparda_plan_staging(&s, i16, i16, 4096, i16, i16, i16, i16, i16, reinterpret_cast<int32_t*>(p), nullptr),
          SPARDA_ERR_INVALID_ARG);
   float* fl = devp<float>(1 << 20);

@@ -202,6 +202,15 @@ def test_attention_noalloc_argument_errors(lib):
     assert worst == 510 * 16 * 130 * 4
 
 
+def test_stage_append_argument_errors(lib):
+    s = shape()
+    a = sp.sparda_stage_append_kv
+    assert rc_of(a, s, FAKE, FAKE, 4096, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG  # q_pos >= t_cap
+    assert rc_of(a, s, FAKE, FAKE, -1, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, s, FAKE, None, 10, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(a, shape(block_size=32), FAKE, FAKE, 10, FAKE, FAKE, FAKE, FAKE, 0) == sp.SPARDA_ERR_UNSUPPORTED
+
+
 def test_gather_argument_errors(lib):
     s = shape()
     g = sp.sparda_gather_blocks

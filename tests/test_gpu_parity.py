@@ -355,6 +355,47 @@ def test_gather_bitwise_and_host_checks(dev):
     exact.free()
 
 
+@pytest.mark.parametrize("K,p", [(16, 4095), (64, 3000), (100, 64 * 70)])
+def test_stage_append_bitwise(dev, K, p):
+    """The decoded token into the staged copy of its own block, bitwise against the oracle: rows
+    listing the block once, twice (k > 64: the second listing past entry 64), or not at all, and a
+    row whose count leaves it out; every other staged byte unchanged."""
+    say(f"stage append K{K} p{p}")
+    B, H, T = 3, 2, 8192
+    s, o = shapes(B, H, 4, K, T, T // 64)
+    rng = np.random.default_rng(K + p)
+    j = p // 64
+    sel = np.full((B, H, K), -1, np.int16)
+    cnt = np.zeros((B, H), np.int16)
+    for b in range(B):
+        for m in range(H):
+            n = int(rng.integers(1, K + 1))
+            blocks = rng.choice(j + 1, size=n, replace=n > j + 1).astype(np.int16)
+            case = (b * H + m) % 4
+            if case == 1:
+                blocks[int(rng.integers(n))] = j
+            elif case == 2 and n >= 2:
+                blocks[0] = j
+                blocks[n - 1] = j
+            elif case == 3:
+                blocks[blocks == j] = max(j - 1, 0)
+            sel[b, m, :n] = blocks
+            cnt[b, m] = n
+    sel[0, 0, :] = j  # every slot holds the block, but the count covers only the first three
+    cnt[0, 0] = 3
+    stage_k = rng.integers(0, 0x7F00, size=(B, H, K, 64, 128), dtype=np.uint16)
+    stage_v = rng.integers(0, 0x7F00, size=(B, H, K, 64, 128), dtype=np.uint16)
+    k_new = rng.integers(0, 0x7F00, size=(B, H, 128), dtype=np.uint16)
+    v_new = rng.integers(0, 0x7F00, size=(B, H, 128), dtype=np.uint16)
+    want_k, want_v = oracle.stage_append_kv(o, k_new, v_new, p, sel, cnt, stage_k, stage_v)
+    sk, sv = inputs.from_u16(stage_k, dev), inputs.from_u16(stage_v, dev)
+    sp.sparda_stage_append_kv(s, inputs.from_u16(k_new, dev), inputs.from_u16(v_new, dev), p,
+                              torch.from_numpy(sel).to(dev), torch.from_numpy(cnt).to(dev), sk, sv)
+    torch.cuda.synchronize()
+    assert np.array_equal(inputs.to_u16(sk), want_k) and np.array_equal(inputs.to_u16(sv), want_v)
+    assert not np.array_equal(want_k, stage_k)  # something was appended
+
+
 @pytest.mark.parametrize("n_new,pos0,nwg", [(1, 8191, 16), (1, 4000, 1), (300, 1000, 7), (64, 0, 64)])
 def test_writeback_bitwise_and_host_checks(dev, n_new, pos0, nwg):
     say(f"write-back n_new {n_new} pos0 {pos0} workgroups {nwg}")

@@ -719,6 +719,42 @@ def test_writeback_places_new_rows_and_touches_nothing_else(oracle_lib):
         oracle_lib.writeback_kv(s, new_k, new_v, 5, 636, pool_k, pool_v)
 
 
+def test_stage_append_completes_the_gather_of_the_appended_cache(oracle_lib):
+    """Alg. 2 appends the decoded token to the cache.  Gathering a cache that does not hold the
+    token yet and then appending the token to the staged copy of its block gives exactly the
+    gather of the cache that holds it; a slot listing the block twice gets it twice, other slots
+    keep their bytes, and a row whose set lacks the token's block is not written."""
+    B, H, K, T = 2, 3, 6, 640
+    s = shape_for(oracle_lib, B, H, 4, T, K)
+    p = 64 * 7 + 21
+    full_k = rnd_u16((B, H, T, 128), 91, 1)
+    full_v = rnd_u16((B, H, T, 128), 91, 2)
+    pool_k, pool_v = full_k.copy(), full_v.copy()
+    pool_k[:, :, p:] = 0x7FC0  # not written back yet: a NaN pattern
+    pool_v[:, :, p:] = 0x7FC0
+    sel = np.full((B, H, K), -1, np.int16)
+    cnt = np.zeros((B, H), np.int16)
+    sets = {(0, 0): [0, 3, 6, 7], (0, 1): [7, 1, 7], (0, 2): [2, 5], (1, 0): [0, 7], (1, 1): [7], (1, 2): [0, 4, 6, 7]}
+    for (b, m), blocks in sets.items():
+        sel[b, m, :len(blocks)] = blocks
+        cnt[b, m] = len(blocks)
+    stage_k, stage_v = oracle_lib.gather_blocks(s, pool_k, pool_v, sel, cnt)
+    sk, sv = oracle_lib.stage_append_kv(s, full_k[:, :, p], full_v[:, :, p], p, sel, cnt, stage_k, stage_v)
+    want_k, want_v = oracle_lib.gather_blocks(s, full_k, full_v, sel, cnt, stage_k.copy(), stage_v.copy())
+    for (b, m), blocks in sets.items():
+        for slot, j in enumerate(blocks):
+            if j == p // 64:  # the token's own block: equal to the appended cache up to p
+                assert np.array_equal(sk[b, m, slot, :p % 64 + 1], want_k[b, m, slot, :p % 64 + 1])
+                assert np.array_equal(sv[b, m, slot, :p % 64 + 1], want_v[b, m, slot, :p % 64 + 1])
+                assert np.all(sk[b, m, slot, p % 64 + 1:] == 0x7FC0)  # later rows untouched
+            else:
+                assert np.array_equal(sk[b, m, slot], stage_k[b, m, slot])
+                assert np.array_equal(sk[b, m, slot], want_k[b, m, slot])
+    assert np.array_equal(sk[0, 2], stage_k[0, 2]) and np.array_equal(sv[0, 2], stage_v[0, 2])  # no own block
+    with pytest.raises(oracle_lib.OracleError):
+        oracle_lib.stage_append_kv(s, full_k[:, :, 0], full_v[:, :, 0], T, sel, cnt, stage_k, stage_v)
+
+
 def test_plan_first_step_is_the_plain_gather_layout(oracle_lib):
     s = _plan_shape(oracle_lib)
     rng = np.random.default_rng(90)
