@@ -157,7 +157,66 @@ def time_events(fn, iters, stream):
     return float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
 
 
-def prefill_leg(dev, warmup, iters):
+class Flusher:
+    """Writes a 1 GiB scratch buffer between timed repetitions (untimed): four times the 256 MB
+    Infinity Cache and far beyond the eight 4 MB L2s, so each repetition starts from HBM."""
+
+    def __init__(self, dev):
+        self.buf = torch.empty((1 << 30) // 4, dtype=torch.float32, device=dev)
+        self.n = 0
+
+    def __call__(self):
+        self.n += 1
+        self.buf.fill_(float(self.n))
+
+
+def rep_stats(fn, reps, stream, flush=None):
+    """Per-launch HIP-event times of `reps` repetitions of fn() on `stream`, each after a cache
+    flush when `flush` is given: median, p10, p90 and mean in ms."""
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    for i in range(reps):
+        if flush is not None:
+            flush()
+        starts[i].record(stream)
+        fn()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
+    return {"reps": reps, "median_ms": float(np.median(t)), "p10_ms": float(np.percentile(t, 10)),
+            "p90_ms": float(np.percentile(t, 90)), "mean_ms": float(t.mean()), "cache_flushed": flush is not None}
+
+
+def decode_small_leg(dev, reps, flush):
+    """Decode at 4K (B1, k = 16) and 32K (B8, k = 64), 32 query / 8 KV heads: select + attention
+    per layer, each repetition after a 1 GiB cache flush (the 32K step's 143 MB would otherwise
+    stay in the Infinity Cache)."""
+    stream = torch.cuda.current_stream()
+    rows = []
+    for name in ("decode_b1_t4k", "decode_b8_t32k"):
+        w = inputs.WORKLOADS[name]
+        layer = DecodeLayer(w, dev)
+        for _ in range(5):
+            layer.step()
+        step = rep_stats(layer.step, reps, stream, flush)
+        sel = rep_stats(layer.select, reps, stream, flush)
+        att = rep_stats(layer.attend, reps, stream, flush)
+        parts = layer.bytes()
+        step_bytes = parts["select"] + parts["attend"]
+        rows.append({
+            "workload": f"decode layer B{w.batch} T={w.seq_len} Hq32/Hkv8 D128 block64 k{w.k_total}, select + sparse "
+                        "attention on precomputed K~",
+            "us_per_layer_median": step["median_ms"] * 1e3, "us_per_layer_p10": step["p10_ms"] * 1e3,
+            "us_per_layer_p90": step["p90_ms"] * 1e3, "GBps_median": step_bytes / (step["median_ms"] * 1e-3) / 1e9,
+            "frac_hbm_peak_median": step_bytes / (step["median_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "step_bytes": step_bytes, "select_us_median": sel["median_ms"] * 1e3,
+            "attend_us_median": att["median_ms"] * 1e3, "step_stats": step})
+        layer.case = None
+        del layer
+    return rows
+
+
+def prefill_leg(dev, warmup, iters, flush=None):
     w = inputs.WORKLOADS["prefill_b1_t32k"]
     T, nb = w.seq_len, w.n_blocks
     shape = sp.SpardaShape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size, k_total=w.k_total,
@@ -183,6 +242,7 @@ def prefill_leg(dev, warmup, iters):
     for _ in range(warmup):
         select()
     ms_sel = time_events(select, iters, stream)
+    sel_stats = rep_stats(select, max(50, iters), stream, flush)
     attend()
     ms_att = time_events(attend, max(2, iters // 10), stream)
 
@@ -235,7 +295,14 @@ def prefill_leg(dev, warmup, iters):
         "select_ms": ms_sel,
         "select_tflops": flops / (ms_sel * 1e-3) / 1e12,
         "select_frac_bf16_peak": flops / (ms_sel * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+        # two flop counts: the rows that must rank their candidates (the kernel skips rows whose
+        # candidates all fit the set), and every causal (row, candidate) pair
         "select_gflop": flops / 1e9,
+        "select_gflop_scored_rows": flops / 1e9,
+        "select_gflop_all_causal_pairs": score_flops / 1e9,
+        "select_tflops_all_causal_pairs": score_flops / (ms_sel * 1e-3) / 1e12,
+        "select_stats": sel_stats,
+        "select_tflops_median_flushed": flops / (sel_stats["median_ms"] * 1e-3) / 1e12,
         "attn_ms": ms_att,
         "attn_tflops": attn_flops / (ms_att * 1e-3) / 1e12,
         "select_grid_32_16_ms": ms_sel_g,
@@ -409,7 +476,7 @@ def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
     kc = np.stack([inputs.to_u16(layer.kc[b, m]) for b, m in pairs])[:, None].copy()
     oshape = oracle.Shape(batch=n_rows, n_kv_heads=1, group_size=G, k_total=w.k_total, t_cap=T, nc_cap=nb,
                           n_init=w.n_init, n_local=w.n_local)
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle.set_threads(0)  # the OpenMP threads the oracle's loops use
     reps = 0
     t0 = time.perf_counter()
     while True:  # repeat the sample until about min_seconds of CPU work
@@ -425,7 +492,54 @@ def cpu_baseline(layer: DecodeLayer, n_rows: int, min_seconds: float = 10.0):
     return {"value": sample_bytes / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{n_rows} of {rows_total} (batch, group) rows of the 128K decode step "
                       f"(select + attend), {dt:.3f}s per pass, {reps} passes",
-            "us_per_layer_equiv": dt * rows_total / n_rows * 1e6}
+            "us_per_layer_equiv": dt * rows_total / n_rows * 1e6,
+            "host": host_info(), "threads": threads, "small_workloads": oracle_small_workloads(threads)}
+
+
+def host_info():
+    """nproc and the lscpu topology of this host."""
+    info = {"nproc": os.cpu_count()}
+    try:
+        import subprocess
+        text = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        keys = {"Socket(s)": "sockets", "Core(s) per socket": "cores_per_socket", "Thread(s) per core": "threads_per_core",
+                "Model name": "model"}
+        for line in text.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in keys:
+                v = v.strip()
+                info[keys[k.strip()]] = int(v) if v.isdigit() else v
+    except (OSError, ValueError):
+        pass
+    return info
+
+
+def oracle_small_workloads(threads):
+    """The oracle's select + attend over every row of the 4K (B1) and 32K (B8) decode workloads,
+    on one thread and on `threads`, median of 3 runs each (seconds per decode layer)."""
+    import oracle
+    out = {}
+    for name in ("decode_b1_t4k", "decode_b8_t32k"):
+        w = inputs.WORKLOADS[name]
+        case = inputs.make_case(w)
+        T, nb = w.seq_len, w.n_blocks
+        o = oracle.Shape(batch=w.batch, n_kv_heads=w.n_kv_heads, group_size=w.group_size, k_total=w.k_total, t_cap=T,
+                         nc_cap=nb, n_init=w.n_init, n_local=w.n_local)
+        q, f, k, v = (inputs.to_u16(case[n]) for n in ("q", "f", "k", "v"))
+        kc = oracle.compress_keys(o, k, T, 0, nb)
+        res = {}
+        for nt in (1, threads):
+            oracle.set_threads(nt)
+            times = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                sel, cnt = oracle.forecast_select(o, f, 1, T - 1, kc)
+                oracle.sparse_attn(o, q, 1, T - 1, k, v, 0, sel, cnt, SCALE)
+                times.append(time.perf_counter() - t0)
+            res[f"s_per_layer_{nt}_threads"] = float(np.median(times))
+        out[name] = res
+    oracle.set_threads(threads)
+    return out
 
 
 def pipeline_leg(dev, steps):
@@ -675,6 +789,7 @@ def main():
     ap.add_argument("--no-paper-config", action="store_true",
                     help="skip the decode and prefill at the paper's model configuration")
     ap.add_argument("--cpu-rows", type=int, default=32)
+    ap.add_argument("--reps", type=int, default=60, help="repetitions of each flushed per-call timing (>= 50)")
     ap.add_argument("--calib-copy", action="store_true", help="run a plain 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -730,6 +845,13 @@ def main():
     ms_sel = time_events(layer.select, args.steps, stream)
     ms_att = time_events(layer.attend, args.steps, stream)
     ms_cmp = time_events(layer.compress_new, args.steps, stream)
+    # the same calls one at a time after a 1 GiB cache flush: median, p10 and p90
+    flush = Flusher(dev)
+    step_stats = {"step": rep_stats(layer.step, args.reps, stream, flush),
+                  "select": rep_stats(layer.select, args.reps, stream, flush),
+                  "attend": rep_stats(layer.attend, args.reps, stream, flush)}
+    log(f"[bench] decode step after a cache flush: median {step_stats['step']['median_ms'] * 1e3:.1f} us "
+        f"(p10 {step_stats['step']['p10_ms'] * 1e3:.1f}, p90 {step_stats['step']['p90_ms'] * 1e3:.1f})")
     att_bytes = parts["attend"]
     achieved = att_bytes / (ms_att * 1e-3) / 1e9
     out = {
@@ -761,7 +883,14 @@ def main():
                      "frac_measured_peak": achieved / peaks["hbm_block_read_GBps"]},
         "peaks": peaks,
         "frac_measured_read_peak": step_bytes / (ms_step * 1e-3) / 1e9 / peaks["hbm_block_read_GBps"],
+        "flushed_stats": step_stats,
+        "us_per_layer_median_flushed": step_stats["step"]["median_ms"] * 1e3,
+        "GBps_median_flushed": step_bytes / (step_stats["step"]["median_ms"] * 1e-3) / 1e9,
     }
+    out["decode_small"] = decode_small_leg(dev, args.reps, flush)
+    for r in out["decode_small"]:
+        log(f"[bench] {r['workload'][:32]}: {r['us_per_layer_median']:.1f} us per layer (median after a flush, "
+            f"p10 {r['us_per_layer_p10']:.1f}, p90 {r['us_per_layer_p90']:.1f}), {r['GBps_median']:.0f} GB/s")
     if not args.no_grid:
         out["paper_grid"] = grid_leg(layer, dev, args.warmup, args.steps, stream)
         log(f"[bench] (32, 16) grid decode step {out['paper_grid']['us_per_layer']:.1f} us, "
@@ -784,7 +913,7 @@ def main():
             f"{out['indexer_training']['target_tflops']:.1f} TFLOP/s on the target scores")
     if not args.no_prefill:
         layer.case = None
-        out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2))
+        out["prefill"] = prefill_leg(dev, args.warmup, max(10, args.steps // 2), flush)
         out["prefill"]["select_frac_measured_mfma_peak"] = out["prefill"]["select_tflops"] / peaks["mfma_bf16_TFLOPs"]
         # against the rate of the 16x16x32 instruction the select kernel's layout needs
         out["prefill"]["select_frac_measured_16x16x32_rate"] = (out["prefill"]["select_tflops"]

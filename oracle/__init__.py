@@ -100,6 +100,8 @@ def open_library(path: str):
     lib.sparda_ref_bf16_to_f64.restype = f64
     lib.sparda_ref_f64_to_bf16.argtypes = [f64]
     lib.sparda_ref_f64_to_bf16.restype = ctypes.c_uint16
+    lib.sparda_ref_set_threads.argtypes = [ctypes.c_int]
+    lib.sparda_ref_set_threads.restype = ctypes.c_int
     lib.sparda_ref_compress_keys.argtypes = [S, P, i64, i32, i32, P]
     lib.sparda_ref_select_row.argtypes = [S, P, i32, i64, P, i32, i32, i32, P, P, P, P]
     lib.sparda_ref_forecast_select.argtypes = [S, P, i32, i64, P, P, P]
@@ -186,6 +188,11 @@ def _u16(a: np.ndarray) -> np.ndarray:
     if a.dtype != np.uint16:
         raise TypeError("bf16 tensors are passed as uint16 bit patterns")
     return a
+
+
+def set_threads(n: int) -> int:
+    """Threads of the oracle's OpenMP loops (n < 1 only reports); returns the count in effect."""
+    return int(_load().sparda_ref_set_threads(int(n)))
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -53,6 +53,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define REF_OK 0
 #define REF_ERR_INVALID_ARG (-1)
@@ -70,6 +73,18 @@ typedef struct {
   int32_t n_init, n_local, k_total;
   int64_t t_cap, nc_cap;
 } ref_shape;
+
+/* Threads of the OpenMP loops over independent rows (the CPU baseline times the oracle on one
+ * thread and on every host core).  Returns the count in effect; n < 1 leaves it unchanged. */
+int sparda_ref_set_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
+}
 
 /* ---- bf16 <-> float64 ------------------------------------------------------------------ */
 
