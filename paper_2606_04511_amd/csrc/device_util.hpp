@@ -183,6 +183,18 @@ __device__ __forceinline__ uint4 ld16_nt(const void* p) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+// z with P(Z > z) = p for a standard normal Z (rational approximation of Abramowitz and Stegun
+// 26.2.23, |error| < 4.5e-4).  Only a first guess for the exact searches that use it.
+__device__ __forceinline__ float upper_normal_quantile(float p) {
+  p = fminf(fmaxf(p, 1e-7f), 1.f - 1e-7f);
+  const bool upper = p <= 0.5f;
+  const float q = upper ? p : 1.f - p;
+  const float t = __builtin_amdgcn_sqrtf(-1.3862944f * __builtin_amdgcn_logf(q));  // -2 ln q
+  const float z = t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
+                          (1.f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
+  return upper ? z : -z;
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
 
 __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {

@@ -18,14 +18,23 @@ __device__ __forceinline__ void emit_forced(int16_t* out, const RowGeom& g, int 
 }
 
 
-// Block-wide exclusive rank of `flag` in thread order within one pass over kDecThreads items,
-// plus the pass total.  wave_cnt: kDecThreads/64 ints of LDS.  Contains two barriers.
-__device__ __forceinline__ int block_rank(bool flag, int* wave_cnt, int* total) {
+// Block-wide count of flagged items before each thread's first item, where thread t holds the
+// P consecutive items P t .. P t + P - 1 in order, plus the total.  Ballots and mbcnt inside the
+// wavefront, one LDS exchange of the wavefront totals (wave_cnt: kDecThreads/64 ints).  Contains
+// two barriers (the second lets the next call reuse wave_cnt).
+template <int P>
+__device__ __forceinline__ int block_flag_prefix(const bool (&f)[P], int* wave_cnt, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint64_t b = __ballot(flag);
-  if (lane == 0) wave_cnt[wave] = __popcll(b);
+  int in_wave = 0, before = 0;
+#pragma unroll
+  for (int e = 0; e < P; ++e) {
+    const uint64_t b = __ballot(f[e]);
+    in_wave += (int)__popcll(b);
+    before += mbcnt64(b);
+  }
+  if (lane == 0) wave_cnt[wave] = in_wave;
   __syncthreads();
-  int before = 0, all = 0;
+  int all = 0;
 #pragma unroll
   for (int w = 0; w < kDecThreads / 64; ++w) {
     const int c = wave_cnt[w];
@@ -34,7 +43,7 @@ __device__ __forceinline__ int block_rank(bool flag, int* wave_cnt, int* total) 
   }
   __syncthreads();
   *total = all;
-  return before + mbcnt64(b);
+  return before;
 }
 
 // The whole workgroup selects the n_take largest of the C block scores bs[0 .. C) (ties: lower
@@ -88,24 +97,44 @@ __device__ __forceinline__ void block_topk_emit(const float* bs, int C, int n_ta
   }
 
   // Emit in ascending candidate order; equal keys at the threshold go to the lowest indices.
+  // Thread t takes candidates 4 t .. 4 t + 3 of each run of 4 kDecThreads, so thread order is
+  // candidate order and one flag prefix per run places them (two in the tie case).
+  constexpr int kPer = 4;
   int base = 0, tie_base = 0;
-  for (int i0 = 0; i0 < C; i0 += kDecThreads) {
-    const int i = i0 + tid;
-    const bool valid = i < C;
-    const uint32_t kk = valid ? score_key(bs[i]) : 0u;
-    bool chosen;
+  for (int c0 = 0; c0 < C; c0 += kPer * kDecThreads) {
+    uint32_t kk[kPer];
+    bool valid[kPer], ch[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+      const int i = c0 + kPer * tid + e;
+      valid[e] = i < C;
+      kk[e] = score_key(bs[min(i, C - 1)]);  // in bounds for every thread
+    }
     if (take_all) {
-      chosen = valid && (kk & mask) >= prefix;
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) ch[e] = valid[e] && (kk[e] & mask) >= prefix;
     } else {
-      const bool tie = valid && kk == prefix;
+      bool tie[kPer];
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) tie[e] = valid[e] && kk[e] == prefix;
       int n_ties;
-      const int trank = tie_base + block_rank(tie, wave_cnt, &n_ties);
+      int trank = tie_base + block_flag_prefix(tie, wave_cnt, &n_ties);
       tie_base += n_ties;
-      chosen = valid && (kk > prefix || (tie && trank < remaining));
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        ch[e] = valid[e] && (kk[e] > prefix || (tie[e] && trank < remaining));
+        trank += tie[e] ? 1 : 0;
+      }
     }
     int n_chosen;
-    const int pos = base + block_rank(chosen, wave_cnt, &n_chosen);
-    if (chosen && pos < n_take) chosen_out[pos] = (int16_t)(cand_lo + i);
+    int pos = base + block_flag_prefix(ch, wave_cnt, &n_chosen);
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+      if (ch[e]) {
+        if (pos < n_take) chosen_out[pos] = (int16_t)(cand_lo + c0 + kPer * tid + e);  // never past the row's slots
+        ++pos;
+      }
+    }
     base += n_chosen;
   }
 }

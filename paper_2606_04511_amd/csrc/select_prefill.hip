@@ -96,18 +96,6 @@ __device__ __forceinline__ int row4_excl_scan(int x, int j, int* total) {
   return ((j & 1) ? (int)p[0] : 0) + ((j & 2) ? (int)q[0] : 0);
 }
 
-// z with P(Z > z) = p for a standard normal Z (rational approximation of Abramowitz and Stegun
-// 26.2.23, |error| < 4.5e-4).  Only a first guess; the search is exact regardless.
-__device__ __forceinline__ float upper_normal_quantile(float p) {
-  p = fminf(fmaxf(p, 1e-7f), 1.f - 1e-7f);
-  const bool upper = p <= 0.5f;
-  const float q = upper ? p : 1.f - p;
-  const float t = __builtin_amdgcn_sqrtf(-1.3862944f * __builtin_amdgcn_logf(q));  // -2 ln q
-  const float z = t - (2.515517f + t * (0.802853f + t * 0.010328f)) /
-                          (1.f + t * (1.432788f + t * (0.189269f + t * 0.001308f)));
-  return upper ? z : -z;
-}
-
 __device__ __forceinline__ uint32_t key_of_value(float v) {
   // score_key without the -0 branch: v + 0 turns -0 into +0 in round-to-nearest.
   const uint32_t u = __float_as_uint(v + 0.0f);

@@ -116,6 +116,7 @@ DECODE_SELECT = [
     (1, 2, 4, 131072, 64, 1, 2),
     (2, 2, 4, 20000, 40, 0, 3),
     (1, 2, 16, 50000, 96, 1, 32),
+    (1, 2, 4, 600000, 64, 1, 2),  # 9372 candidates: 5 chunks of the workgroup top-k
 ]
 
 
@@ -723,6 +724,37 @@ def test_select_exact_ties_take_lowest_index(dev, T, n_q, k_total):
     kc = torch.randint(-1, 2, (B, H, nb, 128), generator=g).to(torch.bfloat16)
     m3 = nb // 3
     kc[:, :, 0:3 * m3:3] = kc[:, :, 1:3 * m3:3]  # duplicated K~ rows: exact score ties
+    q_pos0 = T - n_q
+    sel, cnt = gpu_select(s, f.to(dev), n_q, q_pos0, kc.to(dev), dev)
+    ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(sel.cpu().numpy(), ref_sel)
+
+
+@pytest.mark.parametrize("B,T,n_q,k_total,zero", [
+    (1, 8192, 4096, 16, True), (1, 20000, 3000, 100, True), (1, 16384, 4096, 16, False),
+    # decode rows: one workgroup per row over 2048-candidate chunks (1 chunk at 128K, 4 at 400K,
+    # 8 at 1M), fused (>= 256 rows) and split (fewer rows) paths
+    (1, 131072, 1, 64, True), (1, 131072, 1, 64, False), (1, 400000, 1, 64, False), (1, 1048000, 1, 96, True),
+    (128, 131072, 1, 64, False), (128, 400000, 1, 64, True), (128, 400000, 1, 64, False)])
+def test_select_flat_and_clustered_scores(dev, B, T, n_q, k_total, zero):
+    """Score distributions far from the normal model the selection's first threshold guess is
+    drawn from: F = 0 (every score of a row is 0: every row takes its lowest candidates), and
+    K~ built from 3 distinct rows (each row's scores take 3 values with many ties, so brackets
+    collapse onto single values).  Sets must equal the oracle's exactly."""
+    say(f"flat/clustered B{B} T{T} n_q{n_q} k{k_total} zero {zero}")
+    H = 2
+    nb = T // 64
+    t_cap = -(-T // 64) * 64
+    s, o = shapes(B, H, 4, k_total, t_cap, nb)
+    g = torch.Generator().manual_seed(T + 7 + B)
+    f = torch.randn((B, H, n_q, 128), generator=g).to(torch.bfloat16)
+    if zero:
+        f.zero_()
+        kc = torch.randn((B, H, nb, 128), generator=g).to(torch.bfloat16)
+    else:
+        kc = torch.randn((1, 1, 3, 128), generator=g).to(torch.bfloat16)
+        kc = kc[:, :, torch.randint(0, 3, (nb,), generator=g)].expand(B, H, nb, 128).contiguous()
     q_pos0 = T - n_q
     sel, cnt = gpu_select(s, f.to(dev), n_q, q_pos0, kc.to(dev), dev)
     ref_sel, ref_cnt = oracle.forecast_select(o, inputs.to_u16(f), n_q, q_pos0, inputs.to_u16(kc))
