@@ -216,6 +216,71 @@ def decode_small_leg(dev, reps, flush):
     return rows
 
 
+def overlap_leg(layer: "DecodeLayer", dev, n_layers=32, reps=5):
+    """Alg. 2's order of a decode step over n_layers layers of the 128K B32 shape (each layer
+    re-using the one layer's buffers): layer l+1's selection runs on a second stream of the same
+    priority while layer l attends, two (sel, cnt) sets alternating between layers and events
+    ordering each attention after its selection and each selection after the attention that
+    last read its set.  Reported beside the same layers run serially on one stream.  Streams
+    map onto a few hardware queues, so a second stream can land on the compute stream's queue
+    and serialise with it: four side streams are tried and each one's time is reported."""
+    main = torch.cuda.current_stream()
+    sets = [(layer.sel, layer.cnt), (torch.empty_like(layer.sel), torch.empty_like(layer.cnt))]
+    ws = [layer.ws_sel, torch.empty_like(layer.ws_sel)]
+
+    def select(i, stream):
+        with torch.cuda.stream(stream):
+            sp.sparda_forecast_select(layer.shape, layer.f, 1, layer.T - 1, layer.kc, sets[i][0], sets[i][1], ws[i])
+
+    def attend(i):
+        sp.sparda_sparse_attn(layer.shape, layer.q, 1, layer.T - 1, layer.k, layer.v, 0, sets[i][0], sets[i][1],
+                              SCALE, layer.o, layer.ws_att)
+
+    def serial():
+        for l in range(n_layers):
+            select(l % 2, main)
+            attend(l % 2)
+
+    def overlapped(side):
+        ev_sel = [torch.cuda.Event(), torch.cuda.Event()]
+        ev_att = [torch.cuda.Event(), torch.cuda.Event()]
+        start = torch.cuda.Event()
+        start.record(main)
+        side.wait_event(start)
+        select(0, main)
+        ev_sel[0].record(main)
+        for l in range(n_layers):
+            cur, nxt = l % 2, 1 - l % 2
+            if l + 1 < n_layers:
+                if l >= 1:
+                    side.wait_event(ev_att[nxt])  # attention l-1 read set nxt
+                select(nxt, side)
+                ev_sel[nxt].record(side)
+            main.wait_event(ev_sel[cur])
+            attend(cur)
+            ev_att[cur].record(main)
+        main.wait_event(ev_sel[(n_layers - 1) % 2])
+
+    def wall(fn):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / n_layers
+
+    serial()
+    ser = float(np.median([wall(serial) for _ in range(reps)]))
+    per_side = []
+    for _ in range(4):
+        side = torch.cuda.Stream(device=dev)
+        overlapped(side)
+        per_side.append(float(np.median([wall(lambda: overlapped(side)) for _ in range(reps)])))
+    best = min(per_side)
+    return {"layers": n_layers, "us_per_layer_serial": ser * 1e3, "us_per_layer_overlapped": best * 1e3,
+            "us_per_layer_overlapped_per_side_stream": [x * 1e3 for x in per_side],
+            "overlap_gain": ser / best}
+
+
 def prefill_leg(dev, warmup, iters, flush=None):
     w = inputs.WORKLOADS["prefill_b1_t32k"]
     T, nb = w.seq_len, w.n_blocks
@@ -887,6 +952,9 @@ def main():
         "us_per_layer_median_flushed": step_stats["step"]["median_ms"] * 1e3,
         "GBps_median_flushed": step_bytes / (step_stats["step"]["median_ms"] * 1e-3) / 1e9,
     }
+    out["decode_overlap"] = overlap_leg(layer, dev)
+    log(f"[bench] decode layers with select(l+1) beside attention(l): {out['decode_overlap']['us_per_layer_overlapped']:.1f} "
+        f"us per layer (serial {out['decode_overlap']['us_per_layer_serial']:.1f})")
     out["decode_small"] = decode_small_leg(dev, args.reps, flush)
     for r in out["decode_small"]:
         log(f"[bench] {r['workload'][:32]}: {r['us_per_layer_median']:.1f} us per layer (median after a flush, "
