@@ -2,16 +2,18 @@
 // prefill): paper Sec. 4.1, Eq. 5, over the per-row attended sets of Eq. 1 (Alg. 1 selects per
 // query token, so neighbouring rows attend different blocks).
 //
-// Work unit: a tile of 256/G consecutive query rows of one (batch, group), i.e. 256 query-head
-// rows, on one 512-thread workgroup.  Wavefront w owns query-head rows [32 w, 32 w + 32): two
-// MFMA N-tiles of 16 query-heads (16/G rows each), whose online-softmax state and output
-// accumulators stay in registers for the whole tile.
+// Work unit: a tile of 128/G consecutive query rows of one (batch, group), i.e. 128 query-head
+// rows, on one 256-thread workgroup; two workgroups share a CU, so a block's barrier waits for 4
+// wavefronts while the other workgroup's wavefronts keep the SIMDs busy.  Wavefront w owns
+// query-head rows [32 w, 32 w + 32): two MFMA N-tiles of 16 query-heads (16/G rows each), whose
+// online-softmax state and output accumulators stay in registers for the whole tile.
 //   1. Each row's attended blocks become a bitmap in LDS (entries outside [0, blk(p)] are
 //      dropped; a block listed twice sets one bit, so it is attended once).  Their union, in
-//      ascending order, is the tile's block list.
+//      ascending order, is the tile's block list.  The bitmaps and the list are dynamic LDS
+//      sized by the call's last row.
 //   2. The tile walks its block list.  Block j's 16 KiB of K and 16 KiB of V are read from HBM
-//      once per tile (16-byte loads, 1 KiB contiguous per wavefront instruction) into a
-//      double-buffered LDS stage, two blocks ahead of the math.  K rows keep their 16-byte pieces
+//      once per tile (16-byte loads, 1 KiB contiguous per wavefront instruction; every thread
+//      loads four pieces of each) into a double-buffered LDS stage, one block ahead of the math.  K rows keep their 16-byte pieces
 //      XOR-swizzled by the row; V is stored transposed (head dim x token, XOR-swizzled as well) so
 //      that it can be the A operand of P V.  Both swizzles make the operand reads conflict-free
 //      whether LDS serves 16 lanes of a 16-byte read from 64 banks or 32 lanes from 128.
@@ -32,13 +34,17 @@
 
 namespace sparda {
 
+// The prefill attention's dynamic LDS (row bitmaps, union bitmap, union list).
+extern __shared__ __align__(16) uint32_t pa_dyn[];
+
 namespace {
 
-constexpr int kPaThreads = 512;
-constexpr int kPaQh = 256;                 // query-head rows per tile
+constexpr int kPaThreads = 256;            // 4 wavefronts; two workgroups share a CU
+constexpr int kPaQh = 128;                 // query-head rows per tile
 constexpr int kPaKLd = kHeadDim;           // bf16 per staged K row; piece x of row r sits at x ^ (r % 16)
-constexpr int kPaMaxWords = 8192;          // row-bitmap words (32 KiB)
 constexpr int kPaMaxBlocks = 4096;         // causal blocks a tile may span
+constexpr int kPaStaticLds = 2 * 2 * kBlock * kHeadDim * 2 + 16;  // the K and V^T double buffers, n_union
+constexpr int kPaLdsMax = 160 * 1024;      // LDS of one CU
 constexpr float kLog2eP = 1.4426950408889634f;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -49,17 +55,24 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
+// Row bitmaps, union bitmap and union list live in dynamic LDS sized by the call (its last row's
+// causal blocks): wc words per row bitmap.
+__host__ __device__ inline int pa_dyn_lds_bytes(int rows, int nbt) {
+  const int wc = (nbt + 31) >> 5;
+  return ((4 * (rows * wc + wc) + 2 * nbt) + 15) & ~15;
+}
+
 template <int G>
-__global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, int n_tiles, int n_groups) {
+__global__ __launch_bounds__(kPaThreads, 2) void prefill_attn_kernel(AttnArgs a, int n_tiles, int n_groups, int wc) {
   constexpr int TR = kPaQh / G;  // rows per tile
   constexpr int RN = 16 / G;     // rows per N-tile
   static_assert(16 % G == 0, "an N-tile holds whole rows");
   __shared__ __align__(16) uint16_t kst[2][kBlock * kPaKLd];
   __shared__ __align__(16) uint16_t vst[2][kHeadDim * kBlock];
-  __shared__ uint32_t rbm[kPaMaxWords];
-  __shared__ uint32_t ubm[kPaMaxBlocks / 32];
-  __shared__ int16_t ulist[kPaMaxBlocks];
   __shared__ int n_union;
+  uint32_t* rbm = pa_dyn;                                   // [TR][wc] (a tile uses [nrows][W])
+  uint32_t* ubm = pa_dyn + TR * wc;                         // [wc]
+  int16_t* ulist = reinterpret_cast<int16_t*>(ubm + wc);    // [wc * 32] >= nbt
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
@@ -151,11 +164,11 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
 #pragma unroll
     for (int md = 0; md < 8; ++md) acc[nt][md] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // ---- staging roles.  Threads 0..255 copy K: token u/16, 16-byte part u%16 for u = lt + 256 x.
-  // Threads 256..511 copy V: tokens tau + 16 x (x = 0..3), dims 8 part .. 8 part + 7, with lane l
-  // of V wavefront w taking tau = 4 w + l % 4, part = l / 4 (each wavefront load instruction still
-  // covers 4 whole token rows, 1 KiB contiguous).  Two register sets keep the loads of the next
-  // two blocks in flight.
+  // ---- staging roles.  Every thread copies four 16-byte pieces of K and four of V per block.
+  // K: token u/16, 16-byte part u%16 for u = tid + 256 x.  V: tokens tau + 16 x (x = 0..3), dims
+  // 8 part .. 8 part + 7, with lane l of wavefront w taking tau = 4 w + l % 4, part = l / 4 (each
+  // wavefront load instruction covers 4 whole token rows, 1 KiB contiguous).  One register set
+  // holds the next block's loads while the current block is computed.
   //
   // Staged V^T: row d (head dim) holds the block's 64 tokens in slots 4 tau + x <-> token
   // tau + 16 x, 32 dwords per row; dword w of row d sits at w ^ vsw(d).  An operand read takes
@@ -164,44 +177,41 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
   // wavefront 128 of 128.  Its high bits (from dim bits 4, 5, constant over one read) spread the
   // transposing writes (once per block) to two lanes per bank, the least that 32 lanes of 8-byte
   // writes into one bank half can take.
-  const int lt = tid & 255;
-  const bool load_k = __builtin_amdgcn_readfirstlane(tid) < 256;  // whole wavefronts
-  const int v_tau = 4 * (lt >> 6) + (lt & 3), v_part = (lt & 63) >> 2;
-  const int ld_off = load_k ? lt * 8 : v_tau * kHeadDim + 8 * v_part;
-  const uint16_t* kv = (load_k ? a.k : a.v) + bm * a.t_cap * kHeadDim + ld_off;
+  const int v_tau = 4 * (tid >> 6) + (tid & 3), v_part = (tid & 63) >> 2;
+  const uint16_t* kp = a.k + bm * a.t_cap * kHeadDim + tid * 8;
+  const uint16_t* vp = a.v + bm * a.t_cap * kHeadDim + v_tau * kHeadDim + 8 * v_part;
   auto vsw = [](int d) { return 2 * ((((d >> 2) & 3) | (((d >> 1) & 1) << 3)) ^ (((d >> 4) & 3) << 2)); };
-  uint4 pre[2][4];
-  auto issue = [&](uint4 (&r)[4], int j) {
-    const uint16_t* src = kv + (int64_t)j * kBlock * kHeadDim;
+  uint4 pre[8];  // K pieces 0..3, V pieces 4..7
+  auto issue = [&](int j) {
+    const int64_t off = (int64_t)j * kBlock * kHeadDim;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) r[x] = ld16(src + x * 16 * kHeadDim);
+    for (int x = 0; x < 4; ++x) pre[x] = ld16(kp + off + x * 16 * kHeadDim);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) pre[4 + x] = ld16(vp + off + x * 16 * kHeadDim);
   };
-  auto stage = [&](const uint4 (&r)[4], int buf) {
-    if (load_k) {
+  auto stage = [&](int buf) {
 #pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const int u = lt + 256 * x;
-        *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (((u & 15) ^ ((u >> 4) & 15)) * 8)]) = r[x];
-      }
-    } else {
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&r[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&r[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&r[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&r[3]);
+    for (int x = 0; x < 4; ++x) {
+      const int u = tid + 256 * x;
+      *reinterpret_cast<uint4*>(&kst[buf][(u >> 4) * kPaKLd + (((u & 15) ^ ((u >> 4) & 15)) * 8)]) = pre[x];
+    }
+    const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&pre[4]);
+    const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&pre[5]);
+    const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&pre[6]);
+    const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&pre[7]);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int wi = i >> 1;
-        uint2 d;
-        if (i & 1) {
-          d.x = (w0[wi] >> 16) | (w1[wi] & 0xffff0000u);
-          d.y = (w2[wi] >> 16) | (w3[wi] & 0xffff0000u);
-        } else {
-          d.x = (w0[wi] & 0xffffu) | (w1[wi] << 16);
-          d.y = (w2[wi] & 0xffffu) | (w3[wi] << 16);
-        }
-        const int dim = 8 * v_part + i;
-        *reinterpret_cast<uint2*>(&vst[buf][2 * (dim * 32 + ((2 * v_tau) ^ vsw(dim)))]) = d;
+    for (int i = 0; i < 8; ++i) {
+      const int wi = i >> 1;
+      uint2 d;
+      if (i & 1) {
+        d.x = (w0[wi] >> 16) | (w1[wi] & 0xffff0000u);
+        d.y = (w2[wi] >> 16) | (w3[wi] & 0xffff0000u);
+      } else {
+        d.x = (w0[wi] & 0xffffu) | (w1[wi] << 16);
+        d.y = (w2[wi] & 0xffffu) | (w3[wi] << 16);
       }
+      const int dim = 8 * v_part + i;
+      *reinterpret_cast<uint2*>(&vst[buf][2 * (dim * 32 + ((2 * v_tau) ^ vsw(dim)))]) = d;
     }
   };
 
@@ -335,22 +345,17 @@ __global__ __launch_bounds__(kPaThreads) void prefill_attn_kernel(AttnArgs a, in
   // flight and the compiler's waits only ever cover the block being staged.
   auto blk_at = [&](int i) { return (int)ulist[min(i, max(nu - 1, 0))]; };
   if (nu > 0) {
-    issue(pre[0], blk_at(0));
-    issue(pre[1], blk_at(1));
-    stage(pre[0], 0);
+    issue(blk_at(0));
+    stage(0);
   }
   __syncthreads();
 
-  // Iteration it computes block it from buffer it % 2, requests block it + 2 into the register
-  // set block it used, and stages block it + 1 (requested one iteration earlier).
-  for (int it = 0; it < nu; it += 2) {
-    issue(pre[0], blk_at(it + 2));
-    compute(blk_at(it), 0);
-    stage(pre[1], 1);
-    __syncthreads();
-    issue(pre[1], blk_at(it + 3));
-    if (it + 1 < nu) compute(blk_at(it + 1), 1);
-    stage(pre[0], 0);
+  // Iteration it requests block it + 1, computes block it from buffer it % 2 meanwhile, then
+  // stages block it + 1 into the other buffer.
+  for (int it = 0; it < nu; ++it) {
+    issue(blk_at(it + 1));
+    compute(blk_at(it), it & 1);
+    stage((it + 1) & 1);
     __syncthreads();
   }
 
@@ -379,8 +384,9 @@ hipError_t launch_tiles(const AttnArgs& a, hipStream_t stream) {
   const int tr = kPaQh / G;
   const int n_tiles = (a.n_q + tr - 1) / tr;
   const int n_groups = a.batch * a.n_kv_heads;
-  hipLaunchKernelGGL(prefill_attn_kernel<G>, dim3((unsigned)((int64_t)n_groups * n_tiles)), dim3(kPaThreads), 0,
-                     stream, a, n_tiles, n_groups);
+  const int nbt = (int)((a.q_pos0 + a.n_q - 1) / kBlock) + 1;  // causal blocks of the call's last row
+  hipLaunchKernelGGL(prefill_attn_kernel<G>, dim3((unsigned)((int64_t)n_groups * n_tiles)), dim3(kPaThreads),
+                     pa_dyn_lds_bytes(tr, nbt), stream, a, n_tiles, n_groups, (nbt + 31) >> 5);
   return hipGetLastError();
 }
 
@@ -389,11 +395,10 @@ hipError_t launch_tiles(const AttnArgs& a, hipStream_t stream) {
 bool attn_uses_tiles(int32_t group_size, int32_t n_q, int64_t q_pos0) {
   if (n_q < 16 || group_size < 1 || group_size > 16 || 16 % group_size != 0) return false;
   const int64_t tr = kPaQh / group_size;
-  // the widest tile: its last row decides the bitmap width
-  const int64_t rows = n_q < tr ? n_q : tr;
+  // the call's last row decides the bitmap width; two workgroups share a CU while the dynamic
+  // part stays within 16 KiB (contexts up to about 190K tokens at G = 4), one beyond
   const int64_t nbt = (q_pos0 + n_q - 1) / kBlock + 1;
-  const int64_t words = (nbt + 31) / 32;
-  return nbt <= kPaMaxBlocks && rows * words <= kPaMaxWords;
+  return nbt <= kPaMaxBlocks && kPaStaticLds + pa_dyn_lds_bytes((int)tr, (int)nbt) <= kPaLdsMax;
 }
 
 hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream) {
