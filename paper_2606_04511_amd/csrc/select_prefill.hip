@@ -223,6 +223,215 @@ __device__ __forceinline__ void copy_out(const SelectArgs& a, int64_t bm, int s,
   }
 }
 
+// Exact n-th largest score of each row of a slice and the ordered emission of its chosen
+// candidates (steps 2 and 3 above) over the key slots a scoring step left in acc.  nmt: the
+// slice's M-tiles (its first four are sampled), ntg = ceil(nmt / 4), Q = 4 nmt key slots per
+// lane, v: this lane's valid slots, n / Cr: the row's budget and candidate count, search: the row
+// takes a strict subset, g: the row's geometry, out: the row's selection (LDS row when kStaged),
+// dummy: a padding slot of that LDS row (lanes with nothing left to write store there).
+template <bool kStaged>
+__device__ __forceinline__ void search_emit(float (&acc)[kPsMaxMt][4], int nmt, int ntg, int Q, int v, int n, int Cr,
+                                            bool search, int lg, const RowGeom& g, int16_t* out, int16_t* dummy) {
+  // ---- exact n-th largest per row
+  // Mean and variance of a sample: the first 16 slots of each of the row's lanes.
+  float s1 = 0.f, s2 = 0.f, ns = 0.f;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool ok = t < nmt && 4 * t + i < v;
+      const float x = ok ? acc[t][i] : 0.f;
+      s1 += x;
+      s2 = fmaf(x, x, s2);
+      ns += ok ? 1.f : 0.f;
+    }
+  }
+  s1 = row4_sum(s1);
+  s2 = row4_sum(s2);
+  ns = fmaxf(row4_sum(ns), 1.f);
+  const float inv_s = __builtin_amdgcn_rcpf(ns);
+  const float mu = s1 * inv_s;
+  const float sigma = __builtin_amdgcn_sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
+  const float inv = __builtin_amdgcn_rcpf((float)(Cr > 0 ? Cr : 1));
+  const float z0 = upper_normal_quantile(((float)n - 0.5f) * inv);
+  // Counts per unit of score near the guess (normal model) and the first pass's spacing: about
+  // 1.5 sqrt(n) + 2 counts, the typical binomial error of the model guess.
+  const float dens = fmaxf((float)Cr * 0.39894228f * __expf(-0.5f * z0 * z0) / sigma, 1e-30f);
+  const float step = (1.5f * __builtin_amdgcn_sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
+  const float t_mid = mu + sigma * z0;
+
+  // Bracket [lo, hi) in key space: count(key >= lo) = c_lo >= n > c_hi = count(key >= hi).
+  // lo starts just above -inf (every real score counts), hi just above +inf (none does).
+  constexpr uint32_t kKeyNegInf = 0x007fffffu;  // key of -inf: below every threshold used
+  uint32_t lo = kKeyNegInf + 1u, hi = 0xff800001u;
+  int c_lo = Cr, c_hi = 0;
+  float vlo = 0.f, vhi = 0.f;
+  bool lo_b = false, hi_b = false;  // vlo / vhi hold the score value of lo / hi
+  bool done = !search;
+  {  // first pass: three thresholds around the guess
+    const float va = t_mid - step, vb = t_mid, vc = t_mid + step;
+    const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
+    // compare against the exact values of the keys (non-finite guesses never enter the bracket)
+    const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
+#pragma unroll
+    for (int tg = 0; tg < kPsMaxMt / 4; ++tg) {
+      if (tg < ntg) {
+#pragma unroll
+        for (int t = 4 * tg; t < 4 * tg + 4; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[t][i] += 0.0f;  // -0 becomes +0 (shift_below relies on it)
+      }
+    }
+    int la = 0, lb = 0, lc = 0;  // slots below each threshold
+#pragma unroll
+    for (int d = 0; d < kPsMaxMt / 8; ++d) {
+      if (2 * d < ntg) {
+        uint32_t ma = 0u, mb = 0u, mc = 0u;
+#pragma unroll
+        for (int t = 8 * d; t < 8 * d + 8; ++t) {
+          if (t < 8 * d + 4 || 2 * d + 1 < ntg) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              ma = shift_below(ma, acc[t][i], fa);
+              mb = shift_below(mb, acc[t][i], fb);
+              mc = shift_below(mc, acc[t][i], fc);
+            }
+          }
+        }
+        la += __popc(ma);
+        lb += __popc(mb);
+        lc += __popc(mc);
+      }
+    }
+    const int ca = 64 * ntg - row4_sum(la);
+    const int cb = 64 * ntg - row4_sum(lb);
+    const int cc = 64 * ntg - row4_sum(lc);
+    if (!done) {
+      const uint32_t tt[3] = {ta, tb, tc};
+      const int cs[3] = {ca, cb, cc};
+      const float vs[3] = {va, vb, vc};
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+        if (tt[i] > lo && tt[i] < hi) {
+          if (cs[i] >= n) { lo = tt[i]; c_lo = cs[i]; vlo = vs[i]; lo_b = true; }
+          else { hi = tt[i]; c_hi = cs[i]; vhi = vs[i]; hi_b = true; }
+        }
+      }
+      done = (c_lo == n) || (hi - lo <= 1u);
+    }
+  }
+  float grow = 2.f * step;
+  for (int it = 0; it < 200; ++it) {  // every sixth step bisects the key range: done within 6 * 33
+    const bool want_max = !done && hi_b && (n - c_hi == 1);
+    const bool want_cnt = !done && !want_max;
+    if (__ballot(want_cnt) != 0ull) {
+      uint32_t t = lo + ((hi - lo) >> 1);  // key-space bisection unless a model step is taken
+      float tv = 0.f;
+      bool have_v = false;
+      if (want_cnt) {
+        if (lo_b && hi_b) {
+          if (it % 6 != 5) {
+            tv = vlo + (vhi - vlo) * (((float)(c_lo - n) + 0.5f) * __builtin_amdgcn_rcpf((float)(c_lo - c_hi)));
+            have_v = true;
+          }
+        } else if (it < 6) {  // one side still open: step outwards, doubling
+          tv = lo_b ? vlo + grow : vhi - grow;
+          grow *= 2.f;
+          have_v = true;
+        }
+        if (have_v) {
+          if (isfinite(tv))
+            t = key_of_value(tv);
+          else
+            have_v = false;
+        }
+        if (t <= lo) { t = lo + 1u; have_v = false; }
+        if (t >= hi) { t = hi - 1u; have_v = false; }
+      }
+      const int c = count_ge(acc, ntg, key_value(t));
+      if (want_cnt) {
+        const float vt = have_v ? tv : key_value(t);
+        if (c >= n) { lo = t; c_lo = c; vlo = vt; lo_b = true; }
+        else { hi = t; c_hi = c; vhi = vt; hi_b = true; }
+        done = (c_lo == n) || (hi - lo <= 1u);
+      }
+    } else if (__ballot(want_max) != 0ull) {
+      // n - 1 scores lie at or above hi: the n-th largest is the largest score below hi.  No
+      // score lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
+      const float fhi = key_value(hi);
+      float mv = -INFINITY;
+      for_slots(acc, ntg, [&](float x, int) { mv = x < fhi ? fmaxf(mv, x) : mv; });
+      const uint32_t m = row4_max(mv == -INFINITY ? 0u : key_of_value(mv));
+      if (want_max) {
+        lo = m;
+        hi = m + 1u;
+        c_lo = -1;  // unknown: the emission takes the n - c_hi lowest-index scores equal to lo
+        done = true;
+      }
+    } else {
+      break;
+    }
+  }
+
+  // ---- emission.  The chosen scores are those >= value(lo): exactly n of them unless several
+  // scores share that value (the bracket closed on one key, or the max pass found a repeated
+  // value).  Then (tie case) they are the scores > value(lo) -- c_hi of them, since hi = lo + 1
+  // -- plus the lowest-index n - c_hi of the scores equal to value(lo).
+  uint32_t ch[4];
+  ge_masks(acc, ntg, key_value(lo), ch);
+  int ccnt = 0;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
+  int ctot;
+  int cb = row4_excl_scan(ccnt, lg, &ctot);
+  const bool tie_mode = search && ctot != n;
+  if (__ballot(tie_mode) != 0ull) {
+    uint32_t gt[4], tm[4];
+    ge_masks(acc, ntg, key_value(lo + 1u), gt);
+    eq_masks(acc, ntg, key_value(lo), tm);
+    int tcnt = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) tcnt += __popc(tm[d]);
+    int ttot;
+    const int tb = row4_excl_scan(tcnt, lg, &ttot);
+    if (tie_mode) {
+      int take = min(max(n - c_hi - tb, 0), tcnt);
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        ch[d] = gt[d];
+        while (take > 0 && tm[d] != 0u) {
+          const uint32_t low = tm[d] & (~tm[d] + 1u);
+          ch[d] |= low;
+          tm[d] ^= low;
+          --take;
+        }
+      }
+    }
+    ccnt = 0;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
+    cb = row4_excl_scan(ccnt, lg, &ctot);
+  }
+  if (kStaged) {
+    // every lane runs the wave-uniform loops; rows without a search write nothing
+    emit_bits(ch, (Q + 31) >> 5, out + g.init_hi, cb, search ? n : 0, g.cand_lo + lg * Q, dummy);
+  } else if (search) {
+    int16_t* dst = out + g.init_hi;
+    const int cand0 = g.cand_lo + lg * Q;
+    int k = cb;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      uint32_t m = 32 * d < Q ? ch[d] : 0u;
+      while (m) {
+        const int e = __builtin_ctz(m);
+        if (k < n) dst[k] = (int16_t)(cand0 + 32 * d + e);  // never past the row's slots
+        ++k;
+        m &= m - 1u;
+      }
+    }
+  }
+}
+
 // kStaged: every set is assembled in the wavefront's LDS rows (k_total <= kPsStageK) and written
 // out with 16-byte stores; otherwise entries go straight to the output.  kWin: keys on the (32, 16)
 // window grid, max-pooled to blocks; otherwise one key per block.
@@ -433,208 +642,268 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     }
     if (kWin) load_f(s, fnext);  // s is already the next slice
 
-    // ---- exact n-th largest per row
-    // Mean and variance of a sample: the first 16 slots of each of the row's lanes.
-    float s1 = 0.f, s2 = 0.f, ns = 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool ok = t < nmt && 4 * t + i < v;
-        const float x = ok ? acc[t][i] : 0.f;
-        s1 += x;
-        s2 = fmaf(x, x, s2);
-        ns += ok ? 1.f : 0.f;
-      }
-    }
-    s1 = row4_sum(s1);
-    s2 = row4_sum(s2);
-    ns = fmaxf(row4_sum(ns), 1.f);
-    const float inv_s = __builtin_amdgcn_rcpf(ns);
-    const float mu = s1 * inv_s;
-    const float sigma = __builtin_amdgcn_sqrtf(fmaxf(s2 * inv_s - mu * mu, 1e-20f));
-    const float inv = __builtin_amdgcn_rcpf((float)(Cr > 0 ? Cr : 1));
-    const float z0 = upper_normal_quantile(((float)n - 0.5f) * inv);
-    // Counts per unit of score near the guess (normal model) and the first pass's spacing: about
-    // 1.5 sqrt(n) + 2 counts, the typical binomial error of the model guess.
-    const float dens = fmaxf((float)Cr * 0.39894228f * __expf(-0.5f * z0 * z0) / sigma, 1e-30f);
-    const float step = (1.5f * __builtin_amdgcn_sqrtf((float)n) + 2.f) * __builtin_amdgcn_rcpf(dens);
-    const float t_mid = mu + sigma * z0;
-
-    // Bracket [lo, hi) in key space: count(key >= lo) = c_lo >= n > c_hi = count(key >= hi).
-    // lo starts just above -inf (every real score counts), hi just above +inf (none does).
-    constexpr uint32_t kKeyNegInf = 0x007fffffu;  // key of -inf: below every threshold used
-    uint32_t lo = kKeyNegInf + 1u, hi = 0xff800001u;
-    int c_lo = Cr, c_hi = 0;
-    float vlo = 0.f, vhi = 0.f;
-    bool lo_b = false, hi_b = false;  // vlo / vhi hold the score value of lo / hi
-    bool done = !search;
-    {  // first pass: three thresholds around the guess
-      const float va = t_mid - step, vb = t_mid, vc = t_mid + step;
-      const uint32_t ta = key_of_value(va), tb = key_of_value(vb), tc = key_of_value(vc);
-      // compare against the exact values of the keys (non-finite guesses never enter the bracket)
-      const float fa = key_value(ta), fb = key_value(tb), fc = key_value(tc);
-#pragma unroll
-      for (int tg = 0; tg < kPsMaxMt / 4; ++tg) {
-        if (tg < ntg) {
-#pragma unroll
-          for (int t = 4 * tg; t < 4 * tg + 4; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[t][i] += 0.0f;  // -0 becomes +0 (shift_below relies on it)
-        }
-      }
-      int la = 0, lb = 0, lc = 0;  // slots below each threshold
-#pragma unroll
-      for (int d = 0; d < kPsMaxMt / 8; ++d) {
-        if (2 * d < ntg) {
-          uint32_t ma = 0u, mb = 0u, mc = 0u;
-#pragma unroll
-          for (int t = 8 * d; t < 8 * d + 8; ++t) {
-            if (t < 8 * d + 4 || 2 * d + 1 < ntg) {
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                ma = shift_below(ma, acc[t][i], fa);
-                mb = shift_below(mb, acc[t][i], fb);
-                mc = shift_below(mc, acc[t][i], fc);
-              }
-            }
-          }
-          la += __popc(ma);
-          lb += __popc(mb);
-          lc += __popc(mc);
-        }
-      }
-      const int ca = 64 * ntg - row4_sum(la);
-      const int cb = 64 * ntg - row4_sum(lb);
-      const int cc = 64 * ntg - row4_sum(lc);
-      if (!done) {
-        const uint32_t tt[3] = {ta, tb, tc};
-        const int cs[3] = {ca, cb, cc};
-        const float vs[3] = {va, vb, vc};
-#pragma unroll
-        for (int i = 0; i < 3; ++i) {
-          if (tt[i] > lo && tt[i] < hi) {
-            if (cs[i] >= n) { lo = tt[i]; c_lo = cs[i]; vlo = vs[i]; lo_b = true; }
-            else { hi = tt[i]; c_hi = cs[i]; vhi = vs[i]; hi_b = true; }
-          }
-        }
-        done = (c_lo == n) || (hi - lo <= 1u);
-      }
-    }
-    float grow = 2.f * step;
-    for (int it = 0; it < 200; ++it) {  // every sixth step bisects the key range: done within 6 * 33
-      const bool want_max = !done && hi_b && (n - c_hi == 1);
-      const bool want_cnt = !done && !want_max;
-      if (__ballot(want_cnt) != 0ull) {
-        uint32_t t = lo + ((hi - lo) >> 1);  // key-space bisection unless a model step is taken
-        float tv = 0.f;
-        bool have_v = false;
-        if (want_cnt) {
-          if (lo_b && hi_b) {
-            if (it % 6 != 5) {
-              tv = vlo + (vhi - vlo) * (((float)(c_lo - n) + 0.5f) * __builtin_amdgcn_rcpf((float)(c_lo - c_hi)));
-              have_v = true;
-            }
-          } else if (it < 6) {  // one side still open: step outwards, doubling
-            tv = lo_b ? vlo + grow : vhi - grow;
-            grow *= 2.f;
-            have_v = true;
-          }
-          if (have_v) {
-            if (isfinite(tv))
-              t = key_of_value(tv);
-            else
-              have_v = false;
-          }
-          if (t <= lo) { t = lo + 1u; have_v = false; }
-          if (t >= hi) { t = hi - 1u; have_v = false; }
-        }
-        const int c = count_ge(acc, ntg, key_value(t));
-        if (want_cnt) {
-          const float vt = have_v ? tv : key_value(t);
-          if (c >= n) { lo = t; c_lo = c; vlo = vt; lo_b = true; }
-          else { hi = t; c_hi = c; vhi = vt; hi_b = true; }
-          done = (c_lo == n) || (hi - lo <= 1u);
-        }
-      } else if (__ballot(want_max) != 0ull) {
-        // n - 1 scores lie at or above hi: the n-th largest is the largest score below hi.  No
-        // score lies strictly between it and hi, so count(key >= m + 1) is still c_hi.
-        const float fhi = key_value(hi);
-        float mv = -INFINITY;
-        for_slots(acc, ntg, [&](float x, int) { mv = x < fhi ? fmaxf(mv, x) : mv; });
-        const uint32_t m = row4_max(mv == -INFINITY ? 0u : key_of_value(mv));
-        if (want_max) {
-          lo = m;
-          hi = m + 1u;
-          c_lo = -1;  // unknown: the emission takes the n - c_hi lowest-index scores equal to lo
-          done = true;
-        }
-      } else {
-        break;
-      }
-    }
-
-    // ---- emission.  The chosen scores are those >= value(lo): exactly n of them unless several
-    // scores share that value (the bracket closed on one key, or the max pass found a repeated
-    // value).  Then (tie case) they are the scores > value(lo) -- c_hi of them, since hi = lo + 1
-    // -- plus the lowest-index n - c_hi of the scores equal to value(lo).
-    uint32_t ch[4];
-    ge_masks(acc, ntg, key_value(lo), ch);
-    int ccnt = 0;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
-    int ctot;
-    int cb = row4_excl_scan(ccnt, lg, &ctot);
-    const bool tie_mode = search && ctot != n;
-    if (__ballot(tie_mode) != 0ull) {
-      uint32_t gt[4], tm[4];
-      ge_masks(acc, ntg, key_value(lo + 1u), gt);
-      eq_masks(acc, ntg, key_value(lo), tm);
-      int tcnt = 0;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) tcnt += __popc(tm[d]);
-      int ttot;
-      const int tb = row4_excl_scan(tcnt, lg, &ttot);
-      if (tie_mode) {
-        int take = min(max(n - c_hi - tb, 0), tcnt);
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          ch[d] = gt[d];
-          while (take > 0 && tm[d] != 0u) {
-            const uint32_t low = tm[d] & (~tm[d] + 1u);
-            ch[d] |= low;
-            tm[d] ^= low;
-            --take;
-          }
-        }
-      }
-      ccnt = 0;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) ccnt += __popc(ch[d]);
-      cb = row4_excl_scan(ccnt, lg, &ctot);
-    }
-    if (kStaged) {
-      // every lane runs the wave-uniform loops; rows without a search write nothing
-      emit_bits(ch, (Q + 31) >> 5, out + g.init_hi, cb, search ? n : 0, g.cand_lo + lg * Q, out + kPsStageK + lg);
-    } else if (search) {
-      int16_t* dst = out + g.init_hi;
-      const int cand0 = g.cand_lo + lg * Q;
-      int k = cb;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        uint32_t m = 32 * d < Q ? ch[d] : 0u;
-        while (m) {
-          const int e = __builtin_ctz(m);
-          if (k < n) dst[k] = (int16_t)(cand0 + 32 * d + e);  // never past the row's slots
-          ++k;
-          m &= m - 1u;
-        }
-      }
-    }
+    search_emit<kStaged>(acc, nmt, ntg, Q, v, n, Cr, search, lg, g, out, out + kPsStageK + lg);
   }
   if (kStaged && s_prev >= 0) {
     wave_lds_sync();
     copy_out(a, bm, s_prev, ost, lane);
+  }
+}
+
+// ---- the (32, 16) window grid, scored in lockstep from LDS
+//
+// Read straight from L2 by every wavefront, the window keys of a unit are fetched once per slice:
+// about 4 TB at the 32K prefill, and the kernel above waits on them.  This kernel takes a unit's
+// slices in groups of kPsWaves consecutive ones, one per wavefront, all laid out with the
+// quarter Q of the group's last slice (the one with the most candidates; rows with fewer get
+// -inf slots).  Every wavefront of the group then reads the same window keys: chunks of
+// kPwTiles window-tiles (4 kPwTiles windows of each quarter) are staged once per workgroup in
+// LDS, double-buffered (a chunk is loaded two pieces per M-tile while the previous one is
+// scored), and the A fragments come from there.  Search and emission are the block grid's.
+// Once a group is scored the chunk buffers are free: each wavefront assembles its slice's sets
+// there (rows of k_total rounded up to 8, plus 8 padding slots) and copies them out with 16-byte
+// stores, for any k_total up to kPwStageKMax; larger sets are written straight to the output.
+constexpr int kPwTiles = 16;                        // window-tiles per staged chunk (4 M-tiles)
+constexpr int kPwWin = 4 * kPwTiles;                // windows per quarter per chunk
+constexpr int kPwQuarter = kPwWin * kPsPitch + 32;  // uint16 per staged quarter; the extra 64 B put
+                                                    // the 16 rows one A read takes (4 quarters x 4
+                                                    // windows) on distinct banks
+constexpr int kPwChunk = 4 * kPwQuarter;            // uint16 per chunk buffer
+constexpr int kPwStageLd = 4 * kPwWin * 16 / kPsThreads;  // 16-byte staging pieces per thread
+static_assert(kPwStageLd == 8 && kPwWin == 64, "staging: thread t takes windows t / 16 and t / 16 + 32 of each quarter");
+constexpr int kPwStageKMax = 256;                   // largest k_total assembled in LDS
+static_assert(kPsWaves * kPsRows * (kPwStageKMax + 8) <= 2 * kPwChunk, "set rows fit in the chunk buffers");
+
+__host__ __device__ inline int pw_out_pitch(int k_total) { return ((k_total + 7) & ~7) + 8; }
+
+// Copies the assembled sets of a slice's valid rows (LDS rows `pitch` apart) to the output.
+__device__ __forceinline__ void copy_out_rows(const SelectArgs& a, int64_t bm, int s, const int16_t* ost, int pitch,
+                                              int lane) {
+  const int nr = min(kPsRows, a.n_q - s * kPsRows);
+  const int k = a.k_total;
+  int16_t* dst = a.sel + (bm * a.n_q + (int64_t)s * kPsRows) * k;
+  if (((reinterpret_cast<uintptr_t>(dst) | (uintptr_t)(2 * k)) & 15u) == 0) {
+    const int per_row = k / 8;  // 16-byte chunks per row
+    for (int i = lane; i < nr * per_row; i += 64) {
+      const int r = i / per_row, c = i - r * per_row;
+      *reinterpret_cast<uint4*>(dst + r * k + 8 * c) = *reinterpret_cast<const uint4*>(ost + r * pitch + 8 * c);
+    }
+  } else {
+    for (int i = lane; i < nr * k; i += 64) {
+      const int r = i / k;
+      dst[i] = ost[r * pitch + (i - r * k)];
+    }
+  }
+}
+
+// kOut: where a slice's sets are assembled.  0: LDS rows of their own (k_total <= kPsStageK; the
+// copy-out of one slice waits until the next group has been scored), 1: the chunk buffers (after
+// the group is scored; k_total <= kPwStageKMax), 2: straight to the output.
+template <int kOut>
+__global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
+  constexpr bool kStaged = kOut != 2;
+  __shared__ __align__(16) uint16_t wst[2 * kPwChunk];
+  __shared__ __align__(16) int16_t ost_all[kOut == 0 ? kPsWaves * kPsRows * kPsOutPitch : 8];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t bm = blockIdx.x % n_groups;
+  const int u = (int)(blockIdx.x / n_groups);
+  const int s_begin = plan.bound[u], s_end = plan.bound[u + 1];
+  if (s_begin >= s_end) return;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int opitch = kOut == 0 ? kPsOutPitch : pw_out_pitch(a.k_total);
+  int16_t* ost = (kOut == 0 ? ost_all : reinterpret_cast<int16_t*>(wst)) + wave * kPsRows * opitch;  // set rows
+  const uint16_t* kcg = a.kc + bm * a.nc_cap * kHeadDim;  // the group's window keys
+  auto load_f = [&](int s, uint4 (&fw)[4]) {
+    const int r = s * kPsRows + lr;
+    if (s >= s_begin && r < a.n_q) {
+      const uint16_t* fp = a.f + (bm * a.n_q + r) * kHeadDim + 8 * lg;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fw[ks] = ld16(fp + 32 * ks);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fw[ks] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+
+  uint4 fnext[4];
+  load_f(s_end - 1 - wave, fnext);
+  int s_prev = -1;  // kOut 0: the slice whose sets still wait in LDS
+  // Groups from the end of the range (most candidates first); wavefront w takes slice g_hi - 1 - w.
+  for (int g_hi = s_end; g_hi > s_begin; g_hi -= kPsWaves) {
+    const int s = g_hi - 1 - wave;
+    const bool have = s >= s_begin;
+    uint4 fw[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
+    if (kOut == 0 && s_prev >= 0) {
+      wave_lds_sync();
+      copy_out_rows(a, bm, s_prev, ost, opitch, lane);
+    }
+
+    const int r = s * kPsRows + lr;
+    const bool row_ok = have && r < a.n_q;
+    const int64_t row = bm * a.n_q + r;
+    const RowGeom g = row_geom(a.q_pos0 + (row_ok ? r : 0), a.n_init, a.n_local, a.k_total);
+    int16_t* out = kStaged ? ost + lr * opitch : a.sel + row * a.k_total;
+    // The group's last row (the most candidates and windows of any row of the group), and this
+    // wavefront's slice.
+    const int64_t pg_last = a.q_pos0 + min((int64_t)a.n_q, (int64_t)g_hi * kPsRows) - 1;
+    const RowGeom gg = row_geom(pg_last, a.n_init, a.n_local, a.k_total);
+    const bool group_scores = gg.n_take < gg.n_cand;  // else every row of the group takes everything
+    const int64_t p_last = have ? a.q_pos0 + min(a.n_q, (s + 1) * kPsRows) - 1 : pg_last;
+    const RowGeom gs = row_geom(p_last, a.n_init, a.n_local, a.k_total);
+    const int64_t p_first = a.q_pos0 + (int64_t)(have ? s : 0) * kPsRows;
+    const bool score = have && gs.n_take < gs.n_cand;  // uniform over the wavefront
+    // forced blocks, padding, rows that take every candidate
+    auto forced = [&]() {
+      if (row_ok) {
+        for (int i = lg; i < g.init_hi; i += 4) out[i] = (int16_t)i;
+        const int n_loc = g.blk - g.local_lo + 1;
+        for (int i = lg; i < n_loc; i += 4) out[g.init_hi + g.n_take + i] = (int16_t)(g.local_lo + i);
+        for (int i = g.n_forced + g.n_take + lg; i < a.k_total; i += 4) out[i] = (int16_t)-1;
+        if (lg == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+        if (g.n_take >= g.n_cand)
+          for (int i = lg; i < g.n_cand; i += 4) out[g.init_hi + i] = (int16_t)(g.cand_lo + i);
+      }
+    };
+    if (kOut != 1) forced();
+
+    const int nmt = (gg.n_cand + 15) >> 4;  // uniform over the workgroup
+    const int ntg = (nmt + 3) >> 2;         // chunks
+    const int Q = 4 * nmt;
+    const int n = g.n_take, Cr = g.n_cand;
+    const bool search = row_ok && n > 0 && n < Cr;
+    const int v = search ? min(max(Cr - lg * Q, 0), Q) : Q;  // this lane's valid key slots
+    float acc[kPsMaxMt][4];
+    if (group_scores) {
+      int32_t wg_first, wg_last;
+      row_windows(gg, a.grid, pg_last, &wg_first, &wg_last);
+      (void)wg_first;
+      const int cl = gg.cand_lo;
+      // Chunk c holds, for quarter q, windows 4 (cl + q Q + kPwTiles c) .. + kPwWin - 1; windows
+      // past the group's last one repeat it (their scores never reach a valid slot).  Thread t
+      // stages 16-byte part t % 16 of windows t / 16 and t / 16 + 32 of every quarter: pieces
+      // x = 0 .. 7.
+      const int st_w = tid >> 4, st_part = tid & 15;
+      auto stage_piece = [&](int c, int x) -> uint4 {
+        const int q = x >> 1, w = st_w + 32 * (x & 1);
+        const int win = min(4 * (cl + q * Q + kPwTiles * c) + w, wg_last);
+        return ld16(kcg + (int64_t)win * kHeadDim + st_part * 8);
+      };
+      auto stage_put = [&](int b, int x, uint4 val) {
+        const int q = x >> 1, w = st_w + 32 * (x & 1);
+        *reinterpret_cast<uint4*>(wst + b * kPwChunk + q * kPwQuarter + w * kPsPitch + st_part * 8) = val;
+      };
+      bf16x8 fb[4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) fb[ks] = as_bf16x8(fw[ks]);
+      const int bo = cl + lg * Q;  // first block of the scores this lane holds
+      // Windows past the row's last complete one score -inf; only a slice whose candidate windows
+      // reach past its first row's last complete window has any (n_local = 1).
+      const bool need_vis = score && grid_win_hi(a.grid, gs.cand_lo + gs.n_cand - 1) > grid_win_vis(a.grid, p_first);
+      const int vis = need_vis ? grid_win_vis(a.grid, a.q_pos0 + r) : 0x7fffffff;
+      float carry = -INFINITY;  // window 4 b - 1 of the next block: the previous tile's last window
+      {
+        uint4 sw[kPwStageLd];
+#pragma unroll
+        for (int x = 0; x < kPwStageLd; ++x) sw[x] = stage_piece(0, x);
+        if (score) {
+          // window-tile -1 (its last window is window 4 bo - 1), from the key cache
+          const int wa = min(max(4 * (cl + (lr >> 2) * Q - 1) + (lr & 3), 0), wg_last);
+          const uint16_t* pa = kcg + (int64_t)wa * kHeadDim + 8 * lg;
+          f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(ld16(pa + 32 * ks)), fb[ks], c);
+          carry = 4 * bo - 1 >= 0 ? c[3] : -INFINITY;  // window 4 bo - 1 exists unless bo = 0
+        }
+        if (kOut == 1) __syncthreads();  // the previous group's set rows have left the buffers
+#pragma unroll
+        for (int x = 0; x < kPwStageLd; ++x) stage_put(0, x, sw[x]);
+      }
+      __syncthreads();  // chunk 0 staged
+#pragma unroll
+      for (int c = 0; c < kPsMaxMt / 4; ++c) {
+        if (c < ntg) {  // uniform over the workgroup
+          const uint16_t* ab = wst + (c & 1) * kPwChunk + (lr >> 2) * kPwQuarter + (lr & 3) * kPsPitch + 8 * lg;
+          const bool st_next = c + 1 < ntg;  // then chunk c has all four M-tiles
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int mt = 4 * c + k;
+            if (mt < nmt) {
+              // the next chunk, two pieces per M-tile
+              uint4 sp0, sp1;
+              if (st_next) {
+                sp0 = stage_piece(c + 1, 2 * k);
+                sp1 = stage_piece(c + 1, 2 * k + 1);
+              }
+              if (score) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  const uint16_t* ap = ab + 4 * (4 * k + i) * kPsPitch;  // window-tile 4 k + i of the chunk
+                  f32x4 cc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                  for (int ks = 0; ks < 4; ++ks)
+                    cc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const uint4*>(ap + 32 * ks)), fb[ks], cc);
+                  // window 4 (bo + u) + e is visible iff it is <= vis: all-ones mask selects -inf
+                  const int d = vis - 4 * (bo + 4 * mt + i);
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    const uint32_t m = (uint32_t)((d - e) >> 31);
+                    cc[e] = __uint_as_float((m & 0xff800000u) | (~m & __float_as_uint(cc[e])));
+                  }
+                  acc[mt][i] = fmaxf(fmaxf(fmaxf(cc[0], cc[1]), fmaxf(cc[2], cc[3])), carry);
+                  carry = cc[3];
+                }
+              } else {  // defined on every path, so that no slot lives on from an earlier group
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[mt][i] = -INFINITY;
+              }
+              if (st_next) {
+                stage_put((c + 1) & 1, 2 * k, sp0);
+                stage_put((c + 1) & 1, 2 * k + 1, sp1);
+              }
+            } else {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) acc[mt][i] = -INFINITY;
+            }
+          }
+          __syncthreads();  // chunk c scored everywhere; chunk c + 1 staged
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[4 * c + k][i] = -INFINITY;
+        }
+      }
+    } else if (kOut == 1) {
+      __syncthreads();  // the previous group's set rows have left the buffers
+    }
+    // the next group's F rows, requested after the scoring, whose registers they would crowd
+    load_f(s - kPsWaves, fnext);
+    if (kOut == 1) forced();  // the buffers are free now
+
+    if (score) {
+      // Key slots past the row's candidates (the last lane group's tail, rows with fewer
+      // candidates than the group's last row) hold -inf, which no threshold admits.
+#pragma unroll
+      for (int t = 0; t < kPsMaxMt; ++t) {
+        if (t < nmt && __ballot(4 * t + 4 > v) != 0ull) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (4 * t + i >= v) acc[t][i] = -INFINITY;
+        }
+      }
+      search_emit<kStaged>(acc, nmt, ntg, Q, v, n, Cr, search, lg, g, out, out + opitch - 8 + lg);
+    }
+    if (kOut == 1 && have) {
+      wave_lds_sync();
+      copy_out_rows(a, bm, s, ost, opitch, lane);
+    }
+    if (kOut == 0) s_prev = have ? s : -1;
+  }
+  if (kOut == 0 && s_prev >= 0) {
+    wave_lds_sync();
+    copy_out_rows(a, bm, s_prev, ost, opitch, lane);
   }
 }
 
@@ -665,6 +934,33 @@ static void plan_units(const SelectArgs& a, int units, int per_cand, PrefillPlan
   plan->bound[units] = (uint16_t)ns;
 }
 
+// The window-grid kernel scores kPsWaves slices at a time in lockstep: units take whole groups of
+// kPsWaves slices (aligned from slice 0), costed by the group's last slice.
+static void plan_unit_groups(const SelectArgs& a, int units, int per_cand, PrefillPlan* plan) {
+  const int ns = (a.n_q + kPsRows - 1) / kPsRows;
+  const int ng = (ns + kPsWaves - 1) / kPsWaves;
+  plan->n_slices = ns;
+  plan->units = units;
+  auto cost = [&](int gi) -> int64_t {
+    const int s_last = std::min(ns, (gi + 1) * kPsWaves) - 1;
+    const RowGeom g = row_geom(a.q_pos0 + std::min<int64_t>(a.n_q, (int64_t)(s_last + 1) * kPsRows) - 1, a.n_init,
+                               a.n_local, a.k_total);
+    if (g.n_take >= g.n_cand) return 40;
+    return 230 + per_cand * 16 * ((g.n_cand + 15) / 16);
+  };
+  int64_t total = 0;
+  for (int gi = 0; gi < ng; ++gi) total += cost(gi);
+  int64_t acc = 0;
+  int gi = 0;
+  plan->bound[0] = 0;
+  for (int uu = 1; uu < units; ++uu) {
+    const int64_t target = total * uu / units;
+    while (gi < ng && acc + cost(gi) <= target) acc += cost(gi++);
+    plan->bound[uu] = (uint16_t)std::min(ns, gi * kPsWaves);
+  }
+  plan->bound[units] = (uint16_t)ns;
+}
+
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int n_groups = a.batch * a.n_kv_heads;
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
@@ -675,13 +971,18 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const bool win = !grid_is_blocks(a.grid);
   if (win && !(a.grid.l == 32 && a.grid.s == 16)) return hipErrorInvalidValue;
   PrefillPlan plan;
-  plan_units(a, units, win ? 3 : 1, &plan);
+  if (win)
+    plan_unit_groups(a, units, 3, &plan);
+  else
+    plan_units(a, units, 1, &plan);
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
   if (win && staged)
-    hipLaunchKernelGGL((prefill_select_kernel<true, true>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<0>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+  else if (win && a.k_total <= kPwStageKMax)
+    hipLaunchKernelGGL((prefill_select_win_kernel<1>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else if (win)
-    hipLaunchKernelGGL((prefill_select_kernel<false, true>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<2>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else if (staged)
     hipLaunchKernelGGL((prefill_select_kernel<true, false>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else
