@@ -34,14 +34,14 @@
 //      indices in ascending order.
 //
 // On the paper's (32, 16) key grid (Sec. 3: windows of 32 tokens at stride 16, max-pooled to
-// blocks) step 1 scores windows instead: block b's score is the largest score among windows
-// 4b - 1 .. 4b + 3 that are complete at the row's position.  Window-tile u puts window
-// 4 (n_init + (m / 4) Q + u) + m % 4 in A row m, so lane (n, j) receives windows 4b .. 4b + 3 of
-// block b = n_init + j Q + u in its accumulators and pools them with the previous tile's
-// last window (a tile u = -1 supplies it for u = 0).  The pooled score lands in the key slot the
-// block grid uses for block b, and steps 2-3 run unchanged.  The window keys (four times as many)
-// do not fit in LDS, so A fragments come from the K~ cache (L2-resident: 0.5 MB per group at 32K),
-// two tiles ahead.
+// blocks) step 1 scores windows instead (prefill_select_win_kernel): block b's score is the
+// largest score among windows 4b - 1 .. 4b + 3 that are complete at the row's position.
+// Window-tile u puts window 4 (n_init + (m / 4) Q + u) + m % 4 in A row m, so lane (n, j)
+// receives windows 4b .. 4b + 3 of block b = n_init + j Q + u in its accumulators and pools them
+// with the previous tile's last window (a tile u = -1 supplies it for u = 0).  The pooled score
+// lands in the key slot the block grid uses for block b, and steps 2-3 run unchanged.  The
+// window keys (four times as many) do not fit in LDS at once; they are staged in chunks shared by
+// a workgroup's wavefronts, which score eight slices in lockstep (see that kernel).
 #include <math.h>
 
 #include <algorithm>
@@ -432,12 +432,12 @@ __device__ __forceinline__ void search_emit(float (&acc)[kPsMaxMt][4], int nmt, 
   }
 }
 
-// kStaged: every set is assembled in the wavefront's LDS rows (k_total <= kPsStageK) and written
-// out with 16-byte stores; otherwise entries go straight to the output.  kWin: keys on the (32, 16)
-// window grid, max-pooled to blocks; otherwise one key per block.
-template <bool kStaged, bool kWin>
+// The block grid (one key per block).  kStaged: every set is assembled in the wavefront's LDS rows
+// (k_total <= kPsStageK) and written out with 16-byte stores; otherwise entries go straight to the
+// output.
+template <bool kStaged>
 __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
-  __shared__ __align__(16) uint16_t kst[kWin ? 8 : kPsStageRows * kPsPitch];
+  __shared__ __align__(16) uint16_t kst[kPsStageRows * kPsPitch];
   __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsOutPitch : 8];
   __shared__ int next_slice;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
   // whole M-tiles and the read-ahead rows.  Rows that take every candidate are never scored, and
   // neither is a unit whose last row takes every candidate (earlier rows have at most as many
   // candidates and at least as large a budget).
-  if (!kWin) {
+  {
     const RowGeom gl = row_geom(a.q_pos0 + min(a.n_q, s_end * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
     const int c_stage = gl.n_take < gl.n_cand ? gl.n_cand : 0;
     const int c_fill = c_stage > 0 ? ((c_stage + 15) & ~15) + 8 : 0;
@@ -494,9 +494,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
     const int s_next = grab();
-    // On the window grid the next slice's F rows are requested after the scoring, whose A
-    // read-ahead needs the registers.
-    if (!kWin) load_f(s_next, fnext);
+    load_f(s_next, fnext);
     // The previous slice's sets leave LDS now: these stores are long complete when the next
     // slice waits for the F rows requested just above.
     if (kStaged && s_prev >= 0) {
@@ -521,13 +519,9 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
     }
     const int64_t p_last = a.q_pos0 + min(a.n_q, (s + 1) * kPsRows) - 1;  // the slice's last row
     const RowGeom gs = row_geom(p_last, a.n_init, a.n_local, a.k_total);
-    const int64_t p_first = a.q_pos0 + (int64_t)s * kPsRows;
     s_prev = s;
     s = s_next;
-    if (gs.n_take >= gs.n_cand) {  // the slice's last row takes every candidate: all rows do
-      if (kWin) load_f(s, fnext);
-      continue;
-    }
+    if (gs.n_take >= gs.n_cand) continue;  // the slice's last row takes every candidate: all rows do
 
     // ---- scores: S^T = K~ F^T, one M-tile of 16 candidates at a time
     const int C = gs.n_cand;
@@ -542,68 +536,6 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       bf16x8 fb[4];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) fb[ks] = as_bf16x8(fw[ks]);
-      if constexpr (kWin) {
-        int32_t w_first, w_last;  // windows the slice's last row reads (the most of any row)
-        row_windows(gs, a.grid, p_last, &w_first, &w_last);
-        (void)w_first;
-        // The lane loads A row m = lr (quarter lr / 4) but accumulates query row lr of quarter lg:
-        // ba is the first block of the row it loads, bo the first block of the scores it holds.
-        const int ba = gs.cand_lo + (lr >> 2) * Q, bo = gs.cand_lo + lg * Q;
-        const uint16_t* kcb = a.kc + bm * a.nc_cap * kHeadDim + 8 * lg;
-        // A row of window-tile u; reads past the slice's last window (padding slots, read-ahead)
-        // are clamped to it and their scores never reach a valid slot.
-        auto arow = [&](int u) {
-          const int w = min(max(4 * (ba + u) + (lr & 3), 0), w_last);
-          return kcb + (int64_t)w * kHeadDim;
-        };
-        // Windows past the row's last complete one score -inf; only a slice whose candidate
-        // windows reach past its first row's last complete window has any (n_local = 1).
-        const bool need_vis = grid_win_hi(a.grid, gs.cand_lo + C - 1) > grid_win_vis(a.grid, p_first);
-        const int vis = need_vis ? grid_win_vis(a.grid, a.q_pos0 + r) : 0x7fffffff;
-        constexpr int kAhead = 3;  // window-tiles of read-ahead
-        constexpr int kNb = kAhead + 1;
-        uint4 aw[kNb][4];  // window-tile u lives in aw[(u + 1) % kNb]
-#pragma unroll
-        for (int b = 0; b < kNb; ++b) {
-          const uint16_t* pb = arow(b - 1);
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) aw[b][ks] = ld16(pb + 32 * ks);
-        }
-        float carry;  // window 4b - 1 of the next block: the previous tile's last window
-        {
-          f32x4 c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[0][ks]), fb[ks], c);
-          carry = 4 * bo - 1 >= 0 ? c[3] : -INFINITY;  // window 4 bo - 1 exists unless bo = 0
-        }
-#pragma unroll
-        for (int mt = 0; mt < kPsMaxMt; ++mt) {
-          if (mt < nmt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int u = 4 * mt + i;
-              const uint16_t* pn = arow(u + kAhead);
-#pragma unroll
-              for (int ks = 0; ks < 4; ++ks) aw[u % kNb][ks] = ld16(pn + 32 * ks);
-              f32x4 c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(aw[(u + 1) % kNb][ks]), fb[ks], c);
-              // window 4 (bo + u) + e is visible iff it is <= vis: all-ones mask selects -inf
-              const int d = vis - 4 * (bo + u);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const uint32_t m = (uint32_t)((d - e) >> 31);
-                c[e] = __uint_as_float((m & 0xff800000u) | (~m & __float_as_uint(c[e])));
-              }
-              acc[mt][i] = fmaxf(fmaxf(fmaxf(c[0], c[1]), fmaxf(c[2], c[3])), carry);
-              carry = c[3];
-            }
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[mt][i] = -INFINITY;
-          }
-        }
-      } else {
       const uint16_t* ab = kst + ((lr >> 2) * Q + (lr & 3)) * kPsPitch + 8 * lg;
       // A fragments are read two M-tiles ahead of the MFMAs that use them (past the last M-tile
       // this reads rows up to 16 nmt + 7: inside the staged array).
@@ -628,7 +560,6 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
           for (int i = 0; i < 4; ++i) acc[t][i] = -INFINITY;
         }
       }
-      }
       // Key slots past the row's candidates (the last lane group's tail, rows with fewer
       // candidates than the slice) hold -inf, which no threshold admits.
 #pragma unroll
@@ -640,7 +571,6 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
         }
       }
     }
-    if (kWin) load_f(s, fnext);  // s is already the next slice
 
     search_emit<kStaged>(acc, nmt, ntg, Q, v, n, Cr, search, lg, g, out, out + kPsStageK + lg);
   }
@@ -984,9 +914,9 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   else if (win)
     hipLaunchKernelGGL((prefill_select_win_kernel<2>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else if (staged)
-    hipLaunchKernelGGL((prefill_select_kernel<true, false>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_kernel<true>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else
-    hipLaunchKernelGGL((prefill_select_kernel<false, false>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_kernel<false>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   return hipGetLastError();
 }
 
