@@ -583,26 +583,35 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 // ---- the (32, 16) window grid, scored in lockstep from LDS
 //
 // Read straight from L2 by every wavefront, the window keys of a unit are fetched once per slice:
-// about 4 TB at the 32K prefill, and the kernel above waits on them.  This kernel takes a unit's
-// slices in groups of kPsWaves consecutive ones, one per wavefront, all laid out with the
+// about 4 TB at the 32K prefill, and a kernel that does so waits on them.  This kernel takes a
+// unit's slices in groups of kPwWaves consecutive ones, one per wavefront, all laid out with the
 // quarter Q of the group's last slice (the one with the most candidates; rows with fewer get
 // -inf slots).  Every wavefront of the group then reads the same window keys: chunks of
 // kPwTiles window-tiles (4 kPwTiles windows of each quarter) are staged once per workgroup in
-// LDS, double-buffered (a chunk is loaded two pieces per M-tile while the previous one is
-// scored), and the A fragments come from there.  Search and emission are the block grid's.
+// LDS, double-buffered (a chunk is loaded piece by piece, M-tile by M-tile, while the previous
+// one is scored), and the A fragments come from there.  Search and emission are the block grid's.
+// Two 4-wavefront workgroups share a CU and drift apart, so that one's MFMA scoring overlaps the
+// other's VALU search (a group's wavefronts are otherwise in the same phase).
 // Once a group is scored the chunk buffers are free: each wavefront assembles its slice's sets
 // there (rows of k_total rounded up to 8, plus 8 padding slots) and copies them out with 16-byte
 // stores, for any k_total up to kPwStageKMax; larger sets are written straight to the output.
-constexpr int kPwTiles = 16;                        // window-tiles per staged chunk (4 M-tiles)
+constexpr int kPwWaves = 4;                         // wavefronts (slices in lockstep) per workgroup
+constexpr int kPwThreads = 64 * kPwWaves;
+constexpr int kPwMt = 2;                            // M-tiles per staged chunk
+constexpr int kPwTiles = 4 * kPwMt;                 // window-tiles per staged chunk
 constexpr int kPwWin = 4 * kPwTiles;                // windows per quarter per chunk
 constexpr int kPwQuarter = kPwWin * kPsPitch + 32;  // uint16 per staged quarter; the extra 64 B put
                                                     // the 16 rows one A read takes (4 quarters x 4
                                                     // windows) on distinct banks
 constexpr int kPwChunk = 4 * kPwQuarter;            // uint16 per chunk buffer
-constexpr int kPwStageLd = 4 * kPwWin * 16 / kPsThreads;  // 16-byte staging pieces per thread
-static_assert(kPwStageLd == 8 && kPwWin == 64, "staging: thread t takes windows t / 16 and t / 16 + 32 of each quarter");
+constexpr int kPwStageLd = 4 * kPwWin * 16 / kPwThreads;  // 16-byte staging pieces per thread
+constexpr int kPwWinPerThr = kPwThreads / 16;       // windows of a quarter covered by one piece index
+static_assert(kPwStageLd == 8 && kPwWin == 2 * kPwWinPerThr,
+              "staging: thread t takes windows t / 16 and t / 16 + kPwWinPerThr of each quarter");
+static_assert(kPwStageLd % kPwMt == 0, "each M-tile stages the same number of pieces");
 constexpr int kPwStageKMax = 256;                   // largest k_total assembled in LDS
-static_assert(kPsWaves * kPsRows * (kPwStageKMax + 8) <= 2 * kPwChunk, "set rows fit in the chunk buffers");
+static_assert(kPwWaves * kPsRows * (kPwStageKMax + 8) <= 2 * kPwChunk, "set rows fit in the chunk buffers");
+static_assert(2 * (2 * kPwChunk * 2 + kPwWaves * kPsRows * kPsOutPitch * 2) <= 160 * 1024, "two workgroups per CU");
 
 __host__ __device__ inline int pw_out_pitch(int k_total) { return ((k_total + 7) & ~7) + 8; }
 
@@ -630,10 +639,10 @@ __device__ __forceinline__ void copy_out_rows(const SelectArgs& a, int64_t bm, i
 // copy-out of one slice waits until the next group has been scored), 1: the chunk buffers (after
 // the group is scored; k_total <= kPwStageKMax), 2: straight to the output.
 template <int kOut>
-__global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
+__global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
   constexpr bool kStaged = kOut != 2;
   __shared__ __align__(16) uint16_t wst[2 * kPwChunk];
-  __shared__ __align__(16) int16_t ost_all[kOut == 0 ? kPsWaves * kPsRows * kPsOutPitch : 8];
+  __shared__ __align__(16) int16_t ost_all[kOut == 0 ? kPwWaves * kPsRows * kPsOutPitch : 8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
@@ -659,7 +668,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
   load_f(s_end - 1 - wave, fnext);
   int s_prev = -1;  // kOut 0: the slice whose sets still wait in LDS
   // Groups from the end of the range (most candidates first); wavefront w takes slice g_hi - 1 - w.
-  for (int g_hi = s_end; g_hi > s_begin; g_hi -= kPsWaves) {
+  for (int g_hi = s_end; g_hi > s_begin; g_hi -= kPwWaves) {
     const int s = g_hi - 1 - wave;
     const bool have = s >= s_begin;
     uint4 fw[4];
@@ -699,7 +708,8 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
     if (kOut != 1) forced();
 
     const int nmt = (gg.n_cand + 15) >> 4;  // uniform over the workgroup
-    const int ntg = (nmt + 3) >> 2;         // chunks
+    const int ntg = (nmt + 3) >> 2;         // groups of 4 M-tiles the search's slot loops run over
+    const int nch = (nmt + kPwMt - 1) / kPwMt;  // chunks
     const int Q = 4 * nmt;
     const int n = g.n_take, Cr = g.n_cand;
     const bool search = row_ok && n > 0 && n < Cr;
@@ -712,16 +722,16 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
       const int cl = gg.cand_lo;
       // Chunk c holds, for quarter q, windows 4 (cl + q Q + kPwTiles c) .. + kPwWin - 1; windows
       // past the group's last one repeat it (their scores never reach a valid slot).  Thread t
-      // stages 16-byte part t % 16 of windows t / 16 and t / 16 + 32 of every quarter: pieces
-      // x = 0 .. 7.
+      // stages 16-byte part t % 16 of windows t / 16 and t / 16 + kPwWinPerThr of every quarter:
+      // pieces x = 0 .. 7.
       const int st_w = tid >> 4, st_part = tid & 15;
       auto stage_piece = [&](int c, int x) -> uint4 {
-        const int q = x >> 1, w = st_w + 32 * (x & 1);
+        const int q = x >> 1, w = st_w + kPwWinPerThr * (x & 1);
         const int win = min(4 * (cl + q * Q + kPwTiles * c) + w, wg_last);
         return ld16(kcg + (int64_t)win * kHeadDim + st_part * 8);
       };
       auto stage_put = [&](int b, int x, uint4 val) {
-        const int q = x >> 1, w = st_w + 32 * (x & 1);
+        const int q = x >> 1, w = st_w + kPwWinPerThr * (x & 1);
         *reinterpret_cast<uint4*>(wst + b * kPwChunk + q * kPwQuarter + w * kPsPitch + st_part * 8) = val;
       };
       bf16x8 fb[4];
@@ -732,6 +742,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
       // reach past its first row's last complete window has any (n_local = 1).
       const bool need_vis = score && grid_win_hi(a.grid, gs.cand_lo + gs.n_cand - 1) > grid_win_vis(a.grid, p_first);
       const int vis = need_vis ? grid_win_vis(a.grid, a.q_pos0 + r) : 0x7fffffff;
+      const bool vis_on = __ballot(need_vis) != 0ull;  // uniform: whether any window needs the mask
       float carry = -INFINITY;  // window 4 b - 1 of the next block: the previous tile's last window
       {
         uint4 sw[kPwStageLd];
@@ -751,20 +762,20 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
         for (int x = 0; x < kPwStageLd; ++x) stage_put(0, x, sw[x]);
       }
       __syncthreads();  // chunk 0 staged
+      constexpr int kPer = kPwStageLd / kPwMt;  // pieces of the next chunk staged per M-tile
 #pragma unroll
-      for (int c = 0; c < kPsMaxMt / 4; ++c) {
-        if (c < ntg) {  // uniform over the workgroup
+      for (int c = 0; c < kPsMaxMt / kPwMt; ++c) {
+        if (c < nch) {  // uniform over the workgroup
           const uint16_t* ab = wst + (c & 1) * kPwChunk + (lr >> 2) * kPwQuarter + (lr & 3) * kPsPitch + 8 * lg;
-          const bool st_next = c + 1 < ntg;  // then chunk c has all four M-tiles
+          const bool st_next = c + 1 < nch;  // then chunk c has all its M-tiles
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const int mt = 4 * c + k;
+          for (int k = 0; k < kPwMt; ++k) {
+            const int mt = kPwMt * c + k;
             if (mt < nmt) {
-              // the next chunk, two pieces per M-tile
-              uint4 sp0, sp1;
+              uint4 sp[kPer];
               if (st_next) {
-                sp0 = stage_piece(c + 1, 2 * k);
-                sp1 = stage_piece(c + 1, 2 * k + 1);
+#pragma unroll
+                for (int x = 0; x < kPer; ++x) sp[x] = stage_piece(c + 1, kPer * k + x);
               }
               if (score) {
 #pragma unroll
@@ -774,12 +785,14 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
 #pragma unroll
                   for (int ks = 0; ks < 4; ++ks)
                     cc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const uint4*>(ap + 32 * ks)), fb[ks], cc);
-                  // window 4 (bo + u) + e is visible iff it is <= vis: all-ones mask selects -inf
-                  const int d = vis - 4 * (bo + 4 * mt + i);
+                  if (vis_on) {
+                    // window 4 (bo + u) + e is visible iff it is <= vis: all-ones mask selects -inf
+                    const int d = vis - 4 * (bo + 4 * mt + i);
 #pragma unroll
-                  for (int e = 0; e < 4; ++e) {
-                    const uint32_t m = (uint32_t)((d - e) >> 31);
-                    cc[e] = __uint_as_float((m & 0xff800000u) | (~m & __float_as_uint(cc[e])));
+                    for (int e = 0; e < 4; ++e) {
+                      const uint32_t m = (uint32_t)((d - e) >> 31);
+                      cc[e] = __uint_as_float((m & 0xff800000u) | (~m & __float_as_uint(cc[e])));
+                    }
                   }
                   acc[mt][i] = fmaxf(fmaxf(fmaxf(cc[0], cc[1]), fmaxf(cc[2], cc[3])), carry);
                   carry = cc[3];
@@ -789,8 +802,8 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
                 for (int i = 0; i < 4; ++i) acc[mt][i] = -INFINITY;
               }
               if (st_next) {
-                stage_put((c + 1) & 1, 2 * k, sp0);
-                stage_put((c + 1) & 1, 2 * k + 1, sp1);
+#pragma unroll
+                for (int x = 0; x < kPer; ++x) stage_put((c + 1) & 1, kPer * k + x, sp[x]);
               }
             } else {
 #pragma unroll
@@ -800,16 +813,16 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_win_kernel(SelectAr
           __syncthreads();  // chunk c scored everywhere; chunk c + 1 staged
         } else {
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
+          for (int k = 0; k < kPwMt; ++k)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[4 * c + k][i] = -INFINITY;
+            for (int i = 0; i < 4; ++i) acc[kPwMt * c + k][i] = -INFINITY;
         }
       }
     } else if (kOut == 1) {
       __syncthreads();  // the previous group's set rows have left the buffers
     }
     // the next group's F rows, requested after the scoring, whose registers they would crowd
-    load_f(s - kPsWaves, fnext);
+    load_f(s - kPwWaves, fnext);
     if (kOut == 1) forced();  // the buffers are free now
 
     if (score) {
@@ -864,15 +877,15 @@ static void plan_units(const SelectArgs& a, int units, int per_cand, PrefillPlan
   plan->bound[units] = (uint16_t)ns;
 }
 
-// The window-grid kernel scores kPsWaves slices at a time in lockstep: units take whole groups of
-// kPsWaves slices (aligned from slice 0), costed by the group's last slice.
+// The window-grid kernel scores kPwWaves slices at a time in lockstep: units take whole groups of
+// kPwWaves slices (aligned from slice 0), costed by the group's last slice.
 static void plan_unit_groups(const SelectArgs& a, int units, int per_cand, PrefillPlan* plan) {
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
-  const int ng = (ns + kPsWaves - 1) / kPsWaves;
+  const int ng = (ns + kPwWaves - 1) / kPwWaves;
   plan->n_slices = ns;
   plan->units = units;
   auto cost = [&](int gi) -> int64_t {
-    const int s_last = std::min(ns, (gi + 1) * kPsWaves) - 1;
+    const int s_last = std::min(ns, (gi + 1) * kPwWaves) - 1;
     const RowGeom g = row_geom(a.q_pos0 + std::min<int64_t>(a.n_q, (int64_t)(s_last + 1) * kPsRows) - 1, a.n_init,
                                a.n_local, a.k_total);
     if (g.n_take >= g.n_cand) return 40;
@@ -886,7 +899,7 @@ static void plan_unit_groups(const SelectArgs& a, int units, int per_cand, Prefi
   for (int uu = 1; uu < units; ++uu) {
     const int64_t target = total * uu / units;
     while (gi < ng && acc + cost(gi) <= target) acc += cost(gi++);
-    plan->bound[uu] = (uint16_t)std::min(ns, gi * kPsWaves);
+    plan->bound[uu] = (uint16_t)std::min(ns, gi * kPwWaves);
   }
   plan->bound[units] = (uint16_t)ns;
 }
@@ -895,11 +908,12 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int n_groups = a.batch * a.n_kv_heads;
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
   if (ns > 65535) return hipErrorInvalidValue;
-  constexpr int kUnitsTarget = 256;  // one persistent unit per CU
-  int units = n_groups >= kUnitsTarget ? 1 : kUnitsTarget / n_groups;
-  units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
   const bool win = !grid_is_blocks(a.grid);
   if (win && !(a.grid.l == 32 && a.grid.s == 16)) return hipErrorInvalidValue;
+  // persistent units: one per CU for the block grid, two per CU for the window grid
+  const int units_target = win ? 512 : 256;
+  int units = n_groups >= units_target ? 1 : units_target / n_groups;
+  units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
   PrefillPlan plan;
   if (win)
     plan_unit_groups(a, units, 3, &plan);
@@ -908,11 +922,11 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
   if (win && staged)
-    hipLaunchKernelGGL((prefill_select_win_kernel<0>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<0>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
   else if (win && a.k_total <= kPwStageKMax)
-    hipLaunchKernelGGL((prefill_select_win_kernel<1>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<1>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
   else if (win)
-    hipLaunchKernelGGL((prefill_select_win_kernel<2>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<2>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
   else if (staged)
     hipLaunchKernelGGL((prefill_select_kernel<true>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else
