@@ -832,7 +832,9 @@ GRID_PREFILL = [
     (2, 1, 3000, 700, 2300, 12, 2, 1),      # chunk off a block boundary, ragged last slice
     (1, 2, 6000, 333, 5601, 20, 1, 1),      # one local block: edge windows hidden until complete
     (1, 1, 5000, 1000, 4000, 16, 1, 0),     # no initial block: block 0 has no window 4b - 1
-    (1, 2, 8192, 2000, 6192, 96, 2, 1),     # sets longer than 64 entries: written straight out
+    (1, 2, 8192, 2000, 6192, 96, 2, 1),     # sets longer than 64 entries: assembled in the chunk buffers
+    (1, 2, 20000, 500, 19500, 256, 2, 1),   # the longest sets assembled in the chunk buffers
+    (1, 2, 32960, 300, 32660, 300, 2, 1),   # sets past 256 entries: written straight to the output
     (1, 2, 32960, 500, 32460, 64, 2, 1),    # the last row has 512 candidates: the tile kernel's maximum
     (1, 2, 36000, 200, 35800, 64, 2, 1),    # more candidates: the row-wise path (MFMA window scores)
     (1, 1, 70000, 130, 69870, 40, 1, 1),    # 2176 windows per row, one local block: edge windows
@@ -883,7 +885,8 @@ def test_grid_prefill_full_t32k_samples(dev):
     say(f"  sampled {len(rows_r) * len(ms)} rows, tie swaps {swaps}")
 
 
-@pytest.mark.parametrize("T,n_q,k_total,n_local", [(8192, 1024, 16, 2), (20000, 700, 64, 1), (20000, 1, 64, 2)])
+@pytest.mark.parametrize("T,n_q,k_total,n_local", [(8192, 1024, 16, 2), (20000, 700, 64, 1), (20000, 700, 128, 2),
+                                                   (20000, 1, 64, 2)])
 def test_grid_select_exact_ties_take_lowest_index(dev, T, n_q, k_total, n_local):
     """Integer F and window keys: every window score, and so every pooled block score, is an exact
     integer on both sides, and duplicated windows make many blocks tie; the GPU must take the
