@@ -594,15 +594,19 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
 // other's VALU search (a group's wavefronts are otherwise in the same phase).
 // Once a group is scored the chunk buffers are free: each wavefront assembles its slice's sets
 // there (rows of k_total rounded up to 8, plus 8 padding slots) and copies them out with 16-byte
-// stores, for any k_total up to kPwStageKMax; larger sets are written straight to the output.
+// stores, for any k_total up to kPwStageKMax (a barrier before the next group's first staging
+// protects them); larger sets are written straight to the output.
 constexpr int kPwWaves = 4;                         // wavefronts (slices in lockstep) per workgroup
 constexpr int kPwThreads = 64 * kPwWaves;
 constexpr int kPwMt = 2;                            // M-tiles per staged chunk
 constexpr int kPwTiles = 4 * kPwMt;                 // window-tiles per staged chunk
 constexpr int kPwWin = 4 * kPwTiles;                // windows per quarter per chunk
-constexpr int kPwQuarter = kPwWin * kPsPitch + 32;  // uint16 per staged quarter; the extra 64 B put
-                                                    // the 16 rows one A read takes (4 quarters x 4
-                                                    // windows) on distinct banks
+constexpr int kPwPitch = kHeadDim + 16;             // bf16 per staged window row (288 B)
+constexpr int kPwQuarter = kPwWin * kPwPitch + 64;  // uint16 per staged quarter (+128 B): with the
+                                                    // 288-byte rows, the 16 rows one A read takes
+                                                    // (4 quarters x 4 windows) count no LDS bank
+                                                    // conflicts (272-byte rows with a 64-byte
+                                                    // quarter shift count 3.8 cycles per read)
 constexpr int kPwChunk = 4 * kPwQuarter;            // uint16 per chunk buffer
 constexpr int kPwStageLd = 4 * kPwWin * 16 / kPwThreads;  // 16-byte staging pieces per thread
 constexpr int kPwWinPerThr = kPwThreads / 16;       // windows of a quarter covered by one piece index
@@ -611,7 +615,7 @@ static_assert(kPwStageLd == 8 && kPwWin == 2 * kPwWinPerThr,
 static_assert(kPwStageLd % kPwMt == 0, "each M-tile stages the same number of pieces");
 constexpr int kPwStageKMax = 256;                   // largest k_total assembled in LDS
 static_assert(kPwWaves * kPsRows * (kPwStageKMax + 8) <= 2 * kPwChunk, "set rows fit in the chunk buffers");
-static_assert(2 * (2 * kPwChunk * 2 + kPwWaves * kPsRows * kPsOutPitch * 2) <= 160 * 1024, "two workgroups per CU");
+static_assert(2 * (2 * kPwChunk * 2) <= 160 * 1024, "two workgroups per CU");
 
 __host__ __device__ inline int pw_out_pitch(int k_total) { return ((k_total + 7) & ~7) + 8; }
 
@@ -635,22 +639,19 @@ __device__ __forceinline__ void copy_out_rows(const SelectArgs& a, int64_t bm, i
   }
 }
 
-// kOut: where a slice's sets are assembled.  0: LDS rows of their own (k_total <= kPsStageK; the
-// copy-out of one slice waits until the next group has been scored), 1: the chunk buffers (after
-// the group is scored; k_total <= kPwStageKMax), 2: straight to the output.
-template <int kOut>
+// kStaged: a slice's sets are assembled in the chunk buffers once the group is scored (k_total <=
+// kPwStageKMax); otherwise they go straight to the output.
+template <bool kStaged>
 __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
-  constexpr bool kStaged = kOut != 2;
   __shared__ __align__(16) uint16_t wst[2 * kPwChunk];
-  __shared__ __align__(16) int16_t ost_all[kOut == 0 ? kPwWaves * kPsRows * kPsOutPitch : 8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
   const int s_begin = plan.bound[u], s_end = plan.bound[u + 1];
   if (s_begin >= s_end) return;
   const int lr = lane & 15, lg = lane >> 4;
-  const int opitch = kOut == 0 ? kPsOutPitch : pw_out_pitch(a.k_total);
-  int16_t* ost = (kOut == 0 ? ost_all : reinterpret_cast<int16_t*>(wst)) + wave * kPsRows * opitch;  // set rows
+  const int opitch = pw_out_pitch(a.k_total);
+  int16_t* ost = reinterpret_cast<int16_t*>(wst) + wave * kPsRows * opitch;  // this wavefront's set rows
   const uint16_t* kcg = a.kc + bm * a.nc_cap * kHeadDim;  // the group's window keys
   auto load_f = [&](int s, uint4 (&fw)[4]) {
     const int r = s * kPsRows + lr;
@@ -666,7 +667,6 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
 
   uint4 fnext[4];
   load_f(s_end - 1 - wave, fnext);
-  int s_prev = -1;  // kOut 0: the slice whose sets still wait in LDS
   // Groups from the end of the range (most candidates first); wavefront w takes slice g_hi - 1 - w.
   for (int g_hi = s_end; g_hi > s_begin; g_hi -= kPwWaves) {
     const int s = g_hi - 1 - wave;
@@ -674,10 +674,6 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
     uint4 fw[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
-    if (kOut == 0 && s_prev >= 0) {
-      wave_lds_sync();
-      copy_out_rows(a, bm, s_prev, ost, opitch, lane);
-    }
 
     const int r = s * kPsRows + lr;
     const bool row_ok = have && r < a.n_q;
@@ -705,7 +701,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
           for (int i = lg; i < g.n_cand; i += 4) out[g.init_hi + i] = (int16_t)(g.cand_lo + i);
       }
     };
-    if (kOut != 1) forced();
+    if (!kStaged) forced();
 
     const int nmt = (gg.n_cand + 15) >> 4;  // uniform over the workgroup
     const int ntg = (nmt + 3) >> 2;         // groups of 4 M-tiles the search's slot loops run over
@@ -732,7 +728,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
       };
       auto stage_put = [&](int b, int x, uint4 val) {
         const int q = x >> 1, w = st_w + kPwWinPerThr * (x & 1);
-        *reinterpret_cast<uint4*>(wst + b * kPwChunk + q * kPwQuarter + w * kPsPitch + st_part * 8) = val;
+        *reinterpret_cast<uint4*>(wst + b * kPwChunk + q * kPwQuarter + w * kPwPitch + st_part * 8) = val;
       };
       bf16x8 fb[4];
 #pragma unroll
@@ -757,7 +753,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
           for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(ld16(pa + 32 * ks)), fb[ks], c);
           carry = 4 * bo - 1 >= 0 ? c[3] : -INFINITY;  // window 4 bo - 1 exists unless bo = 0
         }
-        if (kOut == 1) __syncthreads();  // the previous group's set rows have left the buffers
+        if (kStaged) __syncthreads();  // the previous group's set rows have left the buffers
 #pragma unroll
         for (int x = 0; x < kPwStageLd; ++x) stage_put(0, x, sw[x]);
       }
@@ -766,7 +762,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
 #pragma unroll
       for (int c = 0; c < kPsMaxMt / kPwMt; ++c) {
         if (c < nch) {  // uniform over the workgroup
-          const uint16_t* ab = wst + (c & 1) * kPwChunk + (lr >> 2) * kPwQuarter + (lr & 3) * kPsPitch + 8 * lg;
+          const uint16_t* ab = wst + (c & 1) * kPwChunk + (lr >> 2) * kPwQuarter + (lr & 3) * kPwPitch + 8 * lg;
           const bool st_next = c + 1 < nch;  // then chunk c has all its M-tiles
 #pragma unroll
           for (int k = 0; k < kPwMt; ++k) {
@@ -780,7 +776,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
               if (score) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                  const uint16_t* ap = ab + 4 * (4 * k + i) * kPsPitch;  // window-tile 4 k + i of the chunk
+                  const uint16_t* ap = ab + 4 * (4 * k + i) * kPwPitch;  // window-tile 4 k + i of the chunk
                   f32x4 cc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                   for (int ks = 0; ks < 4; ++ks)
@@ -818,12 +814,12 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
             for (int i = 0; i < 4; ++i) acc[kPwMt * c + k][i] = -INFINITY;
         }
       }
-    } else if (kOut == 1) {
+    } else if (kStaged) {
       __syncthreads();  // the previous group's set rows have left the buffers
     }
     // the next group's F rows, requested after the scoring, whose registers they would crowd
     load_f(s - kPwWaves, fnext);
-    if (kOut == 1) forced();  // the buffers are free now
+    if (kStaged) forced();  // the buffers are free now
 
     if (score) {
       // Key slots past the row's candidates (the last lane group's tail, rows with fewer
@@ -838,15 +834,10 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
       }
       search_emit<kStaged>(acc, nmt, ntg, Q, v, n, Cr, search, lg, g, out, out + opitch - 8 + lg);
     }
-    if (kOut == 1 && have) {
+    if (kStaged && have) {
       wave_lds_sync();
       copy_out_rows(a, bm, s, ost, opitch, lane);
     }
-    if (kOut == 0) s_prev = have ? s : -1;
-  }
-  if (kOut == 0 && s_prev >= 0) {
-    wave_lds_sync();
-    copy_out_rows(a, bm, s_prev, ost, opitch, lane);
   }
 }
 
@@ -921,12 +912,10 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
     plan_units(a, units, 1, &plan);
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
-  if (win && staged)
-    hipLaunchKernelGGL((prefill_select_win_kernel<0>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
-  else if (win && a.k_total <= kPwStageKMax)
-    hipLaunchKernelGGL((prefill_select_win_kernel<1>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
+  if (win && a.k_total <= kPwStageKMax)
+    hipLaunchKernelGGL((prefill_select_win_kernel<true>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
   else if (win)
-    hipLaunchKernelGGL((prefill_select_win_kernel<2>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
+    hipLaunchKernelGGL((prefill_select_win_kernel<false>), grid, dim3(kPwThreads), 0, stream, a, plan, n_groups);
   else if (staged)
     hipLaunchKernelGGL((prefill_select_kernel<true>), grid, dim3(kPsThreads), 0, stream, a, plan, n_groups);
   else
