@@ -30,12 +30,20 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kAttnWaves = 8;        // wavefronts per attention workgroup
 constexpr int kRowsFillChip = 256;   // rows at which one workgroup per row fills 256 CUs
 constexpr int kMaxSplits = 64;
+constexpr int kKstPitch = kHeadDim + 16;  // uint16 per staged K row (288 B)
 
 template <int G, int NW>
 __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
+  // K of the wavefront's current block, transposed through LDS: read from HBM as 1 KiB rows of 4
+  // tokens (the access pattern streams faster than 16 token rows x 64 bytes), stored at a
+  // 288-byte row pitch whose A-operand reads (16 rows x 4 chunks) count no bank conflicts.  The
+  // merge of the wavefront states reuses this space after the loop.
+  __shared__ __align__(16) uint16_t kst[NW][kBlock * kKstPitch];
   __shared__ __align__(16) float p_lds[NW][64][G];
   __shared__ float st_m[NW][G], st_l[NW][G];
-  __shared__ __align__(16) float st_acc[NW][G][kHeadDim];
+  static_assert(sizeof(float) * G * kHeadDim <= sizeof(uint16_t) * kBlock * kKstPitch, "a wavefront's merge state fits in its K slice");
+  // wavefront w's (G x kHeadDim) partial output, in its own K slice once its blocks are done
+  auto st_acc = [&](int w) { return reinterpret_cast<float (*)[kHeadDim]>(&kst[w][0]); };
   const int64_t row = blockIdx.x;
   const int split = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -87,21 +95,26 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
       base = ((bm * a.k_total + s) * kBlock) * kHeadDim;
     const uint16_t* kb = a.k + base;
     const uint16_t* vb = a.v + base;
-    uint4 kw[4][4];
+    uint4 kw[16];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) kw[tt][ks] = ld16_nt(kb + (16 * tt + hh) * kHeadDim + 32 * ks + 8 * grp);
+    for (int it = 0; it < 16; ++it) kw[it] = ld16_nt(kb + (4 * it + grp) * kHeadDim + 8 * hh);
     uint4 vw[16];
 #pragma unroll
     for (int it = 0; it < 16; ++it) vw[it] = ld16_nt(vb + (4 * it + grp) * kHeadDim + 8 * hh);
+    uint16_t* ks_w = &kst[wave][0];
+#pragma unroll
+    for (int it = 0; it < 16; ++it) *reinterpret_cast<uint4*>(ks_w + (4 * it + grp) * kKstPitch + 8 * hh) = kw[it];
+    wave_lds_sync();
 
     f32x4 st[4];
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
       st[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) st[tt] = mfma16x16x32(as_bf16x8(kw[tt][ks]), qb[ks], st[tt]);
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 kf = *reinterpret_cast<const uint4*>(ks_w + (16 * tt + hh) * kKstPitch + 32 * ks + 8 * grp);
+        st[tt] = mfma16x16x32(as_bf16x8(kf), qb[ks], st[tt]);
+      }
     }
     // lane holds S^T[token 16 tt + 4 grp + i][head hh]
     const int last = (j == blk) ? (int)(p - (int64_t)j * kBlock) : kBlock - 1;
@@ -174,7 +187,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) st_acc[wave][h][8 * lane + e] = acc[h][e];
+      for (int e = 0; e < 8; ++e) st_acc(wave)[h][8 * lane + e] = acc[h][e];
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < G * kHeadDim; idx += NW * 64) {
@@ -190,7 +203,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
         if (mw != -INFINITY) {
           const float sc = exp2f(mw - M);
           L = fmaf(st_l[w][h], sc, L);
-          A = fmaf(st_acc[w][h][d], sc, A);
+          A = fmaf(st_acc(w)[h][d], sc, A);
         }
       }
     }
