@@ -77,31 +77,59 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
 
   const int16_t* srow = a.sel + row * a.k_total;
   // The attended tokens are a union of blocks: an entry whose block an earlier entry of the row
-  // already lists is skipped.  Lane e holds entry e (e < 64) for that test.
+  // already lists is skipped.  Lane e holds entry e (e < 64): the walk reads entries below 64 from
+  // it, so it issues no loads of its own between the blocks' loads.
   const int entry = lane < n ? (int)srow[lane] : -1;
-  for (int s = s_begin + wave; s < s_end; s += NW) {
-    const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
-    if (j < 0 || j > blk) continue;
-    bool dup = __ballot(lane < s && entry == j) != 0ull;
-    for (int e0 = 64; e0 < s; e0 += 64) {
-      const int e = e0 + lane;
-      dup |= __ballot(e < s && (int)srow[e] == j) != 0ull;
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the query and the entries are in registers
+  // First entry at or after s (stepping by NW) that names a visible block no earlier entry names;
+  // *jo gets its block.  Returns a value >= s_end when there is none.
+  auto next_block = [&](int s, int* jo) {
+    for (; s < s_end; s += NW) {
+      const int j = s < 64 ? __builtin_amdgcn_readlane(entry, s) : __builtin_amdgcn_readfirstlane((int)srow[s]);
+      if (j < 0 || j > blk) continue;
+      bool dup = __ballot(lane < s && entry == j) != 0ull;
+      for (int e0 = 64; e0 < s; e0 += 64) {
+        const int e = e0 + lane;
+        dup |= __ballot(e < s && (int)srow[e] == j) != 0ull;
+      }
+      if (!dup) {
+        *jo = j;
+        return s;
+      }
     }
-    if (dup) continue;
-    int64_t base;
-    if (a.kv_mode == 0)
-      base = (bm * a.t_cap + (int64_t)j * kBlock) * kHeadDim;
-    else
-      base = ((bm * a.k_total + s) * kBlock) * kHeadDim;
-    const uint16_t* kb = a.k + base;
-    const uint16_t* vb = a.v + base;
-    uint4 kw[16];
+    return s;
+  };
+  auto kv_base = [&](int s, int j) -> int64_t {
+    return a.kv_mode == 0 ? (bm * a.t_cap + (int64_t)j * kBlock) * kHeadDim : ((bm * a.k_total + s) * kBlock) * kHeadDim;
+  };
+  // Rows of 4 tokens, 1 KiB per wavefront load, for K and V alike.  K pieces [lo, hi).
+  uint4 kw[16], vw[16];
+  auto load_k = [&](int64_t base, int lo, int hi) {
 #pragma unroll
-    for (int it = 0; it < 16; ++it) kw[it] = ld16_nt(kb + (4 * it + grp) * kHeadDim + 8 * hh);
-    uint4 vw[16];
+    for (int it = 0; it < 16; ++it)
+      if (it >= lo && it < hi) kw[it] = ld16_nt(a.k + base + (4 * it + grp) * kHeadDim + 8 * hh);
+  };
+  auto load_v = [&](int64_t base) {
 #pragma unroll
-    for (int it = 0; it < 16; ++it) vw[it] = ld16_nt(vb + (4 * it + grp) * kHeadDim + 8 * hh);
-    uint16_t* ks_w = &kst[wave][0];
+    for (int it = 0; it < 16; ++it) vw[it] = ld16_nt(a.v + base + (4 * it + grp) * kHeadDim + 8 * hh);
+  };
+  uint16_t* ks_w = &kst[wave][0];
+  // Software pipeline over the wavefront's blocks: the first half of the next block's K is
+  // requested as soon as the current K has gone through the MFMAs (its registers are free once the
+  // K is in the LDS slice), so the wavefront has loads in flight while it computes; the rest of
+  // that K and its V follow at the top of the next iteration (all of it would not fit beside V).
+  constexpr int kKAhead = 4;  // K pieces requested one block ahead
+  int j = 0;
+  int s = next_block(s_begin + wave, &j);
+  if (s < s_end) load_k(kv_base(s, j), 0, kKAhead);
+  while (s < s_end) {
+    int jn = 0;
+    const int sn = next_block(s + NW, &jn);
+    const int64_t base = kv_base(s, j);
+    const int64_t base_n = sn < s_end ? kv_base(sn, jn) : 0;
+    load_k(base, kKAhead, 16);
+    load_v(base);
+    wave_lds_sync();  // the previous block's K reads are done
 #pragma unroll
     for (int it = 0; it < 16; ++it) *reinterpret_cast<uint4*>(ks_w + (4 * it + grp) * kKstPitch + 8 * hh) = kw[it];
     wave_lds_sync();
@@ -116,6 +144,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
         st[tt] = mfma16x16x32(as_bf16x8(kf), qb[ks], st[tt]);
       }
     }
+    if (sn < s_end) load_k(base_n, 0, kKAhead);
     // lane holds S^T[token 16 tt + 4 grp + i][head hh]
     const int last = (j == blk) ? (int)(p - (int64_t)j * kBlock) : kBlock - 1;
     float z[4][4];
@@ -168,6 +197,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
         for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr[h], v8[e], acc[h][e]);
     }
     wave_lds_sync();
+    s = sn;
+    j = jn;
   }
   // Sum the four token phases of each head-dim chunk.
 #pragma unroll
