@@ -87,6 +87,7 @@ class DecodeLayer:
         self.o = torch.empty(w.batch, w.n_q_heads, 1, 128, dtype=torch.bfloat16, device=dev)
         self.ws_sel = ws_tensor(self.shape, sp.SPARDA_OP_FORECAST_SELECT, 1, T - 1, dev)
         self.ws_att = ws_tensor(self.shape, sp.SPARDA_OP_SPARSE_ATTN, 1, T - 1, dev)
+        self.ws_step = ws_tensor(self.shape, sp.SPARDA_OP_DECODE_STEP, 1, T - 1, dev)
         # K~ of every complete window is precomputed (not timed); the step refreshes the newest one.
         sp.sparda_compress_keys(self.shape, self.k, T, 0, self.nw, self.kc)
         torch.cuda.synchronize()
@@ -102,13 +103,18 @@ class DecodeLayer:
                               self.ws_att)
 
     def step(self):
+        """Select + attention: one fused launch where both run one workgroup per row (the 128K B32
+        layer), the two calls otherwise."""
+        sp.sparda_decode_step(self.shape, self.f, self.T - 1, self.kc, self.q, self.k, self.v, SCALE, self.sel,
+                              self.cnt, self.o, self.ws_step)
+
+    def step_separate(self):
         self.select()
         self.attend()
 
     def step_with_refresh(self):
         self.compress_new()
-        self.select()
-        self.attend()
+        self.step()
 
     def bytes(self):
         """Algorithmic HBM bytes of the step's parts (compress_new is the separate K~ refresh).
@@ -907,15 +913,26 @@ def main():
     ms_step = wall * 1e3 / args.steps
     parts = layer.bytes()
     step_bytes = parts["select"] + parts["attend"]
-    log(f"[bench] decode step {ms_step * 1e3:.1f} us")
+    log(f"[bench] decode step {ms_step * 1e3:.1f} us (one fused launch)")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         layer.step_with_refresh()
     torch.cuda.synchronize()
     ms_step_refresh = (time.perf_counter() - t0) * 1e3 / args.steps
+    # the same step as two calls (select, then attention), timed the same way
+    for _ in range(args.warmup):
+        layer.step_separate()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        layer.step_separate()
+    torch.cuda.synchronize()
+    ms_sep = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # per-call event timing (the dominant kernel is the attention)
+    # per-call event timing: the step is one launch of the fused kernel, the dominant (only) kernel;
+    # the select and attention calls alone for context
+    ms_launch = time_events(layer.step, args.steps, stream)
     ms_sel = time_events(layer.select, args.steps, stream)
     ms_att = time_events(layer.attend, args.steps, stream)
     ms_cmp = time_events(layer.compress_new, args.steps, stream)
@@ -924,10 +941,12 @@ def main():
     step_stats = {"step": rep_stats(layer.step, args.reps, stream, flush),
                   "select": rep_stats(layer.select, args.reps, stream, flush),
                   "attend": rep_stats(layer.attend, args.reps, stream, flush)}
+    log(f"[bench] the same step as two calls: {ms_sep * 1e3:.1f} us")
     log(f"[bench] decode step after a cache flush: median {step_stats['step']['median_ms'] * 1e3:.1f} us "
         f"(p10 {step_stats['step']['p10_ms'] * 1e3:.1f}, p90 {step_stats['step']['p90_ms'] * 1e3:.1f})")
     att_bytes = parts["attend"]
-    achieved = att_bytes / (ms_att * 1e-3) / 1e9
+    achieved = step_bytes / (ms_launch * 1e-3) / 1e9
+    achieved_att = att_bytes / (ms_att * 1e-3) / 1e9
     out = {
         "metric": METRIC,
         "value": step_bytes / (ms_step * 1e-3) / 1e9,
@@ -949,12 +968,17 @@ def main():
         "frac_hbm_peak": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_bytes": step_bytes,
         "parts_us": {"compress_new": ms_cmp * 1e3, "select": ms_sel * 1e3, "attend": ms_att * 1e3},
-        "roofline": {"bound": "hbm", "kernel": "sparse_attn_kernel<4, 8> (decode, one workgroup per row)",
+        "us_per_layer_separate_calls": ms_sep * 1e3,
+        "roofline": {"bound": "hbm", "kernel": "decode_step_kernel<4, 8> (select + attention of a decode row in "
+                                               "one workgroup, one launch per step)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": counted_traffic("sparse_attn_kernel<4, 8>"),
-                     "algorithmic_bytes_per_launch": att_bytes, "avg_launch_ms": ms_att,
+                     "traffic": counted_traffic("decode_step_kernel<4, 8>"),
+                     "algorithmic_bytes_per_launch": step_bytes, "avg_launch_ms": ms_launch,
                      "measured_peak": peaks["hbm_block_read_GBps"],
                      "frac_measured_peak": achieved / peaks["hbm_block_read_GBps"]},
+        "attention_alone": {"kernel": "sparse_attn_kernel<4, 8>", "avg_launch_ms": ms_att, "achieved_GBps": achieved_att,
+                            "frac": achieved_att / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": att_bytes,
+                            "traffic": counted_traffic("sparse_attn_kernel<4, 8>")},
         "peaks": peaks,
         "frac_measured_read_peak": step_bytes / (ms_step * 1e-3) / 1e9 / peaks["hbm_block_read_GBps"],
         "flushed_stats": step_stats,

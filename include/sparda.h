@@ -14,6 +14,9 @@
  *   sparda_sparse_attn      Q, K, V, sets -> O    (Sec. 4.1, Eq. 5 with Eq. 1)
  *   sparda_sparse_attn_noalloc  the same without a workspace argument (a static scratch array),
  *                           for callers that cannot allocate
+ *   sparda_decode_step      F, K~, Q, K, V -> block sets and O: one decode step of a layer, the
+ *                           select and the attention in one launch where they fit one workgroup
+ *                           per row (Sec. 4.1, Eq. 4 then Eq. 5, with Eq. 1)
  *   sparda_multihead_select Q, K~ -> block sets   (the InfLLM-V2 selector of Sec. 3 that the
  *                           Forecast indexer replaces; a baseline)
  *   sparda_gather_blocks    host KV pool -> HBM staging of the selected blocks, meant for a side
@@ -96,7 +99,8 @@ enum sparda_op {
   SPARDA_OP_FORECAST_SELECT = 1,
   SPARDA_OP_SPARSE_ATTN = 2,
   SPARDA_OP_MULTIHEAD_SELECT = 3,
-  SPARDA_OP_INDEXER_KL = 4
+  SPARDA_OP_INDEXER_KL = 4,
+  SPARDA_OP_DECODE_STEP = 5
 };
 
 /*
@@ -200,6 +204,29 @@ int sparda_multihead_select(const sparda_shape* shape, const void* q, int32_t n_
 int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k,
                        const void* v, int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale,
                        void* o, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sparda_decode_step -- one decode step of a layer (n_q == 1, full K/V caches): the Forecast
+ * selection of every (batch, group) row (Sec. 4.1, Eq. 4 with Eq. 1) followed by the block-sparse
+ * attention over the selected sets (Eq. 5).  The results are those of
+ *     sparda_forecast_select(shape, f, 1, q_pos, k_cmp, sel, cnt, ws, ws_bytes, stream);
+ *     sparda_sparse_attn(shape, q, 1, q_pos, k, v, 0, sel, cnt, sm_scale, o, ws, ws_bytes, stream);
+ * bit for bit.  Where both calls would run one workgroup per row (at least as many rows as the
+ * chip has CUs, the selection's scores fit its LDS, G <= 5) one kernel does both per row, so
+ * that rows that finish their selection early already stream their K and V while others
+ * select; otherwise it enqueues the two calls.
+ *   f, k_cmp   : as for sparda_forecast_select with n_q = 1; q_pos is the row's position.
+ *   q, k, v    : as for sparda_sparse_attn with n_q = 1 and kv_mode 0.
+ *   sm_scale   : logit scale, finite.
+ *   sel, cnt out: the sets, as sparda_forecast_select writes them.
+ *   o      out : bf16 [B][Hq][1][D] device.
+ *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_DECODE_STEP, n_q = 1)
+ *                (0 bytes where the fused kernel runs).
+ * Errors: those of the two calls, all reported before anything is enqueued.
+ */
+int sparda_decode_step(const sparda_shape* shape, const void* f, int64_t q_pos, const void* k_cmp, const void* q,
+                       const void* k, const void* v, float sm_scale, int16_t* sel, int16_t* cnt, void* o, void* ws,
+                       size_t ws_bytes, hipStream_t stream);
 
 /*
  * sparda_sparse_attn_noalloc -- sparda_sparse_attn without a workspace argument, for callers that

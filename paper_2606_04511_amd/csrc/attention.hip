@@ -23,6 +23,7 @@
 
 #include "device_util.hpp"
 #include "launch.hpp"
+#include "select_block.hpp"
 
 namespace sparda {
 
@@ -32,20 +33,28 @@ constexpr int kRowsFillChip = 256;   // rows at which one workgroup per row fill
 constexpr int kMaxSplits = 64;
 constexpr int kKstPitch = kHeadDim + 16;  // uint16 per staged K row (288 B)
 
+// LDS of one attention workgroup.  kst: K of each wavefront's current block, transposed through
+// LDS: read from HBM as 1 KiB rows of 4 tokens (the access pattern streams faster than 16 token
+// rows x 64 bytes), stored at a 288-byte row pitch whose A-operand reads (16 rows x 4 chunks)
+// count no bank conflicts.  The merge of the wavefront states reuses this space after the loop.
 template <int G, int NW>
-__global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
-  // K of the wavefront's current block, transposed through LDS: read from HBM as 1 KiB rows of 4
-  // tokens (the access pattern streams faster than 16 token rows x 64 bytes), stored at a
-  // 288-byte row pitch whose A-operand reads (16 rows x 4 chunks) count no bank conflicts.  The
-  // merge of the wavefront states reuses this space after the loop.
-  __shared__ __align__(16) uint16_t kst[NW][kBlock * kKstPitch];
-  __shared__ __align__(16) float p_lds[NW][64][G];
-  __shared__ float st_m[NW][G], st_l[NW][G];
+struct AttnLds {
+  uint16_t kst[NW][kBlock * kKstPitch];
+  float p_lds[NW][64][G];
+  float st_m[NW][G], st_l[NW][G];
+};
+
+// Attention of query row `row`, split `split` of its block list, by a workgroup of NW
+// wavefronts (every thread must call it).
+template <int G, int NW>
+__device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int split, AttnLds<G, NW>& L) {
+  auto& kst = L.kst;
+  auto& p_lds = L.p_lds;
+  auto& st_m = L.st_m;
+  auto& st_l = L.st_l;
   static_assert(sizeof(float) * G * kHeadDim <= sizeof(uint16_t) * kBlock * kKstPitch, "a wavefront's merge state fits in its K slice");
   // wavefront w's (G x kHeadDim) partial output, in its own K slice once its blocks are done
   auto st_acc = [&](int w) { return reinterpret_cast<float (*)[kHeadDim]>(&kst[w][0]); };
-  const int64_t row = blockIdx.x;
-  const int split = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = (int)(row % a.n_q);
   const int64_t bm = row / a.n_q;
@@ -118,7 +127,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
   // requested as soon as the current K has gone through the MFMAs (its registers are free once the
   // K is in the LDS slice), so the wavefront has loads in flight while it computes; the rest of
   // that K and its V follow at the top of the next iteration (all of it would not fit beside V).
-  constexpr int kKAhead = 4;  // K pieces requested one block ahead
+  constexpr int kKAhead = G <= 4 ? 4 : 0;  // K pieces requested one block ahead (none above 4 heads: they would spill)
   int j = 0;
   int s = next_block(s_begin + wave, &j);
   if (s < s_end) load_k(kv_base(s, j), 0, kKAhead);
@@ -249,6 +258,32 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
       pp[2 + d] = A;
     }
   }
+}
+
+template <int G, int NW>
+__global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
+  __shared__ __align__(16) AttnLds<G, NW> lds;
+  attend_row<G, NW>(a, blockIdx.x, blockIdx.y, lds);
+}
+
+// One decode step of a (batch, group) row in one workgroup: the row's Forecast selection
+// (Sec. 4.1, Eq. 4 with Eq. 1), written to s.sel and s.cnt, then its sparse attention over that
+// set (Eq. 5).  The selection's scores live in the K slices and its histogram in the P space,
+// both free until the attention starts.  Rows finish their selection at different times, so some
+// rows' attention loads already run while others select: the HBM stays busier than with a
+// selection kernel followed by an attention kernel.
+template <int G, int NW>
+__global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, AttnArgs a) {
+  static_assert(NW * 64 == kDecThreads, "the selection runs on the attention workgroup");
+  static_assert(sizeof(float) * kDecodeMaxCand <= sizeof(uint16_t) * NW * kBlock * kKstPitch, "scores fit in the K slices");
+  static_assert(sizeof(uint32_t) * kTopkLds <= sizeof(float) * NW * 64 * G, "the top-k histogram fits in the P space");
+  __shared__ __align__(16) AttnLds<G, NW> lds;
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  decode_select_row(s, blockIdx.x, reinterpret_cast<float*>(&lds.kst[0][0]), reinterpret_cast<uint32_t*>(&lds.p_lds[0][0][0]),
+                    wave_cnt, pick);
+  __syncthreads();  // the row's set is in a.sel / a.cnt, and the LDS is free
+  attend_row<G, NW>(a, blockIdx.x, 0, lds);
 }
 
 // Decode attention for groups of 7 to 16 heads: P V on MFMA.  With this many query rows per
@@ -517,6 +552,32 @@ static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
   if (e != hipSuccess || a.n_splits == 1) return e;
   hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)(rows * G)), dim3(128), 0, stream, a);
   return hipGetLastError();
+}
+
+template <int G>
+static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves>), dim3((unsigned)((int64_t)a.batch * a.n_kv_heads)),
+                     dim3(kAttnWaves * 64), 0, stream, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
+  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.n_splits == 1 && a.group_size <= 5 &&
+                     select_is_fused_decode(rows, 1, s.q_pos0, s.n_init, s.n_local, s.grid);
+  if (fused) {
+    switch (a.group_size) {
+      case 1: return launch_step_g<1>(s, a, stream);
+      case 2: return launch_step_g<2>(s, a, stream);
+      case 3: return launch_step_g<3>(s, a, stream);
+      case 4: return launch_step_g<4>(s, a, stream);
+      case 5: return launch_step_g<5>(s, a, stream);
+      default: break;
+    }
+  }
+  hipError_t e = launch_select(s, stream);
+  if (e != hipSuccess) return e;
+  return launch_sparse_attn(a, stream);
 }
 
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream) {

@@ -114,6 +114,27 @@ __device__ __forceinline__ uint32_t row16_max(uint32_t x) {
   return x;
 }
 
+__device__ __forceinline__ uint32_t row16_min(uint32_t x) {
+  x = min(x, (uint32_t)dpp_i<0x128>((int)x));  // row_ror:8
+  x = min(x, (uint32_t)dpp_i<0x124>((int)x));  // row_ror:4
+  x = min(x, (uint32_t)dpp_i<0x122>((int)x));  // row_ror:2
+  x = min(x, (uint32_t)dpp_i<0x121>((int)x));  // row_ror:1
+  return x;
+}
+
+// Inclusive prefix sum over the wavefront on DPP: row_shr 1, 2, 4, 8 inside each 16-lane row
+// (lanes shifted in from outside the row add 0), then row_bcast:15 adds row r's last lane to row
+// r + 1 (rows 1 and 3), and row_bcast:31 adds lane 31 to rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan_dpp(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2 and 3
+  return x;
+}
+
 // Exclusive prefix sum within each 16-lane row; sub = lane index inside the row.
 __device__ __forceinline__ int row16_excl_scan(int x, int sub) {
   int incl = x;

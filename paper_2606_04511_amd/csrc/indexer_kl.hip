@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kDecThreads) void kl_row_kernel(KlArgs a) {
   float* Pp = kl_lds + a.lds_pos;
   int16_t* idx = reinterpret_cast<int16_t*>(Pp + a.lds_pos);
   uint8_t* chosen = reinterpret_cast<uint8_t*>(idx + a.lds_top);
-  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
   __shared__ float red[kDecThreads / 64];

@@ -111,6 +111,8 @@ __host__ __device__ inline void row_windows(const RowGeom& g, const WinGrid& w, 
 // calls with fewer rows than CUs (scored by many workgroups per row).
 bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+// True when a select call runs the fused decode kernel (one workgroup per row, scores in LDS).
+bool select_is_fused_decode(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
 
@@ -142,6 +144,10 @@ hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream);
 // Split count and blocks per split the attention launcher uses for `rows` query rows.
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
+// One decode step: the select call s, then the attention call a over the sets it writes.  One
+// fused kernel (decode_step_kernel) where both would run one workgroup per row (the fused
+// decode select, unsplit attention with G <= 5, full caches); otherwise the two launches.
+hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream);
 // True when a multi-row call takes the tiled kernel (attention_prefill.hip), which needs no
 // workspace: at least 16 rows, 16 % G == 0, and the tile's row bitmaps fit in LDS.
 bool attn_uses_tiles(int32_t group_size, int32_t n_q, int64_t q_pos0);

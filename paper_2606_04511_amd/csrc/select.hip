@@ -14,82 +14,13 @@
 //    wavefront per row that finds the exact k-th key by an 8-bit-digit radix select over a
 //    wave-private LDS histogram and emits the chosen indices in ascending order with ballots.
 //  * fused decode (one row per (batch, group), <= 16384 candidates): one workgroup per row keeps
-//    the row's scores in LDS and runs a block-wide radix select there.
+//    the row's scores in LDS and runs the block-wide top-k there (select_block.hpp).
 //  * fused tile (multi-row prefill with <= 512 candidates per 64-row tile): select_prefill.hip.
 #include "device_util.hpp"
 #include "launch.hpp"
 #include "select_block.hpp"
 
 namespace sparda {
-
-// One wavefront selects the n_take largest keys among n_cand candidates (ties: lower index) and
-// writes their indices cand_lo + i in ascending order to out[0 .. n_take).  key_of(i) returns
-// score_key of candidate i.  hist: 256 uint32 of wave-private, 16-byte aligned LDS.
-template <class KeyFn>
-__device__ void wave_topk_emit(KeyFn key_of, int n_cand, int n_take, int cand_lo, uint32_t* hist, int16_t* out) {
-  const int lane = threadIdx.x & (kWave - 1);
-  if (n_take >= n_cand) {
-    for (int i = lane; i < n_cand; i += kWave) out[i] = (int16_t)(cand_lo + i);
-    return;
-  }
-  if (n_take <= 0) return;
-  uint32_t prefix = 0u, mask = 0u;
-  int remaining = n_take;  // still to take among keys that match `prefix` under `mask`
-  bool take_all = false;
-  for (int pass = 0; pass < 4 && !take_all; ++pass) {
-    const int shift = 24 - 8 * pass;
-    reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
-    wave_lds_sync();
-    for (int i = lane; i < n_cand; i += kWave) {
-      const uint32_t kk = key_of(i);
-      if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> shift) & 255u], 1u);
-    }
-    wave_lds_sync();
-    // Lane l owns digits 255-4l (h.w) down to 252-4l (h.x): a descending scan over lanes.
-    const uint4 h = reinterpret_cast<const uint4*>(hist)[63 - lane];
-    const int lsum = (int)(h.x + h.y + h.z + h.w);
-    const int incl = wave_incl_scan(lsum);
-    const int excl = incl - lsum;
-    const uint64_t hit = __ballot(excl < remaining && remaining <= incl);
-    const int src = hit ? (int)__builtin_ctzll(hit) : 0;  // exactly one lane holds the k-th key
-    int above = excl, d = 255 - 4 * lane, eq = (int)h.w;
-    if (above + (int)h.w < remaining) {
-      above += (int)h.w; d -= 1; eq = (int)h.z;
-      if (above + (int)h.z < remaining) {
-        above += (int)h.z; d -= 1; eq = (int)h.y;
-        if (above + (int)h.y < remaining) { above += (int)h.y; d -= 1; eq = (int)h.x; }
-      }
-    }
-    above = readlane_i(above, src);
-    d = readlane_i(d, src);
-    eq = readlane_i(eq, src);
-    remaining -= above;
-    prefix |= (uint32_t)d << shift;
-    mask |= 0xffu << shift;
-    take_all = (eq == remaining);
-    wave_lds_sync();
-  }
-  int base = 0, tie_base = 0;
-  for (int i0 = 0; i0 < n_cand; i0 += kWave) {
-    const int i = i0 + lane;
-    const bool valid = i < n_cand;
-    const uint32_t kk = valid ? key_of(i) : 0u;
-    bool chosen;
-    if (take_all) {
-      chosen = valid && (kk & mask) >= prefix;
-    } else {  // prefix is the exact k-th key; equal keys go to the lowest indices
-      const bool tie = valid && kk == prefix;
-      const uint64_t tb = __ballot(tie);
-      const int trank = tie_base + mbcnt64(tb);
-      tie_base += __popcll(tb);
-      chosen = valid && (kk > prefix || (tie && trank < remaining));
-    }
-    const uint64_t cb = __ballot(chosen);
-    const int pos = base + mbcnt64(cb);
-    if (chosen && pos < n_take) out[pos] = (int16_t)(cand_lo + i);  // never past the row's slots
-    base += __popcll(cb);
-  }
-}
 
 // ---- row-wise path ----------------------------------------------------------------------
 
@@ -187,89 +118,14 @@ __global__ __launch_bounds__(256) void rowwise_topk_kernel(SelectArgs a, int64_t
 
 // One workgroup per decode row (batch, group): the Forecast GEMV over all scored windows into LDS,
 // the max-pool of window scores to block scores (skipped for the one-key-per-block grid), then
-// a block-wide radix select over the block scores and an ordered emission.  Scores never leave
-// the CU.
+// the block-wide top-k (value bins, the threshold bin ranked exactly) and an ordered emission.
+// Scores never leave the CU.
 __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a) {
   __shared__ float sc[kDecodeMaxCand];
-  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
-  const int64_t row = blockIdx.x;  // (b * Hkv + m), one query row each
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
-  int16_t* out = a.sel + row * a.k_total;
-  if (wave == 0) emit_forced(out, g, a.k_total, lane);
-  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
-  int16_t* chosen_out = out + g.init_hi;
-  const int C = g.n_cand;
-  if (g.n_take >= C) {
-    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
-    return;
-  }
-  if (g.n_take <= 0) return;
-
-  // Window scores: lane reads dims 8*(lane%16).. of window wf + base + 4 i + lane/16 (1 KiB per
-  // load) into sc[base + 4 i + lane/16].
-  int32_t wf, wl;
-  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
-  const int NW = wl - wf + 1;  // windows scored (C for the one-key-per-block grid)
-  {
-    const int c = lane & 15, rs = lane >> 4;
-    const uint4 fw = ld16(a.f + row * kHeadDim + c * 8);
-    const float f0 = bf16lo(fw.x), f1 = bf16hi(fw.x), f2 = bf16lo(fw.y), f3 = bf16hi(fw.y);
-    const float f4 = bf16lo(fw.z), f5 = bf16hi(fw.z), f6 = bf16lo(fw.w), f7 = bf16hi(fw.w);
-    const uint16_t* kbase = a.kc + (row * a.nc_cap + wf) * kHeadDim + c * 8;
-    // Double-buffered: the next 64 windows' loads are in flight while this wave scores the
-    // current ones.
-    uint4 kw[16], kn[16];
-    // Indices past the last window read the last one again (never stored), so the loads stay
-    // branch-free.
-    auto load = [&](int base, uint4 (&w)[16]) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int idx = min(base + 4 * i + rs, NW - 1);
-        w[i] = ld16_nt(kbase + (int64_t)idx * kHeadDim);
-      }
-    };
-    int base = wave * 64;
-    if (base < NW) load(base, kw);
-    for (; base < NW; base += kDecThreads) {
-      if (base + kDecThreads < NW) load(base + kDecThreads, kn);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float d = f0 * bf16lo(kw[i].x);
-        d = fmaf(f1, bf16hi(kw[i].x), d);
-        d = fmaf(f2, bf16lo(kw[i].y), d);
-        d = fmaf(f3, bf16hi(kw[i].y), d);
-        d = fmaf(f4, bf16lo(kw[i].z), d);
-        d = fmaf(f5, bf16hi(kw[i].z), d);
-        d = fmaf(f6, bf16lo(kw[i].w), d);
-        d = fmaf(f7, bf16hi(kw[i].w), d);
-        d = row16_sum(d);
-        const int idx = base + 4 * i + rs;
-        if (c == 0 && idx < NW) sc[idx] = d;
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) kw[i] = kn[i];
-    }
-  }
-  __syncthreads();
-  // Block scores: the window scores themselves, or their max-pool into sc[NW .. NW + C).
-  const float* bs = sc;
-  if (!grid_is_blocks(a.grid)) {
-    const int32_t wvis = grid_win_vis(a.grid, a.q_pos0);
-    for (int i = tid; i < C; i += kDecThreads) {
-      const int32_t j = g.cand_lo + i;
-      const int32_t lo = grid_win_lo(a.grid, j), hi = min(grid_win_hi(a.grid, j), wvis);
-      float m = sc[lo - wf];
-      for (int32_t w = lo + 1; w <= hi; ++w) m = fmaxf(m, sc[w - wf]);
-      sc[NW + i] = m;
-    }
-    bs = sc + NW;
-    __syncthreads();
-  }
-
-  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+  decode_select_row(a, blockIdx.x, sc, hist, wave_cnt, pick);
 }
 
 // Decode rows with their window scores already in the workspace (row stride ws_stride, window
@@ -277,7 +133,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
 // scores and runs the block-wide radix select.  The second kernel of the split decode path.
 __global__ __launch_bounds__(kDecThreads) void decode_topk_kernel(SelectArgs a) {
   __shared__ float sc[kDecodeMaxCand];
-  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
   const int64_t row = blockIdx.x;
@@ -344,6 +200,10 @@ static SelectPath select_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t
   // multi-row: the fused tile kernel serves both grids up to kSelTileMaxCand candidates per row
   const bool tile_grid = grid_is_blocks(grid) || (grid.l == 32 && grid.s == 16);
   return tile_grid && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
+}
+
+bool select_is_fused_decode(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  return select_path(rows, n_q, q_pos0, n_init, n_local, grid) == kPathDecode;
 }
 
 bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {

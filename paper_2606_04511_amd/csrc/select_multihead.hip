@@ -78,7 +78,7 @@ __device__ __forceinline__ float dot8(const float (&q)[8], const uint4& k) {
 template <int G>
 __global__ __launch_bounds__(kDecThreads) void mh_decode_kernel(SelectArgs a) {
   __shared__ float zs[kMhLdsFloats];  // head h's score of window i at zs[h NV + i]
-  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
   __shared__ float red[kDecThreads / 64][G];
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kDecThreads) void mh_decode_kernel(SelectArgs a) {
 // score of window 16 t + 4 j + e.
 __global__ __launch_bounds__(kDecThreads) void mh_decode2_kernel(SelectArgs a) {
   __shared__ float zs[kMhLdsFloats];  // shared scores of windows [0, NV), then block scores
-  __shared__ __align__(16) uint32_t hist[256];
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
   __shared__ float red_m[kDecThreads / 64][16], red_s[kDecThreads / 64][16];

@@ -174,9 +174,10 @@ int scratch_address(void** out) {
 }
 
 // sparda_sparse_attn and its no-allocation variant (static_ws: the partials go to `scratch`).
-int attn_call(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k, const void* v,
-              int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale, void* o, void* ws,
-              size_t ws_bytes, bool static_ws, hipStream_t stream) {
+// Validates an attention call and fills its kernel arguments; nothing is enqueued.
+int attn_prepare(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k, const void* v,
+                 int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale, void* o, void* ws,
+                 size_t ws_bytes, bool static_ws, sparda::AttnArgs* out) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_dev(q, "q", 16)) || (rc = check_dev(k, "k", 16)) || (rc = check_dev(v, "v", 16)) ||
@@ -198,7 +199,7 @@ int attn_call(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_p
     if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
     if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   }
-  sparda::AttnArgs a;
+  sparda::AttnArgs& a = *out;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
@@ -217,7 +218,58 @@ int attn_call(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_p
   a.sm_scale = sm_scale;
   a.n_splits = ns;
   a.blocks_per_split = bps;
+  return ok();
+}
+
+int attn_call(const sparda_shape* shape, const void* q, int32_t n_q, int64_t q_pos0, const void* k, const void* v,
+              int32_t kv_mode, const int16_t* sel, const int16_t* cnt, float sm_scale, void* o, void* ws,
+              size_t ws_bytes, bool static_ws, hipStream_t stream) {
+  sparda::AttnArgs a;
+  const int rc = attn_prepare(shape, q, n_q, q_pos0, k, v, kv_mode, sel, cnt, sm_scale, o, ws, ws_bytes, static_ws, &a);
+  if (rc) return rc;
   return hip_status(sparda::launch_sparse_attn(a, stream), "attention launch");
+
+}
+
+// Validates a select call and fills its kernel arguments; nothing is enqueued.
+int select_prepare(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0, const void* k_cmp,
+                   int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes, sparda::SelectArgs* out) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_dev(f, "f", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(sel, "sel", 2)) ||
+      (rc = check_dev(cnt, "cnt", 2)))
+    return rc;
+  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
+  const int64_t pl = q_pos0 + n_q - 1;
+  const sparda::RowGeom gl = sparda::row_geom(pl, shape->n_init, shape->n_local, shape->k_total);
+  int32_t wf, wl;
+  sparda::row_windows(gl, grid_of(shape), pl, &wf, &wl);
+  if (gl.n_cand > 0 && (int64_t)wl >= shape->nc_cap)
+    return fail(SPARDA_ERR_INVALID_ARG, "compressed key %d (for block %d) beyond nc_cap %lld", wl,
+                gl.cand_lo + gl.n_cand - 1, (long long)shape->nc_cap);
+  int64_t stride = 0;
+  const size_t need = select_ws(shape, n_q, q_pos0, &stride);
+  if (need > 0) {
+    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  sparda::SelectArgs& a = *out;
+  a.f = static_cast<const uint16_t*>(f);
+  a.kc = static_cast<const uint16_t*>(k_cmp);
+  a.sel = sel;
+  a.cnt = cnt;
+  a.ws = static_cast<float*>(ws);
+  a.ws_stride = stride;
+  a.batch = shape->batch;
+  a.n_kv_heads = shape->n_kv_heads;
+  a.n_q = n_q;
+  a.q_pos0 = q_pos0;
+  a.nc_cap = shape->nc_cap;
+  a.n_init = shape->n_init;
+  a.n_local = shape->n_local;
+  a.k_total = shape->k_total;
+  a.grid = grid_of(shape);
+  return ok();
 }
 
 }  // namespace
@@ -254,6 +306,12 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
     *bytes = multihead_ws(shape, n_q, q_pos0, &stride);
   } else if (op == SPARDA_OP_INDEXER_KL) {
     *bytes = kl_ws(shape, n_q, q_pos0);
+  } else if (op == SPARDA_OP_DECODE_STEP) {
+    if (n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "a decode step has n_q == 1");
+    int64_t stride;
+    int32_t ns, bps;
+    const size_t a = select_ws(shape, 1, q_pos0, &stride), b = attn_ws(shape, 1, q_pos0, &ns, &bps);
+    *bytes = a > b ? a : b;
   } else {
     return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
   }
@@ -280,42 +338,22 @@ int sparda_compress_keys(const sparda_shape* shape, const void* k_cache, int64_t
 int sparda_forecast_select(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,
                            const void* k_cmp, int16_t* sel, int16_t* cnt, void* ws, size_t ws_bytes,
                            hipStream_t stream) {
-  int rc = check_shape(shape);
-  if (rc) return rc;
-  if ((rc = check_dev(f, "f", 16)) || (rc = check_dev(k_cmp, "k_cmp", 16)) || (rc = check_dev(sel, "sel", 2)) ||
-      (rc = check_dev(cnt, "cnt", 2)))
-    return rc;
-  if ((rc = check_rows(shape, n_q, q_pos0))) return rc;
-  const int64_t pl = q_pos0 + n_q - 1;
-  const sparda::RowGeom gl = sparda::row_geom(pl, shape->n_init, shape->n_local, shape->k_total);
-  int32_t wf, wl;
-  sparda::row_windows(gl, grid_of(shape), pl, &wf, &wl);
-  if (gl.n_cand > 0 && (int64_t)wl >= shape->nc_cap)
-    return fail(SPARDA_ERR_INVALID_ARG, "compressed key %d (for block %d) beyond nc_cap %lld", wl,
-                gl.cand_lo + gl.n_cand - 1, (long long)shape->nc_cap);
-  int64_t stride = 0;
-  const size_t need = select_ws(shape, n_q, q_pos0, &stride);
-  if (need > 0) {
-    if (!ws || !aligned(ws, 16)) return fail(SPARDA_ERR_WORKSPACE, "workspace of %zu bytes required", need);
-    if (ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  }
   sparda::SelectArgs a;
-  a.f = static_cast<const uint16_t*>(f);
-  a.kc = static_cast<const uint16_t*>(k_cmp);
-  a.sel = sel;
-  a.cnt = cnt;
-  a.ws = static_cast<float*>(ws);
-  a.ws_stride = stride;
-  a.batch = shape->batch;
-  a.n_kv_heads = shape->n_kv_heads;
-  a.n_q = n_q;
-  a.q_pos0 = q_pos0;
-  a.nc_cap = shape->nc_cap;
-  a.n_init = shape->n_init;
-  a.n_local = shape->n_local;
-  a.k_total = shape->k_total;
-  a.grid = grid_of(shape);
+  const int rc = select_prepare(shape, f, n_q, q_pos0, k_cmp, sel, cnt, ws, ws_bytes, &a);
+  if (rc) return rc;
   return hip_status(sparda::launch_select(a, stream), "select launch");
+}
+
+int sparda_decode_step(const sparda_shape* shape, const void* f, int64_t q_pos, const void* k_cmp, const void* q,
+                       const void* k, const void* v, float sm_scale, int16_t* sel, int16_t* cnt, void* o, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  sparda::SelectArgs sa;
+  sparda::AttnArgs aa;
+  int rc = select_prepare(shape, f, 1, q_pos, k_cmp, sel, cnt, ws, ws_bytes, &sa);
+  if (rc) return rc;
+  if ((rc = attn_prepare(shape, q, 1, q_pos, k, v, 0, sel, cnt, sm_scale, o, ws, ws_bytes, false, &aa))) return rc;
+  return hip_status(sparda::launch_decode_step(sa, aa, stream), "decode step launch");
+
 }
 
 int sparda_forecast_score_max(const sparda_shape* shape, const void* f, int32_t n_q, int64_t q_pos0,

@@ -26,6 +26,7 @@ SPARDA_OP_FORECAST_SELECT = 1
 SPARDA_OP_SPARSE_ATTN = 2
 SPARDA_OP_MULTIHEAD_SELECT = 3
 SPARDA_OP_INDEXER_KL = 4
+SPARDA_OP_DECODE_STEP = 5
 SPARDA_NOALLOC_SCRATCH_BYTES = 4718592  # the static scratch of sparda_sparse_attn_noalloc (include/sparda.h)
 
 EXPORTED = ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max", "sparda_multihead_select",
@@ -97,6 +98,7 @@ def load() -> ctypes.CDLL:
         lib.sparda_multihead_select.argtypes = [S, P, i32, i64, P, ctypes.c_float, P, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P, ctypes.c_size_t, P]
         lib.sparda_sparse_attn_noalloc.argtypes = [S, P, i32, i64, P, P, i32, P, P, ctypes.c_float, P, P]
+        lib.sparda_decode_step.argtypes = [S, P, i64, P, P, P, P, ctypes.c_float, P, P, P, P, ctypes.c_size_t, P]
         lib.sparda_plan_staging.argtypes = [S, P, P, i64, P, P, P, P, P, P, P]
         lib.sparda_indexer_kl.argtypes = [S, P, P, P, P, i32, i64, ctypes.c_float, i32, P, P, P, ctypes.c_size_t, P]
         lib.sparda_gather_blocks.argtypes = [S, P, P, P, P, P, P, i32, P]
@@ -104,7 +106,8 @@ def load() -> ctypes.CDLL:
         lib.sparda_stage_append_kv.argtypes = [S, P, P, i64, P, P, P, P, P]
         lib.sparda_workspace_size.argtypes = [S, i32, i32, i64, ctypes.POINTER(ctypes.c_size_t)]
         for name in ("sparda_compress_keys", "sparda_forecast_select", "sparda_forecast_score_max",
-                     "sparda_multihead_select", "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_gather_blocks",
+                     "sparda_multihead_select", "sparda_sparse_attn", "sparda_sparse_attn_noalloc", "sparda_decode_step",
+                     "sparda_gather_blocks",
                      "sparda_stage_append_kv", "sparda_writeback_kv", "sparda_plan_staging", "sparda_indexer_kl",
                      "sparda_workspace_size"):
             getattr(lib, name).restype = ctypes.c_int
@@ -190,6 +193,15 @@ def sparda_sparse_attn(shape: SpardaShape, q, n_q: int, q_pos0: int, k, v, kv_mo
         ws_bytes = ws.numel() * ws.element_size()
     _check(load().sparda_sparse_attn(ctypes.byref(cs), _p(q), n_q, q_pos0, _p(k), _p(v), kv_mode, _p(sel), _p(cnt),
                                      float(sm_scale), _p(o), _p(ws), ws_bytes, _stream(stream)), "sparda_sparse_attn")
+
+
+def sparda_decode_step(shape: SpardaShape, f, q_pos: int, k_cmp, q, k, v, sm_scale: float, sel, cnt, o, ws=None,
+                       ws_bytes: int = 0, stream=None):
+    cs = shape.c()
+    if ws is not None and not isinstance(ws, int) and ws_bytes == 0:
+        ws_bytes = ws.numel() * ws.element_size()
+    _check(load().sparda_decode_step(ctypes.byref(cs), _p(f), q_pos, _p(k_cmp), _p(q), _p(k), _p(v), float(sm_scale),
+                                     _p(sel), _p(cnt), _p(o), _p(ws), ws_bytes, _stream(stream)), "sparda_decode_step")
 
 
 def sparda_sparse_attn_noalloc(shape: SpardaShape, q, n_q: int, q_pos0: int, k, v, kv_mode: int, sel, cnt,

@@ -202,6 +202,32 @@ def test_attention_noalloc_argument_errors(lib):
     assert worst == 510 * 16 * 130 * 4
 
 
+def test_decode_step_argument_errors(lib):
+    """The fused decode step validates both halves (select, then attention) before any HIP call,
+    and its workspace is the larger of the two calls' workspaces."""
+    s = shape()
+    d = sp.sparda_decode_step
+    sc = 1 / math.sqrt(128)
+    # f, q_pos, k_cmp, q, k, v, sm_scale, sel, cnt, o, ws, ws_bytes, stream
+    assert rc_of(d, s, None, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(d, s, FAKE, 4096, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(d, s, FAKE, 4095, FAKE, None, FAKE, FAKE, sc, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, float("inf"), FAKE, FAKE, FAKE, None, 0, 0) == \
+        sp.SPARDA_ERR_INVALID_ARG
+    assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, None, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
+    # 16 rows: the attention splits its rows, so the step needs the attention's workspace
+    need = sp.sparda_workspace_size(s, sp.SPARDA_OP_DECODE_STEP, 1, 4095)
+    assert need == max(sp.sparda_workspace_size(s, sp.SPARDA_OP_FORECAST_SELECT, 1, 4095),
+                       sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, 4095)) > 0
+    assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
+    assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, FAKE, need - 16, 0) == \
+        sp.SPARDA_ERR_WORKSPACE
+    # 128K, B32, 8 KV heads: both halves run one workgroup per row (the fused kernel): no workspace
+    big = shape(batch=32, k_total=64, t_cap=131072, nc_cap=2048)
+    assert sp.sparda_workspace_size(big, sp.SPARDA_OP_DECODE_STEP, 1, 131071) == 0
+    assert rc_of(sp.sparda_workspace_size, big, sp.SPARDA_OP_DECODE_STEP, 2, 131070) == sp.SPARDA_ERR_INVALID_ARG
+
+
 def test_stage_append_argument_errors(lib):
     s = shape()
     a = sp.sparda_stage_append_kv

@@ -70,6 +70,17 @@ def gpu_attend(s, q_dev, n_q, q_pos0, k_dev, v_dev, kv_mode, sel_dev, cnt_dev, d
     return o
 
 
+def gpu_step(s, f_dev, q_pos, kc_dev, q_dev, k_dev, v_dev, dev):
+    """sparda_decode_step: the sets and the attention output of one decode step."""
+    sel = torch.full((s.batch, s.n_kv_heads, 1, s.k_total), 777, dtype=torch.int16, device=dev)
+    cnt = torch.full((s.batch, s.n_kv_heads, 1), 777, dtype=torch.int16, device=dev)
+    o = torch.full((s.batch, s.n_q_heads, 1, 128), float("nan"), dtype=torch.bfloat16, device=dev)
+    sp.sparda_decode_step(s, f_dev, q_pos, kc_dev, q_dev, k_dev, v_dev, SCALE, sel, cnt, o,
+                          ws(s, sp.SPARDA_OP_DECODE_STEP, 1, q_pos, dev))
+    torch.cuda.synchronize()
+    return sel, cnt, o
+
+
 def make(B, H, G, T, n_q, k_total, seed, t_cap=None, n_init=1, n_local=2):
     w = inputs.Workload("t", batch=B, seq_len=T, n_q=n_q, n_kv_heads=H, group_size=G, k_total=k_total,
                         n_init=n_init, n_local=n_local, seed=seed)
@@ -213,6 +224,9 @@ ATTN = [
     (1, 2, 8, 8192, 1, 32),
     (1, 1, 16, 8192, 1, 32),
     (1, 1, 4, 77, 1, 3),
+    (1, 2, 5, 8192, 1, 32),
+    (1, 2, 6, 8192, 1, 32),
+    (1, 1, 12, 8192, 1, 32),
     (1, 2, 4, 640, 640, 4),
     (1, 1, 4, 8192, 300, 16),
     # multi-row calls on the tiled kernel (256/G rows per tile): every G it takes, ragged last
@@ -464,6 +478,12 @@ def _decode_full(dev, name, n_sample_rows, n_sample_heads):
         got = out[b:b + 1, m * w.group_size:(m + 1) * w.group_size].float().cpu().numpy()
         worst = max(worst, compare_attention(got, ref, f"{name} {(b, m)}", wab))
     say(f"  sampled {len(pairs)} rows, tie swaps {swaps}, attention max err {worst:.3g}")
+    # the fused decode step on the same inputs: the same sets, and the same output bit for bit as
+    # the attention call over those sets
+    sel2, cnt2, out2 = gpu_step(s, case["f"], T - 1, kc, case["q"], case["k"], case["v"], dev)
+    assert torch.equal(sel2, sel) and torch.equal(cnt2, cnt)
+    out_own = gpu_attend(s, case["q"], 1, T - 1, case["k"], case["v"], 0, sel, cnt, dev)
+    assert torch.equal(out2.view(torch.int16), out_own.view(torch.int16))
 
 
 def test_full_decode_b1_t4k_all_rows(dev):
@@ -707,21 +727,78 @@ def test_score_max_full_prefill_t32k(dev):
     say(f"  2 x {T} rows, worst error / bound {worst:.3g}")
 
 
+# ----------------------------------------------------------------------------- decode step
+
+DECODE_STEP = [
+    # B, H, G, T, k_total, lw, sw: 256 or more rows with G <= 5 run the fused kernel, the others
+    # the two launches
+    (64, 4, 4, 8192, 64, 64, 64),
+    (32, 8, 1, 4096, 16, 64, 64),
+    (128, 2, 2, 6000, 40, 64, 64),  # ragged last block
+    (86, 3, 3, 3000, 24, 64, 64),   # 258 rows
+    (64, 4, 5, 4096, 32, 64, 64),
+    (64, 4, 4, 8192, 96, 32, 16),   # the paper's (32, 16) grid: window scores max-pooled in LDS
+    (64, 4, 4, 200, 16, 64, 64),    # fewer candidates than slots: every candidate is taken
+    (4, 8, 4, 8192, 64, 64, 64),    # 32 rows: split attention, two launches
+    (64, 4, 8, 4096, 32, 64, 64),   # 8 heads: the MFMA P V kernel, two launches
+]
+
+
+@pytest.mark.parametrize("B,H,G,T,k_total,lw,sw", DECODE_STEP)
+def test_decode_step_matches_separate_calls(dev, B, H, G, T, k_total, lw, sw):
+    """sparda_decode_step writes the sets of sparda_forecast_select and the output of
+    sparda_sparse_attn over them, bit for bit; a few rows are checked against the oracle too."""
+    say(f"decode step B{B} H{H} G{G} T{T} k{k_total} grid ({lw}, {sw})")
+    w = inputs.Workload("t", batch=B, seq_len=T, n_q=1, n_kv_heads=H, group_size=G, k_total=k_total, n_init=1,
+                        n_local=2, seed=6100 + T + G)
+    t_cap = -(-T // 64) * 64
+    case = inputs.make_case(w, t_cap=t_cap, device=dev)
+    nw = (T - lw) // sw + 1
+    s, o = shapes(B, H, G, k_total, t_cap, nw, lw=lw, sw=sw)
+    f, q, k, v = (case[x] for x in ("f", "q", "k", "v"))
+    kc = gpu_compress(s, k, T, nw, nw, dev)
+    sel, cnt = gpu_select(s, f, 1, T - 1, kc, dev)
+    out = gpu_attend(s, q, 1, T - 1, k, v, 0, sel, cnt, dev)
+    sel2, cnt2, out2 = gpu_step(s, f, T - 1, kc, q, k, v, dev)
+    assert torch.equal(cnt2, cnt)
+    assert torch.equal(sel2, sel)
+    assert torch.equal(out2.view(torch.int16), out.view(torch.int16))
+    rows = [(0, 0, 0), (B - 1, H - 1, 0), (B // 2, H // 2, 0)]
+    kc16 = inputs.to_u16(kc)
+    n, swaps = compare_selection(o, inputs.to_u16(case["f"]), kc16, 1, T - 1, sel2.cpu().numpy(), cnt2.cpu().numpy(),
+                                 rows)
+    _, o1 = shapes(1, 1, G, k_total, t_cap, nw, lw=lw, sw=sw)
+    for (b, m, _) in rows:
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][b:b + 1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][b:b + 1, m * G:(m + 1) * G])
+        ssel = sel2[b:b + 1, m:m + 1].cpu().numpy()
+        scnt = cnt2[b:b + 1, m:m + 1].cpu().numpy()
+        ref = oracle.sparse_attn(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE)
+        wab = oracle.sparse_attn(o1, q16, 1, T - 1, k16, abs_bits(v16), 0, ssel, scnt, SCALE)
+        compare_attention(out2[b:b + 1, m * G:(m + 1) * G].float().cpu().numpy(), ref, f"step {(b, m)}", wab)
+    say(f"  rows {n}, tie swaps {swaps}")
+
+
 # ----------------------------------------------------------------------------- exact ties
 
-@pytest.mark.parametrize("T,n_q,k_total", [(8192, 1, 16), (8192, 1024, 16), (32768, 2048, 64), (65536, 3, 64),
-                                           (40000, 1, 200)])
-def test_select_exact_ties_take_lowest_index(dev, T, n_q, k_total):
+@pytest.mark.parametrize("B,T,n_q,k_total,spread", [
+    (1, 8192, 1, 16, 1), (1, 8192, 1024, 16, 1), (1, 32768, 2048, 64, 1), (1, 65536, 3, 64, 1), (1, 40000, 1, 200, 1),
+    # integers in [-8, 8]: scores spread over about 2000 values, so the bin that holds the k-th
+    # score mixes distinct values and exact ties (decode: split path below 256 rows, fused above)
+    (1, 131072, 1, 64, 8), (128, 131072, 1, 64, 8), (128, 32768, 1, 96, 8), (1, 65536, 3, 64, 8),
+    (1, 8192, 1024, 16, 8)])
+def test_select_exact_ties_take_lowest_index(dev, B, T, n_q, k_total, spread):
     """F and K~ hold small integers, so every score is an exact integer in fp32 and in fp64 and
     many candidates tie; the GPU must break ties by the lower block index exactly as the oracle."""
-    say(f"exact ties T{T} n_q{n_q} k{k_total}")
-    B, H = 1, 2
+    say(f"exact ties B{B} T{T} n_q{n_q} k{k_total} spread {spread}")
+    H = 2
     nb = T // 64
     t_cap = -(-T // 64) * 64
     s, o = shapes(B, H, 4, k_total, t_cap, nb)
-    g = torch.Generator().manual_seed(T + n_q)
-    f = torch.randint(-1, 2, (B, H, n_q, 128), generator=g).to(torch.bfloat16)
-    kc = torch.randint(-1, 2, (B, H, nb, 128), generator=g).to(torch.bfloat16)
+    g = torch.Generator().manual_seed(T + n_q + (B - 1) + 1000 * (spread - 1))
+    f = torch.randint(-spread, spread + 1, (B, H, n_q, 128), generator=g).to(torch.bfloat16)
+    kc = torch.randint(-spread, spread + 1, (B, H, nb, 128), generator=g).to(torch.bfloat16)
     m3 = nb // 3
     kc[:, :, 0:3 * m3:3] = kc[:, :, 1:3 * m3:3]  # duplicated K~ rows: exact score ties
     q_pos0 = T - n_q
