@@ -32,6 +32,7 @@ constexpr int kAttnWaves = 8;        // wavefronts per attention workgroup
 constexpr int kRowsFillChip = 256;   // rows at which one workgroup per row fills 256 CUs
 constexpr int kMaxSplits = 64;
 constexpr int kKstPitch = kHeadDim + 16;  // uint16 per staged K row (288 B)
+constexpr int kStepMaxK = 1024;           // largest k_total of the fused decode step (its set lives in LDS)
 
 // LDS of one attention workgroup.  kst: K of each wavefront's current block, transposed through
 // LDS: read from HBM as 1 KiB rows of 4 tokens (the access pattern streams faster than 16 token
@@ -45,9 +46,11 @@ struct AttnLds {
 };
 
 // Attention of query row `row`, split `split` of its block list, by a workgroup of NW
-// wavefronts (every thread must call it).
+// wavefronts (every thread must call it).  srow: the row's a.k_total entries (global or LDS),
+// n_listed: its count.
 template <int G, int NW>
-__device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int split, AttnLds<G, NW>& L) {
+__device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int split, AttnLds<G, NW>& L,
+                                           const int16_t* srow, int n_listed) {
   auto& kst = L.kst;
   auto& p_lds = L.p_lds;
   auto& st_m = L.st_m;
@@ -62,8 +65,7 @@ __device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int s
   const int b = (int)(bm / a.n_kv_heads);
   const int64_t p = a.q_pos0 + r;
   const int blk = (int)(p / kBlock);
-  int n = a.cnt[row];
-  n = n > a.k_total ? a.k_total : (n < 0 ? 0 : n);
+  const int n = n_listed > a.k_total ? a.k_total : (n_listed < 0 ? 0 : n_listed);
   const int s_begin = split * a.blocks_per_split;
   const int s_end = min(n, s_begin + a.blocks_per_split);
   const int64_t Hq = (int64_t)a.n_kv_heads * G;
@@ -84,7 +86,6 @@ __device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int s
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
 
-  const int16_t* srow = a.sel + row * a.k_total;
   // The attended tokens are a union of blocks: an entry whose block an earlier entry of the row
   // already lists is skipped.  Lane e holds entry e (e < 64): the walk reads entries below 64 from
   // it, so it issues no loads of its own between the blocks' loads.
@@ -263,15 +264,19 @@ __device__ __forceinline__ void attend_row(const AttnArgs& a, int64_t row, int s
 template <int G, int NW>
 __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
   __shared__ __align__(16) AttnLds<G, NW> lds;
-  attend_row<G, NW>(a, blockIdx.x, blockIdx.y, lds);
+  const int64_t row = blockIdx.x;
+  attend_row<G, NW>(a, row, blockIdx.y, lds, a.sel + row * a.k_total, a.cnt[row]);
 }
 
-// One decode step of a (batch, group) row in one workgroup: the row's Forecast selection
-// (Sec. 4.1, Eq. 4 with Eq. 1), written to s.sel and s.cnt, then its sparse attention over that
-// set (Eq. 5).  The selection's scores live in the K slices and its histogram in the P space,
-// both free until the attention starts.  Rows finish their selection at different times, so some
-// rows' attention loads already run while others select: the HBM stays busier than with a
-// selection kernel followed by an attention kernel.
+// One decode step of a (batch, group) row: the row's Forecast selection (Sec. 4.1, Eq. 4 with
+// Eq. 1), then its sparse attention over that set (Eq. 5), in one workgroup per (row, split).
+// The selection's scores live in the K slices and its histogram in the P space, both free until
+// the attention starts; the set itself is kept in LDS, and split 0 writes it to s.sel / s.cnt.
+// With splits (fewer rows than CUs) every split's workgroup computes the same selection: the
+// selection reads a fraction of the attention's bytes, and the rows' attention then starts
+// without a second launch.  Rows finish their selection at different times, so some rows'
+// attention loads already run while others select: the HBM stays busier than with a selection
+// kernel followed by an attention kernel.
 template <int G, int NW>
 __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, AttnArgs a) {
   static_assert(NW * 64 == kDecThreads, "the selection runs on the attention workgroup");
@@ -280,10 +285,17 @@ __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, Attn
   __shared__ __align__(16) AttnLds<G, NW> lds;
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
-  decode_select_row(s, blockIdx.x, reinterpret_cast<float*>(&lds.kst[0][0]), reinterpret_cast<uint32_t*>(&lds.p_lds[0][0][0]),
-                    wave_cnt, pick);
-  __syncthreads();  // the row's set is in a.sel / a.cnt, and the LDS is free
-  attend_row<G, NW>(a, blockIdx.x, 0, lds);
+  __shared__ __align__(16) int16_t set[kStepMaxK];
+  __shared__ int16_t set_cnt;
+  const int64_t row = blockIdx.x;
+  decode_select_row(s, row, reinterpret_cast<float*>(&lds.kst[0][0]), reinterpret_cast<uint32_t*>(&lds.p_lds[0][0][0]),
+                    wave_cnt, pick, set, &set_cnt);
+  __syncthreads();  // the row's set is in LDS, and the rest of the LDS is free
+  if (blockIdx.y == 0) {
+    for (int i = threadIdx.x; i < s.k_total; i += NW * 64) s.sel[row * s.k_total + i] = set[i];
+    if (threadIdx.x == 0) s.cnt[row] = set_cnt;
+  }
+  attend_row<G, NW>(a, row, blockIdx.y, lds, set, set_cnt);
 }
 
 // Decode attention for groups of 7 to 16 heads: P V on MFMA.  With this many query rows per
@@ -556,14 +568,18 @@ static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
 
 template <int G>
 static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves>), dim3((unsigned)((int64_t)a.batch * a.n_kv_heads)),
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
+  hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves>), dim3((unsigned)rows, (unsigned)a.n_splits),
                      dim3(kAttnWaves * 64), 0, stream, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_splits == 1) return e;
+  hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)(rows * G)), dim3(128), 0, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
-  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.n_splits == 1 && a.group_size <= 5 &&
+  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.group_size <= 5 && a.k_total <= kStepMaxK &&
                      select_is_fused_decode(rows, 1, s.q_pos0, s.n_init, s.n_local, s.grid);
   if (fused) {
     switch (a.group_size) {

@@ -145,8 +145,9 @@ hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream);
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
 // One decode step: the select call s, then the attention call a over the sets it writes.  One
-// fused kernel (decode_step_kernel) where both would run one workgroup per row (the fused
-// decode select, unsplit attention with G <= 5, full caches); otherwise the two launches.
+// fused kernel (decode_step_kernel, one workgroup per row and attention split; plus the split
+// combine) where the select takes its fused decode path, G <= 5, k_total <= 1024 and the caches
+// are full; otherwise the two calls.
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream);
 // True when a multi-row call takes the tiled kernel (attention_prefill.hip), which needs no
 // workspace: at least 16 rows, 16 % G == 0, and the tile's row bitmaps fit in LDS.

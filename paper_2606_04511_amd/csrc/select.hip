@@ -125,7 +125,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
   __shared__ __align__(16) uint32_t hist[kTopkLds];
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
-  decode_select_row(a, blockIdx.x, sc, hist, wave_cnt, pick);
+  const int64_t row = blockIdx.x;
+  decode_select_row(a, row, sc, hist, wave_cnt, pick, a.sel + row * a.k_total, a.cnt + row);
 }
 
 // Decode rows with their window scores already in the workspace (row stride ws_stride, window

@@ -385,16 +385,16 @@ __device__ __forceinline__ void block_topk_emit(const float* bs, int C, int n_ta
 // a workgroup of kDecThreads threads (every thread must call it): the forced blocks, the window
 // scores F_row . K~_i into sc (LDS, kDecodeMaxCand floats), their max-pool to block scores on a
 // windowed grid, then block_topk_emit.  hist (kTopkLds uint32, 16-byte aligned), wave_cnt
-// (kDecThreads / 64 ints) and pick (3 ints) are LDS.  The row's set and count are in a.sel and
-// a.cnt once every thread has returned.
+// (kDecThreads / 64 ints) and pick (3 ints) are LDS.  The row's set (a.k_total entries) goes to
+// out and its count to *cnt_out (global or LDS), complete once every thread has returned and
+// synchronised.
 __device__ __forceinline__ void decode_select_row(const SelectArgs& a, int64_t row, float* sc, uint32_t* hist,
-                                                  int* wave_cnt, int* pick) {
+                                                  int* wave_cnt, int* pick, int16_t* out, int16_t* cnt_out) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
-  int16_t* out = a.sel + row * a.k_total;
   if (wave == 0) emit_forced(out, g, a.k_total, lane);
-  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
+  if (tid == 0) *cnt_out = (int16_t)(g.n_forced + g.n_take);
   int16_t* chosen_out = out + g.init_hi;
   const int C = g.n_cand;
   if (g.n_take >= C) {

@@ -730,8 +730,8 @@ def test_score_max_full_prefill_t32k(dev):
 # ----------------------------------------------------------------------------- decode step
 
 DECODE_STEP = [
-    # B, H, G, T, k_total, lw, sw: 256 or more rows with G <= 5 run the fused kernel, the others
-    # the two launches
+    # B, H, G, T, k_total, lw, sw: G <= 5 on the fused decode select path runs the fused kernel
+    # (one workgroup per row and split), the others the two calls
     (64, 4, 4, 8192, 64, 64, 64),
     (32, 8, 1, 4096, 16, 64, 64),
     (128, 2, 2, 6000, 40, 64, 64),  # ragged last block
@@ -739,8 +739,11 @@ DECODE_STEP = [
     (64, 4, 5, 4096, 32, 64, 64),
     (64, 4, 4, 8192, 96, 32, 16),   # the paper's (32, 16) grid: window scores max-pooled in LDS
     (64, 4, 4, 200, 16, 64, 64),    # fewer candidates than slots: every candidate is taken
-    (4, 8, 4, 8192, 64, 64, 64),    # 32 rows: split attention, two launches
-    (64, 4, 8, 4096, 32, 64, 64),   # 8 heads: the MFMA P V kernel, two launches
+    (4, 8, 4, 8192, 64, 64, 64),    # 32 rows: 8 splits per row, each split's workgroup selects
+    (1, 2, 4, 4096, 16, 64, 64),    # 2 rows, 2 splits
+    (3, 8, 4, 20000, 200, 64, 64),  # 24 rows, k = 200: splits of 25 blocks
+    (1, 2, 4, 131072, 64, 64, 64),  # 2 rows of 2045 candidates: the split select path, two calls
+    (64, 4, 8, 4096, 32, 64, 64),   # 8 heads: the MFMA P V kernel, two calls
 ]
 
 
