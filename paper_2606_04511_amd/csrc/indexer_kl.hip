@@ -28,7 +28,7 @@
 //                           columns and max-pools it into its positions in LDS (atomic max on the
 //                           float bits: all values are >= 0).  Prediction: the Forecast GEMV over
 //                           the positions into LDS and its softmax.  Selection: the block-wide
-//                           radix select of select_block.hpp over the candidate positions.  Then
+//                           top-k of select_block.hpp over the candidate positions.  Then
 //                           the bucket sums, the loss and the gradient GEMV.
 #include <math.h>
 

@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_select_kernel(SelectArgs a
 
 // Decode rows with their window scores already in the workspace (row stride ws_stride, window
 // wf of the row at offset 0): one workgroup per row loads them into LDS, max-pools them to block
-// scores and runs the block-wide radix select.  The second kernel of the split decode path.
+// scores and runs the block-wide top-k.  The second kernel of the split decode path.
 __global__ __launch_bounds__(kDecThreads) void decode_topk_kernel(SelectArgs a) {
   __shared__ float sc[kDecodeMaxCand];
   __shared__ __align__(16) uint32_t hist[kTopkLds];

@@ -15,8 +15,8 @@
 //  * fused decode (n_q == 1, G in {1, 2, 4, 8}, G * windows + candidates <= kMhLdsFloats): one
 //    512-thread workgroup per (batch, group) row.  K~ is read once, 1 KiB per wavefront load as
 //    in the Forecast decode kernel, and each loaded window is scored by all G heads into LDS;
-//    the per-head maximum and sum, the shared scores, the max-pool and the block-wide radix
-//    select (select_block.hpp) all stay on the CU.
+//    the per-head maximum and sum, the shared scores, the max-pool and the block-wide top-k
+//    (select_block.hpp) all stay on the CU.
 //  * fused two-pass decode (n_q == 1, any other G <= 16, windows + candidates <= kMhLdsFloats):
 //    a 16-window tile times the group's heads is one MFMA chain (A = 16 windows' keys, B = the
 //    G query rows padded to 16 columns).  Pass 1 keeps an online maximum and sum of 2^z per head,
