@@ -727,6 +727,45 @@ def test_score_max_full_prefill_t32k(dev):
     say(f"  2 x {T} rows, worst error / bound {worst:.3g}")
 
 
+def test_split_attention_workspace_needs_no_clearing(dev):
+    """With fewer rows than CUs the attention splits each row's blocks over workgroups whose
+    partials go through the workspace.  A workspace full of arbitrary bytes, and the same
+    workspace used again and again, give the same output bit for bit, equal to the oracle's
+    within the tight bar."""
+    say("split attention: arbitrary workspace bytes, repeated calls")
+    B, H, G, T, k_total = 1, 2, 4, 8192, 32
+    w, case = make(B, H, G, T, 1, k_total, 7100)
+    s, o = shapes(B, H, G, k_total, T, T // 64)
+    q, k, v = (case[x].to(dev) for x in ("q", "k", "v"))
+    kc_ref = oracle.compress_keys(o, inputs.to_u16(case["k"]), T, 0, T // 64)
+    sel, cnt = gpu_select(s, case["f"].to(dev), 1, T - 1, inputs.from_u16(kc_ref, dev), dev)
+    n = sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, T - 1)
+    assert n > 0
+    g = torch.Generator(device="cpu").manual_seed(5)
+    outs = []
+    for fill in ("random", "same", "same", "ones", "same"):
+        if fill == "random":
+            wsb = torch.randint(0, 256, (n,), dtype=torch.uint8, generator=g).to(dev)
+        elif fill == "ones":
+            wsb.fill_(255)
+        o_dev = torch.full((B, H * G, 1, 128), float("nan"), dtype=torch.bfloat16, device=dev)
+        sp.sparda_sparse_attn(s, q, 1, T - 1, k, v, 0, sel, cnt, SCALE, o_dev, wsb)
+        torch.cuda.synchronize()
+        outs.append(o_dev.clone())
+    for x in outs[1:]:
+        assert torch.equal(x.view(torch.int16), outs[0].view(torch.int16))
+    for (b, m) in ((0, 0), (0, 1)):
+        k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
+        v16 = inputs.to_u16(case["v"][b:b + 1, m:m + 1])
+        q16 = inputs.to_u16(case["q"][b:b + 1, m * G:(m + 1) * G])
+        _, o1 = shapes(1, 1, G, k_total, T, T // 64)
+        ssel = sel[b:b + 1, m:m + 1].cpu().numpy()
+        scnt = cnt[b:b + 1, m:m + 1].cpu().numpy()
+        ref = oracle.sparse_attn(o1, q16, 1, T - 1, k16, v16, 0, ssel, scnt, SCALE)
+        wab = oracle.sparse_attn(o1, q16, 1, T - 1, k16, abs_bits(v16), 0, ssel, scnt, SCALE)
+        compare_attention(outs[0][b:b + 1, m * G:(m + 1) * G].float().cpu().numpy(), ref, f"split {(b, m)}", wab)
+
+
 # ----------------------------------------------------------------------------- decode step
 
 DECODE_STEP = [
