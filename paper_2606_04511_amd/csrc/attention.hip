@@ -270,14 +270,30 @@ __global__ __launch_bounds__(NW * 64) void sparse_attn_kernel(AttnArgs a) {
 
 // One decode step of a (batch, group) row: the row's Forecast selection (Sec. 4.1, Eq. 4 with
 // Eq. 1), then its sparse attention over that set (Eq. 5), in one workgroup per (row, split).
-// The selection's scores live in the K slices and its histogram in the P space, both free until
-// the attention starts; the set itself is kept in LDS, and split 0 writes it to s.sel / s.cnt.
-// With splits (fewer rows than CUs) every split's workgroup computes the same selection: the
-// selection reads a fraction of the attention's bytes, and the rows' attention then starts
-// without a second launch.  Rows finish their selection at different times, so some rows'
+// kSplitSel: the row's window scores were written to the workspace by the split decode path's
+// scoring launch, and the workgroup only selects (decode_topk_row); otherwise it scores and
+// selects (decode_select_row).  The selection's scores live in the attention's K (or V) slices,
+// both free until the attention starts; the set itself is kept in LDS, and split 0 writes it to
+// s.sel / s.cnt.  With splits (fewer rows than CUs) every split's workgroup computes the same
+// selection: it reads a fraction of the attention's bytes, and the rows' attention then starts
+// without another launch.  Rows finish their selection at different times, so some rows'
 // attention loads already run while others select: the HBM stays busier than with a selection
 // kernel followed by an attention kernel.
-template <int G, int NW>
+template <bool kSplitSel>
+__device__ __forceinline__ void step_select(const SelectArgs& s, int64_t row, float* sc, uint32_t* hist, int* wave_cnt,
+                                            int* pick, int16_t* set, int16_t* set_cnt) {
+  if constexpr (kSplitSel)
+    decode_topk_row(s, row, sc, hist, wave_cnt, pick, set, set_cnt);
+  else
+    decode_select_row(s, row, sc, hist, wave_cnt, pick, set, set_cnt);
+  __syncthreads();  // the row's set is in LDS, and the selection's LDS is free
+  if (blockIdx.y == 0) {
+    for (int i = threadIdx.x; i < s.k_total; i += kDecThreads) s.sel[row * s.k_total + i] = set[i];
+    if (threadIdx.x == 0) s.cnt[row] = *set_cnt;
+  }
+}
+
+template <int G, int NW, bool kSplitSel>
 __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, AttnArgs a) {
   static_assert(NW * 64 == kDecThreads, "the selection runs on the attention workgroup");
   static_assert(sizeof(float) * kDecodeMaxCand <= sizeof(uint16_t) * NW * kBlock * kKstPitch, "scores fit in the K slices");
@@ -288,13 +304,8 @@ __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, Attn
   __shared__ __align__(16) int16_t set[kStepMaxK];
   __shared__ int16_t set_cnt;
   const int64_t row = blockIdx.x;
-  decode_select_row(s, row, reinterpret_cast<float*>(&lds.kst[0][0]), reinterpret_cast<uint32_t*>(&lds.p_lds[0][0][0]),
-                    wave_cnt, pick, set, &set_cnt);
-  __syncthreads();  // the row's set is in LDS, and the rest of the LDS is free
-  if (blockIdx.y == 0) {
-    for (int i = threadIdx.x; i < s.k_total; i += NW * 64) s.sel[row * s.k_total + i] = set[i];
-    if (threadIdx.x == 0) s.cnt[row] = set_cnt;
-  }
+  step_select<kSplitSel>(s, row, reinterpret_cast<float*>(&lds.kst[0][0]), reinterpret_cast<uint32_t*>(&lds.p_lds[0][0][0]),
+                         wave_cnt, pick, set, &set_cnt);
   attend_row<G, NW>(a, row, blockIdx.y, lds, set, set_cnt);
 }
 
@@ -312,12 +323,18 @@ __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, Attn
 // through LDS (the V slices' space) as in sparse_attn_kernel.
 constexpr int kWidePitch = 136;  // uint16 per staged V row (272 B: 16-byte aligned, bank-spread)
 
+// LDS of one workgroup of the wide kernel: the V slices (also the wavefronts' merge space).
+struct WideLds {
+  uint16_t vst[kAttnWaves][kBlock * kWidePitch];
+};
+
+// The wide kernel's attention of query row `row`, split `split`, over srow (a.k_total entries,
+// global or LDS) with n_listed of them valid.  Every thread of the workgroup must call it.
 template <int G>
-__global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnArgs a) {
+__device__ __forceinline__ void attend_row_wide(const AttnArgs& a, int64_t row, int split, WideLds& L,
+                                                const int16_t* srow, int n_listed) {
   constexpr int NW = kAttnWaves;
-  __shared__ __align__(16) uint16_t vst[NW][kBlock * kWidePitch];
-  const int64_t row = blockIdx.x;
-  const int split = blockIdx.y;
+  auto& vst = L.vst;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = (int)(row % a.n_q);
   const int64_t bm = row / a.n_q;
@@ -325,8 +342,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnA
   const int b = (int)(bm / a.n_kv_heads);
   const int64_t p = a.q_pos0 + r;
   const int blk = (int)(p / kBlock);
-  int n = a.cnt[row];
-  n = n > a.k_total ? a.k_total : (n < 0 ? 0 : n);
+  const int n = n_listed > a.k_total ? a.k_total : (n_listed < 0 ? 0 : n_listed);
   const int s_begin = split * a.blocks_per_split;
   const int s_end = min(n, s_begin + a.blocks_per_split);
   const int64_t Hq = (int64_t)a.n_kv_heads * G;
@@ -349,7 +365,6 @@ __global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnA
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   uint16_t* vs = vst[wave];
 
-  const int16_t* srow = a.sel + row * a.k_total;
   const int entry = lane < n ? (int)srow[lane] : -1;
   for (int s = s_begin + wave; s < s_end; s += NW) {
     const int j = __builtin_amdgcn_readfirstlane((int)srow[s]);
@@ -484,6 +499,29 @@ __global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnA
   }
 }
 
+template <int G>
+__global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnArgs a) {
+  __shared__ __align__(16) WideLds lds;
+  const int64_t row = blockIdx.x;
+  attend_row_wide<G>(a, row, blockIdx.y, lds, a.sel + row * a.k_total, a.cnt[row]);
+}
+
+// The decode step with the wide kernel's attention (7 <= G <= 16): as decode_step_kernel.
+template <int G, bool kSplitSel>
+__global__ __launch_bounds__(kAttnWaves * 64) void decode_step_wide_kernel(SelectArgs s, AttnArgs a) {
+  static_assert(kAttnWaves * 64 == kDecThreads, "the selection runs on the attention workgroup");
+  static_assert(sizeof(float) * kDecodeMaxCand <= sizeof(WideLds), "scores fit in the V slices");
+  __shared__ __align__(16) WideLds lds;
+  __shared__ __align__(16) uint32_t hist[kTopkLds];
+  __shared__ int wave_cnt[kDecThreads / 64];
+  __shared__ int pick[3];
+  __shared__ __align__(16) int16_t set[kStepMaxK];
+  __shared__ int16_t set_cnt;
+  const int64_t row = blockIdx.x;
+  step_select<kSplitSel>(s, row, reinterpret_cast<float*>(&lds.vst[0][0]), hist, wave_cnt, pick, set, &set_cnt);
+  attend_row_wide<G>(a, row, blockIdx.y, lds, set, set_cnt);
+}
+
 // Merge the split partials of one (row, head) by log-sum-exp: 128 threads, one per head dim.
 template <int G>
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
@@ -566,11 +604,21 @@ static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int G>
-static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
+template <int G, bool kWide>
+static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, bool split_sel, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
-  hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves>), dim3((unsigned)rows, (unsigned)a.n_splits),
-                     dim3(kAttnWaves * 64), 0, stream, s, a);
+  const dim3 grid((unsigned)rows, (unsigned)a.n_splits), block(kAttnWaves * 64);
+  if constexpr (kWide) {
+    if (split_sel)
+      hipLaunchKernelGGL((decode_step_wide_kernel<G, true>), grid, block, 0, stream, s, a);
+    else
+      hipLaunchKernelGGL((decode_step_wide_kernel<G, false>), grid, block, 0, stream, s, a);
+  } else {
+    if (split_sel)
+      hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves, true>), grid, block, 0, stream, s, a);
+    else
+      hipLaunchKernelGGL((decode_step_kernel<G, kAttnWaves, false>), grid, block, 0, stream, s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
   hipLaunchKernelGGL(attn_combine_kernel<G>, dim3((unsigned)(rows * G)), dim3(128), 0, stream, a);
@@ -579,16 +627,32 @@ static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, hipStrea
 
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
-  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.group_size <= 5 && a.k_total <= kStepMaxK &&
-                     select_is_fused_decode(rows, 1, s.q_pos0, s.n_init, s.n_local, s.grid);
+  const int path = select_decode_path(rows, 1, s.q_pos0, s.n_init, s.n_local, s.grid);
+  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.k_total <= kStepMaxK && path >= 0 &&
+                     a.group_size != 6;
   if (fused) {
+    const bool split_sel = path == 1;
+    if (split_sel) {
+      hipError_t e = launch_decode_split_scores(s, stream);
+      if (e != hipSuccess) return e;
+    }
     switch (a.group_size) {
-      case 1: return launch_step_g<1>(s, a, stream);
-      case 2: return launch_step_g<2>(s, a, stream);
-      case 3: return launch_step_g<3>(s, a, stream);
-      case 4: return launch_step_g<4>(s, a, stream);
-      case 5: return launch_step_g<5>(s, a, stream);
-      default: break;
+      case 1: return launch_step_g<1, false>(s, a, split_sel, stream);
+      case 2: return launch_step_g<2, false>(s, a, split_sel, stream);
+      case 3: return launch_step_g<3, false>(s, a, split_sel, stream);
+      case 4: return launch_step_g<4, false>(s, a, split_sel, stream);
+      case 5: return launch_step_g<5, false>(s, a, split_sel, stream);
+      case 7: return launch_step_g<7, true>(s, a, split_sel, stream);
+      case 8: return launch_step_g<8, true>(s, a, split_sel, stream);
+      case 9: return launch_step_g<9, true>(s, a, split_sel, stream);
+      case 10: return launch_step_g<10, true>(s, a, split_sel, stream);
+      case 11: return launch_step_g<11, true>(s, a, split_sel, stream);
+      case 12: return launch_step_g<12, true>(s, a, split_sel, stream);
+      case 13: return launch_step_g<13, true>(s, a, split_sel, stream);
+      case 14: return launch_step_g<14, true>(s, a, split_sel, stream);
+      case 15: return launch_step_g<15, true>(s, a, split_sel, stream);
+      case 16: return launch_step_g<16, true>(s, a, split_sel, stream);
+      default: return hipErrorInvalidValue;
     }
   }
   hipError_t e = launch_select(s, stream);

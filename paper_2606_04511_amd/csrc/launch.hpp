@@ -111,8 +111,12 @@ __host__ __device__ inline void row_windows(const RowGeom& g, const WinGrid& w, 
 // calls with fewer rows than CUs (scored by many workgroups per row).
 bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
-// True when a select call runs the fused decode kernel (one workgroup per row, scores in LDS).
-bool select_is_fused_decode(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
+// Which decode path a select call takes: 0 the fused kernel (one workgroup per row, scores in
+// LDS), 1 the split path (window scores by many workgroups per row into the workspace, then one
+// workgroup per row selects), -1 neither (multi-row or too many windows).
+int select_decode_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid);
+// The split decode path's scoring launch alone (its selection runs in decode_topk_row).
+hipError_t launch_decode_split_scores(const SelectArgs& a, hipStream_t stream);
 // Multi-row tiles of 64 rows with at most kSelTileMaxCand candidates (select_prefill.hip).
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream);
 
@@ -144,10 +148,11 @@ hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream);
 // Split count and blocks per split the attention launcher uses for `rows` query rows.
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
-// One decode step: the select call s, then the attention call a over the sets it writes.  One
-// fused kernel (decode_step_kernel, one workgroup per row and attention split; plus the split
-// combine) where the select takes its fused decode path, G <= 5, k_total <= 1024 and the caches
-// are full; otherwise the two calls.
+// One decode step: the select call s, then the attention call a over the sets it writes.  Where
+// the select takes a decode path (fused, or split: its scoring launch first), G != 6, k_total <=
+// 1024 and the caches are full, one kernel per (row, attention split) selects and attends
+// (decode_step_kernel for G <= 5, decode_step_wide_kernel for 7 <= G <= 16; plus the split
+// combine); otherwise the two calls.
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream);
 // True when a multi-row call takes the tiled kernel (attention_prefill.hip), which needs no
 // workspace: at least 16 rows, 16 % G == 0, and the tile's row bitmaps fit in LDS.

@@ -69,15 +69,6 @@ __global__ __launch_bounds__(256) void rowwise_score_kernel(SelectArgs a, int n_
   }
 }
 
-// Max-pooled score of candidate i (block cand_lo + i) over the window scores w[0 .. ] of windows
-// wf, wf + 1, ...: the windows that overlap the block and are complete at the row's position.
-__device__ __forceinline__ float pooled_score(const float* w, const WinGrid& grid, int32_t j, int32_t wf,
-                                              int32_t wvis) {
-  const int32_t lo = grid_win_lo(grid, j), hi = min(grid_win_hi(grid, j), wvis);
-  float m = w[lo - wf];
-  for (int32_t i = lo + 1; i <= hi; ++i) m = fmaxf(m, w[i - wf]);
-  return m;
-}
 
 // Rows with at most this many candidates keep their pooled block keys in LDS for the radix passes
 // (8 KiB per wavefront); longer rows pool from the workspace on every pass.
@@ -138,42 +129,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_topk_kernel(SelectArgs a) 
   __shared__ int wave_cnt[kDecThreads / 64];
   __shared__ int pick[3];
   const int64_t row = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
-  int16_t* out = a.sel + row * a.k_total;
-  if (wave == 0) emit_forced(out, g, a.k_total, lane);
-  if (tid == 0) a.cnt[row] = (int16_t)(g.n_forced + g.n_take);
-  int16_t* chosen_out = out + g.init_hi;
-  const int C = g.n_cand;
-  if (g.n_take >= C) {
-    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
-    return;
-  }
-  if (g.n_take <= 0) return;
-  int32_t wf, wl;
-  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
-  const int NW = wl - wf + 1;
-  const float* src = a.ws + row * a.ws_stride;
-  // Sixteen loads in flight per thread before any is stored (indices past the row read its last
-  // score again and are not stored): one memory latency per 8192 scores instead of sixteen.
-  constexpr int kLdBatch = 16;
-  for (int b0 = 0; b0 < NW; b0 += kLdBatch * kDecThreads) {
-    float t[kLdBatch];
-#pragma unroll
-    for (int k = 0; k < kLdBatch; ++k) t[k] = src[min(b0 + k * kDecThreads + tid, NW - 1)];
-#pragma unroll
-    for (int k = 0; k < kLdBatch; ++k)
-      if (b0 + k * kDecThreads + tid < NW) sc[b0 + k * kDecThreads + tid] = t[k];
-  }
-  __syncthreads();
-  const float* bs = sc;
-  if (!grid_is_blocks(a.grid)) {
-    const int32_t wvis = grid_win_vis(a.grid, a.q_pos0);
-    for (int i = tid; i < C; i += kDecThreads) sc[NW + i] = pooled_score(sc, a.grid, g.cand_lo + i, wf, wvis);
-    bs = sc + NW;
-    __syncthreads();
-  }
-  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+  decode_topk_row(a, row, sc, hist, wave_cnt, pick, a.sel + row * a.k_total, a.cnt + row);
 }
 
 // Which kernels serve a select call.
@@ -203,8 +159,20 @@ static SelectPath select_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t
   return tile_grid && g.n_cand <= kSelTileMaxCand ? kPathTile : kPathRowwise;
 }
 
-bool select_is_fused_decode(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
-  return select_path(rows, n_q, q_pos0, n_init, n_local, grid) == kPathDecode;
+int select_decode_path(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {
+  const SelectPath path = select_path(rows, n_q, q_pos0, n_init, n_local, grid);
+  return path == kPathDecode ? 0 : path == kPathDecodeSplit ? 1 : -1;
+}
+
+hipError_t launch_decode_split_scores(const SelectArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
+  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
+  int32_t wf, wl;
+  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
+  if (g.n_cand <= 0 || wl < wf) return hipSuccess;
+  const int n_chunks = (wl - wf + 1 + 255) / 256;
+  hipLaunchKernelGGL(rowwise_score_kernel, dim3((unsigned)(rows * n_chunks)), dim3(256), 0, stream, a, n_chunks);
+  return hipGetLastError();
 }
 
 bool select_needs_scratch(int64_t rows, int32_t n_q, int64_t q_pos0, int32_t n_init, int32_t n_local, WinGrid grid) {

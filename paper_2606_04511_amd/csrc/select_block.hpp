@@ -467,4 +467,59 @@ __device__ __forceinline__ void decode_select_row(const SelectArgs& a, int64_t r
   block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
 }
 
+// Max-pooled score of candidate i (block cand_lo + i) over the window scores w[0 .. ] of windows
+// wf, wf + 1, ...: the windows that overlap the block and are complete at the row's position.
+__device__ __forceinline__ float pooled_score(const float* w, const WinGrid& grid, int32_t j, int32_t wf,
+                                              int32_t wvis) {
+  const int32_t lo = grid_win_lo(grid, j), hi = min(grid_win_hi(grid, j), wvis);
+  float m = w[lo - wf];
+  for (int32_t i = lo + 1; i <= hi; ++i) m = fmaxf(m, w[i - wf]);
+  return m;
+}
+
+// The split decode path's selection of row `row`: its window scores are already in the
+// workspace (row stride a.ws_stride, window wf at offset 0).  They are loaded into sc (LDS,
+// kDecodeMaxCand floats), max-pooled to block scores on a windowed grid, and block_topk_emit
+// selects; the set goes to out and the count to *cnt_out, complete once every thread has
+// returned and synchronised.  Every thread of a kDecThreads workgroup must call it.
+__device__ __forceinline__ void decode_topk_row(const SelectArgs& a, int64_t row, float* sc, uint32_t* hist,
+                                                int* wave_cnt, int* pick, int16_t* out, int16_t* cnt_out) {
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const RowGeom g = row_geom(a.q_pos0, a.n_init, a.n_local, a.k_total);
+  if (wave == 0) emit_forced(out, g, a.k_total, lane);
+  if (tid == 0) *cnt_out = (int16_t)(g.n_forced + g.n_take);
+  int16_t* chosen_out = out + g.init_hi;
+  const int C = g.n_cand;
+  if (g.n_take >= C) {
+    for (int i = tid; i < C; i += kDecThreads) chosen_out[i] = (int16_t)(g.cand_lo + i);
+    return;
+  }
+  if (g.n_take <= 0) return;
+  int32_t wf, wl;
+  row_windows(g, a.grid, a.q_pos0, &wf, &wl);
+  const int NW = wl - wf + 1;
+  const float* src = a.ws + row * a.ws_stride;
+  // Sixteen loads in flight per thread before any is stored (indices past the row read its last
+  // score again and are not stored): one memory latency per 8192 scores instead of sixteen.
+  constexpr int kLdBatch = 16;
+  for (int b0 = 0; b0 < NW; b0 += kLdBatch * kDecThreads) {
+    float t[kLdBatch];
+#pragma unroll
+    for (int k = 0; k < kLdBatch; ++k) t[k] = src[min(b0 + k * kDecThreads + tid, NW - 1)];
+#pragma unroll
+    for (int k = 0; k < kLdBatch; ++k)
+      if (b0 + k * kDecThreads + tid < NW) sc[b0 + k * kDecThreads + tid] = t[k];
+  }
+  __syncthreads();
+  const float* bs = sc;
+  if (!grid_is_blocks(a.grid)) {
+    const int32_t wvis = grid_win_vis(a.grid, a.q_pos0);
+    for (int i = tid; i < C; i += kDecThreads) sc[NW + i] = pooled_score(sc, a.grid, g.cand_lo + i, wf, wvis);
+    bs = sc + NW;
+    __syncthreads();
+  }
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+}
+
 }  // namespace sparda

@@ -769,34 +769,39 @@ def test_split_attention_workspace_needs_no_clearing(dev):
 # ----------------------------------------------------------------------------- decode step
 
 DECODE_STEP = [
-    # B, H, G, T, k_total, lw, sw: G <= 5 on the fused decode select path runs the fused kernel
-    # (one workgroup per row and split), the others the two calls
-    (64, 4, 4, 8192, 64, 64, 64),
-    (32, 8, 1, 4096, 16, 64, 64),
-    (128, 2, 2, 6000, 40, 64, 64),  # ragged last block
-    (86, 3, 3, 3000, 24, 64, 64),   # 258 rows
-    (64, 4, 5, 4096, 32, 64, 64),
-    (64, 4, 4, 8192, 96, 32, 16),   # the paper's (32, 16) grid: window scores max-pooled in LDS
-    (64, 4, 4, 200, 16, 64, 64),    # fewer candidates than slots: every candidate is taken
-    (4, 8, 4, 8192, 64, 64, 64),    # 32 rows: 8 splits per row, each split's workgroup selects
-    (1, 2, 4, 4096, 16, 64, 64),    # 2 rows, 2 splits
-    (3, 8, 4, 20000, 200, 64, 64),  # 24 rows, k = 200: splits of 25 blocks
-    (1, 2, 4, 131072, 64, 64, 64),  # 2 rows of 2045 candidates: the split select path, two calls
-    (64, 4, 8, 4096, 32, 64, 64),   # 8 heads: the MFMA P V kernel, two calls
+    # B, H, G, T, k_total, lw, sw, n_local: G != 6 on a decode select path runs one kernel per row
+    # and attention split (the split select path after its scoring launch), the others the two
+    # calls
+    (64, 4, 4, 8192, 64, 64, 64, 2),
+    (32, 8, 1, 4096, 16, 64, 64, 2),
+    (128, 2, 2, 6000, 40, 64, 64, 2),  # ragged last block
+    (86, 3, 3, 3000, 24, 64, 64, 2),   # 258 rows
+    (64, 4, 5, 4096, 32, 64, 64, 2),
+    (64, 4, 4, 8192, 96, 32, 16, 2),   # the paper's (32, 16) grid: window scores max-pooled in LDS
+    (64, 4, 4, 200, 16, 64, 64, 2),    # fewer candidates than slots: every candidate is taken
+    (4, 8, 4, 8192, 64, 64, 64, 2),    # 32 rows: 8 splits per row, each split's workgroup selects
+    (1, 2, 4, 4096, 16, 64, 64, 2),    # 2 rows, 2 splits
+    (3, 8, 4, 20000, 200, 64, 64, 2),  # 24 rows, k = 200: splits of 25 blocks
+    (1, 2, 4, 131072, 64, 64, 64, 2),  # 2 rows of 2045 candidates: the split select path
+    (64, 4, 8, 4096, 32, 64, 64, 2),   # 8 heads: the MFMA P V attention
+    (8, 2, 16, 16384, 64, 64, 64, 2),  # 16 heads, 16 rows: splits
+    (4, 2, 12, 8192, 32, 32, 16, 2),   # 12 heads on the (32, 16) grid
+    (32, 2, 16, 32768, 96, 32, 16, 32),  # the paper's head layout: split select path, 16 heads
+    (64, 4, 6, 4096, 32, 64, 64, 2),   # 6 heads: the two calls
 ]
 
 
-@pytest.mark.parametrize("B,H,G,T,k_total,lw,sw", DECODE_STEP)
-def test_decode_step_matches_separate_calls(dev, B, H, G, T, k_total, lw, sw):
+@pytest.mark.parametrize("B,H,G,T,k_total,lw,sw,n_local", DECODE_STEP)
+def test_decode_step_matches_separate_calls(dev, B, H, G, T, k_total, lw, sw, n_local):
     """sparda_decode_step writes the sets of sparda_forecast_select and the output of
     sparda_sparse_attn over them, bit for bit; a few rows are checked against the oracle too."""
     say(f"decode step B{B} H{H} G{G} T{T} k{k_total} grid ({lw}, {sw})")
     w = inputs.Workload("t", batch=B, seq_len=T, n_q=1, n_kv_heads=H, group_size=G, k_total=k_total, n_init=1,
-                        n_local=2, seed=6100 + T + G)
+                        n_local=n_local, seed=6100 + T + G)
     t_cap = -(-T // 64) * 64
     case = inputs.make_case(w, t_cap=t_cap, device=dev)
     nw = (T - lw) // sw + 1
-    s, o = shapes(B, H, G, k_total, t_cap, nw, lw=lw, sw=sw)
+    s, o = shapes(B, H, G, k_total, t_cap, nw, 1, n_local, lw=lw, sw=sw)
     f, q, k, v = (case[x] for x in ("f", "q", "k", "v"))
     kc = gpu_compress(s, k, T, nw, nw, dev)
     sel, cnt = gpu_select(s, f, 1, T - 1, kc, dev)
@@ -809,7 +814,7 @@ def test_decode_step_matches_separate_calls(dev, B, H, G, T, k_total, lw, sw):
     kc16 = inputs.to_u16(kc)
     n, swaps = compare_selection(o, inputs.to_u16(case["f"]), kc16, 1, T - 1, sel2.cpu().numpy(), cnt2.cpu().numpy(),
                                  rows)
-    _, o1 = shapes(1, 1, G, k_total, t_cap, nw, lw=lw, sw=sw)
+    _, o1 = shapes(1, 1, G, k_total, t_cap, nw, 1, n_local, lw=lw, sw=sw)
     for (b, m, _) in rows:
         k16 = inputs.to_u16(case["k"][b:b + 1, m:m + 1])
         v16 = inputs.to_u16(case["v"][b:b + 1, m:m + 1])
