@@ -211,8 +211,8 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
  * attention over the selected sets (Eq. 5).  The results are those of
  *     sparda_forecast_select(shape, f, 1, q_pos, k_cmp, sel, cnt, ws, ws_bytes, stream);
  *     sparda_sparse_attn(shape, q, 1, q_pos, k, v, 0, sel, cnt, sm_scale, o, ws, ws_bytes, stream);
- * bit for bit.  Where the selection runs one workgroup per row (its scores fit the LDS; at
- * most 1024 windows per row below 256 rows), G <= 5 and k_total <= 1024, one kernel does both
+ * bit for bit.  Where the selection takes a decode path (one workgroup per row, or its
+ * scoring spread over workgroups below 256 rows) and k_total <= 1024, one kernel does both
  * for each (row, attention split): rows that finish their selection early already stream their
  * K and V while others select, and with splits every split's workgroup computes the row's
  * selection itself; otherwise it enqueues the two calls.

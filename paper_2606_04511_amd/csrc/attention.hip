@@ -309,7 +309,7 @@ __global__ __launch_bounds__(NW * 64) void decode_step_kernel(SelectArgs s, Attn
   attend_row<G, NW>(a, row, blockIdx.y, lds, set, set_cnt);
 }
 
-// Decode attention for groups of 7 to 16 heads: P V on MFMA.  With this many query rows per
+// Decode attention for groups of 6 to 16 heads: P V on MFMA.  With this many query rows per
 // block the VALU P V of sparse_attn_kernel (G x 8 FMAs per token per lane) no longer hides under
 // the loads, while P V fills a 16-column MFMA tile.  Per 64-token block a wavefront:
 //   * loads K and V as sparse_attn_kernel does and computes S^T = K Q^T (lane (n, g) holds
@@ -506,7 +506,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void sparse_attn_wide_kernel(AttnA
   attend_row_wide<G>(a, row, blockIdx.y, lds, a.sel + row * a.k_total, a.cnt[row]);
 }
 
-// The decode step with the wide kernel's attention (7 <= G <= 16): as decode_step_kernel.
+// The decode step with the wide kernel's attention (6 <= G <= 16): as decode_step_kernel.
 template <int G, bool kSplitSel>
 __global__ __launch_bounds__(kAttnWaves * 64) void decode_step_wide_kernel(SelectArgs s, AttnArgs a) {
   static_assert(kAttnWaves * 64 == kDecThreads, "the selection runs on the attention workgroup");
@@ -592,9 +592,10 @@ void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks
 template <int G>
 static hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads * a.n_q;
-  // Up to 6 heads: P V on the VALU.  7 to 16 heads: P V on MFMA (sparse_attn_wide_kernel).
+  // Up to 5 heads: P V on the VALU.  6 to 16 heads: P V on MFMA (sparse_attn_wide_kernel; at 6
+  // heads the VALU kernel's accumulators no longer fit beside a block's K and V without spills).
   dim3 grid((unsigned)rows, (unsigned)a.n_splits);
-  if constexpr (G <= 6)
+  if constexpr (G <= 5)
     hipLaunchKernelGGL((sparse_attn_kernel<G, kAttnWaves>), grid, dim3(kAttnWaves * 64), 0, stream, a);
   else
     hipLaunchKernelGGL((sparse_attn_wide_kernel<G>), grid, dim3(kAttnWaves * 64), 0, stream, a);
@@ -628,8 +629,7 @@ static hipError_t launch_step_g(const SelectArgs& s, const AttnArgs& a, bool spl
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.batch * a.n_kv_heads;
   const int path = select_decode_path(rows, 1, s.q_pos0, s.n_init, s.n_local, s.grid);
-  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.k_total <= kStepMaxK && path >= 0 &&
-                     a.group_size != 6;
+  const bool fused = a.n_q == 1 && s.n_q == 1 && a.kv_mode == 0 && a.k_total <= kStepMaxK && path >= 0;
   if (fused) {
     const bool split_sel = path == 1;
     if (split_sel) {
@@ -642,6 +642,7 @@ hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_
       case 3: return launch_step_g<3, false>(s, a, split_sel, stream);
       case 4: return launch_step_g<4, false>(s, a, split_sel, stream);
       case 5: return launch_step_g<5, false>(s, a, split_sel, stream);
+      case 6: return launch_step_g<6, true>(s, a, split_sel, stream);
       case 7: return launch_step_g<7, true>(s, a, split_sel, stream);
       case 8: return launch_step_g<8, true>(s, a, split_sel, stream);
       case 9: return launch_step_g<9, true>(s, a, split_sel, stream);

@@ -149,9 +149,9 @@ hipError_t launch_multihead_select(const SelectArgs& a, hipStream_t stream);
 void attn_plan(int64_t rows, int32_t k_total, int32_t* n_splits, int32_t* blocks_per_split);
 hipError_t launch_sparse_attn(const AttnArgs& a, hipStream_t stream);
 // One decode step: the select call s, then the attention call a over the sets it writes.  Where
-// the select takes a decode path (fused, or split: its scoring launch first), G != 6, k_total <=
-// 1024 and the caches are full, one kernel per (row, attention split) selects and attends
-// (decode_step_kernel for G <= 5, decode_step_wide_kernel for 7 <= G <= 16; plus the split
+// the select takes a decode path (fused, or split: its scoring launch first), k_total <= 1024
+// and the caches are full, one kernel per (row, attention split) selects and attends
+// (decode_step_kernel for G <= 5, decode_step_wide_kernel for 6 <= G <= 16; plus the split
 // combine); otherwise the two calls.
 hipError_t launch_decode_step(const SelectArgs& s, const AttnArgs& a, hipStream_t stream);
 // True when a multi-row call takes the tiled kernel (attention_prefill.hip), which needs no

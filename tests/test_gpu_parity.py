@@ -238,8 +238,9 @@ ATTN = [
     (1, 1, 4, 64, 64, 3),
     (1, 2, 4, 5000, 16, 16),
     (1, 2, 4, 20000, 700, 64),
-    # multi-row, G does not divide 16: the per-row kernel
+    # multi-row, G does not divide 16: the per-row kernels (VALU P V at 3 heads, MFMA at 6)
     (1, 2, 3, 2048, 100, 8),
+    (1, 2, 6, 2048, 100, 8),
 ]
 
 
@@ -787,7 +788,7 @@ DECODE_STEP = [
     (8, 2, 16, 16384, 64, 64, 64, 2),  # 16 heads, 16 rows: splits
     (4, 2, 12, 8192, 32, 32, 16, 2),   # 12 heads on the (32, 16) grid
     (32, 2, 16, 32768, 96, 32, 16, 32),  # the paper's head layout: split select path, 16 heads
-    (64, 4, 6, 4096, 32, 64, 64, 2),   # 6 heads: the two calls
+    (64, 4, 6, 4096, 32, 64, 64, 2),   # 6 heads: the MFMA P V attention
 ]
 
 
