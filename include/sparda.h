@@ -221,8 +221,9 @@ int sparda_sparse_attn(const sparda_shape* shape, const void* q, int32_t n_q, in
  *   sm_scale   : logit scale, finite.
  *   sel, cnt out: the sets, as sparda_forecast_select writes them.
  *   o      out : bf16 [B][Hq][1][D] device.
- *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_DECODE_STEP, n_q = 1)
- *                (0 bytes where the fused kernel runs).
+ *   ws, ws_bytes: device workspace of at least sparda_workspace_size(SPARDA_OP_DECODE_STEP, n_q = 1):
+ *                the selection's window scores, then (256-byte aligned) the attention's split
+ *                partials, side by side (0 bytes when neither is needed).
  * Errors: those of the two calls, all reported before anything is enqueued.
  */
 int sparda_decode_step(const sparda_shape* shape, const void* f, int64_t q_pos, const void* k_cmp, const void* q,

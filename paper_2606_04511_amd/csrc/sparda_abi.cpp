@@ -119,6 +119,19 @@ size_t kl_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0) {
   return kl_keys_bytes(s, n_q, q_pos0) + (size_t)s->batch * s->n_kv_heads * n_q * (size_t)stride * sizeof(float);
 }
 
+size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps);
+
+// Workspace of a decode step: the selection's window scores, then (from a 256-byte aligned
+// offset) the attention's split partials.  The two live side by side because the fused kernel's
+// workgroups still read scores while others write partials.  *attn_off gets the offset.
+size_t step_ws(const sparda_shape* s, int64_t q_pos, size_t* attn_off) {
+  int64_t stride;
+  int32_t ns, bps;
+  const size_t a = (select_ws(s, 1, q_pos, &stride) + 255) & ~(size_t)255, b = attn_ws(s, 1, q_pos, &ns, &bps);
+  if (attn_off) *attn_off = a;
+  return b > 0 ? a + b : a;
+}
+
 size_t attn_ws(const sparda_shape* s, int32_t n_q, int64_t q_pos0, int32_t* n_splits, int32_t* bps) {
   if (sparda::attn_uses_tiles(s->group_size, n_q, q_pos0)) {  // tiled multi-row kernel: no partials
     *n_splits = 1;
@@ -308,10 +321,7 @@ int sparda_workspace_size(const sparda_shape* shape, int32_t op, int32_t n_q, in
     *bytes = kl_ws(shape, n_q, q_pos0);
   } else if (op == SPARDA_OP_DECODE_STEP) {
     if (n_q != 1) return fail(SPARDA_ERR_INVALID_ARG, "a decode step has n_q == 1");
-    int64_t stride;
-    int32_t ns, bps;
-    const size_t a = select_ws(shape, 1, q_pos0, &stride), b = attn_ws(shape, 1, q_pos0, &ns, &bps);
-    *bytes = a > b ? a : b;
+    *bytes = step_ws(shape, q_pos0, nullptr);
   } else {
     return fail(SPARDA_ERR_INVALID_ARG, "unknown op %d", op);
   }
@@ -349,9 +359,17 @@ int sparda_decode_step(const sparda_shape* shape, const void* f, int64_t q_pos, 
                        size_t ws_bytes, hipStream_t stream) {
   sparda::SelectArgs sa;
   sparda::AttnArgs aa;
-  int rc = select_prepare(shape, f, 1, q_pos, k_cmp, sel, cnt, ws, ws_bytes, &sa);
+  int rc = check_shape(shape);
   if (rc) return rc;
-  if ((rc = attn_prepare(shape, q, 1, q_pos, k, v, 0, sel, cnt, sm_scale, o, ws, ws_bytes, false, &aa))) return rc;
+  if ((rc = check_rows(shape, 1, q_pos))) return rc;
+  size_t off = 0;
+  const size_t need = step_ws(shape, q_pos, &off);
+  // each half checks its arguments and its part of the workspace, then the whole is checked
+  if ((rc = select_prepare(shape, f, 1, q_pos, k_cmp, sel, cnt, ws, off, &sa))) return rc;
+  void* ws_att = (ws && need > off) ? static_cast<char*>(ws) + off : nullptr;
+  if ((rc = attn_prepare(shape, q, 1, q_pos, k, v, 0, sel, cnt, sm_scale, o, ws_att, need - off, false, &aa)))
+    return rc;
+  if (need > 0 && ws_bytes < need) return fail(SPARDA_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   return hip_status(sparda::launch_decode_step(sa, aa, stream), "decode step launch");
 
 }

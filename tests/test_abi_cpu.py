@@ -215,10 +215,19 @@ def test_decode_step_argument_errors(lib):
     assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, float("inf"), FAKE, FAKE, FAKE, None, 0, 0) == \
         sp.SPARDA_ERR_INVALID_ARG
     assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, None, None, 0, 0) == sp.SPARDA_ERR_INVALID_ARG
-    # 16 rows: the attention splits its rows, so the step needs the attention's workspace
+    # 16 rows: the attention splits its rows, so the step needs the attention's workspace beside
+    # the selection's (256-byte aligned), since the fused kernel's workgroups read scores while
+    # others write partials
     need = sp.sparda_workspace_size(s, sp.SPARDA_OP_DECODE_STEP, 1, 4095)
-    assert need == max(sp.sparda_workspace_size(s, sp.SPARDA_OP_FORECAST_SELECT, 1, 4095),
-                       sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, 4095)) > 0
+    sel_ws = sp.sparda_workspace_size(s, sp.SPARDA_OP_FORECAST_SELECT, 1, 4095)
+    att_ws = sp.sparda_workspace_size(s, sp.SPARDA_OP_SPARSE_ATTN, 1, 4095)
+    assert att_ws > 0 and need == -(-sel_ws // 256) * 256 + att_ws
+    # 2 rows of 2045 windows: the split select path's scores and the attention's partials
+    s2 = shape(batch=1, n_kv_heads=2, k_total=64, t_cap=131072, nc_cap=2048)
+    sel_ws = sp.sparda_workspace_size(s2, sp.SPARDA_OP_FORECAST_SELECT, 1, 131071)
+    att_ws = sp.sparda_workspace_size(s2, sp.SPARDA_OP_SPARSE_ATTN, 1, 131071)
+    assert sel_ws > 0 and att_ws > 0
+    assert sp.sparda_workspace_size(s2, sp.SPARDA_OP_DECODE_STEP, 1, 131071) == -(-sel_ws // 256) * 256 + att_ws
     assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, None, 0, 0) == sp.SPARDA_ERR_WORKSPACE
     assert rc_of(d, s, FAKE, 4095, FAKE, FAKE, FAKE, FAKE, sc, FAKE, FAKE, FAKE, FAKE, need - 16, 0) == \
         sp.SPARDA_ERR_WORKSPACE

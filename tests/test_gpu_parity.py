@@ -788,6 +788,9 @@ DECODE_STEP = [
     (8, 2, 16, 16384, 64, 64, 64, 2),  # 16 heads, 16 rows: splits
     (4, 2, 12, 8192, 32, 32, 16, 2),   # 12 heads on the (32, 16) grid
     (32, 2, 16, 32768, 96, 32, 16, 32),  # the paper's head layout: split select path, 16 heads
+    # 200 rows x 2 splits on the split select path: more workgroups than CUs, so some read their
+    # row's window scores after others have written attention partials (separate workspace parts)
+    (100, 2, 4, 16448, 64, 32, 16, 2),
     (64, 4, 6, 4096, 32, 64, 64, 2),   # 6 heads: the MFMA P V attention
 ]
 
