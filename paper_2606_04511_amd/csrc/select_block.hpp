@@ -231,39 +231,56 @@ __device__ __forceinline__ int lin_bin(float s, float lo, float scale) {
 // LDS use: hist[0 .. 256) histogram, [256 .. 272) wavefront extremes, then the emission's
 // wavefront counts (two alternating sets of 8), [272 .. 400) the threshold bin's (key, index)
 // pairs, [400] their count.
-__device__ __forceinline__ void block_topk_emit(const float* bs, int C, int n_take, int cand_lo, int16_t* chosen_out,
-                                                uint32_t* hist, int* wave_cnt, int* pick) {
-  constexpr int kPer = 4, kRun = kPer * kDecThreads, kWaves = kDecThreads / 64;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint32_t* ext = hist + 256;
-  uint32_t* list = hist + 272;
-  uint32_t* list_n = hist + 400;
-  // extremes of the keys: DPP inside 16-lane rows, then the four rows' results
-  uint32_t kmin = 0xffffffffu, kmax = 0u;
-  for (int c0 = 0; c0 < C; c0 += kRun) {
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) {
-      const int i = c0 + kPer * tid + e;
-      if (i < C) {
-        const uint32_t kk = score_key(bs[i]);
-        kmin = min(kmin, kk);
-        kmax = max(kmax, kk);
-      }
-    }
-  }
+// Publish one wavefront's key extremes (kmin, kmax: per lane) for block_topk_emit: DPP inside
+// 16-lane rows, then the four rows' results, into hist[256 + wave] and hist[264 + wave].
+__device__ __forceinline__ void topk_publish_extremes(uint32_t kmin, uint32_t kmax, uint32_t* hist) {
+  constexpr int kWaves = kDecThreads / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   kmin = row16_min(kmin);
   kmax = row16_max(kmax);
   kmin = min(min((uint32_t)readlane_i((int)kmin, 0), (uint32_t)readlane_i((int)kmin, 16)),
              min((uint32_t)readlane_i((int)kmin, 32), (uint32_t)readlane_i((int)kmin, 48)));
   kmax = max(max((uint32_t)readlane_i((int)kmax, 0), (uint32_t)readlane_i((int)kmax, 16)),
              max((uint32_t)readlane_i((int)kmax, 32), (uint32_t)readlane_i((int)kmax, 48)));
-  if (tid < 256) hist[tid] = 0u;
-  if (tid == 0) *list_n = 0u;
   if (lane == 0) {
-    ext[wave] = kmin;
-    ext[kWaves + wave] = kmax;
+    hist[256 + wave] = kmin;
+    hist[256 + kWaves + wave] = kmax;
   }
-  __syncthreads();
+}
+
+// hist's state that block_topk_emit expects when its caller prepared it (prepared = true): the
+// histogram and the threshold bin's count cleared, and every wavefront's key extremes published
+// (topk_publish_extremes over keys that bound every score of bs), followed by a barrier.
+__device__ __forceinline__ void topk_clear(uint32_t* hist) {
+  const int tid = threadIdx.x;
+  if (tid < 256) hist[tid] = 0u;
+  if (tid == 0) hist[400] = 0u;
+}
+
+__device__ __forceinline__ void block_topk_emit(const float* bs, int C, int n_take, int cand_lo, int16_t* chosen_out,
+                                                uint32_t* hist, int* wave_cnt, int* pick, bool prepared = false) {
+  constexpr int kPer = 4, kRun = kPer * kDecThreads, kWaves = kDecThreads / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint32_t* ext = hist + 256;
+  uint32_t* list = hist + 272;
+  uint32_t* list_n = hist + 400;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  if (!prepared) {  // extremes of the keys
+    for (int c0 = 0; c0 < C; c0 += kRun) {
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        const int i = c0 + kPer * tid + e;
+        if (i < C) {
+          const uint32_t kk = score_key(bs[i]);
+          kmin = min(kmin, kk);
+          kmax = max(kmax, kk);
+        }
+      }
+    }
+    topk_publish_extremes(kmin, kmax, hist);
+    topk_clear(hist);
+    __syncthreads();
+  }
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
     kmin = min(kmin, ext[w]);
@@ -417,6 +434,8 @@ __device__ __forceinline__ void decode_select_row(const SelectArgs& a, int64_t r
     // Double-buffered: the next 64 windows' loads are in flight while this wave scores the
     // current ones.
     uint4 kw[16], kn[16];
+    uint32_t kmin = 0xffffffffu, kmax = 0u;  // key extremes of the scores this lane stores
+    topk_clear(hist);
     // Indices past the last window read the last one again (never stored), so the loads stay
     // branch-free.
     auto load = [&](int base, uint4 (&w)[16]) {
@@ -442,11 +461,19 @@ __device__ __forceinline__ void decode_select_row(const SelectArgs& a, int64_t r
         d = fmaf(f7, bf16hi(kw[i].w), d);
         d = row16_sum(d);
         const int idx = base + 4 * i + rs;
-        if (c == 0 && idx < NW) sc[idx] = d;
+        if (c == 0 && idx < NW) {
+          sc[idx] = d;
+          const uint32_t kk = score_key(d);
+          kmin = min(kmin, kk);
+          kmax = max(kmax, kk);
+        }
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) kw[i] = kn[i];
     }
+    // the window scores bound the (max-pooled) block scores: the top-k's bins need no pass of
+    // their own
+    topk_publish_extremes(kmin, kmax, hist);
   }
   __syncthreads();
   // Block scores: the window scores themselves, or their max-pool into sc[NW .. NW + C).
@@ -464,7 +491,7 @@ __device__ __forceinline__ void decode_select_row(const SelectArgs& a, int64_t r
     __syncthreads();
   }
 
-  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick, true);
 }
 
 // Max-pooled score of candidate i (block cand_lo + i) over the window scores w[0 .. ] of windows
@@ -503,14 +530,22 @@ __device__ __forceinline__ void decode_topk_row(const SelectArgs& a, int64_t row
   // Sixteen loads in flight per thread before any is stored (indices past the row read its last
   // score again and are not stored): one memory latency per 8192 scores instead of sixteen.
   constexpr int kLdBatch = 16;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;  // key extremes of the scores this thread stores
+  topk_clear(hist);
   for (int b0 = 0; b0 < NW; b0 += kLdBatch * kDecThreads) {
     float t[kLdBatch];
 #pragma unroll
     for (int k = 0; k < kLdBatch; ++k) t[k] = src[min(b0 + k * kDecThreads + tid, NW - 1)];
 #pragma unroll
     for (int k = 0; k < kLdBatch; ++k)
-      if (b0 + k * kDecThreads + tid < NW) sc[b0 + k * kDecThreads + tid] = t[k];
+      if (b0 + k * kDecThreads + tid < NW) {
+        sc[b0 + k * kDecThreads + tid] = t[k];
+        const uint32_t kk = score_key(t[k]);
+        kmin = min(kmin, kk);
+        kmax = max(kmax, kk);
+      }
   }
+  topk_publish_extremes(kmin, kmax, hist);
   __syncthreads();
   const float* bs = sc;
   if (!grid_is_blocks(a.grid)) {
@@ -519,7 +554,7 @@ __device__ __forceinline__ void decode_topk_row(const SelectArgs& a, int64_t row
     bs = sc + NW;
     __syncthreads();
   }
-  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick);
+  block_topk_emit(bs, C, g.n_take, g.cand_lo, chosen_out, hist, wave_cnt, pick, true);
 }
 
 }  // namespace sparda
