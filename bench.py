@@ -343,8 +343,10 @@ def prefill_leg(dev, warmup, iters, flush=None):
     def select_grid():
         sp.sparda_forecast_select(shape_g, case["f"], T, 0, kc_g, sel, cnt, ws_g)
 
-    select_grid()
-    ms_sel_g = time_events(select_grid, max(2, iters // 5), stream)
+    for _ in range(max(1, warmup)):
+        select_grid()
+    ms_sel_g = time_events(select_grid, iters, stream)
+    sel_g_stats = rep_stats(select_grid, max(50, iters), stream, flush)
     del kc_g, ws_g
     # scored (row, candidate) pairs: rows whose candidates outnumber their free slots
     flops = 0
@@ -380,6 +382,7 @@ def prefill_leg(dev, warmup, iters, flush=None):
         "attn_ms": ms_att,
         "attn_tflops": attn_flops / (ms_att * 1e-3) / 1e12,
         "select_grid_32_16_ms": ms_sel_g,
+        "select_grid_32_16_stats": sel_g_stats,
         "score_only_ms": ms_score,
         "score_only_gflop": score_flops / 1e9,
         "score_only_tflops": score_flops / (ms_score * 1e-3) / 1e12,
@@ -503,7 +506,7 @@ def paper_config_leg(dev, warmup, steps):
     att_fn()
     torch.cuda.synchronize()
     res["prefill"] = {"workload": "prefill B1 T=32768 Hq32/Hkv2 D128 block64 k96 (1 init + 32 local), (32, 16) grid, "
-                                  "all rows", "select_ms": time_events(sel_fn, max(3, steps // 10), stream),
+                                  "all rows", "select_ms": time_events(sel_fn, max(10, steps), stream),
                       "attn_ms": time_events(att_fn, 3, stream)}
     return res
 

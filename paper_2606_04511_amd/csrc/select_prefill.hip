@@ -65,7 +65,7 @@ constexpr int kPsMaxUnits = 256;                // units per (batch, group)
 struct PrefillPlan {
   int32_t n_slices;                   // slices per (batch, group)
   int32_t units;                      // units per (batch, group)
-  uint16_t bound[kPsMaxUnits + 1];    // unit u owns slices [bound[u], bound[u + 1])
+  uint16_t bound[kPsMaxUnits + 1];    // block grid: unit u owns slices [bound[u], bound[u + 1])
 };
 
 // Sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one query row); every one of them receives it.
@@ -647,15 +647,23 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
-  const int s_begin = plan.bound[u], s_end = plan.bound[u + 1];
-  if (s_begin >= s_end) return;
+  // Rounds of U consecutive groups of kPwWaves slices: unit u takes group u of every even round
+  // and group U - 1 - u of every odd one.  A group's cost grows with its position, so this
+  // back-and-forth order gives every unit about the same work without a cost model.
+  const int ns = plan.n_slices, U = plan.units;
+  const int ng = (ns + kPwWaves - 1) / kPwWaves;
+  if (u >= ng) return;  // uniform over the workgroup
+  auto group_of = [&](int i) { return i * U + ((i & 1) ? U - 1 - u : u); };
+  auto group_hi = [&](int gi) { return min(ns, kPwWaves * (gi + 1)); };
+  int i_top = (ng - 1) / U;                // the last round, partial unless U divides ng
+  if (group_of(i_top) >= ng) --i_top;      // then it may not reach this unit (round 0 always does)
   const int lr = lane & 15, lg = lane >> 4;
   const int opitch = pw_out_pitch(a.k_total);
   int16_t* ost = reinterpret_cast<int16_t*>(wst) + wave * kPsRows * opitch;  // this wavefront's set rows
   const uint16_t* kcg = a.kc + bm * a.nc_cap * kHeadDim;  // the group's window keys
-  auto load_f = [&](int s, uint4 (&fw)[4]) {
+  auto load_f = [&](int s, int s_lo, uint4 (&fw)[4]) {
     const int r = s * kPsRows + lr;
-    if (s >= s_begin && r < a.n_q) {
+    if (s >= s_lo && r < a.n_q) {
       const uint16_t* fp = a.f + (bm * a.n_q + r) * kHeadDim + 8 * lg;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) fw[ks] = ld16(fp + 32 * ks);
@@ -666,11 +674,13 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
   };
 
   uint4 fnext[4];
-  load_f(s_end - 1 - wave, fnext);
-  // Groups from the end of the range (most candidates first); wavefront w takes slice g_hi - 1 - w.
-  for (int g_hi = s_end; g_hi > s_begin; g_hi -= kPwWaves) {
+  load_f(group_hi(group_of(i_top)) - 1 - wave, kPwWaves * group_of(i_top), fnext);
+  // Rounds from the last (most candidates first); wavefront w takes slice g_hi - 1 - w.
+  for (int i = i_top; i >= 0; --i) {
+    const int gi = group_of(i);
+    const int g_lo = kPwWaves * gi, g_hi = group_hi(gi);
     const int s = g_hi - 1 - wave;
-    const bool have = s >= s_begin;
+    const bool have = s >= g_lo;
     uint4 fw[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
@@ -818,7 +828,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
       __syncthreads();  // the previous group's set rows have left the buffers
     }
     // the next group's F rows, requested after the scoring, whose registers they would crowd
-    load_f(s - kPwWaves, fnext);
+    if (i > 0) load_f(group_hi(group_of(i - 1)) - 1 - wave, kPwWaves * group_of(i - 1), fnext);
     if (kStaged) forced();  // the buffers are free now
 
     if (score) {
@@ -842,9 +852,8 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
 }
 
 // Splits every (batch, group)'s slices into `units` ranges of about equal estimated cost.  Per
-// slice, measured on the 32K prefill: about 230 candidates' worth of fixed work plus one unit per
-// candidate when its rows are scored (`per_cand` units on the window grid, which scores four
-// windows per candidate), and about 40 when they take every candidate.
+// slice, measured on the 32K prefill: about 230 candidates' worth of fixed work plus `per_cand`
+// units per candidate when its rows are scored, and about 40 when they take every candidate.
 static void plan_units(const SelectArgs& a, int units, int per_cand, PrefillPlan* plan) {
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
   plan->n_slices = ns;
@@ -868,33 +877,6 @@ static void plan_units(const SelectArgs& a, int units, int per_cand, PrefillPlan
   plan->bound[units] = (uint16_t)ns;
 }
 
-// The window-grid kernel scores kPwWaves slices at a time in lockstep: units take whole groups of
-// kPwWaves slices (aligned from slice 0), costed by the group's last slice.
-static void plan_unit_groups(const SelectArgs& a, int units, int per_cand, PrefillPlan* plan) {
-  const int ns = (a.n_q + kPsRows - 1) / kPsRows;
-  const int ng = (ns + kPwWaves - 1) / kPwWaves;
-  plan->n_slices = ns;
-  plan->units = units;
-  auto cost = [&](int gi) -> int64_t {
-    const int s_last = std::min(ns, (gi + 1) * kPwWaves) - 1;
-    const RowGeom g = row_geom(a.q_pos0 + std::min<int64_t>(a.n_q, (int64_t)(s_last + 1) * kPsRows) - 1, a.n_init,
-                               a.n_local, a.k_total);
-    if (g.n_take >= g.n_cand) return 40;
-    return 230 + per_cand * 16 * ((g.n_cand + 15) / 16);
-  };
-  int64_t total = 0;
-  for (int gi = 0; gi < ng; ++gi) total += cost(gi);
-  int64_t acc = 0;
-  int gi = 0;
-  plan->bound[0] = 0;
-  for (int uu = 1; uu < units; ++uu) {
-    const int64_t target = total * uu / units;
-    while (gi < ng && acc + cost(gi) <= target) acc += cost(gi++);
-    plan->bound[uu] = (uint16_t)std::min(ns, gi * kPwWaves);
-  }
-  plan->bound[units] = (uint16_t)ns;
-}
-
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int n_groups = a.batch * a.n_kv_heads;
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
@@ -905,11 +887,15 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int units_target = win ? 512 : 256;
   int units = n_groups >= units_target ? 1 : units_target / n_groups;
   units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
-  PrefillPlan plan;
-  if (win)
-    plan_unit_groups(a, units, 3, &plan);
-  else
+  PrefillPlan plan{};
+  if (win) {
+    // the window-grid kernel takes its groups of slices by unit index in back-and-forth rounds
+    units = std::min(units, (ns + kPwWaves - 1) / kPwWaves);
+    plan.n_slices = ns;
+    plan.units = units;
+  } else {
     plan_units(a, units, 1, &plan);
+  }
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
   if (win && a.k_total <= kPwStageKMax)
