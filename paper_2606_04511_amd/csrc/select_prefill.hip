@@ -7,10 +7,11 @@
 // boundary inside the slice (those have one candidate less, masked below); each row takes its own
 // top-k.
 //
-// Workgroups are persistent units of 8 wavefronts, one unit per (batch, group) and slice range.
-// A host-side plan splits every group's slices into ranges of equal estimated cost; the unit
-// stages the K~ rows of its largest candidate range in LDS once (272-byte row pitch), then its
-// wavefronts take slices from an LDS counter, most candidates first.
+// Workgroups are persistent units of 8 wavefronts, several per (batch, group).  Unit u of U takes
+// slice u of every even round of U consecutive slices and slice U - 1 - u of every odd one, which
+// evens out the work (a slice's cost grows with its position).  The unit stages the K~ rows of
+// its largest candidate range in LDS once (272-byte row pitch), then its wavefronts take its
+// slices from an LDS counter, most candidates first.
 //
 // Per slice:
 //   1. S^T = K~ F^T on v_mfma_f32_16x16x32_bf16: B = the slice's 16 F rows (straight from HBM,
@@ -63,9 +64,8 @@ constexpr int kPsOutPitch = kPsStageK + 8;      // int16 per staged set row: row
 constexpr int kPsMaxUnits = 256;                // units per (batch, group)
 
 struct PrefillPlan {
-  int32_t n_slices;                   // slices per (batch, group)
-  int32_t units;                      // units per (batch, group)
-  uint16_t bound[kPsMaxUnits + 1];    // block grid: unit u owns slices [bound[u], bound[u + 1])
+  int32_t n_slices;  // slices per (batch, group)
+  int32_t units;     // units per (batch, group)
 };
 
 // Sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one query row); every one of them receives it.
@@ -439,19 +439,26 @@ template <bool kStaged>
 __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
   __shared__ __align__(16) uint16_t kst[kPsStageRows * kPsPitch];
   __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsOutPitch : 8];
-  __shared__ int next_slice;
+  __shared__ int next_round;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
-  const int s_begin = plan.bound[u], s_end = plan.bound[u + 1];
-  if (s_begin >= s_end) return;
+  // Rounds of U consecutive slices: unit u takes slice u of every even round and slice U - 1 - u
+  // of every odd one.  A slice's cost grows with its position, so this back-and-forth order gives
+  // every unit about the same work without a cost model.
+  const int ns = plan.n_slices, U = plan.units;
+  if (u >= ns) return;  // uniform over the workgroup
+  auto slice_of = [&](int i) { return i < 0 ? -1 : i * U + ((i & 1) ? U - 1 - u : u); };
+  int i_top = (ns - 1) / U;             // the last round, partial unless U divides ns
+  if (slice_of(i_top) >= ns) --i_top;   // then it may not reach this unit (round 0 always does)
+  const int s_last = slice_of(i_top);   // the unit's last slice
 
   // ---- stage the K~ rows of the unit's largest candidate range (its last row), zero-padded to
   // whole M-tiles and the read-ahead rows.  Rows that take every candidate are never scored, and
   // neither is a unit whose last row takes every candidate (earlier rows have at most as many
   // candidates and at least as large a budget).
   {
-    const RowGeom gl = row_geom(a.q_pos0 + min(a.n_q, s_end * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
+    const RowGeom gl = row_geom(a.q_pos0 + min(a.n_q, (s_last + 1) * kPsRows) - 1, a.n_init, a.n_local, a.k_total);
     const int c_stage = gl.n_take < gl.n_cand ? gl.n_cand : 0;
     const int c_fill = c_stage > 0 ? ((c_stage + 15) & ~15) + 8 : 0;
     const uint16_t* kcb = a.kc + (bm * a.nc_cap + a.n_init) * kHeadDim;
@@ -461,20 +468,20 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       *reinterpret_cast<uint4*>(kst + c * kPsPitch + part * 8) = w;
     }
   }
-  if (tid == 0) next_slice = s_end - 1;
+  if (tid == 0) next_round = i_top;
   __syncthreads();
 
   const int lr = lane & 15, lg = lane >> 4;
   int16_t* ost = ost_all + (kStaged ? wave * kPsRows * kPsOutPitch : 0);
-  // Slices are taken from the end of the range (most candidates first).
+  // Rounds are taken from the last (most candidates first); -1 once none is left.
   auto grab = [&]() -> int {
-    int s = 0;
-    if (lane == 0) s = atomicSub(&next_slice, 1);
-    return __builtin_amdgcn_readfirstlane(s);
+    int i = 0;
+    if (lane == 0) i = atomicSub(&next_round, 1);
+    return slice_of(__builtin_amdgcn_readfirstlane(i));
   };
   auto load_f = [&](int s, uint4 (&fw)[4]) {
     const int r = s * kPsRows + lr;
-    if (s >= s_begin && r < a.n_q) {
+    if (s >= 0 && r < a.n_q) {
       const uint16_t* fp = a.f + (bm * a.n_q + r) * kHeadDim + 8 * lg;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) fw[ks] = ld16(fp + 32 * ks);
@@ -489,7 +496,7 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
   uint4 fnext[4];
   load_f(s, fnext);
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the first slice's F is in registers
-  while (s >= s_begin) {
+  while (s >= 0) {
     uint4 fw[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) fw[ks] = fnext[ks];
@@ -851,32 +858,6 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
   }
 }
 
-// Splits every (batch, group)'s slices into `units` ranges of about equal estimated cost.  Per
-// slice, measured on the 32K prefill: about 230 candidates' worth of fixed work plus `per_cand`
-// units per candidate when its rows are scored, and about 40 when they take every candidate.
-static void plan_units(const SelectArgs& a, int units, int per_cand, PrefillPlan* plan) {
-  const int ns = (a.n_q + kPsRows - 1) / kPsRows;
-  plan->n_slices = ns;
-  plan->units = units;
-  auto cost = [&](int s) -> int64_t {
-    const RowGeom g = row_geom(a.q_pos0 + std::min<int64_t>(a.n_q, (int64_t)(s + 1) * kPsRows) - 1, a.n_init,
-                               a.n_local, a.k_total);
-    if (g.n_take >= g.n_cand) return 40;
-    return 230 + per_cand * 16 * ((g.n_cand + 15) / 16);
-  };
-  int64_t total = 0;
-  for (int s = 0; s < ns; ++s) total += cost(s);
-  int64_t acc = 0;
-  int s = 0;
-  plan->bound[0] = 0;
-  for (int uu = 1; uu < units; ++uu) {
-    const int64_t target = total * uu / units;
-    while (s < ns && acc + cost(s) <= target) acc += cost(s++);
-    plan->bound[uu] = (uint16_t)s;
-  }
-  plan->bound[units] = (uint16_t)ns;
-}
-
 hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int n_groups = a.batch * a.n_kv_heads;
   const int ns = (a.n_q + kPsRows - 1) / kPsRows;
@@ -887,15 +868,12 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   const int units_target = win ? 512 : 256;
   int units = n_groups >= units_target ? 1 : units_target / n_groups;
   units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
-  PrefillPlan plan{};
-  if (win) {
-    // the window-grid kernel takes its groups of slices by unit index in back-and-forth rounds
-    units = std::min(units, (ns + kPwWaves - 1) / kPwWaves);
-    plan.n_slices = ns;
-    plan.units = units;
-  } else {
-    plan_units(a, units, 1, &plan);
-  }
+  // Both kernels take their slices (window grid: groups of kPwWaves slices) by unit index in
+  // back-and-forth rounds.
+  if (win) units = std::min(units, (ns + kPwWaves - 1) / kPwWaves);
+  PrefillPlan plan;
+  plan.n_slices = ns;
+  plan.units = units;
   const dim3 grid((unsigned)((int64_t)n_groups * units));
   const bool staged = a.k_total <= kPsStageK;
   if (win && a.k_total <= kPwStageKMax)
