@@ -8,7 +8,7 @@
 // top-k.
 //
 // Workgroups are persistent units of 8 wavefronts, several per (batch, group).  Unit u of U takes
-// slice u of every even round of U consecutive slices and slice U - 1 - u of every odd one, which
+// slice u of every even sweep of U consecutive slices and slice U - 1 - u of every odd one, which
 // evens out the work (a slice's cost grows with its position).  The unit stages the K~ rows of
 // its largest candidate range in LDS once (272-byte row pitch), then its wavefronts take its
 // slices from an LDS counter, most candidates first.
@@ -439,18 +439,18 @@ template <bool kStaged>
 __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a, PrefillPlan plan, int n_groups) {
   __shared__ __align__(16) uint16_t kst[kPsStageRows * kPsPitch];
   __shared__ __align__(16) int16_t ost_all[kStaged ? kPsWaves * kPsRows * kPsOutPitch : 8];
-  __shared__ int next_round;
+  __shared__ int next_sweep;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
-  // Rounds of U consecutive slices: unit u takes slice u of every even round and slice U - 1 - u
+  // Sweeps of U consecutive slices: unit u takes slice u of every even sweep and slice U - 1 - u
   // of every odd one.  A slice's cost grows with its position, so this back-and-forth order gives
   // every unit about the same work without a cost model.
   const int ns = plan.n_slices, U = plan.units;
   if (u >= ns) return;  // uniform over the workgroup
   auto slice_of = [&](int i) { return i < 0 ? -1 : i * U + ((i & 1) ? U - 1 - u : u); };
-  int i_top = (ns - 1) / U;             // the last round, partial unless U divides ns
-  if (slice_of(i_top) >= ns) --i_top;   // then it may not reach this unit (round 0 always does)
+  int i_top = (ns - 1) / U;             // the last sweep, partial unless U divides ns
+  if (slice_of(i_top) >= ns) --i_top;   // then it may not reach this unit (the first sweep always does)
   const int s_last = slice_of(i_top);   // the unit's last slice
 
   // ---- stage the K~ rows of the unit's largest candidate range (its last row), zero-padded to
@@ -468,15 +468,15 @@ __global__ __launch_bounds__(kPsThreads) void prefill_select_kernel(SelectArgs a
       *reinterpret_cast<uint4*>(kst + c * kPsPitch + part * 8) = w;
     }
   }
-  if (tid == 0) next_round = i_top;
+  if (tid == 0) next_sweep = i_top;
   __syncthreads();
 
   const int lr = lane & 15, lg = lane >> 4;
   int16_t* ost = ost_all + (kStaged ? wave * kPsRows * kPsOutPitch : 0);
-  // Rounds are taken from the last (most candidates first); -1 once none is left.
+  // Sweeps are taken from the last (most candidates first); -1 once none is left.
   auto grab = [&]() -> int {
     int i = 0;
-    if (lane == 0) i = atomicSub(&next_round, 1);
+    if (lane == 0) i = atomicSub(&next_sweep, 1);
     return slice_of(__builtin_amdgcn_readfirstlane(i));
   };
   auto load_f = [&](int s, uint4 (&fw)[4]) {
@@ -654,7 +654,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bm = blockIdx.x % n_groups;
   const int u = (int)(blockIdx.x / n_groups);
-  // Rounds of U consecutive groups of kPwWaves slices: unit u takes group u of every even round
+  // Sweeps of U consecutive groups of kPwWaves slices: unit u takes group u of every even sweep
   // and group U - 1 - u of every odd one.  A group's cost grows with its position, so this
   // back-and-forth order gives every unit about the same work without a cost model.
   const int ns = plan.n_slices, U = plan.units;
@@ -662,8 +662,8 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
   if (u >= ng) return;  // uniform over the workgroup
   auto group_of = [&](int i) { return i * U + ((i & 1) ? U - 1 - u : u); };
   auto group_hi = [&](int gi) { return min(ns, kPwWaves * (gi + 1)); };
-  int i_top = (ng - 1) / U;                // the last round, partial unless U divides ng
-  if (group_of(i_top) >= ng) --i_top;      // then it may not reach this unit (round 0 always does)
+  int i_top = (ng - 1) / U;                // the last sweep, partial unless U divides ng
+  if (group_of(i_top) >= ng) --i_top;      // then it may not reach this unit (the first sweep always does)
   const int lr = lane & 15, lg = lane >> 4;
   const int opitch = pw_out_pitch(a.k_total);
   int16_t* ost = reinterpret_cast<int16_t*>(wst) + wave * kPsRows * opitch;  // this wavefront's set rows
@@ -682,7 +682,7 @@ __global__ __launch_bounds__(kPwThreads, 2) void prefill_select_win_kernel(Selec
 
   uint4 fnext[4];
   load_f(group_hi(group_of(i_top)) - 1 - wave, kPwWaves * group_of(i_top), fnext);
-  // Rounds from the last (most candidates first); wavefront w takes slice g_hi - 1 - w.
+  // Sweeps from the last (most candidates first); wavefront w takes slice g_hi - 1 - w.
   for (int i = i_top; i >= 0; --i) {
     const int gi = group_of(i);
     const int g_lo = kPwWaves * gi, g_hi = group_hi(gi);
@@ -869,7 +869,7 @@ hipError_t launch_prefill_select(const SelectArgs& a, hipStream_t stream) {
   int units = n_groups >= units_target ? 1 : units_target / n_groups;
   units = std::max(1, std::min(units, std::min(ns, kPsMaxUnits)));
   // Both kernels take their slices (window grid: groups of kPwWaves slices) by unit index in
-  // back-and-forth rounds.
+  // back-and-forth sweeps.
   if (win) units = std::min(units, (ns + kPwWaves - 1) / kPwWaves);
   PrefillPlan plan;
   plan.n_slices = ns;

@@ -966,7 +966,7 @@ GRID_PREFILL = [
     (1, 2, 32960, 500, 32460, 64, 2, 1),    # the last row has 512 candidates: the tile kernel's maximum
     (1, 2, 36000, 200, 35800, 64, 2, 1),    # more candidates: the row-wise path (MFMA window scores)
     (1, 1, 70000, 130, 69870, 40, 1, 1),    # 2176 windows per row, one local block: edge windows
-    (1, 2, 21000, 19000, 2000, 64, 2, 1),   # 297 slice groups on 256 units: a partial second round
+    (1, 2, 21000, 19000, 2000, 64, 2, 1),   # 297 slice groups on 256 units: a partial second sweep
 ]
 
 
