@@ -59,6 +59,9 @@ def gpu_select(s, f_dev, n_q, q_pos0, kc_dev, dev):
     sp.sparda_forecast_select(s, f_dev, n_q, q_pos0, kc_dev, sel, cnt, ws(s, sp.SPARDA_OP_FORECAST_SELECT, n_q,
                                                                           q_pos0, dev))
     torch.cuda.synchronize()
+    # every row's count is written (777 exceeds every k_total here): no slice or unit is skipped,
+    # whichever rows the comparisons sample
+    assert not bool((cnt == 777).any()), f"{int((cnt == 777).sum())} rows left without a selection"
     return sel, cnt
 
 
