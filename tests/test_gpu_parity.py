@@ -70,6 +70,9 @@ def gpu_attend(s, q_dev, n_q, q_pos0, k_dev, v_dev, kv_mode, sel_dev, cnt_dev, d
     sp.sparda_sparse_attn(s, q_dev, n_q, q_pos0, k_dev, v_dev, kv_mode, sel_dev, cnt_dev, SCALE, o,
                           ws(s, sp.SPARDA_OP_SPARSE_ATTN, n_q, q_pos0, dev))
     torch.cuda.synchronize()
+    # every output row is written (it starts as NaN, and finite inputs give finite outputs),
+    # whichever rows the oracle comparisons sample
+    assert not bool(torch.isnan(o).any()), f"{int(torch.isnan(o).sum())} output elements left unwritten"
     return o
 
 
